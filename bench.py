@@ -1,0 +1,177 @@
+#!/usr/bin/env python3
+"""Throughput of the GDP policy hot path on one MI355X.
+
+One step = one full pass of the hot path over the 52,000-node GNMT-8-like
+dataflow DAG: gdp_embed (3 GraphSAGE max-pool layers) -> gdp_place (6
+segment-recurrent attention layers with FiLM conditioning, device logits) ->
+gdp_sample (64 whole-graph placements + log-probs).  Inputs are synthetic and
+resident in device memory before the timed region starts.
+
+Prints one JSON line.  `value` is nodes per second (N nodes per step).
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "policy fwd+sample nodes/sec on 50k-node DAG; % HBM / MFMA roofline"
+PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}
+PEAK_HBM_GBS = 8000.0
+
+
+def flop_model(cfg, g, stats):
+    """Algorithmic work per launch of each kernel kind (one layer's launch).
+
+    GEMMs: 2 * M * K * N.  Attention: 4 * d * sum over queries of the keys it
+    attends to (QK^T and PV, all heads).  Gather-max: bytes of the sampled
+    neighbour rows and their ids, the pointer array and the output rows."""
+    import numpy as np
+    N, H, F, d, dff = g.n_nodes, cfg.hidden, cfg.feat_dim, cfg.d_model, cfg.d_ff
+    b = 2 if cfg.dtype == "bf16" else 4
+    keys = 0
+    gp = g.graph_ptr
+    for gi in range(len(gp) - 1):
+        gs, ge = int(gp[gi]), int(gp[gi + 1])
+        for q0 in range(gs, ge, cfg.seg_len):
+            q1 = min(q0 + cfg.seg_len, ge)
+            keys += (q1 - q0) * (q1 - max(gs, q0 - cfg.mem_len))
+    L = cfg.gnn_layers
+    pool = [2.0 * N * (F if l == 0 else H) * H for l in range(L)]
+    upd = [2.0 * N * ((F if l == 0 else H) + H) * H for l in range(L)]
+    gather_bytes = stats["sum_s"] * (H * b + 4) + N * H * b + 4 * (N + 1)
+    return {
+        "gemm_pool_sigmoid": ("mfma", float(np.mean(pool))),
+        "gemm_update_relu": ("mfma", float(np.mean(upd))),
+        "gather_max": ("hbm", float(gather_bytes)),
+        "gemm_qkv": ("mfma", 2.0 * N * d * 3 * d),
+        "seg_attention": ("mfma", 4.0 * d * keys),
+        "gemm_out_ln": ("mfma", 2.0 * N * d * d),
+        "gemm_ffn1_relu": ("mfma", 2.0 * N * d * dff),
+        "gemm_ffn2_ln": ("mfma", 2.0 * N * dff * d),
+    }, keys
+
+
+def cpu_baseline(cfg, g, w, n_sample, cores):
+    """The fp64 oracle (untuned) on the first n_sample nodes of the same DAG."""
+    from threadpoolctl import threadpool_limits
+
+    from oracle import gdp_oracle as O
+    from paper_1910_01578_amd import workloads as W
+    sub = W.prefix_graph(g, n_sample)
+    gnn, pl, hd = w.f64()
+    with threadpool_limits(limits=cores):
+        t0 = time.perf_counter()
+        O.policy_forward(sub.graph_ptr, sub.row_ptr, sub.col_idx, sub.x, gnn, pl, hd["w_out"], hd["b_out"],
+                         fanout=cfg.fanout, nb_seed=cfg.nb_seed, n_heads=cfg.heads, seg_len=cfg.seg_len,
+                         mem_len=cfg.mem_len, k_samples=cfg.k_samples, sample_seed=cfg.sample_seed, film=cfg.film)
+        dt = time.perf_counter() - t0
+    return {"value": n_sample / dt, "unit": "nodes/s", "cores": cores, "kind": "oracle",
+            "sample": f"first {n_sample} nodes of the {g.n_nodes}-node DAG (induced sub-DAG), full embed+place+"
+                      f"sample with K={cfg.k_samples}, numpy float64, {dt:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", default="gnmt8_52000")
+    ap.add_argument("--cpu-sample", type=int, default=12288, help="oracle sample size (0 = skip)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1 "
+                                   "(multi-GPU sharding is described but not built)"}))
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_1910_01578_amd import gdp, workloads as W
+
+    torch.cuda.set_device(0)
+    cfg = W.get_config(args.config)
+    g, w = W.make_graph(cfg), W.make_weights(cfg)
+    stats = W.graph_stats(g, cfg.fanout)
+    runner = gdp.Runner(gdp.DeviceGraph(g, cfg.dtype), gdp.DevicePolicy(cfg, w), cfg.k_samples)
+    seed = cfg.sample_seed
+
+    for _ in range(max(1, args.warmup)):
+        runner.forward(seed)
+    torch.cuda.synchronize()
+
+    # One extra (untimed) step with an event pair around every launch: the breakdown.
+    gdp.timer_begin(range(gdp.K_COUNT))
+    runner.forward(seed)
+    breakdown = gdp.timer_end()
+    work, keys = flop_model(cfg, g, stats)
+    dominant = max(breakdown, key=lambda k: breakdown[k]["ms"])
+
+    # Timed region: K steps; events only around the dominant kernel's launches.
+    torch.cuda.synchronize()
+    gdp.timer_begin([dominant])
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        runner.forward(seed)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    dom = gdp.timer_end()[dominant]
+    elapsed = t1 - t0
+    ms_per_step = 1e3 * elapsed / args.steps
+    value = g.n_nodes * args.steps / elapsed
+
+    def roof(kind, ms_total, launches):
+        if kind not in work or launches == 0:
+            return None
+        bound, amount = work[kind]
+        sec = ms_total / launches / 1e3
+        if bound == "mfma":
+            ach = amount / sec / 1e12
+            peak = PEAK_TFLOPS[cfg.dtype]
+            return {"bound": "mfma", "achieved": round(ach, 2), "peak": peak, "unit": "TFLOP/s",
+                    "frac": round(ach / peak, 4)}
+        ach = amount / sec / 1e9
+        return {"bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": round(ach / PEAK_HBM_GBS, 4)}
+
+    roofline = roof(dominant, dom["ms"], dom["launches"])
+    if roofline is None:
+        roofline = {"bound": "alu", "achieved": None, "peak": None, "unit": None, "frac": None}
+    roofline["kernel"] = dominant
+    roofline["avg_launch_us"] = round(1e3 * dom["ms"] / dom["launches"], 2)
+    roofline["traffic"] = None
+
+    kernels = []
+    for kind, v in sorted(breakdown.items(), key=lambda kv: -kv[1]["ms"]):
+        ent = {"kernel": kind, "ms_per_step": round(v["ms"], 4), "launches": v["launches"]}
+        rf = roof(kind, v["ms"], v["launches"])
+        if rf:
+            ent.update({"achieved": rf["achieved"], "unit": rf["unit"], "frac": rf["frac"], "bound": rf["bound"]})
+        kernels.append(ent)
+
+    cpu = None
+    if args.cpu_sample > 0:
+        cores = min(16, len(os.sched_getaffinity(0)))
+        cpu = cpu_baseline(cfg, g, w, min(args.cpu_sample, g.n_nodes), cores)
+
+    out = {
+        "metric": METRIC, "value": round(value, 1), "unit": "nodes/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": cfg.dtype, "data": "synthetic",
+        "config": {"workload": f"{cfg.name}: GNMT-8-like DAG, N={g.n_nodes}, E={g.n_edges}, GNN 3x{cfg.hidden} "
+                               f"fanout {cfg.fanout}, placer {cfg.placer_layers}x d={cfg.d_model} h={cfg.heads} "
+                               f"S=M={cfg.seg_len}, D={cfg.n_devices}, K={cfg.k_samples}",
+                   "nodes": g.n_nodes, "edges": g.n_edges, "sum_sampled_neighbours": stats["sum_s"],
+                   "attention_keys": keys, "parallelism": "single GPU"},
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+        "kernels": kernels,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,278 @@
+/*
+ * gdp.h -- C ABI of libgdp: the forward pass of the GDP device-placement
+ * policy (Zhou et al., "GDP: Generalized Device Placement for Dataflow
+ * Graphs") and whole-graph sampling of placements, on one AMD Instinct
+ * MI355X (gfx950).
+ *
+ * The problem statement (Section 3): given a dataflow graph G(V, E) whose
+ * vertices are ops and whose edges are data dependencies, a policy assigns a
+ * device to every op of the graph.  The policy is a graph embedding network
+ * (Section 3.1, Eq. 2-3) followed by a segment-recurrent attention placement
+ * network (Section 3.2) whose layers are conditioned on the pooled graph
+ * representation (Section 3.3, Eq. 4); its output is an N x d matrix of
+ * per-op device logits (Fig. 1).
+ *
+ * Three calls make up one forward pass:
+ *   gdp_embed   graph + features + GNN weights  -> node and graph embeddings
+ *   gdp_place   embeddings + placer weights      -> device logits (+ lse)
+ *   gdp_sample  logits + K + seed                -> K placements + log-probs
+ *
+ * Conventions shared by every call
+ *  - Memory.  Every pointer documented "device" is HIP device memory owned by
+ *    the caller; "host" pointers are ordinary host memory read during the
+ *    call only.  The library never allocates or frees device memory.  Scratch
+ *    memory comes from the caller's workspace (gdp_workspace_bytes).
+ *  - Layout.  Matrices are row-major.  Weight matrices are [out, in] (each
+ *    output unit's weights contiguous), so y = x W^T + b.
+ *  - Element type.  A call works either entirely in fp32 (GDP_F32) or with
+ *    bf16 storage and fp32 arithmetic (GDP_BF16): features, weights, biases,
+ *    LayerNorm parameters and node embeddings then use bf16; graph
+ *    embeddings, logits, lse and log-probs are always fp32.
+ *  - Streams.  `stream` is a hipStream_t (NULL = the default stream).  Calls
+ *    only enqueue work and return without synchronising.  A workspace may be
+ *    shared by several calls only if they are ordered on one stream.
+ *  - Errors.  Calls return GDP_OK (0) or a negative gdp_status.  On a
+ *    validation error nothing is enqueued and no output is touched;
+ *    gdp_last_error() then describes the failure (thread-local string).
+ *    Errors of already-enqueued work surface as GDP_E_HIP from a later call
+ *    or from the caller's own synchronisation.  No C++ exception crosses
+ *    this interface.
+ *  - Preconditions on device data.  The device calls do not inspect the CSR
+ *    arrays on the host; callers check them once with
+ *    gdp_validate_graph_host (out-of-range ids in device arrays are
+ *    undefined behaviour).
+ */
+#ifndef GDP_H_
+#define GDP_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define GDP_ABI_VERSION 1
+
+/* Limits of this implementation (violations return GDP_E_UNSUPPORTED). */
+#define GDP_MAX_GRAPHS 128   /* graphs per ragged batch                      */
+#define GDP_MAX_FANOUT 32    /* sampled neighbours per node                  */
+#define GDP_MAX_DEVICES 64   /* devices d of the placement                   */
+
+typedef enum gdp_status {
+  GDP_OK = 0,
+  GDP_E_INVALID_ARG = -1,  /* null pointer, bad size or flag               */
+  GDP_E_BAD_GRAPH = -2,    /* graph structure violates the contract        */
+  GDP_E_UNSUPPORTED = -3,  /* valid but outside this build's limits        */
+  GDP_E_WORKSPACE = -4,    /* workspace smaller than gdp_workspace_bytes   */
+  GDP_E_HIP = -5           /* a HIP runtime call failed                     */
+} gdp_status;
+
+typedef enum gdp_dtype { GDP_F32 = 0, GDP_BF16 = 1 } gdp_dtype;
+
+/* gdp_graph.flags */
+#define GDP_TOPO_IDS 1u  /* every edge u -> v has u < v (checked by the host validator) */
+
+/*
+ * A ragged batch of G dataflow graphs (Section 3: G(V, E); Section 3.3: a
+ * batch of heterogeneous graphs).  Graph g owns the node ids
+ * [graph_ptr_h[g], graph_ptr_h[g+1]); edges never cross graphs.  The CSR
+ * holds out-edges (data dependencies u -> v); the neighbourhood N(v) of
+ * Eq. 2 is taken over in- and out-edges.  Node order is also the order of the
+ * placer's sequence (Section 3.2).
+ */
+typedef struct gdp_graph {
+  int32_t n_graphs;            /* G, 1 .. GDP_MAX_GRAPHS                      */
+  const int32_t* graph_ptr_h;  /* host [G+1]; 0 = ptr[0] < ptr[1] < ... = N   */
+  int32_t n_nodes;             /* N >= 1                                      */
+  const int32_t* row_ptr;      /* device [N+1], row_ptr[0] = 0, row_ptr[N] = E */
+  const int32_t* col_idx;      /* device [E], global ids, no self-loops or
+                                  duplicates, same graph as the row          */
+  int64_t n_edges;             /* E, 0 .. INT32_MAX                           */
+  const void* x;               /* device [N, F] node meta-features (dtype)    */
+  int32_t feat_dim;            /* F, a multiple of 32                          */
+  int32_t dtype;               /* gdp_dtype of x, weights and node_emb        */
+  uint32_t flags;              /* GDP_TOPO_IDS or 0                           */
+} gdp_graph;
+
+/*
+ * One iteration of the graph embedding network (Section 3.1).
+ *   Eq. 2:  h_N(v) = max_{u in S(v)} sigmoid(w_pool h_u + b_pool)   (0 if S(v) is empty)
+ *   Eq. 3:  h_v'   = ReLU(w_self h_v + w_neigh h_N(v) + b_upd),
+ * i.e. f(concat(h_v, h_N(v))) with f's weight [w_self | w_neigh].
+ * All device pointers in the graph's dtype.
+ */
+typedef struct gdp_gnn_layer {
+  const void* w_pool;   /* [H, H_in]  */
+  const void* b_pool;   /* [H]        */
+  const void* w_self;   /* [H, H_in]  */
+  const void* w_neigh;  /* [H, H]     */
+  const void* b_upd;    /* [H]        */
+} gdp_gnn_layer;
+
+/*
+ * The graph embedding network.  H_in is feat_dim for layer 0 and hidden
+ * afterwards.  S(v) is N(v) when |N(v)| <= fanout; otherwise the fanout
+ * members u with the smallest (key(v, u), u), where key is word 0 of
+ * Philox4x64-10(counter = (v - g0, u - g0, 1, 0), key = (nbr_seed, 0)) and g0
+ * is the first node of v's graph.  One sample serves all layers.
+ */
+typedef struct gdp_gnn {
+  int32_t n_layers;               /* >= 1                                   */
+  int32_t in_dim;                 /* F (must equal gdp_graph.feat_dim)      */
+  int32_t hidden;                 /* H: 64, 128 or 256                      */
+  int32_t fanout;                 /* 1 .. GDP_MAX_FANOUT                    */
+  uint64_t nbr_seed;
+  const gdp_gnn_layer* layers;    /* host array [n_layers]                  */
+} gdp_gnn;
+
+/*
+ * One placer layer (Section 3.2 and Eq. 4).  With Y = gamma (.) X + beta the
+ * conditioned layer input (gamma = 1 + film_wg x0 + film_bg,
+ * beta = film_wb x0 + film_bb for the layer's graph), the layer computes
+ *   Z  = LN1(Y + MHA(Y; memory) W_o^T + b_o)
+ *   X' = LN2(Z + W_2 ReLU(W_1 Z + b_1) + b_2)
+ * where MHA has no positional terms and no mask: the queries of a segment
+ * [q0, q1) of graph g attend to the keys [max(g_start, q0 - mem_len), q1).
+ * w_qkv stacks the Q, K and V projections; heads are contiguous column groups.
+ */
+typedef struct gdp_placer_layer {
+  const void *film_wg, *film_bg;  /* [d, H], [d]  (ignored when film = 0)   */
+  const void *film_wb, *film_bb;  /* [d, H], [d]                            */
+  const void *w_qkv, *b_qkv;      /* [3d, d], [3d]                          */
+  const void *w_o, *b_o;          /* [d, d], [d]                            */
+  const void *ln1_g, *ln1_b;      /* [d], [d]                               */
+  const void *w_1, *b_1;          /* [d_ff, d], [d_ff]                      */
+  const void *w_2, *b_2;          /* [d, d_ff], [d]                         */
+  const void *ln2_g, *ln2_b;      /* [d], [d]                               */
+} gdp_placer_layer;
+
+typedef struct gdp_placer {
+  int32_t n_layers;               /* >= 1                                   */
+  int32_t d_model;                /* d = gdp_gnn.hidden                     */
+  int32_t n_heads;                /* d / n_heads in {16, 32, 64}            */
+  int32_t d_ff;                   /* a multiple of 128                      */
+  int32_t seg_len;                /* segment length S >= 1                  */
+  int32_t mem_len;                /* memory length M >= 0                   */
+  int32_t n_devices;              /* D, 2 .. GDP_MAX_DEVICES                */
+  int32_t film;                   /* 1: condition on x0 (Eq. 4), 0: off     */
+  const gdp_placer_layer* layers; /* host array [n_layers]                  */
+  const void* w_out;              /* [D, d] device, dtype                    */
+  const void* b_out;              /* [D]                                    */
+} gdp_placer;
+
+/* Bytes of workspace needed by gdp_embed, gdp_place and gdp_sample for this
+ * problem (the maximum of the three).  Returns 0 on invalid arguments. */
+size_t gdp_workspace_bytes(const gdp_graph* g, const gdp_gnn* gnn, const gdp_placer* placer,
+                           int32_t k_samples);
+
+/*
+ * Graph embedding network (Section 3.1, Eq. 2-3), then the per-graph mean of
+ * the final node embeddings as the graph representation x0 (Eq. 4's x^(0)).
+ *   node_emb   device [N, H], dtype         (output)
+ *   graph_emb  device [G, H], fp32          (output)
+ */
+int gdp_embed(const gdp_graph* g, const gdp_gnn* gnn, void* node_emb, float* graph_emb,
+              void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Placement network (Section 3.2) with feature conditioning (Section 3.3,
+ * Eq. 4) and the output layer producing per-node device logits (Fig. 1).
+ *   node_emb   device [N, d], dtype         (input, from gdp_embed)
+ *   graph_emb  device [G, d], fp32          (input; unused when film = 0)
+ *   logits     device [N, D], fp32          (output)
+ *   lse        device [N],    fp32          (output, may be NULL): log-sum-exp of each row
+ */
+int gdp_place(const gdp_graph* g, const void* node_emb, const float* graph_emb,
+              const gdp_placer* placer, float* logits, float* lse,
+              void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Whole-graph sampling: K placements of every op at once (Section 3), by
+ * Gumbel-max over the device logits, with the log-probability of each
+ * sampled placement (the quantity a PPO update needs, Section 3).
+ *   placements[k, v] = argmax_j (logits[v, j] - ln(-ln u[k, v, j])), ties to the lowest j
+ *   logp[g, k]       = sum over v in graph g of (logits[v, p] - lse[v])
+ * u[k, v, j] = (2 * (h >> 9) + 1) * 2^-24 where h is the 32-bit half (j & 1,
+ * 0 = low) of word (j & 7) >> 1 of Philox4x64-10(counter = (v, k, 2, j >> 3),
+ * key = (seed, 0)), v the global node id.
+ *   logits      device [N, D] fp32 (input)
+ *   lse         device [N] fp32 (input, may be NULL: then recomputed)
+ *   uniforms    device [K, N, D] fp32 or NULL: replaces the generator (testing)
+ *   placements  device [K, N] int32 (output)
+ *   logp        device [G, K] fp32 (output)
+ */
+int gdp_sample(const gdp_graph* g, const float* logits, const float* lse, int32_t n_devices,
+               int32_t k_samples, uint64_t seed, const float* uniforms, int32_t* placements,
+               float* logp, void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Host-side check of a graph batch (all pointers host memory): graph_ptr
+ * strictly increasing from 0, row_ptr monotone from 0 to E, col_idx in range,
+ * no self-loops, no duplicate edges, no edge across graphs, acyclic (Kahn's
+ * algorithm), and u < v on every edge when flags has GDP_TOPO_IDS.
+ * Returns GDP_OK, GDP_E_INVALID_ARG or GDP_E_BAD_GRAPH (with gdp_last_error).
+ */
+int gdp_validate_graph_host(const int32_t* graph_ptr, int32_t n_graphs, const int32_t* row_ptr,
+                            int32_t n_nodes, const int32_t* col_idx, int64_t n_edges,
+                            uint32_t flags);
+
+/* Description of the last failure on the calling thread ("" if none). */
+const char* gdp_last_error(void);
+
+/* GDP_ABI_VERSION of the loaded library. */
+int gdp_abi_version(void);
+
+/* ---- diagnostics (tests and benchmarks) --------------------------------- */
+
+/*
+ * The uniforms u[k, v, j] that gdp_sample draws for (seed, N, K, D), written
+ * to out (device [K, N, D] fp32), for bit-exact checks of the generator.
+ */
+int gdp_debug_uniforms(uint64_t seed, int32_t n_nodes, int32_t k_samples, int32_t n_devices,
+                       float* out, void* stream);
+
+/*
+ * The sampled neighbourhoods S(v) that gdp_embed uses: s_ptr device [N+1]
+ * and s_idx device [capacity] (capacity >= min(2E, N * fanout)).  The order
+ * of ids inside one row is unspecified.
+ */
+int gdp_debug_neighbors(const gdp_graph* g, const gdp_gnn* gnn, int32_t* s_ptr, int32_t* s_idx,
+                        int64_t capacity, void* workspace, size_t workspace_bytes, void* stream);
+
+/* Kernel kinds for the event timer below. */
+typedef enum gdp_kernel_kind {
+  GDP_K_GRAPH_PREP = 0,  /* degree count, scans, reverse-edge fill          */
+  GDP_K_NBR_SAMPLE,      /* neighbour sampling S(v)                          */
+  GDP_K_GEMM_POOL,       /* sigmoid(h W_pool^T + b)                           */
+  GDP_K_GATHER_MAX,      /* Eq. 2 max over S(v)                               */
+  GDP_K_GEMM_UPDATE,     /* Eq. 3 ReLU(h W_self^T + A W_neigh^T + b)          */
+  GDP_K_MEANPOOL,        /* x0 = per-graph mean                              */
+  GDP_K_FILM,            /* gamma/beta GEMVs and the first layer's FiLM       */
+  GDP_K_GEMM_QKV,        /* Y W_qkv^T + b                                    */
+  GDP_K_ATTENTION,       /* segment attention                                */
+  GDP_K_GEMM_OUT_LN,     /* LN1(Y + O W_o^T + b)                              */
+  GDP_K_GEMM_FFN1,       /* ReLU(Z W_1^T + b)                                 */
+  GDP_K_GEMM_FFN2_LN,    /* LN2(Z + H W_2^T + b) (+ next layer's FiLM)        */
+  GDP_K_HEAD,            /* logits and lse                                   */
+  GDP_K_SAMPLE,          /* Gumbel-max sampling                              */
+  GDP_K_LOGP_REDUCE,     /* per-graph log-prob sums                          */
+  GDP_K_COUNT
+} gdp_kernel_kind;
+
+/*
+ * Event timer.  gdp_timer_begin(mask) makes every later launch of a kernel
+ * kind whose bit (1u << kind) is set in mask record a HIP event pair on the
+ * stream it is launched on.  gdp_timer_end synchronises those events and
+ * writes, per kind, the summed elapsed milliseconds and the launch count
+ * (arrays of GDP_K_COUNT entries; either may be NULL), then stops timing.
+ * Process-wide state: not for concurrent use from several threads.
+ */
+int gdp_timer_begin(uint32_t kind_mask);
+int gdp_timer_end(double* total_ms, int64_t* launches);
+const char* gdp_kernel_kind_name(int32_t kind);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* GDP_H_ */

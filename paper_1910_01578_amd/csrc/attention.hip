@@ -1,0 +1,285 @@
+// Section 3.2: segment-recurrent attention without positional terms.
+//
+// Transformer-XL caches each layer's inputs of the previous positions and
+// lets the next segment attend over [memory ; segment].  In a forward pass
+// that is the same as running each layer over all nodes at once with a band:
+// the queries of segment [q0, q1) of graph g attend to the keys
+// [max(g_start, q0 - mem_len), q1) of the same layer's input.  There is no
+// causal mask (the placement of all ops is emitted at once) and no positional
+// term, so every work-group is independent.
+//
+// Work-group = (128 queries of one segment, one head); wave w owns queries
+// [32w, 32w + 32) as two 16-column MFMA blocks.  Scores are formed transposed,
+// S^T = K Q^T, so that a lane owns one query column: the row max is an
+// in-lane max plus a 4-way exchange, and the probabilities feed the P V
+// product (O^T = V^T P^T) straight from the score registers.  K tiles live in
+// LDS row-major, V tiles transposed; both double-buffered over 64-key tiles.
+#include "device_common.h"
+#include "kernels.h"
+
+namespace gdp {
+
+namespace {
+
+constexpr int BQ = kAttnBlockQ;  // queries per work-group
+constexpr int BKV = 64;          // keys per tile
+
+// Contraction over the head dimension: instruction shape per element type.
+template <typename T, int DH> struct QkShape;
+template <int DH> struct QkShape<bf16, DH> {   // DH = 32, 64: 16x16x32
+  static constexpr int K = 32, KV = 8, STEPS = DH / 32;
+};
+template <> struct QkShape<bf16, 16> { static constexpr int K = 16, KV = 4, STEPS = 1; };
+template <int DH> struct QkShape<float, DH> { static constexpr int K = 4, KV = 1, STEPS = DH / 4; };
+
+template <typename T, int DH>
+struct QkFrag;
+template <int DH> struct QkFrag<bf16, DH> {
+  typedef bf16x8 t;
+  static __device__ __forceinline__ t load(const bf16* p) { return *reinterpret_cast<const bf16x8*>(p); }
+  static __device__ __forceinline__ t zero() { t z; for (int i = 0; i < 8; ++i) z[i] = (bf16)0.f; return z; }
+  static __device__ __forceinline__ f32x4 mma(t a, t b, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+  }
+};
+template <> struct QkFrag<bf16, 16> {
+  typedef i16x4 t;
+  static __device__ __forceinline__ t load(const bf16* p) { return *reinterpret_cast<const i16x4*>(p); }
+  static __device__ __forceinline__ t zero() { return i16x4{0, 0, 0, 0}; }
+  static __device__ __forceinline__ f32x4 mma(t a, t b, f32x4 c) { return mfma_16x16x16_bf16(a, b, c); }
+};
+template <int DH> struct QkFrag<float, DH> {
+  typedef float t;
+  static __device__ __forceinline__ t load(const float* p) { return *p; }
+  static __device__ __forceinline__ t zero() { return 0.f; }
+  static __device__ __forceinline__ f32x4 mma(t a, t b, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+  }
+};
+
+}  // namespace
+
+template <typename T, int DH>
+__global__ __launch_bounds__(256) void k_seg_attention(AttnArgs<T> p, GraphTable gt, float scale_log2) {
+  constexpr int EPV = 16 / sizeof(T);
+  constexpr int KS = DH + EPV;          // sK row stride
+  constexpr int VS = BKV + EPV;         // sVt row stride
+  constexpr int DB = DH / 16;           // 16-row blocks of the head dim
+  using QS = QkShape<T, DH>;
+  using QF = QkFrag<T, DH>;
+  __shared__ __attribute__((aligned(16))) T sK[2][BKV * KS];
+  __shared__ __attribute__((aligned(16))) T sVt[2][DH * VS];
+
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int col = lane & 15, g4 = lane >> 4;
+  const int head = blockIdx.x % p.heads;
+  const int qblk = blockIdx.x / p.heads;
+
+  // ---- which graph / segment / query block -----------------------------------
+  const int g = graph_of_block(gt, qblk);
+  const int qbs = (p.seg_len + BQ - 1) / BQ;
+  const int local = qblk - gt.blk[g];
+  const int seg = local / qbs, qb = local % qbs;
+  const int gs = gt.ptr[g], ge = gt.ptr[g + 1];
+  const int seg0 = gs + seg * p.seg_len;
+  const int seg1 = min(seg0 + p.seg_len, ge);
+  const int q0 = seg0 + qb * BQ;
+  const int qend = min(q0 + BQ, seg1);
+  const int k0 = max(gs, seg0 - p.mem_len);
+  const int k1 = seg1;
+  const int ntiles = (k1 - k0 + BKV - 1) / BKV;
+
+  const T* Qp = p.qkv + head * DH;
+  const T* Kp = p.qkv + p.d + head * DH;
+  const T* Vp = p.qkv + 2 * p.d + head * DH;
+
+  // ---- Q fragments (B operand of S^T = K Q^T), kept in registers -------------
+  typename QF::t qf[2][QS::STEPS];
+#pragma unroll
+  for (int c = 0; c < 2; ++c) {
+    const int q = q0 + wave * 32 + c * 16 + col;
+#pragma unroll
+    for (int s = 0; s < QS::STEPS; ++s)
+      qf[c][s] = q < qend ? QF::load(Qp + (size_t)q * p.ldq + s * QS::K + QS::KV * g4) : QF::zero();
+  }
+
+  // ---- K / V tile staging -------------------------------------------------------
+  constexpr int CPR = DH / EPV;                 // 16-byte chunks per key row
+  constexpr int CHUNKS = BKV * CPR;
+  uint4 rk[(CHUNKS + 255) / 256], rv[(CHUNKS + 255) / 256];
+  auto load_tile = [&](int t) {
+    const int kb = k0 + t * BKV;
+#pragma unroll
+    for (int i = 0; i < (CHUNKS + 255) / 256; ++i) {
+      const int c = threadIdx.x + i * 256;
+      const int row = c / CPR, cc = (c % CPR) * EPV;
+      const int key = kb + row;
+      if (c < CHUNKS && key < k1) {
+        rk[i] = *reinterpret_cast<const uint4*>(Kp + (size_t)key * p.ldq + cc);
+        rv[i] = *reinterpret_cast<const uint4*>(Vp + (size_t)key * p.ldq + cc);
+      } else {
+        rk[i] = make_uint4(0u, 0u, 0u, 0u);
+        rv[i] = make_uint4(0u, 0u, 0u, 0u);
+      }
+    }
+  };
+  auto store_tile = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < (CHUNKS + 255) / 256; ++i) {
+      const int c = threadIdx.x + i * 256;
+      if (c < CHUNKS) {
+        const int row = c / CPR, cc = (c % CPR) * EPV;
+        *reinterpret_cast<uint4*>(&sK[buf][row * KS + cc]) = rk[i];
+        const T* v = reinterpret_cast<const T*>(&rv[i]);
+#pragma unroll
+        for (int e = 0; e < EPV; ++e) sVt[buf][(cc + e) * VS + row] = v[e];
+      }
+    }
+  };
+
+  f32x4 oacc[DB][2];
+#pragma unroll
+  for (int b = 0; b < DB; ++b) { oacc[b][0] = zero4(); oacc[b][1] = zero4(); }
+  float mrun[2] = {-INFINITY, -INFINITY};
+  float lrun[2] = {0.f, 0.f};
+
+  load_tile(0);
+  store_tile(0);
+  __syncthreads();
+  for (int t = 0; t < ntiles; ++t) {
+    const int cur = t & 1;
+    if (t + 1 < ntiles) load_tile(t + 1);
+    const int kvalid = k1 - (k0 + t * BKV);     // keys of this tile that exist (>= 1)
+
+    // S^T blocks: 4 key blocks x 2 query blocks
+    f32x4 sacc[4][2];
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb) {
+      sacc[kb][0] = zero4();
+      sacc[kb][1] = zero4();
+#pragma unroll
+      for (int s = 0; s < QS::STEPS; ++s) {
+        const typename QF::t kf = QF::load(&sK[cur][(kb * 16 + col) * KS + s * QS::K + QS::KV * g4]);
+        sacc[kb][0] = QF::mma(kf, qf[0][s], sacc[kb][0]);
+        sacc[kb][1] = QF::mma(kf, qf[1][s], sacc[kb][1]);
+      }
+    }
+    // mask keys past the band end (only the last tile has them)
+    if (kvalid < BKV) {
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          if (kb * 16 + 4 * g4 + r >= kvalid) { sacc[kb][0][r] = -INFINITY; sacc[kb][1][r] = -INFINITY; }
+    }
+
+    // online softmax per query column (scaled log2 domain)
+    float alpha[2];
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+      float mx = -INFINITY;
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) mx = fmaxf(mx, sacc[kb][c][r]);
+      mx = fmaxf(mx, xor_shfl(mx, 16));
+      mx = fmaxf(mx, xor_shfl(mx, 32));
+      const float mnew = fmaxf(mrun[c], mx * scale_log2);
+      alpha[c] = exp2f(mrun[c] - mnew);
+      mrun[c] = mnew;
+      float ls = 0.f;
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float e = exp2f(fmaf(sacc[kb][c][r], scale_log2, -mnew));
+          sacc[kb][c][r] = e;
+          ls += e;
+        }
+      lrun[c] = lrun[c] * alpha[c] + ls;
+#pragma unroll
+      for (int b = 0; b < DB; ++b) oacc[b][c] *= alpha[c];
+    }
+
+    // O^T += V^T P^T
+    if constexpr (sizeof(T) == 2) {
+      // 16x16x32: k slot 8*g4 + i holds key 32c + 4*g4 + i (i < 4) or 32c + 16 + 4*g4 + (i - 4)
+#pragma unroll
+      for (int c2 = 0; c2 < 2; ++c2) {
+        bf16x8 pf[2];
+#pragma unroll
+        for (int c = 0; c < 2; ++c)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            pf[c][i] = (bf16)sacc[2 * c2][c][i];
+            pf[c][4 + i] = (bf16)sacc[2 * c2 + 1][c][i];
+          }
+#pragma unroll
+        for (int b = 0; b < DB; ++b) {
+          const T* vrow = &sVt[cur][(b * 16 + col) * VS + 32 * c2 + 4 * g4];
+          const uint2 lo = *reinterpret_cast<const uint2*>(vrow);
+          const uint2 hi = *reinterpret_cast<const uint2*>(vrow + 16);
+          bf16x8 vf;
+          const bf16* l4 = reinterpret_cast<const bf16*>(&lo);
+          const bf16* h4 = reinterpret_cast<const bf16*>(&hi);
+#pragma unroll
+          for (int i = 0; i < 4; ++i) { vf[i] = l4[i]; vf[4 + i] = h4[i]; }
+          oacc[b][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[0], oacc[b][0], 0, 0, 0);
+          oacc[b][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[1], oacc[b][1], 0, 0, 0);
+        }
+      }
+    } else {
+      // 16x16x4 fp32: chunk (kb, i) puts key 16kb + 4*g4 + i in slot g4
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int b = 0; b < DB; ++b) {
+            const float vf = to_f32(sVt[cur][(b * 16 + col) * VS + kb * 16 + 4 * g4 + i]);
+            oacc[b][0] = __builtin_amdgcn_mfma_f32_16x16x4f32(vf, sacc[kb][0][i], oacc[b][0], 0, 0, 0);
+            oacc[b][1] = __builtin_amdgcn_mfma_f32_16x16x4f32(vf, sacc[kb][1][i], oacc[b][1], 0, 0, 0);
+          }
+    }
+
+    if (t + 1 < ntiles) store_tile(cur ^ 1);
+    __syncthreads();
+  }
+
+  // ---- normalise and store ---------------------------------------------------------
+#pragma unroll
+  for (int c = 0; c < 2; ++c) {
+    float l = lrun[c];
+    l += xor_shfl(l, 16);
+    l += xor_shfl(l, 32);
+    const float inv = 1.0f / l;
+    const int q = q0 + wave * 32 + c * 16 + col;
+    if (q < qend) {
+#pragma unroll
+      for (int b = 0; b < DB; ++b) {
+        T* o = p.out + (size_t)q * p.ldo + head * DH + b * 16 + 4 * g4;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) o[r] = from_f32<T>(oacc[b][c][r] * inv);
+      }
+    }
+  }
+}
+
+template <typename T>
+hipError_t launch_attention(const AttnArgs<T>& a, const GraphTable& gt, hipStream_t s) {
+  if (a.total_qblocks <= 0) return hipSuccess;
+  const int dh = a.d / a.heads;
+  const float scale_log2 = 1.4426950408889634f / sqrtf((float)dh);
+  dim3 grid(a.total_qblocks * a.heads), block(256);
+  switch (dh) {
+    case 16: hipLaunchKernelGGL((k_seg_attention<T, 16>), grid, block, 0, s, a, gt, scale_log2); break;
+    case 32: hipLaunchKernelGGL((k_seg_attention<T, 32>), grid, block, 0, s, a, gt, scale_log2); break;
+    case 64: hipLaunchKernelGGL((k_seg_attention<T, 64>), grid, block, 0, s, a, gt, scale_log2); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+template hipError_t launch_attention<float>(const AttnArgs<float>&, const GraphTable&, hipStream_t);
+template hipError_t launch_attention<bf16>(const AttnArgs<bf16>&, const GraphTable&, hipStream_t);
+
+}  // namespace gdp

@@ -1,0 +1,381 @@
+// C ABI entry points: argument checks, workspace carving and the launch
+// sequence of each call (everything is enqueued on the caller's stream).
+#include <hip/hip_runtime.h>
+#include <string.h>
+
+#include <vector>
+
+#include "device_common.h"
+#include "gdp.h"
+#include "host_plan.h"
+#include "kernels.h"
+
+namespace gdp {
+
+static_assert(kPoolRows == kMeanpoolRows, "mean-pool chunk size");
+static_assert(kAttnQ == kAttnBlockQ, "attention query block");
+static_assert(kSampleRows == kSampleChunk, "sampling chunk");
+
+// ---------------------------------------------------------------------------
+// Event timer (diagnostics): an event pair around every launch of a selected
+// kernel kind, on the stream of that launch.
+// ---------------------------------------------------------------------------
+namespace {
+struct TimerRec {
+  int kind;
+  hipEvent_t a, b;
+};
+struct TimerState {
+  uint32_t mask = 0;
+  std::vector<TimerRec> recs;
+  std::vector<hipEvent_t> pool;
+  hipEvent_t take() {
+    if (!pool.empty()) {
+      hipEvent_t e = pool.back();
+      pool.pop_back();
+      return e;
+    }
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    return e;
+  }
+};
+TimerState g_timer;
+
+struct Timed {
+  hipStream_t s;
+  hipEvent_t b = nullptr;
+  bool on;
+  Timed(int kind, hipStream_t st) : s(st), on(((g_timer.mask >> kind) & 1u) != 0) {
+    if (!on) return;
+    hipEvent_t a = g_timer.take();
+    b = g_timer.take();
+    if (!a || !b) {
+      on = false;
+      return;
+    }
+    hipEventRecord(a, s);
+    g_timer.recs.push_back({kind, a, b});
+  }
+  ~Timed() {
+    if (on) hipEventRecord(b, s);
+  }
+};
+}  // namespace
+
+static int hip_fail(hipError_t e, const char* what) {
+  return fail(GDP_E_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+#define GDP_LAUNCH(kind, call)                      \
+  do {                                              \
+    hipError_t _e;                                  \
+    {                                               \
+      Timed _t((kind), st);                         \
+      _e = (call);                                  \
+    }                                               \
+    if (_e != hipSuccess) return hip_fail(_e, #call); \
+  } while (0)
+
+static GraphTable make_table(const gdp_graph* g) {
+  GraphTable t;
+  memset(&t, 0, sizeof(t));
+  t.n = g->n_graphs;
+  for (int i = 0; i <= g->n_graphs; ++i) t.ptr[i] = g->graph_ptr_h[i];
+  return t;
+}
+
+template <typename T>
+static inline T* at(void* ws, size_t off) {
+  return reinterpret_cast<T*>(static_cast<char*>(ws) + off);
+}
+
+static int pending_hip_error() {
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return hip_fail(e, "earlier HIP work");
+  return GDP_OK;
+}
+
+static int check_ws(void* ws, size_t have, size_t need) {
+  if (need > have) return fail(GDP_E_WORKSPACE, "workspace %zu bytes < %zu required", have, need);
+  if (need > 0 && !ws) return fail(GDP_E_INVALID_ARG, "workspace is NULL");
+  if (((uintptr_t)ws & 255u) != 0) return fail(GDP_E_INVALID_ARG, "workspace must be 256-byte aligned");
+  return GDP_OK;
+}
+
+static bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+// ---------------------------------------------------------------------------
+// Neighbourhoods N(v) (in- and out-edges) and the sample S(v) (Section 3.1).
+// ---------------------------------------------------------------------------
+static int prep_neighbors(const gdp_graph* g, const gdp_gnn* gnn, const EmbedPlan& pl, void* ws, int* s_ptr,
+                          int* s_idx, hipStream_t st) {
+  const int N = g->n_nodes;
+  const GraphTable gt = make_table(g);
+  int* counters = at<int>(ws, pl.counters);
+  int* in_deg = counters;
+  int* cursor = counters + N;
+  int* heavy_count = counters + 2 * N;
+  int* in_ptr = at<int>(ws, pl.in_ptr);
+  int* in_idx = at<int>(ws, pl.in_idx);
+  GDP_LAUNCH(GDP_K_GRAPH_PREP, launch_fill_i32(counters, 2 * (int64_t)N + 1, 0, st));
+  GDP_LAUNCH(GDP_K_GRAPH_PREP, launch_in_degree(g->col_idx, g->n_edges, in_deg, st));
+  GDP_LAUNCH(GDP_K_GRAPH_PREP, launch_scan_degrees(g->row_ptr, in_deg, N, gnn->fanout, in_ptr, s_ptr,
+                                                   at<int>(ws, pl.scan_tmp), st));
+  GDP_LAUNCH(GDP_K_GRAPH_PREP, launch_fill_reverse(g->row_ptr, g->col_idx, in_ptr, N, cursor, in_idx, st));
+  GDP_LAUNCH(GDP_K_NBR_SAMPLE, launch_nbr_sample(g->row_ptr, g->col_idx, in_ptr, in_idx, s_ptr, N, gnn->fanout,
+                                                 gnn->nbr_seed, gt, s_idx, at<int>(ws, pl.heavy), heavy_count, st));
+  return GDP_OK;
+}
+
+// ---------------------------------------------------------------------------
+// gdp_embed: Eq. 2 and Eq. 3 for every layer, then the mean pool.
+// ---------------------------------------------------------------------------
+template <typename T>
+static int embed_impl(const gdp_graph* g, const gdp_gnn* gnn, T* node_emb, float* graph_emb, const EmbedPlan& pl,
+                      void* ws, hipStream_t st) {
+  const int N = g->n_nodes, H = gnn->hidden;
+  int* s_ptr = at<int>(ws, pl.s_ptr);
+  int* s_idx = at<int>(ws, pl.s_idx);
+  int r = prep_neighbors(g, gnn, pl, ws, s_ptr, s_idx, st);
+  if (r != GDP_OK) return r;
+  // Every GNN activation is a GEMM operand (rounded to T for the matrix
+  // cores either way), so the hidden layers are stored in T.
+  T* P = at<T>(ws, pl.P);
+  T* A = at<T>(ws, pl.A);
+  T* hb[2] = {at<T>(ws, pl.h0), at<T>(ws, pl.h1)};
+  const T* h = static_cast<const T*>(g->x);
+  const int L = gnn->n_layers;
+  for (int l = 0; l < L; ++l) {
+    const gdp_gnn_layer& Lw = gnn->layers[l];
+    const int hin = l == 0 ? g->feat_dim : H;
+    T* hout = (l == L - 1) ? node_emb : hb[l & 1];
+    const GemmArgs<T, T, T> pool = {h, hin, static_cast<const T*>(Lw.w_pool), hin, nullptr, 0, nullptr, 0,
+                                    static_cast<const T*>(Lw.b_pool), P, H, N, H};
+    GDP_LAUNCH(GDP_K_GEMM_POOL, (launch_gemm<T, T, T>(pool, EPI_SIGMOID, st)));
+    GDP_LAUNCH(GDP_K_GATHER_MAX, launch_gather_max<T>(P, s_ptr, s_idx, N, H, A, st));
+    const GemmArgs<T, T, T> upd = {h, hin, static_cast<const T*>(Lw.w_self), hin, A, H,
+                                   static_cast<const T*>(Lw.w_neigh), H, static_cast<const T*>(Lw.b_upd), hout, H,
+                                   N, H};
+    GDP_LAUNCH(GDP_K_GEMM_UPDATE, (launch_gemm<T, T, T>(upd, EPI_RELU, st)));
+    h = hout;
+  }
+  GraphTable ct = make_table(g);
+  const int chunks = prefix_blocks_rows(g->graph_ptr_h, g->n_graphs, kPoolRows, ct.blk);
+  GDP_LAUNCH(GDP_K_MEANPOOL, launch_meanpool<T>(node_emb, H, ct, chunks, at<float>(ws, pl.pool), graph_emb, st));
+  return GDP_OK;
+}
+
+// ---------------------------------------------------------------------------
+// gdp_place: FiLM (Eq. 4) + segment-recurrent Transformer layers + head.
+// ---------------------------------------------------------------------------
+template <typename T>
+static int place_impl(const gdp_graph* g, const T* node_emb, const float* graph_emb, const gdp_placer* p,
+                      float* logits, float* lse, const PlacePlan& pl, void* ws, hipStream_t st) {
+  const int N = g->n_nodes, G = g->n_graphs, d = p->d_model, L = p->n_layers;
+  const GraphTable gt = make_table(g);
+  float* film = at<float>(ws, pl.film);       // [L][2][G][d]: gamma then beta
+  auto gamma_of = [&](int l) { return film + (size_t)l * 2 * G * d; };
+  auto beta_of = [&](int l) { return film + (size_t)l * 2 * G * d + (size_t)G * d; };
+  // Residual stream (layer inputs Y and LN1 outputs Z) in fp32; GEMM operands,
+  // attention inputs/outputs and the FFN hidden layer in T.
+  float* ybuf[2] = {at<float>(ws, pl.y0), at<float>(ws, pl.y1)};
+  T* qkv = at<T>(ws, pl.qkv);
+  T* o = at<T>(ws, pl.o);
+  float* z = at<float>(ws, pl.z);
+  T* h1 = at<T>(ws, pl.h1);
+
+  const float* y = ybuf[0];
+  if (p->film) {
+    for (int l = 0; l < L; ++l) {
+      const gdp_placer_layer& Ly = p->layers[l];
+      GDP_LAUNCH(GDP_K_FILM, launch_film_gemv<T>(static_cast<const T*>(Ly.film_wg), static_cast<const T*>(Ly.film_bg),
+                                                 static_cast<const T*>(Ly.film_wb), static_cast<const T*>(Ly.film_bb),
+                                                 graph_emb, G, d, d, gamma_of(l), beta_of(l), st));
+    }
+    GDP_LAUNCH(GDP_K_FILM, launch_film_apply<T>(node_emb, gamma_of(0), beta_of(0), N, d, gt, ybuf[0], st));
+  } else {
+    GDP_LAUNCH(GDP_K_FILM, launch_film_apply<T>(node_emb, nullptr, nullptr, N, d, gt, ybuf[0], st));
+  }
+
+  GraphTable qt = make_table(g);
+  const int qblocks = prefix_blocks_attention(g->graph_ptr_h, G, p->seg_len, kAttnQ, qt.blk);
+  int cur = 0;
+  for (int l = 0; l < L; ++l) {
+    const gdp_placer_layer& Ly = p->layers[l];
+    const GemmArgs<float, T, T> a_qkv = {y, d, static_cast<const T*>(Ly.w_qkv), d, nullptr, 0, nullptr, 0,
+                               static_cast<const T*>(Ly.b_qkv), qkv, 3 * d, N, 3 * d};
+    GDP_LAUNCH(GDP_K_GEMM_QKV, (launch_gemm<float, T, T>(a_qkv, EPI_BIAS, st)));
+    const AttnArgs<T> a_att = {qkv, 3 * d, o, d, d, p->n_heads, p->seg_len, p->mem_len, qblocks};
+    GDP_LAUNCH(GDP_K_ATTENTION, launch_attention<T>(a_att, qt, st));
+    const GemmLnArgs<T> a_out = {o, d, d, static_cast<const T*>(Ly.w_o), static_cast<const T*>(Ly.b_o), y, d,
+                                 static_cast<const T*>(Ly.ln1_g), static_cast<const T*>(Ly.ln1_b),
+                                 nullptr, nullptr, 0, z, d, N, d};
+    GDP_LAUNCH(GDP_K_GEMM_OUT_LN, launch_gemm_ln<T>(a_out, gt, st));
+    const GemmArgs<float, T, T> a_ff1 = {z, d, static_cast<const T*>(Ly.w_1), d, nullptr, 0, nullptr, 0,
+                               static_cast<const T*>(Ly.b_1), h1, p->d_ff, N, p->d_ff};
+    GDP_LAUNCH(GDP_K_GEMM_FFN1, (launch_gemm<float, T, T>(a_ff1, EPI_RELU, st)));
+    const bool next_film = p->film && l + 1 < L;
+    float* ynext = ybuf[cur ^ 1];
+    const GemmLnArgs<T> a_ff2 = {h1, p->d_ff, p->d_ff, static_cast<const T*>(Ly.w_2), static_cast<const T*>(Ly.b_2),
+                                 z, d, static_cast<const T*>(Ly.ln2_g), static_cast<const T*>(Ly.ln2_b),
+                                 next_film ? gamma_of(l + 1) : nullptr, next_film ? beta_of(l + 1) : nullptr, d,
+                                 ynext, d, N, d};
+    GDP_LAUNCH(GDP_K_GEMM_FFN2_LN, launch_gemm_ln<T>(a_ff2, gt, st));
+    cur ^= 1;
+    y = ynext;
+  }
+  GDP_LAUNCH(GDP_K_HEAD, launch_head<T>(y, static_cast<const T*>(p->w_out), static_cast<const T*>(p->b_out), N, d,
+                                        p->n_devices, logits, lse, st));
+  return GDP_OK;
+}
+
+}  // namespace gdp
+
+using namespace gdp;
+
+// ===========================================================================
+extern "C" size_t gdp_workspace_bytes(const gdp_graph* g, const gdp_gnn* gnn, const gdp_placer* placer,
+                                      int32_t k_samples) {
+  clear_error();
+  if (check_graph(g) != GDP_OK) return 0;
+  size_t need = 0;
+  if (gnn) {
+    if (check_gnn(g, gnn) != GDP_OK) return 0;
+    EmbedPlan e;
+    plan_embed(g, gnn, &e);
+    need = e.c.total;
+  }
+  if (placer) {
+    if (check_placer(g, placer) != GDP_OK) return 0;
+    PlacePlan p;
+    plan_place(g, placer, &p);
+    if (p.c.total > need) need = p.c.total;
+  }
+  if (k_samples > 0) {
+    SamplePlan s;
+    plan_sample(g, k_samples, &s);
+    if (s.c.total > need) need = s.c.total;
+  }
+  return need;
+}
+
+extern "C" int gdp_embed(const gdp_graph* g, const gdp_gnn* gnn, void* node_emb, float* graph_emb, void* ws,
+                         size_t ws_bytes, void* stream) {
+  clear_error();
+  int r;
+  if ((r = check_graph(g)) != GDP_OK) return r;
+  if ((r = check_gnn(g, gnn)) != GDP_OK) return r;
+  if (!node_emb || !graph_emb) return fail(GDP_E_INVALID_ARG, "node_emb or graph_emb is NULL");
+  if (!aligned16(node_emb) || !aligned16(g->x)) return fail(GDP_E_INVALID_ARG, "x and node_emb must be 16-byte aligned");
+  EmbedPlan pl;
+  plan_embed(g, gnn, &pl);
+  if ((r = check_ws(ws, ws_bytes, pl.c.total)) != GDP_OK) return r;
+  if ((r = pending_hip_error()) != GDP_OK) return r;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (g->dtype == GDP_BF16) return embed_impl<bf16>(g, gnn, static_cast<bf16*>(node_emb), graph_emb, pl, ws, st);
+  return embed_impl<float>(g, gnn, static_cast<float*>(node_emb), graph_emb, pl, ws, st);
+}
+
+extern "C" int gdp_place(const gdp_graph* g, const void* node_emb, const float* graph_emb, const gdp_placer* placer,
+                         float* logits, float* lse, void* ws, size_t ws_bytes, void* stream) {
+  clear_error();
+  int r;
+  if ((r = check_graph(g)) != GDP_OK) return r;
+  if ((r = check_placer(g, placer)) != GDP_OK) return r;
+  if (!node_emb || !logits) return fail(GDP_E_INVALID_ARG, "node_emb or logits is NULL");
+  if (placer->film && !graph_emb) return fail(GDP_E_INVALID_ARG, "graph_emb is NULL with film = 1");
+  if (!aligned16(node_emb)) return fail(GDP_E_INVALID_ARG, "node_emb must be 16-byte aligned");
+  PlacePlan pl;
+  plan_place(g, placer, &pl);
+  if ((r = check_ws(ws, ws_bytes, pl.c.total)) != GDP_OK) return r;
+  if ((r = pending_hip_error()) != GDP_OK) return r;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (g->dtype == GDP_BF16)
+    return place_impl<bf16>(g, static_cast<const bf16*>(node_emb), graph_emb, placer, logits, lse, pl, ws, st);
+  return place_impl<float>(g, static_cast<const float*>(node_emb), graph_emb, placer, logits, lse, pl, ws, st);
+}
+
+extern "C" int gdp_sample(const gdp_graph* g, const float* logits, const float* lse, int32_t n_devices,
+                          int32_t k_samples, uint64_t seed, const float* uniforms, int32_t* placements, float* logp,
+                          void* ws, size_t ws_bytes, void* stream) {
+  clear_error();
+  int r;
+  if ((r = check_graph(g)) != GDP_OK) return r;
+  if ((r = check_sample(g, n_devices, k_samples)) != GDP_OK) return r;
+  if (!logits || !placements || !logp) return fail(GDP_E_INVALID_ARG, "logits, placements or logp is NULL");
+  SamplePlan pl;
+  plan_sample(g, k_samples, &pl);
+  if ((r = check_ws(ws, ws_bytes, pl.c.total)) != GDP_OK) return r;
+  if ((r = pending_hip_error()) != GDP_OK) return r;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  GraphTable ct = make_table(g);
+  const int chunks = prefix_blocks_rows(g->graph_ptr_h, g->n_graphs, kSampleRows, ct.blk);
+  float* partial = at<float>(ws, pl.partial);
+  GDP_LAUNCH(GDP_K_SAMPLE, launch_sample(logits, lse, g->n_nodes, n_devices, k_samples, seed, uniforms, ct, chunks,
+                                         placements, partial, st));
+  GDP_LAUNCH(GDP_K_LOGP_REDUCE, launch_logp_reduce(partial, ct, chunks, k_samples, logp, st));
+  return GDP_OK;
+}
+
+extern "C" int gdp_debug_uniforms(uint64_t seed, int32_t n, int32_t k, int32_t d, float* out, void* stream) {
+  clear_error();
+  if (n < 1 || k < 1 || d < 1 || d > GDP_MAX_DEVICES || !out) return fail(GDP_E_INVALID_ARG, "bad arguments");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const hipError_t e = launch_debug_uniforms(seed, n, k, d, out, st);
+  if (e != hipSuccess) return hip_fail(e, "launch_debug_uniforms");
+  return GDP_OK;
+}
+
+extern "C" int gdp_debug_neighbors(const gdp_graph* g, const gdp_gnn* gnn, int32_t* s_ptr, int32_t* s_idx,
+                                   int64_t capacity, void* ws, size_t ws_bytes, void* stream) {
+  clear_error();
+  int r;
+  if ((r = check_graph(g)) != GDP_OK) return r;
+  if ((r = check_gnn(g, gnn)) != GDP_OK) return r;
+  EmbedPlan pl;
+  plan_embed(g, gnn, &pl);
+  if (!s_ptr || !s_idx) return fail(GDP_E_INVALID_ARG, "s_ptr or s_idx is NULL");
+  if (capacity < pl.s_cap) return fail(GDP_E_INVALID_ARG, "capacity %lld < %lld", (long long)capacity, (long long)pl.s_cap);
+  if ((r = check_ws(ws, ws_bytes, pl.c.total)) != GDP_OK) return r;
+  if ((r = pending_hip_error()) != GDP_OK) return r;
+  return prep_neighbors(g, gnn, pl, ws, s_ptr, s_idx, static_cast<hipStream_t>(stream));
+}
+
+extern "C" int gdp_timer_begin(uint32_t mask) {
+  clear_error();
+  if (g_timer.mask != 0 || !g_timer.recs.empty()) return fail(GDP_E_INVALID_ARG, "timer already running");
+  g_timer.mask = mask & ((1u << GDP_K_COUNT) - 1u);
+  return GDP_OK;
+}
+
+extern "C" int gdp_timer_end(double* total_ms, int64_t* launches) {
+  clear_error();
+  int r = GDP_OK;
+  if (total_ms)
+    for (int k = 0; k < GDP_K_COUNT; ++k) total_ms[k] = 0.0;
+  if (launches)
+    for (int k = 0; k < GDP_K_COUNT; ++k) launches[k] = 0;
+  for (const TimerRec& rec : g_timer.recs) {
+    float ms = 0.f;
+    hipError_t e = hipEventSynchronize(rec.b);
+    if (e == hipSuccess) e = hipEventElapsedTime(&ms, rec.a, rec.b);
+    if (e != hipSuccess && r == GDP_OK) r = hip_fail(e, "timer event");
+    if (total_ms) total_ms[rec.kind] += ms;
+    if (launches) launches[rec.kind] += 1;
+    g_timer.pool.push_back(rec.a);
+    g_timer.pool.push_back(rec.b);
+  }
+  g_timer.recs.clear();
+  g_timer.mask = 0;
+  return r;
+}
+
+extern "C" const char* gdp_kernel_kind_name(int32_t kind) {
+  static const char* names[GDP_K_COUNT] = {
+      "graph_prep", "nbr_sample", "gemm_pool_sigmoid", "gather_max", "gemm_update_relu", "meanpool",
+      "film",       "gemm_qkv",   "seg_attention",     "gemm_out_ln", "gemm_ffn1_relu",  "gemm_ffn2_ln",
+      "head_lse",   "gumbel_sample", "logp_reduce"};
+  if (kind < 0 || kind >= GDP_K_COUNT) return "";
+  return names[kind];
+}

@@ -1,0 +1,369 @@
+// Dense layers on the matrix cores: out = epilogue(A W^T).
+//
+// A is [M, K] and W is [N, K] (each output unit's weights contiguous), so both
+// MFMA operands are K-contiguous.  K may consist of two segments, each with
+// its own activation source and weight array: that is how Eq. 3's
+// f(concat(h_v, h_N(v))) runs without materialising either concatenation.
+//
+// A 256-thread work-group computes a BM x BN tile with four waves; each wave
+// owns a WM x WN sub-tile of 16 x 16 MFMA blocks.  K advances in BK steps
+// through double-buffered LDS tiles (global -> registers for step k+1 while
+// step k is multiplied).  A may be stored in fp32 (the residual stream) and is
+// rounded to the MFMA type on its way into LDS.  The epilogue stages the
+// finished tile in LDS so that every lane writes whole 16-byte chunks.
+#include "device_common.h"
+#include "kernels.h"
+
+namespace gdp {
+
+namespace {
+
+template <typename T> struct KStep { static constexpr int BK = 64; };
+template <> struct KStep<float> { static constexpr int BK = 32; };
+
+template <typename T>
+struct TileCfg {
+  static constexpr int BK = KStep<T>::BK;
+  static constexpr int EPV = 16 / sizeof(T);   // MFMA-type elements per 16 bytes
+  static constexpr int STRIDE = BK + EPV;       // padded LDS row (conflict-free fragment reads)
+};
+
+template <typename TA, typename T> struct Cvt;
+template <typename T> struct Cvt<T, T> {
+  static __device__ __forceinline__ void store(T* lds, const uint4& r) { *reinterpret_cast<uint4*>(lds) = r; }
+};
+template <> struct Cvt<float, bf16> {
+  // 4 floats -> 4 bf16 (8 bytes)
+  static __device__ __forceinline__ void store(bf16* lds, const uint4& r) {
+    const float* f = reinterpret_cast<const float*>(&r);
+    typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
+    bf16x4_t o;
+    o[0] = (bf16)f[0]; o[1] = (bf16)f[1]; o[2] = (bf16)f[2]; o[3] = (bf16)f[3];
+    *reinterpret_cast<bf16x4_t*>(lds) = o;
+  }
+};
+
+// Global -> register staging of a ROWS x BK tile of TA, stored to LDS as T.
+// Chunk c is row c / CPR, columns (c % CPR) * EPA.  Rows >= rows_valid and
+// columns >= cols_valid (the end of the K segment, a multiple of EPA) are
+// never read and stage zeros.
+template <typename TA, typename T, int ROWS>
+struct TileLoader {
+  static constexpr int BK = TileCfg<T>::BK;
+  static constexpr int EPA = 16 / sizeof(TA);
+  static constexpr int CPR = BK / EPA;
+  static constexpr int CHUNKS = ROWS * CPR;
+  static_assert(CHUNKS % 256 == 0, "tile must split evenly over 256 threads");
+  static constexpr int PER = CHUNKS / 256;
+  uint4 r[PER];
+
+  __device__ __forceinline__ void load(const TA* base, int ld, int rows_valid, int k0, int cols_valid) {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int c = threadIdx.x + i * 256;
+      const int row = c / CPR;
+      const int col = (c % CPR) * EPA;
+      if (row < rows_valid && k0 + col < cols_valid)
+        r[i] = *reinterpret_cast<const uint4*>(base + (size_t)row * ld + k0 + col);
+      else
+        r[i] = make_uint4(0u, 0u, 0u, 0u);
+    }
+  }
+  __device__ __forceinline__ void store(T* lds) const {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int c = threadIdx.x + i * 256;
+      const int row = c / CPR;
+      const int col = (c % CPR) * EPA;
+      Cvt<TA, T>::store(lds + row * TileCfg<T>::STRIDE + col, r[i]);
+    }
+  }
+};
+
+// One BK step of a wave's WM x WN sub-tile from LDS.
+template <typename T, int WM, int WN>
+__device__ __forceinline__ void mma_tile(const T* sA, const T* sB, int lane, f32x4 (&acc)[WM / 16][WN / 16]) {
+  using MF = Mfma<T>;
+  constexpr int S = TileCfg<T>::STRIDE;
+  constexpr int BK = TileCfg<T>::BK;
+  const int r = lane & 15, kq = MF::KV * (lane >> 4);
+#pragma unroll
+  for (int ks = 0; ks < BK / MF::K; ++ks) {
+    typename MF::frag a[WM / 16], b[WN / 16];
+#pragma unroll
+    for (int i = 0; i < WM / 16; ++i) a[i] = MF::load(sA + (i * 16 + r) * S + ks * MF::K + kq);
+#pragma unroll
+    for (int j = 0; j < WN / 16; ++j) b[j] = MF::load(sB + (j * 16 + r) * S + ks * MF::K + kq);
+#pragma unroll
+    for (int i = 0; i < WM / 16; ++i)
+#pragma unroll
+      for (int j = 0; j < WN / 16; ++j) acc[i][j] = MF::mma(a[i], b[j], acc[i][j]);
+  }
+}
+
+// Shared main loop: accumulates the block's BM x BN tile of [a1|a2] [w1|w2]^T.
+// Segment 1 of A is stored as TA (fp32 for the residual stream), segment 2 as T.
+template <typename TA, typename T, int BM, int BN, int WM, int WN>
+__device__ __forceinline__ void gemm_mainloop(const TA* a1, int lda1, const T* w1, int k1, const T* a2, int lda2,
+                                              const T* w2, int k2, int M, int m0, int n0, T* sA, T* sB,
+                                              f32x4 (&acc)[WM / 16][WN / 16]) {
+  constexpr int S = TileCfg<T>::STRIDE;
+  constexpr int BK = TileCfg<T>::BK;
+  constexpr int WAVES_N = BN / WN;
+  constexpr bool kSameA = sizeof(TA) == sizeof(T);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = wave / WAVES_N, wn = wave % WAVES_N;
+  // Each K segment is tiled on its own (a segment's last tile may be partial).
+  const int KT1 = (k1 + BK - 1) / BK;
+  const int KT = KT1 + (k2 + BK - 1) / BK;
+  const int rows_a = M - m0;
+
+#pragma unroll
+  for (int i = 0; i < WM / 16; ++i)
+#pragma unroll
+    for (int j = 0; j < WN / 16; ++j) acc[i][j] = zero4();
+
+  TileLoader<TA, T, BM> la1;
+  TileLoader<T, T, BM> la2;
+  TileLoader<T, T, BN> lb;
+  auto load_k = [&](int kt) {
+    if (kt < KT1) {
+      const int k = kt * BK;
+      la1.load(a1 + (size_t)m0 * lda1, lda1, rows_a, k, k1);
+      lb.load(w1 + (size_t)n0 * k1, k1, BN, k, k1);
+    } else {
+      const int k = (kt - KT1) * BK;
+      if constexpr (kSameA)
+        la1.load(reinterpret_cast<const TA*>(a2) + (size_t)m0 * lda2, lda2, rows_a, k, k2);
+      else
+        la2.load(a2 + (size_t)m0 * lda2, lda2, rows_a, k, k2);
+      lb.load(w2 + (size_t)n0 * k2, k2, BN, k, k2);
+    }
+  };
+  auto store_a = [&](int kt, T* dst) {
+    if (kSameA || kt < KT1) la1.store(dst);
+    else la2.store(dst);
+  };
+
+  load_k(0);
+  store_a(0, sA);
+  lb.store(sB);
+  __syncthreads();
+  for (int kt = 0; kt < KT; ++kt) {
+    const int cur = kt & 1;
+    if (kt + 1 < KT) load_k(kt + 1);
+    mma_tile<T, WM, WN>(sA + cur * BM * S + wm * WM * S, sB + cur * BN * S + wn * WN * S, lane, acc);
+    if (kt + 1 < KT) {
+      store_a(kt + 1, sA + (cur ^ 1) * BM * S);
+      lb.store(sB + (cur ^ 1) * BN * S);
+    }
+    __syncthreads();
+  }
+}
+
+__device__ __forceinline__ float sigmoidf_(float z) { return 1.0f / (1.0f + __expf(-z)); }
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+template <typename TA, typename T, typename TO, int BM, int BN, int WM, int WN, int EPI>
+__global__ __launch_bounds__(256) void k_gemm(GemmArgs<TA, T, TO> p) {
+  constexpr int S = TileCfg<T>::STRIDE;
+  constexpr int BYTES_AB = 2 * (BM + BN) * S * (int)sizeof(T);
+  constexpr int EPO = 16 / sizeof(TO);
+  constexpr int CS = BN + EPO;                              // padded C-tile row
+  constexpr int BYTES_C = BM * CS * (int)sizeof(TO);
+  __shared__ __attribute__((aligned(16))) char smem[BYTES_AB > BYTES_C ? BYTES_AB : BYTES_C];
+  T* sA = reinterpret_cast<T*>(smem);
+  T* sB = sA + 2 * BM * S;
+  const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
+  f32x4 acc[WM / 16][WN / 16];
+  gemm_mainloop<TA, T, BM, BN, WM, WN>(p.a1, p.lda1, p.w1, p.k1, p.a2, p.lda2, p.w2, p.k2, p.M, m0, n0, sA, sB, acc);
+
+  // bias + activation, rounded, into the LDS C tile (the main loop ended on a barrier)
+  constexpr int WAVES_N = BN / WN;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = wave / WAVES_N, wn = wave % WAVES_N;
+  TO* sC = reinterpret_cast<TO*>(smem);
+#pragma unroll
+  for (int j = 0; j < WN / 16; ++j) {
+    const int lc = wn * WN + j * 16 + (lane & 15);
+    const float b = to_f32(p.bias[n0 + lc]);
+#pragma unroll
+    for (int i = 0; i < WM / 16; ++i)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int lr = wm * WM + i * 16 + 4 * (lane >> 4) + r;
+        float v = acc[i][j][r] + b;
+        if (EPI == EPI_RELU) v = fmaxf(v, 0.f);
+        if (EPI == EPI_SIGMOID) v = sigmoidf_(v);
+        sC[lr * CS + lc] = from_f32<TO>(v);
+      }
+  }
+  __syncthreads();
+  constexpr int CPR = BN / EPO;
+  for (int c = threadIdx.x; c < BM * CPR; c += 256) {
+    const int lr = c / CPR, lc = (c % CPR) * EPO;
+    const int row = m0 + lr;
+    if (row < p.M)
+      *reinterpret_cast<uint4*>(p.out + (size_t)row * p.ldo + n0 + lc) =
+          *reinterpret_cast<const uint4*>(sC + lr * CS + lc);
+  }
+}
+
+template <typename TA, typename T, typename TO, int BM, int BN, int WM, int WN>
+static hipError_t launch_gemm_cfg(const GemmArgs<TA, T, TO>& a, int epi, hipStream_t s) {
+  dim3 grid(a.N / BN, (a.M + BM - 1) / BM), block(256);
+  switch (epi) {
+    case EPI_BIAS: hipLaunchKernelGGL((k_gemm<TA, T, TO, BM, BN, WM, WN, EPI_BIAS>), grid, block, 0, s, a); break;
+    case EPI_RELU: hipLaunchKernelGGL((k_gemm<TA, T, TO, BM, BN, WM, WN, EPI_RELU>), grid, block, 0, s, a); break;
+    case EPI_SIGMOID:
+      hipLaunchKernelGGL((k_gemm<TA, T, TO, BM, BN, WM, WN, EPI_SIGMOID>), grid, block, 0, s, a);
+      break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+template <typename TA, typename T, typename TO>
+hipError_t launch_gemm(const GemmArgs<TA, T, TO>& a, int epi, hipStream_t s) {
+  if (a.M <= 0) return hipSuccess;
+  // K segments must be whole 16-byte chunks of both A and W (callers pass multiples of 32).
+  if (a.k1 <= 0 || a.k1 % 8 || a.k2 < 0 || a.k2 % 8 || (a.k2 > 0 && (!a.a2 || !a.w2))) return hipErrorInvalidValue;
+  if (a.N % 128 == 0) return launch_gemm_cfg<TA, T, TO, 128, 128, 64, 64>(a, epi, s);
+  if (a.N % 64 == 0) return launch_gemm_cfg<TA, T, TO, 128, 64, 64, 32>(a, epi, s);
+  return hipErrorInvalidValue;
+}
+template hipError_t launch_gemm<float, float, float>(const GemmArgs<float, float, float>&, int, hipStream_t);
+template hipError_t launch_gemm<bf16, bf16, bf16>(const GemmArgs<bf16, bf16, bf16>&, int, hipStream_t);
+template hipError_t launch_gemm<float, bf16, bf16>(const GemmArgs<float, bf16, bf16>&, int, hipStream_t);
+template hipError_t launch_gemm<bf16, bf16, float>(const GemmArgs<bf16, bf16, float>&, int, hipStream_t);
+template hipError_t launch_gemm<float, bf16, float>(const GemmArgs<float, bf16, float>&, int, hipStream_t);
+
+// ---------------------------------------------------------------------------
+// Residual + LayerNorm epilogue over full rows: BM = 64 rows x the whole
+// N = d output row per work-group, 2 x 2 waves (32 rows x N/2 columns each).
+// The residual input and the output are fp32 (the residual stream).  Row
+// statistics: in-lane sums over the wave's column blocks, a 16-lane
+// butterfly, then the two column-half partials through LDS; two passes (mean,
+// then centred second moment).
+template <typename T, int NOUT>
+__global__ __launch_bounds__(256) void k_gemm_ln(GemmLnArgs<T> p, GraphTable gt) {
+  constexpr int BM = 64, WM = 32, WN = NOUT / 2;
+  constexpr int S = TileCfg<T>::STRIDE;
+  __shared__ __attribute__((aligned(16))) T sA[2 * BM * S];
+  __shared__ __attribute__((aligned(16))) T sB[2 * NOUT * S];
+  __shared__ float red[BM][2];
+  const int m0 = blockIdx.x * BM;
+  f32x4 acc[WM / 16][WN / 16];
+  gemm_mainloop<T, T, BM, NOUT, WM, WN>(p.a, p.lda, p.w, p.K, (const T*)nullptr, 0, (const T*)nullptr, 0, p.M, m0, 0,
+                                        sA, sB, acc);
+
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int g4 = lane >> 4;
+
+  // v = acc + bias + residual
+#pragma unroll
+  for (int j = 0; j < WN / 16; ++j) {
+    const int col = wn * WN + j * 16 + (lane & 15);
+    const float b = to_f32(p.bias[col]);
+#pragma unroll
+    for (int i = 0; i < WM / 16; ++i)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int row = m0 + wm * WM + i * 16 + 4 * g4 + r;
+        const float res = row < p.M ? p.res[(size_t)row * p.ldr + col] : 0.f;
+        acc[i][j][r] += b + res;
+      }
+  }
+
+  float mean[WM / 16][4], rstd[WM / 16][4];
+#pragma unroll
+  for (int i = 0; i < WM / 16; ++i)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      float sum = 0.f;
+#pragma unroll
+      for (int j = 0; j < WN / 16; ++j) sum += acc[i][j][r];
+#pragma unroll
+      for (int off = 1; off < 16; off <<= 1) sum += xor_shfl(sum, off);
+      if ((lane & 15) == 0) red[wm * WM + i * 16 + 4 * g4 + r][wn] = sum;
+    }
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < WM / 16; ++i)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int lr = wm * WM + i * 16 + 4 * g4 + r;
+      mean[i][r] = (red[lr][0] + red[lr][1]) * (1.0f / NOUT);
+    }
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < WM / 16; ++i)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      float sum = 0.f;
+#pragma unroll
+      for (int j = 0; j < WN / 16; ++j) {
+        const float dlt = acc[i][j][r] - mean[i][r];
+        sum += dlt * dlt;
+      }
+#pragma unroll
+      for (int off = 1; off < 16; off <<= 1) sum += xor_shfl(sum, off);
+      if ((lane & 15) == 0) red[wm * WM + i * 16 + 4 * g4 + r][wn] = sum;
+    }
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < WM / 16; ++i)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int lr = wm * WM + i * 16 + 4 * g4 + r;
+      rstd[i][r] = rsqrtf((red[lr][0] + red[lr][1]) * (1.0f / NOUT) + 1e-5f);
+    }
+
+  int gid[WM / 16][4];
+#pragma unroll
+  for (int i = 0; i < WM / 16; ++i)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int row = m0 + wm * WM + i * 16 + 4 * g4 + r;
+      gid[i][r] = p.film_gamma ? graph_of_node(gt, row < p.M ? row : p.M - 1) : 0;
+    }
+
+#pragma unroll
+  for (int j = 0; j < WN / 16; ++j) {
+    const int col = wn * WN + j * 16 + (lane & 15);
+    const float lg = to_f32(p.ln_g[col]), lb = to_f32(p.ln_b[col]);
+#pragma unroll
+    for (int i = 0; i < WM / 16; ++i)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int row = m0 + wm * WM + i * 16 + 4 * g4 + r;
+        float y = (acc[i][j][r] - mean[i][r]) * rstd[i][r] * lg + lb;
+        if (p.film_gamma) {
+          const size_t o = (size_t)gid[i][r] * p.film_stride + col;
+          y = p.film_gamma[o] * y + p.film_beta[o];
+        }
+        if (row < p.M) p.out[(size_t)row * p.ldo + col] = y;
+      }
+  }
+}
+
+template <typename T>
+hipError_t launch_gemm_ln(const GemmLnArgs<T>& a, const GraphTable& gt, hipStream_t s) {
+  if (a.M <= 0) return hipSuccess;
+  if (a.K <= 0 || a.K % 8) return hipErrorInvalidValue;
+  dim3 grid((a.M + 63) / 64), block(256);
+  switch (a.N) {
+    case 64: hipLaunchKernelGGL((k_gemm_ln<T, 64>), grid, block, 0, s, a, gt); break;
+    case 128: hipLaunchKernelGGL((k_gemm_ln<T, 128>), grid, block, 0, s, a, gt); break;
+    case 256: hipLaunchKernelGGL((k_gemm_ln<T, 256>), grid, block, 0, s, a, gt); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+template hipError_t launch_gemm_ln<float>(const GemmLnArgs<float>&, const GraphTable&, hipStream_t);
+template hipError_t launch_gemm_ln<bf16>(const GemmLnArgs<bf16>&, const GraphTable&, hipStream_t);
+
+}  // namespace gdp

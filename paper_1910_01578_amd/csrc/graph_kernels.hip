@@ -1,0 +1,474 @@
+// Section 3.1 kernels: neighbourhood construction, neighbour sampling, the
+// Eq. 2 max-pool gather and the per-graph mean pool.
+#include "device_common.h"
+#include "kernels.h"
+
+namespace gdp {
+
+// ---------------------------------------------------------------------------
+__global__ void k_fill_i32(int* p, int64_t n, int value) {
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x)
+    p[i] = value;
+}
+
+hipError_t launch_fill_i32(int* p, int64_t n, int value, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  int64_t blocks = (n + 255) / 256;
+  if (blocks > 4096) blocks = 4096;
+  hipLaunchKernelGGL(k_fill_i32, dim3((unsigned)blocks), dim3(256), 0, s, p, n, value);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// in_deg[v] += 1 for every edge u -> v (integer atomics: order-independent).
+__global__ void k_in_degree(const int* __restrict__ col_idx, int64_t n_edges, int* in_deg) {
+  for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < n_edges;
+       e += (int64_t)gridDim.x * blockDim.x)
+    atomicAdd(&in_deg[col_idx[e]], 1);
+}
+
+hipError_t launch_in_degree(const int* col_idx, int64_t n_edges, int* in_deg, hipStream_t s) {
+  if (n_edges <= 0) return hipSuccess;
+  int64_t blocks = (n_edges + 255) / 256;
+  if (blocks > 8192) blocks = 8192;
+  hipLaunchKernelGGL(k_in_degree, dim3((unsigned)blocks), dim3(256), 0, s, col_idx, n_edges, in_deg);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Exclusive scans of the two degree arrays, in three launches:
+//   in_ptr[i] = sum_{j<i} in_deg[j]
+//   s_ptr[i]  = sum_{j<i} min(out_deg[j] + in_deg[j], fanout)
+// (1) per-block totals of kScanBlock entries, (2) one work-group scans the
+// block totals, (3) every block scans its entries and adds its offset.
+__device__ __forceinline__ int wave_incl_scan(int v, int lane) {
+#pragma unroll
+  for (int off = 1; off < kWave; off <<= 1) {
+    int t = __shfl_up(v, off, kWave);
+    if (lane >= off) v += t;
+  }
+  return v;
+}
+
+__device__ __forceinline__ void degree_pair(const int* __restrict__ row_ptr, const int* __restrict__ in_deg,
+                                            int i, int n, int fanout, int& da, int& db) {
+  da = 0;
+  db = 0;
+  if (i < n) {
+    da = in_deg[i];
+    const int tot = da + (row_ptr[i + 1] - row_ptr[i]);
+    db = tot < fanout ? tot : fanout;
+  }
+}
+
+// Block-wide exclusive scan of (a, b) pairs held one per thread (256 threads);
+// returns the exclusive prefixes and writes the block totals to *ta / *tb.
+__device__ __forceinline__ void block_scan2(int a, int b, int& ea, int& eb, int* ta, int* tb) {
+  __shared__ int wa[4], wb[4];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int ia = wave_incl_scan(a, lane), ib = wave_incl_scan(b, lane);
+  if (lane == 63) { wa[wave] = ia; wb[wave] = ib; }
+  __syncthreads();
+  int oa = 0, ob = 0;
+  for (int w = 0; w < wave; ++w) { oa += wa[w]; ob += wb[w]; }
+  ea = oa + ia - a;
+  eb = ob + ib - b;
+  if (ta) *ta = wa[0] + wa[1] + wa[2] + wa[3];
+  if (tb) *tb = wb[0] + wb[1] + wb[2] + wb[3];
+  __syncthreads();
+}
+
+__global__ __launch_bounds__(256) void k_scan_block_sums(const int* __restrict__ row_ptr,
+                                                         const int* __restrict__ in_deg, int n, int fanout,
+                                                         int* __restrict__ bsum) {
+  const int base = blockIdx.x * kScanBlock + threadIdx.x * 4;
+  int sa = 0, sb = 0;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    int da, db;
+    degree_pair(row_ptr, in_deg, base + j, n, fanout, da, db);
+    sa += da;
+    sb += db;
+  }
+  int ea, eb, ta, tb;
+  block_scan2(sa, sb, ea, eb, &ta, &tb);
+  if (threadIdx.x == 0) {
+    bsum[2 * blockIdx.x] = ta;
+    bsum[2 * blockIdx.x + 1] = tb;
+  }
+}
+
+__global__ __launch_bounds__(256) void k_scan_block_offsets(int* __restrict__ bsum, int nblocks, int n,
+                                                            int* __restrict__ in_ptr, int* __restrict__ s_ptr) {
+  int carry_a = 0, carry_b = 0;
+  for (int base = 0; base < nblocks; base += 256) {
+    const int i = base + threadIdx.x;
+    const int a = i < nblocks ? bsum[2 * i] : 0, b = i < nblocks ? bsum[2 * i + 1] : 0;
+    int ea, eb, ta, tb;
+    block_scan2(a, b, ea, eb, &ta, &tb);
+    if (i < nblocks) {
+      bsum[2 * i] = carry_a + ea;
+      bsum[2 * i + 1] = carry_b + eb;
+    }
+    carry_a += ta;
+    carry_b += tb;
+  }
+  if (threadIdx.x == 0) {
+    in_ptr[n] = carry_a;
+    s_ptr[n] = carry_b;
+  }
+}
+
+__global__ __launch_bounds__(256) void k_scan_apply(const int* __restrict__ row_ptr, const int* __restrict__ in_deg,
+                                                    int n, int fanout, const int* __restrict__ boff,
+                                                    int* __restrict__ in_ptr, int* __restrict__ s_ptr) {
+  const int base = blockIdx.x * kScanBlock + threadIdx.x * 4;
+  int da[4], db[4], sa = 0, sb = 0;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    degree_pair(row_ptr, in_deg, base + j, n, fanout, da[j], db[j]);
+    sa += da[j];
+    sb += db[j];
+  }
+  int ea, eb;
+  block_scan2(sa, sb, ea, eb, nullptr, nullptr);
+  ea += boff[2 * blockIdx.x];
+  eb += boff[2 * blockIdx.x + 1];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int i = base + j;
+    if (i < n) { in_ptr[i] = ea; s_ptr[i] = eb; }
+    ea += da[j];
+    eb += db[j];
+  }
+}
+
+hipError_t launch_scan_degrees(const int* row_ptr, const int* in_deg, int n, int fanout, int* in_ptr,
+                               int* s_ptr, int* block_tmp, hipStream_t s) {
+  const int nb = (n + kScanBlock - 1) / kScanBlock;
+  hipLaunchKernelGGL(k_scan_block_sums, dim3(nb), dim3(256), 0, s, row_ptr, in_deg, n, fanout, block_tmp);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_scan_block_offsets, dim3(1), dim3(256), 0, s, block_tmp, nb, n, in_ptr, s_ptr);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_scan_apply, dim3(nb), dim3(256), 0, s, row_ptr, in_deg, n, fanout, block_tmp, in_ptr, s_ptr);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Reverse edges: in_idx[in_ptr[v] + slot] = u for every u -> v.  Slot order is
+// whatever the atomics give; every consumer is order-invariant.
+__global__ void k_fill_reverse(const int* __restrict__ row_ptr, const int* __restrict__ col_idx,
+                               const int* __restrict__ in_ptr, int n, int* cursor,
+                               int* __restrict__ in_idx) {
+  const int u = blockIdx.x * blockDim.x + threadIdx.x;
+  if (u >= n) return;
+  for (int e = row_ptr[u]; e < row_ptr[u + 1]; ++e) {
+    const int v = col_idx[e];
+    const int slot = atomicAdd(&cursor[v], 1);
+    in_idx[in_ptr[v] + slot] = u;
+  }
+}
+
+hipError_t launch_fill_reverse(const int* row_ptr, const int* col_idx, const int* in_ptr, int n,
+                               int* cursor, int* in_idx, hipStream_t s) {
+  hipLaunchKernelGGL(k_fill_reverse, dim3((n + 255) / 256), dim3(256), 0, s, row_ptr, col_idx,
+                     in_ptr, n, cursor, in_idx);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// S(v): all neighbours when |N(v)| <= fanout, else the fanout smallest
+// (key, u) with key = word 0 of Philox4x64-10((v-g0, u-g0, 1, 0), (seed, 0)).
+//
+// Pass 1 (one thread per node) copies N(v) for the light nodes and queues the
+// heavy ones (|N(v)| > fanout).  Pass 2 gives every heavy node a wavefront:
+// lanes draw the keys of up to 64 * kHeavyPerLane neighbours at once, a
+// radix select over the 64-bit keys finds the fanout-th smallest key T, and
+// every neighbour with key < T is taken plus the smallest ids among the ones
+// with key == T.  Nodes with more neighbours than that use a sorted register
+// list on one lane.
+__device__ __forceinline__ int nbr_at(const int* __restrict__ col_idx, const int* __restrict__ in_idx, int o0,
+                                      int n_out, int i0, int e) {
+  return e < n_out ? col_idx[o0 + e] : in_idx[i0 + e - n_out];
+}
+
+__global__ __launch_bounds__(256) void k_nbr_light(const int* __restrict__ row_ptr, const int* __restrict__ col_idx,
+                                                   const int* __restrict__ in_ptr, const int* __restrict__ in_idx,
+                                                   const int* __restrict__ s_ptr, int n, int fanout,
+                                                   int* __restrict__ s_idx, int* heavy, int* heavy_count) {
+  const int v = blockIdx.x * blockDim.x + threadIdx.x;
+  if (v >= n) return;
+  const int o0 = row_ptr[v], o1 = row_ptr[v + 1];
+  const int i0 = in_ptr[v], i1 = in_ptr[v + 1];
+  const int deg = (o1 - o0) + (i1 - i0);
+  if (deg > fanout) {
+    heavy[atomicAdd(heavy_count, 1)] = v;
+    return;
+  }
+  int* out = s_idx + s_ptr[v];
+  int w = 0;
+  for (int e = o0; e < o1; ++e) out[w++] = col_idx[e];
+  for (int e = i0; e < i1; ++e) out[w++] = in_idx[e];
+}
+
+__device__ __forceinline__ bool pair_less(uint64_t ka, int ua, uint64_t kb, int ub) {
+  return ka < kb || (ka == kb && ua < ub);
+}
+
+// One lane, any degree: keep the MAXF smallest pairs in a sorted register list.
+template <int MAXF>
+__device__ void select_serial(const int* __restrict__ col_idx, const int* __restrict__ in_idx, int o0, int n_out,
+                              int i0, int deg, int v_loc, int g0, int fanout, uint64_t seed, int* out) {
+  uint64_t key[MAXF];
+  int id[MAXF];
+#pragma unroll
+  for (int i = 0; i < MAXF; ++i) { key[i] = ~0ull; id[i] = 0x7fffffff; }
+  for (int e = 0; e < deg; ++e) {
+    const int u = nbr_at(col_idx, in_idx, o0, n_out, i0, e);
+    const uint64_t k = philox4x64_10((uint64_t)v_loc, (uint64_t)(u - g0), 1ull, 0ull, seed, 0ull).w[0];
+#pragma unroll
+    for (int i = MAXF - 1; i >= 0; --i) {
+      const int ip = i > 0 ? i - 1 : 0;
+      const bool shift = (i > 0) && pair_less(k, u, key[ip], id[ip]);
+      if (shift) { key[i] = key[ip]; id[i] = id[ip]; }
+      else if (pair_less(k, u, key[i], id[i])) { key[i] = k; id[i] = u; }
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < MAXF; ++i)
+    if (i < fanout) out[i] = id[i];
+}
+
+constexpr int kHeavyPerLane = 8;
+
+__global__ __launch_bounds__(256) void k_nbr_heavy(const int* __restrict__ row_ptr, const int* __restrict__ col_idx,
+                                                   const int* __restrict__ in_ptr, const int* __restrict__ in_idx,
+                                                   const int* __restrict__ s_ptr, int fanout, uint64_t seed,
+                                                   GraphTable gt, const int* __restrict__ heavy,
+                                                   const int* __restrict__ heavy_count, int* __restrict__ s_idx) {
+  const int lane = threadIdx.x & 63;
+  const int wave = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int nwaves = gridDim.x * 4;
+  const int count = *heavy_count;
+  for (int h = wave; h < count; h += nwaves) {
+    const int v = heavy[h];
+    const int o0 = row_ptr[v], n_out = row_ptr[v + 1] - o0;
+    const int i0 = in_ptr[v], deg = n_out + (in_ptr[v + 1] - i0);
+    const int g0 = gt.ptr[graph_of_node(gt, v)];
+    int* out = s_idx + s_ptr[v];
+    if (deg > 64 * kHeavyPerLane) {
+      if (lane == 0) select_serial<GDP_MAX_FANOUT>(col_idx, in_idx, o0, n_out, i0, deg, v - g0, g0, fanout, seed, out);
+      continue;
+    }
+    uint64_t key[kHeavyPerLane];
+    int id[kHeavyPerLane];
+#pragma unroll
+    for (int r = 0; r < kHeavyPerLane; ++r) {
+      const int e = lane + 64 * r;
+      key[r] = ~0ull;
+      id[r] = 0x7fffffff;
+      if (e < deg) {
+        id[r] = nbr_at(col_idx, in_idx, o0, n_out, i0, e);
+        key[r] = philox4x64_10((uint64_t)(v - g0), (uint64_t)(id[r] - g0), 1ull, 0ull, seed, 0ull).w[0];
+      }
+    }
+    // radix select: T = the fanout-th smallest key; need = how many key == T to take
+    uint64_t prefix = 0;
+    int need = fanout;
+    for (int bit = 63; bit >= 0; --bit) {
+      const uint64_t hi_mask = (bit == 63) ? 0ull : (~0ull << (bit + 1));
+      int c0 = 0;
+#pragma unroll
+      for (int r = 0; r < kHeavyPerLane; ++r) {
+        const int e = lane + 64 * r;
+        const bool m = e < deg && ((key[r] & hi_mask) == prefix) && !((key[r] >> bit) & 1ull);
+        c0 += __popcll(__ballot(m));
+      }
+      if (need > c0) {
+        prefix |= (1ull << bit);
+        need -= c0;
+      }
+    }
+    const uint64_t T = prefix;
+    // take every key < T, then the `need` smallest ids among key == T
+    int base = 0;
+    const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+#pragma unroll
+    for (int r = 0; r < kHeavyPerLane; ++r) {
+      const int e = lane + 64 * r;
+      const bool sel = e < deg && key[r] < T;
+      const uint64_t bal = __ballot(sel);
+      if (sel) out[base + __popcll(bal & lt_mask)] = id[r];
+      base += __popcll(bal);
+    }
+    int last = -1;   // ids strictly above `last` are still eligible
+    for (int t = 0; t < need; ++t) {
+      int best = 0x7fffffff;
+#pragma unroll
+      for (int r = 0; r < kHeavyPerLane; ++r) {
+        const int e = lane + 64 * r;
+        if (e < deg && key[r] == T && id[r] > last && id[r] < best) best = id[r];
+      }
+#pragma unroll
+      for (int off = 32; off >= 1; off >>= 1) best = min(best, xor_shfl(best, off));
+      if (lane == 0) out[base] = best;
+      ++base;
+      last = best;
+    }
+  }
+}
+
+hipError_t launch_nbr_sample(const int* row_ptr, const int* col_idx, const int* in_ptr, const int* in_idx,
+                             const int* s_ptr, int n, int fanout, uint64_t seed, const GraphTable& gt, int* s_idx,
+                             int* heavy, int* heavy_count, hipStream_t s) {
+  hipLaunchKernelGGL(k_nbr_light, dim3((n + 255) / 256), dim3(256), 0, s, row_ptr, col_idx, in_ptr, in_idx, s_ptr, n,
+                     fanout, s_idx, heavy, heavy_count);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_nbr_heavy, dim3(256), dim3(256), 0, s, row_ptr, col_idx, in_ptr, in_idx, s_ptr, fanout, seed,
+                     gt, heavy, heavy_count, s_idx);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Eq. 2 gather: one wavefront per node.  A row of P is H * sizeof(T) bytes,
+// read as 16-byte lane chunks; LPR lanes cover a row, so 64 / LPR neighbour
+// rows are in flight per load instruction (twice that per unrolled step).
+// The running max starts at 0: sigmoid outputs are positive, so this equals
+// the max over a non-empty set and gives 0 for an empty one.
+template <typename T, int H>
+__global__ __launch_bounds__(256) void k_gather_max(const T* __restrict__ P,
+                                                    const int* __restrict__ s_ptr,
+                                                    const int* __restrict__ s_idx, int n,
+                                                    T* __restrict__ A) {
+  constexpr int VEC = 16 / sizeof(T);
+  constexpr int LPR = H / VEC;
+  static_assert(LPR >= 1 && LPR <= 64 && (64 % LPR) == 0, "row width");
+  constexpr int RPW = 64 / LPR;
+  const int lane = threadIdx.x & 63;
+  const int v = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (v >= n) return;
+  const int grp = lane / LPR;
+  const int col = (lane % LPR) * VEC;
+  const int b = s_ptr[v], e = s_ptr[v + 1];
+  float m[VEC];
+#pragma unroll
+  for (int j = 0; j < VEC; ++j) m[j] = 0.f;
+  int i = b + grp;
+  for (; i + RPW < e; i += 2 * RPW) {
+    const int u0 = s_idx[i], u1 = s_idx[i + RPW];
+    const Vec16<T> r0 = load16(P + (size_t)u0 * H + col);
+    const Vec16<T> r1 = load16(P + (size_t)u1 * H + col);
+#pragma unroll
+    for (int j = 0; j < VEC; ++j) m[j] = fmaxf(m[j], fmaxf(to_f32(r0.v[j]), to_f32(r1.v[j])));
+  }
+  if (i < e) {
+    const Vec16<T> r0 = load16(P + (size_t)s_idx[i] * H + col);
+#pragma unroll
+    for (int j = 0; j < VEC; ++j) m[j] = fmaxf(m[j], to_f32(r0.v[j]));
+  }
+#pragma unroll
+  for (int off = LPR; off < 64; off <<= 1)
+#pragma unroll
+    for (int j = 0; j < VEC; ++j) m[j] = fmaxf(m[j], xor_shfl(m[j], off));
+  if (grp == 0) {
+    Vec16<T> o;
+#pragma unroll
+    for (int j = 0; j < VEC; ++j) o.v[j] = from_f32<T>(m[j]);
+    store16(A + (size_t)v * H + col, o);
+  }
+}
+
+template <typename T>
+hipError_t launch_gather_max(const T* P, const int* s_ptr, const int* s_idx, int n, int H, T* A,
+                             hipStream_t s) {
+  dim3 grid((n + 3) / 4), block(256);
+  switch (H) {
+    case 64: hipLaunchKernelGGL((k_gather_max<T, 64>), grid, block, 0, s, P, s_ptr, s_idx, n, A); break;
+    case 128: hipLaunchKernelGGL((k_gather_max<T, 128>), grid, block, 0, s, P, s_ptr, s_idx, n, A); break;
+    case 256: hipLaunchKernelGGL((k_gather_max<T, 256>), grid, block, 0, s, P, s_ptr, s_idx, n, A); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+template hipError_t launch_gather_max<float>(const float*, const int*, const int*, int, int, float*, hipStream_t);
+template hipError_t launch_gather_max<bf16>(const bf16*, const int*, const int*, int, int, bf16*, hipStream_t);
+
+// ---------------------------------------------------------------------------
+// Mean pool: chunks of kMeanpoolRows rows never cross a graph.  Each chunk sum
+// adds its rows in a fixed order (16-byte row slices, then the row groups in
+// LDS); each graph then adds its chunk sums in 16 interleaved fixed-order
+// slices combined in a fixed tree.  Deterministic.
+template <typename T, int H>
+__global__ __launch_bounds__(256) void k_meanpool_partial(const T* __restrict__ h, GraphTable ct,
+                                                          float* __restrict__ partial) {
+  constexpr int EPV = 16 / sizeof(T);
+  constexpr int TPR = H / EPV;
+  constexpr int RG = 256 / TPR;
+  __shared__ float red[RG][H];
+  const int c = blockIdx.x;
+  const int g = graph_of_block(ct, c);
+  const int r0 = ct.ptr[g] + (c - ct.blk[g]) * kMeanpoolRows;
+  const int r1 = min(r0 + kMeanpoolRows, ct.ptr[g + 1]);
+  const int rg = threadIdx.x / TPR, col = (threadIdx.x % TPR) * EPV;
+  float acc[EPV];
+#pragma unroll
+  for (int e = 0; e < EPV; ++e) acc[e] = 0.f;
+  for (int r = r0 + rg; r < r1; r += RG) {
+    const Vec16<T> x = load16(h + (size_t)r * H + col);
+#pragma unroll
+    for (int e = 0; e < EPV; ++e) acc[e] += to_f32(x.v[e]);
+  }
+#pragma unroll
+  for (int e = 0; e < EPV; ++e) red[rg][col + e] = acc[e];
+  __syncthreads();
+  for (int i = threadIdx.x; i < H; i += 256) {
+    float sum = 0.f;
+    for (int q = 0; q < RG; ++q) sum += red[q][i];
+    partial[(size_t)c * H + i] = sum;
+  }
+}
+
+__global__ __launch_bounds__(256) void k_meanpool_final(const float* __restrict__ partial, int H, GraphTable ct,
+                                                        float* __restrict__ out) {
+  __shared__ float red[16][16];
+  const int g = blockIdx.x;
+  const int cl = threadIdx.x & 15, sl = threadIdx.x >> 4;
+  const int col = blockIdx.y * 16 + cl;
+  float acc = 0.f;
+  if (col < H)
+    for (int c = ct.blk[g] + sl; c < ct.blk[g + 1]; c += 16) acc += partial[(size_t)c * H + col];
+  red[sl][cl] = acc;
+  __syncthreads();
+  if (sl == 0 && col < H) {
+    float t[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) t[i] = red[2 * i][cl] + red[2 * i + 1][cl];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) t[i] = t[2 * i] + t[2 * i + 1];
+    const float sum = (t[0] + t[1]) + (t[2] + t[3]);
+    out[(size_t)g * H + col] = sum / (float)(ct.ptr[g + 1] - ct.ptr[g]);
+  }
+}
+
+template <typename T>
+hipError_t launch_meanpool(const T* h, int H, const GraphTable& ct, int total_chunks, float* partial,
+                           float* graph_emb, hipStream_t s) {
+  switch (H) {
+    case 64: hipLaunchKernelGGL((k_meanpool_partial<T, 64>), dim3(total_chunks), dim3(256), 0, s, h, ct, partial); break;
+    case 128: hipLaunchKernelGGL((k_meanpool_partial<T, 128>), dim3(total_chunks), dim3(256), 0, s, h, ct, partial); break;
+    case 256: hipLaunchKernelGGL((k_meanpool_partial<T, 256>), dim3(total_chunks), dim3(256), 0, s, h, ct, partial); break;
+    default: return hipErrorInvalidValue;
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_meanpool_final, dim3(ct.n, (H + 15) / 16), dim3(256), 0, s, partial, H, ct, graph_emb);
+  return hipGetLastError();
+}
+template hipError_t launch_meanpool<float>(const float*, int, const GraphTable&, int, float*, float*, hipStream_t);
+template hipError_t launch_meanpool<bf16>(const bf16*, int, const GraphTable&, int, float*, float*, hipStream_t);
+
+}  // namespace gdp

@@ -1,0 +1,63 @@
+// Host-only argument checks and workspace planning (no HIP dependency, so the
+// same file also builds with a plain C++ compiler for sanitizer runs).
+#pragma once
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include "gdp.h"
+
+namespace gdp {
+
+// Thread-local error reporting; returns `code` for convenient `return fail(...)`.
+int fail(int code, const char* fmt, ...);
+void clear_error();
+
+// Field checks of the structs (no device memory is read).
+int check_graph(const gdp_graph* g);
+int check_gnn(const gdp_graph* g, const gdp_gnn* gnn);
+int check_placer(const gdp_graph* g, const gdp_placer* p);
+int check_sample(const gdp_graph* g, int32_t n_devices, int32_t k_samples);
+
+size_t elem_size(int32_t dtype);
+
+// Sub-allocations of one call, each 256-byte aligned.
+struct Carve {
+  size_t off[24];
+  size_t total;
+  int n;
+};
+void carve_init(Carve* c);
+size_t carve_add(Carve* c, size_t bytes);   // returns the offset of the new region
+
+// Per-graph block counts -> prefix (blk[0] = 0 .. blk[G] = total).
+int prefix_blocks_rows(const int32_t* graph_ptr, int G, int rows_per_block, int32_t* blk);
+int prefix_blocks_attention(const int32_t* graph_ptr, int G, int seg_len, int block_q, int32_t* blk);
+
+struct EmbedPlan {
+  Carve c;
+  size_t counters;   // [in_deg: N | cursor: N | heavy_count: 1], zeroed by one fill
+  size_t scan_tmp, heavy;
+  size_t in_ptr, in_idx, s_ptr, s_idx, P, A, h0, h1, pool;
+  int64_t s_cap;
+  int pool_chunks;
+};
+struct PlacePlan {
+  Carve c;
+  size_t film, y0, y1, qkv, o, z, h1;
+  int qblocks;
+};
+struct SamplePlan {
+  Carve c;
+  size_t partial;
+  int chunks;
+};
+void plan_embed(const gdp_graph* g, const gdp_gnn* gnn, EmbedPlan* p);
+void plan_place(const gdp_graph* g, const gdp_placer* pl, PlacePlan* p);
+void plan_sample(const gdp_graph* g, int32_t k_samples, SamplePlan* p);
+
+constexpr int kPoolRows = 256;      // rows per mean-pool chunk
+constexpr int kAttnQ = 128;         // queries per attention work-group
+constexpr int kSampleRows = 256;    // nodes per sampling work-group
+
+}  // namespace gdp

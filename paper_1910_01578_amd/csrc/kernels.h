@@ -1,0 +1,112 @@
+// Internal launch interface between the host API (gdp_api.cpp) and the
+// kernels.  Every launcher enqueues on `s` and returns the launch status.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "gdp.h"
+
+namespace gdp {
+
+struct GraphTable;
+
+// ---- graph preparation and Section 3.1 -------------------------------------
+hipError_t launch_fill_i32(int* p, int64_t n, int value, hipStream_t s);
+hipError_t launch_in_degree(const int* col_idx, int64_t n_edges, int* in_deg, hipStream_t s);
+// block_tmp: 2 * ceil(n / kScanBlock) ints of scratch.
+constexpr int kScanBlock = 1024;
+hipError_t launch_scan_degrees(const int* row_ptr, const int* in_deg, int n, int fanout,
+                               int* in_ptr, int* s_ptr, int* block_tmp, hipStream_t s);
+hipError_t launch_fill_reverse(const int* row_ptr, const int* col_idx, const int* in_ptr, int n,
+                               int* cursor, int* in_idx, hipStream_t s);
+// heavy: n ints of scratch; heavy_count: one int, zero on entry.
+hipError_t launch_nbr_sample(const int* row_ptr, const int* col_idx, const int* in_ptr,
+                             const int* in_idx, const int* s_ptr, int n, int fanout,
+                             uint64_t seed, const GraphTable& gt, int* s_idx, int* heavy,
+                             int* heavy_count, hipStream_t s);
+// A[v] = max over S(v) of P rows (0 if empty); P, A: [n, H] of type T.
+template <typename T>
+hipError_t launch_gather_max(const T* P, const int* s_ptr, const int* s_idx, int n, int H, T* A,
+                             hipStream_t s);
+// graph_emb[g] = mean of h rows of graph g (fixed-order two-pass reduction).
+template <typename T>
+hipError_t launch_meanpool(const T* h, int H, const GraphTable& chunks, int total_chunks,
+                           float* partial, float* graph_emb, hipStream_t s);
+constexpr int kMeanpoolRows = 256;
+
+// ---- dense layers -------------------------------------------------------------
+enum Epilogue { EPI_BIAS = 0, EPI_RELU = 1, EPI_SIGMOID = 2 };
+
+// out[M, N] = act([a1 | a2] [w1 | w2]^T + bias): two K-segments, each with its
+// own activation source and weight array (a2/w2 may be null with k2 = 0).
+// TA: storage type of segment 1 of A (fp32 for the residual stream and the
+// GNN's hidden layers); segment 2 of A, the weights and the MFMA use T; TO is
+// the output type.
+template <typename TA, typename T, typename TO>
+struct GemmArgs {
+  const TA* a1; int lda1; const T* w1; int k1;   // a1 [M, lda1], w1 [N, k1]
+  const T* a2; int lda2; const T* w2; int k2;    // a2 [M, lda2], w2 [N, k2]
+  const T* bias;    // [N]
+  TO* out; int ldo;
+  int M, N;
+};
+template <typename TA, typename T, typename TO>
+hipError_t launch_gemm(const GemmArgs<TA, T, TO>& a, int epi, hipStream_t s);
+
+// out[M, N] = FiLM(LN(res + A W^T + bias)), N = the full row (64, 128 or 256).
+// res and out belong to the residual stream and are fp32.  FiLM (optional)
+// applies the per-graph gamma/beta of the *next* layer.
+template <typename T>
+struct GemmLnArgs {
+  const T* a; int lda; int K;
+  const T* w;       // [N, K]
+  const T* bias;    // [N]
+  const float* res; int ldr;
+  const T* ln_g; const T* ln_b;
+  const float* film_gamma;  // [G, film_stride] or null
+  const float* film_beta;   // [G, film_stride]
+  int film_stride;
+  float* out; int ldo;
+  int M, N;
+};
+template <typename T>
+hipError_t launch_gemm_ln(const GemmLnArgs<T>& a, const GraphTable& gt, hipStream_t s);
+
+// ---- Section 3.2 / 3.3 --------------------------------------------------------
+// Segment attention.  qkv: [N, 3d]; out: [N, d].  gt.blk = per-graph prefix of
+// 128-query blocks.
+template <typename T>
+struct AttnArgs {
+  const T* qkv; int ldq;
+  T* out; int ldo;
+  int d, heads, seg_len, mem_len;
+  int total_qblocks;
+};
+constexpr int kAttnBlockQ = 128;
+template <typename T>
+hipError_t launch_attention(const AttnArgs<T>& a, const GraphTable& gt, hipStream_t s);
+
+// gamma[l][g][c] = 1 + W_g x0_g + b_g, beta[l][g][c] = W_b x0_g + b_b for one layer l.
+template <typename T>
+hipError_t launch_film_gemv(const T* wg, const T* bg, const T* wb, const T* bb, const float* x0,
+                            int G, int d, int H, float* gamma, float* beta, hipStream_t s);
+// y (fp32) = gamma[g(v)] * x + beta[g(v)] for every row v; plain widening when gamma is null.
+template <typename T>
+hipError_t launch_film_apply(const T* x, const float* gamma, const float* beta, int n, int d,
+                             const GraphTable& gt, float* y, hipStream_t s);
+// logits[v] = x[v] W_out^T + b_out (fp32), lse[v] (nullable); x is the fp32 residual stream.
+template <typename T>
+hipError_t launch_head(const float* x, const T* w_out, const T* b_out, int n, int d, int D,
+                       float* logits, float* lse, hipStream_t s);
+
+// ---- sampling ---------------------------------------------------------------
+constexpr int kSampleChunk = 256;
+hipError_t launch_sample(const float* logits, const float* lse, int n, int D, int K, uint64_t seed,
+                         const float* uniforms, const GraphTable& chunks, int total_chunks,
+                         int* placements, float* partial, hipStream_t s);
+hipError_t launch_logp_reduce(const float* partial, const GraphTable& chunks, int total_chunks, int K,
+                              float* logp, hipStream_t s);
+hipError_t launch_debug_uniforms(uint64_t seed, int n, int K, int D, float* out, hipStream_t s);
+
+}  // namespace gdp

@@ -1,0 +1,268 @@
+"""Thin ctypes binding of libgdp (the C ABI in include/gdp.h).
+
+Only argument marshalling happens here: torch tensors provide device memory
+and the current HIP stream; every step of the forward pass runs in the
+library's HIP kernels.  Importing this module fails loudly when libgdp.so has
+not been built -- there is no CPU fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from ctypes import POINTER, c_char_p, c_double, c_int32, c_int64, c_size_t, c_uint32, c_uint64, c_void_p
+from typing import Dict, Optional
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libgdp.so")
+
+GDP_OK = 0
+GDP_E_INVALID_ARG = -1
+GDP_E_BAD_GRAPH = -2
+GDP_E_UNSUPPORTED = -3
+GDP_E_WORKSPACE = -4
+GDP_E_HIP = -5
+GDP_F32 = 0
+GDP_BF16 = 1
+GDP_TOPO_IDS = 1
+GDP_MAX_GRAPHS = 128
+
+KERNEL_KINDS = ["graph_prep", "nbr_sample", "gemm_pool_sigmoid", "gather_max", "gemm_update_relu",
+                "meanpool", "film", "gemm_qkv", "seg_attention", "gemm_out_ln", "gemm_ffn1_relu",
+                "gemm_ffn2_ln", "head_lse", "gumbel_sample", "logp_reduce"]
+K_COUNT = len(KERNEL_KINDS)
+
+
+class GdpError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"libgdp error {code}: {msg}")
+        self.code = code
+
+
+class GdpGraph(ctypes.Structure):
+    _fields_ = [("n_graphs", c_int32), ("graph_ptr_h", POINTER(c_int32)), ("n_nodes", c_int32),
+                ("row_ptr", c_void_p), ("col_idx", c_void_p), ("n_edges", c_int64), ("x", c_void_p),
+                ("feat_dim", c_int32), ("dtype", c_int32), ("flags", c_uint32)]
+
+
+class GdpGnnLayer(ctypes.Structure):
+    _fields_ = [(n, c_void_p) for n in ("w_pool", "b_pool", "w_self", "w_neigh", "b_upd")]
+
+
+class GdpGnn(ctypes.Structure):
+    _fields_ = [("n_layers", c_int32), ("in_dim", c_int32), ("hidden", c_int32), ("fanout", c_int32),
+                ("nbr_seed", c_uint64), ("layers", POINTER(GdpGnnLayer))]
+
+
+PLACER_LAYER_FIELDS = ("film_wg", "film_bg", "film_wb", "film_bb", "w_qkv", "b_qkv", "w_o", "b_o",
+                       "ln1_g", "ln1_b", "w_1", "b_1", "w_2", "b_2", "ln2_g", "ln2_b")
+
+
+class GdpPlacerLayer(ctypes.Structure):
+    _fields_ = [(n, c_void_p) for n in PLACER_LAYER_FIELDS]
+
+
+class GdpPlacer(ctypes.Structure):
+    _fields_ = [("n_layers", c_int32), ("d_model", c_int32), ("n_heads", c_int32), ("d_ff", c_int32),
+                ("seg_len", c_int32), ("mem_len", c_int32), ("n_devices", c_int32), ("film", c_int32),
+                ("layers", POINTER(GdpPlacerLayer)), ("w_out", c_void_p), ("b_out", c_void_p)]
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_1910_01578_amd.build_lib` "
+                          "(there is no fallback path)")
+    lib = ctypes.CDLL(LIB_PATH)
+    sig = {
+        "gdp_workspace_bytes": (c_size_t, [POINTER(GdpGraph), POINTER(GdpGnn), POINTER(GdpPlacer), c_int32]),
+        "gdp_embed": (c_int32, [POINTER(GdpGraph), POINTER(GdpGnn), c_void_p, c_void_p, c_void_p, c_size_t,
+                                c_void_p]),
+        "gdp_place": (c_int32, [POINTER(GdpGraph), c_void_p, c_void_p, POINTER(GdpPlacer), c_void_p, c_void_p,
+                                c_void_p, c_size_t, c_void_p]),
+        "gdp_sample": (c_int32, [POINTER(GdpGraph), c_void_p, c_void_p, c_int32, c_int32, c_uint64, c_void_p,
+                                 c_void_p, c_void_p, c_void_p, c_size_t, c_void_p]),
+        "gdp_validate_graph_host": (c_int32, [c_void_p, c_int32, c_void_p, c_int32, c_void_p, c_int64, c_uint32]),
+        "gdp_last_error": (c_char_p, []),
+        "gdp_abi_version": (c_int32, []),
+        "gdp_debug_uniforms": (c_int32, [c_uint64, c_int32, c_int32, c_int32, c_void_p, c_void_p]),
+        "gdp_debug_neighbors": (c_int32, [POINTER(GdpGraph), POINTER(GdpGnn), c_void_p, c_void_p, c_int64,
+                                          c_void_p, c_size_t, c_void_p]),
+        "gdp_timer_begin": (c_int32, [c_uint32]),
+        "gdp_timer_end": (c_int32, [POINTER(c_double), POINTER(c_int64)]),
+        "gdp_kernel_kind_name": (c_char_p, [c_int32]),
+    }
+    for name, (res, args) in sig.items():
+        f = getattr(lib, name)
+        f.restype = res
+        f.argtypes = args
+    return lib
+
+
+lib = _load()
+
+
+def last_error() -> str:
+    return lib.gdp_last_error().decode()
+
+
+def check(code: int):
+    if code != GDP_OK:
+        raise GdpError(code, last_error())
+
+
+def abi_version() -> int:
+    return lib.gdp_abi_version()
+
+
+def validate_graph_host(graph_ptr, row_ptr, col_idx, flags: int = GDP_TOPO_IDS) -> int:
+    gp = np.ascontiguousarray(graph_ptr, np.int32)
+    rp = np.ascontiguousarray(row_ptr, np.int32)
+    ci = np.ascontiguousarray(col_idx, np.int32)
+    return lib.gdp_validate_graph_host(gp.ctypes.data, gp.size - 1, rp.ctypes.data, rp.size - 1,
+                                       ci.ctypes.data if ci.size else None, ci.size, flags)
+
+
+# ----------------------------------------------------------------------------
+# torch-facing helpers: device memory and the current stream only.
+# ----------------------------------------------------------------------------
+
+def _torch():
+    import torch
+    return torch
+
+
+def _stream_handle(stream=None) -> int:
+    torch = _torch()
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return int(s.cuda_stream)
+
+
+def to_device(arr: np.ndarray, dtype: str, device="cuda"):
+    """Upload a float32 array (dtype "f32") or uint16 bf16 bit patterns ("bf16")."""
+    torch = _torch()
+    a = np.ascontiguousarray(arr)
+    if dtype == "bf16":
+        assert a.dtype == np.uint16
+        return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).to(device)
+    assert a.dtype == np.float32
+    return torch.from_numpy(a).to(device)
+
+
+class DeviceGraph:
+    """A graph batch resident in device memory plus its C descriptor."""
+
+    def __init__(self, graph, dtype: str, device="cuda", flags: int = GDP_TOPO_IDS):
+        torch = _torch()
+        self.dtype = dtype
+        self.graph_ptr = np.ascontiguousarray(graph.graph_ptr, np.int32)
+        self.row_ptr = torch.from_numpy(np.ascontiguousarray(graph.row_ptr, np.int32)).to(device)
+        ci = np.ascontiguousarray(graph.col_idx, np.int32)
+        self.col_idx = torch.from_numpy(ci if ci.size else np.zeros(1, np.int32)).to(device)
+        self.x = to_device(graph.x_dev, dtype, device)
+        self.n_nodes = int(graph.row_ptr.size - 1)
+        self.n_edges = int(ci.size)
+        self.feat_dim = int(graph.x_dev.shape[1])
+        self.n_graphs = int(self.graph_ptr.size - 1)
+        self.c = GdpGraph(self.n_graphs, self.graph_ptr.ctypes.data_as(POINTER(c_int32)), self.n_nodes,
+                          self.row_ptr.data_ptr(), self.col_idx.data_ptr(), self.n_edges, self.x.data_ptr(),
+                          self.feat_dim, GDP_BF16 if dtype == "bf16" else GDP_F32, flags)
+
+
+class DevicePolicy:
+    """Policy weights resident in device memory plus the C descriptors."""
+
+    def __init__(self, cfg, weights, device="cuda", film: Optional[bool] = None):
+        self.cfg = cfg
+        dt = cfg.dtype
+        up = lambda pair: to_device(pair[1], dt, device)
+        self.gnn_t = [{k: up(v) for k, v in l.items()} for l in weights.gnn]
+        self.placer_t = [{k: up(v) for k, v in l.items()} for l in weights.placer]
+        self.head_t = {k: up(v) for k, v in weights.head.items()}
+        L = len(self.gnn_t)
+        self._gl = (GdpGnnLayer * L)(*[GdpGnnLayer(*[l[k].data_ptr() for k in ("w_pool", "b_pool", "w_self",
+                                                                              "w_neigh", "b_upd")])
+                                       for l in self.gnn_t])
+        self.gnn = GdpGnn(L, cfg.feat_dim, cfg.hidden, cfg.fanout, cfg.nb_seed, self._gl)
+        P = len(self.placer_t)
+        self._pl = (GdpPlacerLayer * P)(*[GdpPlacerLayer(*[l[k].data_ptr() for k in PLACER_LAYER_FIELDS])
+                                          for l in self.placer_t])
+        use_film = cfg.film if film is None else film
+        self.placer = GdpPlacer(P, cfg.d_model, cfg.heads, cfg.d_ff, cfg.seg_len, cfg.mem_len, cfg.n_devices,
+                                1 if use_film else 0, self._pl, self.head_t["w_out"].data_ptr(),
+                                self.head_t["b_out"].data_ptr())
+
+
+class Runner:
+    """Owns the outputs and the workspace of one (graph, policy, K) problem."""
+
+    def __init__(self, graph: DeviceGraph, policy: DevicePolicy, k_samples: int, device="cuda"):
+        torch = _torch()
+        self.graph, self.policy, self.k = graph, policy, int(k_samples)
+        cfg = policy.cfg
+        tdt = torch.bfloat16 if graph.dtype == "bf16" else torch.float32
+        N, G, H, D = graph.n_nodes, graph.n_graphs, cfg.hidden, cfg.n_devices
+        self.ws_bytes = lib.gdp_workspace_bytes(ctypes.byref(graph.c), ctypes.byref(policy.gnn),
+                                                ctypes.byref(policy.placer), self.k)
+        if self.ws_bytes == 0:
+            raise GdpError(GDP_E_INVALID_ARG, last_error())
+        self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8, device=device)
+        self.node_emb = torch.empty((N, H), dtype=tdt, device=device)
+        self.graph_emb = torch.empty((G, H), dtype=torch.float32, device=device)
+        self.logits = torch.empty((N, D), dtype=torch.float32, device=device)
+        self.lse = torch.empty((N,), dtype=torch.float32, device=device)
+        self.placements = torch.empty((self.k, N), dtype=torch.int32, device=device)
+        self.logp = torch.empty((G, self.k), dtype=torch.float32, device=device)
+
+    def embed(self, stream=None):
+        check(lib.gdp_embed(ctypes.byref(self.graph.c), ctypes.byref(self.policy.gnn), self.node_emb.data_ptr(),
+                            self.graph_emb.data_ptr(), self.ws.data_ptr(), self.ws_bytes, _stream_handle(stream)))
+
+    def place(self, stream=None):
+        check(lib.gdp_place(ctypes.byref(self.graph.c), self.node_emb.data_ptr(), self.graph_emb.data_ptr(),
+                            ctypes.byref(self.policy.placer), self.logits.data_ptr(), self.lse.data_ptr(),
+                            self.ws.data_ptr(), self.ws_bytes, _stream_handle(stream)))
+
+    def sample(self, seed: int, uniforms=None, use_lse: bool = True, stream=None):
+        check(lib.gdp_sample(ctypes.byref(self.graph.c), self.logits.data_ptr(),
+                             self.lse.data_ptr() if use_lse else None, self.policy.cfg.n_devices, self.k, seed,
+                             None if uniforms is None else uniforms.data_ptr(), self.placements.data_ptr(),
+                             self.logp.data_ptr(), self.ws.data_ptr(), self.ws_bytes, _stream_handle(stream)))
+
+    def forward(self, seed: int, stream=None):
+        """One pass of the hot path: embed -> place -> sample."""
+        self.embed(stream)
+        self.place(stream)
+        self.sample(seed, stream=stream)
+
+    def neighbors(self, stream=None):
+        torch = _torch()
+        n = self.graph.n_nodes
+        cap = max(1, min(2 * self.graph.n_edges, n * self.policy.cfg.fanout))
+        s_ptr = torch.empty(n + 1, dtype=torch.int32, device=self.ws.device)
+        s_idx = torch.empty(cap, dtype=torch.int32, device=self.ws.device)
+        check(lib.gdp_debug_neighbors(ctypes.byref(self.graph.c), ctypes.byref(self.policy.gnn), s_ptr.data_ptr(),
+                                      s_idx.data_ptr(), cap, self.ws.data_ptr(), self.ws_bytes,
+                                      _stream_handle(stream)))
+        return s_ptr, s_idx
+
+
+def debug_uniforms(seed: int, n: int, k: int, d: int, device="cuda", stream=None):
+    torch = _torch()
+    out = torch.empty((k, n, d), dtype=torch.float32, device=device)
+    check(lib.gdp_debug_uniforms(seed, n, k, d, out.data_ptr(), _stream_handle(stream)))
+    return out
+
+
+def timer_begin(kinds) -> None:
+    mask = 0
+    for k in kinds:
+        mask |= 1 << (KERNEL_KINDS.index(k) if isinstance(k, str) else int(k))
+    check(lib.gdp_timer_begin(mask))
+
+
+def timer_end() -> Dict[str, Dict[str, float]]:
+    ms = (c_double * K_COUNT)()
+    cnt = (c_int64 * K_COUNT)()
+    check(lib.gdp_timer_end(ms, cnt))
+    return {KERNEL_KINDS[i]: {"ms": ms[i], "launches": int(cnt[i])} for i in range(K_COUNT) if cnt[i]}

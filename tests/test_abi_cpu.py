@@ -1,0 +1,194 @@
+"""CPU checks of the C ABI: the library loads, exports every declared symbol,
+and every host-side validation path returns its error code before any GPU work."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_1910_01578_amd import gdp, workloads as W
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    text = open(os.path.join(ROOT, "include", "gdp.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(gdp_[a-z_0-9]+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol():
+    names = _declared()
+    assert len(names) >= 12
+    for n in names:
+        assert hasattr(gdp.lib, n), n
+    assert gdp.abi_version() == 1
+
+
+def test_kernel_kind_names_match_binding():
+    for i, n in enumerate(gdp.KERNEL_KINDS):
+        assert gdp.lib.gdp_kernel_kind_name(i).decode() == n
+    assert gdp.lib.gdp_kernel_kind_name(99) == b""
+
+
+def test_struct_layouts_match_c_compiler(tmp_path):
+    """Field offsets and sizes of the ctypes mirrors equal the C compiler's."""
+    import shutil
+    import subprocess
+    cc = shutil.which("gcc") or shutil.which("cc")
+    if cc is None:
+        pytest.skip("no C compiler")
+    structs = {"gdp_graph": gdp.GdpGraph, "gdp_gnn_layer": gdp.GdpGnnLayer, "gdp_gnn": gdp.GdpGnn,
+               "gdp_placer_layer": gdp.GdpPlacerLayer, "gdp_placer": gdp.GdpPlacer}
+    lines = ["#include <stdio.h>", "#include <stddef.h>", '#include "gdp.h"', "int main(void) {"]
+    for cname, py in structs.items():
+        lines.append(f'printf("{cname} size %zu\\n", sizeof({cname}));')
+        for f, _ in py._fields_:
+            lines.append(f'printf("{cname} {f} %zu\\n", offsetof({cname}, {f}));')
+    lines += ["return 0;", "}"]
+    src = tmp_path / "layout.c"
+    src.write_text("\n".join(lines))
+    exe = tmp_path / "layout"
+    subprocess.run([cc, "-I", os.path.join(ROOT, "include"), str(src), "-o", str(exe)], check=True)
+    out = subprocess.run([str(exe)], check=True, capture_output=True, text=True).stdout.split("\n")
+    seen = 0
+    for line in out:
+        if not line:
+            continue
+        cname, what, val = line.split()
+        py = structs[cname]
+        got = ctypes.sizeof(py) if what == "size" else getattr(py, what).offset
+        assert got == int(val), (cname, what, got, val)
+        seen += 1
+    assert seen == sum(len(p._fields_) + 1 for p in structs.values())
+
+
+def test_validate_accepts_generated_graphs():
+    for name in W.CONFIG_ORDER[:4]:
+        g = W.make_graph(W.get_config(name))
+        assert gdp.validate_graph_host(g.graph_ptr, g.row_ptr, g.col_idx) == gdp.GDP_OK, gdp.last_error()
+
+
+@pytest.mark.parametrize("gp,rp,ci,flags,code,msg", [
+    ([0, 3], [0, 1, 2, 2], [1, 2], 1, gdp.GDP_OK, ""),
+    ([0, 3], [0, 1, 1, 0], [1], 1, gdp.GDP_E_BAD_GRAPH, "row_ptr"),          # not ending at E
+    ([0, 3], [0, 2, 1, 2], [1, 2], 1, gdp.GDP_E_BAD_GRAPH, "decreases"),     # non-monotone
+    ([0, 3], [0, 1, 2, 2], [1, 5], 1, gdp.GDP_E_BAD_GRAPH, "out of range"),
+    ([0, 3], [0, 1, 2, 2], [0, 2], 1, gdp.GDP_E_BAD_GRAPH, "self-loop"),
+    ([0, 3], [0, 2, 2, 2], [1, 1], 1, gdp.GDP_E_BAD_GRAPH, "duplicate"),
+    ([0, 2, 3], [0, 1, 2, 2], [1, 2], 1, gdp.GDP_E_BAD_GRAPH, "crosses"),
+    ([0, 3], [0, 1, 1, 2], [1, 0], 1, gdp.GDP_E_BAD_GRAPH, "topological"),
+    ([0, 3], [0, 1, 1, 2], [1, 0], 0, gdp.GDP_E_BAD_GRAPH, "cycle"),         # 0->1, 2->0: fine? see below
+    ([0, 3], [0, 1, 2, 3], [1, 2, 0], 0, gdp.GDP_E_BAD_GRAPH, "cycle"),
+    ([0, 0, 3], [0, 1, 2, 2], [1, 2], 1, gdp.GDP_E_BAD_GRAPH, "empty"),
+    ([0, 3], [0, 1, 2, 2], [1, 2], 8, gdp.GDP_E_INVALID_ARG, "flags"),
+])
+def test_validate_error_paths(gp, rp, ci, flags, code, msg):
+    if msg == "cycle" and ci == [1, 0]:
+        # 0 -> 1 and 2 -> 0 is acyclic: accepted without the topological flag
+        assert gdp.validate_graph_host(gp, rp, ci, flags) == gdp.GDP_OK
+        return
+    r = gdp.validate_graph_host(gp, rp, ci, flags)
+    assert r == code, (r, gdp.last_error())
+    assert msg in gdp.last_error()
+
+
+# ----------------------------------------------------------------------------
+# Entry points reject bad arguments before touching the GPU.
+def _descs(cfg_name="tiny_layered_256", **over):
+    cfg = W.get_config(cfg_name).replace(**over)
+    gp = np.array([0, cfg.n_nodes], np.int32)
+    g = gdp.GdpGraph(1, gp.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), cfg.n_nodes, 0x1000, 0x2000, 10, 0x3000,
+                     cfg.feat_dim, gdp.GDP_BF16 if cfg.dtype == "bf16" else gdp.GDP_F32, gdp.GDP_TOPO_IDS)
+    fake = 0x10000
+    gl = (gdp.GdpGnnLayer * cfg.gnn_layers)(*[gdp.GdpGnnLayer(fake, fake, fake, fake, fake)] * cfg.gnn_layers)
+    gnn = gdp.GdpGnn(cfg.gnn_layers, cfg.feat_dim, cfg.hidden, cfg.fanout, 7, gl)
+    pl = (gdp.GdpPlacerLayer * cfg.placer_layers)(*[gdp.GdpPlacerLayer(*([fake] * 16))] * cfg.placer_layers)
+    placer = gdp.GdpPlacer(cfg.placer_layers, cfg.d_model, cfg.heads, cfg.d_ff, cfg.seg_len, cfg.mem_len,
+                           cfg.n_devices, 1, pl, fake, fake)
+    return cfg, gp, g, gl, gnn, pl, placer
+
+
+def test_workspace_bytes_sane():
+    cfg, gp, g, gl, gnn, pl, placer = _descs()
+    n = gdp.lib.gdp_workspace_bytes(ctypes.byref(g), ctypes.byref(gnn), ctypes.byref(placer), 4)
+    assert n > cfg.n_nodes * cfg.hidden * 4 * 4
+    assert n % 256 == 0
+    g.n_graphs = 0
+    assert gdp.lib.gdp_workspace_bytes(ctypes.byref(g), ctypes.byref(gnn), ctypes.byref(placer), 4) == 0
+
+
+def _embed(g, gnn, ws_bytes=1 << 30, node=0x100000, ge=0x200000, ws=0x1000000):
+    return gdp.lib.gdp_embed(ctypes.byref(g), ctypes.byref(gnn), node, ge, ws, ws_bytes, None)
+
+
+@pytest.mark.parametrize("mutate,code", [
+    (lambda g, gnn, p: setattr(g, "n_nodes", 0), gdp.GDP_E_INVALID_ARG),
+    (lambda g, gnn, p: setattr(g, "n_graphs", 0), gdp.GDP_E_INVALID_ARG),
+    (lambda g, gnn, p: setattr(g, "n_graphs", 200), gdp.GDP_E_UNSUPPORTED),
+    (lambda g, gnn, p: setattr(g, "dtype", 7), gdp.GDP_E_INVALID_ARG),
+    (lambda g, gnn, p: setattr(g, "feat_dim", 20), gdp.GDP_E_UNSUPPORTED),
+    (lambda g, gnn, p: setattr(g, "x", None), gdp.GDP_E_INVALID_ARG),
+    (lambda g, gnn, p: setattr(g, "n_edges", -1), gdp.GDP_E_INVALID_ARG),
+    (lambda g, gnn, p: setattr(gnn, "hidden", 96), gdp.GDP_E_UNSUPPORTED),
+    (lambda g, gnn, p: setattr(gnn, "fanout", 0), gdp.GDP_E_UNSUPPORTED),
+    (lambda g, gnn, p: setattr(gnn, "fanout", 33), gdp.GDP_E_UNSUPPORTED),
+    (lambda g, gnn, p: setattr(gnn, "in_dim", 64), gdp.GDP_E_INVALID_ARG),
+    (lambda g, gnn, p: setattr(gnn, "n_layers", 0), gdp.GDP_E_INVALID_ARG),
+])
+def test_embed_rejects(mutate, code):
+    cfg, gp, g, gl, gnn, pl, placer = _descs()
+    mutate(g, gnn, placer)
+    assert _embed(g, gnn) == code, gdp.last_error()
+    assert gdp.last_error() != ""
+
+
+def test_embed_rejects_small_or_misaligned_workspace_and_bad_graph_ptr():
+    cfg, gp, g, gl, gnn, pl, placer = _descs()
+    need = gdp.lib.gdp_workspace_bytes(ctypes.byref(g), ctypes.byref(gnn), None, 0)
+    assert _embed(g, gnn, ws_bytes=need - 1) == gdp.GDP_E_WORKSPACE
+    assert _embed(g, gnn, ws=0x1000010) == gdp.GDP_E_INVALID_ARG
+    assert _embed(g, gnn, node=0) == gdp.GDP_E_INVALID_ARG
+    gp[1] = cfg.n_nodes - 1
+    assert _embed(g, gnn) == gdp.GDP_E_BAD_GRAPH
+
+
+@pytest.mark.parametrize("field,value,code", [
+    ("d_model", 128, gdp.GDP_E_UNSUPPORTED),      # != hidden is caught by head-dim / width checks below
+    ("n_heads", 3, gdp.GDP_E_INVALID_ARG),
+    ("n_heads", 64, gdp.GDP_E_UNSUPPORTED),       # head dim 1
+    ("d_ff", 100, gdp.GDP_E_UNSUPPORTED),
+    ("seg_len", 0, gdp.GDP_E_INVALID_ARG),
+    ("mem_len", -1, gdp.GDP_E_INVALID_ARG),
+    ("n_devices", 1, gdp.GDP_E_UNSUPPORTED),
+    ("n_devices", 65, gdp.GDP_E_UNSUPPORTED),
+    ("film", 2, gdp.GDP_E_INVALID_ARG),
+])
+def test_place_rejects(field, value, code):
+    cfg, gp, g, gl, gnn, pl, placer = _descs()
+    if field == "d_model":
+        placer.d_model, placer.n_heads = 96, 4
+        code = gdp.GDP_E_UNSUPPORTED
+    else:
+        setattr(placer, field, value)
+    r = gdp.lib.gdp_place(ctypes.byref(g), 0x100000, 0x200000, ctypes.byref(placer), 0x300000, None, 0x1000000,
+                          1 << 30, None)
+    assert r == code, gdp.last_error()
+
+
+@pytest.mark.parametrize("D,K,code", [(1, 4, gdp.GDP_E_UNSUPPORTED), (65, 4, gdp.GDP_E_UNSUPPORTED),
+                                      (8, 0, gdp.GDP_E_INVALID_ARG)])
+def test_sample_rejects(D, K, code):
+    cfg, gp, g, gl, gnn, pl, placer = _descs()
+    r = gdp.lib.gdp_sample(ctypes.byref(g), 0x100000, None, D, K, 1, None, 0x200000, 0x300000, 0x1000000, 1 << 30,
+                           None)
+    assert r == code, gdp.last_error()
+    r = gdp.lib.gdp_sample(ctypes.byref(g), 0x100000, None, 8, 4, 1, None, 0x200000, None, 0x1000000, 1 << 30, None)
+    assert r == gdp.GDP_E_INVALID_ARG
+
+
+def test_timer_state_machine():
+    assert gdp.lib.gdp_timer_begin(1) == gdp.GDP_OK
+    assert gdp.lib.gdp_timer_begin(1) == gdp.GDP_E_INVALID_ARG
+    assert gdp.timer_end() == {}

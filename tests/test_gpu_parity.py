@@ -1,0 +1,314 @@
+"""GPU parity of the HIP path (through the C ABI) against the fp64 oracle.
+
+Every comparison runs on the same seeded inputs.  Integer results (sampled
+neighbourhoods, uniforms' bits, placements outside the margin band) must be
+bit-exact; floating-point results must stay within 1e-4 (fp32 configuration)
+or 2e-2 (bf16) row-normwise relative error.
+"""
+import os
+import sys
+
+import numpy as np
+import pytest
+
+from oracle import gdp_oracle as O
+from paper_1910_01578_amd import workloads as W
+from tests.parity import (TOL, check_placements, oracle_embed, oracle_full, oracle_place, rel_err_rows, to_np,
+                          workload)
+
+pytestmark = pytest.mark.gpu
+
+ALL = W.CONFIG_ORDER
+SMALL = ALL[:4]
+
+
+def _log(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+    path = os.environ.get("GDP_PARITY_LOG")
+    if path:
+        with open(path, "a") as f:
+            print(*a, file=f)
+
+
+def _bits(t):
+    """Raw bytes of a tensor (bf16 included)."""
+    import torch
+    t = t.detach().contiguous().cpu()
+    if t.dtype == torch.bfloat16:
+        t = t.view(torch.int16)
+    return t.numpy().tobytes()
+
+
+def _runner(cfg, g, w, film=None):
+    from paper_1910_01578_amd import gdp
+    dg = gdp.DeviceGraph(g, cfg.dtype)
+    pol = gdp.DevicePolicy(cfg, w, film=film)
+    return gdp.Runner(dg, pol, cfg.k_samples)
+
+
+def _sync():
+    import torch
+    torch.cuda.synchronize()
+
+
+# ----------------------------------------------------------------------------
+def test_uniforms_bit_exact():
+    from paper_1910_01578_amd import gdp
+    _log("uniforms N=1000 K=3 D=12")
+    u = gdp.debug_uniforms(seed=2004, n=1000, k=3, d=12)
+    _sync()
+    ref = O.gumbel_uniforms(2004, 1000, 3, 12)
+    assert np.array_equal(u.cpu().numpy().astype(np.float64), ref)
+
+
+@pytest.mark.parametrize("name", ALL)
+def test_neighbors_bit_exact(name):
+    cfg, g, w = workload(name)
+    _log("neighbors", name)
+    r = _runner(cfg, g, w)
+    s_ptr, s_idx = r.neighbors()
+    _sync()
+    s_ptr, s_idx = s_ptr.cpu().numpy(), s_idx.cpu().numpy()
+    nb = O.neighbour_lists(g.row_ptr, g.col_idx)
+    S = O.sample_neighbours(nb, g.graph_ptr, cfg.fanout, cfg.nb_seed)
+    assert s_ptr[0] == 0 and s_ptr[-1] == sum(len(s) for s in S)
+    for v in range(g.n_nodes):
+        got = np.sort(s_idx[s_ptr[v]:s_ptr[v + 1]])
+        assert np.array_equal(got, S[v]), v
+
+
+def test_neighbors_heavy_sampling_and_order_invariance():
+    cfg, g, w = workload("recurrent_12000")
+    cfg = cfg.replace(fanout=2)
+    rng = np.random.default_rng(5)
+    col2 = g.col_idx.copy()
+    for v in range(g.n_nodes):
+        a, b = g.row_ptr[v], g.row_ptr[v + 1]
+        col2[a:b] = rng.permutation(col2[a:b])
+    g2 = W.Graph(g.graph_ptr, g.row_ptr, col2, g.x, g.x_dev)
+    nb = O.neighbour_lists(g.row_ptr, g.col_idx)
+    S = O.sample_neighbours(nb, g.graph_ptr, 2, cfg.nb_seed)
+    for gg in (g, g2):
+        r = _runner(cfg, gg, w)
+        s_ptr, s_idx = r.neighbors()
+        _sync()
+        s_ptr, s_idx = s_ptr.cpu().numpy(), s_idx.cpu().numpy()
+        for v in range(g.n_nodes):
+            assert np.array_equal(np.sort(s_idx[s_ptr[v]:s_ptr[v + 1]]), S[v]), v
+
+
+# ----------------------------------------------------------------------------
+@pytest.mark.parametrize("name", ALL)
+def test_embed_parity(name):
+    cfg, g, w = workload(name)
+    _log("embed", name)
+    r = _runner(cfg, g, w)
+    r.embed()
+    _sync()
+    e, _ = oracle_full(name)
+    tol = TOL[cfg.dtype]
+    err_h = rel_err_rows(to_np(r.node_emb), e["node_emb"])
+    err_x0 = rel_err_rows(to_np(r.graph_emb), e["graph_emb"])
+    _log(f"  node_emb err {err_h:.3e}  graph_emb err {err_x0:.3e}")
+    assert err_h <= tol and err_x0 <= tol
+
+
+@pytest.mark.parametrize("name", ALL)
+def test_place_parity_given_embeddings(name):
+    """The placer alone: the oracle runs on the GPU's own embeddings."""
+    cfg, g, w = workload(name)
+    _log("place", name)
+    r = _runner(cfg, g, w)
+    r.embed()
+    r.place()
+    _sync()
+    p = oracle_place(cfg, w, to_np(r.node_emb), to_np(r.graph_emb), g.graph_ptr)
+    tol = TOL[cfg.dtype]
+    err_l = rel_err_rows(to_np(r.logits), p["logits"])
+    err_s = rel_err_rows(to_np(r.lse), p["lse"])
+    _log(f"  logits err {err_l:.3e}  lse err {err_s:.3e}")
+    assert err_l <= tol and err_s <= tol
+
+
+@pytest.mark.parametrize("name", ALL)
+def test_pipeline_parity(name):
+    """embed -> place -> sample against the oracle end to end."""
+    cfg, g, w = workload(name)
+    _log("pipeline", name)
+    r = _runner(cfg, g, w)
+    r.forward(cfg.sample_seed)
+    _sync()
+    e, p = oracle_full(name)
+    tol = TOL[cfg.dtype]
+    logits = to_np(r.logits)
+    err = rel_err_rows(logits, p["logits"])
+    placements = r.placements.cpu().numpy()
+    exempt = check_placements(logits, p["logits"], placements, cfg.sample_seed, g.graph_ptr)
+    # log-probs: the reduction against fp64 sums of the GPU's own terms, and the
+    # value against the oracle's log-prob of the same placements
+    lse = to_np(r.lse)
+    own = O.log_prob_of(logits.astype(np.float64), lse.astype(np.float64), g.graph_ptr, placements)
+    ref = O.log_prob_of(p["logits"], p["lse"], g.graph_ptr, placements)
+    logp = to_np(r.logp)
+    e_own = float(np.abs(logp - own).max() / np.abs(own).max())
+    e_ref = float(np.abs(logp - ref).max() / np.abs(ref).max())
+    _log(f"  logits err {err:.3e}  exempt {exempt:.4f}  logp(own) {e_own:.2e}  logp(ref) {e_ref:.2e}")
+    assert err <= tol
+    assert e_own <= 1e-5
+    assert e_ref <= tol
+
+
+# ----------------------------------------------------------------------------
+def test_sample_fixed_uniforms_and_zero_noise():
+    import torch
+    cfg, g, w = workload("inception_2500")
+    r = _runner(cfg, g, w)
+    rng = np.random.default_rng(0)
+    N, D, K = g.n_nodes, cfg.n_devices, cfg.k_samples
+    logits = rng.normal(size=(N, D)).astype(np.float32) * 2
+    logits[7] = 0.5                                   # a tie row
+    r.logits.copy_(torch.from_numpy(logits))
+    u = rng.uniform(1e-4, 1 - 1e-4, size=(K, N, D)).astype(np.float32)
+    u[:, 7, :] = np.float32(np.exp(-1.0))
+    ut = torch.from_numpy(u).cuda()
+    r.sample(seed=1, uniforms=ut, use_lse=False)
+    _sync()
+    ref = O.sample(logits.astype(np.float64), O.logsumexp_rows(logits.astype(np.float64)), g.graph_ptr, K, 1,
+                   uniforms=u.astype(np.float64))
+    got = r.placements.cpu().numpy()
+    sc = ref["scores"]
+    srt = np.sort(sc, axis=2)
+    clear = (srt[:, :, -1] - srt[:, :, -2]) > 1e-5
+    assert np.array_equal(got[clear], ref["placements"][clear])
+    assert np.all(got[:, 7] == 0)
+    lp = to_np(r.logp)
+    own = O.log_prob_of(logits.astype(np.float64), O.logsumexp_rows(logits.astype(np.float64)), g.graph_ptr, got)
+    assert np.abs(lp - own).max() / np.abs(own).max() < 1e-5
+
+
+def test_determinism_bitwise():
+    cfg, g, w = workload("superposition_4x")
+    r = _runner(cfg, g, w)
+    outs = []
+    for _ in range(2):
+        r.forward(cfg.sample_seed)
+        _sync()
+        outs.append([t.clone().cpu() for t in (r.node_emb, r.graph_emb, r.logits, r.lse, r.placements, r.logp)])
+    for a, b in zip(*outs):
+        assert _bits(a) == _bits(b)
+
+
+def test_ragged_batch_equals_separate_graphs_bitwise():
+    """I7 on the GPU: each graph of the superposition batch alone gives the
+    same embeddings and logits bit for bit."""
+    cfg, g, w = workload("superposition_4x")
+    r = _runner(cfg, g, w)
+    r.embed()
+    r.place()
+    _sync()
+    full_h, full_l = r.node_emb.cpu(), r.logits.cpu()
+    for gi in range(g.n_graphs):
+        a, b = int(g.graph_ptr[gi]), int(g.graph_ptr[gi + 1])
+        rows = g.row_ptr[a:b + 1] - g.row_ptr[a]
+        cols = g.col_idx[g.row_ptr[a]:g.row_ptr[b]] - a
+        gs = W.Graph(np.array([0, b - a], np.int32), rows.astype(np.int32), cols.astype(np.int32),
+                     g.x[a:b], g.x_dev[a:b])
+        rs = _runner(cfg, gs, w)
+        rs.embed()
+        rs.place()
+        _sync()
+        assert _bits(rs.node_emb) == _bits(full_h[a:b])
+        assert _bits(rs.logits) == _bits(full_l[a:b])
+
+
+@pytest.mark.parametrize("film", [True, False])
+def test_film_identity_equals_off(film):
+    """I8 on the GPU: zero FiLM weights and biases reproduce film = 0 exactly."""
+    cfg, g, w = workload("superposition_4x")
+    w0 = W.make_weights(cfg)
+    for l in w0.placer:
+        for k in ("film_wg", "film_bg", "film_wb", "film_bb"):
+            f64, dev = l[k]
+            l[k] = (np.zeros_like(f64), np.zeros_like(dev))
+    r_on = _runner(cfg, g, w0, film=True)
+    r_off = _runner(cfg, g, w, film=False)
+    for r in (r_on, r_off):
+        r.embed()
+        r.place()
+    _sync()
+    assert _bits(r_on.logits) == _bits(r_off.logits)
+
+
+# ----------------------------------------------------------------------------
+# Edge cases through the whole path.
+EDGE = [
+    # (label, cfg overrides, graph builder)
+    ("single_node", dict(graph_sizes=(1,)), "single"),
+    ("no_edges", dict(graph_sizes=(300,)), "empty"),
+    ("ragged_tail_m0", dict(seg_len=48, mem_len=0), None),
+    ("mem_gt_seg", dict(seg_len=32, mem_len=80), None),
+    ("dh64_d2", dict(heads=1, n_devices=2, k_samples=1), None),
+    ("many_devices", dict(n_devices=64, k_samples=3), None),
+    ("fanout1", dict(fanout=1), None),
+    ("film_off", dict(film=False), None),
+]
+
+
+def _edge_graph(cfg, kind):
+    rng = np.random.default_rng(1)
+    n = cfg.graph_sizes[0]
+    if kind == "single":
+        gp, rp, ci = [0, 1], [0, 0], []
+    else:
+        gp, rp, ci = [0, n], [0] * (n + 1), []
+    x = W.make_features(cfg, n, rng)
+    return W.graph_from_arrays(cfg, gp, rp, np.array(ci, np.int32), x)
+
+
+# bf16 variants use d = 128 (the width of the 2,500-29,000-node configurations):
+# with bf16 activations a d = 64 model sits at the edge of the 2e-2 bar already
+# in an exact bf16-storage emulation, so it is checked in fp32 only.
+BF16_WIDTH = dict(hidden=128, heads=8, d_ff=512)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("label,over,kind", EDGE, ids=[e[0] for e in EDGE])
+def test_edge_cases(label, over, kind, dtype):
+    over = dict(over)
+    if dtype == "bf16":
+        width = dict(BF16_WIDTH)
+        if "heads" in over:
+            width["heads"] = 2          # head dim 64 at d = 128
+            over.pop("heads")
+        over = {**width, **over}
+    base = W.get_config("tiny_layered_256").replace(dtype=dtype, **over)
+    _log("edge", label, dtype)
+    g = W.make_graph(base) if kind is None else _edge_graph(base, kind)
+    w = W.make_weights(base)
+    r = _runner(base, g, w)
+    r.forward(base.sample_seed)
+    _sync()
+    gnn, pl, hd = w.f64()
+    e = O.embed(g.graph_ptr, g.row_ptr, g.col_idx, g.x, gnn, base.fanout, base.nb_seed)
+    p = O.place(e["node_emb"], e["graph_emb"], g.graph_ptr, pl, hd["w_out"], hd["b_out"], base.heads,
+                base.seg_len, base.mem_len, base.film)
+    tol = TOL[dtype]
+    err_h = rel_err_rows(to_np(r.node_emb), e["node_emb"])
+    logits = to_np(r.logits)
+    err_l = rel_err_rows(logits, p["logits"])
+    # the placer alone, on the GPU's own embeddings
+    pg = O.place(to_np(r.node_emb), to_np(r.graph_emb), g.graph_ptr, pl, hd["w_out"], hd["b_out"], base.heads,
+                 base.seg_len, base.mem_len, base.film)
+    err_p = rel_err_rows(logits, pg["logits"])
+    _log(f"  node_emb err {err_h:.3e}  placer err {err_p:.3e}  end-to-end logits err {err_l:.3e}")
+    assert err_h <= tol and err_p <= tol
+    if dtype == "f32":
+        # With bf16 matrix-core operands some of these small inputs are
+        # ill-conditioned end to end (an exact bf16-operand emulation of the
+        # edgeless graph already lands above 2e-2), so bf16 is held to the bar
+        # stage by stage and fp32 end to end.
+        assert err_l <= tol
+    ref = p if dtype == "f32" else pg
+    check_placements(logits, ref["logits"], r.placements.cpu().numpy(), base.sample_seed, g.graph_ptr,
+                     max_exempt=0.2)
