@@ -50,8 +50,7 @@ def flop_model(cfg, g, stats):
         "gemm_qkv": ("mfma", 2.0 * N * d * 3 * d),
         "seg_attention": ("mfma", 4.0 * d * keys),
         "gemm_out_ln": ("mfma", 2.0 * N * d * d),
-        "gemm_ffn1_relu": ("mfma", 2.0 * N * d * dff),
-        "gemm_ffn2_ln": ("mfma", 2.0 * N * dff * d),
+        "ffn_ln": ("mfma", 4.0 * N * d * dff),
     }, keys
 
 

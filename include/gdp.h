@@ -252,8 +252,8 @@ typedef enum gdp_kernel_kind {
   GDP_K_GEMM_QKV,        /* Y W_qkv^T + b                                    */
   GDP_K_ATTENTION,       /* segment attention                                */
   GDP_K_GEMM_OUT_LN,     /* LN1(Y + O W_o^T + b)                              */
-  GDP_K_GEMM_FFN1,       /* ReLU(Z W_1^T + b)                                 */
-  GDP_K_GEMM_FFN2_LN,    /* LN2(Z + H W_2^T + b) (+ next layer's FiLM)        */
+  GDP_K_FFN_LN,          /* LN2(Z + W_2 ReLU(W_1 Z + b_1) + b_2), fused, with
+                            the next layer's FiLM                            */
   GDP_K_HEAD,            /* logits and lse                                   */
   GDP_K_SAMPLE,          /* Gumbel-max sampling                              */
   GDP_K_LOGP_REDUCE,     /* per-graph log-prob sums                          */

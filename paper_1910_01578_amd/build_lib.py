@@ -22,7 +22,7 @@ COMMON = ["-O3", "-std=c++17", "-fPIC", f"-I{INCLUDE}", f"-I{CSRC}", "-Wall", "-
 # Packed FP32 instructions stay disabled for all device code.
 DEVICE = [f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 
-SOURCES = ["graph_kernels.hip", "gemm.hip", "attention.hip", "placer_kernels.hip", "sample.hip",
+SOURCES = ["graph_kernels.hip", "gemm.hip", "ffn.hip", "attention.hip", "placer_kernels.hip", "sample.hip",
            "gdp_api.hip", "host_plan.cpp"]
 
 

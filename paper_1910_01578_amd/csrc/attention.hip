@@ -57,13 +57,41 @@ template <int DH> struct QkFrag<float, DH> {
   }
 };
 
+// Four consecutive elements held as one raw vector (8 bytes of bf16, 16 of fp32),
+// and the 4 x 4 transpose used to stage V^T: column(rows, e) gathers element e
+// of four row blocks.
+template <typename T> struct VBlock;
+template <> struct VBlock<bf16> {
+  typedef uint2 raw;
+  static __device__ __forceinline__ raw zero() { return make_uint2(0u, 0u); }
+  static __device__ __forceinline__ uint32_t half(const raw& r, int e) {
+    const uint32_t w = (e < 2) ? r.x : r.y;
+    return (e & 1) ? (w >> 16) : (w & 0xffffu);
+  }
+  static __device__ __forceinline__ raw column(const raw (&r)[4], int e) {
+    return make_uint2(half(r[0], e) | (half(r[1], e) << 16), half(r[2], e) | (half(r[3], e) << 16));
+  }
+};
+template <> struct VBlock<float> {
+  typedef uint4 raw;
+  static __device__ __forceinline__ raw zero() { return make_uint4(0u, 0u, 0u, 0u); }
+  static __device__ __forceinline__ uint32_t word(const raw& r, int e) {
+    return e == 0 ? r.x : e == 1 ? r.y : e == 2 ? r.z : r.w;
+  }
+  static __device__ __forceinline__ raw column(const raw (&r)[4], int e) {
+    return make_uint4(word(r[0], e), word(r[1], e), word(r[2], e), word(r[3], e));
+  }
+};
+
 }  // namespace
 
 template <typename T, int DH>
 __global__ __launch_bounds__(256) void k_seg_attention(AttnArgs<T> p, GraphTable gt, float scale_log2) {
   constexpr int EPV = 16 / sizeof(T);
   constexpr int KS = DH + EPV;          // sK row stride
-  constexpr int VS = BKV + EPV;         // sVt row stride
+  // sVt row stride: 68 elements puts the 16 rows of an 8-byte bf16 fragment
+  // read on distinct bank pairs (the row stride is an odd number of 8-byte words).
+  constexpr int VS = BKV + 4;
   constexpr int DB = DH / 16;           // 16-row blocks of the head dim
   using QS = QkShape<T, DH>;
   using QF = QkFrag<T, DH>;
@@ -72,8 +100,11 @@ __global__ __launch_bounds__(256) void k_seg_attention(AttnArgs<T> p, GraphTable
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int col = lane & 15, g4 = lane >> 4;
-  const int head = blockIdx.x % p.heads;
-  const int qblk = blockIdx.x / p.heads;
+  // heads fastest, remapped so that the heads of one query block (whose K/V
+  // slices share cache lines) run on one XCD
+  const int logical = xcd_remap(blockIdx.x, gridDim.x);
+  const int head = logical % p.heads;
+  const int qblk = logical / p.heads;
 
   // ---- which graph / segment / query block -----------------------------------
   const int g = graph_of_block(gt, qblk);
@@ -104,9 +135,18 @@ __global__ __launch_bounds__(256) void k_seg_attention(AttnArgs<T> p, GraphTable
   }
 
   // ---- K / V tile staging -------------------------------------------------------
+  // K: 16-byte chunks of key rows.  V is stored transposed; each thread moves
+  // a 4-key x 4-dim block (lanes consecutive along keys) so that every LDS
+  // store writes 4 consecutive keys of one dim and a quarter-wave covers one
+  // contiguous run of a V^T row.
   constexpr int CPR = DH / EPV;                 // 16-byte chunks per key row
   constexpr int CHUNKS = BKV * CPR;
-  uint4 rk[(CHUNKS + 255) / 256], rv[(CHUNKS + 255) / 256];
+  constexpr int VTHREADS = (BKV / 4) * (DH / 4);
+  static_assert(VTHREADS <= 256, "V block split");
+  using V4 = typename VBlock<T>::raw;           // 4 consecutive elements
+  uint4 rk[(CHUNKS + 255) / 256];
+  V4 rv[4];
+  const int vkg = threadIdx.x % (BKV / 4), vdg = threadIdx.x / (BKV / 4);
   auto load_tile = [&](int t) {
     const int kb = k0 + t * BKV;
 #pragma unroll
@@ -114,13 +154,17 @@ __global__ __launch_bounds__(256) void k_seg_attention(AttnArgs<T> p, GraphTable
       const int c = threadIdx.x + i * 256;
       const int row = c / CPR, cc = (c % CPR) * EPV;
       const int key = kb + row;
-      if (c < CHUNKS && key < k1) {
+      if (c < CHUNKS && key < k1)
         rk[i] = *reinterpret_cast<const uint4*>(Kp + (size_t)key * p.ldq + cc);
-        rv[i] = *reinterpret_cast<const uint4*>(Vp + (size_t)key * p.ldq + cc);
-      } else {
+      else
         rk[i] = make_uint4(0u, 0u, 0u, 0u);
-        rv[i] = make_uint4(0u, 0u, 0u, 0u);
-      }
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int key = kb + 4 * vkg + j;
+      rv[j] = (threadIdx.x < VTHREADS && key < k1)
+                  ? *reinterpret_cast<const V4*>(Vp + (size_t)key * p.ldq + 4 * vdg)
+                  : VBlock<T>::zero();
     }
   };
   auto store_tile = [&](int buf) {
@@ -130,10 +174,12 @@ __global__ __launch_bounds__(256) void k_seg_attention(AttnArgs<T> p, GraphTable
       if (c < CHUNKS) {
         const int row = c / CPR, cc = (c % CPR) * EPV;
         *reinterpret_cast<uint4*>(&sK[buf][row * KS + cc]) = rk[i];
-        const T* v = reinterpret_cast<const T*>(&rv[i]);
-#pragma unroll
-        for (int e = 0; e < EPV; ++e) sVt[buf][(cc + e) * VS + row] = v[e];
       }
+    }
+    if (threadIdx.x < VTHREADS) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        *reinterpret_cast<V4*>(&sVt[buf][(4 * vdg + e) * VS + 4 * vkg]) = VBlock<T>::column(rv, e);
     }
   };
 

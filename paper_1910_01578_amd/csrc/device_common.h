@@ -88,6 +88,20 @@ __device__ __forceinline__ float xor_shfl(float v, int mask) { return __shfl_xor
 __device__ __forceinline__ int xor_shfl(int v, int mask) { return __shfl_xor(v, mask, kWave); }
 
 // ---------------------------------------------------------------------------
+// Work-groups of a launch are dealt to the 8 XCDs of the chip round-robin by
+// id, and each XCD has its own L2.  This maps a work-group id to a logical
+// tile id such that every XCD receives a contiguous run of logical tiles, so
+// neighbouring tiles (which share operand rows) share an L2.  Bijective on
+// [0, total).
+// ---------------------------------------------------------------------------
+constexpr int kNumXcd = 8;
+__device__ __forceinline__ int xcd_remap(int p, int total) {
+  const int per = total / kNumXcd, rem = total % kNumXcd;
+  const int xcd = p % kNumXcd, idx = p / kNumXcd;
+  return xcd * per + (xcd < rem ? xcd : rem) + idx;
+}
+
+// ---------------------------------------------------------------------------
 // Graph table passed by value: node starts of every graph of the batch plus a
 // per-graph prefix of work blocks whose meaning depends on the kernel.
 // ---------------------------------------------------------------------------

@@ -183,7 +183,6 @@ static int place_impl(const gdp_graph* g, const T* node_emb, const float* graph_
   T* qkv = at<T>(ws, pl.qkv);
   T* o = at<T>(ws, pl.o);
   float* z = at<float>(ws, pl.z);
-  T* h1 = at<T>(ws, pl.h1);
 
   const float* y = ybuf[0];
   if (p->film) {
@@ -212,16 +211,14 @@ static int place_impl(const gdp_graph* g, const T* node_emb, const float* graph_
                                  static_cast<const T*>(Ly.ln1_g), static_cast<const T*>(Ly.ln1_b),
                                  nullptr, nullptr, 0, z, d, N, d};
     GDP_LAUNCH(GDP_K_GEMM_OUT_LN, launch_gemm_ln<T>(a_out, gt, st));
-    const GemmArgs<float, T, T> a_ff1 = {z, d, static_cast<const T*>(Ly.w_1), d, nullptr, 0, nullptr, 0,
-                               static_cast<const T*>(Ly.b_1), h1, p->d_ff, N, p->d_ff};
-    GDP_LAUNCH(GDP_K_GEMM_FFN1, (launch_gemm<float, T, T>(a_ff1, EPI_RELU, st)));
     const bool next_film = p->film && l + 1 < L;
     float* ynext = ybuf[cur ^ 1];
-    const GemmLnArgs<T> a_ff2 = {h1, p->d_ff, p->d_ff, static_cast<const T*>(Ly.w_2), static_cast<const T*>(Ly.b_2),
-                                 z, d, static_cast<const T*>(Ly.ln2_g), static_cast<const T*>(Ly.ln2_b),
-                                 next_film ? gamma_of(l + 1) : nullptr, next_film ? beta_of(l + 1) : nullptr, d,
-                                 ynext, d, N, d};
-    GDP_LAUNCH(GDP_K_GEMM_FFN2_LN, launch_gemm_ln<T>(a_ff2, gt, st));
+    const FfnArgs<T> a_ffn = {z, d, static_cast<const T*>(Ly.w_1), static_cast<const T*>(Ly.b_1),
+                              static_cast<const T*>(Ly.w_2), static_cast<const T*>(Ly.b_2),
+                              static_cast<const T*>(Ly.ln2_g), static_cast<const T*>(Ly.ln2_b),
+                              next_film ? gamma_of(l + 1) : nullptr, next_film ? beta_of(l + 1) : nullptr, d,
+                              ynext, d, N, d, p->d_ff};
+    GDP_LAUNCH(GDP_K_FFN_LN, launch_ffn_fused<T>(a_ffn, gt, st));
     cur ^= 1;
     y = ynext;
   }
@@ -373,9 +370,9 @@ extern "C" int gdp_timer_end(double* total_ms, int64_t* launches) {
 
 extern "C" const char* gdp_kernel_kind_name(int32_t kind) {
   static const char* names[GDP_K_COUNT] = {
-      "graph_prep", "nbr_sample", "gemm_pool_sigmoid", "gather_max", "gemm_update_relu", "meanpool",
-      "film",       "gemm_qkv",   "seg_attention",     "gemm_out_ln", "gemm_ffn1_relu",  "gemm_ffn2_ln",
-      "head_lse",   "gumbel_sample", "logp_reduce"};
+      "graph_prep", "nbr_sample",    "gemm_pool_sigmoid", "gather_max", "gemm_update_relu",
+      "meanpool",   "film",          "gemm_qkv",          "seg_attention", "gemm_out_ln",
+      "ffn_ln",     "head_lse",      "gumbel_sample",     "logp_reduce"};
   if (kind < 0 || kind >= GDP_K_COUNT) return "";
   return names[kind];
 }

@@ -9,8 +9,9 @@
 // owns a WM x WN sub-tile of 16 x 16 MFMA blocks.  K advances in BK steps
 // through double-buffered LDS tiles (global -> registers for step k+1 while
 // step k is multiplied).  A may be stored in fp32 (the residual stream) and is
-// rounded to the MFMA type on its way into LDS.  The epilogue stages the
-// finished tile in LDS so that every lane writes whole 16-byte chunks.
+// rounded to the MFMA type on its way into LDS.  The product is accumulated
+// transposed so that each lane ends with 4 consecutive outputs of one row,
+// which the epilogue writes as one vector store.
 #include "device_common.h"
 #include "kernels.h"
 
@@ -80,7 +81,10 @@ struct TileLoader {
   }
 };
 
-// One BK step of a wave's WM x WN sub-tile from LDS.
+// One BK step of a wave's WM x WN sub-tile from LDS.  The product is formed
+// transposed (W-block x A-block^T), so in acc[i][j] lane l holds output row
+// i * 16 + (l & 15) and the 4 consecutive output columns j * 16 + 4 * (l >> 4) + r:
+// every lane owns 4 contiguous elements of one output row.
 template <typename T, int WM, int WN>
 __device__ __forceinline__ void mma_tile(const T* sA, const T* sB, int lane, f32x4 (&acc)[WM / 16][WN / 16]) {
   using MF = Mfma<T>;
@@ -97,7 +101,7 @@ __device__ __forceinline__ void mma_tile(const T* sA, const T* sB, int lane, f32
 #pragma unroll
     for (int i = 0; i < WM / 16; ++i)
 #pragma unroll
-      for (int j = 0; j < WN / 16; ++j) acc[i][j] = MF::mma(a[i], b[j], acc[i][j]);
+      for (int j = 0; j < WN / 16; ++j) acc[i][j] = MF::mma(b[j], a[i], acc[i][j]);
   }
 }
 
@@ -163,57 +167,62 @@ __device__ __forceinline__ void gemm_mainloop(const TA* a1, int lda1, const T* w
 
 __device__ __forceinline__ float sigmoidf_(float z) { return 1.0f / (1.0f + __expf(-z)); }
 
+// 4 consecutive outputs as one 16-byte (fp32) or 8-byte (bf16) store.
+__device__ __forceinline__ void store4(float* p, const float (&v)[4]) {
+  *reinterpret_cast<float4*>(p) = make_float4(v[0], v[1], v[2], v[3]);
+}
+__device__ __forceinline__ void store4(bf16* p, const float (&v)[4]) {
+  typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
+  bf16x4_t o;
+  o[0] = (bf16)v[0]; o[1] = (bf16)v[1]; o[2] = (bf16)v[2]; o[3] = (bf16)v[3];
+  *reinterpret_cast<bf16x4_t*>(p) = o;
+}
+
 }  // namespace
 
 // ---------------------------------------------------------------------------
 template <typename TA, typename T, typename TO, int BM, int BN, int WM, int WN, int EPI>
 __global__ __launch_bounds__(256) void k_gemm(GemmArgs<TA, T, TO> p) {
   constexpr int S = TileCfg<T>::STRIDE;
-  constexpr int BYTES_AB = 2 * (BM + BN) * S * (int)sizeof(T);
-  constexpr int EPO = 16 / sizeof(TO);
-  constexpr int CS = BN + EPO;                              // padded C-tile row
-  constexpr int BYTES_C = BM * CS * (int)sizeof(TO);
-  __shared__ __attribute__((aligned(16))) char smem[BYTES_AB > BYTES_C ? BYTES_AB : BYTES_C];
-  T* sA = reinterpret_cast<T*>(smem);
-  T* sB = sA + 2 * BM * S;
-  const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
+  __shared__ __attribute__((aligned(16))) T smem[2 * (BM + BN) * S];
+  T* sA = smem;
+  T* sB = smem + 2 * BM * S;
+  // 1-D grid over (row tile, column tile), column tiles fastest, remapped so
+  // that the column tiles of one row tile (which share its A rows) share an XCD.
+  const int nt = p.N / BN;
+  const int tile = xcd_remap(blockIdx.x, gridDim.x);
+  const int m0 = (tile / nt) * BM, n0 = (tile % nt) * BN;
   f32x4 acc[WM / 16][WN / 16];
   gemm_mainloop<TA, T, BM, BN, WM, WN>(p.a1, p.lda1, p.w1, p.k1, p.a2, p.lda2, p.w2, p.k2, p.M, m0, n0, sA, sB, acc);
 
-  // bias + activation, rounded, into the LDS C tile (the main loop ended on a barrier)
+  // bias + activation; each lane stores 4 contiguous outputs of one row
   constexpr int WAVES_N = BN / WN;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave / WAVES_N, wn = wave % WAVES_N;
-  TO* sC = reinterpret_cast<TO*>(smem);
 #pragma unroll
   for (int j = 0; j < WN / 16; ++j) {
-    const int lc = wn * WN + j * 16 + (lane & 15);
-    const float b = to_f32(p.bias[n0 + lc]);
+    const int n = n0 + wn * WN + j * 16 + 4 * (lane >> 4);
+    float b[4];
 #pragma unroll
-    for (int i = 0; i < WM / 16; ++i)
+    for (int r = 0; r < 4; ++r) b[r] = to_f32(p.bias[n + r]);
+#pragma unroll
+    for (int i = 0; i < WM / 16; ++i) {
+      const int m = m0 + wm * WM + i * 16 + (lane & 15);
+      float v[4];
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int lr = wm * WM + i * 16 + 4 * (lane >> 4) + r;
-        float v = acc[i][j][r] + b;
-        if (EPI == EPI_RELU) v = fmaxf(v, 0.f);
-        if (EPI == EPI_SIGMOID) v = sigmoidf_(v);
-        sC[lr * CS + lc] = from_f32<TO>(v);
+        v[r] = acc[i][j][r] + b[r];
+        if (EPI == EPI_RELU) v[r] = fmaxf(v[r], 0.f);
+        if (EPI == EPI_SIGMOID) v[r] = sigmoidf_(v[r]);
       }
-  }
-  __syncthreads();
-  constexpr int CPR = BN / EPO;
-  for (int c = threadIdx.x; c < BM * CPR; c += 256) {
-    const int lr = c / CPR, lc = (c % CPR) * EPO;
-    const int row = m0 + lr;
-    if (row < p.M)
-      *reinterpret_cast<uint4*>(p.out + (size_t)row * p.ldo + n0 + lc) =
-          *reinterpret_cast<const uint4*>(sC + lr * CS + lc);
+      if (m < p.M) store4(p.out + (size_t)m * p.ldo + n, v);
+    }
   }
 }
 
 template <typename TA, typename T, typename TO, int BM, int BN, int WM, int WN>
 static hipError_t launch_gemm_cfg(const GemmArgs<TA, T, TO>& a, int epi, hipStream_t s) {
-  dim3 grid(a.N / BN, (a.M + BM - 1) / BM), block(256);
+  dim3 grid((a.N / BN) * ((a.M + BM - 1) / BM)), block(256);
   switch (epi) {
     case EPI_BIAS: hipLaunchKernelGGL((k_gemm<TA, T, TO, BM, BN, WM, WN, EPI_BIAS>), grid, block, 0, s, a); break;
     case EPI_RELU: hipLaunchKernelGGL((k_gemm<TA, T, TO, BM, BN, WM, WN, EPI_RELU>), grid, block, 0, s, a); break;
@@ -244,9 +253,7 @@ template hipError_t launch_gemm<float, bf16, float>(const GemmArgs<float, bf16, 
 // Residual + LayerNorm epilogue over full rows: BM = 64 rows x the whole
 // N = d output row per work-group, 2 x 2 waves (32 rows x N/2 columns each).
 // The residual input and the output are fp32 (the residual stream).  Row
-// statistics: in-lane sums over the wave's column blocks, a 16-lane
-// butterfly, then the two column-half partials through LDS; two passes (mean,
-// then centred second moment).
+// statistics are taken in two passes (mean, then centred second moment).
 template <typename T, int NOUT>
 __global__ __launch_bounds__(256) void k_gemm_ln(GemmLnArgs<T> p, GraphTable gt) {
   constexpr int BM = 64, WM = 32, WN = NOUT / 2;
@@ -261,92 +268,85 @@ __global__ __launch_bounds__(256) void k_gemm_ln(GemmLnArgs<T> p, GraphTable gt)
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave >> 1, wn = wave & 1;
-  const int g4 = lane >> 4;
+  const int c4 = 4 * (lane >> 4);
 
-  // v = acc + bias + residual
+  // v = acc + bias + residual; lane owns row lr(i) and columns col(j) + [0, 4)
 #pragma unroll
-  for (int j = 0; j < WN / 16; ++j) {
-    const int col = wn * WN + j * 16 + (lane & 15);
-    const float b = to_f32(p.bias[col]);
+  for (int i = 0; i < WM / 16; ++i) {
+    const int row = m0 + wm * WM + i * 16 + (lane & 15);
 #pragma unroll
-    for (int i = 0; i < WM / 16; ++i)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int row = m0 + wm * WM + i * 16 + 4 * g4 + r;
-        const float res = row < p.M ? p.res[(size_t)row * p.ldr + col] : 0.f;
-        acc[i][j][r] += b + res;
-      }
+    for (int j = 0; j < WN / 16; ++j) {
+      const int col = wn * WN + j * 16 + c4;
+      float4 res = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (row < p.M) res = *reinterpret_cast<const float4*>(p.res + (size_t)row * p.ldr + col);
+      acc[i][j][0] += to_f32(p.bias[col + 0]) + res.x;
+      acc[i][j][1] += to_f32(p.bias[col + 1]) + res.y;
+      acc[i][j][2] += to_f32(p.bias[col + 2]) + res.z;
+      acc[i][j][3] += to_f32(p.bias[col + 3]) + res.w;
+    }
   }
 
-  float mean[WM / 16][4], rstd[WM / 16][4];
+  // Row statistics: in-lane over the lane's columns, then across the 4 lane
+  // groups holding the same row (xor 16, 32), then the two column halves.
+  float mean[WM / 16], rstd[WM / 16];
 #pragma unroll
-  for (int i = 0; i < WM / 16; ++i)
+  for (int i = 0; i < WM / 16; ++i) {
+    float sum = 0.f;
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      float sum = 0.f;
-#pragma unroll
-      for (int j = 0; j < WN / 16; ++j) sum += acc[i][j][r];
-#pragma unroll
-      for (int off = 1; off < 16; off <<= 1) sum += xor_shfl(sum, off);
-      if ((lane & 15) == 0) red[wm * WM + i * 16 + 4 * g4 + r][wn] = sum;
-    }
+    for (int j = 0; j < WN / 16; ++j) sum += (acc[i][j][0] + acc[i][j][1]) + (acc[i][j][2] + acc[i][j][3]);
+    sum += xor_shfl(sum, 16);
+    sum += xor_shfl(sum, 32);
+    if (lane < 16) red[wm * WM + i * 16 + lane][wn] = sum;
+  }
   __syncthreads();
 #pragma unroll
-  for (int i = 0; i < WM / 16; ++i)
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int lr = wm * WM + i * 16 + 4 * g4 + r;
-      mean[i][r] = (red[lr][0] + red[lr][1]) * (1.0f / NOUT);
-    }
+  for (int i = 0; i < WM / 16; ++i) {
+    const int lr = wm * WM + i * 16 + (lane & 15);
+    mean[i] = (red[lr][0] + red[lr][1]) * (1.0f / NOUT);
+  }
   __syncthreads();
 #pragma unroll
-  for (int i = 0; i < WM / 16; ++i)
+  for (int i = 0; i < WM / 16; ++i) {
+    float sum = 0.f;
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      float sum = 0.f;
-#pragma unroll
-      for (int j = 0; j < WN / 16; ++j) {
-        const float dlt = acc[i][j][r] - mean[i][r];
-        sum += dlt * dlt;
-      }
-#pragma unroll
-      for (int off = 1; off < 16; off <<= 1) sum += xor_shfl(sum, off);
-      if ((lane & 15) == 0) red[wm * WM + i * 16 + 4 * g4 + r][wn] = sum;
-    }
-  __syncthreads();
-#pragma unroll
-  for (int i = 0; i < WM / 16; ++i)
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int lr = wm * WM + i * 16 + 4 * g4 + r;
-      rstd[i][r] = rsqrtf((red[lr][0] + red[lr][1]) * (1.0f / NOUT) + 1e-5f);
-    }
-
-  int gid[WM / 16][4];
-#pragma unroll
-  for (int i = 0; i < WM / 16; ++i)
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int row = m0 + wm * WM + i * 16 + 4 * g4 + r;
-      gid[i][r] = p.film_gamma ? graph_of_node(gt, row < p.M ? row : p.M - 1) : 0;
-    }
-
-#pragma unroll
-  for (int j = 0; j < WN / 16; ++j) {
-    const int col = wn * WN + j * 16 + (lane & 15);
-    const float lg = to_f32(p.ln_g[col]), lb = to_f32(p.ln_b[col]);
-#pragma unroll
-    for (int i = 0; i < WM / 16; ++i)
+    for (int j = 0; j < WN / 16; ++j)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int row = m0 + wm * WM + i * 16 + 4 * g4 + r;
-        float y = (acc[i][j][r] - mean[i][r]) * rstd[i][r] * lg + lb;
-        if (p.film_gamma) {
-          const size_t o = (size_t)gid[i][r] * p.film_stride + col;
-          y = p.film_gamma[o] * y + p.film_beta[o];
-        }
-        if (row < p.M) p.out[(size_t)row * p.ldo + col] = y;
+        const float dlt = acc[i][j][r] - mean[i];
+        sum += dlt * dlt;
       }
+    sum += xor_shfl(sum, 16);
+    sum += xor_shfl(sum, 32);
+    if (lane < 16) red[wm * WM + i * 16 + lane][wn] = sum;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < WM / 16; ++i) {
+    const int lr = wm * WM + i * 16 + (lane & 15);
+    rstd[i] = rsqrtf((red[lr][0] + red[lr][1]) * (1.0f / NOUT) + 1e-5f);
+  }
+
+#pragma unroll
+  for (int i = 0; i < WM / 16; ++i) {
+    const int row = m0 + wm * WM + i * 16 + (lane & 15);
+    const float* fg = nullptr;
+    const float* fb = nullptr;
+    if (p.film_gamma) {
+      const size_t g = (size_t)graph_of_node(gt, row < p.M ? row : p.M - 1) * p.film_stride;
+      fg = p.film_gamma + g;
+      fb = p.film_beta + g;
+    }
+#pragma unroll
+    for (int j = 0; j < WN / 16; ++j) {
+      const int col = wn * WN + j * 16 + c4;
+      float y[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        y[r] = (acc[i][j][r] - mean[i]) * rstd[i] * to_f32(p.ln_g[col + r]) + to_f32(p.ln_b[col + r]);
+        if (fg) y[r] = fg[col + r] * y[r] + fb[col + r];
+      }
+      if (row < p.M) *reinterpret_cast<float4*>(p.out + (size_t)row * p.ldo + col) = make_float4(y[0], y[1], y[2], y[3]);
+    }
   }
 }
 

@@ -44,7 +44,7 @@ struct EmbedPlan {
 };
 struct PlacePlan {
   Carve c;
-  size_t film, y0, y1, qkv, o, z, h1;
+  size_t film, y0, y1, qkv, o, z;
   int qblocks;
 };
 struct SamplePlan {

@@ -73,6 +73,23 @@ struct GemmLnArgs {
 template <typename T>
 hipError_t launch_gemm_ln(const GemmLnArgs<T>& a, const GraphTable& gt, hipStream_t s);
 
+// Fused feed-forward half of a placer layer:
+//   out = FiLM(LN2(z + W2 ReLU(W1 z + b1) + b2)); z and out are the fp32 residual stream.
+template <typename T>
+struct FfnArgs {
+  const float* z; int ldz;          // [M, d]
+  const T* w1; const T* b1;         // [d_ff, d], [d_ff]
+  const T* w2; const T* b2;         // [d, d_ff], [d]
+  const T* ln_g; const T* ln_b;     // [d]
+  const float* film_gamma;          // [G, film_stride] or null
+  const float* film_beta;
+  int film_stride;
+  float* out; int ldo;
+  int M, d, d_ff;
+};
+template <typename T>
+hipError_t launch_ffn_fused(const FfnArgs<T>& a, const GraphTable& gt, hipStream_t s);
+
 // ---- Section 3.2 / 3.3 --------------------------------------------------------
 // Segment attention.  qkv: [N, 3d]; out: [N, d].  gt.blk = per-graph prefix of
 // 128-query blocks.

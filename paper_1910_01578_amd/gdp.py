@@ -29,8 +29,8 @@ GDP_TOPO_IDS = 1
 GDP_MAX_GRAPHS = 128
 
 KERNEL_KINDS = ["graph_prep", "nbr_sample", "gemm_pool_sigmoid", "gather_max", "gemm_update_relu",
-                "meanpool", "film", "gemm_qkv", "seg_attention", "gemm_out_ln", "gemm_ffn1_relu",
-                "gemm_ffn2_ln", "head_lse", "gumbel_sample", "logp_reduce"]
+                "meanpool", "film", "gemm_qkv", "seg_attention", "gemm_out_ln", "ffn_ln",
+                "head_lse", "gumbel_sample", "logp_reduce"]
 K_COUNT = len(KERNEL_KINDS)
 
 

@@ -61,3 +61,20 @@ def test_partial_tiles(k1, k2):
     for dtype in ("f32", "bf16"):
         for ab in (2, 4):
             _replay(ab, k1, k2, BK[dtype])
+
+
+def _xcd_remap(p, total, nx=8):
+    per, rem = divmod(total, nx)
+    x, idx = p % nx, p // nx
+    return x * per + min(x, rem) + idx
+
+
+@pytest.mark.parametrize("total", [1, 2, 7, 8, 9, 10, 63, 64, 65, 813, 2442, 3264, 5000])
+def test_xcd_remap_is_a_bijection_with_contiguous_runs(total):
+    """Work-group ids are dealt to 8 XCDs round-robin; the kernels map them to
+    logical tiles so that every XCD owns one contiguous run of tiles."""
+    logical = [_xcd_remap(p, total) for p in range(total)]
+    assert sorted(logical) == list(range(total))
+    for x in range(8):
+        mine = sorted(logical[p] for p in range(x, total, 8))
+        assert mine == list(range(mine[0], mine[0] + len(mine))) if mine else True
