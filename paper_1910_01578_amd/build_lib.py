@@ -22,6 +22,11 @@ COMMON = ["-O3", "-std=c++17", "-fPIC", f"-I{INCLUDE}", f"-I{CSRC}", "-Wall", "-
 # Packed FP32 instructions stay disabled for all device code.
 DEVICE = [f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 
+# Per-file device flags.  Attention applies vector ALU work (softmax scaling)
+# to its MFMA accumulators on every tile: keeping them in ordinary VGPRs
+# avoids a copy to and from the accumulation registers around each use.
+FILE_FLAGS = {"attention.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
+
 SOURCES = ["graph_kernels.hip", "gemm.hip", "ffn.hip", "attention.hip", "placer_kernels.hip", "sample.hip",
            "gdp_api.hip", "host_plan.cpp"]
 
@@ -30,7 +35,7 @@ def _compile(src: str) -> str:
     path = os.path.join(CSRC, src)
     obj = os.path.join(BUILD, src + ".o")
     if src.endswith(".hip"):
-        cmd = [HIPCC, *COMMON, *DEVICE, "-c", path, "-o", obj]
+        cmd = [HIPCC, *COMMON, *DEVICE, *FILE_FLAGS.get(src, []), "-c", path, "-o", obj]
     else:
         cmd = [HIPCC, *COMMON, "-x", "c++", "-c", path, "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)

@@ -23,6 +23,11 @@ namespace {
 
 constexpr int BQ = kAttnBlockQ;  // queries per work-group
 constexpr int BKV = 64;          // keys per tile
+constexpr float kLazyRescale = 8.0f;
+
+// 2^x on the transcendental unit; results below the normal range flush to 0,
+// which only drops probabilities that are negligible against the row's maximum.
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
 // Contraction over the head dimension: instruction shape per element type.
 template <typename T, int DH> struct QkShape;
@@ -194,7 +199,6 @@ __global__ __launch_bounds__(256) void k_seg_attention(AttnArgs<T> p, GraphTable
   __syncthreads();
   for (int t = 0; t < ntiles; ++t) {
     const int cur = t & 1;
-    if (t + 1 < ntiles) load_tile(t + 1);
     const int kvalid = k1 - (k0 + t * BKV);     // keys of this tile that exist (>= 1)
 
     // S^T blocks: 4 key blocks x 2 query blocks
@@ -210,6 +214,24 @@ __global__ __launch_bounds__(256) void k_seg_attention(AttnArgs<T> p, GraphTable
         sacc[kb][1] = QF::mma(kf, qf[1][s], sacc[kb][1]);
       }
     }
+    // bf16: this tile's V^T fragments for the P V product, read now so that
+    // their LDS latency hides under the softmax.  16x16x32 k slot 8*g4 + i holds
+    // key 32c + 4*g4 + i (i < 4) or 32c + 16 + 4*g4 + (i - 4).
+    bf16x8 vfr[2][DB];
+    if constexpr (sizeof(T) == 2) {
+#pragma unroll
+      for (int c2 = 0; c2 < 2; ++c2)
+#pragma unroll
+        for (int b = 0; b < DB; ++b) {
+          const T* vrow = &sVt[cur][(b * 16 + col) * VS + 32 * c2 + 4 * g4];
+          const uint2 lo = *reinterpret_cast<const uint2*>(vrow);
+          const uint2 hi = *reinterpret_cast<const uint2*>(vrow + 16);
+          vfr[c2][b] = __builtin_bit_cast(bf16x8, make_uint4(lo.x, lo.y, hi.x, hi.y));
+        }
+    }
+    // the next tile travels global -> registers during this one
+    if (t + 1 < ntiles) load_tile(t + 1);
+
     // mask keys past the band end (only the last tile has them)
     if (kvalid < BKV) {
 #pragma unroll
@@ -219,37 +241,51 @@ __global__ __launch_bounds__(256) void k_seg_attention(AttnArgs<T> p, GraphTable
           if (kb * 16 + 4 * g4 + r >= kvalid) { sacc[kb][0][r] = -INFINITY; sacc[kb][1][r] = -INFINITY; }
     }
 
-    // online softmax per query column (scaled log2 domain)
-    float alpha[2];
+    // Online softmax per query column in the scaled log2 domain.  The running
+    // offset m is only raised when a tile's maximum exceeds it by more than
+    // kLazyRescale (a factor 2^8): below that the exponentials stay in range,
+    // and the normalised result does not depend on the offset.  So the O and
+    // l rescale runs only on the few tiles where some lane's offset moves.
+    float mx[2];
 #pragma unroll
     for (int c = 0; c < 2; ++c) {
-      float mx = -INFINITY;
+      float m = -INFINITY;
 #pragma unroll
       for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) mx = fmaxf(mx, sacc[kb][c][r]);
-      mx = fmaxf(mx, xor_shfl(mx, 16));
-      mx = fmaxf(mx, xor_shfl(mx, 32));
-      const float mnew = fmaxf(mrun[c], mx * scale_log2);
-      alpha[c] = exp2f(mrun[c] - mnew);
-      mrun[c] = mnew;
+        for (int r = 0; r < 4; ++r) m = fmaxf(m, sacc[kb][c][r]);
+      m = fmaxf(m, xor_shfl(m, 16));
+      m = fmaxf(m, xor_shfl(m, 32));
+      mx[c] = m * scale_log2;
+    }
+    const bool raise = (mx[0] > mrun[0] + kLazyRescale) || (mx[1] > mrun[1] + kLazyRescale);
+    if (__ballot(raise)) {
+#pragma unroll
+      for (int c = 0; c < 2; ++c) {
+        const float mnew = fmaxf(mrun[c], mx[c]);
+        const float alpha = fast_exp2(mrun[c] - mnew);   // 0 on the first tile (mrun = -inf)
+        mrun[c] = mnew;
+        lrun[c] *= alpha;
+#pragma unroll
+        for (int b = 0; b < DB; ++b) oacc[b][c] *= alpha;
+      }
+    }
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
       float ls = 0.f;
 #pragma unroll
       for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const float e = exp2f(fmaf(sacc[kb][c][r], scale_log2, -mnew));
+          const float e = fast_exp2(fmaf(sacc[kb][c][r], scale_log2, -mrun[c]));
           sacc[kb][c][r] = e;
           ls += e;
         }
-      lrun[c] = lrun[c] * alpha[c] + ls;
-#pragma unroll
-      for (int b = 0; b < DB; ++b) oacc[b][c] *= alpha[c];
+      lrun[c] += ls;
     }
 
     // O^T += V^T P^T
     if constexpr (sizeof(T) == 2) {
-      // 16x16x32: k slot 8*g4 + i holds key 32c + 4*g4 + i (i < 4) or 32c + 16 + 4*g4 + (i - 4)
 #pragma unroll
       for (int c2 = 0; c2 < 2; ++c2) {
         bf16x8 pf[2];
@@ -262,16 +298,8 @@ __global__ __launch_bounds__(256) void k_seg_attention(AttnArgs<T> p, GraphTable
           }
 #pragma unroll
         for (int b = 0; b < DB; ++b) {
-          const T* vrow = &sVt[cur][(b * 16 + col) * VS + 32 * c2 + 4 * g4];
-          const uint2 lo = *reinterpret_cast<const uint2*>(vrow);
-          const uint2 hi = *reinterpret_cast<const uint2*>(vrow + 16);
-          bf16x8 vf;
-          const bf16* l4 = reinterpret_cast<const bf16*>(&lo);
-          const bf16* h4 = reinterpret_cast<const bf16*>(&hi);
-#pragma unroll
-          for (int i = 0; i < 4; ++i) { vf[i] = l4[i]; vf[4 + i] = h4[i]; }
-          oacc[b][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[0], oacc[b][0], 0, 0, 0);
-          oacc[b][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[1], oacc[b][1], 0, 0, 0);
+          oacc[b][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vfr[c2][b], pf[0], oacc[b][0], 0, 0, 0);
+          oacc[b][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vfr[c2][b], pf[1], oacc[b][1], 0, 0, 0);
         }
       }
     } else {

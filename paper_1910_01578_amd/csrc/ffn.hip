@@ -2,17 +2,21 @@
 //
 //   Y' = FiLM_{l+1}( LN2( Z + W_2 ReLU(W_1 Z + b_1) + b_2 ) )
 //
-// One 512-thread work-group (8 waves) owns BM = 64 rows and the whole d-wide
+// One 512-thread work-group (8 waves) owns BM = 128 rows and the whole d-wide
 // output row.  The d_ff hidden layer never leaves the chip: it is produced
 // and consumed in chunks of FC = 64 hidden units (32 in fp32).
-//   phase 1  H_c = ReLU(Z W1_c^T + b1_c)   [64 x FC],  K = d    (4 x 2 waves of 16 x FC/2)
-//   phase 2  Out += H_c W2_c^T             [64 x d],   K = FC   (waves split over rows x columns)
+//   phase 1  H_c = ReLU(Z W1_c^T + b1_c)   [128 x FC], K = d
+//            wave = 32 rows (16 in fp32) x its share of the chunk's units;
+//            its rows of Z stay in registers as operand fragments for every
+//            chunk, so each W1 fragment read from LDS feeds 2 (1) MFMAs.
+//   phase 2  Out += H_c W2_c^T             [128 x d], K = FC
+//            2 x 4 waves of 64 rows x d/4 columns: each fragment read feeds 4
+//            MFMAs.
 // Both products are formed transposed (weights x activations^T), so every
 // lane ends up with 4 consecutive columns of one row: H is written to LDS and
 // the output to memory as whole vectors, and LayerNorm's row sums are mostly
-// in-lane.  Each wave keeps its 16 rows of Z as operand fragments in registers
-// for every chunk; W1_c and W2_c sit in double-buffered LDS, chunk c+1 travelling
-// global -> registers for the whole of chunk c.  Z (fp32, the residual
+// in-lane.  W1_c, W2_c and b1_c sit in double-buffered LDS; chunk c+1
+// travels global -> registers during phase 1 of chunk c.  Z (fp32, the residual
 // stream) is read twice: as the operand and as the residual.
 #include "device_common.h"
 #include "kernels.h"
@@ -20,12 +24,14 @@
 namespace gdp {
 
 namespace {
-constexpr int FBM = 64;    // rows per work-group
-// Hidden units per chunk: 64 for bf16; 32 for fp32 so that the two weight
-// buffers of a d = 256 layer still fit in LDS.
-template <typename T> struct FfnChunk { static constexpr int FC = 64; };
-template <> struct FfnChunk<float> { static constexpr int FC = 32; };
-constexpr int FNT = 512;   // threads per work-group
+constexpr int FBM = 128;       // rows per work-group
+constexpr int kFfnWaves = 8;
+constexpr int FNT = 64 * kFfnWaves;
+// Hidden units per chunk and phase-1 row blocks per wave: 64 and 2 for bf16;
+// 32 and 1 for fp32, so that the weight buffers of a d = 256 layer still fit
+// in LDS and the fp32 Z fragments in registers.
+template <typename T> struct FfnCfg { static constexpr int FC = 64, RB1 = 2; };
+template <> struct FfnCfg<float> { static constexpr int FC = 32, RB1 = 1; };
 
 // Register staging of a ROWS x COLS weight block, read from a row-major
 // matrix with leading dimension ld and written to LDS with row stride S.
@@ -93,23 +99,26 @@ __device__ __forceinline__ void store4(bf16* p, const float (&v)[4]) {
 template <typename T, int D>
 __global__ __launch_bounds__(FNT) void k_ffn_fused(FfnArgs<T> p, GraphTable gt) {
   using MF = Mfma<T>;
-  constexpr int FC = FfnChunk<T>::FC;
-  constexpr int JB1 = FC / 32;     // phase-1 column blocks per wave (FC / 2 columns)
+  constexpr int FC = FfnCfg<T>::FC;
+  constexpr int RB1 = FfnCfg<T>::RB1;       // phase-1 row blocks per wave
+  constexpr int P1M = FBM / (16 * RB1);     // phase-1 wave grid: P1M row groups x P1N unit groups
+  constexpr int P1N = kFfnWaves / P1M;
+  constexpr int HPW = FC / P1N;             // hidden units per wave in phase 1
+  constexpr int JB1 = HPW / 16;
   constexpr int EPV = 16 / sizeof(T);
-  constexpr int S1 = D + EPV;      // sW1 row stride: W1_c rows (hidden units), K = d
-  constexpr int S2 = FC + EPV;     // sW2 row stride: W2 rows (outputs), K = the chunk's hidden units
-  constexpr int SH = FC + EPV;     // sH row stride
-  constexpr int KS1 = D / MF::K;   // phase-1 k-steps
-  constexpr int KS2 = FC / MF::K;  // phase-2 k-steps
-  // phase-2 wave grid: WN2 waves over the d columns, WM2 over the 64 rows
-  constexpr int WN2 = (D / 16) < 8 ? (D / 16) : 8;
-  constexpr int WM2 = 8 / WN2;
-  constexpr int MB2 = FBM / WM2 / 16;   // row blocks per wave
-  constexpr int NB2 = D / WN2 / 16;     // column blocks per wave
-  static_assert(MB2 >= 1 && NB2 >= 1, "phase-2 wave grid");
-  __shared__ __attribute__((aligned(16))) T sW1[2][FC * S1];   // double-buffered weight chunks
+  constexpr int S1 = D + EPV;               // sW1 row stride: W1_c rows (hidden units), K = d
+  constexpr int S2 = FC + EPV;              // sW2 row stride: W2 rows (outputs), K = the chunk's units
+  constexpr int SH = FC + EPV;              // sH row stride
+  constexpr int KS1 = D / MF::K;
+  constexpr int KS2 = FC / MF::K;
+  constexpr int WM2 = 2, WN2 = 4;           // phase-2 wave grid
+  constexpr int MB2 = FBM / WM2 / 16;       // row blocks per wave
+  constexpr int NB2 = D / WN2 / 16;         // column blocks per wave
+  static_assert(P1M * P1N == kFfnWaves && JB1 >= 1 && NB2 >= 1, "wave grids");
+  __shared__ __attribute__((aligned(16))) T sW1[2][FC * S1];
   __shared__ __attribute__((aligned(16))) T sW2[2][D * S2];
   __shared__ __attribute__((aligned(16))) T sH[FBM * SH];
+  __shared__ __attribute__((aligned(16))) T sB1[2][FC];
   __shared__ float red[FBM][WN2];
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -117,22 +126,27 @@ __global__ __launch_bounds__(FNT) void k_ffn_fused(FfnArgs<T> p, GraphTable gt) 
   const int m0 = blockIdx.x * FBM;
   const int NC = p.d_ff / FC;
 
-  // ---- this wave's 16 rows of Z as phase-1 A fragments ----------------------
-  const int w1m = wave >> 1, w1n = wave & 1;          // phase-1: 16 rows x 32 hidden units
-  typename MF::frag zf[KS1];
-  {
-    const int row = m0 + w1m * 16 + col;
+  // ---- this wave's phase-1 rows of Z as operand fragments -------------------
+  const int p1m = wave / P1N, p1n = wave % P1N;
+  typename MF::frag zf[RB1][KS1];
+#pragma unroll
+  for (int i = 0; i < RB1; ++i) {
+    const int row = m0 + (p1m * RB1 + i) * 16 + col;
     const float* zr = p.z + (size_t)(row < p.M ? row : p.M - 1) * p.ldz;
 #pragma unroll
-    for (int s = 0; s < KS1; ++s) zf[s] = ZFrag<T>::load(zr, s * MF::K + MF::KV * g4);
+    for (int s = 0; s < KS1; ++s) zf[i][s] = ZFrag<T>::load(zr, s * MF::K + MF::KV * g4);
   }
-  const int w2m = wave / WN2, w2n = wave % WN2;       // phase-2 position
+  const int w2m = wave / WN2, w2n = wave % WN2;
 
-  // ---- weight staging: W1_c = W1 rows [c*FC, c*FC+FC) x d; W2_c = W2 rows 0..d x cols
-  // [c*FC, c*FC+FC).  Chunk c+1 travels global -> registers during the whole of
-  // chunk c and lands in the other LDS buffer at its end.
+  // ---- weight staging: W1_c = W1 rows [c*FC, c*FC+FC) x d; W2_c = W2 rows 0..d x
+  // columns [c*FC, c*FC+FC).  The chunk's FC biases travel with its weights
+  // (16-byte pieces held by the first BCH threads) and are read from LDS, so
+  // that no wait in phase 1 is a wait on global memory (which would include
+  // the next chunk's prefetch).
   WStage<T, FC, D, S1> st1;
   WStage<T, D, FC, S2> st2;
+  constexpr int BCH = FC / EPV;
+  uint4 bst = make_uint4(0u, 0u, 0u, 0u);
 
   f32x4 oacc[MB2][NB2];
 #pragma unroll
@@ -140,10 +154,12 @@ __global__ __launch_bounds__(FNT) void k_ffn_fused(FfnArgs<T> p, GraphTable gt) 
 #pragma unroll
     for (int j = 0; j < NB2; ++j) oacc[i][j] = zero4();
 
+  if (threadIdx.x < BCH) bst = *reinterpret_cast<const uint4*>(p.b1 + threadIdx.x * EPV);
   st1.load(p.w1, D);
   st2.load(p.w2, p.d_ff);
   st1.store(sW1[0]);
   st2.store(sW2[0]);
+  if (threadIdx.x < BCH) *reinterpret_cast<uint4*>(&sB1[0][threadIdx.x * EPV]) = bst;
   __syncthreads();
 
   for (int c = 0; c < NC; ++c) {
@@ -151,32 +167,49 @@ __global__ __launch_bounds__(FNT) void k_ffn_fused(FfnArgs<T> p, GraphTable gt) 
     if (c + 1 < NC) {
       st1.load(p.w1 + (size_t)(c + 1) * FC * D, D);
       st2.load(p.w2 + (size_t)(c + 1) * FC, p.d_ff);
+      if (threadIdx.x < BCH) bst = *reinterpret_cast<const uint4*>(p.b1 + (c + 1) * FC + threadIdx.x * EPV);
     }
-    // phase 1: this wave's 16 x FC/2 block of H_c
-    f32x4 hacc[JB1];
+    // phase 1: H_c on this wave's RB1 x 16 rows x HPW units
+    f32x4 hacc[RB1][JB1];
 #pragma unroll
-    for (int j = 0; j < JB1; ++j) hacc[j] = zero4();
+    for (int i = 0; i < RB1; ++i)
+#pragma unroll
+      for (int j = 0; j < JB1; ++j) hacc[i][j] = zero4();
 #pragma unroll
     for (int s = 0; s < KS1; ++s) {
 #pragma unroll
       for (int j = 0; j < JB1; ++j) {
-        const typename MF::frag bw =
-            MF::load(&sW1[cur][(w1n * (FC / 2) + j * 16 + col) * S1 + s * MF::K + MF::KV * g4]);
-        hacc[j] = MF::mma(bw, zf[s], hacc[j]);
+        const typename MF::frag bw = MF::load(&sW1[cur][(p1n * HPW + j * 16 + col) * S1 + s * MF::K + MF::KV * g4]);
+#pragma unroll
+        for (int i = 0; i < RB1; ++i) hacc[i][j] = MF::mma(bw, zf[i][s], hacc[i][j]);
       }
     }
-    // lane holds row w1m * 16 + col and 4 consecutive hidden units hc + [0, 4)
+    // Chunk c + 1 lands in the other buffers now: they were last read in
+    // chunk c - 1, before its final barrier, and phase 2 needs no staging
+    // registers this way.
+    if (c + 1 < NC) {
+      st1.store(sW1[cur ^ 1]);
+      st2.store(sW2[cur ^ 1]);
+      if (threadIdx.x < BCH) *reinterpret_cast<uint4*>(&sB1[cur ^ 1][threadIdx.x * EPV]) = bst;
+    }
+    // lane holds row (p1m * RB1 + i) * 16 + col and the 4 consecutive units hc + [0, 4)
 #pragma unroll
     for (int j = 0; j < JB1; ++j) {
-      const int hc = w1n * (FC / 2) + j * 16 + 4 * g4;
-      float h[4];
+      const int hc = p1n * HPW + j * 16 + 4 * g4;
+      float b[4];
 #pragma unroll
-      for (int r = 0; r < 4; ++r) h[r] = fmaxf(hacc[j][r] + to_f32(p.b1[c * FC + hc + r]), 0.f);
-      store4(&sH[(w1m * 16 + col) * SH + hc], h);
+      for (int r = 0; r < 4; ++r) b[r] = to_f32(sB1[cur][hc + r]);
+#pragma unroll
+      for (int i = 0; i < RB1; ++i) {
+        float h[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) h[r] = fmaxf(hacc[i][j][r] + b[r], 0.f);
+        store4(&sH[((p1m * RB1 + i) * 16 + col) * SH + hc], h);
+      }
     }
-    __syncthreads();                 // sH complete
+    __syncthreads();                 // sH and chunk c + 1 complete
 
-    // phase 2: Out += H_c W2_c^T on this wave's rows x columns
+    // phase 2: Out += H_c W2_c^T on this wave's 64 rows x d/4 columns
 #pragma unroll
     for (int s = 0; s < KS2; ++s) {
       typename MF::frag af[MB2], bf[NB2];
@@ -191,12 +224,7 @@ __global__ __launch_bounds__(FNT) void k_ffn_fused(FfnArgs<T> p, GraphTable gt) 
 #pragma unroll
         for (int j = 0; j < NB2; ++j) oacc[i][j] = MF::mma(bf[j], af[i], oacc[i][j]);
     }
-    if (c + 1 < NC) {
-      // the other buffers were last read during chunk c - 1, before its final barrier
-      st1.store(sW1[cur ^ 1]);
-      st2.store(sW2[cur ^ 1]);
-    }
-    __syncthreads();                 // chunk c + 1 staged; sH free
+    __syncthreads();                 // sH and this chunk's buffers free
   }
 
   // ---- epilogue: + b2 + residual Z, LayerNorm over the d columns, FiLM ------
@@ -286,7 +314,7 @@ __global__ __launch_bounds__(FNT) void k_ffn_fused(FfnArgs<T> p, GraphTable gt) 
 template <typename T>
 hipError_t launch_ffn_fused(const FfnArgs<T>& a, const GraphTable& gt, hipStream_t s) {
   if (a.M <= 0) return hipSuccess;
-  if (a.d_ff <= 0 || a.d_ff % FfnChunk<T>::FC) return hipErrorInvalidValue;
+  if (a.d_ff <= 0 || a.d_ff % FfnCfg<T>::FC) return hipErrorInvalidValue;
   dim3 grid((a.M + FBM - 1) / FBM), block(FNT);
   switch (a.d) {
     case 64: hipLaunchKernelGGL((k_ffn_fused<T, 64>), grid, block, 0, s, a, gt); break;
