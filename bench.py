@@ -49,8 +49,10 @@ def flop_model(cfg, g, stats):
         "gather_max": ("hbm", float(gather_bytes)),
         "gemm_qkv": ("mfma", 2.0 * N * d * 3 * d),
         "seg_attention": ("mfma", 4.0 * d * keys),
-        "gemm_out_ln": ("mfma", 2.0 * N * d * d),
-        "ffn_ln": ("mfma", 4.0 * N * d * dff),
+        # per launch, averaged over the placer layers: W_o, the FFN, and (all but
+        # the last layer) the next layer's QKV projection
+        "post_attn": ("mfma", 2.0 * N * d * d + 4.0 * N * d * dff
+                      + (cfg.placer_layers - 1) / cfg.placer_layers * 2.0 * N * d * 3 * d),
     }, keys
 
 

@@ -249,11 +249,10 @@ typedef enum gdp_kernel_kind {
   GDP_K_GEMM_UPDATE,     /* Eq. 3 ReLU(h W_self^T + A W_neigh^T + b)          */
   GDP_K_MEANPOOL,        /* x0 = per-graph mean                              */
   GDP_K_FILM,            /* gamma/beta GEMVs and the first layer's FiLM       */
-  GDP_K_GEMM_QKV,        /* Y W_qkv^T + b                                    */
+  GDP_K_GEMM_QKV,        /* the first layer's Y W_qkv^T + b                  */
   GDP_K_ATTENTION,       /* segment attention                                */
-  GDP_K_GEMM_OUT_LN,     /* LN1(Y + O W_o^T + b)                              */
-  GDP_K_FFN_LN,          /* LN2(Z + W_2 ReLU(W_1 Z + b_1) + b_2), fused, with
-                            the next layer's FiLM                            */
+  GDP_K_POST_ATTN,       /* fused rest of a layer: LN1(Y + O W_o^T + b),
+                            LN2(Z + FFN(Z)), the next layer's FiLM and QKV  */
   GDP_K_HEAD,            /* logits and lse                                   */
   GDP_K_SAMPLE,          /* Gumbel-max sampling                              */
   GDP_K_LOGP_REDUCE,     /* per-graph log-prob sums                          */

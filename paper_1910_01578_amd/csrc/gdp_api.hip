@@ -177,12 +177,10 @@ static int place_impl(const gdp_graph* g, const T* node_emb, const float* graph_
   float* film = at<float>(ws, pl.film);       // [L][2][G][d]: gamma then beta
   auto gamma_of = [&](int l) { return film + (size_t)l * 2 * G * d; };
   auto beta_of = [&](int l) { return film + (size_t)l * 2 * G * d + (size_t)G * d; };
-  // Residual stream (layer inputs Y and LN1 outputs Z) in fp32; GEMM operands,
-  // attention inputs/outputs and the FFN hidden layer in T.
+  // Residual stream (layer inputs Y) in fp32; attention inputs and outputs in T.
   float* ybuf[2] = {at<float>(ws, pl.y0), at<float>(ws, pl.y1)};
   T* qkv = at<T>(ws, pl.qkv);
   T* o = at<T>(ws, pl.o);
-  float* z = at<float>(ws, pl.z);
 
   const float* y = ybuf[0];
   if (p->film) {
@@ -199,26 +197,35 @@ static int place_impl(const gdp_graph* g, const T* node_emb, const float* graph_
 
   GraphTable qt = make_table(g);
   const int qblocks = prefix_blocks_attention(g->graph_ptr_h, G, p->seg_len, kAttnQ, qt.blk);
+  // Layer 0's projection runs on its own; every later one is fused into the
+  // previous layer's post-attention kernel.
+  {
+    const gdp_placer_layer& L0 = p->layers[0];
+    const GemmArgs<float, T, T> a_qkv = {y, d, static_cast<const T*>(L0.w_qkv), d, nullptr, 0, nullptr, 0,
+                                         static_cast<const T*>(L0.b_qkv), qkv, 3 * d, N, 3 * d};
+    GDP_LAUNCH(GDP_K_GEMM_QKV, (launch_gemm<float, T, T>(a_qkv, EPI_BIAS, st)));
+  }
   int cur = 0;
   for (int l = 0; l < L; ++l) {
     const gdp_placer_layer& Ly = p->layers[l];
-    const GemmArgs<float, T, T> a_qkv = {y, d, static_cast<const T*>(Ly.w_qkv), d, nullptr, 0, nullptr, 0,
-                               static_cast<const T*>(Ly.b_qkv), qkv, 3 * d, N, 3 * d};
-    GDP_LAUNCH(GDP_K_GEMM_QKV, (launch_gemm<float, T, T>(a_qkv, EPI_BIAS, st)));
     const AttnArgs<T> a_att = {qkv, 3 * d, o, d, d, p->n_heads, p->seg_len, p->mem_len, qblocks};
     GDP_LAUNCH(GDP_K_ATTENTION, launch_attention<T>(a_att, qt, st));
-    const GemmLnArgs<T> a_out = {o, d, d, static_cast<const T*>(Ly.w_o), static_cast<const T*>(Ly.b_o), y, d,
-                                 static_cast<const T*>(Ly.ln1_g), static_cast<const T*>(Ly.ln1_b),
-                                 nullptr, nullptr, 0, z, d, N, d};
-    GDP_LAUNCH(GDP_K_GEMM_OUT_LN, launch_gemm_ln<T>(a_out, gt, st));
-    const bool next_film = p->film && l + 1 < L;
+    const bool last = l + 1 == L;
+    const bool next_film = p->film && !last;
+    const gdp_placer_layer* Ln = last ? nullptr : &p->layers[l + 1];
     float* ynext = ybuf[cur ^ 1];
-    const FfnArgs<T> a_ffn = {z, d, static_cast<const T*>(Ly.w_1), static_cast<const T*>(Ly.b_1),
-                              static_cast<const T*>(Ly.w_2), static_cast<const T*>(Ly.b_2),
-                              static_cast<const T*>(Ly.ln2_g), static_cast<const T*>(Ly.ln2_b),
-                              next_film ? gamma_of(l + 1) : nullptr, next_film ? beta_of(l + 1) : nullptr, d,
-                              ynext, d, N, d, p->d_ff};
-    GDP_LAUNCH(GDP_K_FFN_LN, launch_ffn_fused<T>(a_ffn, gt, st));
+    const PostAttnArgs<T> a_post = {o, d, y, d,
+                                    static_cast<const T*>(Ly.w_o), static_cast<const T*>(Ly.b_o),
+                                    static_cast<const T*>(Ly.ln1_g), static_cast<const T*>(Ly.ln1_b),
+                                    static_cast<const T*>(Ly.w_1), static_cast<const T*>(Ly.b_1),
+                                    static_cast<const T*>(Ly.w_2), static_cast<const T*>(Ly.b_2),
+                                    static_cast<const T*>(Ly.ln2_g), static_cast<const T*>(Ly.ln2_b),
+                                    next_film ? gamma_of(l + 1) : nullptr, next_film ? beta_of(l + 1) : nullptr, d,
+                                    ynext, d,
+                                    Ln ? static_cast<const T*>(Ln->w_qkv) : nullptr,
+                                    Ln ? static_cast<const T*>(Ln->b_qkv) : nullptr,
+                                    Ln ? qkv : nullptr, 3 * d, N, d, p->d_ff};
+    GDP_LAUNCH(GDP_K_POST_ATTN, launch_post_attention<T>(a_post, gt, st));
     cur ^= 1;
     y = ynext;
   }
@@ -371,8 +378,8 @@ extern "C" int gdp_timer_end(double* total_ms, int64_t* launches) {
 extern "C" const char* gdp_kernel_kind_name(int32_t kind) {
   static const char* names[GDP_K_COUNT] = {
       "graph_prep", "nbr_sample",    "gemm_pool_sigmoid", "gather_max", "gemm_update_relu",
-      "meanpool",   "film",          "gemm_qkv",          "seg_attention", "gemm_out_ln",
-      "ffn_ln",     "head_lse",      "gumbel_sample",     "logp_reduce"};
+      "meanpool",   "film",          "gemm_qkv",          "seg_attention", "post_attn",
+      "head_lse",   "gumbel_sample", "logp_reduce"};
   if (kind < 0 || kind >= GDP_K_COUNT) return "";
   return names[kind];
 }

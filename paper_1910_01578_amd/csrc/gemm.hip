@@ -249,121 +249,4 @@ template hipError_t launch_gemm<float, bf16, bf16>(const GemmArgs<float, bf16, b
 template hipError_t launch_gemm<bf16, bf16, float>(const GemmArgs<bf16, bf16, float>&, int, hipStream_t);
 template hipError_t launch_gemm<float, bf16, float>(const GemmArgs<float, bf16, float>&, int, hipStream_t);
 
-// ---------------------------------------------------------------------------
-// Residual + LayerNorm epilogue over full rows: BM = 64 rows x the whole
-// N = d output row per work-group, 2 x 2 waves (32 rows x N/2 columns each).
-// The residual input and the output are fp32 (the residual stream).  Row
-// statistics are taken in two passes (mean, then centred second moment).
-template <typename T, int NOUT>
-__global__ __launch_bounds__(256) void k_gemm_ln(GemmLnArgs<T> p, GraphTable gt) {
-  constexpr int BM = 64, WM = 32, WN = NOUT / 2;
-  constexpr int S = TileCfg<T>::STRIDE;
-  __shared__ __attribute__((aligned(16))) T sA[2 * BM * S];
-  __shared__ __attribute__((aligned(16))) T sB[2 * NOUT * S];
-  __shared__ float red[BM][2];
-  const int m0 = blockIdx.x * BM;
-  f32x4 acc[WM / 16][WN / 16];
-  gemm_mainloop<T, T, BM, NOUT, WM, WN>(p.a, p.lda, p.w, p.K, (const T*)nullptr, 0, (const T*)nullptr, 0, p.M, m0, 0,
-                                        sA, sB, acc);
-
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
-  const int c4 = 4 * (lane >> 4);
-
-  // v = acc + bias + residual; lane owns row lr(i) and columns col(j) + [0, 4)
-#pragma unroll
-  for (int i = 0; i < WM / 16; ++i) {
-    const int row = m0 + wm * WM + i * 16 + (lane & 15);
-#pragma unroll
-    for (int j = 0; j < WN / 16; ++j) {
-      const int col = wn * WN + j * 16 + c4;
-      float4 res = make_float4(0.f, 0.f, 0.f, 0.f);
-      if (row < p.M) res = *reinterpret_cast<const float4*>(p.res + (size_t)row * p.ldr + col);
-      acc[i][j][0] += to_f32(p.bias[col + 0]) + res.x;
-      acc[i][j][1] += to_f32(p.bias[col + 1]) + res.y;
-      acc[i][j][2] += to_f32(p.bias[col + 2]) + res.z;
-      acc[i][j][3] += to_f32(p.bias[col + 3]) + res.w;
-    }
-  }
-
-  // Row statistics: in-lane over the lane's columns, then across the 4 lane
-  // groups holding the same row (xor 16, 32), then the two column halves.
-  float mean[WM / 16], rstd[WM / 16];
-#pragma unroll
-  for (int i = 0; i < WM / 16; ++i) {
-    float sum = 0.f;
-#pragma unroll
-    for (int j = 0; j < WN / 16; ++j) sum += (acc[i][j][0] + acc[i][j][1]) + (acc[i][j][2] + acc[i][j][3]);
-    sum += xor_shfl(sum, 16);
-    sum += xor_shfl(sum, 32);
-    if (lane < 16) red[wm * WM + i * 16 + lane][wn] = sum;
-  }
-  __syncthreads();
-#pragma unroll
-  for (int i = 0; i < WM / 16; ++i) {
-    const int lr = wm * WM + i * 16 + (lane & 15);
-    mean[i] = (red[lr][0] + red[lr][1]) * (1.0f / NOUT);
-  }
-  __syncthreads();
-#pragma unroll
-  for (int i = 0; i < WM / 16; ++i) {
-    float sum = 0.f;
-#pragma unroll
-    for (int j = 0; j < WN / 16; ++j)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const float dlt = acc[i][j][r] - mean[i];
-        sum += dlt * dlt;
-      }
-    sum += xor_shfl(sum, 16);
-    sum += xor_shfl(sum, 32);
-    if (lane < 16) red[wm * WM + i * 16 + lane][wn] = sum;
-  }
-  __syncthreads();
-#pragma unroll
-  for (int i = 0; i < WM / 16; ++i) {
-    const int lr = wm * WM + i * 16 + (lane & 15);
-    rstd[i] = rsqrtf((red[lr][0] + red[lr][1]) * (1.0f / NOUT) + 1e-5f);
-  }
-
-#pragma unroll
-  for (int i = 0; i < WM / 16; ++i) {
-    const int row = m0 + wm * WM + i * 16 + (lane & 15);
-    const float* fg = nullptr;
-    const float* fb = nullptr;
-    if (p.film_gamma) {
-      const size_t g = (size_t)graph_of_node(gt, row < p.M ? row : p.M - 1) * p.film_stride;
-      fg = p.film_gamma + g;
-      fb = p.film_beta + g;
-    }
-#pragma unroll
-    for (int j = 0; j < WN / 16; ++j) {
-      const int col = wn * WN + j * 16 + c4;
-      float y[4];
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        y[r] = (acc[i][j][r] - mean[i]) * rstd[i] * to_f32(p.ln_g[col + r]) + to_f32(p.ln_b[col + r]);
-        if (fg) y[r] = fg[col + r] * y[r] + fb[col + r];
-      }
-      if (row < p.M) *reinterpret_cast<float4*>(p.out + (size_t)row * p.ldo + col) = make_float4(y[0], y[1], y[2], y[3]);
-    }
-  }
-}
-
-template <typename T>
-hipError_t launch_gemm_ln(const GemmLnArgs<T>& a, const GraphTable& gt, hipStream_t s) {
-  if (a.M <= 0) return hipSuccess;
-  if (a.K <= 0 || a.K % 8) return hipErrorInvalidValue;
-  dim3 grid((a.M + 63) / 64), block(256);
-  switch (a.N) {
-    case 64: hipLaunchKernelGGL((k_gemm_ln<T, 64>), grid, block, 0, s, a, gt); break;
-    case 128: hipLaunchKernelGGL((k_gemm_ln<T, 128>), grid, block, 0, s, a, gt); break;
-    case 256: hipLaunchKernelGGL((k_gemm_ln<T, 256>), grid, block, 0, s, a, gt); break;
-    default: return hipErrorInvalidValue;
-  }
-  return hipGetLastError();
-}
-template hipError_t launch_gemm_ln<float>(const GemmLnArgs<float>&, const GraphTable&, hipStream_t);
-template hipError_t launch_gemm_ln<bf16>(const GemmLnArgs<bf16>&, const GraphTable&, hipStream_t);
-
 }  // namespace gdp

@@ -168,7 +168,6 @@ void plan_place(const gdp_graph* g, const gdp_placer* pl, PlacePlan* p) {
   p->y1 = carve_add(&p->c, N * d * 4);
   p->qkv = carve_add(&p->c, N * 3 * d * es);
   p->o = carve_add(&p->c, N * d * es);
-  p->z = carve_add(&p->c, N * d * 4);
 }
 
 void plan_sample(const gdp_graph* g, int32_t k, SamplePlan* p) {

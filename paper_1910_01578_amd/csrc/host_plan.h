@@ -44,7 +44,7 @@ struct EmbedPlan {
 };
 struct PlacePlan {
   Carve c;
-  size_t film, y0, y1, qkv, o, z;
+  size_t film, y0, y1, qkv, o;
   int qblocks;
 };
 struct SamplePlan {

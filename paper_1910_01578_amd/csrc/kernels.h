@@ -54,41 +54,30 @@ struct GemmArgs {
 template <typename TA, typename T, typename TO>
 hipError_t launch_gemm(const GemmArgs<TA, T, TO>& a, int epi, hipStream_t s);
 
-// out[M, N] = FiLM(LN(res + A W^T + bias)), N = the full row (64, 128 or 256).
-// res and out belong to the residual stream and are fp32.  FiLM (optional)
-// applies the per-graph gamma/beta of the *next* layer.
+// Everything of a placer layer after its attention, and the start of the next:
+//   Z    = LN1(y + o W_o^T + b_o)
+//   y'   = FiLM(LN2(Z + W_2 ReLU(W_1 Z + b_1) + b_2))   (FiLM of the next layer, optional)
+//   qkv' = y' W_qkv^T + b_qkv                           (next layer's projection, optional)
+// y and y' are the fp32 residual stream; d is 64, 128 or 256.
 template <typename T>
-struct GemmLnArgs {
-  const T* a; int lda; int K;
-  const T* w;       // [N, K]
-  const T* bias;    // [N]
-  const float* res; int ldr;
-  const T* ln_g; const T* ln_b;
-  const float* film_gamma;  // [G, film_stride] or null
-  const float* film_beta;   // [G, film_stride]
-  int film_stride;
-  float* out; int ldo;
-  int M, N;
-};
-template <typename T>
-hipError_t launch_gemm_ln(const GemmLnArgs<T>& a, const GraphTable& gt, hipStream_t s);
-
-// Fused feed-forward half of a placer layer:
-//   out = FiLM(LN2(z + W2 ReLU(W1 z + b1) + b2)); z and out are the fp32 residual stream.
-template <typename T>
-struct FfnArgs {
-  const float* z; int ldz;          // [M, d]
+struct PostAttnArgs {
+  const T* o; int ldo;              // attention output [M, d]
+  const float* y; int ldy;          // layer input [M, d]
+  const T* w_o; const T* b_o;       // [d, d], [d]
+  const T* ln1_g; const T* ln1_b;   // [d]
   const T* w1; const T* b1;         // [d_ff, d], [d_ff]
   const T* w2; const T* b2;         // [d, d_ff], [d]
-  const T* ln_g; const T* ln_b;     // [d]
+  const T* ln2_g; const T* ln2_b;   // [d]
   const float* film_gamma;          // [G, film_stride] or null
   const float* film_beta;
   int film_stride;
-  float* out; int ldo;
+  float* y_out; int ldyo;           // [M, d]
+  const T* w_qkv; const T* b_qkv;   // [3d, d], [3d] or null
+  T* qkv_out; int ldq;              // [M, ldq >= 3d]
   int M, d, d_ff;
 };
 template <typename T>
-hipError_t launch_ffn_fused(const FfnArgs<T>& a, const GraphTable& gt, hipStream_t s);
+hipError_t launch_post_attention(const PostAttnArgs<T>& a, const GraphTable& gt, hipStream_t s);
 
 // ---- Section 3.2 / 3.3 --------------------------------------------------------
 // Segment attention.  qkv: [N, 3d]; out: [N, d].  gt.blk = per-graph prefix of

@@ -1,11 +1,12 @@
-"""CPU replay of the GEMM tile loader's index arithmetic.
+"""CPU replay of the index arithmetic of the matrix-core kernels' staging.
 
-The matrix-core GEMM stages ROWS x BK tiles in 16-byte chunks; every K
-segment is tiled on its own and chunks at or past the segment end are never
-read.  This test replays that arithmetic (the same constants as the kernel:
-BK = 64 for bf16, 32 for fp32; 16-byte chunks of the staged type) for every
-GEMM each workload issues and checks that every read lands inside its row
-and that every K column is covered exactly once."""
+The GEMM stages ROWS x BK tiles in 16-byte chunks; every K segment is tiled
+on its own and chunks at or past the segment end are never read.  The
+post-attention layer kernel stages weight and activation chunks of FC units
+in 16-byte pieces spread over its 512 threads.  These tests replay both (the
+same constants as the kernels) for every call each workload issues and check
+that every read lands inside its matrix and that every element is covered
+exactly once."""
 import pytest
 
 from paper_1910_01578_amd import workloads as W
@@ -21,11 +22,7 @@ def _gemm_calls(cfg):
         hin = cfg.feat_dim if l == 0 else cfg.hidden
         calls.append(("pool", b, hin, 0))
         calls.append(("update", b, hin, cfg.hidden))
-    for _ in range(cfg.placer_layers):
-        calls.append(("qkv", 4, cfg.d_model, 0))       # A = fp32 residual stream
-        calls.append(("out_ln", b, cfg.d_model, 0))
-        calls.append(("ffn1", 4, cfg.d_model, 0))
-        calls.append(("ffn2_ln", b, cfg.d_ff, 0))
+    calls.append(("qkv", 4, cfg.d_model, 0))           # layer 0; A = fp32 residual stream
     return calls
 
 
@@ -78,3 +75,64 @@ def test_xcd_remap_is_a_bijection_with_contiguous_runs(total):
     for x in range(8):
         mine = sorted(logical[p] for p in range(x, total, 8))
         assert mine == list(range(mine[0], mine[0] + len(mine))) if mine else True
+
+
+# ---- post-attention layer kernel ------------------------------------------------
+LAYER_FC = {"bf16": 64, "f32": 32}
+LAYER_ROWS = 128
+LAYER_THREADS = 512
+
+
+def _stage_reads(rows, cols, elem_bytes, base, ld, rows_valid=None):
+    """Element offsets read by Stage<T, rows, cols>.load(base, ld, rows_valid)."""
+    epv = 16 // elem_bytes
+    cpr = cols // epv
+    chunks = rows * cpr
+    assert chunks % LAYER_THREADS == 0, "block must split evenly over the work-group"
+    rv = rows if rows_valid is None else rows_valid
+    out = []
+    for q in range(chunks):
+        r, c = q // cpr, (q % cpr) * epv
+        if r < rv:
+            out.append((base + r * ld + c, epv))
+    return out
+
+
+def _check_cover(reads, size, expect):
+    seen = []
+    for off, n in reads:
+        assert 0 <= off and off + n <= size, (off, n, size)
+        seen.extend(range(off, off + n))
+    assert sorted(seen) == sorted(expect)
+
+
+@pytest.mark.parametrize("name", W.CONFIG_ORDER)
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_layer_kernel_staging_stays_in_bounds(name, dtype):
+    cfg = W.get_config(name).replace(dtype=dtype)
+    d, dff, eb, fc = cfg.d_model, cfg.d_ff, (2 if dtype == "bf16" else 4), LAYER_FC[dtype]
+    assert d % fc == 0 and dff % fc == 0
+    # W_1 [dff, d]: chunk c = rows [c fc, c fc + fc) x d;  W_qkv [3d, d] likewise
+    for rows_total, mat in ((dff, "w1"), (3 * d, "wqkv")):
+        reads = []
+        for c in range(rows_total // fc):
+            reads += _stage_reads(fc, d, eb, c * fc * d, d)
+        _check_cover(reads, rows_total * d, range(rows_total * d))
+    # W_2 [d, dff]: chunk c = all d rows x columns [c fc, c fc + fc);  W_o [d, d] likewise
+    for k_total in (dff, d):
+        reads = []
+        for c in range(k_total // fc):
+            reads += _stage_reads(d, fc, eb, c * fc, k_total)
+        _check_cover(reads, d * k_total, range(d * k_total))
+    # O [M, d]: block m0 = rows [m0, m0 + 128) (rows >= M not read) x column chunks
+    M = 300 if cfg.n_nodes > 300 else cfg.n_nodes
+    reads = []
+    for m0 in range(0, M, LAYER_ROWS):
+        for c in range(d // fc):
+            reads += _stage_reads(LAYER_ROWS, fc, eb, m0 * d + c * fc, d, rows_valid=M - m0)
+    _check_cover(reads, M * d, range(M * d))
+    # biases: the first fc / epv threads read 16 bytes each
+    epv = 16 // eb
+    for n_total in (dff, 3 * d):
+        seen = [c * fc + t * epv + e for c in range(n_total // fc) for t in range(fc // epv) for e in range(epv)]
+        assert sorted(seen) == list(range(n_total))
