@@ -91,7 +91,7 @@ template <> struct VBlock<float> {
 }  // namespace
 
 template <typename T, int DH>
-__global__ __launch_bounds__(256) void k_seg_attention(AttnArgs<T> p, GraphTable gt, float scale_log2) {
+__global__ __launch_bounds__(256) void k_seg_attention(AttnArgs<T> p, GraphTable gt) {
   constexpr int EPV = 16 / sizeof(T);
   constexpr int KS = DH + EPV;          // sK row stride
   // sVt row stride: 68 elements puts the 16 rows of an 8-byte bf16 fragment
@@ -149,8 +149,8 @@ __global__ __launch_bounds__(256) void k_seg_attention(AttnArgs<T> p, GraphTable
   constexpr int VTHREADS = (BKV / 4) * (DH / 4);
   static_assert(VTHREADS <= 256, "V block split");
   using V4 = typename VBlock<T>::raw;           // 4 consecutive elements
-  uint4 rk[(CHUNKS + 255) / 256];
-  V4 rv[4];
+  uint4 rk[(CHUNKS + 255) / 256] = {};
+  V4 rv[4] = {};
   const int vkg = threadIdx.x % (BKV / 4), vdg = threadIdx.x / (BKV / 4);
   auto load_tile = [&](int t) {
     const int kb = k0 + t * BKV;
@@ -158,18 +158,17 @@ __global__ __launch_bounds__(256) void k_seg_attention(AttnArgs<T> p, GraphTable
     for (int i = 0; i < (CHUNKS + 255) / 256; ++i) {
       const int c = threadIdx.x + i * 256;
       const int row = c / CPR, cc = (c % CPR) * EPV;
-      const int key = kb + row;
-      if (c < CHUNKS && key < k1)
-        rk[i] = *reinterpret_cast<const uint4*>(Kp + (size_t)key * p.ldq + cc);
-      else
-        rk[i] = make_uint4(0u, 0u, 0u, 0u);
+      // Keys past the band end read the last valid row instead: their scores
+      // are masked to -inf, so they carry P = 0 against finite values.
+      const int key = min(kb + row, k1 - 1);
+      if (CHUNKS % 256 == 0 || c < CHUNKS) rk[i] = *reinterpret_cast<const uint4*>(Kp + (size_t)key * p.ldq + cc);
     }
+    if (threadIdx.x < VTHREADS) {                 // whole waves
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int key = kb + 4 * vkg + j;
-      rv[j] = (threadIdx.x < VTHREADS && key < k1)
-                  ? *reinterpret_cast<const V4*>(Vp + (size_t)key * p.ldq + 4 * vdg)
-                  : VBlock<T>::zero();
+      for (int j = 0; j < 4; ++j) {
+        const int key = min(kb + 4 * vkg + j, k1 - 1);
+        rv[j] = *reinterpret_cast<const V4*>(Vp + (size_t)key * p.ldq + 4 * vdg);
+      }
     }
   };
   auto store_tile = [&](int buf) {
@@ -188,11 +187,14 @@ __global__ __launch_bounds__(256) void k_seg_attention(AttnArgs<T> p, GraphTable
     }
   };
 
+  // O^T accumulators, and the softmax denominators: every row of osum[c]
+  // holds sum_k P[k][q] for the lane's query column (a matrix-core product
+  // with a block of ones, from the same rounded P as the numerator).
   f32x4 oacc[DB][2];
+  f32x4 osum[2] = {zero4(), zero4()};
 #pragma unroll
   for (int b = 0; b < DB; ++b) { oacc[b][0] = zero4(); oacc[b][1] = zero4(); }
-  float mrun[2] = {-INFINITY, -INFINITY};
-  float lrun[2] = {0.f, 0.f};
+  float mrun[2] = {0.f, 0.f};     // running offset m of each query column (log2 domain)
 
   load_tile(0);
   store_tile(0);
@@ -201,12 +203,16 @@ __global__ __launch_bounds__(256) void k_seg_attention(AttnArgs<T> p, GraphTable
     const int cur = t & 1;
     const int kvalid = k1 - (k0 + t * BKV);     // keys of this tile that exist (>= 1)
 
-    // S^T blocks: 4 key blocks x 2 query blocks
+    // S^T blocks: 4 key blocks x 2 query blocks.  Q arrives pre-scaled by
+    // log2(e) / sqrt(d_head) and every block starts from -m, so the MFMA
+    // leaves the offset score s - m of the log2 domain.
     f32x4 sacc[4][2];
+    const f32x4 negm[2] = {f32x4{-mrun[0], -mrun[0], -mrun[0], -mrun[0]},
+                           f32x4{-mrun[1], -mrun[1], -mrun[1], -mrun[1]}};
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) {
-      sacc[kb][0] = zero4();
-      sacc[kb][1] = zero4();
+      sacc[kb][0] = negm[0];
+      sacc[kb][1] = negm[1];
 #pragma unroll
       for (int s = 0; s < QS::STEPS; ++s) {
         const typename QF::t kf = QF::load(&sK[cur][(kb * 16 + col) * KS + s * QS::K + QS::KV * g4]);
@@ -241,11 +247,13 @@ __global__ __launch_bounds__(256) void k_seg_attention(AttnArgs<T> p, GraphTable
           if (kb * 16 + 4 * g4 + r >= kvalid) { sacc[kb][0][r] = -INFINITY; sacc[kb][1][r] = -INFINITY; }
     }
 
-    // Online softmax per query column in the scaled log2 domain.  The running
-    // offset m is only raised when a tile's maximum exceeds it by more than
+    // Online softmax per query column.  The offset m is the first tile's
+    // maximum and is only raised when a later tile exceeds it by more than
     // kLazyRescale (a factor 2^8): below that the exponentials stay in range,
-    // and the normalised result does not depend on the offset.  So the O and
-    // l rescale runs only on the few tiles where some lane's offset moves.
+    // and the normalised result does not depend on the offset.  The common
+    // case needs only each lane's own maximum and a wave vote; the exchange
+    // between the 4 lanes of a query column and the O and denominator
+    // rescale run on the few tiles where some offset moves.
     float mx[2];
 #pragma unroll
     for (int c = 0; c < 2; ++c) {
@@ -254,38 +262,36 @@ __global__ __launch_bounds__(256) void k_seg_attention(AttnArgs<T> p, GraphTable
       for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
         for (int r = 0; r < 4; ++r) m = fmaxf(m, sacc[kb][c][r]);
-      m = fmaxf(m, xor_shfl(m, 16));
-      m = fmaxf(m, xor_shfl(m, 32));
-      mx[c] = m * scale_log2;
+      mx[c] = m;                              // this lane's keys, relative to the offset
     }
-    const bool raise = (mx[0] > mrun[0] + kLazyRescale) || (mx[1] > mrun[1] + kLazyRescale);
-    if (__ballot(raise)) {
+    const bool first = t == 0;
+    if (__ballot(first || mx[0] > kLazyRescale || mx[1] > kLazyRescale)) {
 #pragma unroll
       for (int c = 0; c < 2; ++c) {
-        const float mnew = fmaxf(mrun[c], mx[c]);
-        const float alpha = fast_exp2(mrun[c] - mnew);   // 0 on the first tile (mrun = -inf)
-        mrun[c] = mnew;
-        lrun[c] *= alpha;
+        float m = fmaxf(mx[c], xor_shfl(mx[c], 16));
+        m = fmaxf(m, xor_shfl(m, 32));        // the column's maximum
+        const float delta = first ? m : fmaxf(m, 0.f);
+        const float alpha = first ? 0.f : fast_exp2(-delta);   // nothing accumulated before the first tile
+        mrun[c] += delta;
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb) sacc[kb][c] -= delta;
+        osum[c] *= alpha;
 #pragma unroll
         for (int b = 0; b < DB; ++b) oacc[b][c] *= alpha;
       }
     }
 #pragma unroll
-    for (int c = 0; c < 2; ++c) {
-      float ls = 0.f;
+    for (int c = 0; c < 2; ++c)
 #pragma unroll
       for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const float e = fast_exp2(fmaf(sacc[kb][c][r], scale_log2, -mrun[c]));
-          sacc[kb][c][r] = e;
-          ls += e;
-        }
-      lrun[c] += ls;
-    }
+        for (int r = 0; r < 4; ++r) sacc[kb][c][r] = fast_exp2(sacc[kb][c][r]);
 
     // O^T += V^T P^T
     if constexpr (sizeof(T) == 2) {
+      bf16x8 ones;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) ones[i] = (bf16)1.0f;
 #pragma unroll
       for (int c2 = 0; c2 < 2; ++c2) {
         bf16x8 pf[2];
@@ -301,6 +307,8 @@ __global__ __launch_bounds__(256) void k_seg_attention(AttnArgs<T> p, GraphTable
           oacc[b][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vfr[c2][b], pf[0], oacc[b][0], 0, 0, 0);
           oacc[b][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vfr[c2][b], pf[1], oacc[b][1], 0, 0, 0);
         }
+        osum[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pf[0], osum[0], 0, 0, 0);
+        osum[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pf[1], osum[1], 0, 0, 0);
       }
     } else {
       // 16x16x4 fp32: chunk (kb, i) puts key 16kb + 4*g4 + i in slot g4
@@ -314,6 +322,13 @@ __global__ __launch_bounds__(256) void k_seg_attention(AttnArgs<T> p, GraphTable
             oacc[b][0] = __builtin_amdgcn_mfma_f32_16x16x4f32(vf, sacc[kb][0][i], oacc[b][0], 0, 0, 0);
             oacc[b][1] = __builtin_amdgcn_mfma_f32_16x16x4f32(vf, sacc[kb][1][i], oacc[b][1], 0, 0, 0);
           }
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          osum[0] = __builtin_amdgcn_mfma_f32_16x16x4f32(1.0f, sacc[kb][0][i], osum[0], 0, 0, 0);
+          osum[1] = __builtin_amdgcn_mfma_f32_16x16x4f32(1.0f, sacc[kb][1][i], osum[1], 0, 0, 0);
+        }
     }
 
     if (t + 1 < ntiles) store_tile(cur ^ 1);
@@ -323,10 +338,7 @@ __global__ __launch_bounds__(256) void k_seg_attention(AttnArgs<T> p, GraphTable
   // ---- normalise and store ---------------------------------------------------------
 #pragma unroll
   for (int c = 0; c < 2; ++c) {
-    float l = lrun[c];
-    l += xor_shfl(l, 16);
-    l += xor_shfl(l, 32);
-    const float inv = 1.0f / l;
+    const float inv = 1.0f / osum[c][0];
     const int q = q0 + wave * 32 + c * 16 + col;
     if (q < qend) {
 #pragma unroll
@@ -343,12 +355,11 @@ template <typename T>
 hipError_t launch_attention(const AttnArgs<T>& a, const GraphTable& gt, hipStream_t s) {
   if (a.total_qblocks <= 0) return hipSuccess;
   const int dh = a.d / a.heads;
-  const float scale_log2 = 1.4426950408889634f / sqrtf((float)dh);
   dim3 grid(a.total_qblocks * a.heads), block(256);
   switch (dh) {
-    case 16: hipLaunchKernelGGL((k_seg_attention<T, 16>), grid, block, 0, s, a, gt, scale_log2); break;
-    case 32: hipLaunchKernelGGL((k_seg_attention<T, 32>), grid, block, 0, s, a, gt, scale_log2); break;
-    case 64: hipLaunchKernelGGL((k_seg_attention<T, 64>), grid, block, 0, s, a, gt, scale_log2); break;
+    case 16: hipLaunchKernelGGL((k_seg_attention<T, 16>), grid, block, 0, s, a, gt); break;
+    case 32: hipLaunchKernelGGL((k_seg_attention<T, 32>), grid, block, 0, s, a, gt); break;
+    case 64: hipLaunchKernelGGL((k_seg_attention<T, 64>), grid, block, 0, s, a, gt); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

@@ -197,12 +197,15 @@ static int place_impl(const gdp_graph* g, const T* node_emb, const float* graph_
 
   GraphTable qt = make_table(g);
   const int qblocks = prefix_blocks_attention(g->graph_ptr_h, G, p->seg_len, kAttnQ, qt.blk);
+  const float q_scale = attn_q_scale(d / p->n_heads);
   // Layer 0's projection runs on its own; every later one is fused into the
   // previous layer's post-attention kernel.
   {
     const gdp_placer_layer& L0 = p->layers[0];
-    const GemmArgs<float, T, T> a_qkv = {y, d, static_cast<const T*>(L0.w_qkv), d, nullptr, 0, nullptr, 0,
-                                         static_cast<const T*>(L0.b_qkv), qkv, 3 * d, N, 3 * d};
+    GemmArgs<float, T, T> a_qkv = {y, d, static_cast<const T*>(L0.w_qkv), d, nullptr, 0, nullptr, 0,
+                                   static_cast<const T*>(L0.b_qkv), qkv, 3 * d, N, 3 * d};
+    a_qkv.scale_cols = d;
+    a_qkv.col_scale = q_scale;
     GDP_LAUNCH(GDP_K_GEMM_QKV, (launch_gemm<float, T, T>(a_qkv, EPI_BIAS, st)));
   }
   int cur = 0;
@@ -224,7 +227,7 @@ static int place_impl(const gdp_graph* g, const T* node_emb, const float* graph_
                                     ynext, d,
                                     Ln ? static_cast<const T*>(Ln->w_qkv) : nullptr,
                                     Ln ? static_cast<const T*>(Ln->b_qkv) : nullptr,
-                                    Ln ? qkv : nullptr, 3 * d, N, d, p->d_ff};
+                                    Ln ? qkv : nullptr, 3 * d, N, d, p->d_ff, q_scale};
     GDP_LAUNCH(GDP_K_POST_ATTN, launch_post_attention<T>(a_post, gt, st));
     cur ^= 1;
     y = ynext;

@@ -212,6 +212,7 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs<TA, T, TO> p) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         v[r] = acc[i][j][r] + b[r];
+        if (EPI == EPI_BIAS && n < p.scale_cols) v[r] *= p.col_scale;
         if (EPI == EPI_RELU) v[r] = fmaxf(v[r], 0.f);
         if (EPI == EPI_SIGMOID) v[r] = sigmoidf_(v[r]);
       }

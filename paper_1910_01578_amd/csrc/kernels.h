@@ -50,6 +50,10 @@ struct GemmArgs {
   const T* bias;    // [N]
   TO* out; int ldo;
   int M, N;
+  // EPI_BIAS only: output columns [0, scale_cols) are multiplied by col_scale
+  // (the pre-scaled Q of the attention's QKV projection).
+  int scale_cols = 0;
+  float col_scale = 1.0f;
 };
 template <typename TA, typename T, typename TO>
 hipError_t launch_gemm(const GemmArgs<TA, T, TO>& a, int epi, hipStream_t s);
@@ -75,13 +79,15 @@ struct PostAttnArgs {
   const T* w_qkv; const T* b_qkv;   // [3d, d], [3d] or null
   T* qkv_out; int ldq;              // [M, ldq >= 3d]
   int M, d, d_ff;
+  float q_scale = 1.0f;             // multiplies the q columns of qkv_out
 };
 template <typename T>
 hipError_t launch_post_attention(const PostAttnArgs<T>& a, const GraphTable& gt, hipStream_t s);
 
 // ---- Section 3.2 / 3.3 --------------------------------------------------------
-// Segment attention.  qkv: [N, 3d]; out: [N, d].  gt.blk = per-graph prefix of
-// 128-query blocks.
+// Segment attention.  qkv: [N, 3d] with the q columns pre-scaled by
+// attn_q_scale(d / heads); out: [N, d].  gt.blk = per-graph prefix of 128-query
+// blocks.
 template <typename T>
 struct AttnArgs {
   const T* qkv; int ldq;
@@ -90,6 +96,8 @@ struct AttnArgs {
   int total_qblocks;
 };
 constexpr int kAttnBlockQ = 128;
+// log2(e) / sqrt(d_head): the softmax runs in the log2 domain on 2^x.
+inline float attn_q_scale(int d_head) { return 1.4426950408889634f / sqrtf((float)d_head); }
 template <typename T>
 hipError_t launch_attention(const AttnArgs<T>& a, const GraphTable& gt, hipStream_t s);
 

@@ -475,6 +475,7 @@ __global__ __launch_bounds__(LNT) void k_post_attention(PostAttnArgs<T> p, Graph
         st.store(sW1 + (cur ^ 1) * FC * G::S1);
         sb.store(sB + (cur ^ 1) * FC);
       }
+      const float scale = q * FC < D ? p.q_scale : 1.0f;   // a chunk lies wholly in q, k or v
 #pragma unroll
       for (int j = 0; j < G::JB1; ++j) {
         const int hc = ln.p1n * G::HPW + j * 16 + 4 * ln.g4;
@@ -486,7 +487,7 @@ __global__ __launch_bounds__(LNT) void k_post_attention(PostAttnArgs<T> p, Graph
           const int row = m0 + (ln.p1m * G::RB1 + i) * 16 + ln.col;
           float v[4];
 #pragma unroll
-          for (int r = 0; r < 4; ++r) v[r] = hacc[i][j][r] + b[r];
+          for (int r = 0; r < 4; ++r) v[r] = (hacc[i][j][r] + b[r]) * scale;
           if (row < p.M) store4(p.qkv_out + (size_t)row * p.ldq + q * FC + hc, v);
         }
       }
