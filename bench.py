@@ -10,6 +10,7 @@ resident in device memory before the timed region starts.
 Prints one JSON line.  `value` is nodes per second (N nodes per step).
 """
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -56,6 +57,32 @@ def flop_model(cfg, g, stats):
     }, keys
 
 
+# Kernel kind -> the source file that defines it (for the staleness check of
+# the recorded counter measurements).
+KERNEL_SOURCES = {"post_attn": "layer.hip", "seg_attention": "attention.hip", "gather_max": "graph_kernels.hip"}
+
+
+def measured_traffic(kind):
+    """HBM bytes per launch of `kind` from the committed rocprofv3 counter
+    summary (FETCH_SIZE and WRITE_SIZE, each scaled by the same counter's
+    reading for a plain copy of known size), or None when there is none or
+    the kernel's source has changed since the counters were taken."""
+    path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "profiles", "traffic.json")
+    if kind not in KERNEL_SOURCES or not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f).get(kind)
+    if not rec:
+        return None
+    src = os.path.join(os.path.dirname(os.path.abspath(__file__)), "paper_1910_01578_amd", "csrc", KERNEL_SOURCES[kind])
+    with open(src, "rb") as f:
+        if hashlib.sha256(f.read()).hexdigest() != rec["source_sha256"]:
+            return None
+    return {"bytes_per_launch": rec["bytes_per_launch"], "fetch_bytes": rec["fetch_bytes"],
+            "write_bytes": rec["write_bytes"], "algorithmic_bytes": rec.get("algorithmic_bytes"),
+            "summary": rec["summary"]}
+
+
 def cpu_baseline(cfg, g, w, n_sample, cores):
     """The fp64 oracle (untuned) on the first n_sample nodes of the same DAG."""
     from threadpoolctl import threadpool_limits
@@ -70,9 +97,10 @@ def cpu_baseline(cfg, g, w, n_sample, cores):
                          fanout=cfg.fanout, nb_seed=cfg.nb_seed, n_heads=cfg.heads, seg_len=cfg.seg_len,
                          mem_len=cfg.mem_len, k_samples=cfg.k_samples, sample_seed=cfg.sample_seed, film=cfg.film)
         dt = time.perf_counter() - t0
+    what = (f"the whole {g.n_nodes}-node DAG" if n_sample == g.n_nodes else
+            f"first {n_sample} nodes of the {g.n_nodes}-node DAG (induced sub-DAG)")
     return {"value": n_sample / dt, "unit": "nodes/s", "cores": cores, "kind": "oracle",
-            "sample": f"first {n_sample} nodes of the {g.n_nodes}-node DAG (induced sub-DAG), full embed+place+"
-                      f"sample with K={cfg.k_samples}, numpy float64, {dt:.1f} s"}
+            "sample": f"{what}, full embed+place+sample with K={cfg.k_samples}, numpy float64, {dt:.1f} s"}
 
 
 def main():
@@ -81,7 +109,10 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", default="gnmt8_52000")
-    ap.add_argument("--cpu-sample", type=int, default=12288, help="oracle sample size (0 = skip)")
+    ap.add_argument("--cpu-sample", type=int, default=-1,
+                    help="oracle sample: first N nodes (-1 = the whole workload, 0 = skip)")
+    ap.add_argument("--calib-copy-mib", type=int, default=0,
+                    help="run one plain device copy of this many MiB before the warm-up (counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1 "
@@ -99,6 +130,15 @@ def main():
     stats = W.graph_stats(g, cfg.fanout)
     runner = gdp.Runner(gdp.DeviceGraph(g, cfg.dtype), gdp.DevicePolicy(cfg, w), cfg.k_samples)
     seed = cfg.sample_seed
+
+    if args.calib_copy_mib > 0:
+        n = args.calib_copy_mib * (1 << 20) // 4
+        src = torch.ones(n, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     for _ in range(max(1, args.warmup)):
         runner.forward(seed)
@@ -143,7 +183,7 @@ def main():
         roofline = {"bound": "alu", "achieved": None, "peak": None, "unit": None, "frac": None}
     roofline["kernel"] = dominant
     roofline["avg_launch_us"] = round(1e3 * dom["ms"] / dom["launches"], 2)
-    roofline["traffic"] = None
+    roofline["traffic"] = measured_traffic(dominant)
 
     kernels = []
     for kind, v in sorted(breakdown.items(), key=lambda kv: -kv[1]["ms"]):
@@ -154,9 +194,10 @@ def main():
         kernels.append(ent)
 
     cpu = None
-    if args.cpu_sample > 0:
+    if args.cpu_sample != 0:
         cores = min(16, len(os.sched_getaffinity(0)))
-        cpu = cpu_baseline(cfg, g, w, min(args.cpu_sample, g.n_nodes), cores)
+        n = g.n_nodes if args.cpu_sample < 0 else min(args.cpu_sample, g.n_nodes)
+        cpu = cpu_baseline(cfg, g, w, n, cores)
 
     out = {
         "metric": METRIC, "value": round(value, 1), "unit": "nodes/s", "n_gpus": 1, "steps": args.steps,

@@ -64,13 +64,14 @@ struct Stage {
       r[4 * i + 3] = v.w;
     }
   }
+  __device__ __forceinline__ void store_piece(T* lds, int i) const {
+    const int q = threadIdx.x + i * LNT;
+    *reinterpret_cast<uint4*>(lds + (q / CPR) * S + (q % CPR) * EPV) =
+        make_uint4(r[4 * i], r[4 * i + 1], r[4 * i + 2], r[4 * i + 3]);
+  }
   __device__ __forceinline__ void store(T* lds) const {
 #pragma unroll
-    for (int i = 0; i < PER; ++i) {
-      const int q = threadIdx.x + i * LNT;
-      *reinterpret_cast<uint4*>(lds + (q / CPR) * S + (q % CPR) * EPV) =
-          make_uint4(r[4 * i], r[4 * i + 1], r[4 * i + 2], r[4 * i + 3]);
-    }
+    for (int i = 0; i < PER; ++i) store_piece(lds, i);
   }
 };
 
@@ -162,10 +163,12 @@ struct Lanes {
   int w2m, w2n;        // row tiling
 };
 
-// unit tiling: hacc[i][j] += W_c(rows p1n*HPW + j*16 + ..) x act(rows (p1m*RB1 + i)*16 + ..)^T
-template <typename T, int D>
+// unit tiling: hacc[i][j] = W_c(rows p1n*HPW + j*16 + ..) x act(rows (p1m*RB1 + i)*16 + ..)^T.
+// after_step(s) runs after the MFMAs of k step s have been issued: other
+// work placed there executes while they are in the matrix pipe.
+template <typename T, int D, typename Hook>
 __device__ __forceinline__ void unit_mma(typename Geo<T, D>::UnitAcc& hacc, const typename Geo<T, D>::ActFrags& af,
-                                         const T* sW, const Lanes& ln) {
+                                         const T* sW, const Lanes& ln, Hook&& after_step) {
   using G = Geo<T, D>;
   using MF = Mfma<T>;
 #pragma unroll
@@ -180,7 +183,13 @@ __device__ __forceinline__ void unit_mma(typename Geo<T, D>::UnitAcc& hacc, cons
 #pragma unroll
       for (int i = 0; i < G::RB1; ++i) hacc[i][j] = MF::mma(bw, af[i][s], hacc[i][j]);
     }
+    after_step(s);
   }
+}
+template <typename T, int D>
+__device__ __forceinline__ void unit_mma(typename Geo<T, D>::UnitAcc& hacc, const typename Geo<T, D>::ActFrags& af,
+                                         const T* sW, const Lanes& ln) {
+  unit_mma<T, D>(hacc, af, sW, ln, [](int) {});
 }
 
 // row tiling: acc += A_c W_c^T with A_c = sA rows [LBM x FC] (stride SH), W_c = sW rows [d x FC] (stride S2)
@@ -377,28 +386,39 @@ __global__ __launch_bounds__(LNT) void k_post_attention(PostAttnArgs<T> p, Graph
     st1.load(p.w1, D);
     st2.load(p.w2, p.d_ff);
     sb.load(p.b1);
+    auto load_chunk = [&](int c) {
+      st1.load(p.w1 + (size_t)c * FC * D, D);
+      st2.load(p.w2 + (size_t)c * FC, p.d_ff);
+      sb.load(p.b1 + c * FC);
+    };
     to_unit_tiling<T, D>(acc, reinterpret_cast<T*>(smem), af, ln);
     st1.store(sW1);
     st2.store(sW2);
     sb.store(sB);
+    if (NC > 1) load_chunk(1);
     __syncthreads();
+    // Chunk c + 1 sits in registers from the start of the second product of
+    // chunk c - 1 until after the first product of chunk c, so its global
+    // latency hides under both.
     for (int c = 0; c < NC; ++c) {
       const int cur = c & 1;
-      if (c + 1 < NC) {
-        st1.load(p.w1 + (size_t)(c + 1) * FC * D, D);
-        st2.load(p.w2 + (size_t)(c + 1) * FC, p.d_ff);
-        sb.load(p.b1 + (c + 1) * FC);
-      }
       typename G::UnitAcc hacc;
-      unit_mma<T, D>(hacc, af, sW1 + cur * FC * G::S1, ln);
-      // Chunk c + 1 lands in the other buffers now: they were last read in
-      // chunk c - 1, before its final barrier, and the second product needs no
-      // staging registers this way.
-      if (c + 1 < NC) {
-        st1.store(sW1 + (cur ^ 1) * FC * G::S1);
-        st2.store(sW2 + (cur ^ 1) * D * G::S2);
-        sb.store(sB + (cur ^ 1) * FC);
-      }
+      // Chunk c + 1 lands in the other buffers during the first product, one
+      // 16-byte piece per thread after each k step: those buffers were last
+      // read in chunk c - 1, before its final barrier.
+      constexpr int P1 = decltype(st1)::PER, P2 = decltype(st2)::PER;
+      const bool more = c + 1 < NC;
+      T* n1 = sW1 + (cur ^ 1) * FC * G::S1;
+      T* n2 = sW2 + (cur ^ 1) * D * G::S2;
+      unit_mma<T, D>(hacc, af, sW1 + cur * FC * G::S1, ln, [&](int s) {
+        if (!more) return;
+#pragma unroll
+        for (int k = (s * (P1 + P2)) / G::KS1; k < ((s + 1) * (P1 + P2)) / G::KS1; ++k) {
+          if (k < P1) st1.store_piece(n1, k);
+          else st2.store_piece(n2, k - P1);
+        }
+      });
+      if (more) sb.store(sB + (cur ^ 1) * FC);
       // lane holds hidden row (p1m * RB1 + i) * 16 + col, units hc + [0, 4)
 #pragma unroll
       for (int j = 0; j < G::JB1; ++j) {
@@ -415,6 +435,7 @@ __global__ __launch_bounds__(LNT) void k_post_attention(PostAttnArgs<T> p, Graph
         }
       }
       __syncthreads();                 // H and chunk c + 1 complete
+      if (c + 2 < NC) load_chunk(c + 2);
       row_mma<T, D>(acc, sH, sW2 + cur * D * G::S2, ln);
       __syncthreads();                 // H and this chunk's buffers free
     }
@@ -453,27 +474,35 @@ __global__ __launch_bounds__(LNT) void k_post_attention(PostAttnArgs<T> p, Graph
   if (!p.w_qkv) return;
 
   // ---- next layer's QKV' = Y' W_qkv^T + b_qkv, chunks of FC output units -------
+  // Two register sets alternate so that chunk q + 2 is requested while chunk q
+  // is multiplied.
   {
-    Stage<T, FC, D, G::S1> st;
-    BiasStage<T, FC> sb;
+    Stage<T, FC, D, G::S1> stA, stB;
+    BiasStage<T, FC> sbA, sbB;
     constexpr int NQ = 3 * D / FC;
-    st.load(p.w_qkv, D);
-    sb.load(p.b_qkv);
+    stA.load(p.w_qkv, D);
+    sbA.load(p.b_qkv);
+    if (NQ > 1) {
+      stB.load(p.w_qkv + (size_t)FC * D, D);
+      sbB.load(p.b_qkv + FC);
+    }
     to_unit_tiling<T, D>(acc, reinterpret_cast<T*>(smem), af, ln);
-    st.store(sW1);
-    sb.store(sB);
+    stA.store(sW1);
+    sbA.store(sB);
     __syncthreads();
-    for (int q = 0; q < NQ; ++q) {
+    // chunk q: weights in buffer q & 1; `next` holds chunk q + 1, `mine` is free
+    auto step = [&](int q, Stage<T, FC, D, G::S1>& mine, BiasStage<T, FC>& mine_b, Stage<T, FC, D, G::S1>& next,
+                    BiasStage<T, FC>& next_b) {
       const int cur = q & 1;
-      if (q + 1 < NQ) {
-        st.load(p.w_qkv + (size_t)(q + 1) * FC * D, D);
-        sb.load(p.b_qkv + (q + 1) * FC);
-      }
       typename G::UnitAcc hacc;
       unit_mma<T, D>(hacc, af, sW1 + cur * FC * G::S1, ln);
       if (q + 1 < NQ) {
-        st.store(sW1 + (cur ^ 1) * FC * G::S1);
-        sb.store(sB + (cur ^ 1) * FC);
+        next.store(sW1 + (cur ^ 1) * FC * G::S1);   // last read in chunk q - 1
+        next_b.store(sB + (cur ^ 1) * FC);
+      }
+      if (q + 2 < NQ) {
+        mine.load(p.w_qkv + (size_t)(q + 2) * FC * D, D);
+        mine_b.load(p.b_qkv + (q + 2) * FC);
       }
       const float scale = q * FC < D ? p.q_scale : 1.0f;   // a chunk lies wholly in q, k or v
 #pragma unroll
@@ -492,6 +521,10 @@ __global__ __launch_bounds__(LNT) void k_post_attention(PostAttnArgs<T> p, Graph
         }
       }
       __syncthreads();                 // this chunk's buffers free
+    };
+    for (int q = 0; q < NQ; q += 2) {
+      step(q, stA, sbA, stB, sbB);
+      if (q + 1 < NQ) step(q + 1, stB, sbB, stA, sbA);
     }
   }
 }

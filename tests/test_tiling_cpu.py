@@ -78,9 +78,12 @@ def test_xcd_remap_is_a_bijection_with_contiguous_runs(total):
 
 
 # ---- post-attention layer kernel ------------------------------------------------
-LAYER_FC = {"bf16": 64, "f32": 32}
+LAYER_FC = {"bf16": 64, "f32": 32}      # FFN, W_o and QKV chunks
+LAYER_FCQ = LAYER_FC
+LAYER_RB1 = {"bf16": 2, "f32": 1}       # unit-tiling row blocks per wave
 LAYER_ROWS = 128
 LAYER_THREADS = 512
+LAYER_WAVES = 8
 
 
 def _stage_reads(rows, cols, elem_bytes, base, ld, rows_valid=None):
@@ -88,13 +91,14 @@ def _stage_reads(rows, cols, elem_bytes, base, ld, rows_valid=None):
     epv = 16 // elem_bytes
     cpr = cols // epv
     chunks = rows * cpr
-    assert chunks % LAYER_THREADS == 0, "block must split evenly over the work-group"
+    per = -(-chunks // LAYER_THREADS)
     rv = rows if rows_valid is None else rows_valid
     out = []
-    for q in range(chunks):
-        r, c = q // cpr, (q % cpr) * epv
-        if r < rv:
-            out.append((base + r * ld + c, epv))
+    for t in range(LAYER_THREADS):
+        for i in range(per):
+            q = t + i * LAYER_THREADS
+            if q < chunks and q // cpr < rv:
+                out.append((base + (q // cpr) * ld + (q % cpr) * epv, epv))
     return out
 
 
@@ -106,19 +110,35 @@ def _check_cover(reads, size, expect):
     assert sorted(seen) == sorted(expect)
 
 
+def _lane_bias_units(dtype, fcx):
+    """Units u0 + 16 j + [0, 4) each lane reads from a chunk's biases."""
+    rb1 = LAYER_RB1[dtype]
+    p1m = LAYER_ROWS // (16 * rb1)
+    p1n = LAYER_WAVES // p1m
+    hpw = fcx // p1n
+    units = set()
+    for wave in range(LAYER_WAVES):
+        for lane in range(64):
+            u0 = (wave % p1n) * hpw + 4 * (lane >> 4)
+            for j in range(hpw // 16):
+                units.update(range(u0 + 16 * j, u0 + 16 * j + 4))
+    return units
+
+
 @pytest.mark.parametrize("name", W.CONFIG_ORDER)
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_layer_kernel_staging_stays_in_bounds(name, dtype):
     cfg = W.get_config(name).replace(dtype=dtype)
-    d, dff, eb, fc = cfg.d_model, cfg.d_ff, (2 if dtype == "bf16" else 4), LAYER_FC[dtype]
-    assert d % fc == 0 and dff % fc == 0
-    # W_1 [dff, d]: chunk c = rows [c fc, c fc + fc) x d;  W_qkv [3d, d] likewise
-    for rows_total, mat in ((dff, "w1"), (3 * d, "wqkv")):
+    d, dff, eb = cfg.d_model, cfg.d_ff, (2 if dtype == "bf16" else 4)
+    fc, fcq = LAYER_FC[dtype], LAYER_FCQ[dtype]
+    assert d % fc == 0 and dff % fc == 0 and (3 * d) % fcq == 0
+    # W_1 [dff, d] in chunks of fc rows, W_qkv [3d, d] in chunks of fcq rows
+    for rows_total, step in ((dff, fc), (3 * d, fcq)):
         reads = []
-        for c in range(rows_total // fc):
-            reads += _stage_reads(fc, d, eb, c * fc * d, d)
+        for c in range(rows_total // step):
+            reads += _stage_reads(step, d, eb, c * step * d, d)
         _check_cover(reads, rows_total * d, range(rows_total * d))
-    # W_2 [d, dff]: chunk c = all d rows x columns [c fc, c fc + fc);  W_o [d, d] likewise
+    # W_2 [d, dff] and W_o [d, d]: all d rows x columns [c fc, c fc + fc)
     for k_total in (dff, d):
         reads = []
         for c in range(k_total // fc):
@@ -131,8 +151,6 @@ def test_layer_kernel_staging_stays_in_bounds(name, dtype):
         for c in range(d // fc):
             reads += _stage_reads(LAYER_ROWS, fc, eb, m0 * d + c * fc, d, rows_valid=M - m0)
     _check_cover(reads, M * d, range(M * d))
-    # biases: the first fc / epv threads read 16 bytes each
-    epv = 16 // eb
-    for n_total in (dff, 3 * d):
-        seen = [c * fc + t * epv + e for c in range(n_total // fc) for t in range(fc // epv) for e in range(epv)]
-        assert sorted(seen) == list(range(n_total))
+    # biases: every lane's 4-unit pieces cover each chunk exactly within its range
+    assert _lane_bias_units(dtype, fc) == set(range(fc))
+    assert _lane_bias_units(dtype, fcq) == set(range(fcq))
