@@ -48,7 +48,7 @@ def flop_model(cfg, g, stats):
         "gemm_pool_sigmoid": ("mfma", float(np.mean(pool))),
         "gemm_update_relu": ("mfma", float(np.mean(upd))),
         "gather_max": ("hbm", float(gather_bytes)),
-        "gemm_qkv": ("mfma", 2.0 * N * d * 3 * d),
+        "pre_layer": ("mfma", 2.0 * N * d * 3 * d),
         "seg_attention": ("mfma", 4.0 * d * keys),
         # per launch, averaged over the placer layers: W_o, the FFN, and (all but
         # the last layer) the next layer's QKV projection

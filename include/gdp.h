@@ -248,12 +248,13 @@ typedef enum gdp_kernel_kind {
   GDP_K_GATHER_MAX,      /* Eq. 2 max over S(v)                               */
   GDP_K_GEMM_UPDATE,     /* Eq. 3 ReLU(h W_self^T + A W_neigh^T + b)          */
   GDP_K_MEANPOOL,        /* x0 = per-graph mean                              */
-  GDP_K_FILM,            /* gamma/beta GEMVs and the first layer's FiLM       */
-  GDP_K_GEMM_QKV,        /* the first layer's Y W_qkv^T + b                  */
+  GDP_K_FILM,            /* gamma/beta GEMVs of all placer layers             */
+  GDP_K_PRE_LAYER,       /* the first layer's Y = FiLM(X) and Y W_qkv^T + b   */
   GDP_K_ATTENTION,       /* segment attention                                */
   GDP_K_POST_ATTN,       /* fused rest of a layer: LN1(Y + O W_o^T + b),
-                            LN2(Z + FFN(Z)), the next layer's FiLM and QKV  */
-  GDP_K_HEAD,            /* logits and lse                                   */
+                            LN2(Z + FFN(Z)), the next layer's FiLM and QKV,
+                            and in the last layer the head (D <= 8)          */
+  GDP_K_HEAD,            /* logits and lse when not fused (D > 8)            */
   GDP_K_SAMPLE,          /* Gumbel-max sampling                              */
   GDP_K_LOGP_REDUCE,     /* per-graph log-prob sums                          */
   GDP_K_COUNT

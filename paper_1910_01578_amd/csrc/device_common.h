@@ -137,6 +137,18 @@ __device__ __forceinline__ int graph_of_node(const GraphTable& t, int v) {
 // ---------------------------------------------------------------------------
 struct U64x4 { uint64_t w[4]; };
 
+// hi:lo = a * b (64 x 64 -> 128 bits) from four 32 x 32 -> 64 partial
+// products, each carry folded into the next multiply-add, so that the low
+// and high halves share their partial products.
+__device__ __forceinline__ void mul64wide(uint64_t a, uint64_t b, uint64_t& lo, uint64_t& hi) {
+  const uint32_t a0 = (uint32_t)a, a1 = (uint32_t)(a >> 32), b0 = (uint32_t)b, b1 = (uint32_t)(b >> 32);
+  const uint64_t p00 = (uint64_t)a0 * b0;
+  const uint64_t p01 = (uint64_t)a0 * b1 + (p00 >> 32);   // < 2^64
+  const uint64_t t = (uint64_t)a1 * b0 + (uint32_t)p01;   // < 2^64
+  lo = (t << 32) | (uint32_t)p00;
+  hi = (uint64_t)a1 * b1 + ((p01 >> 32) + (t >> 32));
+}
+
 __device__ __forceinline__ U64x4 philox4x64_10(uint64_t c0, uint64_t c1, uint64_t c2, uint64_t c3,
                                                uint64_t k0, uint64_t k1) {
   const uint64_t M0 = 0xD2E7470EE14C6C93ull, M1 = 0xCA5A826395121157ull;
@@ -144,8 +156,9 @@ __device__ __forceinline__ U64x4 philox4x64_10(uint64_t c0, uint64_t c1, uint64_
 #pragma unroll
   for (int r = 0; r < 10; ++r) {
     if (r > 0) { k0 += W0; k1 += W1; }
-    const uint64_t lo0 = M0 * c0, hi0 = __umul64hi(M0, c0);
-    const uint64_t lo1 = M1 * c2, hi1 = __umul64hi(M1, c2);
+    uint64_t lo0, hi0, lo1, hi1;
+    mul64wide(M0, c0, lo0, hi0);
+    mul64wide(M1, c2, lo1, hi1);
     const uint64_t n0 = hi1 ^ c1 ^ k0, n2 = hi0 ^ c3 ^ k1;
     c0 = n0; c1 = lo1; c2 = n2; c3 = lo0;
   }

@@ -3,6 +3,7 @@
 #include <hip/hip_runtime.h>
 #include <string.h>
 
+#include <algorithm>
 #include <vector>
 
 #include "device_common.h"
@@ -184,30 +185,34 @@ static int place_impl(const gdp_graph* g, const T* node_emb, const float* graph_
 
   const float* y = ybuf[0];
   if (p->film) {
-    for (int l = 0; l < L; ++l) {
-      const gdp_placer_layer& Ly = p->layers[l];
-      GDP_LAUNCH(GDP_K_FILM, launch_film_gemv<T>(static_cast<const T*>(Ly.film_wg), static_cast<const T*>(Ly.film_bg),
-                                                 static_cast<const T*>(Ly.film_wb), static_cast<const T*>(Ly.film_bb),
-                                                 graph_emb, G, d, d, gamma_of(l), beta_of(l), st));
+    for (int l0 = 0; l0 < L; l0 += kFilmLayersPerLaunch) {
+      const int nl = std::min(kFilmLayersPerLaunch, L - l0);
+      FilmLayers<T> fw;
+      for (int i = 0; i < nl; ++i) {
+        const gdp_placer_layer& Ly = p->layers[l0 + i];
+        fw.wg[i] = static_cast<const T*>(Ly.film_wg);
+        fw.bg[i] = static_cast<const T*>(Ly.film_bg);
+        fw.wb[i] = static_cast<const T*>(Ly.film_wb);
+        fw.bb[i] = static_cast<const T*>(Ly.film_bb);
+      }
+      GDP_LAUNCH(GDP_K_FILM, launch_film_gemv<T>(fw, nl, graph_emb, G, d, d, gamma_of(l0), st));
     }
-    GDP_LAUNCH(GDP_K_FILM, launch_film_apply<T>(node_emb, gamma_of(0), beta_of(0), N, d, gt, ybuf[0], st));
-  } else {
-    GDP_LAUNCH(GDP_K_FILM, launch_film_apply<T>(node_emb, nullptr, nullptr, N, d, gt, ybuf[0], st));
   }
 
   GraphTable qt = make_table(g);
   const int qblocks = prefix_blocks_attention(g->graph_ptr_h, G, p->seg_len, kAttnQ, qt.blk);
   const float q_scale = attn_q_scale(d / p->n_heads);
-  // Layer 0's projection runs on its own; every later one is fused into the
-  // previous layer's post-attention kernel.
+  // Layer 0's FiLM and projection run in their own kernel; every later
+  // projection is fused into the previous layer's post-attention kernel.
   {
     const gdp_placer_layer& L0 = p->layers[0];
-    GemmArgs<float, T, T> a_qkv = {y, d, static_cast<const T*>(L0.w_qkv), d, nullptr, 0, nullptr, 0,
-                                   static_cast<const T*>(L0.b_qkv), qkv, 3 * d, N, 3 * d};
-    a_qkv.scale_cols = d;
-    a_qkv.col_scale = q_scale;
-    GDP_LAUNCH(GDP_K_GEMM_QKV, (launch_gemm<float, T, T>(a_qkv, EPI_BIAS, st)));
+    const PreLayerArgs<T> a_pre = {node_emb, d, p->film ? gamma_of(0) : nullptr, p->film ? beta_of(0) : nullptr, d,
+                                   ybuf[0], d, static_cast<const T*>(L0.w_qkv), static_cast<const T*>(L0.b_qkv),
+                                   qkv, 3 * d, N, d, q_scale};
+    GDP_LAUNCH(GDP_K_PRE_LAYER, launch_pre_layer<T>(a_pre, gt, st));
   }
+  // The head runs inside the last layer's kernel when D is small enough.
+  const bool fused_head = p->n_devices <= kFusedHeadDevices;
   int cur = 0;
   for (int l = 0; l < L; ++l) {
     const gdp_placer_layer& Ly = p->layers[l];
@@ -217,7 +222,7 @@ static int place_impl(const gdp_graph* g, const T* node_emb, const float* graph_
     const bool next_film = p->film && !last;
     const gdp_placer_layer* Ln = last ? nullptr : &p->layers[l + 1];
     float* ynext = ybuf[cur ^ 1];
-    const PostAttnArgs<T> a_post = {o, d, y, d,
+    PostAttnArgs<T> a_post = {o, d, y, d,
                                     static_cast<const T*>(Ly.w_o), static_cast<const T*>(Ly.b_o),
                                     static_cast<const T*>(Ly.ln1_g), static_cast<const T*>(Ly.ln1_b),
                                     static_cast<const T*>(Ly.w_1), static_cast<const T*>(Ly.b_1),
@@ -228,12 +233,21 @@ static int place_impl(const gdp_graph* g, const T* node_emb, const float* graph_
                                     Ln ? static_cast<const T*>(Ln->w_qkv) : nullptr,
                                     Ln ? static_cast<const T*>(Ln->b_qkv) : nullptr,
                                     Ln ? qkv : nullptr, 3 * d, N, d, p->d_ff, q_scale};
+    if (last && fused_head) {
+      a_post.y_out = nullptr;                // only the head reads the last layer's output
+      a_post.w_out = static_cast<const T*>(p->w_out);
+      a_post.b_out = static_cast<const T*>(p->b_out);
+      a_post.n_dev = p->n_devices;
+      a_post.logits = logits;
+      a_post.lse = lse;
+    }
     GDP_LAUNCH(GDP_K_POST_ATTN, launch_post_attention<T>(a_post, gt, st));
     cur ^= 1;
     y = ynext;
   }
-  GDP_LAUNCH(GDP_K_HEAD, launch_head<T>(y, static_cast<const T*>(p->w_out), static_cast<const T*>(p->b_out), N, d,
-                                        p->n_devices, logits, lse, st));
+  if (!fused_head)
+    GDP_LAUNCH(GDP_K_HEAD, launch_head<T>(y, static_cast<const T*>(p->w_out), static_cast<const T*>(p->b_out), N,
+                                          d, p->n_devices, logits, lse, st));
   return GDP_OK;
 }
 
@@ -381,7 +395,7 @@ extern "C" int gdp_timer_end(double* total_ms, int64_t* launches) {
 extern "C" const char* gdp_kernel_kind_name(int32_t kind) {
   static const char* names[GDP_K_COUNT] = {
       "graph_prep", "nbr_sample",    "gemm_pool_sigmoid", "gather_max", "gemm_update_relu",
-      "meanpool",   "film",          "gemm_qkv",          "seg_attention", "post_attn",
+      "meanpool",   "film",          "pre_layer",         "seg_attention", "post_attn",
       "head_lse",   "gumbel_sample", "logp_reduce"};
   if (kind < 0 || kind >= GDP_K_COUNT) return "";
   return names[kind];

@@ -80,9 +80,32 @@ struct PostAttnArgs {
   T* qkv_out; int ldq;              // [M, ldq >= 3d]
   int M, d, d_ff;
   float q_scale = 1.0f;             // multiplies the q columns of qkv_out
+  // Last layer only (then w_qkv is null and y_out may be null): the head,
+  // logits [M, n_dev] = y' W_out^T + b_out and lse [M], for n_dev <= kFusedHeadDevices.
+  const T* w_out = nullptr; const T* b_out = nullptr; int n_dev = 0;
+  float* logits = nullptr; float* lse = nullptr;
 };
+constexpr int kFusedHeadDevices = 8;
 template <typename T>
 hipError_t launch_post_attention(const PostAttnArgs<T>& a, const GraphTable& gt, hipStream_t s);
+
+// The first layer's input and projection: y = FiLM_0(x) (identity when
+// film_gamma is null) into the fp32 residual stream, qkv = y W_qkv^T + b_qkv
+// with the q columns multiplied by q_scale.
+template <typename T>
+struct PreLayerArgs {
+  const T* x; int ldx;              // node embeddings [M, d]
+  const float* film_gamma;          // [G, film_stride] or null
+  const float* film_beta;
+  int film_stride;
+  float* y_out; int ldyo;           // [M, d]
+  const T* w_qkv; const T* b_qkv;   // [3d, d], [3d]
+  T* qkv_out; int ldq;              // [M, ldq >= 3d]
+  int M, d;
+  float q_scale;
+};
+template <typename T>
+hipError_t launch_pre_layer(const PreLayerArgs<T>& a, const GraphTable& gt, hipStream_t s);
 
 // ---- Section 3.2 / 3.3 --------------------------------------------------------
 // Segment attention.  qkv: [N, 3d] with the q columns pre-scaled by
@@ -101,14 +124,19 @@ inline float attn_q_scale(int d_head) { return 1.4426950408889634f / sqrtf((floa
 template <typename T>
 hipError_t launch_attention(const AttnArgs<T>& a, const GraphTable& gt, hipStream_t s);
 
-// gamma[l][g][c] = 1 + W_g x0_g + b_g, beta[l][g][c] = W_b x0_g + b_b for one layer l.
+// gamma_l[g][c] = 1 + W_g,l x0_g + b_g,l and beta_l[g][c] = W_b,l x0_g + b_b,l for
+// up to kFilmLayersPerLaunch placer layers l per launch; layer l at out + l * 2 * G * d.
+constexpr int kFilmLayersPerLaunch = 16;
 template <typename T>
-hipError_t launch_film_gemv(const T* wg, const T* bg, const T* wb, const T* bb, const float* x0,
-                            int G, int d, int H, float* gamma, float* beta, hipStream_t s);
-// y (fp32) = gamma[g(v)] * x + beta[g(v)] for every row v; plain widening when gamma is null.
+struct FilmLayers {
+  const T* wg[kFilmLayersPerLaunch];
+  const T* bg[kFilmLayersPerLaunch];
+  const T* wb[kFilmLayersPerLaunch];
+  const T* bb[kFilmLayersPerLaunch];
+};
 template <typename T>
-hipError_t launch_film_apply(const T* x, const float* gamma, const float* beta, int n, int d,
-                             const GraphTable& gt, float* y, hipStream_t s);
+hipError_t launch_film_gemv(const FilmLayers<T>& w, int n_layers, const float* x0, int G, int d, int H,
+                            float* out, hipStream_t s);
 // logits[v] = x[v] W_out^T + b_out (fp32), lse[v] (nullable); x is the fp32 residual stream.
 template <typename T>
 hipError_t launch_head(const float* x, const T* w_out, const T* b_out, int n, int d, int D,

@@ -97,6 +97,17 @@ __device__ __forceinline__ uint32_t pack2_bf16(float lo, float hi) {
   return __builtin_bit_cast(uint32_t, v);
 }
 
+// 4 consecutive elements of T read as one vector and widened.
+__device__ __forceinline__ void load4f(const float* p, float (&v)[4]) {
+  const float4 x = *reinterpret_cast<const float4*>(p);
+  v[0] = x.x; v[1] = x.y; v[2] = x.z; v[3] = x.w;
+}
+__device__ __forceinline__ void load4f(const bf16* p, float (&v)[4]) {
+  const uint2 x = *reinterpret_cast<const uint2*>(p);
+  v[0] = __uint_as_float(x.x << 16); v[1] = __uint_as_float(x.x & 0xffff0000u);
+  v[2] = __uint_as_float(x.y << 16); v[3] = __uint_as_float(x.y & 0xffff0000u);
+}
+
 // 4 consecutive values as one store (8 bytes in bf16, 16 in fp32).
 __device__ __forceinline__ void store4(float* p, const float (&v)[4]) {
   *reinterpret_cast<float4*>(p) = make_float4(v[0], v[1], v[2], v[3]);
@@ -304,9 +315,143 @@ __device__ __forceinline__ void to_unit_tiling(const typename Geo<T, D>::RowAcc&
   __syncthreads();
 }
 
+// QKV = act W_qkv^T + b_qkv for the work-group's rows, chunks of FC output
+// units, with the activation in the row tiling in acc (it passes to the unit
+// tiling through LDS; every LDS region must be free on entry).  The q columns
+// are multiplied by q_scale.  Two register sets alternate so that chunk q + 2
+// is requested while chunk q is multiplied.
+template <typename T, int D>
+__device__ __forceinline__ void qkv_phase(const typename Geo<T, D>::RowAcc& acc, char* smem,
+                                          typename Geo<T, D>::ActFrags& af, const Lanes& ln, int m0, int M,
+                                          const T* w_qkv, const T* b_qkv, T* qkv_out, int ldq, float q_scale) {
+  using G = Geo<T, D>;
+  constexpr int FC = G::FC;
+  T* sW1 = reinterpret_cast<T*>(smem + G::OFF_W1);
+  T* sB = reinterpret_cast<T*>(smem + G::OFF_B1);
+  {
+    Stage<T, FC, D, G::S1> stA, stB;
+    BiasStage<T, FC> sbA, sbB;
+    constexpr int NQ = 3 * D / FC;
+    stA.load(w_qkv, D);
+    sbA.load(b_qkv);
+    if (NQ > 1) {
+      stB.load(w_qkv + (size_t)FC * D, D);
+      sbB.load(b_qkv + FC);
+    }
+    to_unit_tiling<T, D>(acc, reinterpret_cast<T*>(smem), af, ln);
+    stA.store(sW1);
+    sbA.store(sB);
+    __syncthreads();
+    // chunk q: weights in buffer q & 1; `next` holds chunk q + 1, `mine` is free
+    auto step = [&](int q, Stage<T, FC, D, G::S1>& mine, BiasStage<T, FC>& mine_b, Stage<T, FC, D, G::S1>& next,
+                    BiasStage<T, FC>& next_b) {
+      const int cur = q & 1;
+      typename G::UnitAcc hacc;
+      unit_mma<T, D>(hacc, af, sW1 + cur * FC * G::S1, ln);
+      if (q + 1 < NQ) {
+        next.store(sW1 + (cur ^ 1) * FC * G::S1);   // last read in chunk q - 1
+        next_b.store(sB + (cur ^ 1) * FC);
+      }
+      if (q + 2 < NQ) {
+        mine.load(w_qkv + (size_t)(q + 2) * FC * D, D);
+        mine_b.load(b_qkv + (q + 2) * FC);
+      }
+      const float scale = q * FC < D ? q_scale : 1.0f;   // a chunk lies wholly in q, k or v
+#pragma unroll
+      for (int j = 0; j < G::JB1; ++j) {
+        const int hc = ln.p1n * G::HPW + j * 16 + 4 * ln.g4;
+        float b[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) b[r] = to_f32(sB[cur * FC + hc + r]);
+#pragma unroll
+        for (int i = 0; i < G::RB1; ++i) {
+          const int row = m0 + (ln.p1m * G::RB1 + i) * 16 + ln.col;
+          float v[4];
+#pragma unroll
+          for (int r = 0; r < 4; ++r) v[r] = (hacc[i][j][r] + b[r]) * scale;
+          if (row < M) store4(qkv_out + (size_t)row * ldq + q * FC + hc, v);
+        }
+      }
+      __syncthreads();                 // this chunk's buffers free
+    };
+    for (int q = 0; q < NQ; q += 2) {
+      step(q, stA, sbA, stB, sbB);
+      if (q + 1 < NQ) step(q + 1, stB, sbB, stA, sbA);
+    }
+  }
+}
+
+
+// The placement head on the rows held in the row tiling (Fig. 1's N x d
+// output): logits[row][e] = act[row] . W_out[e] + b_out[e] for e < n_dev <=
+// kFusedHeadDevices, and their logsumexp.  W_out goes to LDS as fp32; each
+// lane forms the partial sums of its rows over its columns, the 4 lane groups
+// of a row combine by butterfly and the WN2 column waves through LDS.  Every
+// LDS region must be free on entry.
+template <typename T, int D>
+__device__ __forceinline__ void head_epilogue(const typename Geo<T, D>::RowAcc& acc, char* smem, const Lanes& ln,
+                                              int m0, int M, const T* w_out, const T* b_out, int n_dev,
+                                              float* logits, float* lse) {
+  using G = Geo<T, D>;
+  constexpr int E = kFusedHeadDevices;
+  float* sW = reinterpret_cast<float*>(smem);                                  // [E][D]
+  float (*hred)[G::WN2][E] = reinterpret_cast<float (*)[G::WN2][E]>(smem + E * D * sizeof(float));
+  const int rbase = ln.w2m * G::MB2 * 16 + ln.col;
+  const int cbase = ln.w2n * G::NB2 * 16 + 4 * ln.g4;
+  for (int i = threadIdx.x; i < E * D; i += LNT) sW[i] = i < n_dev * D ? to_f32(w_out[i]) : 0.f;
+  __syncthreads();
+  float part[G::MB2][E];
+#pragma unroll
+  for (int i = 0; i < G::MB2; ++i)
+#pragma unroll
+    for (int e = 0; e < E; ++e) part[i][e] = 0.f;
+#pragma unroll
+  for (int j = 0; j < G::NB2; ++j)
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+      const float4 w = *reinterpret_cast<const float4*>(&sW[e * D + cbase + j * 16]);
+#pragma unroll
+      for (int i = 0; i < G::MB2; ++i)
+        part[i][e] += acc[i][j][0] * w.x + acc[i][j][1] * w.y + acc[i][j][2] * w.z + acc[i][j][3] * w.w;
+    }
+#pragma unroll
+  for (int i = 0; i < G::MB2; ++i)
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+      float v = part[i][e];
+      v += xor_shfl(v, 16);
+      v += xor_shfl(v, 32);
+      if (ln.g4 == 0) hred[rbase + i * 16][ln.w2n][e] = v;
+    }
+  __syncthreads();
+  if (threadIdx.x < LBM) {
+    const int row = m0 + threadIdx.x;
+    if (row < M) {
+      float l[E], mx = -INFINITY;
+#pragma unroll
+      for (int e = 0; e < E; ++e) {
+        float v = 0.f;
+#pragma unroll
+        for (int q = 0; q < G::WN2; ++q) v += hred[threadIdx.x][q][e];
+        l[e] = e < n_dev ? v + to_f32(b_out[e < n_dev ? e : 0]) : -INFINITY;
+        mx = fmaxf(mx, l[e]);
+      }
+      float sum = 0.f;
+#pragma unroll
+      for (int e = 0; e < E; ++e)
+        if (e < n_dev) {
+          sum += expf(l[e] - mx);
+          logits[(size_t)row * n_dev + e] = l[e];
+        }
+      lse[row] = mx + logf(sum);
+    }
+  }
+}
+
 }  // namespace
 
-template <typename T, int D>
+// HEAD: the last layer's variant, with the placement head instead of a QKV projection.
+template <typename T, int D, bool HEAD>
 __global__ __launch_bounds__(LNT) void k_post_attention(PostAttnArgs<T> p, GraphTable gt) {
   using G = Geo<T, D>;
   using MF = Mfma<T>;
@@ -464,68 +609,18 @@ __global__ __launch_bounds__(LNT) void k_post_attention(PostAttnArgs<T> p, Graph
           acc[i][j][r] = p.film_gamma[g + cn] * acc[i][j][r] + p.film_beta[g + cn];
         }
     }
-    if (row < p.M) {
+    if (p.y_out && row < p.M) {
 #pragma unroll
       for (int j = 0; j < G::NB2; ++j)
         *reinterpret_cast<float4*>(p.y_out + (size_t)row * p.ldyo + cbase + j * 16) =
             make_float4(acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
     }
   }
-  if (!p.w_qkv) return;
-
-  // ---- next layer's QKV' = Y' W_qkv^T + b_qkv, chunks of FC output units -------
-  // Two register sets alternate so that chunk q + 2 is requested while chunk q
-  // is multiplied.
-  {
-    Stage<T, FC, D, G::S1> stA, stB;
-    BiasStage<T, FC> sbA, sbB;
-    constexpr int NQ = 3 * D / FC;
-    stA.load(p.w_qkv, D);
-    sbA.load(p.b_qkv);
-    if (NQ > 1) {
-      stB.load(p.w_qkv + (size_t)FC * D, D);
-      sbB.load(p.b_qkv + FC);
-    }
-    to_unit_tiling<T, D>(acc, reinterpret_cast<T*>(smem), af, ln);
-    stA.store(sW1);
-    sbA.store(sB);
-    __syncthreads();
-    // chunk q: weights in buffer q & 1; `next` holds chunk q + 1, `mine` is free
-    auto step = [&](int q, Stage<T, FC, D, G::S1>& mine, BiasStage<T, FC>& mine_b, Stage<T, FC, D, G::S1>& next,
-                    BiasStage<T, FC>& next_b) {
-      const int cur = q & 1;
-      typename G::UnitAcc hacc;
-      unit_mma<T, D>(hacc, af, sW1 + cur * FC * G::S1, ln);
-      if (q + 1 < NQ) {
-        next.store(sW1 + (cur ^ 1) * FC * G::S1);   // last read in chunk q - 1
-        next_b.store(sB + (cur ^ 1) * FC);
-      }
-      if (q + 2 < NQ) {
-        mine.load(p.w_qkv + (size_t)(q + 2) * FC * D, D);
-        mine_b.load(p.b_qkv + (q + 2) * FC);
-      }
-      const float scale = q * FC < D ? p.q_scale : 1.0f;   // a chunk lies wholly in q, k or v
-#pragma unroll
-      for (int j = 0; j < G::JB1; ++j) {
-        const int hc = ln.p1n * G::HPW + j * 16 + 4 * ln.g4;
-        float b[4];
-#pragma unroll
-        for (int r = 0; r < 4; ++r) b[r] = to_f32(sB[cur * FC + hc + r]);
-#pragma unroll
-        for (int i = 0; i < G::RB1; ++i) {
-          const int row = m0 + (ln.p1m * G::RB1 + i) * 16 + ln.col;
-          float v[4];
-#pragma unroll
-          for (int r = 0; r < 4; ++r) v[r] = (hacc[i][j][r] + b[r]) * scale;
-          if (row < p.M) store4(p.qkv_out + (size_t)row * p.ldq + q * FC + hc, v);
-        }
-      }
-      __syncthreads();                 // this chunk's buffers free
-    };
-    for (int q = 0; q < NQ; q += 2) {
-      step(q, stA, sbA, stB, sbB);
-      if (q + 1 < NQ) step(q + 1, stB, sbB, stA, sbA);
-    }
+  if constexpr (HEAD) {
+    head_epilogue<T, D>(acc, smem, ln, m0, p.M, p.w_out, p.b_out, p.n_dev, p.logits, p.lse);
+  } else {
+    if (!p.w_qkv) return;
+    qkv_phase<T, D>(acc, smem, af, ln, m0, p.M, p.w_qkv, p.b_qkv, p.qkv_out, p.ldq, p.q_scale);
   }
 }
 
@@ -534,16 +629,93 @@ hipError_t launch_post_attention(const PostAttnArgs<T>& a, const GraphTable& gt,
   if (a.M <= 0) return hipSuccess;
   if (a.d_ff <= 0 || a.d_ff % LayerCfg<T>::FC) return hipErrorInvalidValue;
   if (a.w_qkv && (!a.b_qkv || !a.qkv_out || a.ldq < 3 * a.d)) return hipErrorInvalidValue;
+  if (a.w_out && (!a.b_out || !a.logits || !a.lse || a.n_dev < 1 || a.n_dev > kFusedHeadDevices || a.w_qkv))
+    return hipErrorInvalidValue;
   dim3 grid((a.M + LBM - 1) / LBM), block(LNT);
+  const bool head = a.w_out != nullptr;
   switch (a.d) {
-    case 64: hipLaunchKernelGGL((k_post_attention<T, 64>), grid, block, 0, s, a, gt); break;
-    case 128: hipLaunchKernelGGL((k_post_attention<T, 128>), grid, block, 0, s, a, gt); break;
-    case 256: hipLaunchKernelGGL((k_post_attention<T, 256>), grid, block, 0, s, a, gt); break;
+    case 64:
+      if (head) hipLaunchKernelGGL((k_post_attention<T, 64, true>), grid, block, 0, s, a, gt);
+      else hipLaunchKernelGGL((k_post_attention<T, 64, false>), grid, block, 0, s, a, gt);
+      break;
+    case 128:
+      if (head) hipLaunchKernelGGL((k_post_attention<T, 128, true>), grid, block, 0, s, a, gt);
+      else hipLaunchKernelGGL((k_post_attention<T, 128, false>), grid, block, 0, s, a, gt);
+      break;
+    case 256:
+      if (head) hipLaunchKernelGGL((k_post_attention<T, 256, true>), grid, block, 0, s, a, gt);
+      else hipLaunchKernelGGL((k_post_attention<T, 256, false>), grid, block, 0, s, a, gt);
+      break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
 }
 template hipError_t launch_post_attention<float>(const PostAttnArgs<float>&, const GraphTable&, hipStream_t);
 template hipError_t launch_post_attention<bf16>(const PostAttnArgs<bf16>&, const GraphTable&, hipStream_t);
+
+
+// The first placer layer's input and projection (Eq. 4, Section 3.2):
+//   Y = FiLM_0(X) (X = the node embeddings; identity without conditioning) into
+//   the fp32 residual stream, and QKV = Y W_qkv^T + b_qkv,
+// with the same tiles as the post-attention kernel's QKV phase.
+template <typename T, int D>
+__global__ __launch_bounds__(LNT) void k_pre_layer(PreLayerArgs<T> p, GraphTable gt) {
+  using G = Geo<T, D>;
+  __shared__ __attribute__((aligned(16))) char smem[G::TOTAL];
+  Lanes ln;
+  ln.lane = threadIdx.x & 63;
+  ln.wave = threadIdx.x >> 6;
+  ln.col = ln.lane & 15;
+  ln.g4 = ln.lane >> 4;
+  ln.p1m = ln.wave / G::P1N;
+  ln.p1n = ln.wave % G::P1N;
+  ln.w2m = ln.wave / G::WN2;
+  ln.w2n = ln.wave % G::WN2;
+  const int m0 = blockIdx.x * LBM;
+  const int rbase = ln.w2m * G::MB2 * 16 + ln.col;
+  const int cbase = ln.w2n * G::NB2 * 16 + 4 * ln.g4;
+  typename G::RowAcc acc;
+#pragma unroll
+  for (int i = 0; i < G::MB2; ++i) {
+    const int row = m0 + rbase + i * 16;
+    const int rr = row < p.M ? row : p.M - 1;
+    const float* fg = nullptr;
+    const float* fb = nullptr;
+    if (p.film_gamma) {
+      const size_t g = (size_t)graph_of_node(gt, rr) * p.film_stride;
+      fg = p.film_gamma + g;
+      fb = p.film_beta + g;
+    }
+#pragma unroll
+    for (int j = 0; j < G::NB2; ++j) {
+      const int cn = cbase + j * 16;
+      float x[4];
+      load4f(p.x + (size_t)rr * p.ldx + cn, x);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) acc[i][j][r] = fg ? fg[cn + r] * x[r] + fb[cn + r] : x[r];
+      if (row < p.M)
+        *reinterpret_cast<float4*>(p.y_out + (size_t)row * p.ldyo + cn) =
+            make_float4(acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
+    }
+  }
+  typename G::ActFrags af;
+  qkv_phase<T, D>(acc, smem, af, ln, m0, p.M, p.w_qkv, p.b_qkv, p.qkv_out, p.ldq, p.q_scale);
+}
+
+template <typename T>
+hipError_t launch_pre_layer(const PreLayerArgs<T>& a, const GraphTable& gt, hipStream_t s) {
+  if (a.M <= 0) return hipSuccess;
+  if (!a.x || !a.y_out || !a.w_qkv || !a.b_qkv || !a.qkv_out || a.ldq < 3 * a.d) return hipErrorInvalidValue;
+  dim3 grid((a.M + LBM - 1) / LBM), block(LNT);
+  switch (a.d) {
+    case 64: hipLaunchKernelGGL((k_pre_layer<T, 64>), grid, block, 0, s, a, gt); break;
+    case 128: hipLaunchKernelGGL((k_pre_layer<T, 128>), grid, block, 0, s, a, gt); break;
+    case 256: hipLaunchKernelGGL((k_pre_layer<T, 256>), grid, block, 0, s, a, gt); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+template hipError_t launch_pre_layer<float>(const PreLayerArgs<float>&, const GraphTable&, hipStream_t);
+template hipError_t launch_pre_layer<bf16>(const PreLayerArgs<bf16>&, const GraphTable&, hipStream_t);
 
 }  // namespace gdp

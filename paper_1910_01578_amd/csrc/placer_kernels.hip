@@ -4,81 +4,45 @@
 
 namespace gdp {
 
-// gamma[g][c] = 1 + W_g[c] . x0_g + b_g[c];  beta[g][c] = W_b[c] . x0_g + b_b[c].
-// One wavefront per output element, lanes over the H inputs.
+// For every placer layer l of a group:
+//   gamma_l[g][c] = 1 + W_g,l[c] . x0_g + b_g,l[c];  beta_l[g][c] = W_b,l[c] . x0_g + b_b,l[c].
+// One launch covers up to kFilmLayersPerLaunch layers; one wavefront per output
+// element, lanes over the H inputs.  Output of layer l at out + l * 2 * G * d
+// (gamma, then beta).
 template <typename T>
-__global__ __launch_bounds__(256) void k_film_gemv(const T* __restrict__ wg, const T* __restrict__ bg,
-                                                   const T* __restrict__ wb, const T* __restrict__ bb,
-                                                   const float* __restrict__ x0, int G, int d, int H,
-                                                   float* __restrict__ gamma, float* __restrict__ beta) {
+__global__ __launch_bounds__(256) void k_film_gemv(FilmLayers<T> w, int n_layers, const float* __restrict__ x0,
+                                                   int G, int d, int H, float* __restrict__ out) {
   const int lane = threadIdx.x & 63;
-  const int idx = blockIdx.x * 4 + (threadIdx.x >> 6);   // over G * 2 * d
-  if (idx >= G * 2 * d) return;
-  const int g = idx / (2 * d);
-  const int which = (idx / d) & 1;
-  const int c = idx % d;
-  const T* w = (which ? wb : wg) + (size_t)c * H;
+  const int idx = blockIdx.x * 4 + (threadIdx.x >> 6);   // over n_layers * G * 2 * d
+  if (idx >= n_layers * G * 2 * d) return;
+  const int l = idx / (G * 2 * d);
+  const int rem = idx % (G * 2 * d);
+  const int g = rem / (2 * d);
+  const int which = (rem / d) & 1;
+  const int c = rem % d;
+  const T* wr = (which ? w.wb[l] : w.wg[l]) + (size_t)c * H;
   float acc = 0.f;
-  for (int k = lane; k < H; k += 64) acc += to_f32(w[k]) * x0[(size_t)g * H + k];
+  for (int k = lane; k < H; k += 64) acc += to_f32(wr[k]) * x0[(size_t)g * H + k];
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) acc += xor_shfl(acc, off);
   if (lane == 0) {
-    if (which) beta[(size_t)g * d + c] = acc + to_f32(bb[c]);
-    else gamma[(size_t)g * d + c] = 1.0f + acc + to_f32(bg[c]);
+    float* o = out + (size_t)l * 2 * G * d + (size_t)which * G * d + (size_t)g * d + c;
+    *o = which ? acc + to_f32(w.bb[l][c]) : 1.0f + acc + to_f32(w.bg[l][c]);
   }
 }
 
 template <typename T>
-hipError_t launch_film_gemv(const T* wg, const T* bg, const T* wb, const T* bb, const float* x0, int G,
-                            int d, int H, float* gamma, float* beta, hipStream_t s) {
-  const int n = G * 2 * d;
-  hipLaunchKernelGGL((k_film_gemv<T>), dim3((n + 3) / 4), dim3(256), 0, s, wg, bg, wb, bb, x0, G, d, H,
-                     gamma, beta);
+hipError_t launch_film_gemv(const FilmLayers<T>& w, int n_layers, const float* x0, int G, int d, int H,
+                            float* out, hipStream_t s) {
+  if (n_layers < 1 || n_layers > kFilmLayersPerLaunch) return hipErrorInvalidValue;
+  const int n = n_layers * G * 2 * d;
+  hipLaunchKernelGGL((k_film_gemv<T>), dim3((n + 3) / 4), dim3(256), 0, s, w, n_layers, x0, G, d, H, out);
   return hipGetLastError();
 }
-template hipError_t launch_film_gemv<float>(const float*, const float*, const float*, const float*,
-                                            const float*, int, int, int, float*, float*, hipStream_t);
-template hipError_t launch_film_gemv<bf16>(const bf16*, const bf16*, const bf16*, const bf16*,
-                                           const float*, int, int, int, float*, float*, hipStream_t);
-
-// y[v] = gamma[g(v)] * x[v] + beta[g(v)] into the fp32 residual stream; with
-// gamma == null the rows are only widened.  Each thread handles 4 columns.
-template <typename T>
-__global__ __launch_bounds__(256) void k_film_apply(const T* __restrict__ x, const float* __restrict__ gamma,
-                                                    const float* __restrict__ beta, int n, int d,
-                                                    GraphTable gt, float* __restrict__ y) {
-  const int per_row = d / 4;
-  const int64_t total = (int64_t)n * per_row;
-  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < total;
-       i += (int64_t)gridDim.x * blockDim.x) {
-    const int v = (int)(i / per_row);
-    const int c = (int)(i % per_row) * 4;
-    float4 o;
-    float* of = reinterpret_cast<float*>(&o);
-#pragma unroll
-    for (int e = 0; e < 4; ++e) of[e] = to_f32(x[(size_t)v * d + c + e]);
-    if (gamma) {
-      const int g = graph_of_node(gt, v);
-#pragma unroll
-      for (int e = 0; e < 4; ++e) of[e] = gamma[(size_t)g * d + c + e] * of[e] + beta[(size_t)g * d + c + e];
-    }
-    *reinterpret_cast<float4*>(y + (size_t)v * d + c) = o;
-  }
-}
-
-template <typename T>
-hipError_t launch_film_apply(const T* x, const float* gamma, const float* beta, int n, int d,
-                             const GraphTable& gt, float* y, hipStream_t s) {
-  const int64_t total = (int64_t)n * (d / 4);
-  int64_t blocks = (total + 255) / 256;
-  if (blocks > 8192) blocks = 8192;
-  hipLaunchKernelGGL((k_film_apply<T>), dim3((unsigned)blocks), dim3(256), 0, s, x, gamma, beta, n, d, gt, y);
-  return hipGetLastError();
-}
-template hipError_t launch_film_apply<float>(const float*, const float*, const float*, int, int,
-                                             const GraphTable&, float*, hipStream_t);
-template hipError_t launch_film_apply<bf16>(const bf16*, const float*, const float*, int, int,
-                                            const GraphTable&, float*, hipStream_t);
+template hipError_t launch_film_gemv<float>(const FilmLayers<float>&, int, const float*, int, int, int, float*,
+                                            hipStream_t);
+template hipError_t launch_film_gemv<bf16>(const FilmLayers<bf16>&, int, const float*, int, int, int, float*,
+                                           hipStream_t);
 
 // logits[v][j] = x[v] . W_out[j] + b_out[j] in fp32, lse[v] = log sum_j exp(logits[v][j]).
 // DL lanes (the power of two >= D) serve one node, lane j computing logit j

@@ -4,8 +4,8 @@
 // and key (seed, 0) (one call yields 8 devices), Gumbel noise -ln(-ln u),
 // argmax of logits + noise (first maximum wins), and the chosen device's
 // log-softmax term.  The log-prob terms are summed per work-group in a fixed
-// tree order; a second kernel adds the work-group partials of each graph in
-// chunk order, so results are bit-reproducible.
+// order; a second kernel adds the work-group partials of each graph in chunk
+// order, so results are bit-reproducible.
 #include "device_common.h"
 #include "kernels.h"
 
@@ -17,13 +17,24 @@ __device__ __forceinline__ float uniform_at(const U64x4& r, int j) {
   return half_to_uniform(h);
 }
 
+// 2^x and log2 on the transcendental unit.
+__device__ __forceinline__ float fast_log2(float x) { return __builtin_amdgcn_logf(x); }
+
+// The Gumbel-max decision argmax_j (l_j - ln(-ln u_j)) in base 2: dividing
+// every score by ln 2 and dropping the common constant log2(ln 2) leaves
+// argmax_j (l_j / ln 2 - log2(-log2 u_j)).  -log2 u lies in [2^-23.5, 24]
+// for the uniforms used here, so both logarithms see normal inputs.
+__device__ __forceinline__ float gumbel_score(float logit, float u) {
+  return fmaf(logit, 1.4426950408889634f, -fast_log2(-fast_log2(u)));
+}
+
 __global__ __launch_bounds__(kSampleChunk) void k_sample(const float* __restrict__ logits,
                                                          const float* __restrict__ lse, int n, int D,
                                                          uint64_t seed, const float* __restrict__ uniforms,
                                                          GraphTable ct, int total_chunks,
                                                          int* __restrict__ placements,
                                                          float* __restrict__ partial) {
-  __shared__ float red[kSampleChunk];
+  __shared__ float red[kSampleChunk / kWave];
   const int c = blockIdx.x, k = blockIdx.y;
   const int g = graph_of_block(ct, c);
   const int v = ct.ptr[g] + (c - ct.blk[g]) * kSampleChunk + threadIdx.x;
@@ -42,29 +53,35 @@ __global__ __launch_bounds__(kSampleChunk) void k_sample(const float* __restrict
     }
     float best = -INFINITY;
     int arg = 0;
-    float best_logit = row[0];
+    // one Philox call covers 8 devices; the 8 are unrolled so that every
+    // uniform is taken from a fixed word of the result
     for (int jb = 0; jb < D; jb += 8) {
       U64x4 r;
       if (!uniforms) r = philox4x64_10((uint64_t)v, (uint64_t)k, 2ull, (uint64_t)(jb >> 3), seed, 0ull);
-      const int jend = min(jb + 8, D);
-      for (int j = jb; j < jend; ++j) {
-        const float u = uniforms ? uniforms[((size_t)k * n + v) * D + j] : uniform_at(r, j);
-        const float lg = row[j];
-        const float sc = lg - logf(-logf(u));
-        if (sc > best) { best = sc; arg = j; best_logit = lg; }
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int j = jb + e;
+        if (j < D) {
+          const float u = uniforms ? uniforms[((size_t)k * n + v) * D + j] : uniform_at(r, e);
+          const float sc = gumbel_score(row[j], u);
+          if (sc > best) { best = sc; arg = j; }   // first maximum wins
+        }
       }
     }
     placements[(size_t)k * n + v] = arg;
-    term = best_logit - lz;
+    term = row[arg] - lz;
   }
-  red[threadIdx.x] = term;
-  __syncthreads();
+  // work-group sum in a fixed order: each wave's butterfly, then the waves in index order
 #pragma unroll
-  for (int w = kSampleChunk / 2; w >= 1; w >>= 1) {
-    if (threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
-    __syncthreads();
+  for (int off = kWave / 2; off >= 1; off >>= 1) term += xor_shfl(term, off);
+  if ((threadIdx.x & (kWave - 1)) == 0) red[threadIdx.x / kWave] = term;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    float sum = 0.f;
+#pragma unroll
+    for (int w = 0; w < kSampleChunk / kWave; ++w) sum += red[w];
+    partial[(size_t)k * total_chunks + c] = sum;
   }
-  if (threadIdx.x == 0) partial[(size_t)k * total_chunks + c] = red[0];
 }
 
 hipError_t launch_sample(const float* logits, const float* lse, int n, int D, int K, uint64_t seed,

@@ -29,7 +29,7 @@ GDP_TOPO_IDS = 1
 GDP_MAX_GRAPHS = 128
 
 KERNEL_KINDS = ["graph_prep", "nbr_sample", "gemm_pool_sigmoid", "gather_max", "gemm_update_relu",
-                "meanpool", "film", "gemm_qkv", "seg_attention", "post_attn",
+                "meanpool", "film", "pre_layer", "seg_attention", "post_attn",
                 "head_lse", "gumbel_sample", "logp_reduce"]
 K_COUNT = len(KERNEL_KINDS)
 
