@@ -123,7 +123,8 @@ static int prep_neighbors(const gdp_graph* g, const gdp_gnn* gnn, const EmbedPla
   GDP_LAUNCH(GDP_K_GRAPH_PREP, launch_in_degree(g->col_idx, g->n_edges, in_deg, st));
   GDP_LAUNCH(GDP_K_GRAPH_PREP, launch_scan_degrees(g->row_ptr, in_deg, N, gnn->fanout, in_ptr, s_ptr,
                                                    at<int>(ws, pl.scan_tmp), st));
-  GDP_LAUNCH(GDP_K_GRAPH_PREP, launch_fill_reverse(g->row_ptr, g->col_idx, in_ptr, N, cursor, in_idx, st));
+  GDP_LAUNCH(GDP_K_GRAPH_PREP, launch_fill_reverse(g->row_ptr, g->col_idx, in_ptr, N, g->n_edges, cursor, in_idx,
+                                                   st));
   GDP_LAUNCH(GDP_K_NBR_SAMPLE, launch_nbr_sample(g->row_ptr, g->col_idx, in_ptr, in_idx, s_ptr, N, gnn->fanout,
                                                  gnn->nbr_seed, gt, s_idx, at<int>(ws, pl.heavy), heavy_count, st));
   return GDP_OK;

@@ -160,22 +160,31 @@ hipError_t launch_scan_degrees(const int* row_ptr, const int* in_deg, int n, int
 // ---------------------------------------------------------------------------
 // Reverse edges: in_idx[in_ptr[v] + slot] = u for every u -> v.  Slot order is
 // whatever the atomics give; every consumer is order-invariant.
+// One thread per edge e = (u -> v): u is the row whose [row_ptr[u], row_ptr[u+1])
+// holds e (binary search), so high out-degree nodes spread over many threads.
 __global__ void k_fill_reverse(const int* __restrict__ row_ptr, const int* __restrict__ col_idx,
-                               const int* __restrict__ in_ptr, int n, int* cursor,
+                               const int* __restrict__ in_ptr, int n, int64_t n_edges, int* cursor,
                                int* __restrict__ in_idx) {
-  const int u = blockIdx.x * blockDim.x + threadIdx.x;
-  if (u >= n) return;
-  for (int e = row_ptr[u]; e < row_ptr[u + 1]; ++e) {
+  for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < n_edges;
+       e += (int64_t)gridDim.x * blockDim.x) {
+    int lo = 0, hi = n - 1;                  // largest u with row_ptr[u] <= e
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (row_ptr[mid] <= e) lo = mid; else hi = mid - 1;
+    }
     const int v = col_idx[e];
     const int slot = atomicAdd(&cursor[v], 1);
-    in_idx[in_ptr[v] + slot] = u;
+    in_idx[in_ptr[v] + slot] = lo;
   }
 }
 
 hipError_t launch_fill_reverse(const int* row_ptr, const int* col_idx, const int* in_ptr, int n,
-                               int* cursor, int* in_idx, hipStream_t s) {
-  hipLaunchKernelGGL(k_fill_reverse, dim3((n + 255) / 256), dim3(256), 0, s, row_ptr, col_idx,
-                     in_ptr, n, cursor, in_idx);
+                               int64_t n_edges, int* cursor, int* in_idx, hipStream_t s) {
+  if (n_edges <= 0) return hipSuccess;
+  int64_t blocks = (n_edges + 255) / 256;
+  if (blocks > 8192) blocks = 8192;
+  hipLaunchKernelGGL(k_fill_reverse, dim3((unsigned)blocks), dim3(256), 0, s, row_ptr, col_idx, in_ptr, n,
+                     n_edges, cursor, in_idx);
   return hipGetLastError();
 }
 
@@ -263,6 +272,8 @@ __global__ __launch_bounds__(256) void k_nbr_heavy(const int* __restrict__ row_p
       if (lane == 0) select_serial<GDP_MAX_FANOUT>(col_idx, in_idx, o0, n_out, i0, deg, v - g0, g0, fanout, seed, out);
       continue;
     }
+    // R = key registers in use (wave-uniform): every loop below skips the rest.
+    const int R = (deg + 63) >> 6;
     uint64_t key[kHeavyPerLane];
     int id[kHeavyPerLane];
 #pragma unroll
@@ -270,7 +281,7 @@ __global__ __launch_bounds__(256) void k_nbr_heavy(const int* __restrict__ row_p
       const int e = lane + 64 * r;
       key[r] = ~0ull;
       id[r] = 0x7fffffff;
-      if (e < deg) {
+      if (r < R && e < deg) {
         id[r] = nbr_at(col_idx, in_idx, o0, n_out, i0, e);
         key[r] = philox4x64_10((uint64_t)(v - g0), (uint64_t)(id[r] - g0), 1ull, 0ull, seed, 0ull).w[0];
       }
@@ -283,6 +294,7 @@ __global__ __launch_bounds__(256) void k_nbr_heavy(const int* __restrict__ row_p
       int c0 = 0;
 #pragma unroll
       for (int r = 0; r < kHeavyPerLane; ++r) {
+        if (r >= R) break;
         const int e = lane + 64 * r;
         const bool m = e < deg && ((key[r] & hi_mask) == prefix) && !((key[r] >> bit) & 1ull);
         c0 += __popcll(__ballot(m));
@@ -298,6 +310,7 @@ __global__ __launch_bounds__(256) void k_nbr_heavy(const int* __restrict__ row_p
     const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
 #pragma unroll
     for (int r = 0; r < kHeavyPerLane; ++r) {
+      if (r >= R) break;
       const int e = lane + 64 * r;
       const bool sel = e < deg && key[r] < T;
       const uint64_t bal = __ballot(sel);
@@ -309,6 +322,7 @@ __global__ __launch_bounds__(256) void k_nbr_heavy(const int* __restrict__ row_p
       int best = 0x7fffffff;
 #pragma unroll
       for (int r = 0; r < kHeavyPerLane; ++r) {
+        if (r >= R) break;
         const int e = lane + 64 * r;
         if (e < deg && key[r] == T && id[r] > last && id[r] < best) best = id[r];
       }

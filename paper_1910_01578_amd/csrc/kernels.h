@@ -1,4 +1,4 @@
-// Internal launch interface between the host API (gdp_api.cpp) and the
+// Internal launch interface between the host API (gdp_api.hip) and the
 // kernels.  Every launcher enqueues on `s` and returns the launch status.
 #pragma once
 
@@ -19,7 +19,7 @@ constexpr int kScanBlock = 1024;
 hipError_t launch_scan_degrees(const int* row_ptr, const int* in_deg, int n, int fanout,
                                int* in_ptr, int* s_ptr, int* block_tmp, hipStream_t s);
 hipError_t launch_fill_reverse(const int* row_ptr, const int* col_idx, const int* in_ptr, int n,
-                               int* cursor, int* in_idx, hipStream_t s);
+                               int64_t n_edges, int* cursor, int* in_idx, hipStream_t s);
 // heavy: n ints of scratch; heavy_count: one int, zero on entry.
 hipError_t launch_nbr_sample(const int* row_ptr, const int* col_idx, const int* in_ptr,
                              const int* in_idx, const int* s_ptr, int n, int fanout,

@@ -73,6 +73,11 @@ def _load():
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_1910_01578_amd.build_lib` "
                           "(there is no fallback path)")
+    # torch ships its own HIP runtime under the same soname (libamdhip64.so.7).
+    # Loading torch first makes libgdp bind to that copy; loaded the other way
+    # round the process would hold two runtimes, and pointers and streams from
+    # torch would not be valid in the one libgdp calls.
+    import torch  # noqa: F401
     lib = ctypes.CDLL(LIB_PATH)
     sig = {
         "gdp_workspace_bytes": (c_size_t, [POINTER(GdpGraph), POINTER(GdpGnn), POINTER(GdpPlacer), c_int32]),

@@ -192,3 +192,15 @@ def test_timer_state_machine():
     assert gdp.lib.gdp_timer_begin(1) == gdp.GDP_OK
     assert gdp.lib.gdp_timer_begin(1) == gdp.GDP_E_INVALID_ARG
     assert gdp.timer_end() == {}
+
+
+def test_one_hip_runtime_in_process():
+    """libgdp binds to the HIP runtime torch has loaded, not a second copy."""
+    import subprocess
+    import sys
+    code = ("from paper_1910_01578_amd import gdp\n"
+            "import torch\n"
+            "paths = {l.split()[-1] for l in open('/proc/self/maps') if 'libamdhip64' in l}\n"
+            "print(len(paths))\n")
+    out = subprocess.run([sys.executable, "-c", code], cwd=ROOT, check=True, capture_output=True, text=True)
+    assert out.stdout.strip().split("\n")[-1] == "1", out.stdout
