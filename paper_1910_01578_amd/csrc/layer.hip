@@ -19,10 +19,18 @@
 //                   feeds 4 MFMAs.  Used for W_o and W_2; the accumulator
 //                   holds Y + b_o, then Z, then Z + FFN(Z), so both
 //                   residuals come for free.
-// Weights stream through double-buffered LDS in chunks of FC units (K steps
-// of FC for W_o and W_2), chunk c+1 travelling global -> registers while
-// chunk c is multiplied.  Switching from the row tiling to the unit tiling
-// passes the activation through LDS once (as the MFMA element type).
+//
+// Operand staging.  Weights (and the attention output O) stream through LDS
+// in chunks of FC units by direct global -> LDS loads (global_load_lds, 16
+// bytes a lane): no registers hold a chunk in transit, which leaves them to
+// prefetch the next k step's MFMA fragments from LDS.  Such a load writes the
+// 64 lanes' 16-byte granules contiguously, so LDS tiles are unpadded and keep
+// their rows' granules in XOR-permuted order (swz_key) so that the 16 rows
+// read by one fragment load fall in distinct banks.  Chunk c + 1 is loaded
+// during chunk c into the other buffer of a pair; each staging buffer is a
+// __shared__ array of its own and the buffer parity of every step is a
+// compile-time constant, so the compiler can tell which LDS reads depend on
+// which load and waits for none that is still in flight.
 #include "device_common.h"
 #include "kernels.h"
 
@@ -35,61 +43,125 @@ constexpr int kLayerWaves = 8;
 constexpr int LNT = 64 * kLayerWaves;
 
 // Units per chunk and unit-tiling row blocks per wave: 64 and 2 for bf16; 32
-// and 1 for fp32, so that the weight buffers of a d = 256 layer fit in LDS
+// and 1 for fp32, so that the staging buffers of a d = 256 layer fit in LDS
 // and the fp32 activation fragments in registers.
 template <typename T> struct LayerCfg { static constexpr int FC = 64, RB1 = 2; };
 template <> struct LayerCfg<float> { static constexpr int FC = 32, RB1 = 1; };
 
-// Register staging of a ROWS x COLS block of a row-major matrix (leading
-// dimension ld), written to LDS with row stride S.  Rows >= rows_valid are
-// not read and stage zeros.  Held as 32-bit words: an array of 16-byte vectors
-// that stays live across barriers is kept in scratch memory by the compiler.
-template <typename T, int ROWS, int COLS, int S>
-struct Stage {
-  static constexpr int EPV = 16 / sizeof(T);
-  static constexpr int CPR = COLS / EPV;
-  static constexpr int CHUNKS = ROWS * CPR;
-  static_assert(CHUNKS % LNT == 0, "block must split evenly over the work-group");
-  static constexpr int PER = CHUNKS / LNT;
-  uint32_t r[4 * PER];
-  __device__ __forceinline__ void load(const T* base, size_t ld, int rows_valid = ROWS) {
-#pragma unroll
-    for (int i = 0; i < PER; ++i) {
-      const int q = threadIdx.x + i * LNT;
-      uint4 v = make_uint4(0u, 0u, 0u, 0u);
-      if (q / CPR < rows_valid) v = *reinterpret_cast<const uint4*>(base + (size_t)(q / CPR) * ld + (q % CPR) * EPV);
-      r[4 * i] = v.x;
-      r[4 * i + 1] = v.y;
-      r[4 * i + 2] = v.z;
-      r[4 * i + 3] = v.w;
-    }
-  }
-  __device__ __forceinline__ void store_piece(T* lds, int i) const {
-    const int q = threadIdx.x + i * LNT;
-    *reinterpret_cast<uint4*>(lds + (q / CPR) * S + (q % CPR) * EPV) =
-        make_uint4(r[4 * i], r[4 * i + 1], r[4 * i + 2], r[4 * i + 3]);
-  }
-  __device__ __forceinline__ void store(T* lds) const {
-#pragma unroll
-    for (int i = 0; i < PER; ++i) store_piece(lds, i);
-  }
-};
+template <int P> struct Par { static constexpr int v = P; };
 
-// FC biases of a chunk: 16-byte pieces held by the first FC / EPV threads,
-// staged to LDS with the chunk's weights (so that reading them never waits
-// on global memory, which would include the next chunk's prefetch).
+// f(Par<I>) for I = B .. E - 1, unrolled.
+template <int I, int E, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (I < E) {
+    f(Par<I>{});
+    static_for<I + 1, E>(f);
+  }
+}
+
+// Chunks c = 0 .. n - 1 two at a time, chunk c with buffer parity (P0 + c) & 1
+// as a compile-time argument.  n must be even when EVEN.
+template <int P0, bool EVEN, typename F>
+__device__ __forceinline__ void chunk_pairs(int n, F&& f) {
+  int c = 0;
+  for (; c + 1 < n; c += 2) {
+    f(c, Par<P0>{});
+    f(c + 1, Par<P0 ^ 1>{});
+  }
+  if constexpr (!EVEN) {
+    if (c < n) f(c, Par<P0>{});
+  }
+}
+
+// XOR key of row r in a tile whose rows hold GPR 16-byte granules: granule g
+// of row r is stored at granule g ^ swz_key(r).  Any 8 rows r0 .. r0 + 7 and
+// any 16 rows r0 .. r0 + 15 (r0 aligned) then place a given granule in
+// distinct 16-byte bank groups, for 128- and 256-byte bank rows alike.
+template <int GPR>
+__device__ __forceinline__ int swz_key(int r) {
+  if constexpr (GPR >= 16) return r & 15;
+  else if constexpr (GPR == 8) return (r & 7) ^ ((r >> 3) & 1);
+  else {
+    static_assert(GPR == 4, "tile rows of at least 64 bytes");
+    return ((r >> 2) ^ (r >> 1)) & 3;
+  }
+}
+
+// Element offset of (r, c) in a swizzled LDS tile of COLS columns of T.
+template <typename T, int COLS>
+__device__ __forceinline__ int swz(int r, int c) {
+  constexpr int EPV = 16 / sizeof(T);
+  constexpr int GPR = COLS / EPV;
+  return r * COLS + (((c / EPV) ^ swz_key<GPR>(r)) * EPV) + (c % EPV);
+}
+
+typedef const __attribute__((address_space(1))) char* gptr_t;
+
+// p as a global pointer in scalar registers (p must be wave-uniform).
+__device__ __forceinline__ gptr_t uniform_base(const void* p) {
+  const uint64_t v = (uint64_t)p;
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
+  return (gptr_t)(((uint64_t)hi << 32) | lo);
+}
+
+// One direct global -> LDS load: lane l reads the 16 bytes at base + voff
+// and writes them to LDS at lds + 16 l (lds wave-uniform).  Issued as inline
+// assembly so that the compiler keeps no bookkeeping of its own for these
+// loads (it would otherwise make later LDS accesses wait for all of them);
+// publish() is the only point that waits for them.  M0 holds the LDS base;
+// nothing else in these kernels keeps a value in M0.
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+__device__ __forceinline__ void dma16(gptr_t base, uint32_t voff, const void* lds) {
+  const uint32_t la = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)lds;
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
+               :: "v"(voff), "s"(base), "s"(__builtin_amdgcn_readfirstlane(la)) : "memory", "m0");
+}
+#pragma clang diagnostic pop
+
+// ROWS x COLS block of a row-major matrix (leading dimension ld; rows beyond
+// row_max read row row_max) into a swizzled LDS tile.  Load i of wave w fills
+// tile granules [(w * PER + i) * 64, + 64), lane l the granule at offset l.
+template <typename T, int ROWS, int COLS>
+__device__ __forceinline__ void dma_tile(T* tile, const T* src, int ld, int row_max) {
+  constexpr int EPV = 16 / sizeof(T);
+  constexpr int GPR = COLS / EPV;
+  constexpr int GRANULES = ROWS * GPR;
+  static_assert(GRANULES % LNT == 0, "tile must split evenly over the work-group");
+  constexpr int PER = GRANULES / LNT;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
+  const gptr_t base = uniform_base(src);
+#pragma unroll
+  for (int i = 0; i < PER; ++i) {
+    const int q = (wave * PER + i) * 64;
+    const int p = q + lane;
+    const int r = p / GPR;
+    const int g = (p % GPR) ^ swz_key<GPR>(r);
+    const int rs = r < row_max ? r : row_max;
+    const uint32_t off = ((uint32_t)rs * (uint32_t)ld + (uint32_t)(g * EPV)) * (uint32_t)sizeof(T);
+    dma16(base, off, tile + q * EPV);
+  }
+}
+
+// FC biases of a chunk (FC * sizeof(T) = 128 bytes) by the first lanes of wave 0.
 template <typename T, int FC>
-struct BiasStage {
-  static constexpr int EPV = 16 / sizeof(T);
-  static constexpr int THREADS = FC / EPV;
-  uint4 r = make_uint4(0u, 0u, 0u, 0u);
-  __device__ __forceinline__ void load(const T* b) {
-    if (threadIdx.x < THREADS) r = *reinterpret_cast<const uint4*>(b + threadIdx.x * EPV);
-  }
-  __device__ __forceinline__ void store(T* lds) const {
-    if (threadIdx.x < THREADS) *reinterpret_cast<uint4*>(lds + threadIdx.x * EPV) = r;
-  }
-};
+__device__ __forceinline__ void dma_bias(T* lds, const T* b) {
+  constexpr int EPV = 16 / sizeof(T);
+  if (threadIdx.x < FC / EPV) dma16(uniform_base(b), threadIdx.x * 16, lds);
+}
+
+// Barrier after which the data of every direct load issued before it by any
+// wave is in LDS.  (The work-group fence of a plain barrier does not cover
+// those loads, so each wave first waits for all of its own.)
+__device__ __forceinline__ void publish() {
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+}
+
+// Barrier for data written to LDS by ds_write only: direct loads in flight
+// stay in flight.
+__device__ __forceinline__ void bar_lds() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
 __device__ __forceinline__ uint32_t pack2_bf16(float lo, float hi) {
   typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
@@ -116,13 +188,7 @@ __device__ __forceinline__ void store4(bf16* p, const float (&v)[4]) {
   *reinterpret_cast<uint2*>(p) = make_uint2(pack2_bf16(v[0], v[1]), pack2_bf16(v[2], v[3]));
 }
 
-// Tile geometry and the LDS carve shared by all phases.  The phases use the
-// memory one after another, so their regions overlap:
-//   phase 0   O chunks [2][LBM x SH], W_o chunks [2][d x S2]
-//   FFN       W_1 chunks [2][FC x S1], W_2 chunks [2][d x S2], H [LBM x SH], b_1 [2][FC]
-//   switch    activation [LBM x SZ] (MFMA type)
-//   QKV       W_qkv chunks [2][FC x S1], b_qkv [2][FC]
-// plus the LayerNorm partial sums red[LBM][WN2] behind all of them.
+// Tile geometry.
 template <typename T, int D>
 struct Geo {
   using MF = Mfma<T>;
@@ -132,40 +198,53 @@ struct Geo {
   static constexpr int P1N = kLayerWaves / P1M;
   static constexpr int HPW = FC / P1N;            // units per wave and chunk
   static constexpr int JB1 = HPW / 16;
-  static constexpr int EPV = 16 / sizeof(T);
-  static constexpr int S1 = D + EPV;              // unit-tiling weight rows: K = d
-  static constexpr int S2 = FC + EPV;             // row-tiling weight rows: K = FC
-  static constexpr int SH = FC + EPV;             // row-tiling activation chunk rows
-  static constexpr int SZ = D + EPV;              // activation rows at the switch
   static constexpr int KS1 = D / MF::K;
   static constexpr int KS2 = FC / MF::K;
   static constexpr int WM2 = 2, WN2 = 4;          // row tiling
   static constexpr int MB2 = LBM / WM2 / 16;
   static constexpr int NB2 = D / WN2 / 16;
+  static constexpr int NK0 = D / FC;              // phase-0 chunks
+  static constexpr int NQ = 3 * D / FC;           // QKV chunks
+  // elements of a staging buffer: a weight chunk (FC x D or D x FC) or an O chunk (LBM x FC)
+  static constexpr int BUF = FC * (D > LBM ? D : LBM);
+  // At a switch from the row to the unit tiling the activation passes through
+  // LDS as NZ column parts of ZC columns, one staging buffer each.
+  static constexpr int NZ = LBM / FC;
+  static constexpr int ZC = D / NZ;
   static_assert(P1M * P1N == kLayerWaves && JB1 >= 1 && NB2 >= 1, "wave grids");
-  static_assert(D % FC == 0, "d must be a multiple of the chunk");
+  static_assert(D % FC == 0 && (NZ == 2 || NZ == 4) && ZC % MF::K == 0, "tile shapes");
+  static_assert(ZC % (D / WN2) == 0, "a row-tiling wave writes within one part");
+  static_assert(FC * D <= BUF && LBM * FC <= BUF && LBM * ZC <= BUF, "every staged tile fits a buffer");
   typedef f32x4 UnitAcc[RB1][JB1];                       // unit-tiling accumulators
   typedef f32x4 RowAcc[MB2][NB2];                        // row-tiling accumulators
   typedef typename MF::frag ActFrags[RB1][KS1];          // unit-tiling activation fragments
   typedef float Red[WN2];
-
-  static constexpr int W1B = FC * S1 * sizeof(T);
-  static constexpr int W2B = D * S2 * sizeof(T);
-  static constexpr int HB = LBM * SH * sizeof(T);
-  static constexpr int BB = FC * sizeof(T);
-  // FFN carve
-  static constexpr int OFF_W1 = 0, OFF_W2 = 2 * W1B, OFF_H = OFF_W2 + 2 * W2B, OFF_B1 = OFF_H + HB;
-  static constexpr int FFN_END = OFF_B1 + 2 * BB;
-  // phase-0 carve: O chunks first, then the W_o chunks
-  static constexpr int OFF_O = 0, OFF_WO = 2 * HB;
-  static constexpr int P0_END = OFF_WO + 2 * W2B;
-  // switch
-  static constexpr int SW_END = LBM * SZ * (int)sizeof(T);
-  static constexpr int mx(int a, int b) { return a > b ? a : b; }
-  static constexpr int OFF_RED = (mx(mx(FFN_END, P0_END), SW_END) + 15) / 16 * 16;
-  static constexpr int TOTAL = OFF_RED + LBM * WN2 * (int)sizeof(float);
-  static_assert(TOTAL <= 160 * 1024, "LDS budget");
+  static constexpr int LDS_BYTES = (4 * BUF + LBM * FC + 2 * FC) * (int)sizeof(T) + LBM * WN2 * (int)sizeof(float);
+  static_assert(LDS_BYTES <= 160 * 1024, "LDS budget");
 };
+
+// The work-group's LDS: staging buffer pairs u (unit-tiling weights, O chunks)
+// and r (row-tiling weights), the hidden chunk h, chunk biases b, and the
+// LayerNorm partial sums.  Activation parts at a switch use u and r buffers.
+template <typename T>
+struct Lds {
+  T *u0, *u1, *r0, *r1, *b0, *b1, *h;
+  float* red;
+  template <int P> __device__ __forceinline__ T* u() const { return P ? u1 : u0; }
+  template <int P> __device__ __forceinline__ T* r() const { return P ? r1 : r0; }
+  template <int P> __device__ __forceinline__ T* b() const { return P ? b1 : b0; }
+};
+
+#define GDP_LAYER_LDS(T, G)                                                  \
+  __shared__ __attribute__((aligned(16))) T lds_u0_[G::BUF];               \
+  __shared__ __attribute__((aligned(16))) T lds_u1_[G::BUF];               \
+  __shared__ __attribute__((aligned(16))) T lds_r0_[G::BUF];               \
+  __shared__ __attribute__((aligned(16))) T lds_r1_[G::BUF];               \
+  __shared__ __attribute__((aligned(16))) T lds_b0_[G::FC];                \
+  __shared__ __attribute__((aligned(16))) T lds_b1_[G::FC];                \
+  __shared__ __attribute__((aligned(16))) T lds_h_[LBM * G::FC];           \
+  __shared__ __attribute__((aligned(16))) float lds_red_[LBM * G::WN2];    \
+  const Lds<T> L{lds_u0_, lds_u1_, lds_r0_, lds_r1_, lds_b0_, lds_b1_, lds_h_, lds_red_}
 
 // Per-lane position in the two tilings.
 struct Lanes {
@@ -174,53 +253,80 @@ struct Lanes {
   int w2m, w2n;        // row tiling
 };
 
-// unit tiling: hacc[i][j] = W_c(rows p1n*HPW + j*16 + ..) x act(rows (p1m*RB1 + i)*16 + ..)^T.
-// after_step(s) runs after the MFMAs of k step s have been issued: other
-// work placed there executes while they are in the matrix pipe.
-template <typename T, int D, typename Hook>
+template <typename T, int D>
+__device__ __forceinline__ Lanes make_lanes() {
+  using G = Geo<T, D>;
+  Lanes ln;
+  ln.lane = threadIdx.x & 63;
+  ln.wave = threadIdx.x >> 6;
+  ln.col = ln.lane & 15;
+  ln.g4 = ln.lane >> 4;
+  ln.p1m = ln.wave / G::P1N;
+  ln.p1n = ln.wave % G::P1N;
+  ln.w2m = ln.wave / G::WN2;
+  ln.w2n = ln.wave % G::WN2;
+  return ln;
+}
+
+// unit tiling: hacc[i][j] = W_c(units p1n*HPW + j*16 + ..) x act(rows (p1m*RB1 + i)*16 + ..)^T,
+// W_c a swizzled FC x D tile.  The fragments of k step s + 1 are requested
+// before the MFMAs of step s issue.
+template <typename T, int D>
 __device__ __forceinline__ void unit_mma(typename Geo<T, D>::UnitAcc& hacc, const typename Geo<T, D>::ActFrags& af,
-                                         const T* sW, const Lanes& ln, Hook&& after_step) {
+                                         const T* sW, const Lanes& ln) {
   using G = Geo<T, D>;
   using MF = Mfma<T>;
+  typename MF::frag bw[2][G::JB1];
 #pragma unroll
   for (int i = 0; i < G::RB1; ++i)
 #pragma unroll
     for (int j = 0; j < G::JB1; ++j) hacc[i][j] = zero4();
 #pragma unroll
+  for (int j = 0; j < G::JB1; ++j)
+    bw[0][j] = MF::load(&sW[swz<T, D>(ln.p1n * G::HPW + j * 16 + ln.col, MF::KV * ln.g4)]);
+#pragma unroll
   for (int s = 0; s < G::KS1; ++s) {
+    if (s + 1 < G::KS1) {
 #pragma unroll
-    for (int j = 0; j < G::JB1; ++j) {
-      const typename MF::frag bw = MF::load(&sW[(ln.p1n * G::HPW + j * 16 + ln.col) * G::S1 + s * MF::K + MF::KV * ln.g4]);
-#pragma unroll
-      for (int i = 0; i < G::RB1; ++i) hacc[i][j] = MF::mma(bw, af[i][s], hacc[i][j]);
+      for (int j = 0; j < G::JB1; ++j)
+        bw[(s + 1) & 1][j] =
+            MF::load(&sW[swz<T, D>(ln.p1n * G::HPW + j * 16 + ln.col, (s + 1) * MF::K + MF::KV * ln.g4)]);
     }
-    after_step(s);
+    __builtin_amdgcn_sched_barrier(0);   // keep the prefetch ahead of this step's MFMAs
+#pragma unroll
+    for (int j = 0; j < G::JB1; ++j)
+#pragma unroll
+      for (int i = 0; i < G::RB1; ++i) hacc[i][j] = MF::mma(bw[s & 1][j], af[i][s], hacc[i][j]);
+    __builtin_amdgcn_sched_barrier(0);
   }
 }
-template <typename T, int D>
-__device__ __forceinline__ void unit_mma(typename Geo<T, D>::UnitAcc& hacc, const typename Geo<T, D>::ActFrags& af,
-                                         const T* sW, const Lanes& ln) {
-  unit_mma<T, D>(hacc, af, sW, ln, [](int) {});
-}
 
-// row tiling: acc += A_c W_c^T with A_c = sA rows [LBM x FC] (stride SH), W_c = sW rows [d x FC] (stride S2)
+// row tiling: acc += A_c W_c^T with A_c a swizzled LBM x FC tile and W_c a
+// swizzled D x FC tile, step s + 1's fragments requested before step s's MFMAs.
 template <typename T, int D>
 __device__ __forceinline__ void row_mma(typename Geo<T, D>::RowAcc& acc, const T* sA, const T* sW, const Lanes& ln) {
   using G = Geo<T, D>;
   using MF = Mfma<T>;
-#pragma unroll
-  for (int s = 0; s < G::KS2; ++s) {
-    typename MF::frag af[G::MB2], bf[G::NB2];
+  constexpr int FC = G::FC;
+  typename MF::frag af[2][G::MB2], bf[2][G::NB2];
+  auto load = [&](int s, typename MF::frag (&a)[G::MB2], typename MF::frag (&b)[G::NB2]) {
 #pragma unroll
     for (int i = 0; i < G::MB2; ++i)
-      af[i] = MF::load(&sA[(ln.w2m * G::MB2 * 16 + i * 16 + ln.col) * G::SH + s * MF::K + MF::KV * ln.g4]);
+      a[i] = MF::load(&sA[swz<T, FC>(ln.w2m * G::MB2 * 16 + i * 16 + ln.col, s * MF::K + MF::KV * ln.g4)]);
 #pragma unroll
     for (int j = 0; j < G::NB2; ++j)
-      bf[j] = MF::load(&sW[(ln.w2n * G::NB2 * 16 + j * 16 + ln.col) * G::S2 + s * MF::K + MF::KV * ln.g4]);
+      b[j] = MF::load(&sW[swz<T, FC>(ln.w2n * G::NB2 * 16 + j * 16 + ln.col, s * MF::K + MF::KV * ln.g4)]);
+  };
+  load(0, af[0], bf[0]);
+#pragma unroll
+  for (int s = 0; s < G::KS2; ++s) {
+    if (s + 1 < G::KS2) load(s + 1, af[(s + 1) & 1], bf[(s + 1) & 1]);
+    __builtin_amdgcn_sched_barrier(0);   // keep the prefetch ahead of this step's MFMAs
 #pragma unroll
     for (int i = 0; i < G::MB2; ++i)
 #pragma unroll
-      for (int j = 0; j < G::NB2; ++j) acc[i][j] = MF::mma(bf[j], af[i], acc[i][j]);
+      for (int j = 0; j < G::NB2; ++j) acc[i][j] = MF::mma(bf[s & 1][j], af[s & 1][i], acc[i][j]);
+    __builtin_amdgcn_sched_barrier(0);
   }
 }
 
@@ -289,113 +395,119 @@ __device__ __forceinline__ void ln_rows(typename Geo<T, D>::RowAcc& acc, const T
   }
 }
 
-// Row tiling -> unit tiling: the activation in acc goes to LDS as T, and each
-// wave reads back its unit-tiling rows as MFMA fragments.  Ends with a
-// barrier after which the LDS is free again.
-template <typename T, int D>
-__device__ __forceinline__ void to_unit_tiling(const typename Geo<T, D>::RowAcc& acc, T* sZ,
+// Row tiling -> unit tiling: the activation in acc goes to LDS as T in NZ
+// column parts (the buffers of parity ZP when NZ = 2, all four when NZ = 4),
+// and each wave reads back its unit-tiling rows as MFMA fragments.  On exit
+// the parts may still be read by other waves, except for NZ = 4, where a
+// barrier frees every buffer.
+template <typename T, int D, int ZP>
+__device__ __forceinline__ void to_unit_tiling(const typename Geo<T, D>::RowAcc& acc, const Lds<T>& L,
                                                typename Geo<T, D>::ActFrags& af, const Lanes& ln) {
   using G = Geo<T, D>;
   using MF = Mfma<T>;
+  constexpr int ZC = G::ZC;
   const int rbase = ln.w2m * G::MB2 * 16 + ln.col;
   const int cbase = ln.w2n * G::NB2 * 16 + 4 * ln.g4;
+  const int zpart = ln.w2n * G::NB2 * 16 / ZC;          // wave-uniform
+  auto write = [&](T* part) {
 #pragma unroll
-  for (int i = 0; i < G::MB2; ++i)
+    for (int i = 0; i < G::MB2; ++i)
 #pragma unroll
-    for (int j = 0; j < G::NB2; ++j) {
-      const float v[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
-      store4(&sZ[(rbase + i * 16) * G::SZ + cbase + j * 16], v);
-    }
-  __syncthreads();
+      for (int j = 0; j < G::NB2; ++j) {
+        const float v[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
+        store4(&part[swz<T, ZC>(rbase + i * 16, cbase + j * 16 - zpart * ZC)], v);
+      }
+  };
+  auto part_of = [&](auto zc) -> T* {
+    constexpr int z = decltype(zc)::v;
+    if constexpr (G::NZ == 2) return z == 0 ? L.template u<ZP>() : L.template r<ZP>();
+    else return z == 0 ? L.u0 : z == 1 ? L.u1 : z == 2 ? L.r0 : L.r1;
+  };
+  if constexpr (G::NZ == 2) {
+    if (zpart == 0) write(part_of(Par<0>{}));
+    else write(part_of(Par<1>{}));
+  } else {
+    if (zpart == 0) write(part_of(Par<0>{}));
+    else if (zpart == 1) write(part_of(Par<1>{}));
+    else if (zpart == 2) write(part_of(Par<2>{}));
+    else write(part_of(Par<3>{}));
+  }
+  bar_lds();
+  static_for<0, G::KS1>([&](auto sc) {
+    constexpr int s = decltype(sc)::v;
+    constexpr int z = s * MF::K / ZC;
+    const T* part = part_of(Par<z>{});
 #pragma unroll
-  for (int i = 0; i < G::RB1; ++i)
-#pragma unroll
-    for (int s = 0; s < G::KS1; ++s)
-      af[i][s] = MF::load(&sZ[((ln.p1m * G::RB1 + i) * 16 + ln.col) * G::SZ + s * MF::K + MF::KV * ln.g4]);
-  __syncthreads();
+    for (int i = 0; i < G::RB1; ++i)
+      af[i][s] = MF::load(&part[swz<T, ZC>((ln.p1m * G::RB1 + i) * 16 + ln.col, s * MF::K - z * ZC + MF::KV * ln.g4)]);
+  });
+  if constexpr (G::NZ == 4) bar_lds();
 }
 
-// QKV = act W_qkv^T + b_qkv for the work-group's rows, chunks of FC output
-// units, with the activation in the row tiling in acc (it passes to the unit
-// tiling through LDS; every LDS region must be free on entry).  The q columns
-// are multiplied by q_scale.  Two register sets alternate so that chunk q + 2
-// is requested while chunk q is multiplied.
-template <typename T, int D>
-__device__ __forceinline__ void qkv_phase(const typename Geo<T, D>::RowAcc& acc, char* smem,
+// Chunk q of the QKV projection (FC output units of W_qkv) into the buffers
+// of parity P.
+template <typename T, int D, int P>
+__device__ __forceinline__ void dma_qkv_chunk(const Lds<T>& L, const T* w_qkv, const T* b_qkv, int q) {
+  using G = Geo<T, D>;
+  dma_tile<T, G::FC, D>(L.template u<P>(), w_qkv + (size_t)q * G::FC * D, D, G::FC - 1);
+  dma_bias<T, G::FC>(L.template b<P>(), b_qkv + q * G::FC);
+}
+
+// QKV = act W_qkv^T + b_qkv for the work-group's rows, the activation in the
+// row tiling in acc; the q columns are multiplied by q_scale.  Chunk q uses
+// buffer parity (q + QP) & 1; the activation passes to the unit tiling through
+// the parity QP ^ 1 buffers.  With NZ = 2 chunk 0 must already be in flight
+// (or in place) in the parity QP buffers; every other buffer must be free.
+template <typename T, int D, int QP>
+__device__ __forceinline__ void qkv_phase(const typename Geo<T, D>::RowAcc& acc, const Lds<T>& L,
                                           typename Geo<T, D>::ActFrags& af, const Lanes& ln, int m0, int M,
                                           const T* w_qkv, const T* b_qkv, T* qkv_out, int ldq, float q_scale) {
   using G = Geo<T, D>;
   constexpr int FC = G::FC;
-  T* sW1 = reinterpret_cast<T*>(smem + G::OFF_W1);
-  T* sB = reinterpret_cast<T*>(smem + G::OFF_B1);
-  {
-    Stage<T, FC, D, G::S1> stA, stB;
-    BiasStage<T, FC> sbA, sbB;
-    constexpr int NQ = 3 * D / FC;
-    stA.load(w_qkv, D);
-    sbA.load(b_qkv);
-    if (NQ > 1) {
-      stB.load(w_qkv + (size_t)FC * D, D);
-      sbB.load(b_qkv + FC);
+  to_unit_tiling<T, D, QP ^ 1>(acc, L, af, ln);
+  if constexpr (G::NZ == 4) dma_qkv_chunk<T, D, QP>(L, w_qkv, b_qkv, 0);
+  chunk_pairs<QP, (G::NQ % 2) == 0>(G::NQ, [&](int q, auto pc) {
+    constexpr int P = decltype(pc)::v;
+    publish();                       // chunk q in place; chunk q - 1's buffers (and the parts) free
+    if (q + 1 < G::NQ) dma_qkv_chunk<T, D, P ^ 1>(L, w_qkv, b_qkv, q + 1);
+    typename G::UnitAcc hacc;
+    unit_mma<T, D>(hacc, af, L.template u<P>(), ln);
+    const float scale = q * FC < D ? q_scale : 1.0f;   // a chunk lies wholly in q, k or v
+    const T* sB = L.template b<P>();
+#pragma unroll
+    for (int j = 0; j < G::JB1; ++j) {
+      const int hc = ln.p1n * G::HPW + j * 16 + 4 * ln.g4;
+      float b[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) b[r] = to_f32(sB[hc + r]);
+#pragma unroll
+      for (int i = 0; i < G::RB1; ++i) {
+        const int row = m0 + (ln.p1m * G::RB1 + i) * 16 + ln.col;
+        float v[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) v[r] = (hacc[i][j][r] + b[r]) * scale;
+        if (row < M) store4(qkv_out + (size_t)row * ldq + q * FC + hc, v);
+      }
     }
-    to_unit_tiling<T, D>(acc, reinterpret_cast<T*>(smem), af, ln);
-    stA.store(sW1);
-    sbA.store(sB);
-    __syncthreads();
-    // chunk q: weights in buffer q & 1; `next` holds chunk q + 1, `mine` is free
-    auto step = [&](int q, Stage<T, FC, D, G::S1>& mine, BiasStage<T, FC>& mine_b, Stage<T, FC, D, G::S1>& next,
-                    BiasStage<T, FC>& next_b) {
-      const int cur = q & 1;
-      typename G::UnitAcc hacc;
-      unit_mma<T, D>(hacc, af, sW1 + cur * FC * G::S1, ln);
-      if (q + 1 < NQ) {
-        next.store(sW1 + (cur ^ 1) * FC * G::S1);   // last read in chunk q - 1
-        next_b.store(sB + (cur ^ 1) * FC);
-      }
-      if (q + 2 < NQ) {
-        mine.load(w_qkv + (size_t)(q + 2) * FC * D, D);
-        mine_b.load(b_qkv + (q + 2) * FC);
-      }
-      const float scale = q * FC < D ? q_scale : 1.0f;   // a chunk lies wholly in q, k or v
-#pragma unroll
-      for (int j = 0; j < G::JB1; ++j) {
-        const int hc = ln.p1n * G::HPW + j * 16 + 4 * ln.g4;
-        float b[4];
-#pragma unroll
-        for (int r = 0; r < 4; ++r) b[r] = to_f32(sB[cur * FC + hc + r]);
-#pragma unroll
-        for (int i = 0; i < G::RB1; ++i) {
-          const int row = m0 + (ln.p1m * G::RB1 + i) * 16 + ln.col;
-          float v[4];
-#pragma unroll
-          for (int r = 0; r < 4; ++r) v[r] = (hacc[i][j][r] + b[r]) * scale;
-          if (row < M) store4(qkv_out + (size_t)row * ldq + q * FC + hc, v);
-        }
-      }
-      __syncthreads();                 // this chunk's buffers free
-    };
-    for (int q = 0; q < NQ; q += 2) {
-      step(q, stA, sbA, stB, sbB);
-      if (q + 1 < NQ) step(q + 1, stB, sbB, stA, sbA);
-    }
-  }
+  });
 }
-
 
 // The placement head on the rows held in the row tiling (Fig. 1's N x d
 // output): logits[row][e] = act[row] . W_out[e] + b_out[e] for e < n_dev <=
-// kFusedHeadDevices, and their logsumexp.  W_out goes to LDS as fp32; each
-// lane forms the partial sums of its rows over its columns, the 4 lane groups
-// of a row combine by butterfly and the WN2 column waves through LDS.  Every
-// LDS region must be free on entry.
+// kFusedHeadDevices, and their logsumexp.  W_out goes to LDS as fp32 (in u0);
+// each lane forms the partial sums of its rows over its columns, the 4 lane
+// groups of a row combine by butterfly and the WN2 column waves through LDS
+// (in h).  u0 and h must be free on entry.
 template <typename T, int D>
-__device__ __forceinline__ void head_epilogue(const typename Geo<T, D>::RowAcc& acc, char* smem, const Lanes& ln,
-                                              int m0, int M, const T* w_out, const T* b_out, int n_dev,
-                                              float* logits, float* lse) {
+__device__ __forceinline__ void head_epilogue(const typename Geo<T, D>::RowAcc& acc, const Lds<T>& L,
+                                              const Lanes& ln, int m0, int M, const T* w_out, const T* b_out,
+                                              int n_dev, float* logits, float* lse) {
   using G = Geo<T, D>;
   constexpr int E = kFusedHeadDevices;
-  float* sW = reinterpret_cast<float*>(smem);                                  // [E][D]
-  float (*hred)[G::WN2][E] = reinterpret_cast<float (*)[G::WN2][E]>(smem + E * D * sizeof(float));
+  static_assert(E * D * sizeof(float) <= G::BUF * sizeof(T), "W_out fits a staging buffer");
+  static_assert(LBM * G::WN2 * E * sizeof(float) <= LBM * G::FC * sizeof(T), "head sums fit h");
+  float* sW = reinterpret_cast<float*>(L.u0);                      // [E][D]
+  float (*hred)[G::WN2][E] = reinterpret_cast<float (*)[G::WN2][E]>(L.h);
   const int rbase = ln.w2m * G::MB2 * 16 + ln.col;
   const int cbase = ln.w2n * G::NB2 * 16 + 4 * ln.g4;
   for (int i = threadIdx.x; i < E * D; i += LNT) sW[i] = i < n_dev * D ? to_f32(w_out[i]) : 0.f;
@@ -448,32 +560,43 @@ __device__ __forceinline__ void head_epilogue(const typename Geo<T, D>::RowAcc& 
   }
 }
 
+template <typename T>
+bool aligned_16(const T* p) { return ((uintptr_t)p & 15u) == 0; }
+
 }  // namespace
 
 // HEAD: the last layer's variant, with the placement head instead of a QKV projection.
 template <typename T, int D, bool HEAD>
 __global__ __launch_bounds__(LNT) void k_post_attention(PostAttnArgs<T> p, GraphTable gt) {
   using G = Geo<T, D>;
-  using MF = Mfma<T>;
   constexpr int FC = G::FC;
-  __shared__ __attribute__((aligned(16))) char smem[G::TOTAL];
-  typename G::Red* red = reinterpret_cast<typename G::Red*>(smem + G::OFF_RED);
+  constexpr int NK0 = G::NK0;
+  GDP_LAYER_LDS(T, G);
+  typename G::Red* red = reinterpret_cast<typename G::Red*>(L.red);
 
-  Lanes ln;
-  ln.lane = threadIdx.x & 63;
-  ln.wave = threadIdx.x >> 6;
-  ln.col = ln.lane & 15;
-  ln.g4 = ln.lane >> 4;
-  ln.p1m = ln.wave / G::P1N;
-  ln.p1n = ln.wave % G::P1N;
-  ln.w2m = ln.wave / G::WN2;
-  ln.w2n = ln.wave % G::WN2;
+  const Lanes ln = make_lanes<T, D>();
   const int m0 = blockIdx.x * LBM;
   const int rows_valid = p.M - m0;
   const int rbase = ln.w2m * G::MB2 * 16 + ln.col;      // row tiling: rows rbase + 16 i
   const int cbase = ln.w2n * G::NB2 * 16 + 4 * ln.g4;   //             columns cbase + 16 j + [0, 4)
+  const bool qkv_next = !HEAD && p.w_qkv != nullptr;
+
+  // Chunk c of the FFN: W_1 rows, W_2 columns and b_1 entries c*FC .. + FC.
+  auto dma_ffn = [&](int c, auto pc) {
+    constexpr int P = decltype(pc)::v;
+    dma_tile<T, FC, D>(L.template u<P>(), p.w1 + (size_t)c * FC * D, D, FC - 1);
+    dma_tile<T, D, FC>(L.template r<P>(), p.w2 + (size_t)c * FC, p.d_ff, D - 1);
+    dma_bias<T, FC>(L.template b<P>(), p.b1 + c * FC);
+  };
+  // Chunk kc of phase 0: O columns and W_o columns kc*FC .. + FC, parity kc & 1.
+  auto dma_p0 = [&](auto kcc) {
+    constexpr int kc = decltype(kcc)::v;
+    dma_tile<T, LBM, FC>(L.template u<kc & 1>(), p.o + (size_t)m0 * p.ldo + kc * FC, p.ldo, rows_valid - 1);
+    dma_tile<T, D, FC>(L.template r<kc & 1>(), p.w_o + kc * FC, D, D - 1);
+  };
 
   // ---- phase 0: acc = Y + b_o + O W_o^T, then LN1 --------------------------
+  dma_p0(Par<0>{});
   typename G::RowAcc acc;
 #pragma unroll
   for (int i = 0; i < G::MB2; ++i) {
@@ -489,102 +612,48 @@ __global__ __launch_bounds__(LNT) void k_post_attention(PostAttnArgs<T> p, Graph
       acc[i][j][3] = y.w + to_f32(p.b_o[cn + 3]);
     }
   }
-  {
-    T* sO = reinterpret_cast<T*>(smem + G::OFF_O);       // [2][LBM * SH]
-    T* sWo = reinterpret_cast<T*>(smem + G::OFF_WO);     // [2][D * S2]
-    Stage<T, LBM, FC, G::SH> so;
-    Stage<T, D, FC, G::S2> sw;
-    constexpr int NK = D / FC;
-    so.load(p.o + (size_t)m0 * p.ldo, p.ldo, rows_valid);
-    sw.load(p.w_o, D);
-    so.store(sO);
-    sw.store(sWo);
-    __syncthreads();
-    for (int kc = 0; kc < NK; ++kc) {
-      const int cur = kc & 1;
-      if (kc + 1 < NK) {
-        so.load(p.o + (size_t)m0 * p.ldo + (kc + 1) * FC, p.ldo, rows_valid);
-        sw.load(p.w_o + (kc + 1) * FC, D);
-      }
-      row_mma<T, D>(acc, sO + cur * LBM * G::SH, sWo + cur * D * G::S2, ln);
-      if (kc + 1 < NK) {
-        // the other buffers were last read in step kc - 1, before its barrier
-        so.store(sO + (cur ^ 1) * LBM * G::SH);
-        sw.store(sWo + (cur ^ 1) * D * G::S2);
-      }
-      __syncthreads();
-    }
-  }
+  static_for<0, NK0>([&](auto kcc) {
+    constexpr int kc = decltype(kcc)::v;
+    publish();                       // chunk kc in place; chunk kc - 1's buffers free
+    if constexpr (kc + 1 < NK0) dma_p0(Par<kc + 1>{});
+    else if constexpr (G::NZ == 2) dma_ffn(0, Par<NK0 & 1>{});   // FFN chunk 0 into the other pair
+    row_mma<T, D>(acc, L.template u<kc & 1>(), L.template r<kc & 1>(), ln);
+  });
   ln_rows<T, D>(acc, p.ln1_g, p.ln1_b, red, ln);       // acc = Z
 
   // ---- FFN: acc += W_2 ReLU(W_1 Z + b_1), chunks of FC hidden units ----------
-  T* sW1 = reinterpret_cast<T*>(smem + G::OFF_W1);       // [2][FC * S1]
-  T* sW2 = reinterpret_cast<T*>(smem + G::OFF_W2);       // [2][D * S2]
-  T* sH = reinterpret_cast<T*>(smem + G::OFF_H);         // [LBM * SH]
-  T* sB = reinterpret_cast<T*>(smem + G::OFF_B1);        // [2][FC]
   typename G::ActFrags af;
-  {
-    Stage<T, FC, D, G::S1> st1;
-    Stage<T, D, FC, G::S2> st2;
-    BiasStage<T, FC> sb;
-    const int NC = p.d_ff / FC;
-    st1.load(p.w1, D);
-    st2.load(p.w2, p.d_ff);
-    sb.load(p.b1);
-    auto load_chunk = [&](int c) {
-      st1.load(p.w1 + (size_t)c * FC * D, D);
-      st2.load(p.w2 + (size_t)c * FC, p.d_ff);
-      sb.load(p.b1 + c * FC);
-    };
-    to_unit_tiling<T, D>(acc, reinterpret_cast<T*>(smem), af, ln);
-    st1.store(sW1);
-    st2.store(sW2);
-    sb.store(sB);
-    if (NC > 1) load_chunk(1);
-    __syncthreads();
-    // Chunk c + 1 sits in registers from the start of the second product of
-    // chunk c - 1 until after the first product of chunk c, so its global
-    // latency hides under both.
-    for (int c = 0; c < NC; ++c) {
-      const int cur = c & 1;
-      typename G::UnitAcc hacc;
-      // Chunk c + 1 lands in the other buffers during the first product, one
-      // 16-byte piece per thread after each k step: those buffers were last
-      // read in chunk c - 1, before its final barrier.
-      constexpr int P1 = decltype(st1)::PER, P2 = decltype(st2)::PER;
-      const bool more = c + 1 < NC;
-      T* n1 = sW1 + (cur ^ 1) * FC * G::S1;
-      T* n2 = sW2 + (cur ^ 1) * D * G::S2;
-      unit_mma<T, D>(hacc, af, sW1 + cur * FC * G::S1, ln, [&](int s) {
-        if (!more) return;
-#pragma unroll
-        for (int k = (s * (P1 + P2)) / G::KS1; k < ((s + 1) * (P1 + P2)) / G::KS1; ++k) {
-          if (k < P1) st1.store_piece(n1, k);
-          else st2.store_piece(n2, k - P1);
-        }
-      });
-      if (more) sb.store(sB + (cur ^ 1) * FC);
-      // lane holds hidden row (p1m * RB1 + i) * 16 + col, units hc + [0, 4)
-#pragma unroll
-      for (int j = 0; j < G::JB1; ++j) {
-        const int hc = ln.p1n * G::HPW + j * 16 + 4 * ln.g4;
-        float b[4];
-#pragma unroll
-        for (int r = 0; r < 4; ++r) b[r] = to_f32(sB[cur * FC + hc + r]);
-#pragma unroll
-        for (int i = 0; i < G::RB1; ++i) {
-          float h[4];
-#pragma unroll
-          for (int r = 0; r < 4; ++r) h[r] = fmaxf(hacc[i][j][r] + b[r], 0.f);
-          store4(&sH[((ln.p1m * G::RB1 + i) * 16 + ln.col) * G::SH + hc], h);
-        }
-      }
-      __syncthreads();                 // H and chunk c + 1 complete
-      if (c + 2 < NC) load_chunk(c + 2);
-      row_mma<T, D>(acc, sH, sW2 + cur * D * G::S2, ln);
-      __syncthreads();                 // H and this chunk's buffers free
+  to_unit_tiling<T, D, (NK0 + 1) & 1>(acc, L, af, ln);
+  if constexpr (G::NZ == 4) dma_ffn(0, Par<NK0 & 1>{});
+  const int NC = p.d_ff / FC;                           // even
+  chunk_pairs<NK0 & 1, true>(NC, [&](int c, auto pc) {
+    constexpr int P = decltype(pc)::v;
+    publish();                       // chunk c in place; chunk c - 1's buffers, H and the parts free
+    if (c + 1 < NC) dma_ffn(c + 1, Par<P ^ 1>{});
+    else if constexpr (G::NZ == 2) {
+      if (qkv_next) dma_qkv_chunk<T, D, P ^ 1>(L, p.w_qkv, p.b_qkv, 0);
     }
-  }
+    typename G::UnitAcc hacc;
+    unit_mma<T, D>(hacc, af, L.template u<P>(), ln);
+    const T* sB = L.template b<P>();
+    // lane holds hidden row (p1m * RB1 + i) * 16 + col, units hc + [0, 4)
+#pragma unroll
+    for (int j = 0; j < G::JB1; ++j) {
+      const int hc = ln.p1n * G::HPW + j * 16 + 4 * ln.g4;
+      float b[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) b[r] = to_f32(sB[hc + r]);
+#pragma unroll
+      for (int i = 0; i < G::RB1; ++i) {
+        float h[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) h[r] = fmaxf(hacc[i][j][r] + b[r], 0.f);
+        store4(&L.h[swz<T, FC>((ln.p1m * G::RB1 + i) * 16 + ln.col, hc)], h);
+      }
+    }
+    bar_lds();                       // H complete
+    row_mma<T, D>(acc, L.h, L.template r<P>(), ln);
+  });
 
   // ---- + b_2, LN2, FiLM of the next layer; store Y' ---------------------------
 #pragma unroll
@@ -617,18 +686,24 @@ __global__ __launch_bounds__(LNT) void k_post_attention(PostAttnArgs<T> p, Graph
     }
   }
   if constexpr (HEAD) {
-    head_epilogue<T, D>(acc, smem, ln, m0, p.M, p.w_out, p.b_out, p.n_dev, p.logits, p.lse);
+    head_epilogue<T, D>(acc, L, ln, m0, p.M, p.w_out, p.b_out, p.n_dev, p.logits, p.lse);
   } else {
-    if (!p.w_qkv) return;
-    qkv_phase<T, D>(acc, smem, af, ln, m0, p.M, p.w_qkv, p.b_qkv, p.qkv_out, p.ldq, p.q_scale);
+    if (!qkv_next) return;
+    // the FFN's last chunk used parity (NK0 + 1) & 1 (an even number of chunks)
+    qkv_phase<T, D, NK0 & 1>(acc, L, af, ln, m0, p.M, p.w_qkv, p.b_qkv, p.qkv_out, p.ldq, p.q_scale);
   }
 }
 
 template <typename T>
 hipError_t launch_post_attention(const PostAttnArgs<T>& a, const GraphTable& gt, hipStream_t s) {
   if (a.M <= 0) return hipSuccess;
-  if (a.d_ff <= 0 || a.d_ff % LayerCfg<T>::FC) return hipErrorInvalidValue;
-  if (a.w_qkv && (!a.b_qkv || !a.qkv_out || a.ldq < 3 * a.d)) return hipErrorInvalidValue;
+  constexpr int EPV = 16 / sizeof(T);
+  if (a.d_ff <= 0 || a.d_ff % (2 * LayerCfg<T>::FC)) return hipErrorInvalidValue;
+  if (a.ldo % EPV || !aligned_16(a.o) || !aligned_16(a.w_o) || !aligned_16(a.w1) || !aligned_16(a.w2) ||
+      !aligned_16(a.b1))
+    return hipErrorInvalidValue;
+  if (a.w_qkv && (!a.b_qkv || !a.qkv_out || a.ldq < 3 * a.d || !aligned_16(a.w_qkv) || !aligned_16(a.b_qkv)))
+    return hipErrorInvalidValue;
   if (a.w_out && (!a.b_out || !a.logits || !a.lse || a.n_dev < 1 || a.n_dev > kFusedHeadDevices || a.w_qkv))
     return hipErrorInvalidValue;
   dim3 grid((a.M + LBM - 1) / LBM), block(LNT);
@@ -661,19 +736,12 @@ template hipError_t launch_post_attention<bf16>(const PostAttnArgs<bf16>&, const
 template <typename T, int D>
 __global__ __launch_bounds__(LNT) void k_pre_layer(PreLayerArgs<T> p, GraphTable gt) {
   using G = Geo<T, D>;
-  __shared__ __attribute__((aligned(16))) char smem[G::TOTAL];
-  Lanes ln;
-  ln.lane = threadIdx.x & 63;
-  ln.wave = threadIdx.x >> 6;
-  ln.col = ln.lane & 15;
-  ln.g4 = ln.lane >> 4;
-  ln.p1m = ln.wave / G::P1N;
-  ln.p1n = ln.wave % G::P1N;
-  ln.w2m = ln.wave / G::WN2;
-  ln.w2n = ln.wave % G::WN2;
+  GDP_LAYER_LDS(T, G);
+  const Lanes ln = make_lanes<T, D>();
   const int m0 = blockIdx.x * LBM;
   const int rbase = ln.w2m * G::MB2 * 16 + ln.col;
   const int cbase = ln.w2n * G::NB2 * 16 + 4 * ln.g4;
+  if constexpr (G::NZ == 2) dma_qkv_chunk<T, D, 0>(L, p.w_qkv, p.b_qkv, 0);
   typename G::RowAcc acc;
 #pragma unroll
   for (int i = 0; i < G::MB2; ++i) {
@@ -699,13 +767,14 @@ __global__ __launch_bounds__(LNT) void k_pre_layer(PreLayerArgs<T> p, GraphTable
     }
   }
   typename G::ActFrags af;
-  qkv_phase<T, D>(acc, smem, af, ln, m0, p.M, p.w_qkv, p.b_qkv, p.qkv_out, p.ldq, p.q_scale);
+  qkv_phase<T, D, 0>(acc, L, af, ln, m0, p.M, p.w_qkv, p.b_qkv, p.qkv_out, p.ldq, p.q_scale);
 }
 
 template <typename T>
 hipError_t launch_pre_layer(const PreLayerArgs<T>& a, const GraphTable& gt, hipStream_t s) {
   if (a.M <= 0) return hipSuccess;
   if (!a.x || !a.y_out || !a.w_qkv || !a.b_qkv || !a.qkv_out || a.ldq < 3 * a.d) return hipErrorInvalidValue;
+  if (!aligned_16(a.w_qkv) || !aligned_16(a.b_qkv)) return hipErrorInvalidValue;
   dim3 grid((a.M + LBM - 1) / LBM), block(LNT);
   switch (a.d) {
     case 64: hipLaunchKernelGGL((k_pre_layer<T, 64>), grid, block, 0, s, a, gt); break;

@@ -2,8 +2,8 @@
 
 The GEMM stages ROWS x BK tiles in 16-byte chunks; every K segment is tiled
 on its own and chunks at or past the segment end are never read.  The
-post-attention layer kernel stages weight and activation chunks of FC units
-in 16-byte pieces spread over its 512 threads.  These tests replay both (the
+post-attention layer kernel moves weight and activation chunks of FC units
+to LDS by direct loads into XOR-swizzled tiles.  These tests replay both (the
 same constants as the kernels) for every call each workload issues and check
 that every read lands inside its matrix and that every element is covered
 exactly once."""
@@ -78,79 +78,176 @@ def test_xcd_remap_is_a_bijection_with_contiguous_runs(total):
 
 
 # ---- post-attention layer kernel ------------------------------------------------
-LAYER_FC = {"bf16": 64, "f32": 32}      # FFN, W_o and QKV chunks
-LAYER_FCQ = LAYER_FC
+# Operands reach LDS by direct global -> LDS loads: load i of wave w writes
+# the 64 lanes' 16-byte granules to tile granules (w * PER + i) * 64 + lane,
+# and granule g of tile row r sits at granule g ^ key(r) of that row.
+LAYER_FC = {"bf16": 64, "f32": 32}      # units per chunk (FFN, W_o and QKV)
 LAYER_RB1 = {"bf16": 2, "f32": 1}       # unit-tiling row blocks per wave
+LAYER_MFMA_K = {"bf16": 32, "f32": 4}
 LAYER_ROWS = 128
 LAYER_THREADS = 512
 LAYER_WAVES = 8
+EB = {"bf16": 2, "f32": 4}
 
 
-def _stage_reads(rows, cols, elem_bytes, base, ld, rows_valid=None):
-    """Element offsets read by Stage<T, rows, cols>.load(base, ld, rows_valid)."""
-    epv = 16 // elem_bytes
-    cpr = cols // epv
-    chunks = rows * cpr
-    per = -(-chunks // LAYER_THREADS)
-    rv = rows if rows_valid is None else rows_valid
+def _key(gpr, r):
+    if gpr >= 16:
+        return r & 15
+    if gpr == 8:
+        return (r & 7) ^ ((r >> 3) & 1)
+    assert gpr == 4
+    return ((r >> 2) ^ (r >> 1)) & 3
+
+
+def _swz(cols, epv, r, c):
+    return r * cols + ((c // epv) ^ _key(cols // epv, r)) * epv + c % epv
+
+
+def _dma_tile(rows, cols, eb, ld, row_max):
+    """(tile element offset, source element offset) of every element moved by
+    dma_tile<T, rows, cols>(tile, src, ld, row_max)."""
+    epv = 16 // eb
+    gpr = cols // epv
+    granules = rows * gpr
+    assert granules % LAYER_THREADS == 0
+    per = granules // LAYER_THREADS
     out = []
-    for t in range(LAYER_THREADS):
+    for wave in range(LAYER_WAVES):
         for i in range(per):
-            q = t + i * LAYER_THREADS
-            if q < chunks and q // cpr < rv:
-                out.append((base + (q // cpr) * ld + (q % cpr) * epv, epv))
+            q = (wave * per + i) * 64
+            for lane in range(64):
+                p = q + lane
+                r = p // gpr
+                g = (p % gpr) ^ _key(gpr, r)
+                rs = min(r, row_max)
+                off_bytes = (rs * ld + g * epv) * eb
+                assert 0 <= off_bytes < 2 ** 32
+                for e in range(epv):
+                    out.append((p * epv + e, rs * ld + g * epv + e, r, g * epv + e))
     return out
 
 
-def _check_cover(reads, size, expect):
-    seen = []
-    for off, n in reads:
-        assert 0 <= off and off + n <= size, (off, n, size)
-        seen.extend(range(off, off + n))
-    assert sorted(seen) == sorted(expect)
-
-
-def _lane_bias_units(dtype, fcx):
-    """Units u0 + 16 j + [0, 4) each lane reads from a chunk's biases."""
-    rb1 = LAYER_RB1[dtype]
+def _geo(dtype, d):
+    fc, rb1, k = LAYER_FC[dtype], LAYER_RB1[dtype], LAYER_MFMA_K[dtype]
     p1m = LAYER_ROWS // (16 * rb1)
     p1n = LAYER_WAVES // p1m
-    hpw = fcx // p1n
-    units = set()
+    nz = LAYER_ROWS // fc
+    return dict(fc=fc, rb1=rb1, k=k, p1m=p1m, p1n=p1n, hpw=fc // p1n, buf=fc * max(d, LAYER_ROWS), nz=nz, zc=d // nz,
+                epv=16 // EB[dtype], mb2=LAYER_ROWS // 2 // 16, nb2=d // 4 // 16)
+
+
+def _check_tile(rows, cols, dtype, d, ld, src_rows, row_max=None):
+    """The DMA of a rows x cols tile writes every tile element exactly once,
+    inside the staging buffer, with the source element that swz() reads there."""
+    g = _geo(dtype, d)
+    eb, epv = EB[dtype], g["epv"]
+    row_max = rows - 1 if row_max is None else row_max
+    moved = _dma_tile(rows, cols, eb, ld, row_max)
+    dst = [m[0] for m in moved]
+    assert sorted(dst) == list(range(rows * cols))
+    assert rows * cols <= g["buf"]
+    for t, srcoff, r, c in moved:
+        assert _swz(cols, epv, r, c) == t
+        assert 0 <= srcoff < src_rows * ld
+        assert srcoff == min(r, row_max) * ld + c
+    return moved
+
+
+@pytest.mark.parametrize("d", [64, 128, 256])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_layer_kernel_dma_tiles(d, dtype):
+    g = _geo(dtype, d)
+    fc = g["fc"]
+    dff = 4 * d
+    # W_1 / W_qkv chunk: fc rows x d (ld d); W_2 / W_o chunk: d rows x fc (ld d_ff / d)
+    _check_tile(fc, d, dtype, d, d, fc)
+    for ld in (dff, d):
+        _check_tile(d, fc, dtype, d, ld, d)
+    # O chunk: 128 rows x fc of an [M, d] matrix; a ragged last block clamps rows
+    for rows_valid in (128, 100, 1):
+        moved = _check_tile(LAYER_ROWS, fc, dtype, d, d, rows_valid, row_max=rows_valid - 1)
+        assert {r for _, _, r, _ in moved if r < rows_valid} == set(range(rows_valid))
+    # every chunk of W_1, W_2, W_qkv, W_o covers its matrix exactly once
+    for total_rows in (dff, 3 * d):
+        cover = []
+        for c in range(total_rows // fc):
+            cover += [c * fc * d + s for _, s, _, _ in _dma_tile(fc, d, EB[dtype], d, fc - 1)]
+        assert sorted(cover) == list(range(total_rows * d))
+    for kt in (dff, d):
+        cover = []
+        for c in range(kt // fc):
+            cover += [c * fc + s for _, s, _, _ in _dma_tile(d, fc, EB[dtype], kt, d - 1)]
+        assert sorted(cover) == list(range(d * kt))
+
+
+@pytest.mark.parametrize("gpr", [4, 8, 16, 32, 64])
+def test_layer_swizzle_is_bank_conflict_free(gpr):
+    """A fragment load reads one granule from each of 16 consecutive rows: the
+    16 (and any 8 aligned) land in distinct 16-byte bank groups."""
+    for r0 in range(0, 64, 16):
+        for gl in range(gpr):
+            pos = [(r * gpr + (gl ^ _key(gpr, r))) for r in range(r0, r0 + 16)]
+            assert len({p % 16 for p in pos}) == 16 or gpr < 16 and len({p % 16 for p in pos}) == 16
+            for h in (0, 8):
+                assert len({p % 8 for p in pos[h:h + 8]}) == 8
+    for r in range(64):
+        assert sorted(gl ^ _key(gpr, r) for gl in range(gpr)) == list(range(gpr))
+
+
+@pytest.mark.parametrize("d", [64, 128, 256])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_layer_kernel_lds_reads_in_range(d, dtype):
+    g = _geo(dtype, d)
+    fc, k, epv, zc = g["fc"], g["k"], g["epv"], g["zc"]
+    kv = k // 4
+    ks1, ks2 = d // k, fc // k
+    assert ks1 >= 1 and ks2 >= 1 and d % fc == 0 and zc % k == 0 and zc % (d // 4) == 0
+    jb1 = g["hpw"] // 16
     for wave in range(LAYER_WAVES):
+        p1m, p1n = wave // g["p1n"], wave % g["p1n"]
+        w2m, w2n = wave // 4, wave % 4
+        zpart = w2n * g["nb2"] * 16 // zc
+        assert zpart < g["nz"]
         for lane in range(64):
-            u0 = (wave % p1n) * hpw + 4 * (lane >> 4)
-            for j in range(hpw // 16):
-                units.update(range(u0 + 16 * j, u0 + 16 * j + 4))
-    return units
+            col, g4 = lane & 15, lane >> 4
+            # unit tiling: weight rows (units) x k in an fc x d tile; bias units
+            for j in range(jb1):
+                u = p1n * g["hpw"] + j * 16 + col
+                assert u < fc
+                for s in range(ks1):
+                    assert 0 <= _swz(d, epv, u, s * k + kv * g4) < fc * d
+                hc = p1n * g["hpw"] + j * 16 + 4 * g4
+                assert hc + 4 <= fc and hc % epv + 4 <= epv       # H store within a granule
+                for i in range(g["rb1"]):
+                    assert 0 <= _swz(fc, epv, (p1m * g["rb1"] + i) * 16 + col, hc) < LAYER_ROWS * fc
+            # activation parts (128 x zc, one staging buffer each): writes and reads
+            assert LAYER_ROWS * zc <= g["buf"]
+            for i in range(g["mb2"]):
+                for j in range(g["nb2"]):
+                    c = w2n * g["nb2"] * 16 + 4 * g4 + j * 16 - zpart * zc
+                    assert 0 <= c and c + 4 <= zc and c % epv + 4 <= epv
+                    assert _swz(zc, epv, w2m * g["mb2"] * 16 + col + i * 16, c) < LAYER_ROWS * zc
+            for i in range(g["rb1"]):
+                for s in range(ks1):
+                    z = s * k // zc
+                    cc = s * k - z * zc + kv * g4
+                    assert z < g["nz"] and 0 <= cc < zc
+                    assert _swz(zc, epv, (p1m * g["rb1"] + i) * 16 + col, cc) < LAYER_ROWS * zc
+            # row tiling: A (128 x fc) and W (d x fc) fragments
+            for s in range(ks2):
+                for i in range(g["mb2"]):
+                    assert _swz(fc, epv, w2m * g["mb2"] * 16 + i * 16 + col, s * k + kv * g4) < LAYER_ROWS * fc
+                for j in range(g["nb2"]):
+                    assert _swz(fc, epv, w2n * g["nb2"] * 16 + j * 16 + col, s * k + kv * g4) < d * fc
+    # LDS budget: 4 staging buffers + H + 2 bias chunks + LayerNorm sums
+    total = (4 * g["buf"] + LAYER_ROWS * fc + 2 * fc) * EB[dtype] + LAYER_ROWS * 4 * 4
+    assert total <= 160 * 1024
 
 
 @pytest.mark.parametrize("name", W.CONFIG_ORDER)
-@pytest.mark.parametrize("dtype", ["f32", "bf16"])
-def test_layer_kernel_staging_stays_in_bounds(name, dtype):
-    cfg = W.get_config(name).replace(dtype=dtype)
-    d, dff, eb = cfg.d_model, cfg.d_ff, (2 if dtype == "bf16" else 4)
-    fc, fcq = LAYER_FC[dtype], LAYER_FCQ[dtype]
-    assert d % fc == 0 and dff % fc == 0 and (3 * d) % fcq == 0
-    # W_1 [dff, d] in chunks of fc rows, W_qkv [3d, d] in chunks of fcq rows
-    for rows_total, step in ((dff, fc), (3 * d, fcq)):
-        reads = []
-        for c in range(rows_total // step):
-            reads += _stage_reads(step, d, eb, c * step * d, d)
-        _check_cover(reads, rows_total * d, range(rows_total * d))
-    # W_2 [d, dff] and W_o [d, d]: all d rows x columns [c fc, c fc + fc)
-    for k_total in (dff, d):
-        reads = []
-        for c in range(k_total // fc):
-            reads += _stage_reads(d, fc, eb, c * fc, k_total)
-        _check_cover(reads, d * k_total, range(d * k_total))
-    # O [M, d]: block m0 = rows [m0, m0 + 128) (rows >= M not read) x column chunks
-    M = 300 if cfg.n_nodes > 300 else cfg.n_nodes
-    reads = []
-    for m0 in range(0, M, LAYER_ROWS):
-        for c in range(d // fc):
-            reads += _stage_reads(LAYER_ROWS, fc, eb, m0 * d + c * fc, d, rows_valid=M - m0)
-    _check_cover(reads, M * d, range(M * d))
-    # biases: every lane's 4-unit pieces cover each chunk exactly within its range
-    assert _lane_bias_units(dtype, fc) == set(range(fc))
-    assert _lane_bias_units(dtype, fcq) == set(range(fcq))
+def test_layer_kernel_accepts_workload_shapes(name):
+    cfg = W.get_config(name)
+    for dtype in ("f32", "bf16"):
+        fc = LAYER_FC[dtype]
+        assert cfg.d_ff % (2 * fc) == 0 and cfg.d_model % fc == 0
+        assert cfg.d_model in (64, 128, 256)
