@@ -114,41 +114,71 @@ __device__ __forceinline__ gptr_t uniform_base(const void* p) {
 #pragma clang diagnostic push
 #pragma clang diagnostic ignored "-Winline-asm"
 __device__ __forceinline__ void dma16(gptr_t base, uint32_t voff, const void* lds) {
-  const uint32_t la = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)lds;
+  const uint32_t la = (uint32_t)(uintptr_t)lds;   // a generic LDS address's low word is the LDS offset
   asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
                :: "v"(voff), "s"(base), "s"(__builtin_amdgcn_readfirstlane(la)) : "memory", "m0");
 }
 #pragma clang diagnostic pop
 
 // ROWS x COLS block of a row-major matrix (leading dimension ld; rows beyond
-// row_max read row row_max) into a swizzled LDS tile.  Load i of wave w fills
-// tile granules [(w * PER + i) * 64, + 64), lane l the granule at offset l.
+// row_max read row row_max) into a swizzled LDS tile, in DmaTile::PER loads
+// per wave.  Load i of wave w fills tile granules [(w * PER + i) * 64, + 64),
+// lane l the granule at offset l.
+template <typename T, int ROWS, int COLS>
+struct DmaTile {
+  static constexpr int EPV = 16 / sizeof(T);
+  static constexpr int GPR = COLS / EPV;
+  static constexpr int GRANULES = ROWS * GPR;
+  static_assert(GRANULES % LNT == 0, "tile must split evenly over the work-group");
+  static_assert(GPR >= 4 && GPR <= 64, "a load covers whole rows or one row");
+  static constexpr int PER = GRANULES / LNT;
+  T* tile;
+  gptr_t base;
+  int ld, row_max;
+  __device__ __forceinline__ DmaTile(T* tile_, const T* src, int ld_, int row_max_)
+      : tile(tile_), base(uniform_base(src)), ld(ld_), row_max(row_max_) {}
+  // A load covers 64 / GPR whole rows from rb = q / GPR on (rb aligned to
+  // that count), so lane l handles row rb + l / GPR, granule l % GPR, and
+  // swz_key(rb + l / GPR) = swz_key(rb) ^ swz_key(l / GPR): the row base and
+  // its key are wave-uniform, the rest a per-lane constant.
+  template <bool CLAMP>
+  __device__ __forceinline__ void piece(int i) const {
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int lane = threadIdx.x & 63;
+    const int q = (wave * PER + i) * 64;
+    const int rb = q / GPR;
+    const int lr = lane / GPR;
+    const int g = (lane % GPR) ^ swz_key<GPR>(lr) ^ swz_key<GPR>(rb);
+    int r0 = rb, rel = lr;
+    if (CLAMP) {
+      r0 = rb < row_max ? rb : row_max;
+      rel = (rb + lr < row_max ? rb + lr : row_max) - r0;
+    }
+    const uint32_t off = ((uint32_t)rel * (uint32_t)ld + (uint32_t)(g * EPV)) * (uint32_t)sizeof(T);
+    dma16(base + (size_t)r0 * ld * sizeof(T), off, tile + q * EPV);
+  }
+  __device__ __forceinline__ void piece(int i) const { piece<false>(i); }
+  template <bool CLAMP = false>
+  __device__ __forceinline__ void all() const {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) piece<CLAMP>(i);
+  }
+};
+
+// Rows beyond row_max are read as row row_max (a ragged block of O); weight
+// tiles are whole.
 template <typename T, int ROWS, int COLS>
 __device__ __forceinline__ void dma_tile(T* tile, const T* src, int ld, int row_max) {
-  constexpr int EPV = 16 / sizeof(T);
-  constexpr int GPR = COLS / EPV;
-  constexpr int GRANULES = ROWS * GPR;
-  static_assert(GRANULES % LNT == 0, "tile must split evenly over the work-group");
-  constexpr int PER = GRANULES / LNT;
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
-  const gptr_t base = uniform_base(src);
-#pragma unroll
-  for (int i = 0; i < PER; ++i) {
-    const int q = (wave * PER + i) * 64;
-    const int p = q + lane;
-    const int r = p / GPR;
-    const int g = (p % GPR) ^ swz_key<GPR>(r);
-    const int rs = r < row_max ? r : row_max;
-    const uint32_t off = ((uint32_t)rs * (uint32_t)ld + (uint32_t)(g * EPV)) * (uint32_t)sizeof(T);
-    dma16(base, off, tile + q * EPV);
-  }
+  if (row_max < ROWS - 1) DmaTile<T, ROWS, COLS>(tile, src, ld, row_max).template all<true>();
+  else DmaTile<T, ROWS, COLS>(tile, src, ld, row_max).template all<false>();
 }
 
-// FC biases of a chunk (FC * sizeof(T) = 128 bytes) by the first lanes of wave 0.
-template <typename T, int FC>
+// UNITS biases of a chunk (a multiple of 16 bytes, at most 1 KB) by the first lanes of wave 0.
+template <typename T, int UNITS>
 __device__ __forceinline__ void dma_bias(T* lds, const T* b) {
   constexpr int EPV = 16 / sizeof(T);
-  if (threadIdx.x < FC / EPV) dma16(uniform_base(b), threadIdx.x * 16, lds);
+  static_assert(UNITS % EPV == 0 && UNITS / EPV <= 64, "bias chunk");
+  if (threadIdx.x < UNITS / EPV) dma16(uniform_base(b), threadIdx.x * 16, lds);
 }
 
 // Barrier after which the data of every direct load issued before it by any
@@ -204,7 +234,13 @@ struct Geo {
   static constexpr int MB2 = LBM / WM2 / 16;
   static constexpr int NB2 = D / WN2 / 16;
   static constexpr int NK0 = D / FC;              // phase-0 chunks
-  static constexpr int NQ = 3 * D / FC;           // QKV chunks
+  // QKV chunks of FCQ = QH * FC units, half h of a chunk in the u (h = 0) or
+  // r (h = 1) buffer of its parity; a unit-tiling wave covers one half.
+  static constexpr int QH = P1N == 2 && (3 * D) % (2 * FC) == 0 ? 2 : 1;
+  static constexpr int FCQ = QH * FC;
+  static constexpr int NQ = 3 * D / FCQ;
+  static constexpr int HPWQ = FCQ / P1N;
+  static constexpr int JBQ = HPWQ / 16;
   // elements of a staging buffer: a weight chunk (FC x D or D x FC) or an O chunk (LBM x FC)
   static constexpr int BUF = FC * (D > LBM ? D : LBM);
   // At a switch from the row to the unit tiling the activation passes through
@@ -215,11 +251,14 @@ struct Geo {
   static_assert(D % FC == 0 && (NZ == 2 || NZ == 4) && ZC % MF::K == 0, "tile shapes");
   static_assert(ZC % (D / WN2) == 0, "a row-tiling wave writes within one part");
   static_assert(FC * D <= BUF && LBM * FC <= BUF && LBM * ZC <= BUF, "every staged tile fits a buffer");
-  typedef f32x4 UnitAcc[RB1][JB1];                       // unit-tiling accumulators
+  static_assert(QH == 1 || HPWQ == FC, "a wave's QKV units lie in one half");
+  static_assert(D % FCQ == 0, "a QKV chunk lies wholly in q, k or v");
+  typedef f32x4 UnitAcc[RB1][JB1];                       // unit-tiling accumulators (FFN)
+  typedef f32x4 UnitAccQ[RB1][JBQ];                      // (QKV)
   typedef f32x4 RowAcc[MB2][NB2];                        // row-tiling accumulators
   typedef typename MF::frag ActFrags[RB1][KS1];          // unit-tiling activation fragments
   typedef float Red[WN2];
-  static constexpr int LDS_BYTES = (4 * BUF + LBM * FC + 2 * FC) * (int)sizeof(T) + LBM * WN2 * (int)sizeof(float);
+  static constexpr int LDS_BYTES = (4 * BUF + LBM * FC + 2 * FCQ) * (int)sizeof(T) + LBM * WN2 * (int)sizeof(float);
   static_assert(LDS_BYTES <= 160 * 1024, "LDS budget");
 };
 
@@ -240,8 +279,8 @@ struct Lds {
   __shared__ __attribute__((aligned(16))) T lds_u1_[G::BUF];               \
   __shared__ __attribute__((aligned(16))) T lds_r0_[G::BUF];               \
   __shared__ __attribute__((aligned(16))) T lds_r1_[G::BUF];               \
-  __shared__ __attribute__((aligned(16))) T lds_b0_[G::FC];                \
-  __shared__ __attribute__((aligned(16))) T lds_b1_[G::FC];                \
+  __shared__ __attribute__((aligned(16))) T lds_b0_[G::FCQ];               \
+  __shared__ __attribute__((aligned(16))) T lds_b1_[G::FCQ];               \
   __shared__ __attribute__((aligned(16))) T lds_h_[LBM * G::FC];           \
   __shared__ __attribute__((aligned(16))) float lds_red_[LBM * G::WN2];    \
   const Lds<T> L{lds_u0_, lds_u1_, lds_r0_, lds_r1_, lds_b0_, lds_b1_, lds_h_, lds_red_}
@@ -268,36 +307,41 @@ __device__ __forceinline__ Lanes make_lanes() {
   return ln;
 }
 
-// unit tiling: hacc[i][j] = W_c(units p1n*HPW + j*16 + ..) x act(rows (p1m*RB1 + i)*16 + ..)^T,
+// unit tiling: hacc[i][j] = W_c(tile rows u0 + j*16 + ..) x act(rows (p1m*RB1 + i)*16 + ..)^T,
 // W_c a swizzled FC x D tile.  The fragments of k step s + 1 are requested
 // before the MFMAs of step s issue.
-template <typename T, int D>
-__device__ __forceinline__ void unit_mma(typename Geo<T, D>::UnitAcc& hacc, const typename Geo<T, D>::ActFrags& af,
-                                         const T* sW, const Lanes& ln) {
+// after_step(s) runs once the MFMAs of k step s are issued, so that work
+// placed there (issuing the next chunk's loads) executes in their shadow.
+template <typename T, int D, int JB>
+using UnitAccJ = f32x4[Geo<T, D>::RB1][JB];
+
+template <typename T, int D, int JB, typename Hook>
+__device__ __forceinline__ void unit_mma(UnitAccJ<T, D, JB>& hacc, const typename Geo<T, D>::ActFrags& af,
+                                         const T* sW, int u0, const Lanes& ln, Hook&& after_step) {
   using G = Geo<T, D>;
   using MF = Mfma<T>;
-  typename MF::frag bw[2][G::JB1];
+  typename MF::frag bw[2][JB];
 #pragma unroll
   for (int i = 0; i < G::RB1; ++i)
 #pragma unroll
-    for (int j = 0; j < G::JB1; ++j) hacc[i][j] = zero4();
+    for (int j = 0; j < JB; ++j) hacc[i][j] = zero4();
 #pragma unroll
-  for (int j = 0; j < G::JB1; ++j)
-    bw[0][j] = MF::load(&sW[swz<T, D>(ln.p1n * G::HPW + j * 16 + ln.col, MF::KV * ln.g4)]);
+  for (int j = 0; j < JB; ++j)
+    bw[0][j] = MF::load(&sW[swz<T, D>(u0 + j * 16 + ln.col, MF::KV * ln.g4)]);
 #pragma unroll
   for (int s = 0; s < G::KS1; ++s) {
     if (s + 1 < G::KS1) {
 #pragma unroll
-      for (int j = 0; j < G::JB1; ++j)
-        bw[(s + 1) & 1][j] =
-            MF::load(&sW[swz<T, D>(ln.p1n * G::HPW + j * 16 + ln.col, (s + 1) * MF::K + MF::KV * ln.g4)]);
+      for (int j = 0; j < JB; ++j)
+        bw[(s + 1) & 1][j] = MF::load(&sW[swz<T, D>(u0 + j * 16 + ln.col, (s + 1) * MF::K + MF::KV * ln.g4)]);
     }
     __builtin_amdgcn_sched_barrier(0);   // keep the prefetch ahead of this step's MFMAs
 #pragma unroll
-    for (int j = 0; j < G::JB1; ++j)
+    for (int j = 0; j < JB; ++j)
 #pragma unroll
       for (int i = 0; i < G::RB1; ++i) hacc[i][j] = MF::mma(bw[s & 1][j], af[i][s], hacc[i][j]);
     __builtin_amdgcn_sched_barrier(0);
+    after_step(s);
   }
 }
 
@@ -444,13 +488,48 @@ __device__ __forceinline__ void to_unit_tiling(const typename Geo<T, D>::RowAcc&
   if constexpr (G::NZ == 4) bar_lds();
 }
 
-// Chunk q of the QKV projection (FC output units of W_qkv) into the buffers
-// of parity P.
-template <typename T, int D, int P>
-__device__ __forceinline__ void dma_qkv_chunk(const Lds<T>& L, const T* w_qkv, const T* b_qkv, int q) {
+template <bool C, typename A, typename B> struct Pick { typedef A type; };
+template <typename A, typename B> struct Pick<false, A, B> { typedef B type; };
+
+// The loads of one chunk, all at once (all()) or spread over the k steps of a
+// unit-tiling product (step()): tile A (FC x D), an optional tile B (D x FC
+// when BT = 1, FC x D when BT = 2) and BU biases.
+template <typename T, int D, int BT, int BU>
+struct ChunkDma {
   using G = Geo<T, D>;
-  dma_tile<T, G::FC, D>(L.template u<P>(), w_qkv + (size_t)q * G::FC * D, D, G::FC - 1);
-  dma_bias<T, G::FC>(L.template b<P>(), b_qkv + q * G::FC);
+  using TA = DmaTile<T, G::FC, D>;
+  using TB = typename Pick<BT == 1, DmaTile<T, D, G::FC>, DmaTile<T, G::FC, D>>::type;
+  static constexpr int NA = TA::PER, NB = BT ? TB::PER : 0, N = NA + NB + 1;
+  TA ta;
+  TB tb;
+  T* bias_lds;
+  const T* bias;
+  __device__ __forceinline__ ChunkDma(T* a, const T* wa, T* b, const T* wb, int ldb, T* b_lds, const T* bsrc)
+      : ta(a, wa, D, G::FC - 1), tb(b, wb, ldb, BT == 1 ? D - 1 : G::FC - 1), bias_lds(b_lds), bias(bsrc) {}
+  __device__ __forceinline__ void piece(int k) const {
+    if (k < NA) ta.piece(k);
+    else if (k < NA + NB) tb.piece(k - NA);
+    else dma_bias<T, BU>(bias_lds, bias);
+  }
+  __device__ __forceinline__ void step(int s) const {
+#pragma unroll
+    for (int k = s * N / G::KS1; k < (s + 1) * N / G::KS1; ++k) piece(k);
+  }
+  __device__ __forceinline__ void all() const {
+#pragma unroll
+    for (int k = 0; k < N; ++k) piece(k);
+  }
+};
+
+// Loads of QKV chunk q (units q*FCQ .. + FCQ of W_qkv and b_qkv) into the
+// buffers of parity P.
+template <typename T, int D, int P>
+__device__ __forceinline__ ChunkDma<T, D, Geo<T, D>::QH == 2 ? 2 : 0, Geo<T, D>::FCQ> qkv_chunk(
+    const Lds<T>& L, const T* w_qkv, const T* b_qkv, int q) {
+  using G = Geo<T, D>;
+  const T* w = w_qkv + (size_t)q * G::FCQ * D;
+  return ChunkDma<T, D, G::QH == 2 ? 2 : 0, G::FCQ>(L.template u<P>(), w, L.template r<P>(), w + (size_t)G::FC * D, D,
+                                                     L.template b<P>(), b_qkv + q * G::FCQ);
 }
 
 // QKV = act W_qkv^T + b_qkv for the work-group's rows, the activation in the
@@ -465,31 +544,54 @@ __device__ __forceinline__ void qkv_phase(const typename Geo<T, D>::RowAcc& acc,
   using G = Geo<T, D>;
   constexpr int FC = G::FC;
   to_unit_tiling<T, D, QP ^ 1>(acc, L, af, ln);
-  if constexpr (G::NZ == 4) dma_qkv_chunk<T, D, QP>(L, w_qkv, b_qkv, 0);
+  if constexpr (G::NZ == 4) qkv_chunk<T, D, QP>(L, w_qkv, b_qkv, 0).all();
+  constexpr int FCQ = G::FCQ, JB = G::JBQ;
+  // Chunk q's outputs stay in registers until after the barrier that opens
+  // chunk q + 1: that barrier waits for all of a wave's outstanding memory
+  // operations, stores included, and a store issued a chunk earlier has
+  // completed by then.
+  float out[G::RB1][JB][4];
+  int out_q = -1;
+  auto store_out = [&]() {
+    if (out_q < 0) return;
+#pragma unroll
+    for (int j = 0; j < JB; ++j) {
+      const int hc = ln.p1n * G::HPWQ + j * 16 + 4 * ln.g4;
+#pragma unroll
+      for (int i = 0; i < G::RB1; ++i) {
+        const int row = m0 + (ln.p1m * G::RB1 + i) * 16 + ln.col;
+        if (row < M) store4(qkv_out + (size_t)row * ldq + out_q * FCQ + hc, out[i][j]);
+      }
+    }
+  };
   chunk_pairs<QP, (G::NQ % 2) == 0>(G::NQ, [&](int q, auto pc) {
     constexpr int P = decltype(pc)::v;
     publish();                       // chunk q in place; chunk q - 1's buffers (and the parts) free
-    if (q + 1 < G::NQ) dma_qkv_chunk<T, D, P ^ 1>(L, w_qkv, b_qkv, q + 1);
-    typename G::UnitAcc hacc;
-    unit_mma<T, D>(hacc, af, L.template u<P>(), ln);
-    const float scale = q * FC < D ? q_scale : 1.0f;   // a chunk lies wholly in q, k or v
+    store_out();
+    const bool more = q + 1 < G::NQ;
+    const auto next = qkv_chunk<T, D, P ^ 1>(L, w_qkv, b_qkv, more ? q + 1 : q);
+    f32x4 hacc[G::RB1][JB];
+    // the wave's units: half p1n of the chunk (or a share of a one-buffer chunk)
+    const T* sW = G::QH == 2 && ln.p1n ? L.template r<P>() : L.template u<P>();
+    unit_mma<T, D, JB>(hacc, af, sW, G::QH == 2 ? 0 : ln.p1n * G::HPWQ, ln, [&](int s) {
+      if (more) next.step(s);
+    });
+    const float scale = q * FCQ < D ? q_scale : 1.0f;   // a chunk lies wholly in q, k or v
     const T* sB = L.template b<P>();
 #pragma unroll
-    for (int j = 0; j < G::JB1; ++j) {
-      const int hc = ln.p1n * G::HPW + j * 16 + 4 * ln.g4;
+    for (int j = 0; j < JB; ++j) {
+      const int hc = ln.p1n * G::HPWQ + j * 16 + 4 * ln.g4;
       float b[4];
 #pragma unroll
       for (int r = 0; r < 4; ++r) b[r] = to_f32(sB[hc + r]);
 #pragma unroll
-      for (int i = 0; i < G::RB1; ++i) {
-        const int row = m0 + (ln.p1m * G::RB1 + i) * 16 + ln.col;
-        float v[4];
+      for (int i = 0; i < G::RB1; ++i)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) v[r] = (hacc[i][j][r] + b[r]) * scale;
-        if (row < M) store4(qkv_out + (size_t)row * ldq + q * FC + hc, v);
-      }
+        for (int r = 0; r < 4; ++r) out[i][j][r] = (hacc[i][j][r] + b[r]) * scale;
     }
+    out_q = q;
   });
+  store_out();
 }
 
 // The placement head on the rows held in the row tiling (Fig. 1's N x d
@@ -629,12 +731,19 @@ __global__ __launch_bounds__(LNT) void k_post_attention(PostAttnArgs<T> p, Graph
   chunk_pairs<NK0 & 1, true>(NC, [&](int c, auto pc) {
     constexpr int P = decltype(pc)::v;
     publish();                       // chunk c in place; chunk c - 1's buffers, H and the parts free
-    if (c + 1 < NC) dma_ffn(c + 1, Par<P ^ 1>{});
-    else if constexpr (G::NZ == 2) {
-      if (qkv_next) dma_qkv_chunk<T, D, P ^ 1>(L, p.w_qkv, p.b_qkv, 0);
-    }
+    // during this chunk: FFN chunk c + 1, or after the last one the first
+    // QKV chunk (whose W_qkv tile has the W_1 tile's shape)
+    const bool more = c + 1 < NC;
+    const bool first_qkv = !more && G::NZ == 2 && qkv_next;
+    const int cn = more ? c + 1 : 0;
+    const ChunkDma<T, D, 1, FC> next_ffn(L.template u<P ^ 1>(), p.w1 + (size_t)cn * FC * D, L.template r<P ^ 1>(),
+                                         p.w2 + (size_t)cn * FC, p.d_ff, L.template b<P ^ 1>(), p.b1 + cn * FC);
+    const auto next_qkv = qkv_chunk<T, D, P ^ 1>(L, p.w_qkv, p.b_qkv, 0);
     typename G::UnitAcc hacc;
-    unit_mma<T, D>(hacc, af, L.template u<P>(), ln);
+    unit_mma<T, D, G::JB1>(hacc, af, L.template u<P>(), ln.p1n * G::HPW, ln, [&](int s) {
+      if (more) next_ffn.step(s);
+      else if (first_qkv) next_qkv.step(s);
+    });
     const T* sB = L.template b<P>();
     // lane holds hidden row (p1m * RB1 + i) * 16 + col, units hc + [0, 4)
 #pragma unroll
@@ -665,18 +774,31 @@ __global__ __launch_bounds__(LNT) void k_post_attention(PostAttnArgs<T> p, Graph
       for (int i = 0; i < G::MB2; ++i) acc[i][j][r] += b;
     }
   ln_rows<T, D>(acc, p.ln2_g, p.ln2_b, red, ln);
+  // FiLM gamma / beta of the lane's columns, loaded again only when a row
+  // belongs to another graph than the previous one
+  float4 fgm[G::NB2], fbt[G::NB2];
+  int gprev = -1;
 #pragma unroll
   for (int i = 0; i < G::MB2; ++i) {
     const int row = m0 + rbase + i * 16;
     if (p.film_gamma) {
-      const size_t g = (size_t)graph_of_node(gt, row < p.M ? row : p.M - 1) * p.film_stride;
+      const int gi = graph_of_node(gt, row < p.M ? row : p.M - 1);
+      if (gi != gprev) {
+        const size_t g = (size_t)gi * p.film_stride;
 #pragma unroll
-      for (int j = 0; j < G::NB2; ++j)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int cn = cbase + j * 16 + r;
-          acc[i][j][r] = p.film_gamma[g + cn] * acc[i][j][r] + p.film_beta[g + cn];
+        for (int j = 0; j < G::NB2; ++j) {
+          fgm[j] = *reinterpret_cast<const float4*>(p.film_gamma + g + cbase + j * 16);
+          fbt[j] = *reinterpret_cast<const float4*>(p.film_beta + g + cbase + j * 16);
         }
+        gprev = gi;
+      }
+#pragma unroll
+      for (int j = 0; j < G::NB2; ++j) {
+        acc[i][j][0] = fgm[j].x * acc[i][j][0] + fbt[j].x;
+        acc[i][j][1] = fgm[j].y * acc[i][j][1] + fbt[j].y;
+        acc[i][j][2] = fgm[j].z * acc[i][j][2] + fbt[j].z;
+        acc[i][j][3] = fgm[j].w * acc[i][j][3] + fbt[j].w;
+      }
     }
     if (p.y_out && row < p.M) {
 #pragma unroll
@@ -705,6 +827,8 @@ hipError_t launch_post_attention(const PostAttnArgs<T>& a, const GraphTable& gt,
   if (a.w_qkv && (!a.b_qkv || !a.qkv_out || a.ldq < 3 * a.d || !aligned_16(a.w_qkv) || !aligned_16(a.b_qkv)))
     return hipErrorInvalidValue;
   if (a.w_out && (!a.b_out || !a.logits || !a.lse || a.n_dev < 1 || a.n_dev > kFusedHeadDevices || a.w_qkv))
+    return hipErrorInvalidValue;
+  if (a.film_gamma && (!a.film_beta || a.film_stride % 4 || !aligned_16(a.film_gamma) || !aligned_16(a.film_beta)))
     return hipErrorInvalidValue;
   dim3 grid((a.M + LBM - 1) / LBM), block(LNT);
   const bool head = a.w_out != nullptr;
@@ -741,7 +865,7 @@ __global__ __launch_bounds__(LNT) void k_pre_layer(PreLayerArgs<T> p, GraphTable
   const int m0 = blockIdx.x * LBM;
   const int rbase = ln.w2m * G::MB2 * 16 + ln.col;
   const int cbase = ln.w2n * G::NB2 * 16 + 4 * ln.g4;
-  if constexpr (G::NZ == 2) dma_qkv_chunk<T, D, 0>(L, p.w_qkv, p.b_qkv, 0);
+  if constexpr (G::NZ == 2) qkv_chunk<T, D, 0>(L, p.w_qkv, p.b_qkv, 0).all();
   typename G::RowAcc acc;
 #pragma unroll
   for (int i = 0; i < G::MB2; ++i) {

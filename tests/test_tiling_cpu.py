@@ -104,26 +104,38 @@ def _swz(cols, epv, r, c):
 
 
 def _dma_tile(rows, cols, eb, ld, row_max):
-    """(tile element offset, source element offset) of every element moved by
-    dma_tile<T, rows, cols>(tile, src, ld, row_max)."""
+    """(tile element offset, source element offset, row, column) of every
+    element moved by dma_tile<T, rows, cols>(tile, src, ld, row_max), from the
+    kernel's split of each address into a wave-uniform row base and a per-lane
+    offset."""
     epv = 16 // eb
     gpr = cols // epv
     granules = rows * gpr
-    assert granules % LAYER_THREADS == 0
+    assert granules % LAYER_THREADS == 0 and 4 <= gpr <= 64
     per = granules // LAYER_THREADS
+    clamp = row_max < rows - 1
     out = []
     for wave in range(LAYER_WAVES):
         for i in range(per):
             q = (wave * per + i) * 64
+            rb = q // gpr
             for lane in range(64):
+                lr = lane // gpr
+                g = (lane % gpr) ^ _key(gpr, lr) ^ _key(gpr, rb)
+                # the split equals the plain per-granule formula
                 p = q + lane
-                r = p // gpr
-                g = (p % gpr) ^ _key(gpr, r)
-                rs = min(r, row_max)
-                off_bytes = (rs * ld + g * epv) * eb
+                assert p // gpr == rb + lr and g == (p % gpr) ^ _key(gpr, p // gpr)
+                r0, rel = rb, lr
+                if clamp:
+                    r0 = min(rb, row_max)
+                    rel = min(rb + lr, row_max) - r0
+                assert rel >= 0
+                off_bytes = (rel * ld + g * epv) * eb
                 assert 0 <= off_bytes < 2 ** 32
+                src_row = r0 + rel
+                assert src_row == min(rb + lr, row_max)
                 for e in range(epv):
-                    out.append((p * epv + e, rs * ld + g * epv + e, r, g * epv + e))
+                    out.append((p * epv + e, src_row * ld + g * epv + e, rb + lr, g * epv + e))
     return out
 
 
@@ -132,7 +144,8 @@ def _geo(dtype, d):
     p1m = LAYER_ROWS // (16 * rb1)
     p1n = LAYER_WAVES // p1m
     nz = LAYER_ROWS // fc
-    return dict(fc=fc, rb1=rb1, k=k, p1m=p1m, p1n=p1n, hpw=fc // p1n, buf=fc * max(d, LAYER_ROWS), nz=nz, zc=d // nz,
+    qh = 2 if (LAYER_WAVES // p1m) == 2 and (3 * d) % (2 * fc) == 0 else 1
+    return dict(qh=qh, fcq=qh * fc, hpwq=qh * fc // p1n, fc=fc, rb1=rb1, k=k, p1m=p1m, p1n=p1n, hpw=fc // p1n, buf=fc * max(d, LAYER_ROWS), nz=nz, zc=d // nz,
                 epv=16 // EB[dtype], mb2=LAYER_ROWS // 2 // 16, nb2=d // 4 // 16)
 
 
@@ -167,6 +180,14 @@ def test_layer_kernel_dma_tiles(d, dtype):
     for rows_valid in (128, 100, 1):
         moved = _check_tile(LAYER_ROWS, fc, dtype, d, d, rows_valid, row_max=rows_valid - 1)
         assert {r for _, _, r, _ in moved if r < rows_valid} == set(range(rows_valid))
+    # QKV chunks: FCQ = QH * FC units as QH tiles of FC rows; together they cover W_qkv once
+    cover = []
+    for q in range(3 * d // g["fcq"]):
+        for h in range(g["qh"]):
+            r0 = q * g["fcq"] + h * fc
+            cover += [r0 * d + s for _, s, _, _ in _dma_tile(fc, d, EB[dtype], d, fc - 1)]
+    assert sorted(cover) == list(range(3 * d * d))
+    assert d % g["fcq"] == 0            # a QKV chunk lies within q, k or v
     # every chunk of W_1, W_2, W_qkv, W_o covers its matrix exactly once
     for total_rows in (dff, 3 * d):
         cover = []
@@ -220,6 +241,14 @@ def test_layer_kernel_lds_reads_in_range(d, dtype):
                 assert hc + 4 <= fc and hc % epv + 4 <= epv       # H store within a granule
                 for i in range(g["rb1"]):
                     assert 0 <= _swz(fc, epv, (p1m * g["rb1"] + i) * 16 + col, hc) < LAYER_ROWS * fc
+            # QKV: the wave's units lie in one FC-row tile (its half of the chunk)
+            for j in range(g["hpwq"] // 16):
+                u0 = 0 if g["qh"] == 2 else p1n * g["hpwq"]
+                assert u0 + j * 16 + col < fc
+                hcq = p1n * g["hpwq"] + j * 16 + 4 * g4
+                assert hcq + 4 <= g["fcq"]
+                if g["qh"] == 2:
+                    assert hcq // fc == p1n           # bias entry of the wave's own half
             # activation parts (128 x zc, one staging buffer each): writes and reads
             assert LAYER_ROWS * zc <= g["buf"]
             for i in range(g["mb2"]):
@@ -240,7 +269,7 @@ def test_layer_kernel_lds_reads_in_range(d, dtype):
                 for j in range(g["nb2"]):
                     assert _swz(fc, epv, w2n * g["nb2"] * 16 + j * 16 + col, s * k + kv * g4) < d * fc
     # LDS budget: 4 staging buffers + H + 2 bias chunks + LayerNorm sums
-    total = (4 * g["buf"] + LAYER_ROWS * fc + 2 * fc) * EB[dtype] + LAYER_ROWS * 4 * 4
+    total = (4 * g["buf"] + LAYER_ROWS * fc + 2 * g["fcq"]) * EB[dtype] + LAYER_ROWS * 4 * 4
     assert total <= 160 * 1024
 
 
