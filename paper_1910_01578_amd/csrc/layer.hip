@@ -554,13 +554,37 @@ __device__ __forceinline__ void qkv_phase(const typename Geo<T, D>::RowAcc& acc,
   int out_q = -1;
   auto store_out = [&]() {
     if (out_q < 0) return;
-#pragma unroll
-    for (int j = 0; j < JB; ++j) {
-      const int hc = ln.p1n * G::HPWQ + j * 16 + 4 * ln.g4;
+    if constexpr (G::QH == 2) {
+      // The MFMA layout gives a lane 4 units of one row; a store instruction
+      // would write 16 rows x 32 bytes.  Each wave passes its 16-row blocks
+      // (64 units = 128 bytes a row) through its own 2 KB of H, read back as
+      // 16-byte pieces of 8 whole rows, and writes full 128-byte lines.  The
+      // region is the wave's own, so LDS program order is the only ordering.
+      constexpr int WU = G::HPWQ;                                  // 64 units a row
+      static_assert(kLayerWaves * 16 * WU <= LBM * G::FC && WU * sizeof(T) == 128, "per-wave staging in H");
+      T* reg = L.h + ln.wave * (16 * WU);
+      const int col0 = out_q * FCQ + ln.p1n * WU;
 #pragma unroll
       for (int i = 0; i < G::RB1; ++i) {
-        const int row = m0 + (ln.p1m * G::RB1 + i) * 16 + ln.col;
-        if (row < M) store4(qkv_out + (size_t)row * ldq + out_q * FCQ + hc, out[i][j]);
+#pragma unroll
+        for (int j = 0; j < JB; ++j) store4(&reg[swz<T, WU>(ln.col, j * 16 + 4 * ln.g4)], out[i][j]);
+        const int rblk = m0 + (ln.p1m * G::RB1 + i) * 16;
+#pragma unroll
+        for (int hf = 0; hf < 2; ++hf) {
+          const int rr = (ln.lane >> 3) + 8 * hf, gg = ln.lane & 7;
+          const uint4 v = *reinterpret_cast<const uint4*>(&reg[swz<T, WU>(rr, gg * 8)]);
+          if (rblk + rr < M) *reinterpret_cast<uint4*>(qkv_out + (size_t)(rblk + rr) * ldq + col0 + gg * 8) = v;
+        }
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < JB; ++j) {
+        const int hc = ln.p1n * G::HPWQ + j * 16 + 4 * ln.g4;
+#pragma unroll
+        for (int i = 0; i < G::RB1; ++i) {
+          const int row = m0 + (ln.p1m * G::RB1 + i) * 16 + ln.col;
+          if (row < M) store4(qkv_out + (size_t)row * ldq + out_q * FCQ + hc, out[i][j]);
+        }
       }
     }
   };
@@ -824,7 +848,8 @@ hipError_t launch_post_attention(const PostAttnArgs<T>& a, const GraphTable& gt,
   if (a.ldo % EPV || !aligned_16(a.o) || !aligned_16(a.w_o) || !aligned_16(a.w1) || !aligned_16(a.w2) ||
       !aligned_16(a.b1))
     return hipErrorInvalidValue;
-  if (a.w_qkv && (!a.b_qkv || !a.qkv_out || a.ldq < 3 * a.d || !aligned_16(a.w_qkv) || !aligned_16(a.b_qkv)))
+  if (a.w_qkv && (!a.b_qkv || !a.qkv_out || a.ldq < 3 * a.d || a.ldq % EPV || !aligned_16(a.w_qkv) ||
+                  !aligned_16(a.b_qkv) || !aligned_16(a.qkv_out)))
     return hipErrorInvalidValue;
   if (a.w_out && (!a.b_out || !a.logits || !a.lse || a.n_dev < 1 || a.n_dev > kFusedHeadDevices || a.w_qkv))
     return hipErrorInvalidValue;
@@ -898,7 +923,8 @@ template <typename T>
 hipError_t launch_pre_layer(const PreLayerArgs<T>& a, const GraphTable& gt, hipStream_t s) {
   if (a.M <= 0) return hipSuccess;
   if (!a.x || !a.y_out || !a.w_qkv || !a.b_qkv || !a.qkv_out || a.ldq < 3 * a.d) return hipErrorInvalidValue;
-  if (!aligned_16(a.w_qkv) || !aligned_16(a.b_qkv)) return hipErrorInvalidValue;
+  if (!aligned_16(a.w_qkv) || !aligned_16(a.b_qkv) || !aligned_16(a.qkv_out) || a.ldq % (16 / (int)sizeof(T)))
+    return hipErrorInvalidValue;
   dim3 grid((a.M + LBM - 1) / LBM), block(LNT);
   switch (a.d) {
     case 64: hipLaunchKernelGGL((k_pre_layer<T, 64>), grid, block, 0, s, a, gt); break;

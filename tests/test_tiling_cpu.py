@@ -280,3 +280,38 @@ def test_layer_kernel_accepts_workload_shapes(name):
         fc = LAYER_FC[dtype]
         assert cfg.d_ff % (2 * fc) == 0 and cfg.d_model % fc == 0
         assert cfg.d_model in (64, 128, 256)
+
+
+@pytest.mark.parametrize("d", [128, 256])
+def test_layer_qkv_store_transpose(d):
+    """bf16 QKV outputs pass through each wave's 2 KB of H: the 16 x 64 block a
+    wave writes (4 units a lane) is read back as 16-byte pieces of whole rows,
+    every (row, unit) exactly once and to its own global position."""
+    g = _geo("bf16", d)
+    assert g["qh"] == 2
+    wu, epv = g["hpwq"], 8
+    assert wu * 2 == 128 and LAYER_WAVES * 16 * wu <= LAYER_ROWS * g["fc"]
+    for wave in range(LAYER_WAVES):
+        p1n = wave % g["p1n"]
+        base = wave * 16 * wu
+        written = {}
+        for lane in range(64):
+            col, g4 = lane & 15, lane >> 4
+            for j in range(wu // 16):
+                u = j * 16 + 4 * g4
+                t = _swz(wu, epv, col, u)
+                assert u % epv + 4 <= epv
+                for e in range(4):
+                    written[base + t + e] = (col, u + e)
+        assert len(written) == 16 * wu
+        read = []
+        for hf in range(2):
+            for lane in range(64):
+                rr, gg = (lane >> 3) + 8 * hf, lane & 7
+                t = base + _swz(wu, epv, rr, gg * 8)
+                for e in range(8):
+                    row, unit = written[t + e]
+                    assert row == rr and unit == gg * 8 + e      # stored at column p1n*64 + gg*8 + e
+                    read.append((row, unit))
+        assert sorted(read) == sorted(written.values())
+        assert 0 <= base and base + 16 * wu <= LAYER_ROWS * g["fc"]
