@@ -121,17 +121,17 @@ __device__ __forceinline__ void dma16(gptr_t base, uint32_t voff, const void* ld
 #pragma clang diagnostic pop
 
 // ROWS x COLS block of a row-major matrix (leading dimension ld; rows beyond
-// row_max read row row_max) into a swizzled LDS tile, in DmaTile::PER loads
-// per wave.  Load i of wave w fills tile granules [(w * PER + i) * 64, + 64),
-// lane l the granule at offset l.
-template <typename T, int ROWS, int COLS>
+// row_max read row row_max) into a swizzled LDS tile, by waves 0 .. NW - 1
+// with DmaTile::PER loads each.  Load i of wave w fills tile granules
+// [(w * PER + i) * 64, + 64), lane l the granule at offset l.
+template <typename T, int ROWS, int COLS, int NW = kLayerWaves>
 struct DmaTile {
   static constexpr int EPV = 16 / sizeof(T);
   static constexpr int GPR = COLS / EPV;
   static constexpr int GRANULES = ROWS * GPR;
-  static_assert(GRANULES % LNT == 0, "tile must split evenly over the work-group");
+  static_assert(GRANULES % (64 * NW) == 0, "tile must split evenly over the loading waves");
   static_assert(GPR >= 4 && GPR <= 64, "a load covers whole rows or one row");
-  static constexpr int PER = GRANULES / LNT;
+  static constexpr int PER = GRANULES / (64 * NW);
   T* tile;
   gptr_t base;
   int ld, row_max;
@@ -493,12 +493,13 @@ template <typename A, typename B> struct Pick<false, A, B> { typedef B type; };
 
 // The loads of one chunk, all at once (all()) or spread over the k steps of a
 // unit-tiling product (step()): tile A (FC x D), an optional tile B (D x FC
-// when BT = 1, FC x D when BT = 2) and BU biases.
-template <typename T, int D, int BT, int BU>
+// when BT = 1, FC x D when BT = 2) and BU biases, issued by waves 0 .. NW - 1
+// (the callers' branch).
+template <typename T, int D, int BT, int BU, int NW = kLayerWaves>
 struct ChunkDma {
   using G = Geo<T, D>;
-  using TA = DmaTile<T, G::FC, D>;
-  using TB = typename Pick<BT == 1, DmaTile<T, D, G::FC>, DmaTile<T, G::FC, D>>::type;
+  using TA = DmaTile<T, G::FC, D, NW>;
+  using TB = typename Pick<BT == 1, DmaTile<T, D, G::FC, NW>, DmaTile<T, G::FC, D, NW>>::type;
   static constexpr int NA = TA::PER, NB = BT ? TB::PER : 0, N = NA + NB + 1;
   TA ta;
   TB tb;
@@ -522,15 +523,22 @@ struct ChunkDma {
 };
 
 // Loads of QKV chunk q (units q*FCQ .. + FCQ of W_qkv and b_qkv) into the
-// buffers of parity P.
-template <typename T, int D, int P>
-__device__ __forceinline__ ChunkDma<T, D, Geo<T, D>::QH == 2 ? 2 : 0, Geo<T, D>::FCQ> qkv_chunk(
+// buffers of parity P, by waves 0 .. NW - 1.
+template <typename T, int D, int P, int NW = kLayerWaves>
+__device__ __forceinline__ ChunkDma<T, D, Geo<T, D>::QH == 2 ? 2 : 0, Geo<T, D>::FCQ, NW> qkv_chunk(
     const Lds<T>& L, const T* w_qkv, const T* b_qkv, int q) {
   using G = Geo<T, D>;
   const T* w = w_qkv + (size_t)q * G::FCQ * D;
-  return ChunkDma<T, D, G::QH == 2 ? 2 : 0, G::FCQ>(L.template u<P>(), w, L.template r<P>(), w + (size_t)G::FC * D, D,
-                                                     L.template b<P>(), b_qkv + q * G::FCQ);
+  return ChunkDma<T, D, G::QH == 2 ? 2 : 0, G::FCQ, NW>(L.template u<P>(), w, L.template r<P>(), w + (size_t)G::FC * D,
+                                                         D, L.template b<P>(), b_qkv + q * G::FCQ);
 }
+
+// Waves issuing the loads spread over a product.  (Leaving them to waves 0-3,
+// so that each SIMD keeps one wave free of load stalls, measured slower.)
+constexpr int kDmaWaves = kLayerWaves;
+
+// wave index as a scalar (uniform) value
+__device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6); }
 
 // QKV = act W_qkv^T + b_qkv for the work-group's rows, the activation in the
 // row tiling in acc; the q columns are multiplied by q_scale.  Chunk q uses
@@ -593,12 +601,13 @@ __device__ __forceinline__ void qkv_phase(const typename Geo<T, D>::RowAcc& acc,
     publish();                       // chunk q in place; chunk q - 1's buffers (and the parts) free
     store_out();
     const bool more = q + 1 < G::NQ;
-    const auto next = qkv_chunk<T, D, P ^ 1>(L, w_qkv, b_qkv, more ? q + 1 : q);
+    const auto next = qkv_chunk<T, D, P ^ 1, kDmaWaves>(L, w_qkv, b_qkv, more ? q + 1 : q);
+    const bool loader = wave_id() < kDmaWaves;
     f32x4 hacc[G::RB1][JB];
     // the wave's units: half p1n of the chunk (or a share of a one-buffer chunk)
     const T* sW = G::QH == 2 && ln.p1n ? L.template r<P>() : L.template u<P>();
     unit_mma<T, D, JB>(hacc, af, sW, G::QH == 2 ? 0 : ln.p1n * G::HPWQ, ln, [&](int s) {
-      if (more) next.step(s);
+      if (more && loader) next.step(s);
     });
     const float scale = q * FCQ < D ? q_scale : 1.0f;   // a chunk lies wholly in q, k or v
     const T* sB = L.template b<P>();
@@ -760,13 +769,17 @@ __global__ __launch_bounds__(LNT) void k_post_attention(PostAttnArgs<T> p, Graph
     const bool more = c + 1 < NC;
     const bool first_qkv = !more && G::NZ == 2 && qkv_next;
     const int cn = more ? c + 1 : 0;
-    const ChunkDma<T, D, 1, FC> next_ffn(L.template u<P ^ 1>(), p.w1 + (size_t)cn * FC * D, L.template r<P ^ 1>(),
-                                         p.w2 + (size_t)cn * FC, p.d_ff, L.template b<P ^ 1>(), p.b1 + cn * FC);
-    const auto next_qkv = qkv_chunk<T, D, P ^ 1>(L, p.w_qkv, p.b_qkv, 0);
+    const ChunkDma<T, D, 1, FC, kDmaWaves> next_ffn(L.template u<P ^ 1>(), p.w1 + (size_t)cn * FC * D,
+                                                    L.template r<P ^ 1>(), p.w2 + (size_t)cn * FC, p.d_ff,
+                                                    L.template b<P ^ 1>(), p.b1 + cn * FC);
+    const auto next_qkv = qkv_chunk<T, D, P ^ 1, kDmaWaves>(L, p.w_qkv, p.b_qkv, 0);
+    const bool loader = wave_id() < kDmaWaves;
     typename G::UnitAcc hacc;
     unit_mma<T, D, G::JB1>(hacc, af, L.template u<P>(), ln.p1n * G::HPW, ln, [&](int s) {
-      if (more) next_ffn.step(s);
-      else if (first_qkv) next_qkv.step(s);
+      if (loader) {
+        if (more) next_ffn.step(s);
+        else if (first_qkv) next_qkv.step(s);
+      }
     });
     const T* sB = L.template b<P>();
     // lane holds hidden row (p1m * RB1 + i) * 16 + col, units hc + [0, 4)
@@ -824,11 +837,42 @@ __global__ __launch_bounds__(LNT) void k_post_attention(PostAttnArgs<T> p, Graph
         acc[i][j][3] = fgm[j].w * acc[i][j][3] + fbt[j].w;
       }
     }
-    if (p.y_out && row < p.M) {
+    if constexpr (G::NB2 % 2 != 0) {
+      if (p.y_out && row < p.M) {
 #pragma unroll
-      for (int j = 0; j < G::NB2; ++j)
-        *reinterpret_cast<float4*>(p.y_out + (size_t)row * p.ldyo + cbase + j * 16) =
-            make_float4(acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
+        for (int j = 0; j < G::NB2; ++j)
+          *reinterpret_cast<float4*>(p.y_out + (size_t)row * p.ldyo + cbase + j * 16) =
+              make_float4(acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
+      }
+    }
+  }
+  if constexpr (G::NB2 % 2 == 0) {
+    // Y' leaves in 16-row x 32-column pieces through the wave's own 2 KB of
+    // H (free here), read back as 16-byte parts of whole 128-byte row
+    // segments: a store then writes 8 full lines instead of 16 half lines.
+    if (p.y_out) {
+      static_assert(kLayerWaves * 16 * 32 * sizeof(float) <= LBM * G::FC * sizeof(T), "per-wave staging in H");
+      float* reg = reinterpret_cast<float*>(L.h) + ln.wave * (16 * 32);
+#pragma unroll
+      for (int i = 0; i < G::MB2; ++i) {
+        const int rblk = m0 + ln.w2m * G::MB2 * 16 + i * 16;
+#pragma unroll
+        for (int jh = 0; jh < G::NB2 / 2; ++jh) {
+#pragma unroll
+          for (int jj = 0; jj < 2; ++jj) {
+            const f32x4 a4 = acc[i][2 * jh + jj];
+            const float v[4] = {a4[0], a4[1], a4[2], a4[3]};
+            store4(&reg[swz<float, 32>(ln.col, jj * 16 + 4 * ln.g4)], v);
+          }
+          const int c0 = ln.w2n * G::NB2 * 16 + jh * 32;
+#pragma unroll
+          for (int hf = 0; hf < 2; ++hf) {
+            const int rr = (ln.lane >> 3) + 8 * hf, gg = ln.lane & 7;
+            const float4 v = *reinterpret_cast<const float4*>(&reg[swz<float, 32>(rr, gg * 4)]);
+            if (rblk + rr < p.M) *reinterpret_cast<float4*>(p.y_out + (size_t)(rblk + rr) * p.ldyo + c0 + gg * 4) = v;
+          }
+        }
+      }
     }
   }
   if constexpr (HEAD) {
@@ -855,6 +899,7 @@ hipError_t launch_post_attention(const PostAttnArgs<T>& a, const GraphTable& gt,
     return hipErrorInvalidValue;
   if (a.film_gamma && (!a.film_beta || a.film_stride % 4 || !aligned_16(a.film_gamma) || !aligned_16(a.film_beta)))
     return hipErrorInvalidValue;
+  if (a.y_out && (a.ldyo % 4 || !aligned_16(a.y_out))) return hipErrorInvalidValue;
   dim3 grid((a.M + LBM - 1) / LBM), block(LNT);
   const bool head = a.w_out != nullptr;
   switch (a.d) {

@@ -103,7 +103,7 @@ def _swz(cols, epv, r, c):
     return r * cols + ((c // epv) ^ _key(cols // epv, r)) * epv + c % epv
 
 
-def _dma_tile(rows, cols, eb, ld, row_max):
+def _dma_tile(rows, cols, eb, ld, row_max, nw=LAYER_WAVES):
     """(tile element offset, source element offset, row, column) of every
     element moved by dma_tile<T, rows, cols>(tile, src, ld, row_max), from the
     kernel's split of each address into a wave-uniform row base and a per-lane
@@ -111,11 +111,11 @@ def _dma_tile(rows, cols, eb, ld, row_max):
     epv = 16 // eb
     gpr = cols // epv
     granules = rows * gpr
-    assert granules % LAYER_THREADS == 0 and 4 <= gpr <= 64
-    per = granules // LAYER_THREADS
+    assert granules % (64 * nw) == 0 and 4 <= gpr <= 64
+    per = granules // (64 * nw)
     clamp = row_max < rows - 1
     out = []
-    for wave in range(LAYER_WAVES):
+    for wave in range(nw):
         for i in range(per):
             q = (wave * per + i) * 64
             rb = q // gpr
@@ -149,13 +149,13 @@ def _geo(dtype, d):
                 epv=16 // EB[dtype], mb2=LAYER_ROWS // 2 // 16, nb2=d // 4 // 16)
 
 
-def _check_tile(rows, cols, dtype, d, ld, src_rows, row_max=None):
+def _check_tile(rows, cols, dtype, d, ld, src_rows, row_max=None, nw=LAYER_WAVES):
     """The DMA of a rows x cols tile writes every tile element exactly once,
     inside the staging buffer, with the source element that swz() reads there."""
     g = _geo(dtype, d)
     eb, epv = EB[dtype], g["epv"]
     row_max = rows - 1 if row_max is None else row_max
-    moved = _dma_tile(rows, cols, eb, ld, row_max)
+    moved = _dma_tile(rows, cols, eb, ld, row_max, nw)
     dst = [m[0] for m in moved]
     assert sorted(dst) == list(range(rows * cols))
     assert rows * cols <= g["buf"]
@@ -172,10 +172,12 @@ def test_layer_kernel_dma_tiles(d, dtype):
     g = _geo(dtype, d)
     fc = g["fc"]
     dff = 4 * d
-    # W_1 / W_qkv chunk: fc rows x d (ld d); W_2 / W_o chunk: d rows x fc (ld d_ff / d)
-    _check_tile(fc, d, dtype, d, d, fc)
-    for ld in (dff, d):
-        _check_tile(d, fc, dtype, d, ld, d)
+    # W_1 / W_qkv chunk: fc rows x d (ld d); W_2 / W_o chunk: d rows x fc (ld d_ff / d);
+    # loaded by all 8 waves or (spread over a product) by waves 0 .. 3
+    for nw in (8, 4):
+        _check_tile(fc, d, dtype, d, d, fc, nw=nw)
+        for ld in (dff, d):
+            _check_tile(d, fc, dtype, d, ld, d, nw=nw)
     # O chunk: 128 rows x fc of an [M, d] matrix; a ragged last block clamps rows
     for rows_valid in (128, 100, 1):
         moved = _check_tile(LAYER_ROWS, fc, dtype, d, d, rows_valid, row_max=rows_valid - 1)
@@ -315,3 +317,39 @@ def test_layer_qkv_store_transpose(d):
                     read.append((row, unit))
         assert sorted(read) == sorted(written.values())
         assert 0 <= base and base + 16 * wu <= LAYER_ROWS * g["fc"]
+
+
+@pytest.mark.parametrize("d", [128, 256])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_layer_residual_store_transpose(d, dtype):
+    """Y' (fp32) leaves the row tiling through each wave's 2 KB of H in
+    16-row x 32-column pieces: every (row, column) of the wave's 64 x d/4
+    block is stored exactly once, from the lane that holds it."""
+    g = _geo(dtype, d)
+    nb2, mb2 = g["nb2"], g["mb2"]
+    assert nb2 % 2 == 0 and LAYER_WAVES * 16 * 32 * 4 <= LAYER_ROWS * g["fc"] * EB[dtype]
+    for wave in range(LAYER_WAVES):
+        w2m, w2n = wave // 4, wave % 4
+        base = wave * 16 * 32
+        stored = []
+        for i in range(mb2):
+            for jh in range(nb2 // 2):
+                lds = {}
+                for lane in range(64):
+                    col, g4 = lane & 15, lane >> 4
+                    for jj in range(2):
+                        c = w2n * nb2 * 16 + 4 * g4 + (2 * jh + jj) * 16      # the lane's columns
+                        t = base + _swz(32, 4, col, jj * 16 + 4 * g4)
+                        for e in range(4):
+                            lds[t + e] = (w2m * mb2 * 16 + i * 16 + col, c + e)
+                assert len(lds) == 16 * 32
+                c0 = w2n * nb2 * 16 + jh * 32
+                for hf in range(2):
+                    for lane in range(64):
+                        rr, gg = (lane >> 3) + 8 * hf, lane & 7
+                        t = base + _swz(32, 4, rr, gg * 4)
+                        for e in range(4):
+                            assert lds[t + e] == (w2m * mb2 * 16 + i * 16 + rr, c0 + gg * 4 + e)
+                            stored.append(lds[t + e])
+        expect = [(w2m * 64 + r, w2n * nb2 * 16 + c) for r in range(64) for c in range(nb2 * 16)]
+        assert sorted(stored) == sorted(expect)
