@@ -16,6 +16,7 @@
 // LDS row-major, V tiles transposed; both double-buffered over 64-key tiles.
 #include "device_common.h"
 #include "kernels.h"
+#include "lds_dma.h"
 
 namespace gdp {
 
@@ -73,8 +74,13 @@ template <> struct VBlock<bf16> {
     const uint32_t w = (e < 2) ? r.x : r.y;
     return (e & 1) ? (w >> 16) : (w & 0xffffu);
   }
+  // element e of rows 0, 1 (and 2, 3) packed into one word: a byte permute of
+  // the two source words (bytes 0-1 from the first, 2-3 from the second)
   static __device__ __forceinline__ raw column(const raw (&r)[4], int e) {
-    return make_uint2(half(r[0], e) | (half(r[1], e) << 16), half(r[2], e) | (half(r[3], e) << 16));
+    const uint32_t sel = (e & 1) ? 0x07060302u : 0x05040100u;
+    const uint32_t w0 = e < 2 ? r[0].x : r[0].y, w1 = e < 2 ? r[1].x : r[1].y;
+    const uint32_t w2 = e < 2 ? r[2].x : r[2].y, w3 = e < 2 ? r[3].x : r[3].y;
+    return make_uint2(__builtin_amdgcn_perm(w1, w0, sel), __builtin_amdgcn_perm(w3, w2, sel));
   }
 };
 template <> struct VBlock<float> {
@@ -90,10 +96,18 @@ template <> struct VBlock<float> {
 
 }  // namespace
 
+// Four waves per SIMD (at most 128 VGPRs): the exponentials of one wave
+// overlap the matrix-core products of another.  (The fp32 d_h = 64 variant
+// needs more registers and runs at two.)
 template <typename T, int DH>
-__global__ __launch_bounds__(256) void k_seg_attention(AttnArgs<T> p, GraphTable gt) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void k_seg_attention(AttnArgs<T> p,
+                                                                                               GraphTable gt) {
   constexpr int EPV = 16 / sizeof(T);
-  constexpr int KS = DH + EPV;          // sK row stride
+  // bf16 with d_h >= 32: K tiles arrive by direct global -> LDS loads into an
+  // unpadded, XOR-swizzled tile (one or two loads per wave); otherwise through
+  // registers into rows padded to KS.
+  constexpr bool KDMA = sizeof(T) == 2 && DH >= 32;
+  constexpr int KS = KDMA ? DH : DH + EPV;  // sK row stride
   // sVt row stride: 68 elements puts the 16 rows of an 8-byte bf16 fragment
   // read on distinct bank pairs (the row stride is an odd number of 8-byte words).
   constexpr int VS = BKV + 4;
@@ -154,6 +168,12 @@ __global__ __launch_bounds__(256) void k_seg_attention(AttnArgs<T> p, GraphTable
   const int vkg = threadIdx.x % (BKV / 4), vdg = threadIdx.x / (BKV / 4);
   auto load_tile = [&](int t) {
     const int kb = k0 + t * BKV;
+    if constexpr (KDMA) {
+      // keys past the band end read the last valid row (see below)
+      const dma::DmaTile<T, BKV, DH, 4> kt(&sK[t & 1][0], Kp + (size_t)kb * p.ldq, p.ldq, k1 - 1 - kb);
+      if (k1 - 1 - kb < BKV - 1) kt.template all<true>();
+      else kt.template all<false>();
+    } else {
 #pragma unroll
     for (int i = 0; i < (CHUNKS + 255) / 256; ++i) {
       const int c = threadIdx.x + i * 256;
@@ -162,6 +182,7 @@ __global__ __launch_bounds__(256) void k_seg_attention(AttnArgs<T> p, GraphTable
       // are masked to -inf, so they carry P = 0 against finite values.
       const int key = min(kb + row, k1 - 1);
       if (CHUNKS % 256 == 0 || c < CHUNKS) rk[i] = *reinterpret_cast<const uint4*>(Kp + (size_t)key * p.ldq + cc);
+    }
     }
     if (threadIdx.x < VTHREADS) {                 // whole waves
 #pragma unroll
@@ -172,12 +193,14 @@ __global__ __launch_bounds__(256) void k_seg_attention(AttnArgs<T> p, GraphTable
     }
   };
   auto store_tile = [&](int buf) {
+    if constexpr (!KDMA) {
 #pragma unroll
-    for (int i = 0; i < (CHUNKS + 255) / 256; ++i) {
-      const int c = threadIdx.x + i * 256;
-      if (c < CHUNKS) {
-        const int row = c / CPR, cc = (c % CPR) * EPV;
-        *reinterpret_cast<uint4*>(&sK[buf][row * KS + cc]) = rk[i];
+      for (int i = 0; i < (CHUNKS + 255) / 256; ++i) {
+        const int c = threadIdx.x + i * 256;
+        if (c < CHUNKS) {
+          const int row = c / CPR, cc = (c % CPR) * EPV;
+          *reinterpret_cast<uint4*>(&sK[buf][row * KS + cc]) = rk[i];
+        }
       }
     }
     if (threadIdx.x < VTHREADS) {
@@ -198,7 +221,7 @@ __global__ __launch_bounds__(256) void k_seg_attention(AttnArgs<T> p, GraphTable
 
   load_tile(0);
   store_tile(0);
-  __syncthreads();
+  dma::wait_loads_then_barrier();
   for (int t = 0; t < ntiles; ++t) {
     const int cur = t & 1;
     const int kvalid = k1 - (k0 + t * BKV);     // keys of this tile that exist (>= 1)
@@ -215,7 +238,11 @@ __global__ __launch_bounds__(256) void k_seg_attention(AttnArgs<T> p, GraphTable
       sacc[kb][1] = negm[1];
 #pragma unroll
       for (int s = 0; s < QS::STEPS; ++s) {
-        const typename QF::t kf = QF::load(&sK[cur][(kb * 16 + col) * KS + s * QS::K + QS::KV * g4]);
+        const int krow = kb * 16 + col, kcol = s * QS::K + QS::KV * g4;
+        int kidx;
+        if constexpr (KDMA) kidx = dma::swz<T, DH>(krow, kcol);
+        else kidx = krow * KS + kcol;
+        const typename QF::t kf = QF::load(&sK[cur][kidx]);
         sacc[kb][0] = QF::mma(kf, qf[0][s], sacc[kb][0]);
         sacc[kb][1] = QF::mma(kf, qf[1][s], sacc[kb][1]);
       }
@@ -332,7 +359,7 @@ __global__ __launch_bounds__(256) void k_seg_attention(AttnArgs<T> p, GraphTable
     }
 
     if (t + 1 < ntiles) store_tile(cur ^ 1);
-    __syncthreads();
+    dma::wait_loads_then_barrier();  // the next tile's direct loads (if any) in place
   }
 
   // ---- normalise and store ---------------------------------------------------------
