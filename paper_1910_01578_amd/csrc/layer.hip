@@ -434,6 +434,53 @@ struct ChunkDma {
   }
 };
 
+// The fp32 residual rows held in the row tiling, to y_out[M, ldyo].  With an
+// even NB2 they leave in 16-row x 32-column pieces through the wave's own 2 KB
+// of H (which must be free of other waves' use), read back as 16-byte parts
+// of whole 128-byte row segments: a store then writes 8 full lines instead
+// of 16 half lines.
+template <typename T, int D>
+__device__ __forceinline__ void store_residual(const typename Geo<T, D>::RowAcc& acc, const Lds<T>& L,
+                                               const Lanes& ln, int m0, int M, float* y_out, int ldyo) {
+  using G = Geo<T, D>;
+  if constexpr (G::NB2 % 2 != 0) {
+    const int cbase = ln.w2n * G::NB2 * 16 + 4 * ln.g4;
+#pragma unroll
+    for (int i = 0; i < G::MB2; ++i) {
+      const int row = m0 + ln.w2m * G::MB2 * 16 + ln.col + i * 16;
+      if (row < M) {
+#pragma unroll
+        for (int j = 0; j < G::NB2; ++j)
+          *reinterpret_cast<float4*>(y_out + (size_t)row * ldyo + cbase + j * 16) =
+              make_float4(acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
+      }
+    }
+  } else {
+    static_assert(kLayerWaves * 16 * 32 * sizeof(float) <= LBM * G::FC * sizeof(T), "per-wave staging in H");
+    float* reg = reinterpret_cast<float*>(L.h) + ln.wave * (16 * 32);
+#pragma unroll
+    for (int i = 0; i < G::MB2; ++i) {
+      const int rblk = m0 + ln.w2m * G::MB2 * 16 + i * 16;
+#pragma unroll
+      for (int jh = 0; jh < G::NB2 / 2; ++jh) {
+#pragma unroll
+        for (int jj = 0; jj < 2; ++jj) {
+          const f32x4 a4 = acc[i][2 * jh + jj];
+          const float v[4] = {a4[0], a4[1], a4[2], a4[3]};
+          store4(&reg[swz<float, 32>(ln.col, jj * 16 + 4 * ln.g4)], v);
+        }
+        const int c0 = ln.w2n * G::NB2 * 16 + jh * 32;
+#pragma unroll
+        for (int hf = 0; hf < 2; ++hf) {
+          const int rr = (ln.lane >> 3) + 8 * hf, gg = ln.lane & 7;
+          const float4 v = *reinterpret_cast<const float4*>(&reg[swz<float, 32>(rr, gg * 4)]);
+          if (rblk + rr < M) *reinterpret_cast<float4*>(y_out + (size_t)(rblk + rr) * ldyo + c0 + gg * 4) = v;
+        }
+      }
+    }
+  }
+}
+
 // Loads of QKV chunk q (units q*FCQ .. + FCQ of W_qkv and b_qkv) into the
 // buffers of parity P, by waves 0 .. NW - 1.
 template <typename T, int D, int P, int NW = kLayerWaves>
@@ -749,44 +796,11 @@ __global__ __launch_bounds__(LNT) void k_post_attention(PostAttnArgs<T> p, Graph
         acc[i][j][3] = fgm[j].w * acc[i][j][3] + fbt[j].w;
       }
     }
-    if constexpr (G::NB2 % 2 != 0) {
-      if (p.y_out && row < p.M) {
-#pragma unroll
-        for (int j = 0; j < G::NB2; ++j)
-          *reinterpret_cast<float4*>(p.y_out + (size_t)row * p.ldyo + cbase + j * 16) =
-              make_float4(acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
-      }
-    }
   }
-  if constexpr (G::NB2 % 2 == 0) {
-    // Y' leaves in 16-row x 32-column pieces through the wave's own 2 KB of
-    // H (free here), read back as 16-byte parts of whole 128-byte row
-    // segments: a store then writes 8 full lines instead of 16 half lines.
-    if (p.y_out) {
-      static_assert(kLayerWaves * 16 * 32 * sizeof(float) <= LBM * G::FC * sizeof(T), "per-wave staging in H");
-      float* reg = reinterpret_cast<float*>(L.h) + ln.wave * (16 * 32);
-#pragma unroll
-      for (int i = 0; i < G::MB2; ++i) {
-        const int rblk = m0 + ln.w2m * G::MB2 * 16 + i * 16;
-#pragma unroll
-        for (int jh = 0; jh < G::NB2 / 2; ++jh) {
-#pragma unroll
-          for (int jj = 0; jj < 2; ++jj) {
-            const f32x4 a4 = acc[i][2 * jh + jj];
-            const float v[4] = {a4[0], a4[1], a4[2], a4[3]};
-            store4(&reg[swz<float, 32>(ln.col, jj * 16 + 4 * ln.g4)], v);
-          }
-          const int c0 = ln.w2n * G::NB2 * 16 + jh * 32;
-#pragma unroll
-          for (int hf = 0; hf < 2; ++hf) {
-            const int rr = (ln.lane >> 3) + 8 * hf, gg = ln.lane & 7;
-            const float4 v = *reinterpret_cast<const float4*>(&reg[swz<float, 32>(rr, gg * 4)]);
-            if (rblk + rr < p.M) *reinterpret_cast<float4*>(p.y_out + (size_t)(rblk + rr) * p.ldyo + c0 + gg * 4) = v;
-          }
-        }
-      }
-    }
-  }
+  // (issuing these stores after the first QKV barrier instead, to overlap
+  // their HBM writes with its products, keeps acc live there and measured
+  // 12 % slower)
+  if (p.y_out) store_residual<T, D>(acc, L, ln, m0, p.M, p.y_out, p.ldyo);
   if constexpr (HEAD) {
     head_epilogue<T, D>(acc, L, ln, m0, p.M, p.w_out, p.b_out, p.n_dev, p.logits, p.lse);
   } else {
@@ -867,11 +881,9 @@ __global__ __launch_bounds__(LNT) void k_pre_layer(PreLayerArgs<T> p, GraphTable
       load4f(p.x + (size_t)rr * p.ldx + cn, x);
 #pragma unroll
       for (int r = 0; r < 4; ++r) acc[i][j][r] = fg ? fg[cn + r] * x[r] + fb[cn + r] : x[r];
-      if (row < p.M)
-        *reinterpret_cast<float4*>(p.y_out + (size_t)row * p.ldyo + cn) =
-            make_float4(acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
     }
   }
+  store_residual<T, D>(acc, L, ln, m0, p.M, p.y_out, p.ldyo);
   typename G::ActFrags af;
   qkv_phase<T, D, 0>(acc, L, af, ln, m0, p.M, p.w_qkv, p.b_qkv, p.qkv_out, p.ldq, p.q_scale);
 }
@@ -882,6 +894,7 @@ hipError_t launch_pre_layer(const PreLayerArgs<T>& a, const GraphTable& gt, hipS
   if (!a.x || !a.y_out || !a.w_qkv || !a.b_qkv || !a.qkv_out || a.ldq < 3 * a.d) return hipErrorInvalidValue;
   if (!aligned_16(a.w_qkv) || !aligned_16(a.b_qkv) || !aligned_16(a.qkv_out) || a.ldq % (16 / (int)sizeof(T)))
     return hipErrorInvalidValue;
+  if (a.ldyo % 4 || !aligned_16(a.y_out)) return hipErrorInvalidValue;
   dim3 grid((a.M + LBM - 1) / LBM), block(LNT);
   switch (a.d) {
     case 64: hipLaunchKernelGGL((k_pre_layer<T, 64>), grid, block, 0, s, a, gt); break;
