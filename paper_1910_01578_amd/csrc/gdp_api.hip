@@ -154,12 +154,14 @@ static int embed_impl(const gdp_graph* g, const gdp_gnn* gnn, T* node_emb, float
     T* hout = (l == L - 1) ? node_emb : hb[l & 1];
     const GemmArgs<T, T, T> pool = {h, hin, static_cast<const T*>(Lw.w_pool), hin, nullptr, 0, nullptr, 0,
                                     static_cast<const T*>(Lw.b_pool), P, H, N, H};
-    GDP_LAUNCH(GDP_K_GEMM_POOL, (launch_gemm<T, T, T>(pool, EPI_SIGMOID, st)));
+    if (row_gemm_supported(pool)) GDP_LAUNCH(GDP_K_GEMM_POOL, (launch_row_gemm<T>(pool, EPI_SIGMOID, st)));
+    else GDP_LAUNCH(GDP_K_GEMM_POOL, (launch_gemm<T, T, T>(pool, EPI_SIGMOID, st)));
     GDP_LAUNCH(GDP_K_GATHER_MAX, launch_gather_max<T>(P, s_ptr, s_idx, N, H, A, st));
     const GemmArgs<T, T, T> upd = {h, hin, static_cast<const T*>(Lw.w_self), hin, A, H,
                                    static_cast<const T*>(Lw.w_neigh), H, static_cast<const T*>(Lw.b_upd), hout, H,
                                    N, H};
-    GDP_LAUNCH(GDP_K_GEMM_UPDATE, (launch_gemm<T, T, T>(upd, EPI_RELU, st)));
+    if (row_gemm_supported(upd)) GDP_LAUNCH(GDP_K_GEMM_UPDATE, (launch_row_gemm<T>(upd, EPI_RELU, st)));
+    else GDP_LAUNCH(GDP_K_GEMM_UPDATE, (launch_gemm<T, T, T>(upd, EPI_RELU, st)));
     h = hout;
   }
   GraphTable ct = make_table(g);

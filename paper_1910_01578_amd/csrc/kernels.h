@@ -57,6 +57,13 @@ struct GemmArgs {
 };
 template <typename TA, typename T, typename TO>
 hipError_t launch_gemm(const GemmArgs<TA, T, TO>& a, int epi, hipStream_t s);
+// The same product for N = 64, 128 or 256 and K segments that are multiples of
+// the layer kernel's chunk (64 bf16 / 32 fp32 elements), with the whole output
+// row held on chip; row_gemm_supported says whether a call qualifies.
+template <typename T>
+bool row_gemm_supported(const GemmArgs<T, T, T>& a);
+template <typename T>
+hipError_t launch_row_gemm(const GemmArgs<T, T, T>& a, int epi, hipStream_t s);
 
 // Everything of a placer layer after its attention, and the start of the next:
 //   Z    = LN1(y + o W_o^T + b_o)

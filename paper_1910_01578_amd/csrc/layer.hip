@@ -907,4 +907,158 @@ hipError_t launch_pre_layer(const PreLayerArgs<T>& a, const GraphTable& gt, hipS
 template hipError_t launch_pre_layer<float>(const PreLayerArgs<float>&, const GraphTable&, hipStream_t);
 template hipError_t launch_pre_layer<bf16>(const PreLayerArgs<bf16>&, const GraphTable&, hipStream_t);
 
+
+// Section 3.1, Eq. 2 and Eq. 3: the GNN's dense layers,
+//   out = act([A1 | A2] [W1 | W2]^T + b)      (act = sigmoid or ReLU),
+// over blocks of 128 rows with the row tiling of the kernel above: the
+// accumulator holds the block's whole d-wide output, A and W stream through
+// LDS in K chunks of FC by direct loads, and the result leaves through each
+// wave's slice of H as whole row segments.  K1 and K2 are multiples of FC;
+// d = N is 64, 128 or 256.
+//
+// A comes from HBM, W from L2: the A chunks run through a ring of R slots,
+// R - 1 chunks ahead, and W chunks through two buffers.  Chunk c - 1's top
+// issues W(c) and then A(c + R - 2); in this loop the loads are a wave's only
+// memory operations and complete in order, so chunk c waits for all but the
+// A(c + R - 2) loads (vmcnt) before its barrier.
+template <int N>
+__device__ __forceinline__ void wait_vm_barrier() {
+  asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"i"(N) : "memory");
+}
+
+template <typename T, int D, int EPI>
+__global__ __launch_bounds__(LNT) void k_row_gemm(GemmArgs<T, T, T> p) {
+  using G = Geo<T, D>;
+  constexpr int FC = G::FC;
+  constexpr int R = D >= 256 ? 4 : 2;                     // A ring slots
+  constexpr int AS = LBM * FC, WS = D * FC;               // elements of an A / W chunk
+  constexpr int WC = G::NB2 * 16;                         // a row-tiling wave's columns
+  using TA = DmaTile<T, LBM, FC>;
+  __shared__ __attribute__((aligned(16))) T sA[R * AS];
+  __shared__ __attribute__((aligned(16))) T sW0[WS];
+  __shared__ __attribute__((aligned(16))) T sW1[WS];
+  __shared__ __attribute__((aligned(16))) T sH[kLayerWaves * 16 * WC];
+  const Lanes ln = make_lanes<T, D>();
+  const int m0 = blockIdx.x * LBM;
+  const int rows_valid = p.M - m0;
+  const int nk1 = p.k1 / FC, nk = nk1 + p.k2 / FC;
+  typename G::RowAcc acc;
+#pragma unroll
+  for (int i = 0; i < G::MB2; ++i)
+#pragma unroll
+    for (int j = 0; j < G::NB2; ++j) acc[i][j] = zero4();
+  // chunk c: columns c*FC .. + FC of [A1 | A2] (rows m0 .. + 128) and of [W1 | W2]
+  auto issue_a = [&](int c) {
+    const bool s1 = c < nk1;
+    const int cc = (s1 ? c : c - nk1) * FC;
+    const T* a = s1 ? p.a1 + (size_t)m0 * p.lda1 + cc : p.a2 + (size_t)m0 * p.lda2 + cc;
+    dma_tile<T, LBM, FC>(sA + (c % R) * AS, a, s1 ? p.lda1 : p.lda2, rows_valid - 1);
+  };
+  auto issue_w = [&](int c, T* buf) {
+    const bool s1 = c < nk1;
+    const int cc = (s1 ? c : c - nk1) * FC;
+    dma_tile<T, D, FC>(buf, (s1 ? p.w1 : p.w2) + cc, s1 ? p.k1 : p.k2, D - 1);
+  };
+  for (int c = 0; c < R - 1 && c < nk; ++c) issue_a(c);
+  issue_w(0, sW0);
+  chunk_pairs<0, false>(nk, [&](int c, auto pc) {
+    constexpr int P = decltype(pc)::v;
+    // A(c) and W(c) in place (each wave waits for its own loads, then the barrier)
+    if (R > 2 && c >= 1 && c + R - 2 < nk) wait_vm_barrier<TA::PER>();
+    else wait_vm_barrier<0>();
+    if (c + 1 < nk) issue_w(c + 1, P ? sW0 : sW1);      // buffer of chunk c - 1
+    if (c + R - 1 < nk) issue_a(c + R - 1);             // slot of chunk c - 1
+    row_mma<T, D>(acc, sA + (c % R) * AS, P ? sW1 : sW0, ln);
+  });
+
+  // bias + activation
+  const int cbase = ln.w2n * G::NB2 * 16 + 4 * ln.g4;
+#pragma unroll
+  for (int j = 0; j < G::NB2; ++j) {
+    float b[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) b[r] = to_f32(p.bias[cbase + j * 16 + r]);
+#pragma unroll
+    for (int i = 0; i < G::MB2; ++i)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        float v = acc[i][j][r] + b[r];
+        if (EPI == EPI_RELU) v = fmaxf(v, 0.f);
+        // the reciprocal instruction (about 1 ulp) instead of an IEEE division
+        if (EPI == EPI_SIGMOID) v = __builtin_amdgcn_rcpf(1.0f + __expf(-v));
+        acc[i][j][r] = v;
+      }
+  }
+  constexpr int RB = WC * (int)sizeof(T);                 // bytes of a row of the wave's columns
+  if constexpr (sizeof(T) == 2 && RB >= 64) {
+    // 16-row blocks through the wave's own slice of sH, read back as 16-byte
+    // parts of whole row segments
+    constexpr int LPR = RB / 16, RPI = 64 / LPR, EPV = 16 / (int)sizeof(T);
+    T* reg = sH + ln.wave * (16 * WC);
+#pragma unroll
+    for (int i = 0; i < G::MB2; ++i) {
+#pragma unroll
+      for (int j = 0; j < G::NB2; ++j) {
+        const float v[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
+        store4(&reg[swz<T, WC>(ln.col, j * 16 + 4 * ln.g4)], v);
+      }
+      const int rblk = m0 + ln.w2m * G::MB2 * 16 + i * 16;
+#pragma unroll
+      for (int hf = 0; hf < 16 / RPI; ++hf) {
+        const int rr = ln.lane / LPR + RPI * hf, gg = ln.lane % LPR;
+        const uint4 v = *reinterpret_cast<const uint4*>(&reg[swz<T, WC>(rr, gg * EPV)]);
+        if (rblk + rr < p.M)
+          *reinterpret_cast<uint4*>(p.out + (size_t)(rblk + rr) * p.ldo + ln.w2n * WC + gg * EPV) = v;
+      }
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < G::MB2; ++i) {
+      const int row = m0 + ln.w2m * G::MB2 * 16 + ln.col + i * 16;
+      if (row < p.M) {
+#pragma unroll
+        for (int j = 0; j < G::NB2; ++j) {
+          const float v[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
+          store4(p.out + (size_t)row * p.ldo + cbase + j * 16, v);
+        }
+      }
+    }
+  }
+}
+
+template <typename T>
+bool row_gemm_supported(const GemmArgs<T, T, T>& a) {
+  constexpr int FC = LayerCfg<T>::FC, EPV = 16 / sizeof(T);
+  return (a.N == 64 || a.N == 128 || a.N == 256) && a.k1 > 0 && a.k1 % FC == 0 && a.k2 >= 0 && a.k2 % FC == 0 &&
+         (a.k2 == 0 || (a.a2 && a.w2 && a.lda2 % EPV == 0 && aligned_16(a.a2) && aligned_16(a.w2))) &&
+         a.lda1 % EPV == 0 && a.ldo % EPV == 0 && aligned_16(a.a1) && aligned_16(a.w1) && aligned_16(a.out) &&
+         a.scale_cols == 0;
+}
+template bool row_gemm_supported<float>(const GemmArgs<float, float, float>&);
+template bool row_gemm_supported<bf16>(const GemmArgs<bf16, bf16, bf16>&);
+
+template <typename T>
+hipError_t launch_row_gemm(const GemmArgs<T, T, T>& a, int epi, hipStream_t s) {
+  if (a.M <= 0) return hipSuccess;
+  if (!row_gemm_supported(a)) return hipErrorInvalidValue;
+  dim3 grid((a.M + LBM - 1) / LBM), block(LNT);
+#define GDP_ROW_GEMM(DV)                                                                                      \
+  switch (epi) {                                                                                              \
+    case EPI_BIAS: hipLaunchKernelGGL((k_row_gemm<T, DV, EPI_BIAS>), grid, block, 0, s, a); break;            \
+    case EPI_RELU: hipLaunchKernelGGL((k_row_gemm<T, DV, EPI_RELU>), grid, block, 0, s, a); break;            \
+    case EPI_SIGMOID: hipLaunchKernelGGL((k_row_gemm<T, DV, EPI_SIGMOID>), grid, block, 0, s, a); break;      \
+    default: return hipErrorInvalidValue;                                                                     \
+  }
+  switch (a.N) {
+    case 64: GDP_ROW_GEMM(64) break;
+    case 128: GDP_ROW_GEMM(128) break;
+    case 256: GDP_ROW_GEMM(256) break;
+    default: return hipErrorInvalidValue;
+  }
+#undef GDP_ROW_GEMM
+  return hipGetLastError();
+}
+template hipError_t launch_row_gemm<float>(const GemmArgs<float, float, float>&, int, hipStream_t);
+template hipError_t launch_row_gemm<bf16>(const GemmArgs<bf16, bf16, bf16>&, int, hipStream_t);
+
 }  // namespace gdp

@@ -353,3 +353,73 @@ def test_layer_residual_store_transpose(d, dtype):
                             stored.append(lds[t + e])
         expect = [(w2m * 64 + r, w2n * nb2 * 16 + c) for r in range(64) for c in range(nb2 * 16)]
         assert sorted(stored) == sorted(expect)
+
+
+@pytest.mark.parametrize("d", [128, 256])
+def test_row_gemm_store_transpose(d):
+    """The GNN dense-layer kernel's bf16 output leaves the row tiling through
+    each wave's slice of H: the wave's 16-row x WC block (WC = d/4 columns, 4 a
+    lane) is read back as 16-byte parts of whole rows; every element is stored
+    once, at its own position, and the slice stays inside H."""
+    g = _geo("bf16", d)
+    wc = g["nb2"] * 16
+    lpr = wc * 2 // 16
+    rpi = 64 // lpr
+    assert LAYER_WAVES * 16 * wc <= LAYER_ROWS * g["fc"]
+    for wave in range(LAYER_WAVES):
+        base = wave * 16 * wc
+        lds = {}
+        for lane in range(64):
+            col, g4 = lane & 15, lane >> 4
+            for j in range(g["nb2"]):
+                c = j * 16 + 4 * g4
+                t = base + _swz(wc, 8, col, c)
+                assert c % 8 + 4 <= 8
+                for e in range(4):
+                    lds[t + e] = (col, c + e)
+        assert len(lds) == 16 * wc
+        out = []
+        for hf in range(16 // rpi):
+            for lane in range(64):
+                rr, gg = lane // lpr + rpi * hf, lane % lpr
+                t = base + _swz(wc, 8, rr, gg * 8)
+                for e in range(8):
+                    assert lds[t + e] == (rr, gg * 8 + e)
+                    out.append(lds[t + e])
+        assert sorted(out) == sorted(lds.values())
+
+
+@pytest.mark.parametrize("R", [2, 4])
+@pytest.mark.parametrize("nk", [1, 2, 3, 4, 5, 8])
+def test_row_gemm_chunk_schedule(R, nk):
+    """Replay of the GNN dense-layer kernel's load schedule: the prologue loads
+    A(0 .. R-2) and W(0); the top of chunk c loads W(c+1) then A(c+R-1).
+    Every chunk's A and W are loaded exactly once, before the chunk that
+    reads them, into a slot / buffer not read since the previous barrier, and
+    the loads that may still be in flight at chunk c's wait are exactly the
+    ones issued after W(c) (A(c+R-2) when it exists)."""
+    issued = []                       # (kind, chunk, slot) in issue order
+    for c in range(min(R - 1, nk)):
+        issued.append(("A", c, c % R))
+    issued.append(("W", 0, 0))
+    last_read = {}                    # ("A", slot) / ("W", buf) -> chunk that last read it
+    for c in range(nk):
+        # the kernel's wait leaves the newest group in flight (the A(c+R-2) loads)
+        # when R > 2, c >= 1 and c + R - 2 < nk, and nothing otherwise
+        partial = R > 2 and c >= 1 and c + R - 2 < nk
+        in_flight = issued[-1:] if partial else []
+        if partial:
+            assert in_flight == [("A", c + R - 2, (c + R - 2) % R)], (c, issued[-3:])
+        done = issued[:len(issued) - len(in_flight)]
+        assert ("A", c, c % R) in done and ("W", c, c % 2) in done, c
+        # issues at the top of chunk c write buffers last read in chunk c - 1 (or never)
+        if c + 1 < nk:
+            assert last_read.get(("W", (c + 1) % 2), -1) <= c - 1
+            issued.append(("W", c + 1, (c + 1) % 2))
+        if c + R - 1 < nk:
+            assert last_read.get(("A", (c + R - 1) % R), -1) <= c - 1
+            issued.append(("A", c + R - 1, (c + R - 1) % R))
+        last_read[("A", c % R)] = c
+        last_read[("W", c % 2)] = c
+    assert sorted(x[1] for x in issued if x[0] == "A") == list(range(nk))
+    assert sorted(x[1] for x in issued if x[0] == "W") == list(range(nk))
