@@ -12,8 +12,10 @@
 // [32w, 32w + 32) as two 16-column MFMA blocks.  Scores are formed transposed,
 // S^T = K Q^T, so that a lane owns one query column: the row max is an
 // in-lane max plus a 4-way exchange, and the probabilities feed the P V
-// product (O^T = V^T P^T) straight from the score registers.  K tiles live in
-// LDS row-major, V tiles transposed; both double-buffered over 64-key tiles.
+// product (O^T = V^T P^T) straight from the score registers.  K and V tiles
+// are double-buffered in LDS over 64-key tiles.
+#include <type_traits>
+
 #include "device_common.h"
 #include "kernels.h"
 #include "lds_dma.h"
@@ -96,26 +98,61 @@ template <> struct VBlock<float> {
 
 }  // namespace
 
-// Four waves per SIMD (at most 128 VGPRs): the exponentials of one wave
-// overlap the matrix-core products of another.  (The fp32 d_h = 64 variant
-// needs more registers and runs at two.)
+// Bounds of the max-free pass (see the kernel): a query column's sum of 2^s
+// inside [2^-50, 2^100] puts its largest term inside [2^-60, 2^100], where no
+// term overflows and the terms flushed to zero are below 2^-66 of it.
+constexpr float kFastSumLo = 0x1p-50f;
+constexpr float kFastSumHi = 0x1p100f;
+
+// Direct loads for both K and V (bf16, d_h >= 32): V stays row-major in LDS
+// and its MFMA fragments come from transposing reads.
 template <typename T, int DH>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void k_seg_attention(AttnArgs<T> p,
-                                                                                               GraphTable gt) {
+struct AttnCfg {
+  static constexpr bool KDMA = sizeof(T) == 2 && DH >= 32;
+  static constexpr bool VDMA = KDMA;
+  static constexpr int WPE = DH >= 64 || (sizeof(T) == 4 && DH >= 32) ? 2 : 4;   // waves per SIMD the registers allow
+};
+
+// ds_read_b64_tr_b16: within each group of 16 lanes, destination lane 4q + p
+// receives in slot e element p of the 8-byte word addressed by source lane
+// 4e + q.
+__device__ __forceinline__ uint2 lds_read_tr16(const bf16* p) {
+  typedef __attribute__((__vector_size__(4 * sizeof(__bf16)))) __bf16 bf16x4_t;
+  const bf16x4_t v = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+      (__attribute__((address_space(3))) bf16x4_t*)((__attribute__((address_space(3))) bf16*)p));
+  return __builtin_bit_cast(uint2, v);
+}
+
+// Four waves per SIMD (at most 128 VGPRs) where d_h <= 32: the exponentials
+// of one wave overlap the matrix-core products of another.
+//
+// Softmax.  Scores arrive in the log2 domain (Q pre-scaled by log2(e)/sqrt(d_h)).
+// A first pass forms 2^s with no offset at all: fp32 and bf16 share an 8-bit
+// exponent, so unless a query's scores leave roughly [-60, 100] nothing
+// overflows or vanishes, and the normalised result is the same as with a
+// running maximum.  The sum of each query column, which the pass produces
+// anyway, tells whether that held; if it fails for any column, the whole
+// work-group repeats the segment with the running-offset softmax (the
+// offset is raised only when a tile exceeds it by 2^8).
+template <typename T, int DH>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(AttnCfg<T, DH>::WPE)))
+void k_seg_attention(AttnArgs<T> p, GraphTable gt) {
   constexpr int EPV = 16 / sizeof(T);
-  // bf16 with d_h >= 32: K tiles arrive by direct global -> LDS loads into an
-  // unpadded, XOR-swizzled tile (one or two loads per wave); otherwise through
-  // registers into rows padded to KS.
-  constexpr bool KDMA = sizeof(T) == 2 && DH >= 32;
+  // bf16 with d_h >= 32: K and V tiles arrive by direct global -> LDS loads
+  // into unpadded, XOR-swizzled row-major tiles; otherwise through registers,
+  // K into rows padded to KS and V transposed.
+  constexpr bool KDMA = AttnCfg<T, DH>::KDMA;
+  constexpr bool VDMA = AttnCfg<T, DH>::VDMA;
   constexpr int KS = KDMA ? DH : DH + EPV;  // sK row stride
-  // sVt row stride: 68 elements puts the 16 rows of an 8-byte bf16 fragment
-  // read on distinct bank pairs (the row stride is an odd number of 8-byte words).
+  // sV^T row stride on the register path: 68 elements puts the 16 rows of an
+  // 8-byte bf16 fragment read on distinct bank pairs (an odd number of 8-byte words).
   constexpr int VS = BKV + 4;
   constexpr int DB = DH / 16;           // 16-row blocks of the head dim
   using QS = QkShape<T, DH>;
   using QF = QkFrag<T, DH>;
   __shared__ __attribute__((aligned(16))) T sK[2][BKV * KS];
-  __shared__ __attribute__((aligned(16))) T sVt[2][DH * VS];
+  __shared__ __attribute__((aligned(16))) T sV[2][VDMA ? BKV * DH : DH * VS];
+  __shared__ int s_redo;
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int col = lane & 15, g4 = lane >> 4;
@@ -154,39 +191,44 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void k
   }
 
   // ---- K / V tile staging -------------------------------------------------------
-  // K: 16-byte chunks of key rows.  V is stored transposed; each thread moves
-  // a 4-key x 4-dim block (lanes consecutive along keys) so that every LDS
-  // store writes 4 consecutive keys of one dim and a quarter-wave covers one
-  // contiguous run of a V^T row.
+  // Register path: K in 16-byte chunks of key rows; V transposed, each thread
+  // moving a 4-key x 4-dim block (lanes consecutive along keys) so that every
+  // LDS store writes 4 consecutive keys of one dim.
   constexpr int CPR = DH / EPV;                 // 16-byte chunks per key row
   constexpr int CHUNKS = BKV * CPR;
   constexpr int VTHREADS = (BKV / 4) * (DH / 4);
   static_assert(VTHREADS <= 256, "V block split");
   using V4 = typename VBlock<T>::raw;           // 4 consecutive elements
-  uint4 rk[(CHUNKS + 255) / 256] = {};
-  V4 rv[4] = {};
+  constexpr int RK = KDMA ? 1 : (CHUNKS + 255) / 256;
+  constexpr int RV = VDMA ? 1 : 4;
+  uint4 rk[RK] = {};
+  V4 rv[RV] = {};
   const int vkg = threadIdx.x % (BKV / 4), vdg = threadIdx.x / (BKV / 4);
   auto load_tile = [&](int t) {
     const int kb = k0 + t * BKV;
+    // keys past the band end read the last valid row: their scores are masked
+    // to -inf, so they carry P = 0 against finite values
+    const int row_max = k1 - 1 - kb;
     if constexpr (KDMA) {
-      // keys past the band end read the last valid row (see below)
-      const dma::DmaTile<T, BKV, DH, 4> kt(&sK[t & 1][0], Kp + (size_t)kb * p.ldq, p.ldq, k1 - 1 - kb);
-      if (k1 - 1 - kb < BKV - 1) kt.template all<true>();
+      const dma::DmaTile<T, BKV, DH, 4> kt(&sK[t & 1][0], Kp + (size_t)kb * p.ldq, p.ldq, row_max);
+      if (row_max < BKV - 1) kt.template all<true>();
       else kt.template all<false>();
     } else {
 #pragma unroll
-    for (int i = 0; i < (CHUNKS + 255) / 256; ++i) {
-      const int c = threadIdx.x + i * 256;
-      const int row = c / CPR, cc = (c % CPR) * EPV;
-      // Keys past the band end read the last valid row instead: their scores
-      // are masked to -inf, so they carry P = 0 against finite values.
-      const int key = min(kb + row, k1 - 1);
-      if (CHUNKS % 256 == 0 || c < CHUNKS) rk[i] = *reinterpret_cast<const uint4*>(Kp + (size_t)key * p.ldq + cc);
+      for (int i = 0; i < RK; ++i) {
+        const int c = threadIdx.x + i * 256;
+        const int row = c / CPR, cc = (c % CPR) * EPV;
+        const int key = min(kb + row, k1 - 1);
+        if (CHUNKS % 256 == 0 || c < CHUNKS) rk[i] = *reinterpret_cast<const uint4*>(Kp + (size_t)key * p.ldq + cc);
+      }
     }
-    }
-    if (threadIdx.x < VTHREADS) {                 // whole waves
+    if constexpr (VDMA) {
+      const dma::DmaTile<T, BKV, DH, 4> vt(&sV[t & 1][0], Vp + (size_t)kb * p.ldq, p.ldq, row_max);
+      if (row_max < BKV - 1) vt.template all<true>();
+      else vt.template all<false>();
+    } else if (threadIdx.x < VTHREADS) {          // whole waves
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
+      for (int j = 0; j < RV; ++j) {
         const int key = min(kb + 4 * vkg + j, k1 - 1);
         rv[j] = *reinterpret_cast<const V4*>(Vp + (size_t)key * p.ldq + 4 * vdg);
       }
@@ -195,7 +237,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void k
   auto store_tile = [&](int buf) {
     if constexpr (!KDMA) {
 #pragma unroll
-      for (int i = 0; i < (CHUNKS + 255) / 256; ++i) {
+      for (int i = 0; i < RK; ++i) {
         const int c = threadIdx.x + i * 256;
         if (c < CHUNKS) {
           const int row = c / CPR, cc = (c % CPR) * EPV;
@@ -203,10 +245,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void k
         }
       }
     }
-    if (threadIdx.x < VTHREADS) {
+    if constexpr (!VDMA) {
+      if (threadIdx.x < VTHREADS) {
 #pragma unroll
-      for (int e = 0; e < 4; ++e)
-        *reinterpret_cast<V4*>(&sVt[buf][(4 * vdg + e) * VS + 4 * vkg]) = VBlock<T>::column(rv, e);
+        for (int e = 0; e < 4; ++e)
+          *reinterpret_cast<V4*>(&sV[buf][(4 * vdg + e) * VS + 4 * vkg]) = VBlock<T>::column(rv, e);
+      }
     }
   };
 
@@ -214,153 +258,187 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void k
   // holds sum_k P[k][q] for the lane's query column (a matrix-core product
   // with a block of ones, from the same rounded P as the numerator).
   f32x4 oacc[DB][2];
-  f32x4 osum[2] = {zero4(), zero4()};
-#pragma unroll
-  for (int b = 0; b < DB; ++b) { oacc[b][0] = zero4(); oacc[b][1] = zero4(); }
-  float mrun[2] = {0.f, 0.f};     // running offset m of each query column (log2 domain)
+  f32x4 osum[2];
 
-  load_tile(0);
-  store_tile(0);
-  dma::wait_loads_then_barrier();
-  for (int t = 0; t < ntiles; ++t) {
-    const int cur = t & 1;
-    const int kvalid = k1 - (k0 + t * BKV);     // keys of this tile that exist (>= 1)
+  // One pass over the segment's key tiles.  EXACT: scores relative to a
+  // running offset m per query column (log2 domain).
+  auto run = [&](auto exact_tag) {
+    constexpr bool EXACT = decltype(exact_tag)::value;
+    osum[0] = zero4();
+    osum[1] = zero4();
+#pragma unroll
+    for (int b = 0; b < DB; ++b) { oacc[b][0] = zero4(); oacc[b][1] = zero4(); }
+    float mrun[2] = {0.f, 0.f};
 
-    // S^T blocks: 4 key blocks x 2 query blocks.  Q arrives pre-scaled by
-    // log2(e) / sqrt(d_head) and every block starts from -m, so the MFMA
-    // leaves the offset score s - m of the log2 domain.
-    f32x4 sacc[4][2];
-    const f32x4 negm[2] = {f32x4{-mrun[0], -mrun[0], -mrun[0], -mrun[0]},
-                           f32x4{-mrun[1], -mrun[1], -mrun[1], -mrun[1]}};
+    load_tile(0);
+    store_tile(0);
+    dma::wait_loads_then_barrier();
+    for (int t = 0; t < ntiles; ++t) {
+      const int cur = t & 1;
+      const int kvalid = k1 - (k0 + t * BKV);     // keys of this tile that exist (>= 1)
+
+      // S^T blocks: 4 key blocks x 2 query blocks; in the exact pass every
+      // block starts from -m, so the MFMA leaves the offset score s - m.
+      f32x4 sacc[4][2];
 #pragma unroll
-    for (int kb = 0; kb < 4; ++kb) {
-      sacc[kb][0] = negm[0];
-      sacc[kb][1] = negm[1];
-#pragma unroll
-      for (int s = 0; s < QS::STEPS; ++s) {
-        const int krow = kb * 16 + col, kcol = s * QS::K + QS::KV * g4;
-        int kidx;
-        if constexpr (KDMA) kidx = dma::swz<T, DH>(krow, kcol);
-        else kidx = krow * KS + kcol;
-        const typename QF::t kf = QF::load(&sK[cur][kidx]);
-        sacc[kb][0] = QF::mma(kf, qf[0][s], sacc[kb][0]);
-        sacc[kb][1] = QF::mma(kf, qf[1][s], sacc[kb][1]);
-      }
-    }
-    // bf16: this tile's V^T fragments for the P V product, read now so that
-    // their LDS latency hides under the softmax.  16x16x32 k slot 8*g4 + i holds
-    // key 32c + 4*g4 + i (i < 4) or 32c + 16 + 4*g4 + (i - 4).
-    bf16x8 vfr[2][DB];
-    if constexpr (sizeof(T) == 2) {
-#pragma unroll
-      for (int c2 = 0; c2 < 2; ++c2)
-#pragma unroll
-        for (int b = 0; b < DB; ++b) {
-          const T* vrow = &sVt[cur][(b * 16 + col) * VS + 32 * c2 + 4 * g4];
-          const uint2 lo = *reinterpret_cast<const uint2*>(vrow);
-          const uint2 hi = *reinterpret_cast<const uint2*>(vrow + 16);
-          vfr[c2][b] = __builtin_bit_cast(bf16x8, make_uint4(lo.x, lo.y, hi.x, hi.y));
+      for (int kb = 0; kb < 4; ++kb) {
+        if constexpr (EXACT) {
+          sacc[kb][0] = f32x4{-mrun[0], -mrun[0], -mrun[0], -mrun[0]};
+          sacc[kb][1] = f32x4{-mrun[1], -mrun[1], -mrun[1], -mrun[1]};
+        } else {
+          sacc[kb][0] = zero4();
+          sacc[kb][1] = zero4();
         }
-    }
-    // the next tile travels global -> registers during this one
-    if (t + 1 < ntiles) load_tile(t + 1);
-
-    // mask keys past the band end (only the last tile has them)
-    if (kvalid < BKV) {
 #pragma unroll
-      for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-        for (int r = 0; r < 4; ++r)
-          if (kb * 16 + 4 * g4 + r >= kvalid) { sacc[kb][0][r] = -INFINITY; sacc[kb][1][r] = -INFINITY; }
-    }
-
-    // Online softmax per query column.  The offset m is the first tile's
-    // maximum and is only raised when a later tile exceeds it by more than
-    // kLazyRescale (a factor 2^8): below that the exponentials stay in range,
-    // and the normalised result does not depend on the offset.  The common
-    // case needs only each lane's own maximum and a wave vote; the exchange
-    // between the 4 lanes of a query column and the O and denominator
-    // rescale run on the few tiles where some offset moves.
-    float mx[2];
-#pragma unroll
-    for (int c = 0; c < 2; ++c) {
-      float m = -INFINITY;
-#pragma unroll
-      for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) m = fmaxf(m, sacc[kb][c][r]);
-      mx[c] = m;                              // this lane's keys, relative to the offset
-    }
-    const bool first = t == 0;
-    if (__ballot(first || mx[0] > kLazyRescale || mx[1] > kLazyRescale)) {
-#pragma unroll
-      for (int c = 0; c < 2; ++c) {
-        float m = fmaxf(mx[c], xor_shfl(mx[c], 16));
-        m = fmaxf(m, xor_shfl(m, 32));        // the column's maximum
-        const float delta = first ? m : fmaxf(m, 0.f);
-        const float alpha = first ? 0.f : fast_exp2(-delta);   // nothing accumulated before the first tile
-        mrun[c] += delta;
-#pragma unroll
-        for (int kb = 0; kb < 4; ++kb) sacc[kb][c] -= delta;
-        osum[c] *= alpha;
-#pragma unroll
-        for (int b = 0; b < DB; ++b) oacc[b][c] *= alpha;
-      }
-    }
-#pragma unroll
-    for (int c = 0; c < 2; ++c)
-#pragma unroll
-      for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) sacc[kb][c][r] = fast_exp2(sacc[kb][c][r]);
-
-    // O^T += V^T P^T
-    if constexpr (sizeof(T) == 2) {
-      bf16x8 ones;
-#pragma unroll
-      for (int i = 0; i < 8; ++i) ones[i] = (bf16)1.0f;
-#pragma unroll
-      for (int c2 = 0; c2 < 2; ++c2) {
-        bf16x8 pf[2];
-#pragma unroll
-        for (int c = 0; c < 2; ++c)
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            pf[c][i] = (bf16)sacc[2 * c2][c][i];
-            pf[c][4 + i] = (bf16)sacc[2 * c2 + 1][c][i];
-          }
-#pragma unroll
-        for (int b = 0; b < DB; ++b) {
-          oacc[b][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vfr[c2][b], pf[0], oacc[b][0], 0, 0, 0);
-          oacc[b][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vfr[c2][b], pf[1], oacc[b][1], 0, 0, 0);
+        for (int s = 0; s < QS::STEPS; ++s) {
+          const int krow = kb * 16 + col, kcol = s * QS::K + QS::KV * g4;
+          int kidx;
+          if constexpr (KDMA) kidx = dma::swz<T, DH>(krow, kcol);
+          else kidx = krow * KS + kcol;
+          const typename QF::t kf = QF::load(&sK[cur][kidx]);
+          sacc[kb][0] = QF::mma(kf, qf[0][s], sacc[kb][0]);
+          sacc[kb][1] = QF::mma(kf, qf[1][s], sacc[kb][1]);
         }
-        osum[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pf[0], osum[0], 0, 0, 0);
-        osum[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pf[1], osum[1], 0, 0, 0);
       }
-    } else {
-      // 16x16x4 fp32: chunk (kb, i) puts key 16kb + 4*g4 + i in slot g4
+      // bf16: this tile's V^T fragments for the P V product, read now so that
+      // their LDS latency hides under the softmax.  16x16x32 k slot 8*g4 + i holds
+      // key 32c + 4*g4 + i (i < 4) or 32c + 16 + 4*g4 + (i - 4).
+      bf16x8 vfr[2][DB];
+      if constexpr (VDMA) {
+        // transposing reads of the row-major tile: source lane (g4, s) addresses
+        // key 32c + 16h + 4*g4 + s/4, dims 16b + 4(s%4) .. + 3, so that lane
+        // (g4, d) receives dim 16b + d of keys 32c + 16h + 4*g4 + e in slot e
 #pragma unroll
-      for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
+        for (int c2 = 0; c2 < 2; ++c2)
 #pragma unroll
           for (int b = 0; b < DB; ++b) {
-            const float vf = to_f32(sVt[cur][(b * 16 + col) * VS + kb * 16 + 4 * g4 + i]);
-            oacc[b][0] = __builtin_amdgcn_mfma_f32_16x16x4f32(vf, sacc[kb][0][i], oacc[b][0], 0, 0, 0);
-            oacc[b][1] = __builtin_amdgcn_mfma_f32_16x16x4f32(vf, sacc[kb][1][i], oacc[b][1], 0, 0, 0);
+            const int key = 32 * c2 + 4 * g4 + (col >> 2), dim = 16 * b + 4 * (col & 3);
+            const uint2 lo = lds_read_tr16(&sV[cur][dma::swz<T, DH>(key, dim)]);
+            const uint2 hi = lds_read_tr16(&sV[cur][dma::swz<T, DH>(key + 16, dim)]);
+            vfr[c2][b] = __builtin_bit_cast(bf16x8, make_uint4(lo.x, lo.y, hi.x, hi.y));
           }
+      } else if constexpr (sizeof(T) == 2) {
 #pragma unroll
-      for (int kb = 0; kb < 4; ++kb)
+        for (int c2 = 0; c2 < 2; ++c2)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          osum[0] = __builtin_amdgcn_mfma_f32_16x16x4f32(1.0f, sacc[kb][0][i], osum[0], 0, 0, 0);
-          osum[1] = __builtin_amdgcn_mfma_f32_16x16x4f32(1.0f, sacc[kb][1][i], osum[1], 0, 0, 0);
-        }
-    }
+          for (int b = 0; b < DB; ++b) {
+            const T* vrow = &sV[cur][(b * 16 + col) * VS + 32 * c2 + 4 * g4];
+            const uint2 lo = *reinterpret_cast<const uint2*>(vrow);
+            const uint2 hi = *reinterpret_cast<const uint2*>(vrow + 16);
+            vfr[c2][b] = __builtin_bit_cast(bf16x8, make_uint4(lo.x, lo.y, hi.x, hi.y));
+          }
+      }
+      // the next tile travels during this one
+      if (t + 1 < ntiles) load_tile(t + 1);
 
-    if (t + 1 < ntiles) store_tile(cur ^ 1);
-    dma::wait_loads_then_barrier();  // the next tile's direct loads (if any) in place
-  }
+      // mask keys past the band end (only the last tile has them)
+      if (kvalid < BKV) {
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            if (kb * 16 + 4 * g4 + r >= kvalid) { sacc[kb][0][r] = -INFINITY; sacc[kb][1][r] = -INFINITY; }
+      }
+
+      if constexpr (EXACT) {
+        // The offset m is the first tile's maximum and is only raised when a
+        // later tile exceeds it by more than kLazyRescale (a factor 2^8):
+        // below that the exponentials stay in range, and the normalised
+        // result does not depend on the offset.  The common case needs only
+        // each lane's own maximum and a wave vote; the exchange between the 4
+        // lanes of a query column and the O and denominator rescale run on
+        // the few tiles where some offset moves.
+        float mx[2];
+#pragma unroll
+        for (int c = 0; c < 2; ++c) {
+          float m = -INFINITY;
+#pragma unroll
+          for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) m = fmaxf(m, sacc[kb][c][r]);
+          mx[c] = m;                              // this lane's keys, relative to the offset
+        }
+        const bool first = t == 0;
+        if (__ballot(first || mx[0] > kLazyRescale || mx[1] > kLazyRescale)) {
+#pragma unroll
+          for (int c = 0; c < 2; ++c) {
+            float m = fmaxf(mx[c], xor_shfl(mx[c], 16));
+            m = fmaxf(m, xor_shfl(m, 32));        // the column's maximum
+            const float delta = first ? m : fmaxf(m, 0.f);
+            const float alpha = first ? 0.f : fast_exp2(-delta);   // nothing accumulated before the first tile
+            mrun[c] += delta;
+#pragma unroll
+            for (int kb = 0; kb < 4; ++kb) sacc[kb][c] -= delta;
+            osum[c] *= alpha;
+#pragma unroll
+            for (int b = 0; b < DB; ++b) oacc[b][c] *= alpha;
+          }
+        }
+      }
+#pragma unroll
+      for (int c = 0; c < 2; ++c)
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) sacc[kb][c][r] = fast_exp2(sacc[kb][c][r]);
+
+      // O^T += V^T P^T
+      if constexpr (sizeof(T) == 2) {
+        bf16x8 ones;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) ones[i] = (bf16)1.0f;
+#pragma unroll
+        for (int c2 = 0; c2 < 2; ++c2) {
+          bf16x8 pf[2];
+#pragma unroll
+          for (int c = 0; c < 2; ++c)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              pf[c][i] = (bf16)sacc[2 * c2][c][i];
+              pf[c][4 + i] = (bf16)sacc[2 * c2 + 1][c][i];
+            }
+#pragma unroll
+          for (int b = 0; b < DB; ++b) {
+            oacc[b][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vfr[c2][b], pf[0], oacc[b][0], 0, 0, 0);
+            oacc[b][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vfr[c2][b], pf[1], oacc[b][1], 0, 0, 0);
+          }
+          osum[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pf[0], osum[0], 0, 0, 0);
+          osum[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pf[1], osum[1], 0, 0, 0);
+        }
+      } else {
+        // 16x16x4 fp32: chunk (kb, i) puts key 16kb + 4*g4 + i in slot g4
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int b = 0; b < DB; ++b) {
+              const float vf = to_f32(sV[cur][(b * 16 + col) * VS + kb * 16 + 4 * g4 + i]);
+              oacc[b][0] = __builtin_amdgcn_mfma_f32_16x16x4f32(vf, sacc[kb][0][i], oacc[b][0], 0, 0, 0);
+              oacc[b][1] = __builtin_amdgcn_mfma_f32_16x16x4f32(vf, sacc[kb][1][i], oacc[b][1], 0, 0, 0);
+            }
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            osum[0] = __builtin_amdgcn_mfma_f32_16x16x4f32(1.0f, sacc[kb][0][i], osum[0], 0, 0, 0);
+            osum[1] = __builtin_amdgcn_mfma_f32_16x16x4f32(1.0f, sacc[kb][1][i], osum[1], 0, 0, 0);
+          }
+      }
+
+      if (t + 1 < ntiles) store_tile(cur ^ 1);
+      dma::wait_loads_then_barrier();  // the next tile's direct loads (if any) in place
+    }
+  };
+
+  if (threadIdx.x == 0) s_redo = 0;   // published by the first tile's barrier
+  run(std::false_type{});
+  // every query column's sum inside the bounds (NaN fails the test too)?
+  const bool ok = osum[0][0] >= kFastSumLo && osum[0][0] <= kFastSumHi && osum[1][0] >= kFastSumLo &&
+                  osum[1][0] <= kFastSumHi;
+  if (__ballot(!ok) && lane == 0) s_redo = 1;
+  __syncthreads();
+  if (s_redo) run(std::true_type{});   // work-group-uniform
 
   // ---- normalise and store ---------------------------------------------------------
 #pragma unroll

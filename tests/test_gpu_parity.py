@@ -312,3 +312,106 @@ def test_edge_cases(label, over, kind, dtype):
     ref = p if dtype == "f32" else pg
     check_placements(logits, ref["logits"], r.placements.cpu().numpy(), base.sample_seed, g.graph_ptr,
                      max_exempt=0.2)
+
+
+# ----------------------------------------------------------------------------
+# Attention scores outside the range of the max-free softmax pass (a query's
+# largest score above 2^100 in the log2 domain): the work-groups that see them
+# repeat their segment with the running-offset softmax.
+def _scaled_q(cfg, w, factor):
+    """The weights with the q rows of every W_qkv and b_qkv multiplied by a
+    power of two (exact in both precisions)."""
+    d = cfg.d_model
+    out = W.Weights(gnn=w.gnn, placer=[], head=w.head)
+    for layer in w.placer:
+        layer = dict(layer)
+        wq, bq = layer["w_qkv"][0].copy(), layer["b_qkv"][0].copy()
+        wq[:d] *= factor
+        bq[:d] *= factor
+        layer["w_qkv"], layer["b_qkv"] = W._finish(cfg, wq), W._finish(cfg, bq)
+        out.placer.append(layer)
+    return out
+
+
+def _layer0_scores_log2(cfg, w, y, graph_ptr):
+    """Every band score of the first layer (FiLM off: its input is y), in the
+    log2 domain the kernel works in, per (head, query): (max, min)."""
+    d, H = cfg.d_model, cfg.heads
+    dh = d // H
+    wqkv, bqkv = w.placer[0]["w_qkv"][0], w.placer[0]["b_qkv"][0]
+    qkv = y @ wqkv.T + bqkv
+    hi, lo = [], []
+    for g in range(len(graph_ptr) - 1):
+        gs, ge = graph_ptr[g], graph_ptr[g + 1]
+        for s0 in range(gs, ge, cfg.seg_len):
+            s1 = min(s0 + cfg.seg_len, ge)
+            k0 = max(gs, s0 - cfg.mem_len)
+            for h in range(H):
+                q = qkv[s0:s1, h * dh:(h + 1) * dh]
+                k = qkv[k0:s1, d + h * dh:d + (h + 1) * dh]
+                s = q @ k.T / np.sqrt(dh) / np.log(2.0)
+                hi.append(s.max(axis=1))
+                lo.append(s.min(axis=1))
+    return np.concatenate(hi), np.concatenate(lo)
+
+
+def test_attention_large_scores_fp32():
+    """fp32 keeps such scores well conditioned: the full tolerance applies."""
+    cfg = W.get_config("tiny_layered_256").replace(film=False)
+    g, w = W.make_graph(cfg), W.make_weights(cfg)
+    r = _runner(cfg, g, w)
+    r.embed()
+    _sync()
+    y = to_np(r.node_emb)
+    smax, _ = _layer0_scores_log2(cfg, w, y, g.graph_ptr)
+    factor = 2.0 ** np.ceil(np.log2(101.0 / smax.max()))
+    assert factor >= 2.0
+    w2 = _scaled_q(cfg, w, factor)
+    smax2, _ = _layer0_scores_log2(cfg, w2, y, g.graph_ptr)
+    _log(f"large scores fp32: q scale {factor:g}, layer-0 max score 2^{smax2.max():.1f}, "
+         f"{int((smax2 > 100).sum())} of {smax2.size} query rows beyond 2^100")
+    assert (smax2 > 100).any() and (smax2 <= 100).any()
+    r2 = _runner(cfg, g, w2)
+    r2.embed()
+    r2.place()
+    _sync()
+    p = oracle_place(cfg, w2, to_np(r2.node_emb), to_np(r2.graph_emb), g.graph_ptr)
+    err_l = rel_err_rows(to_np(r2.logits), p["logits"])
+    err_s = rel_err_rows(to_np(r2.lse), p["lse"])
+    _log(f"  logits err {err_l:.3e}  lse err {err_s:.3e}")
+    assert err_l <= TOL["f32"] and err_s <= TOL["f32"]
+
+
+@pytest.mark.parametrize("sign", [1.0, -1.0])
+def test_attention_large_scores_bf16_uniform(sign):
+    """bf16: identical node rows give every key the same score, so the softmax
+    is uniform however large the scores, and bf16 rounding cannot tilt it.
+    Scores of 2^+-150 and beyond overflow or vanish in the max-free pass."""
+    cfg = W.get_config("tiny_layered_256").replace(dtype="bf16", film=False, **BF16_WIDTH)
+    n = cfg.graph_sizes[0]
+    x = W.make_features(cfg, n, np.random.default_rng(1))
+    x[:] = x[0]
+    g = W.graph_from_arrays(cfg, [0, n], [0] * (n + 1), np.array([], np.int32), x)
+    w = W.make_weights(cfg)
+    r = _runner(cfg, g, w)
+    r.embed()
+    _sync()
+    y = to_np(r.node_emb)
+    assert np.array_equal(y, np.broadcast_to(y[0], y.shape))
+    smax, smin = _layer0_scores_log2(cfg, w, y, g.graph_ptr)
+    s0 = np.abs(np.concatenate([smax, smin])).max()
+    assert s0 > 0
+    factor = sign * 2.0 ** np.ceil(np.log2(150.0 / s0))
+    w2 = _scaled_q(cfg, w, factor)
+    smax2, smin2 = _layer0_scores_log2(cfg, w2, y, g.graph_ptr)
+    _log(f"large scores bf16 uniform: q scale {factor:g}, layer-0 scores in 2^[{smin2.min():.1f}, {smax2.max():.1f}]")
+    assert (smax2 > 100).any() or (smax2 < -60).any()
+    r2 = _runner(cfg, g, w2)
+    r2.embed()
+    r2.place()
+    _sync()
+    p = oracle_place(cfg, w2, to_np(r2.node_emb), to_np(r2.graph_emb), g.graph_ptr)
+    err_l = rel_err_rows(to_np(r2.logits), p["logits"])
+    _log(f"  logits err {err_l:.3e}")
+    assert np.isfinite(to_np(r2.logits)).all()
+    assert err_l <= TOL["bf16"]

@@ -423,3 +423,57 @@ def test_row_gemm_chunk_schedule(R, nk):
         last_read[("W", c % 2)] = c
     assert sorted(x[1] for x in issued if x[0] == "A") == list(range(nk))
     assert sorted(x[1] for x in issued if x[0] == "W") == list(range(nk))
+
+
+# ---- segment attention: V tiles read back transposed ---------------------------
+# ds_read_b64_tr_b16: within each group of 16 lanes, destination lane 4q + p
+# receives in slot e element p of the 8-byte word addressed by source lane 4e + q.
+ATTN_BKV = 64
+
+
+def _tr16(word_elem):
+    """Element offset that (lane, slot) receives, given each lane's word address."""
+    out = {}
+    for lane in range(64):
+        grp, i = lane // 16, lane % 16
+        q, p = i // 4, i % 4
+        for e in range(4):
+            out[(lane, e)] = word_elem[16 * grp + 4 * e + q] + p
+    return out
+
+
+@pytest.mark.parametrize("dh", [32, 64])
+@pytest.mark.parametrize("row_max", [63, 40, 0])
+def test_attention_v_fragments(dh, row_max):
+    """Direct loads put the V tile in LDS row-major and swizzled; the transposing
+    reads give lane (g4, d) dim 16b + d of the keys its MFMA k slots stand for
+    (slot 8*g4 + i: key 32c + 4*g4 + i, or 32c + 16 + 4*g4 + i - 4), and each
+    read's 32-lane halves touch distinct banks."""
+    epv = 8
+    ld = 3 * 8 * dh
+    moved = _dma_tile(ATTN_BKV, dh, 2, ld, row_max, nw=4)
+    tile = {t: (min(r, row_max), c) for t, _, r, c in moved}
+    assert sorted(tile) == list(range(ATTN_BKV * dh))
+    for c2 in range(2):
+        for b in range(dh // 16):
+            frag = {}
+            for h in range(2):
+                words = []
+                for lane in range(64):
+                    col, g4 = lane % 16, lane // 16
+                    key, dim = 32 * c2 + 16 * h + 4 * g4 + (col >> 2), 16 * b + 4 * (col & 3)
+                    w = _swz(dh, epv, key, dim)
+                    assert w % 4 == 0 and w // epv == (w + 3) // epv   # 8 aligned bytes in one granule
+                    words.append(w)
+                for half in range(2):
+                    banks = set()
+                    for w in words[32 * half:32 * half + 32]:
+                        banks |= {(2 * w // 4 + k) % 64 for k in range(2)}
+                    assert len(banks) == 64
+                for (lane, e), t in _tr16(words).items():
+                    frag[(lane, 4 * h + e)] = tile[t]
+            for lane in range(64):
+                col, g4 = lane % 16, lane // 16
+                for i in range(8):
+                    key = 32 * c2 + 4 * g4 + (i if i < 4 else 16 + i - 4)
+                    assert frag[(lane, i)] == (min(key, row_max), 16 * b + col)
