@@ -12,8 +12,9 @@
 // [32w, 32w + 32) as two 16-column MFMA blocks.  Scores are formed transposed,
 // S^T = K Q^T, so that a lane owns one query column: the row max is an
 // in-lane max plus a 4-way exchange, and the probabilities feed the P V
-// product (O^T = V^T P^T) straight from the score registers.  K and V tiles
-// are double-buffered in LDS over 64-key tiles.
+// product (O^T = V^T P^T) straight from the score registers.  K and V move
+// through LDS in 64-key tiles: by direct loads into a ring of three buffers
+// (bf16, d_h >= 32), otherwise through registers into two.
 #include <type_traits>
 
 #include "device_common.h"
@@ -96,6 +97,11 @@ template <> struct VBlock<float> {
   }
 };
 
+// stands in for dma::RowStream where tiles go through registers
+struct NoStream {
+  __device__ __forceinline__ NoStream(const void*, int) {}
+};
+
 }  // namespace
 
 // Bounds of the max-free pass (see the kernel): a query column's sum of 2^s
@@ -110,6 +116,8 @@ template <typename T, int DH>
 struct AttnCfg {
   static constexpr bool KDMA = sizeof(T) == 2 && DH >= 32;
   static constexpr bool VDMA = KDMA;
+  // tile buffers: with direct loads a ring of three, loads two tiles ahead
+  static constexpr int NS = VDMA ? 3 : 2;
   static constexpr int WPE = DH >= 64 || (sizeof(T) == 4 && DH >= 32) ? 2 : 4;   // waves per SIMD the registers allow
 };
 
@@ -150,8 +158,9 @@ void k_seg_attention(AttnArgs<T> p, GraphTable gt) {
   constexpr int DB = DH / 16;           // 16-row blocks of the head dim
   using QS = QkShape<T, DH>;
   using QF = QkFrag<T, DH>;
-  __shared__ __attribute__((aligned(16))) T sK[2][BKV * KS];
-  __shared__ __attribute__((aligned(16))) T sV[2][VDMA ? BKV * DH : DH * VS];
+  constexpr int NS = AttnCfg<T, DH>::NS;
+  __shared__ __attribute__((aligned(16))) T sK[NS][BKV * KS];
+  __shared__ __attribute__((aligned(16))) T sV[NS][VDMA ? BKV * DH : DH * VS];
   __shared__ int s_redo;
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -182,13 +191,15 @@ void k_seg_attention(AttnArgs<T> p, GraphTable gt) {
 
   // ---- Q fragments (B operand of S^T = K Q^T), kept in registers -------------
   typename QF::t qf[2][QS::STEPS];
+  auto load_q = [&]() {
 #pragma unroll
-  for (int c = 0; c < 2; ++c) {
-    const int q = q0 + wave * 32 + c * 16 + col;
+    for (int c = 0; c < 2; ++c) {
+      const int q = q0 + wave * 32 + c * 16 + col;
 #pragma unroll
-    for (int s = 0; s < QS::STEPS; ++s)
-      qf[c][s] = q < qend ? QF::load(Qp + (size_t)q * p.ldq + s * QS::K + QS::KV * g4) : QF::zero();
-  }
+      for (int s = 0; s < QS::STEPS; ++s)
+        qf[c][s] = q < qend ? QF::load(Qp + (size_t)q * p.ldq + s * QS::K + QS::KV * g4) : QF::zero();
+    }
+  };
 
   // ---- K / V tile staging -------------------------------------------------------
   // Register path: K in 16-byte chunks of key rows; V transposed, each thread
@@ -204,15 +215,26 @@ void k_seg_attention(AttnArgs<T> p, GraphTable gt) {
   uint4 rk[RK] = {};
   V4 rv[RV] = {};
   const int vkg = threadIdx.x % (BKV / 4), vdg = threadIdx.x / (BKV / 4);
-  auto load_tile = [&](int t) {
+  // direct loads per wave and tile (K and V)
+  constexpr int VMT = VDMA ? 2 * (BKV * DH / EPV) / (64 * 4) : 0;
+  // direct loads: the key rows of the band, one 64-row block per tile
+  using Stream = typename std::conditional<KDMA, dma::RowStream<T, BKV, DH, 4>, NoStream>::type;
+  const Stream kstream(Kp + (size_t)k0 * p.ldq, p.ldq);
+  const Stream vstream(Vp + (size_t)k0 * p.ldq, p.ldq);
+  auto load_tile = [&](int t, int buf) {
     const int kb = k0 + t * BKV;
     // keys past the band end read the last valid row: their scores are masked
     // to -inf, so they carry P = 0 against finite values
     const int row_max = k1 - 1 - kb;
     if constexpr (KDMA) {
-      const dma::DmaTile<T, BKV, DH, 4> kt(&sK[t & 1][0], Kp + (size_t)kb * p.ldq, p.ldq, row_max);
-      if (row_max < BKV - 1) kt.template all<true>();
-      else kt.template all<false>();
+      static_assert(VDMA, "K and V move the same way");
+      if (row_max < BKV - 1) {
+        kstream.template load<true>(&sK[buf][0], t * BKV, row_max);
+        vstream.template load<true>(&sV[buf][0], t * BKV, row_max);
+      } else {
+        kstream.template load<false>(&sK[buf][0], t * BKV, row_max);
+        vstream.template load<false>(&sV[buf][0], t * BKV, row_max);
+      }
     } else {
 #pragma unroll
       for (int i = 0; i < RK; ++i) {
@@ -222,15 +244,13 @@ void k_seg_attention(AttnArgs<T> p, GraphTable gt) {
         if (CHUNKS % 256 == 0 || c < CHUNKS) rk[i] = *reinterpret_cast<const uint4*>(Kp + (size_t)key * p.ldq + cc);
       }
     }
-    if constexpr (VDMA) {
-      const dma::DmaTile<T, BKV, DH, 4> vt(&sV[t & 1][0], Vp + (size_t)kb * p.ldq, p.ldq, row_max);
-      if (row_max < BKV - 1) vt.template all<true>();
-      else vt.template all<false>();
-    } else if (threadIdx.x < VTHREADS) {          // whole waves
+    if constexpr (!VDMA) {
+      if (threadIdx.x < VTHREADS) {               // whole waves
 #pragma unroll
-      for (int j = 0; j < RV; ++j) {
-        const int key = min(kb + 4 * vkg + j, k1 - 1);
-        rv[j] = *reinterpret_cast<const V4*>(Vp + (size_t)key * p.ldq + 4 * vdg);
+        for (int j = 0; j < RV; ++j) {
+          const int key = min(kb + 4 * vkg + j, k1 - 1);
+          rv[j] = *reinterpret_cast<const V4*>(Vp + (size_t)key * p.ldq + 4 * vdg);
+        }
       }
     }
   };
@@ -270,11 +290,22 @@ void k_seg_attention(AttnArgs<T> p, GraphTable gt) {
     for (int b = 0; b < DB; ++b) { oacc[b][0] = zero4(); oacc[b][1] = zero4(); }
     float mrun[2] = {0.f, 0.f};
 
-    load_tile(0);
+    // Tile t sits in buffer t % NS.  Direct loads: tiles t + 1 and t + 2 are
+    // in flight while tile t is consumed, and a tile's end waits for the
+    // older of the two only.  Register path: tile t + 1 travels through
+    // registers during tile t and is stored at its end.
+    // Q is requested in the first pass after the first tiles, and the wait
+    // for all of them is one the compiler sees: inside the loop it then
+    // tracks no outstanding loads of its own, and the only waits there are
+    // the explicit ones for the tiles.
+    load_tile(0, 0);
+    if (VDMA && ntiles > 1) load_tile(1, 1);
+    if constexpr (!EXACT) load_q();
     store_tile(0);
     dma::wait_loads_then_barrier();
+    int cur = 0;
     for (int t = 0; t < ntiles; ++t) {
-      const int cur = t & 1;
+      const int nxt = cur + 1 == NS ? 0 : cur + 1;
       const int kvalid = k1 - (k0 + t * BKV);     // keys of this tile that exist (>= 1)
 
       // S^T blocks: 4 key blocks x 2 query blocks; in the exact pass every
@@ -328,8 +359,11 @@ void k_seg_attention(AttnArgs<T> p, GraphTable gt) {
             vfr[c2][b] = __builtin_bit_cast(bf16x8, make_uint4(lo.x, lo.y, hi.x, hi.y));
           }
       }
-      // the next tile travels during this one
-      if (t + 1 < ntiles) load_tile(t + 1);
+      if constexpr (VDMA) {
+        if (t + 2 < ntiles) load_tile(t + 2, nxt + 1 == NS ? 0 : nxt + 1);
+      } else {
+        if (t + 1 < ntiles) load_tile(t + 1, nxt);
+      }
 
       // mask keys past the band end (only the last tile has them)
       if (kvalid < BKV) {
@@ -426,8 +460,15 @@ void k_seg_attention(AttnArgs<T> p, GraphTable gt) {
           }
       }
 
-      if (t + 1 < ntiles) store_tile(cur ^ 1);
-      dma::wait_loads_then_barrier();  // the next tile's direct loads (if any) in place
+      if constexpr (VDMA) {
+        // tile t + 1 in place; buffer cur free for tile t + 3
+        if (t + 2 < ntiles) dma::wait_vm_barrier<VMT>();
+        else dma::wait_vm_barrier<0>();
+      } else {
+        if (t + 1 < ntiles) store_tile(nxt);
+        dma::wait_loads_then_barrier();
+      }
+      cur = nxt;
     }
   };
 

@@ -921,10 +921,7 @@ template hipError_t launch_pre_layer<bf16>(const PreLayerArgs<bf16>&, const Grap
 // issues W(c) and then A(c + R - 2); in this loop the loads are a wave's only
 // memory operations and complete in order, so chunk c waits for all but the
 // A(c + R - 2) loads (vmcnt) before its barrier.
-template <int N>
-__device__ __forceinline__ void wait_vm_barrier() {
-  asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"i"(N) : "memory");
-}
+using dma::wait_vm_barrier;
 
 template <typename T, int D, int EPI>
 __global__ __launch_bounds__(LNT) void k_row_gemm(GemmArgs<T, T, T> p) {

@@ -108,12 +108,62 @@ struct DmaTile {
   }
 };
 
+// The tile of DmaTile taken again and again from ROWS-row blocks of one
+// matrix: the per-lane offsets are formed once, and a block's loads add only
+// the block's row offset to the scalar base.
+template <typename T, int ROWS, int COLS, int NW>
+struct RowStream {
+  using Tile = DmaTile<T, ROWS, COLS, NW>;
+  static constexpr int PER = Tile::PER, EPV = Tile::EPV, GPR = Tile::GPR;
+  gptr_t base;          // row 0 of block 0
+  int ld;
+  uint32_t off[PER];    // per lane and piece: row * ld + swizzled column, in bytes
+  __device__ __forceinline__ RowStream(const T* src, int ld_) : base(uniform_base(src)), ld(ld_) {
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int lane = threadIdx.x & 63;
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int q = (wave * PER + i) * 64, rb = q / GPR, lr = lane / GPR;
+      const int g = (lane % GPR) ^ swz_key<GPR>(lr) ^ swz_key<GPR>(rb);
+      off[i] = ((uint32_t)(rb + lr) * (uint32_t)ld + (uint32_t)(g * EPV)) * (uint32_t)sizeof(T);
+    }
+  }
+  // The block whose first row is r0 into tile; with CLAMP, rows past row_max
+  // (counted from r0) read row row_max instead.
+  template <bool CLAMP>
+  __device__ __forceinline__ void load(T* tile, int r0, int row_max) const {
+    const gptr_t b = base + (size_t)r0 * ld * sizeof(T);
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int q = (wave * PER + i) * 64;
+      uint32_t o = off[i];
+      if (CLAMP) {
+        const int lane = threadIdx.x & 63, rb = q / GPR, lr = lane / GPR;
+        const int g = (lane % GPR) ^ swz_key<GPR>(lr) ^ swz_key<GPR>(rb);
+        const int row = rb + lr < row_max ? rb + lr : row_max;
+        o = ((uint32_t)row * (uint32_t)ld + (uint32_t)(g * EPV)) * (uint32_t)sizeof(T);
+      }
+      dma16(b, o, tile + q * EPV);
+    }
+  }
+};
+
 // Barrier after which the data of every direct load issued before it by any
 // wave is in LDS.  (The work-group fence of a plain barrier does not cover
 // those loads, so each wave first waits for all of its own memory operations.)
 __device__ __forceinline__ void wait_loads_then_barrier() {
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
+}
+
+// Barrier after which all but the N most recent vector memory operations of
+// every wave are done.  Valid where a wave's outstanding vector memory
+// operations are all loads, which complete in issue order; LDS operations
+// are drained too.
+template <int N>
+__device__ __forceinline__ void wait_vm_barrier() {
+  asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"i"(N) : "memory");
 }
 
 }  // namespace dma
