@@ -254,6 +254,24 @@ def placer_band(node_emb, graph_ptr, gamma, beta, placer_layers, n_heads, seg_le
     return x
 
 
+# ----------------------------------------------------------------------------
+# Section 4.3 (ablation): the placement network with no attention.
+# ----------------------------------------------------------------------------
+
+def placer_no_attention(node_emb, graph_ptr, gamma, beta, placer_layers):
+    """Every placer layer without its attention sublayer: the conditioned input
+    y = gamma * x + beta goes straight to the feed-forward sublayer,
+    x <- LN(y + FFN(y)) with the layer's second LayerNorm.  Each node's result
+    depends only on its own row and its graph's conditioning."""
+    N, d = node_emb.shape
+    x = np.array(node_emb, dtype=np.float64)
+    gid = np.searchsorted(np.asarray(graph_ptr), np.arange(N), side="right") - 1
+    for l, lw in enumerate(placer_layers):
+        y = gamma[gid, l] * x + beta[gid, l]
+        x = layer_norm(y + ffn(y, lw), lw["ln2_g"], lw["ln2_b"])
+    return x
+
+
 def head(x, w_out, b_out):
     """Per-node device logits (Fig. 1: N x d output) and their log-sum-exp."""
     logits = x @ w_out.T + b_out
@@ -261,10 +279,15 @@ def head(x, w_out, b_out):
 
 
 def place(node_emb, graph_emb, graph_ptr, placer_layers, w_out, b_out, n_heads,
-          seg_len, mem_len, film=True, formulation="recurrent"):
+          seg_len, mem_len, film=True, formulation="recurrent", attention=True):
+    """The placement network and head; attention=False is the ablation's
+    placer without attention (n_heads, seg_len and mem_len then unused)."""
     gamma, beta = film_params(graph_emb, placer_layers, film)
-    fn = placer_recurrent if formulation == "recurrent" else placer_band
-    x = fn(node_emb, graph_ptr, gamma, beta, placer_layers, n_heads, seg_len, mem_len)
+    if not attention:
+        x = placer_no_attention(node_emb, graph_ptr, gamma, beta, placer_layers)
+    else:
+        fn = placer_recurrent if formulation == "recurrent" else placer_band
+        x = fn(node_emb, graph_ptr, gamma, beta, placer_layers, n_heads, seg_len, mem_len)
     logits, lse = head(x, w_out, b_out)
     return {"x": x, "logits": logits, "lse": lse, "gamma": gamma, "beta": beta}
 

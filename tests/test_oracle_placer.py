@@ -210,3 +210,74 @@ def test_i7_ragged_batch_equals_separate_graphs():
         np.testing.assert_allclose(full["node_emb"][sl], one["node_emb"], rtol=0, atol=1e-12)
         np.testing.assert_allclose(full["graph_emb"][i], one["graph_emb"][0], rtol=0, atol=1e-12)
         np.testing.assert_allclose(full["logits"][sl], one["logits"], rtol=0, atol=1e-11)
+
+
+# ---- the ablation's placer without attention (Section 4.3) ---------------------
+def _normalised_rows(rng, n, d, eps=1e-5):
+    """Rows of zero mean and biased variance 1 - eps: LayerNorm with gain 1 and
+    shift 0 maps them to themselves exactly."""
+    y = rng.normal(size=(n, d))
+    y -= y.mean(axis=1, keepdims=True)
+    y *= np.sqrt((1.0 - eps) / (y * y).mean(axis=1, keepdims=True))
+    return y
+
+
+@pytest.mark.parametrize("film", [False, True])
+def test_no_attention_layer_equals_torch_encoder_with_neutral_attention(film):
+    """A Transformer layer whose attention sublayer contributes nothing (each
+    node attends only to itself, V = 0, b_o = 0) and whose first LayerNorm is
+    the identity on its input (gain 1, shift 0, rows of variance 1 - eps) is
+    exactly the no-attention layer: torch's encoder layer pins it."""
+    c, pl, _ = _placer(placer_layers=1)
+    d = c.d_model
+    lw = dict(pl[0])
+    rng = np.random.default_rng(3)
+    G, per = 2, 20
+    gp = np.array([0, per, 2 * per])
+    y = _normalised_rows(rng, G * per, d)
+    if film:
+        x0 = rng.normal(size=(G, d))
+        gamma, beta = O.film_params(x0, [lw], film=True)
+        gid = np.repeat(np.arange(G), per)
+        x = (y - beta[gid, 0]) / gamma[gid, 0]        # conditioned input = y
+    else:
+        gamma, beta = O.film_params(np.zeros((G, d)), [lw], film=False)
+        x = y
+    ours = O.placer_no_attention(x, gp, gamma, beta, [lw])
+    t = dict(lw)
+    t["w_qkv"] = lw["w_qkv"].copy()
+    t["w_qkv"][2 * d:] = 0.0
+    t["b_qkv"] = lw["b_qkv"].copy()
+    t["b_qkv"][2 * d:] = 0.0
+    t["b_o"] = np.zeros(d)
+    t["ln1_g"], t["ln1_b"] = np.ones(d), np.zeros(d)
+    n = G * per
+    self_only = np.where(np.eye(n, dtype=bool), 0.0, -np.inf)
+    ref = _torch_run(_torch_stack([t], d, c.heads, c.d_ff), y, mask=self_only)
+    np.testing.assert_allclose(ours, ref, rtol=0, atol=1e-10)
+
+
+def test_no_attention_placer_is_row_local():
+    """Changing other rows of the same graph leaves a row's result unchanged,
+    and permuting a graph's rows permutes its results."""
+    c, pl, hd = _placer()
+    d = c.d_model
+    rng = np.random.default_rng(4)
+    N = 40
+    gp = np.array([0, 25, N])
+    x = rng.normal(size=(N, d))
+    gamma, beta = O.film_params(rng.normal(size=(2, d)), pl, film=True)
+    base = O.placer_no_attention(x, gp, gamma, beta, pl)
+    x2 = x.copy()
+    x2[[1, 7, 30]] += rng.normal(size=(3, d))
+    other = O.placer_no_attention(x2, gp, gamma, beta, pl)
+    keep = np.setdiff1d(np.arange(N), [1, 7, 30])
+    np.testing.assert_array_equal(base[keep], other[keep])
+    perm = np.concatenate([rng.permutation(25), 25 + rng.permutation(N - 25)])
+    np.testing.assert_allclose(O.placer_no_attention(x[perm], gp, gamma, beta, pl), base[perm], rtol=0, atol=1e-12)
+    # and the graph's own conditioning is what a row sees: moving a row to the other graph changes it
+    moved = O.placer_no_attention(x, np.array([0, 24, N]), gamma, beta, pl)
+    assert not np.allclose(moved[24], base[24])
+    p = O.place(x, rng.normal(size=(2, d)), gp, pl, hd["w_out"], hd["b_out"], c.heads, c.seg_len, c.mem_len,
+                attention=False)
+    assert p["logits"].shape == (N, c.n_devices)
