@@ -54,6 +54,8 @@ def flop_model(cfg, g, stats):
         # the last layer) the next layer's QKV projection
         "post_attn": ("mfma", 2.0 * N * d * d + 4.0 * N * d * dff
                       + (cfg.placer_layers - 1) / cfg.placer_layers * 2.0 * N * d * 3 * d),
+        # the ablation's placer without attention: every layer's FFN and the head, one launch
+        "mlp_placer": ("mfma", 4.0 * N * d * dff * cfg.placer_layers + 2.0 * N * d * cfg.n_devices),
     }, keys
 
 
@@ -193,6 +195,33 @@ def main():
             ent.update({"achieved": rf["achieved"], "unit": rf["unit"], "frac": rf["frac"], "bound": rf["bound"]})
         kernels.append(ent)
 
+    # The ablation's placer without attention (Section 4.3) on the same DAG and
+    # weights: the same embed and sample calls around one fused placer kernel.
+    ab = gdp.Runner(gdp.DeviceGraph(g, cfg.dtype), gdp.DevicePolicy(cfg, w, attention=False), cfg.k_samples)
+    for _ in range(max(1, args.warmup)):
+        ab.forward(seed)
+    torch.cuda.synchronize()
+    gdp.timer_begin(range(gdp.K_COUNT))
+    ab.forward(seed)
+    ab_breakdown = gdp.timer_end()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        ab.forward(seed)
+    torch.cuda.synchronize()
+    ab_elapsed = time.perf_counter() - t0
+    ab_kernels = []
+    for kind, v in sorted(ab_breakdown.items(), key=lambda kv: -kv[1]["ms"]):
+        ent = {"kernel": kind, "ms_per_step": round(v["ms"], 4), "launches": v["launches"]}
+        rf = roof(kind, v["ms"], v["launches"])
+        if rf:
+            ent.update({"achieved": rf["achieved"], "unit": rf["unit"], "frac": rf["frac"], "bound": rf["bound"]})
+        ab_kernels.append(ent)
+    ablation = {"placer": "no attention (Section 4.3 ablation), all layers in one kernel",
+                "value": round(g.n_nodes * args.steps / ab_elapsed, 1), "unit": "nodes/s",
+                "ms_per_step": round(1e3 * ab_elapsed / args.steps, 4), "kernels": ab_kernels}
+    del ab
+
     cpu = None
     if args.cpu_sample != 0:
         cores = min(16, len(os.sched_getaffinity(0)))
@@ -211,6 +240,7 @@ def main():
         "roofline": roofline,
         "cpu_baseline": cpu,
         "kernels": kernels,
+        "ablation_no_attention": ablation,
     }
     print(json.dumps(out), flush=True)
 

@@ -52,7 +52,7 @@
 extern "C" {
 #endif
 
-#define GDP_ABI_VERSION 1
+#define GDP_ABI_VERSION 2
 
 /* Limits of this implementation (violations return GDP_E_UNSUPPORTED). */
 #define GDP_MAX_GRAPHS 128   /* graphs per ragged batch                      */
@@ -147,6 +147,13 @@ typedef struct gdp_placer_layer {
   const void *ln2_g, *ln2_b;      /* [d], [d]                               */
 } gdp_placer_layer;
 
+/*
+ * attention = 0 selects the placement network of the paper's ablation
+ * (Section 4.3) that has no attention: each layer is then
+ *   Y = FiLM_l(X),  X <- LN(Y + W_2 ReLU(W_1 Y + b_1) + b_2)   (LayerNorm ln2)
+ * and w_qkv, b_qkv, w_o, b_o, ln1_g, ln1_b (may be NULL), n_heads, seg_len and
+ * mem_len are not used; at most 16 layers.
+ */
 typedef struct gdp_placer {
   int32_t n_layers;               /* >= 1                                   */
   int32_t d_model;                /* d = gdp_gnn.hidden                     */
@@ -156,6 +163,7 @@ typedef struct gdp_placer {
   int32_t mem_len;                /* memory length M >= 0                   */
   int32_t n_devices;              /* D, 2 .. GDP_MAX_DEVICES                */
   int32_t film;                   /* 1: condition on x0 (Eq. 4), 0: off     */
+  int32_t attention;              /* 1: Section 3.2's placer, 0: the ablation's placer without attention */
   const gdp_placer_layer* layers; /* host array [n_layers]                  */
   const void* w_out;              /* [D, d] device, dtype                    */
   const void* b_out;              /* [D]                                    */
@@ -257,6 +265,7 @@ typedef enum gdp_kernel_kind {
   GDP_K_HEAD,            /* logits and lse when not fused (D > 8)            */
   GDP_K_SAMPLE,          /* Gumbel-max sampling                              */
   GDP_K_LOGP_REDUCE,     /* per-graph log-prob sums                          */
+  GDP_K_MLP_PLACER,      /* the ablation's placer without attention, all layers */
   GDP_K_COUNT
 } gdp_kernel_kind;
 

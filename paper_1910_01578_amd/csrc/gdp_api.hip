@@ -202,6 +202,44 @@ static int place_impl(const gdp_graph* g, const T* node_emb, const float* graph_
     }
   }
 
+  if (!p->attention) {
+    // the ablation's placer: every layer and the head in one row-local kernel
+    MlpPlacerArgs<T> a = {};
+    a.x = node_emb;
+    a.ldx = d;
+    a.film = p->film ? film : nullptr;
+    a.n_graphs = G;
+    a.n_layers = L;
+    for (int l = 0; l < L; ++l) {
+      const gdp_placer_layer& Ly = p->layers[l];
+      a.w1[l] = static_cast<const T*>(Ly.w_1);
+      a.b1[l] = static_cast<const T*>(Ly.b_1);
+      a.w2[l] = static_cast<const T*>(Ly.w_2);
+      a.b2[l] = static_cast<const T*>(Ly.b_2);
+      a.ln_g[l] = static_cast<const T*>(Ly.ln2_g);
+      a.ln_b[l] = static_cast<const T*>(Ly.ln2_b);
+    }
+    a.M = N;
+    a.d = d;
+    a.d_ff = p->d_ff;
+    const bool fused = p->n_devices <= kFusedHeadDevices;
+    if (fused) {
+      a.w_out = static_cast<const T*>(p->w_out);
+      a.b_out = static_cast<const T*>(p->b_out);
+      a.n_dev = p->n_devices;
+      a.logits = logits;
+      a.lse = lse;
+    } else {
+      a.y_out = ybuf[0];
+      a.ldyo = d;
+    }
+    GDP_LAUNCH(GDP_K_MLP_PLACER, launch_mlp_placer<T>(a, gt, st));
+    if (!fused)
+      GDP_LAUNCH(GDP_K_HEAD, launch_head<T>(ybuf[0], static_cast<const T*>(p->w_out),
+                                            static_cast<const T*>(p->b_out), N, d, p->n_devices, logits, lse, st));
+    return GDP_OK;
+  }
+
   GraphTable qt = make_table(g);
   const int qblocks = prefix_blocks_attention(g->graph_ptr_h, G, p->seg_len, kAttnQ, qt.blk);
   const float q_scale = attn_q_scale(d / p->n_heads);
@@ -399,7 +437,7 @@ extern "C" const char* gdp_kernel_kind_name(int32_t kind) {
   static const char* names[GDP_K_COUNT] = {
       "graph_prep", "nbr_sample",    "gemm_pool_sigmoid", "gather_max", "gemm_update_relu",
       "meanpool",   "film",          "pre_layer",         "seg_attention", "post_attn",
-      "head_lse",   "gumbel_sample", "logp_reduce"};
+      "head_lse",   "gumbel_sample", "logp_reduce",       "mlp_placer"};
   if (kind < 0 || kind >= GDP_K_COUNT) return "";
   return names[kind];
 }

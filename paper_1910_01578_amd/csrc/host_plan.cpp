@@ -73,22 +73,28 @@ int check_placer(const gdp_graph* g, const gdp_placer* p) {
   if (!p) return fail(GDP_E_INVALID_ARG, "placer is NULL");
   if (p->n_layers < 1) return fail(GDP_E_INVALID_ARG, "placer.n_layers = %d < 1", p->n_layers);
   if (!supported_width(p->d_model)) return fail(GDP_E_UNSUPPORTED, "d_model = %d not in {64,128,256}", p->d_model);
-  if (p->n_heads < 1 || p->d_model % p->n_heads != 0)
-    return fail(GDP_E_INVALID_ARG, "d_model = %d not divisible by n_heads = %d", p->d_model, p->n_heads);
-  const int dh = p->d_model / p->n_heads;
-  if (dh != 16 && dh != 32 && dh != 64) return fail(GDP_E_UNSUPPORTED, "head dim %d not in {16,32,64}", dh);
+  if (p->attention != 0 && p->attention != 1)
+    return fail(GDP_E_INVALID_ARG, "attention = %d must be 0 or 1", p->attention);
+  if (p->attention) {
+    if (p->n_heads < 1 || p->d_model % p->n_heads != 0)
+      return fail(GDP_E_INVALID_ARG, "d_model = %d not divisible by n_heads = %d", p->d_model, p->n_heads);
+    const int dh = p->d_model / p->n_heads;
+    if (dh != 16 && dh != 32 && dh != 64) return fail(GDP_E_UNSUPPORTED, "head dim %d not in {16,32,64}", dh);
+    if (p->seg_len < 1) return fail(GDP_E_INVALID_ARG, "seg_len = %d < 1", p->seg_len);
+    if (p->mem_len < 0) return fail(GDP_E_INVALID_ARG, "mem_len = %d < 0", p->mem_len);
+  } else if (p->n_layers > 16) {
+    return fail(GDP_E_UNSUPPORTED, "n_layers = %d > 16 without attention", p->n_layers);
+  }
   if (p->d_ff < 128 || p->d_ff % 128 != 0)
     return fail(GDP_E_UNSUPPORTED, "d_ff = %d must be a positive multiple of 128", p->d_ff);
-  if (p->seg_len < 1) return fail(GDP_E_INVALID_ARG, "seg_len = %d < 1", p->seg_len);
-  if (p->mem_len < 0) return fail(GDP_E_INVALID_ARG, "mem_len = %d < 0", p->mem_len);
   if (p->n_devices < 2 || p->n_devices > GDP_MAX_DEVICES)
     return fail(GDP_E_UNSUPPORTED, "n_devices = %d outside 2..%d", p->n_devices, GDP_MAX_DEVICES);
   if (p->film != 0 && p->film != 1) return fail(GDP_E_INVALID_ARG, "film = %d must be 0 or 1", p->film);
   if (!p->layers || !p->w_out || !p->b_out) return fail(GDP_E_INVALID_ARG, "placer weights are NULL");
   for (int l = 0; l < p->n_layers; ++l) {
     const gdp_placer_layer& L = p->layers[l];
-    if (!L.w_qkv || !L.b_qkv || !L.w_o || !L.b_o || !L.ln1_g || !L.ln1_b || !L.w_1 || !L.b_1 || !L.w_2 ||
-        !L.b_2 || !L.ln2_g || !L.ln2_b)
+    if (!L.w_1 || !L.b_1 || !L.w_2 || !L.b_2 || !L.ln2_g || !L.ln2_b ||
+        (p->attention && (!L.w_qkv || !L.b_qkv || !L.w_o || !L.b_o || !L.ln1_g || !L.ln1_b)))
       return fail(GDP_E_INVALID_ARG, "placer layer %d has a NULL weight", l);
     if (p->film && (!L.film_wg || !L.film_bg || !L.film_wb || !L.film_bb))
       return fail(GDP_E_INVALID_ARG, "placer layer %d has a NULL FiLM weight", l);
@@ -161,10 +167,15 @@ void plan_embed(const gdp_graph* g, const gdp_gnn* gnn, EmbedPlan* p) {
 void plan_place(const gdp_graph* g, const gdp_placer* pl, PlacePlan* p) {
   const size_t N = (size_t)g->n_nodes, d = (size_t)pl->d_model, es = elem_size(g->dtype);
   int32_t blk[GDP_MAX_GRAPHS + 1];
-  p->qblocks = prefix_blocks_attention(g->graph_ptr_h, g->n_graphs, pl->seg_len, kAttnQ, blk);
   carve_init(&p->c);
   p->film = carve_add(&p->c, (size_t)pl->n_layers * g->n_graphs * d * 2 * 4);
   p->y0 = carve_add(&p->c, N * d * 4);      // residual stream: fp32
+  if (!pl->attention) {                     // only the head's input, when the head runs on its own
+    p->qblocks = 0;
+    p->y1 = p->qkv = p->o = p->y0;
+    return;
+  }
+  p->qblocks = prefix_blocks_attention(g->graph_ptr_h, g->n_graphs, pl->seg_len, kAttnQ, blk);
   p->y1 = carve_add(&p->c, N * d * 4);
   p->qkv = carve_add(&p->c, N * 3 * d * es);
   p->o = carve_add(&p->c, N * d * es);

@@ -114,6 +114,32 @@ struct PreLayerArgs {
 template <typename T>
 hipError_t launch_pre_layer(const PreLayerArgs<T>& a, const GraphTable& gt, hipStream_t s);
 
+// The ablation's placer without attention (Section 4.3), all layers and the
+// head in one kernel: X_0 = x; per layer Y = FiLM_l(X) (film: [L][2][G][d],
+// gamma then beta, or null), X <- LN2_l(Y + W_2 ReLU(W_1 Y + b_1) + b_2); then
+// logits = X W_out^T + b_out and lse when w_out is set (n_dev <= kFusedHeadDevices),
+// and the final X (fp32) into y_out when that is set.
+constexpr int kMlpMaxLayers = 16;
+template <typename T>
+struct MlpPlacerArgs {
+  const T* x; int ldx;              // node embeddings [M, d]
+  const float* film;
+  int n_graphs;
+  int n_layers;                     // 1 .. kMlpMaxLayers
+  const T* w1[kMlpMaxLayers];       // [d_ff, d]
+  const T* b1[kMlpMaxLayers];       // [d_ff]
+  const T* w2[kMlpMaxLayers];       // [d, d_ff]
+  const T* b2[kMlpMaxLayers];       // [d]
+  const T* ln_g[kMlpMaxLayers];     // [d]
+  const T* ln_b[kMlpMaxLayers];     // [d]
+  int M, d, d_ff;
+  const T* w_out; const T* b_out; int n_dev;
+  float* logits; float* lse;
+  float* y_out; int ldyo;
+};
+template <typename T>
+hipError_t launch_mlp_placer(const MlpPlacerArgs<T>& a, const GraphTable& gt, hipStream_t s);
+
 // ---- Section 3.2 / 3.3 --------------------------------------------------------
 // Segment attention.  qkv: [N, 3d] with the q columns pre-scaled by
 // attn_q_scale(d / heads); out: [N, d].  gt.blk = per-graph prefix of 128-query

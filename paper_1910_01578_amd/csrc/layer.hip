@@ -660,6 +660,106 @@ bool aligned_16(const T* p) { return ((uintptr_t)p & 15u) == 0; }
 }  // namespace
 
 // HEAD: the last layer's variant, with the placement head instead of a QKV projection.
+// acc += W_2 ReLU(W_1 act + b_1) (the position-wise FFN of a placer layer),
+// over d_ff / FC chunks of hidden units that never leave the chip; af holds
+// the activation in the unit tiling.  Chunk c uses the buffers of parity
+// (P0 + c) & 1; chunk 0 must be in flight (or in place) in the parity P0
+// buffers and every other buffer free.  Chunk c + 1 loads during chunk c;
+// during the last chunk tail(s) runs after k step s on the loading waves,
+// to start the next phase's loads into the parity P0 buffers.
+template <typename T, int D, int P0, typename Tail>
+__device__ __forceinline__ void ffn_chunks(typename Geo<T, D>::RowAcc& acc, const typename Geo<T, D>::ActFrags& af,
+                                           const Lds<T>& L, const Lanes& ln, const T* w1, const T* b1, const T* w2,
+                                           int d_ff, Tail&& tail) {
+  using G = Geo<T, D>;
+  constexpr int FC = G::FC;
+  const int NC = d_ff / FC;                           // even
+  chunk_pairs<P0, true>(NC, [&](int c, auto pc) {
+    constexpr int P = decltype(pc)::v;
+    publish();                       // chunk c in place; chunk c - 1's buffers, H and the parts free
+    const bool more = c + 1 < NC;
+    const int cn = more ? c + 1 : 0;
+    const ChunkDma<T, D, 1, FC, kDmaWaves> next_ffn(L.template u<P ^ 1>(), w1 + (size_t)cn * FC * D,
+                                                    L.template r<P ^ 1>(), w2 + (size_t)cn * FC, d_ff,
+                                                    L.template b<P ^ 1>(), b1 + cn * FC);
+    const bool loader = wave_id() < kDmaWaves;
+    typename G::UnitAcc hacc;
+    unit_mma<T, D, G::JB1>(hacc, af, L.template u<P>(), ln.p1n * G::HPW, ln, [&](int s) {
+      if (loader) {
+        if (more) next_ffn.step(s);
+        else tail(s);
+      }
+    });
+    const T* sB = L.template b<P>();
+    // lane holds hidden row (p1m * RB1 + i) * 16 + col, units hc + [0, 4)
+#pragma unroll
+    for (int j = 0; j < G::JB1; ++j) {
+      const int hc = ln.p1n * G::HPW + j * 16 + 4 * ln.g4;
+      float b[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) b[r] = to_f32(sB[hc + r]);
+#pragma unroll
+      for (int i = 0; i < G::RB1; ++i) {
+        float h[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) h[r] = fmaxf(hacc[i][j][r] + b[r], 0.f);
+        store4(&L.h[swz<T, FC>((ln.p1m * G::RB1 + i) * 16 + ln.col, hc)], h);
+      }
+    }
+    bar_lds();                       // H complete
+    row_mma<T, D>(acc, L.h, L.template r<P>(), ln);
+  });
+}
+
+// acc[i][j][r] = gamma[c] * acc + beta[c] for the FiLM vectors of each row's
+// graph (gamma / beta: [G, stride]); the lane's column vectors are loaded
+// again only when a row belongs to another graph than the previous one.
+template <typename T, int D>
+__device__ __forceinline__ void film_rows(typename Geo<T, D>::RowAcc& acc, const float* gamma, const float* beta,
+                                          int stride, const GraphTable& gt, const Lanes& ln, int m0, int M) {
+  using G = Geo<T, D>;
+  const int rbase = ln.w2m * G::MB2 * 16 + ln.col;
+  const int cbase = ln.w2n * G::NB2 * 16 + 4 * ln.g4;
+  float4 fgm[G::NB2], fbt[G::NB2];
+  int gprev = -1;
+#pragma unroll
+  for (int i = 0; i < G::MB2; ++i) {
+    const int row = m0 + rbase + i * 16;
+    const int gi = graph_of_node(gt, row < M ? row : M - 1);
+    if (gi != gprev) {
+      const size_t g = (size_t)gi * stride;
+#pragma unroll
+      for (int j = 0; j < G::NB2; ++j) {
+        fgm[j] = *reinterpret_cast<const float4*>(gamma + g + cbase + j * 16);
+        fbt[j] = *reinterpret_cast<const float4*>(beta + g + cbase + j * 16);
+      }
+      gprev = gi;
+    }
+#pragma unroll
+    for (int j = 0; j < G::NB2; ++j) {
+      acc[i][j][0] = fgm[j].x * acc[i][j][0] + fbt[j].x;
+      acc[i][j][1] = fgm[j].y * acc[i][j][1] + fbt[j].y;
+      acc[i][j][2] = fgm[j].z * acc[i][j][2] + fbt[j].z;
+      acc[i][j][3] = fgm[j].w * acc[i][j][3] + fbt[j].w;
+    }
+  }
+}
+
+// acc[i][j][r] += b[c] (the second FFN bias) for the lane's columns.
+template <typename T, int D>
+__device__ __forceinline__ void add_col_bias(typename Geo<T, D>::RowAcc& acc, const T* b, const Lanes& ln) {
+  using G = Geo<T, D>;
+  const int cbase = ln.w2n * G::NB2 * 16 + 4 * ln.g4;
+#pragma unroll
+  for (int j = 0; j < G::NB2; ++j)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const float bv = to_f32(b[cbase + j * 16 + r]);
+#pragma unroll
+      for (int i = 0; i < G::MB2; ++i) acc[i][j][r] += bv;
+    }
+}
+
 template <typename T, int D, bool HEAD>
 __global__ __launch_bounds__(LNT) void k_post_attention(PostAttnArgs<T> p, GraphTable gt) {
   using G = Geo<T, D>;
@@ -719,84 +819,17 @@ __global__ __launch_bounds__(LNT) void k_post_attention(PostAttnArgs<T> p, Graph
   typename G::ActFrags af;
   to_unit_tiling<T, D, (NK0 + 1) & 1>(acc, L, af, ln);
   if constexpr (G::NZ == 4) dma_ffn(0, Par<NK0 & 1>{});
-  const int NC = p.d_ff / FC;                           // even
-  chunk_pairs<NK0 & 1, true>(NC, [&](int c, auto pc) {
-    constexpr int P = decltype(pc)::v;
-    publish();                       // chunk c in place; chunk c - 1's buffers, H and the parts free
-    // during this chunk: FFN chunk c + 1, or after the last one the first
-    // QKV chunk (whose W_qkv tile has the W_1 tile's shape)
-    const bool more = c + 1 < NC;
-    const bool first_qkv = !more && G::NZ == 2 && qkv_next;
-    const int cn = more ? c + 1 : 0;
-    const ChunkDma<T, D, 1, FC, kDmaWaves> next_ffn(L.template u<P ^ 1>(), p.w1 + (size_t)cn * FC * D,
-                                                    L.template r<P ^ 1>(), p.w2 + (size_t)cn * FC, p.d_ff,
-                                                    L.template b<P ^ 1>(), p.b1 + cn * FC);
-    const auto next_qkv = qkv_chunk<T, D, P ^ 1, kDmaWaves>(L, p.w_qkv, p.b_qkv, 0);
-    const bool loader = wave_id() < kDmaWaves;
-    typename G::UnitAcc hacc;
-    unit_mma<T, D, G::JB1>(hacc, af, L.template u<P>(), ln.p1n * G::HPW, ln, [&](int s) {
-      if (loader) {
-        if (more) next_ffn.step(s);
-        else if (first_qkv) next_qkv.step(s);
-      }
-    });
-    const T* sB = L.template b<P>();
-    // lane holds hidden row (p1m * RB1 + i) * 16 + col, units hc + [0, 4)
-#pragma unroll
-    for (int j = 0; j < G::JB1; ++j) {
-      const int hc = ln.p1n * G::HPW + j * 16 + 4 * ln.g4;
-      float b[4];
-#pragma unroll
-      for (int r = 0; r < 4; ++r) b[r] = to_f32(sB[hc + r]);
-#pragma unroll
-      for (int i = 0; i < G::RB1; ++i) {
-        float h[4];
-#pragma unroll
-        for (int r = 0; r < 4; ++r) h[r] = fmaxf(hacc[i][j][r] + b[r], 0.f);
-        store4(&L.h[swz<T, FC>((ln.p1m * G::RB1 + i) * 16 + ln.col, hc)], h);
-      }
-    }
-    bar_lds();                       // H complete
-    row_mma<T, D>(acc, L.h, L.template r<P>(), ln);
+  // after the last chunk the first QKV chunk (whose W_qkv tile has the W_1
+  // tile's shape) loads during it
+  const auto first_qkv = qkv_chunk<T, D, NK0 & 1, kDmaWaves>(L, p.w_qkv, p.b_qkv, 0);
+  ffn_chunks<T, D, NK0 & 1>(acc, af, L, ln, p.w1, p.b1, p.w2, p.d_ff, [&](int s) {
+    if (G::NZ == 2 && qkv_next) first_qkv.step(s);
   });
 
   // ---- + b_2, LN2, FiLM of the next layer; store Y' ---------------------------
-#pragma unroll
-  for (int j = 0; j < G::NB2; ++j)
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const float b = to_f32(p.b2[cbase + j * 16 + r]);
-#pragma unroll
-      for (int i = 0; i < G::MB2; ++i) acc[i][j][r] += b;
-    }
+  add_col_bias<T, D>(acc, p.b2, ln);
   ln_rows<T, D>(acc, p.ln2_g, p.ln2_b, red, ln);
-  // FiLM gamma / beta of the lane's columns, loaded again only when a row
-  // belongs to another graph than the previous one
-  float4 fgm[G::NB2], fbt[G::NB2];
-  int gprev = -1;
-#pragma unroll
-  for (int i = 0; i < G::MB2; ++i) {
-    const int row = m0 + rbase + i * 16;
-    if (p.film_gamma) {
-      const int gi = graph_of_node(gt, row < p.M ? row : p.M - 1);
-      if (gi != gprev) {
-        const size_t g = (size_t)gi * p.film_stride;
-#pragma unroll
-        for (int j = 0; j < G::NB2; ++j) {
-          fgm[j] = *reinterpret_cast<const float4*>(p.film_gamma + g + cbase + j * 16);
-          fbt[j] = *reinterpret_cast<const float4*>(p.film_beta + g + cbase + j * 16);
-        }
-        gprev = gi;
-      }
-#pragma unroll
-      for (int j = 0; j < G::NB2; ++j) {
-        acc[i][j][0] = fgm[j].x * acc[i][j][0] + fbt[j].x;
-        acc[i][j][1] = fgm[j].y * acc[i][j][1] + fbt[j].y;
-        acc[i][j][2] = fgm[j].z * acc[i][j][2] + fbt[j].z;
-        acc[i][j][3] = fgm[j].w * acc[i][j][3] + fbt[j].w;
-      }
-    }
-  }
+  if (p.film_gamma) film_rows<T, D>(acc, p.film_gamma, p.film_beta, p.film_stride, gt, ln, m0, p.M);
   // (issuing these stores after the first QKV barrier instead, to overlap
   // their HBM writes with its products, keeps acc live there and measured
   // 12 % slower)
@@ -848,6 +881,85 @@ hipError_t launch_post_attention(const PostAttnArgs<T>& a, const GraphTable& gt,
 template hipError_t launch_post_attention<float>(const PostAttnArgs<float>&, const GraphTable&, hipStream_t);
 template hipError_t launch_post_attention<bf16>(const PostAttnArgs<bf16>&, const GraphTable&, hipStream_t);
 
+
+// The ablation's placement network without attention (Section 4.3): every
+// layer is row-local, Y = FiLM_l(X), X <- LN2_l(Y + W_2 ReLU(W_1 Y + b_1) + b_2),
+// so one work-group runs all layers of its 128 rows with the activation in
+// its accumulators, and ends with the head.  Layer l's FFN chunk c uses the
+// buffers of parity c & 1 (an even number of chunks), so every layer starts
+// at parity 0, its first chunk loading during the previous layer's last one.
+template <typename T, int D>
+__global__ __launch_bounds__(LNT) void k_mlp_placer(MlpPlacerArgs<T> p, GraphTable gt) {
+  using G = Geo<T, D>;
+  constexpr int FC = G::FC;
+  GDP_LAYER_LDS(T, G);
+  typename G::Red* red = reinterpret_cast<typename G::Red*>(L.red);
+  const Lanes ln = make_lanes<T, D>();
+  const int m0 = blockIdx.x * LBM;
+  const int rbase = ln.w2m * G::MB2 * 16 + ln.col;
+  const int cbase = ln.w2n * G::NB2 * 16 + 4 * ln.g4;
+  auto first_chunk = [&](int l) {
+    return ChunkDma<T, D, 1, FC, kDmaWaves>(L.template u<0>(), p.w1[l], L.template r<0>(), p.w2[l], p.d_ff,
+                                             L.template b<0>(), p.b1[l]);
+  };
+  if constexpr (G::NZ == 2) first_chunk(0).all();
+  typename G::RowAcc acc;
+#pragma unroll
+  for (int i = 0; i < G::MB2; ++i) {
+    const int row = m0 + rbase + i * 16;
+    const int rr = row < p.M ? row : p.M - 1;
+#pragma unroll
+    for (int j = 0; j < G::NB2; ++j) {
+      float x[4];
+      load4f(p.x + (size_t)rr * p.ldx + cbase + j * 16, x);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) acc[i][j][r] = x[r];
+    }
+  }
+  typename G::ActFrags af;
+  const size_t gd = (size_t)p.n_graphs * D;
+  for (int l = 0; l < p.n_layers; ++l) {
+    if (p.film) film_rows<T, D>(acc, p.film + 2 * l * gd, p.film + (2 * l + 1) * gd, D, gt, ln, m0, p.M);
+    to_unit_tiling<T, D, 1>(acc, L, af, ln);
+    if constexpr (G::NZ == 4) first_chunk(l).all();
+    const bool more = l + 1 < p.n_layers;
+    const auto next = first_chunk(more ? l + 1 : l);
+    ffn_chunks<T, D, 0>(acc, af, L, ln, p.w1[l], p.b1[l], p.w2[l], p.d_ff, [&](int s) {
+      if (G::NZ == 2 && more) next.step(s);
+    });
+    add_col_bias<T, D>(acc, p.b2[l], ln);
+    ln_rows<T, D>(acc, p.ln_g[l], p.ln_b[l], red, ln);   // its barriers free every buffer
+  }
+  if (p.y_out) store_residual<T, D>(acc, L, ln, m0, p.M, p.y_out, p.ldyo);
+  if (p.w_out) head_epilogue<T, D>(acc, L, ln, m0, p.M, p.w_out, p.b_out, p.n_dev, p.logits, p.lse);
+}
+
+template <typename T>
+hipError_t launch_mlp_placer(const MlpPlacerArgs<T>& a, const GraphTable& gt, hipStream_t s) {
+  if (a.M <= 0) return hipSuccess;
+  if (a.n_layers < 1 || a.n_layers > kMlpMaxLayers || !a.x || a.ldx % (16 / (int)sizeof(T)) || !aligned_16(a.x))
+    return hipErrorInvalidValue;
+  if (a.d_ff <= 0 || a.d_ff % (2 * LayerCfg<T>::FC)) return hipErrorInvalidValue;
+  for (int l = 0; l < a.n_layers; ++l)
+    if (!a.w1[l] || !a.b1[l] || !a.w2[l] || !a.b2[l] || !a.ln_g[l] || !a.ln_b[l] || !aligned_16(a.w1[l]) ||
+        !aligned_16(a.w2[l]) || !aligned_16(a.b1[l]))
+      return hipErrorInvalidValue;
+  if (a.film && (a.n_graphs < 1 || !aligned_16(a.film))) return hipErrorInvalidValue;
+  if (a.w_out && (!a.b_out || !a.logits || !a.lse || a.n_dev < 1 || a.n_dev > kFusedHeadDevices))
+    return hipErrorInvalidValue;
+  if (a.y_out && (a.ldyo % 4 || !aligned_16(a.y_out))) return hipErrorInvalidValue;
+  if (!a.w_out && !a.y_out) return hipErrorInvalidValue;
+  dim3 grid((a.M + LBM - 1) / LBM), block(LNT);
+  switch (a.d) {
+    case 64: hipLaunchKernelGGL((k_mlp_placer<T, 64>), grid, block, 0, s, a, gt); break;
+    case 128: hipLaunchKernelGGL((k_mlp_placer<T, 128>), grid, block, 0, s, a, gt); break;
+    case 256: hipLaunchKernelGGL((k_mlp_placer<T, 256>), grid, block, 0, s, a, gt); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+template hipError_t launch_mlp_placer<float>(const MlpPlacerArgs<float>&, const GraphTable&, hipStream_t);
+template hipError_t launch_mlp_placer<bf16>(const MlpPlacerArgs<bf16>&, const GraphTable&, hipStream_t);
 
 // The first placer layer's input and projection (Eq. 4, Section 3.2):
 //   Y = FiLM_0(X) (X = the node embeddings; identity without conditioning) into

@@ -30,7 +30,7 @@ GDP_MAX_GRAPHS = 128
 
 KERNEL_KINDS = ["graph_prep", "nbr_sample", "gemm_pool_sigmoid", "gather_max", "gemm_update_relu",
                 "meanpool", "film", "pre_layer", "seg_attention", "post_attn",
-                "head_lse", "gumbel_sample", "logp_reduce"]
+                "head_lse", "gumbel_sample", "logp_reduce", "mlp_placer"]
 K_COUNT = len(KERNEL_KINDS)
 
 
@@ -66,6 +66,7 @@ class GdpPlacerLayer(ctypes.Structure):
 class GdpPlacer(ctypes.Structure):
     _fields_ = [("n_layers", c_int32), ("d_model", c_int32), ("n_heads", c_int32), ("d_ff", c_int32),
                 ("seg_len", c_int32), ("mem_len", c_int32), ("n_devices", c_int32), ("film", c_int32),
+                ("attention", c_int32),
                 ("layers", POINTER(GdpPlacerLayer)), ("w_out", c_void_p), ("b_out", c_void_p)]
 
 
@@ -177,7 +178,8 @@ class DeviceGraph:
 class DevicePolicy:
     """Policy weights resident in device memory plus the C descriptors."""
 
-    def __init__(self, cfg, weights, device="cuda", film: Optional[bool] = None):
+    def __init__(self, cfg, weights, device="cuda", film: Optional[bool] = None,
+                 attention: Optional[bool] = None):
         self.cfg = cfg
         dt = cfg.dtype
         up = lambda pair: to_device(pair[1], dt, device)
@@ -193,9 +195,10 @@ class DevicePolicy:
         self._pl = (GdpPlacerLayer * P)(*[GdpPlacerLayer(*[l[k].data_ptr() for k in PLACER_LAYER_FIELDS])
                                           for l in self.placer_t])
         use_film = cfg.film if film is None else film
+        use_attention = cfg.attention if attention is None else attention
         self.placer = GdpPlacer(P, cfg.d_model, cfg.heads, cfg.d_ff, cfg.seg_len, cfg.mem_len, cfg.n_devices,
-                                1 if use_film else 0, self._pl, self.head_t["w_out"].data_ptr(),
-                                self.head_t["b_out"].data_ptr())
+                                1 if use_film else 0, 1 if use_attention else 0, self._pl,
+                                self.head_t["w_out"].data_ptr(), self.head_t["b_out"].data_ptr())
 
 
 class Runner:

@@ -23,7 +23,7 @@ def test_exports_every_declared_symbol():
     assert len(names) >= 12
     for n in names:
         assert hasattr(gdp.lib, n), n
-    assert gdp.abi_version() == 1
+    assert gdp.abi_version() == 2
 
 
 def test_kernel_kind_names_match_binding():
@@ -106,7 +106,7 @@ def _descs(cfg_name="tiny_layered_256", **over):
     gnn = gdp.GdpGnn(cfg.gnn_layers, cfg.feat_dim, cfg.hidden, cfg.fanout, 7, gl)
     pl = (gdp.GdpPlacerLayer * cfg.placer_layers)(*[gdp.GdpPlacerLayer(*([fake] * 16))] * cfg.placer_layers)
     placer = gdp.GdpPlacer(cfg.placer_layers, cfg.d_model, cfg.heads, cfg.d_ff, cfg.seg_len, cfg.mem_len,
-                           cfg.n_devices, 1, pl, fake, fake)
+                           cfg.n_devices, 1, 1, pl, fake, fake)
     return cfg, gp, g, gl, gnn, pl, placer
 
 
@@ -164,6 +164,7 @@ def test_embed_rejects_small_or_misaligned_workspace_and_bad_graph_ptr():
     ("n_devices", 1, gdp.GDP_E_UNSUPPORTED),
     ("n_devices", 65, gdp.GDP_E_UNSUPPORTED),
     ("film", 2, gdp.GDP_E_INVALID_ARG),
+    ("attention", 2, gdp.GDP_E_INVALID_ARG),
 ])
 def test_place_rejects(field, value, code):
     cfg, gp, g, gl, gnn, pl, placer = _descs()
@@ -175,6 +176,29 @@ def test_place_rejects(field, value, code):
     r = gdp.lib.gdp_place(ctypes.byref(g), 0x100000, 0x200000, ctypes.byref(placer), 0x300000, None, 0x1000000,
                           1 << 30, None)
     assert r == code, gdp.last_error()
+
+
+def test_place_without_attention_validation():
+    """The ablation's placer needs no attention weights and ignores the
+    attention shape fields; it takes at most 16 layers."""
+    cfg, gp, g, gl, gnn, pl, placer = _descs()
+    placer.attention = 0
+    placer.n_heads, placer.seg_len, placer.mem_len = 7, 0, -3     # not used without attention
+    for l in range(cfg.placer_layers):
+        pl[l].w_qkv = pl[l].b_qkv = pl[l].w_o = pl[l].b_o = pl[l].ln1_g = pl[l].ln1_b = None
+    n = gdp.lib.gdp_workspace_bytes(ctypes.byref(g), None, ctypes.byref(placer), 0)
+    assert n > 0, gdp.last_error()
+    placer.attention = 1
+    assert gdp.lib.gdp_workspace_bytes(ctypes.byref(g), None, ctypes.byref(placer), 0) == 0
+    placer.attention = 0
+    pl[0].w_1 = None
+    assert gdp.lib.gdp_workspace_bytes(ctypes.byref(g), None, ctypes.byref(placer), 0) == 0
+    assert "NULL weight" in gdp.last_error()
+    big = (gdp.GdpPlacerLayer * 17)(*[gdp.GdpPlacerLayer(*([0x10000] * 16))] * 17)
+    placer.layers, placer.n_layers = big, 17
+    r = gdp.lib.gdp_place(ctypes.byref(g), 0x100000, 0x200000, ctypes.byref(placer), 0x300000, None, 0x1000000,
+                          1 << 30, None)
+    assert r == gdp.GDP_E_UNSUPPORTED, gdp.last_error()
 
 
 @pytest.mark.parametrize("D,K,code", [(1, 4, gdp.GDP_E_UNSUPPORTED), (65, 4, gdp.GDP_E_UNSUPPORTED),

@@ -415,3 +415,51 @@ def test_attention_large_scores_bf16_uniform(sign):
     _log(f"  logits err {err_l:.3e}")
     assert np.isfinite(to_np(r2.logits)).all()
     assert err_l <= TOL["bf16"]
+
+
+# ----------------------------------------------------------------------------
+# The ablation's placer without attention (Section 4.3): one fused kernel.
+def _place_no_attention(cfg, g, w):
+    r = _runner(cfg.replace(attention=False), g, w)
+    r.embed()
+    r.place()
+    _sync()
+    _, pl, hd = w.f64()
+    p = O.place(to_np(r.node_emb), to_np(r.graph_emb), g.graph_ptr, pl, hd["w_out"], hd["b_out"], cfg.heads,
+                cfg.seg_len, cfg.mem_len, cfg.film, attention=False)
+    return r, p
+
+
+@pytest.mark.parametrize("name", ALL)
+def test_place_without_attention_parity(name):
+    cfg, g, w = workload(name)
+    _log("place without attention", name)
+    r, p = _place_no_attention(cfg, g, w)
+    tol = TOL[cfg.dtype]
+    err_l = rel_err_rows(to_np(r.logits), p["logits"])
+    err_s = rel_err_rows(to_np(r.lse), p["lse"])
+    _log(f"  logits err {err_l:.3e}  lse err {err_s:.3e}")
+    assert err_l <= tol and err_s <= tol
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("label,over", [
+    ("many_devices", dict(n_devices=64)),          # the head in its own kernel
+    ("sixteen_layers", dict(placer_layers=16)),
+    ("film_off_ragged_tail", dict(film=False, graph_sizes=(300,))),
+    ("single_node", dict(graph_sizes=(1,))),
+], ids=lambda v: v if isinstance(v, str) else None)
+def test_place_without_attention_edges(label, over, dtype):
+    over = dict(over)
+    if dtype == "bf16":
+        over = {**BF16_WIDTH, **over}
+    cfg = W.get_config("tiny_layered_256").replace(dtype=dtype, **over)
+    _log("place without attention, edge", label, dtype)
+    g = W.make_graph(cfg) if "graph_sizes" not in over else _edge_graph(cfg, "single" if cfg.graph_sizes[0] == 1
+                                                                          else "empty")
+    w = W.make_weights(cfg)
+    r, p = _place_no_attention(cfg, g, w)
+    err_l = rel_err_rows(to_np(r.logits), p["logits"])
+    err_s = rel_err_rows(to_np(r.lse), p["lse"])
+    _log(f"  logits err {err_l:.3e}  lse err {err_s:.3e}")
+    assert err_l <= TOL[dtype] and err_s <= TOL[dtype]
