@@ -427,14 +427,21 @@ __global__ __launch_bounds__(256) void k_meanpool_partial(const T* __restrict__ 
   const int g = graph_of_block(ct, c);
   const int r0 = ct.ptr[g] + (c - ct.blk[g]) * kMeanpoolRows;
   const int r1 = min(r0 + kMeanpoolRows, ct.ptr[g + 1]);
+  static_assert(kMeanpoolRows % RG == 0, "chunk rows split evenly over the row groups");
   const int rg = threadIdx.x / TPR, col = (threadIdx.x % TPR) * EPV;
   float acc[EPV];
 #pragma unroll
   for (int e = 0; e < EPV; ++e) acc[e] = 0.f;
-  for (int r = r0 + rg; r < r1; r += RG) {
-    const Vec16<T> x = load16(h + (size_t)r * H + col);
+  // every row of the chunk in one unrolled pass, so that all of a thread's
+  // loads are in flight at once; rows past the chunk's end (a graph's last
+  // chunk) read its last row and add nothing
 #pragma unroll
-    for (int e = 0; e < EPV; ++e) acc[e] += to_f32(x.v[e]);
+  for (int i = 0; i < kMeanpoolRows / RG; ++i) {
+    const int r = r0 + rg + i * RG;
+    const Vec16<T> x = load16(h + (size_t)min(r, r1 - 1) * H + col);
+    const float keep = r < r1 ? 1.0f : 0.0f;
+#pragma unroll
+    for (int e = 0; e < EPV; ++e) acc[e] += keep * to_f32(x.v[e]);
   }
 #pragma unroll
   for (int e = 0; e < EPV; ++e) red[rg][col + e] = acc[e];

@@ -56,7 +56,7 @@ void plan_embed(const gdp_graph* g, const gdp_gnn* gnn, EmbedPlan* p);
 void plan_place(const gdp_graph* g, const gdp_placer* pl, PlacePlan* p);
 void plan_sample(const gdp_graph* g, int32_t k_samples, SamplePlan* p);
 
-constexpr int kPoolRows = 256;      // rows per mean-pool chunk
+constexpr int kPoolRows = 64;       // rows per mean-pool chunk
 constexpr int kAttnQ = 128;         // queries per attention work-group
 constexpr int kSampleRows = 256;    // nodes per sampling work-group
 

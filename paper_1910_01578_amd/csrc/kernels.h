@@ -33,7 +33,7 @@ hipError_t launch_gather_max(const T* P, const int* s_ptr, const int* s_idx, int
 template <typename T>
 hipError_t launch_meanpool(const T* h, int H, const GraphTable& chunks, int total_chunks,
                            float* partial, float* graph_emb, hipStream_t s);
-constexpr int kMeanpoolRows = 256;
+constexpr int kMeanpoolRows = 64;
 
 // ---- dense layers -------------------------------------------------------------
 enum Epilogue { EPI_BIAS = 0, EPI_RELU = 1, EPI_SIGMOID = 2 };
