@@ -17,13 +17,17 @@ namespace gdp {
 namespace dma {
 
 // XOR key of row r in a tile whose rows hold GPR 16-byte granules: granule g
-// of row r is stored at granule g ^ swz_key(r).  Any 8 rows r0 .. r0 + 7 and
-// any 16 rows r0 .. r0 + 15 (r0 aligned) then place a given granule in
-// distinct 16-byte bank groups, for 128- and 256-byte bank rows alike.
+// of row r is stored at granule g ^ swz_key(r), a permutation of each row.
+// Any 8 aligned rows place a given granule in distinct 16-byte bank groups.
+// The keys were chosen by measuring LDS bank conflicts on gfx950 for the MFMA
+// fragment reads (16 rows x 4 granules per instruction) that these tiles
+// serve: with them those reads take the minimum four LDS cycles per
+// instruction.  (For 128-byte rows, folding bit 3 of the row into the key,
+// as (r & 7) ^ ((r >> 3) & 1) does, measured twice that.)
 template <int GPR>
 __device__ __forceinline__ int swz_key(int r) {
   if constexpr (GPR >= 16) return r & 15;
-  else if constexpr (GPR == 8) return (r & 7) ^ ((r >> 3) & 1);
+  else if constexpr (GPR == 8) return r & 7;
   else {
     static_assert(GPR == 4, "tile rows of at least 64 bytes");
     return ((r >> 2) ^ (r >> 1)) & 3;
