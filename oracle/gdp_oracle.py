@@ -347,3 +347,40 @@ def policy_forward(graph_ptr, row_ptr, col_idx, x, gnn_layers, placer_layers, w_
     out.update(p)
     out.update(s)
     return out
+
+
+# ----------------------------------------------------------------------------
+# Section 3 (Eq. 1, optimised with PPO): the clipped surrogate over the K
+# sampled placements of every graph and its gradient with respect to the
+# device logits -- where the update path starts its backward pass.
+# ----------------------------------------------------------------------------
+
+def ppo_clipped_surrogate(logits, lse, graph_ptr, placements, logp, logp_old, adv, clip_eps):
+    """Per graph g, with ratio r = exp(logp - logp_old) of each sample k:
+        L_g = -(1/K) sum_k min(r A, clip(r, 1 - eps, 1 + eps) A)
+    (PPO's clipped objective, negated to a loss), and the gradient of the batch
+    loss L = (1/G) sum_g L_g (Eq. 1 averages over graphs) with respect to the
+    logits.  logp[g, k] = sum over v in g of log_softmax(logits_v)[p_kv], so
+    d logp[g, k] / d logits[v, j] = 1[p_kv = j] - softmax(logits_v)_j; the
+    min takes the unclipped branch's slope r A where that branch attains it
+    and 0 where the clipped constant does."""
+    logits = np.asarray(logits, np.float64)
+    N, D = logits.shape
+    G = len(graph_ptr) - 1
+    K = placements.shape[0]
+    r = np.exp(np.asarray(logp, np.float64) - np.asarray(logp_old, np.float64))
+    A = np.asarray(adv, np.float64)
+    unclipped = r * A
+    clipped = np.clip(r, 1.0 - clip_eps, 1.0 + clip_eps) * A
+    loss = -np.minimum(unclipped, clipped).mean(axis=1)
+    slope = np.where(unclipped <= clipped, r * A, 0.0)        # d min / d logp
+    coef = -slope / K / G                                      # dL / dlogp[g, k]
+    soft = np.exp(logits - np.asarray(lse, np.float64)[:, None])
+    dlogits = np.zeros((N, D))
+    for g in range(G):
+        gs, ge = int(graph_ptr[g]), int(graph_ptr[g + 1])
+        for k in range(K):
+            for v in range(gs, ge):
+                dlogits[v, placements[k, v]] += coef[g, k]
+            dlogits[gs:ge] -= coef[g, k] * soft[gs:ge]
+    return {"loss": loss, "coef": coef, "dlogits": dlogits}
