@@ -195,6 +195,27 @@ def main():
             ent.update({"achieved": rf["achieved"], "unit": rf["unit"], "frac": rf["frac"], "bound": rf["bound"]})
         kernels.append(ent)
 
+    # The update path's first step on the timed step's samples: PPO's clipped
+    # surrogate and its logit gradient (HBM-bound: placements, logits, lse in,
+    # the gradient out).
+    rng = np.random.default_rng(cfg.cfg_id)
+    lp = runner.logp.cpu().numpy()
+    logp_old = torch.from_numpy((lp + rng.normal(scale=0.05, size=lp.shape)).astype(np.float32)).cuda()
+    adv = torch.from_numpy(rng.normal(size=lp.shape).astype(np.float32)).cuda()
+    for _ in range(3):
+        runner.ppo_grad(logp_old, adv, 0.2)
+    torch.cuda.synchronize()
+    gdp.timer_begin(["ppo_grad"])
+    for _ in range(args.steps):
+        runner.ppo_grad(logp_old, adv, 0.2)
+    torch.cuda.synchronize()
+    pr = gdp.timer_end()["ppo_grad"]
+    ppo_us = 1e3 * pr["ms"] / pr["launches"]
+    ppo_bytes = 4.0 * (cfg.k_samples * g.n_nodes + 2 * g.n_nodes * cfg.n_devices + g.n_nodes)
+    ppo = {"us_per_call": round(ppo_us, 2), "algorithmic_bytes": int(ppo_bytes),
+           "achieved": round(ppo_bytes / (ppo_us * 1e-6) / 1e9, 1), "unit": "GB/s", "peak": PEAK_HBM_GBS,
+           "frac": round(ppo_bytes / (ppo_us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4)}
+
     # The ablation's placer without attention (Section 4.3) on the same DAG and
     # weights: the same embed and sample calls around one fused placer kernel.
     ab = gdp.Runner(gdp.DeviceGraph(g, cfg.dtype), gdp.DevicePolicy(cfg, w, attention=False), cfg.k_samples)
@@ -241,6 +262,7 @@ def main():
         "cpu_baseline": cpu,
         "kernels": kernels,
         "ablation_no_attention": ablation,
+        "ppo_grad": ppo,
     }
     print(json.dumps(out), flush=True)
 

@@ -215,6 +215,33 @@ int gdp_sample(const gdp_graph* g, const float* logits, const float* lse, int32_
                float* logp, void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * The first step of the policy update (Section 3: Eq. 1's objective, optimised
+ * with PPO, Schulman et al. 2017): the clipped surrogate over the K sampled
+ * placements of every graph and its gradient with respect to the logits.
+ *   r[g, k]  = exp(logp[g, k] - logp_old[g, k])
+ *   loss[g]  = -(1/K) sum_k min(r A[g, k], clip(r, 1 - clip_eps, 1 + clip_eps) A[g, k])
+ *   dlogits  = d/d logits of (1/G) sum_g loss[g], through
+ *              logp[g, k] = sum over v in g of (logits[v, p_kv] - lse[v])
+ * The min takes the unclipped branch's slope where that branch attains it and
+ * 0 where the clipped constant does.
+ *   logits      device [N, D] fp32 (input, the ones the placements were drawn from)
+ *   lse         device [N] fp32 (input, may be NULL: then recomputed)
+ *   placements  device [K, N] int32 (input, from gdp_sample)
+ *   logp        device [G, K] fp32 (input, from gdp_sample)
+ *   logp_old    device [G, K] fp32 (input: the sampling policy's log-probs)
+ *   advantages  device [G, K] fp32 (input)
+ *   clip_eps    0 < clip_eps < 1
+ *   loss        device [G] fp32 (output)
+ *   dlogits     device [N, D] fp32 (output)
+ * The workspace of gdp_workspace_bytes with the same k_samples suffices.
+ * Deterministic (fixed summation orders).
+ */
+int gdp_ppo_grad(const gdp_graph* g, const float* logits, const float* lse, int32_t n_devices,
+                 int32_t k_samples, const int32_t* placements, const float* logp, const float* logp_old,
+                 const float* advantages, float clip_eps, float* loss, float* dlogits, void* workspace,
+                 size_t workspace_bytes, void* stream);
+
+/*
  * Host-side check of a graph batch (all pointers host memory): graph_ptr
  * strictly increasing from 0, row_ptr monotone from 0 to E, col_idx in range,
  * no self-loops, no duplicate edges, no edge across graphs, acyclic (Kahn's
@@ -266,6 +293,7 @@ typedef enum gdp_kernel_kind {
   GDP_K_SAMPLE,          /* Gumbel-max sampling                              */
   GDP_K_LOGP_REDUCE,     /* per-graph log-prob sums                          */
   GDP_K_MLP_PLACER,      /* the ablation's placer without attention, all layers */
+  GDP_K_PPO,             /* PPO clipped surrogate and its logit gradient     */
   GDP_K_COUNT
 } gdp_kernel_kind;
 

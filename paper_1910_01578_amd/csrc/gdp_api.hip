@@ -380,6 +380,28 @@ extern "C" int gdp_sample(const gdp_graph* g, const float* logits, const float* 
   return GDP_OK;
 }
 
+extern "C" int gdp_ppo_grad(const gdp_graph* g, const float* logits, const float* lse, int32_t n_devices,
+                            int32_t k_samples, const int32_t* placements, const float* logp, const float* logp_old,
+                            const float* advantages, float clip_eps, float* loss, float* dlogits, void* ws,
+                            size_t ws_bytes, void* stream) {
+  clear_error();
+  int r;
+  if ((r = check_graph(g)) != GDP_OK) return r;
+  if ((r = check_sample(g, n_devices, k_samples)) != GDP_OK) return r;
+  if (!logits || !placements || !logp || !logp_old || !advantages || !loss || !dlogits)
+    return fail(GDP_E_INVALID_ARG, "a PPO input or output is NULL");
+  if (!(clip_eps > 0.0f && clip_eps < 1.0f)) return fail(GDP_E_INVALID_ARG, "clip_eps = %g must lie in (0, 1)", clip_eps);
+  SamplePlan pl;
+  plan_sample(g, k_samples, &pl);
+  if ((r = check_ws(ws, ws_bytes, pl.c.total)) != GDP_OK) return r;
+  if ((r = pending_hip_error()) != GDP_OK) return r;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const GraphTable gt = make_table(g);
+  GDP_LAUNCH(GDP_K_PPO, launch_ppo(logits, lse, placements, logp, logp_old, advantages, clip_eps, gt, g->n_nodes,
+                                   n_devices, k_samples, at<float>(ws, pl.coef), loss, dlogits, st));
+  return GDP_OK;
+}
+
 extern "C" int gdp_debug_uniforms(uint64_t seed, int32_t n, int32_t k, int32_t d, float* out, void* stream) {
   clear_error();
   if (n < 1 || k < 1 || d < 1 || d > GDP_MAX_DEVICES || !out) return fail(GDP_E_INVALID_ARG, "bad arguments");
@@ -437,7 +459,7 @@ extern "C" const char* gdp_kernel_kind_name(int32_t kind) {
   static const char* names[GDP_K_COUNT] = {
       "graph_prep", "nbr_sample",    "gemm_pool_sigmoid", "gather_max", "gemm_update_relu",
       "meanpool",   "film",          "pre_layer",         "seg_attention", "post_attn",
-      "head_lse",   "gumbel_sample", "logp_reduce",       "mlp_placer"};
+      "head_lse",   "gumbel_sample", "logp_reduce",       "mlp_placer", "ppo_grad"};
   if (kind < 0 || kind >= GDP_K_COUNT) return "";
   return names[kind];
 }

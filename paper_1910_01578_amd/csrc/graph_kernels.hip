@@ -459,10 +459,16 @@ __global__ __launch_bounds__(256) void k_meanpool_final(const float* __restrict_
   const int g = blockIdx.x;
   const int cl = threadIdx.x & 15, sl = threadIdx.x >> 4;
   const int col = blockIdx.y * 16 + cl;
-  float acc = 0.f;
+  // slice sl adds chunks sl, sl + 16, ... : four running sums (chunks 64q + sl
+  // + 16e into sum e) keep four loads in flight, combined in a fixed order
+  float acc[4] = {0.f, 0.f, 0.f, 0.f};
   if (col < H)
-    for (int c = ct.blk[g] + sl; c < ct.blk[g + 1]; c += 16) acc += partial[(size_t)c * H + col];
-  red[sl][cl] = acc;
+    for (int c = ct.blk[g] + sl; c < ct.blk[g + 1]; c += 64) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        if (c + 16 * e < ct.blk[g + 1]) acc[e] += partial[(size_t)(c + 16 * e) * H + col];
+    }
+  red[sl][cl] = (acc[0] + acc[1]) + (acc[2] + acc[3]);
   __syncthreads();
   if (sl == 0 && col < H) {
     float t[8];

@@ -50,6 +50,7 @@ struct PlacePlan {
 struct SamplePlan {
   Carve c;
   size_t partial;
+  size_t coef;        // gdp_ppo_grad: G * K coefficients
   int chunks;
 };
 void plan_embed(const gdp_graph* g, const gdp_gnn* gnn, EmbedPlan* p);

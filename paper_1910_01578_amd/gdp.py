@@ -9,7 +9,7 @@ from __future__ import annotations
 
 import ctypes
 import os
-from ctypes import POINTER, c_char_p, c_double, c_int32, c_int64, c_size_t, c_uint32, c_uint64, c_void_p
+from ctypes import POINTER, c_char_p, c_double, c_float, c_int32, c_int64, c_size_t, c_uint32, c_uint64, c_void_p
 from typing import Dict, Optional
 
 import numpy as np
@@ -30,7 +30,7 @@ GDP_MAX_GRAPHS = 128
 
 KERNEL_KINDS = ["graph_prep", "nbr_sample", "gemm_pool_sigmoid", "gather_max", "gemm_update_relu",
                 "meanpool", "film", "pre_layer", "seg_attention", "post_attn",
-                "head_lse", "gumbel_sample", "logp_reduce", "mlp_placer"]
+                "head_lse", "gumbel_sample", "logp_reduce", "mlp_placer", "ppo_grad"]
 K_COUNT = len(KERNEL_KINDS)
 
 
@@ -91,6 +91,8 @@ def _load():
         "gdp_validate_graph_host": (c_int32, [c_void_p, c_int32, c_void_p, c_int32, c_void_p, c_int64, c_uint32]),
         "gdp_last_error": (c_char_p, []),
         "gdp_abi_version": (c_int32, []),
+        "gdp_ppo_grad": (c_int32, [POINTER(GdpGraph), c_void_p, c_void_p, c_int32, c_int32, c_void_p, c_void_p,
+                                   c_void_p, c_void_p, c_float, c_void_p, c_void_p, c_void_p, c_size_t, c_void_p]),
         "gdp_debug_uniforms": (c_int32, [c_uint64, c_int32, c_int32, c_int32, c_void_p, c_void_p]),
         "gdp_debug_neighbors": (c_int32, [POINTER(GdpGraph), POINTER(GdpGnn), c_void_p, c_void_p, c_int64,
                                           c_void_p, c_size_t, c_void_p]),
@@ -242,6 +244,20 @@ class Runner:
         self.embed(stream)
         self.place(stream)
         self.sample(seed, stream=stream)
+
+    def ppo_grad(self, logp_old, advantages, clip_eps: float = 0.2, use_lse: bool = True, stream=None):
+        """PPO's clipped surrogate per graph and its gradient with respect to the
+        logits, for the placements and log-probs of the last sample() call."""
+        torch = _torch()
+        G, N, D = self.graph.n_graphs, self.graph.n_nodes, self.policy.cfg.n_devices
+        loss = torch.empty((G,), dtype=torch.float32, device=self.ws.device)
+        dlogits = torch.empty((N, D), dtype=torch.float32, device=self.ws.device)
+        check(lib.gdp_ppo_grad(ctypes.byref(self.graph.c), self.logits.data_ptr(),
+                               self.lse.data_ptr() if use_lse else None, D, self.k, self.placements.data_ptr(),
+                               self.logp.data_ptr(), logp_old.data_ptr(), advantages.data_ptr(), float(clip_eps),
+                               loss.data_ptr(), dlogits.data_ptr(), self.ws.data_ptr(), self.ws_bytes,
+                               _stream_handle(stream)))
+        return loss, dlogits
 
     def neighbors(self, stream=None):
         torch = _torch()

@@ -212,6 +212,20 @@ def test_sample_rejects(D, K, code):
     assert r == gdp.GDP_E_INVALID_ARG
 
 
+def test_ppo_grad_rejects():
+    cfg, gp, g, gl, gnn, pl, placer = _descs()
+    dev = 0x100000
+    args = lambda eps, out=dev: (ctypes.byref(g), dev, None, cfg.n_devices, 4, dev, dev, dev, dev, ctypes.c_float(eps),
+                                 dev, out, 0x1000000, 1 << 30, None)
+    assert gdp.lib.gdp_ppo_grad(*args(0.0)) == gdp.GDP_E_INVALID_ARG
+    assert gdp.lib.gdp_ppo_grad(*args(1.0)) == gdp.GDP_E_INVALID_ARG
+    assert gdp.lib.gdp_ppo_grad(*args(float("nan"))) == gdp.GDP_E_INVALID_ARG
+    assert gdp.lib.gdp_ppo_grad(*args(0.2, out=None)) == gdp.GDP_E_INVALID_ARG
+    r = gdp.lib.gdp_ppo_grad(ctypes.byref(g), dev, None, cfg.n_devices, 4, dev, dev, dev, dev, ctypes.c_float(0.2), dev,
+                             dev, 0x1000000, 16, None)
+    assert r == gdp.GDP_E_WORKSPACE
+
+
 def test_timer_state_machine():
     assert gdp.lib.gdp_timer_begin(1) == gdp.GDP_OK
     assert gdp.lib.gdp_timer_begin(1) == gdp.GDP_E_INVALID_ARG

@@ -463,3 +463,50 @@ def test_place_without_attention_edges(label, over, dtype):
     err_s = rel_err_rows(to_np(r.lse), p["lse"])
     _log(f"  logits err {err_l:.3e}  lse err {err_s:.3e}")
     assert err_l <= TOL[dtype] and err_s <= TOL[dtype]
+
+
+# ----------------------------------------------------------------------------
+# The update path's first step: PPO's clipped surrogate and its logit gradient.
+def _ppo_case(cfg, g, w, seed=7, spread=0.3):
+    import torch
+    r = _runner(cfg, g, w)
+    r.forward(cfg.sample_seed)
+    _sync()
+    G, K = r.logp.shape
+    rng = np.random.default_rng(seed)
+    logp = r.logp.cpu().numpy().astype(np.float64)
+    logp_old = (logp + rng.normal(scale=spread, size=(G, K))).astype(np.float32)
+    adv = rng.normal(size=(G, K)).astype(np.float32)
+    return r, torch.from_numpy(logp_old).cuda(), torch.from_numpy(adv).cuda(), logp_old, adv
+
+
+def _check_ppo(r, g, lo_d, adv_d, lo, adv, eps, use_lse=True):
+    loss, dlogits = r.ppo_grad(lo_d, adv_d, eps, use_lse=use_lse)
+    _sync()
+    ref = O.ppo_clipped_surrogate(to_np(r.logits), to_np(r.lse), g.graph_ptr, r.placements.cpu().numpy(),
+                                  to_np(r.logp), lo.astype(np.float64), adv.astype(np.float64), eps)
+    rat = np.exp(to_np(r.logp) - lo.astype(np.float64))
+    clipped = float(((rat < 1 - eps) | (rat > 1 + eps)).mean())
+    err_d = rel_err_rows(to_np(dlogits), ref["dlogits"])
+    err_l = float(np.abs(to_np(loss) - ref["loss"]).max() / max(1e-30, np.abs(ref["loss"]).max()))
+    _log(f"  ppo: clipped fraction {clipped:.2f}  loss err {err_l:.2e}  dlogits err {err_d:.2e}")
+    assert err_l <= 1e-5 and err_d <= 1e-4
+    return clipped
+
+
+@pytest.mark.parametrize("name", ALL)
+def test_ppo_grad_parity(name):
+    cfg, g, w = workload(name)
+    _log("ppo", name)
+    r, lo_d, adv_d, lo, adv = _ppo_case(cfg, g, w)
+    clipped = _check_ppo(r, g, lo_d, adv_d, lo, adv, 0.2)
+    assert 0.0 < clipped < 1.0        # both branches of the min occur
+
+
+def test_ppo_grad_many_devices_no_lse_both_branches():
+    cfg = W.get_config("tiny_layered_256").replace(n_devices=20, k_samples=9, graph_sizes=(100, 57, 99))
+    _log("ppo edge: D=20, K=9, 3 graphs, lse recomputed")
+    g, w = W.make_graph(cfg), W.make_weights(cfg)
+    r, lo_d, adv_d, lo, adv = _ppo_case(cfg, g, w, spread=0.3)
+    clipped = _check_ppo(r, g, lo_d, adv_d, lo, adv, 0.15, use_lse=False)
+    assert 0.0 < clipped < 1.0
