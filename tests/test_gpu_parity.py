@@ -510,3 +510,68 @@ def test_ppo_grad_many_devices_no_lse_both_branches():
     r, lo_d, adv_d, lo, adv = _ppo_case(cfg, g, w, spread=0.3)
     clipped = _check_ppo(r, g, lo_d, adv_d, lo, adv, 0.15, use_lse=False)
     assert 0.0 < clipped < 1.0
+
+
+# ----------------------------------------------------------------------------
+# The implementation's limits at once: GDP_MAX_GRAPHS graphs of ragged sizes
+# (1 to 59 nodes, many segments with partial tails and memory resets at every
+# graph start), fanout GDP_MAX_FANOUT with hub nodes above it, and
+# GDP_MAX_DEVICES devices.
+def _max_batch(cfg):
+    rng = np.random.default_rng(11)
+    sizes = rng.integers(1, 60, size=128)
+    src, dst, off = [], [], 0
+    for gi, n in enumerate(sizes):
+        n = int(n)
+        for v in range(1, n):                       # 1-3 earlier nodes as inputs
+            for u in rng.choice(v, size=min(v, int(rng.integers(1, 4))), replace=False):
+                src.append(off + int(u)); dst.append(off + v)
+        if gi % 8 == 0 and n > 2:                   # a hub: node 0 feeds every other node
+            for v in range(1, n):
+                src.append(off); dst.append(off + v)
+        off += n
+    N = off
+    key = np.unique(np.asarray(src, np.int64) * N + np.asarray(dst, np.int64))
+    s, d = (key // N).astype(np.int32), (key % N).astype(np.int32)
+    row_ptr = np.zeros(N + 1, np.int64)
+    np.add.at(row_ptr, s + 1, 1)
+    row_ptr = np.cumsum(row_ptr).astype(np.int32)
+    gp = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int32)
+    x = W.make_features(cfg, N, rng)
+    return W.graph_from_arrays(cfg, gp, row_ptr, d, x)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_limits_max_graphs_fanout_devices(dtype):
+    over = dict(fanout=32, n_devices=64, k_samples=3, seg_len=16, mem_len=8)
+    if dtype == "bf16":
+        over = {**BF16_WIDTH, **over}
+    cfg = W.get_config("tiny_layered_256").replace(dtype=dtype, **over)
+    g = _max_batch(cfg)
+    deg = np.diff(g.row_ptr)
+    _log(f"limits {dtype}: {len(g.graph_ptr) - 1} graphs, {g.n_nodes} nodes, max out-degree {deg.max()}")
+    assert len(g.graph_ptr) - 1 == 128 and deg.max() > 32
+    w = W.make_weights(cfg)
+    r = _runner(cfg, g, w)
+    s_ptr, s_idx = r.neighbors()
+    r.forward(cfg.sample_seed)
+    _sync()
+    s_ptr, s_idx = s_ptr.cpu().numpy(), s_idx.cpu().numpy()
+    S = O.sample_neighbours(O.neighbour_lists(g.row_ptr, g.col_idx), g.graph_ptr, cfg.fanout, cfg.nb_seed)
+    for v in range(g.n_nodes):
+        assert np.array_equal(np.sort(s_idx[s_ptr[v]:s_ptr[v + 1]]), S[v]), v
+    gnn, pl, hd = w.f64()
+    e = O.embed(g.graph_ptr, g.row_ptr, g.col_idx, g.x, gnn, cfg.fanout, cfg.nb_seed)
+    pg = O.place(to_np(r.node_emb), to_np(r.graph_emb), g.graph_ptr, pl, hd["w_out"], hd["b_out"], cfg.heads,
+                 cfg.seg_len, cfg.mem_len, cfg.film)
+    tol = TOL[dtype]
+    err_h = rel_err_rows(to_np(r.node_emb), e["node_emb"])
+    err_g = rel_err_rows(to_np(r.graph_emb), e["graph_emb"])
+    logits = to_np(r.logits)
+    err_p = rel_err_rows(logits, pg["logits"])
+    _log(f"  node_emb err {err_h:.3e}  graph_emb err {err_g:.3e}  placer err {err_p:.3e}")
+    assert err_h <= tol and err_g <= tol and err_p <= tol
+    placements = r.placements.cpu().numpy()
+    check_placements(logits, pg["logits"], placements, cfg.sample_seed, g.graph_ptr, max_exempt=0.2)
+    own = O.log_prob_of(logits.astype(np.float64), to_np(r.lse).astype(np.float64), g.graph_ptr, placements)
+    assert float(np.abs(to_np(r.logp) - own).max() / np.abs(own).max()) <= 1e-5
