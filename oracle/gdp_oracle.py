@@ -384,3 +384,11 @@ def ppo_clipped_surrogate(logits, lse, graph_ptr, placements, logp, logp_old, ad
                 dlogits[v, placements[k, v]] += coef[g, k]
             dlogits[gs:ge] -= coef[g, k] * soft[gs:ge]
     return {"loss": loss, "coef": coef, "dlogits": dlogits}
+
+
+def head_backward(x, w_out, dlogits):
+    """The head's backward pass (logits = x W_out^T + b_out): the gradients with
+    respect to its input, weight and bias for a given dL/dlogits."""
+    x = np.asarray(x, np.float64)
+    dl = np.asarray(dlogits, np.float64)
+    return {"dx": dl @ np.asarray(w_out, np.float64), "dw_out": dl.T @ x, "db_out": dl.sum(axis=0)}

@@ -74,3 +74,57 @@ def test_ppo_closed_forms():
     # zero advantages: zero loss and gradient
     z = O.ppo_clipped_surrogate(logits, lse, gp, p, logp, logp + 0.1, np.zeros_like(adv), 0.2)
     assert np.all(z["loss"] == 0) and np.all(z["dlogits"] == 0)
+
+
+def test_head_backward_equals_torch_autograd():
+    rng = np.random.default_rng(9)
+    N, d, D = 37, 16, 5
+    x = rng.normal(size=(N, d))
+    w = rng.normal(size=(D, d))
+    b = rng.normal(size=D)
+    dl = rng.normal(size=(N, D))
+    ours = O.head_backward(x, w, dl)
+    tx = torch.tensor(x, requires_grad=True)
+    tw = torch.tensor(w, requires_grad=True)
+    tb = torch.tensor(b, requires_grad=True)
+    (torch.nn.functional.linear(tx, tw, tb) * torch.from_numpy(dl)).sum().backward()
+    np.testing.assert_allclose(ours["dx"], tx.grad.numpy(), rtol=0, atol=1e-12)
+    np.testing.assert_allclose(ours["dw_out"], tw.grad.numpy(), rtol=0, atol=1e-12)
+    np.testing.assert_allclose(ours["db_out"], tb.grad.numpy(), rtol=0, atol=1e-12)
+    # a one-hot output gradient selects the weight row and the input row
+    e = np.zeros((N, D))
+    e[3, 2] = 1.0
+    one = O.head_backward(x, w, e)
+    np.testing.assert_array_equal(one["dx"][3], w[2])
+    np.testing.assert_array_equal(one["dw_out"][2], x[3])
+
+
+def test_update_chain_equals_torch_autograd():
+    """PPO loss -> logits -> head: the oracle's two steps composed equal torch
+    autograd through the head and the clipped surrogate."""
+    rng = np.random.default_rng(13)
+    gp = np.array([0, 9, 21])
+    N, d, D, K = 21, 8, 4, 6
+    x = rng.normal(size=(N, d))
+    w = rng.normal(size=(D, d)) * 0.5
+    b = rng.normal(size=D) * 0.1
+    logits = x @ w.T + b
+    lse = O.logsumexp_rows(logits)
+    p = rng.integers(0, D, size=(K, N)).astype(np.int32)
+    logp = O.log_prob_of(logits, lse, gp, p)
+    logp_old = logp + rng.normal(scale=0.3, size=logp.shape)
+    adv = rng.normal(size=logp.shape)
+    g = O.ppo_clipped_surrogate(logits, lse, gp, p, logp, logp_old, adv, 0.2)
+    hb = O.head_backward(x, w, g["dlogits"])
+    tx = torch.tensor(x, requires_grad=True)
+    tw = torch.tensor(w, requires_grad=True)
+    ls = torch.log_softmax(torch.nn.functional.linear(tx, tw, torch.from_numpy(b)), dim=1)
+    pick = ls[torch.arange(N)[None, :].expand(K, N), torch.from_numpy(p).long()]
+    total = 0.0
+    for gi in range(2):
+        r = torch.exp(pick[:, gp[gi]:gp[gi + 1]].sum(dim=1) - torch.from_numpy(logp_old[gi]))
+        a = torch.from_numpy(adv[gi])
+        total = total - torch.minimum(r * a, torch.clamp(r, 0.8, 1.2) * a).mean()
+    (total / 2).backward()
+    np.testing.assert_allclose(hb["dx"], tx.grad.numpy(), rtol=0, atol=1e-12)
+    np.testing.assert_allclose(hb["dw_out"], tw.grad.numpy(), rtol=0, atol=1e-12)
