@@ -216,6 +216,26 @@ def main():
            "achieved": round(ppo_bytes / (ppo_us * 1e-6) / 1e9, 1), "unit": "GB/s", "peak": PEAK_HBM_GBS,
            "frac": round(ppo_bytes / (ppo_us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4)}
 
+    # The update path's second step: the head's backward pass on X (kept by
+    # place_train) and the PPO logit gradient.  HBM-bound: X and dlogits in,
+    # dX out (dW_out, db_out and W_out are a few KB).
+    _, dl = runner.ppo_grad(logp_old, adv, 0.2)
+    x_keep = runner.place_train()
+    for _ in range(3):
+        runner.head_backward(x_keep, dl)
+    torch.cuda.synchronize()
+    gdp.timer_begin(["head_backward"])
+    for _ in range(args.steps):
+        runner.head_backward(x_keep, dl)
+    torch.cuda.synchronize()
+    hr = gdp.timer_end()["head_backward"]
+    hb_us = 1e3 * hr["ms"] / hr["launches"]
+    hb_bytes = 4.0 * (2 * g.n_nodes * cfg.d_model + g.n_nodes * cfg.n_devices + cfg.n_devices * (cfg.d_model + 1))
+    head_bwd = {"us_per_call": round(hb_us, 2), "algorithmic_bytes": int(hb_bytes),
+                "achieved": round(hb_bytes / (hb_us * 1e-6) / 1e9, 1), "unit": "GB/s", "peak": PEAK_HBM_GBS,
+                "frac": round(hb_bytes / (hb_us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4)}
+    del x_keep, dl
+
     # The ablation's placer without attention (Section 4.3) on the same DAG and
     # weights: the same embed and sample calls around one fused placer kernel.
     ab = gdp.Runner(gdp.DeviceGraph(g, cfg.dtype), gdp.DevicePolicy(cfg, w, attention=False), cfg.k_samples)
@@ -263,6 +283,7 @@ def main():
         "kernels": kernels,
         "ablation_no_attention": ablation,
         "ppo_grad": ppo,
+        "head_backward": head_bwd,
     }
     print(json.dumps(out), flush=True)
 

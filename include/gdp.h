@@ -236,6 +236,30 @@ int gdp_sample(const gdp_graph* g, const float* logits, const float* lse, int32_
  * The workspace of gdp_workspace_bytes with the same k_samples suffices.
  * Deterministic (fixed summation orders).
  */
+/*
+ * gdp_place that also writes the placement network's output X (the head's
+ * input, the last layer's LN2 output), which the backward pass needs.
+ *   x_out  device [N, d] fp32 (output, 16-byte aligned)
+ */
+int gdp_place_train(const gdp_graph* g, const void* node_emb, const float* graph_emb,
+                    const gdp_placer* placer, float* logits, float* lse, float* x_out,
+                    void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * The head's backward pass (Fig. 1's output layer, logits = X W_out^T + b_out),
+ * the second step of the update path: for a given dL/dlogits,
+ *   dx      = dlogits W_out        device [N, d] fp32 (output, 16-byte aligned)
+ *   dw_out  = dlogits^T X          device [D, d] fp32 (output)
+ *   db_out  = sum_v dlogits[v]     device [D] fp32 (output)
+ *   x       device [N, d] fp32 (input, from gdp_place_train, 16-byte aligned)
+ *   dlogits device [N, D] fp32 (input, e.g. from gdp_ppo_grad)
+ * W_out is read from placer (its dtype is the graph's).  The workspace of
+ * gdp_workspace_bytes for this placer suffices.  Deterministic.
+ */
+int gdp_head_backward(const gdp_graph* g, const gdp_placer* placer, const float* x, const float* dlogits,
+                      float* dx, float* dw_out, float* db_out, void* workspace, size_t workspace_bytes,
+                      void* stream);
+
 int gdp_ppo_grad(const gdp_graph* g, const float* logits, const float* lse, int32_t n_devices,
                  int32_t k_samples, const int32_t* placements, const float* logp, const float* logp_old,
                  const float* advantages, float clip_eps, float* loss, float* dlogits, void* workspace,
@@ -294,6 +318,7 @@ typedef enum gdp_kernel_kind {
   GDP_K_LOGP_REDUCE,     /* per-graph log-prob sums                          */
   GDP_K_MLP_PLACER,      /* the ablation's placer without attention, all layers */
   GDP_K_PPO,             /* PPO clipped surrogate and its logit gradient     */
+  GDP_K_HEAD_BWD,        /* the head's backward pass                        */
   GDP_K_COUNT
 } gdp_kernel_kind;
 

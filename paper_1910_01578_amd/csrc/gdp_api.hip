@@ -175,7 +175,7 @@ static int embed_impl(const gdp_graph* g, const gdp_gnn* gnn, T* node_emb, float
 // ---------------------------------------------------------------------------
 template <typename T>
 static int place_impl(const gdp_graph* g, const T* node_emb, const float* graph_emb, const gdp_placer* p,
-                      float* logits, float* lse, const PlacePlan& pl, void* ws, hipStream_t st) {
+                      float* logits, float* lse, float* x_out, const PlacePlan& pl, void* ws, hipStream_t st) {
   const int N = g->n_nodes, G = g->n_graphs, d = p->d_model, L = p->n_layers;
   const GraphTable gt = make_table(g);
   float* film = at<float>(ws, pl.film);       // [L][2][G][d]: gamma then beta
@@ -223,19 +223,21 @@ static int place_impl(const gdp_graph* g, const T* node_emb, const float* graph_
     a.d = d;
     a.d_ff = p->d_ff;
     const bool fused = p->n_devices <= kFusedHeadDevices;
+    float* xfinal = x_out ? x_out : ybuf[0];
     if (fused) {
       a.w_out = static_cast<const T*>(p->w_out);
       a.b_out = static_cast<const T*>(p->b_out);
       a.n_dev = p->n_devices;
       a.logits = logits;
       a.lse = lse;
-    } else {
-      a.y_out = ybuf[0];
+    }
+    if (!fused || x_out) {
+      a.y_out = xfinal;
       a.ldyo = d;
     }
     GDP_LAUNCH(GDP_K_MLP_PLACER, launch_mlp_placer<T>(a, gt, st));
     if (!fused)
-      GDP_LAUNCH(GDP_K_HEAD, launch_head<T>(ybuf[0], static_cast<const T*>(p->w_out),
+      GDP_LAUNCH(GDP_K_HEAD, launch_head<T>(xfinal, static_cast<const T*>(p->w_out),
                                             static_cast<const T*>(p->b_out), N, d, p->n_devices, logits, lse, st));
     return GDP_OK;
   }
@@ -262,7 +264,7 @@ static int place_impl(const gdp_graph* g, const T* node_emb, const float* graph_
     const bool last = l + 1 == L;
     const bool next_film = p->film && !last;
     const gdp_placer_layer* Ln = last ? nullptr : &p->layers[l + 1];
-    float* ynext = ybuf[cur ^ 1];
+    float* ynext = last && x_out ? x_out : ybuf[cur ^ 1];
     PostAttnArgs<T> a_post = {o, d, y, d,
                                     static_cast<const T*>(Ly.w_o), static_cast<const T*>(Ly.b_o),
                                     static_cast<const T*>(Ly.ln1_g), static_cast<const T*>(Ly.ln1_b),
@@ -275,7 +277,7 @@ static int place_impl(const gdp_graph* g, const T* node_emb, const float* graph_
                                     Ln ? static_cast<const T*>(Ln->b_qkv) : nullptr,
                                     Ln ? qkv : nullptr, 3 * d, N, d, p->d_ff, q_scale};
     if (last && fused_head) {
-      a_post.y_out = nullptr;                // only the head reads the last layer's output
+      a_post.y_out = x_out;                  // only the head reads the last layer's output, unless asked for
       a_post.w_out = static_cast<const T*>(p->w_out);
       a_post.b_out = static_cast<const T*>(p->b_out);
       a_post.n_dev = p->n_devices;
@@ -339,8 +341,8 @@ extern "C" int gdp_embed(const gdp_graph* g, const gdp_gnn* gnn, void* node_emb,
   return embed_impl<float>(g, gnn, static_cast<float*>(node_emb), graph_emb, pl, ws, st);
 }
 
-extern "C" int gdp_place(const gdp_graph* g, const void* node_emb, const float* graph_emb, const gdp_placer* placer,
-                         float* logits, float* lse, void* ws, size_t ws_bytes, void* stream) {
+static int place_entry(const gdp_graph* g, const void* node_emb, const float* graph_emb, const gdp_placer* placer,
+                       float* logits, float* lse, float* x_out, void* ws, size_t ws_bytes, void* stream) {
   clear_error();
   int r;
   if ((r = check_graph(g)) != GDP_OK) return r;
@@ -354,8 +356,47 @@ extern "C" int gdp_place(const gdp_graph* g, const void* node_emb, const float* 
   if ((r = pending_hip_error()) != GDP_OK) return r;
   hipStream_t st = static_cast<hipStream_t>(stream);
   if (g->dtype == GDP_BF16)
-    return place_impl<bf16>(g, static_cast<const bf16*>(node_emb), graph_emb, placer, logits, lse, pl, ws, st);
-  return place_impl<float>(g, static_cast<const float*>(node_emb), graph_emb, placer, logits, lse, pl, ws, st);
+    return place_impl<bf16>(g, static_cast<const bf16*>(node_emb), graph_emb, placer, logits, lse, x_out, pl, ws, st);
+  return place_impl<float>(g, static_cast<const float*>(node_emb), graph_emb, placer, logits, lse, x_out, pl, ws, st);
+}
+
+extern "C" int gdp_place(const gdp_graph* g, const void* node_emb, const float* graph_emb, const gdp_placer* placer,
+                         float* logits, float* lse, void* ws, size_t ws_bytes, void* stream) {
+  return place_entry(g, node_emb, graph_emb, placer, logits, lse, nullptr, ws, ws_bytes, stream);
+}
+
+extern "C" int gdp_place_train(const gdp_graph* g, const void* node_emb, const float* graph_emb,
+                               const gdp_placer* placer, float* logits, float* lse, float* x_out, void* ws,
+                               size_t ws_bytes, void* stream) {
+  if (!x_out || !aligned16(x_out)) {
+    clear_error();
+    return fail(GDP_E_INVALID_ARG, "x_out is NULL or not 16-byte aligned");
+  }
+  return place_entry(g, node_emb, graph_emb, placer, logits, lse, x_out, ws, ws_bytes, stream);
+}
+
+extern "C" int gdp_head_backward(const gdp_graph* g, const gdp_placer* placer, const float* x, const float* dlogits,
+                                 float* dx, float* dw_out, float* db_out, void* ws, size_t ws_bytes, void* stream) {
+  clear_error();
+  int r;
+  if ((r = check_graph(g)) != GDP_OK) return r;
+  if ((r = check_placer(g, placer)) != GDP_OK) return r;
+  if (!x || !dlogits || !dx || !dw_out || !db_out) return fail(GDP_E_INVALID_ARG, "a head-backward input or output is NULL");
+  if (!aligned16(x) || !aligned16(dx)) return fail(GDP_E_INVALID_ARG, "x or dx is not 16-byte aligned");
+  PlacePlan pl;
+  plan_place(g, placer, &pl);
+  if ((r = check_ws(ws, ws_bytes, pl.c.total)) != GDP_OK) return r;
+  if ((r = pending_hip_error()) != GDP_OK) return r;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  float* partial = at<float>(ws, pl.head_partial);
+  const int N = g->n_nodes, d = placer->d_model, D = placer->n_devices;
+  if (g->dtype == GDP_BF16)
+    GDP_LAUNCH(GDP_K_HEAD_BWD, launch_head_backward<bf16>(x, static_cast<const bf16*>(placer->w_out), dlogits, N, d, D,
+                                                          dx, dw_out, db_out, partial, st));
+  else
+    GDP_LAUNCH(GDP_K_HEAD_BWD, launch_head_backward<float>(x, static_cast<const float*>(placer->w_out), dlogits, N, d,
+                                                           D, dx, dw_out, db_out, partial, st));
+  return GDP_OK;
 }
 
 extern "C" int gdp_sample(const gdp_graph* g, const float* logits, const float* lse, int32_t n_devices,
@@ -459,7 +500,7 @@ extern "C" const char* gdp_kernel_kind_name(int32_t kind) {
   static const char* names[GDP_K_COUNT] = {
       "graph_prep", "nbr_sample",    "gemm_pool_sigmoid", "gather_max", "gemm_update_relu",
       "meanpool",   "film",          "pre_layer",         "seg_attention", "post_attn",
-      "head_lse",   "gumbel_sample", "logp_reduce",       "mlp_placer", "ppo_grad"};
+      "head_lse",   "gumbel_sample", "logp_reduce",       "mlp_placer", "ppo_grad",  "head_backward"};
   if (kind < 0 || kind >= GDP_K_COUNT) return "";
   return names[kind];
 }

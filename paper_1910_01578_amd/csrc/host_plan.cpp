@@ -170,6 +170,7 @@ void plan_place(const gdp_graph* g, const gdp_placer* pl, PlacePlan* p) {
   carve_init(&p->c);
   p->film = carve_add(&p->c, (size_t)pl->n_layers * g->n_graphs * d * 2 * 4);
   p->y0 = carve_add(&p->c, N * d * 4);      // residual stream: fp32
+  p->head_partial = carve_add(&p->c, ((N + kHeadBwdRows - 1) / kHeadBwdRows) * (size_t)pl->n_devices * (d + 1) * 4);
   if (!pl->attention) {                     // only the head's input, when the head runs on its own
     p->qblocks = 0;
     p->y1 = p->qkv = p->o = p->y0;

@@ -45,8 +45,10 @@ struct EmbedPlan {
 struct PlacePlan {
   Carve c;
   size_t film, y0, y1, qkv, o;
+  size_t head_partial;   // gdp_head_backward: per row chunk, D x d weight and D bias partial sums
   int qblocks;
 };
+constexpr int kHeadBwdRows = 128;   // rows per head-backward chunk
 struct SamplePlan {
   Carve c;
   size_t partial;

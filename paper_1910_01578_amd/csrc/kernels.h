@@ -190,5 +190,11 @@ hipError_t launch_debug_uniforms(uint64_t seed, int n, int K, int D, float* out,
 hipError_t launch_ppo(const float* logits, const float* lse, const int* placements, const float* logp,
                       const float* logp_old, const float* adv, float eps, const GraphTable& gt, int n, int D, int K,
                       float* coef, float* loss, float* dlogits, hipStream_t s);
+// The head's backward pass: dx [n, d] = dlogits W_out, dw_out [D, d] = dlogits^T x,
+// db_out [D] = column sums of dlogits; partial: ceil(n / kHeadBwdRows) * D * (d + 1)
+// floats of scratch.  d divides 256, D <= 64.
+template <typename T>
+hipError_t launch_head_backward(const float* x, const T* w_out, const float* dlogits, int n, int d, int D, float* dx,
+                                float* dw_out, float* db_out, float* partial, hipStream_t s);
 
 }  // namespace gdp

@@ -30,7 +30,7 @@ GDP_MAX_GRAPHS = 128
 
 KERNEL_KINDS = ["graph_prep", "nbr_sample", "gemm_pool_sigmoid", "gather_max", "gemm_update_relu",
                 "meanpool", "film", "pre_layer", "seg_attention", "post_attn",
-                "head_lse", "gumbel_sample", "logp_reduce", "mlp_placer", "ppo_grad"]
+                "head_lse", "gumbel_sample", "logp_reduce", "mlp_placer", "ppo_grad", "head_backward"]
 K_COUNT = len(KERNEL_KINDS)
 
 
@@ -91,6 +91,10 @@ def _load():
         "gdp_validate_graph_host": (c_int32, [c_void_p, c_int32, c_void_p, c_int32, c_void_p, c_int64, c_uint32]),
         "gdp_last_error": (c_char_p, []),
         "gdp_abi_version": (c_int32, []),
+        "gdp_place_train": (c_int32, [POINTER(GdpGraph), c_void_p, c_void_p, POINTER(GdpPlacer), c_void_p, c_void_p,
+                                      c_void_p, c_void_p, c_size_t, c_void_p]),
+        "gdp_head_backward": (c_int32, [POINTER(GdpGraph), POINTER(GdpPlacer), c_void_p, c_void_p, c_void_p, c_void_p,
+                                        c_void_p, c_void_p, c_size_t, c_void_p]),
         "gdp_ppo_grad": (c_int32, [POINTER(GdpGraph), c_void_p, c_void_p, c_int32, c_int32, c_void_p, c_void_p,
                                    c_void_p, c_void_p, c_float, c_void_p, c_void_p, c_void_p, c_size_t, c_void_p]),
         "gdp_debug_uniforms": (c_int32, [c_uint64, c_int32, c_int32, c_int32, c_void_p, c_void_p]),
@@ -232,6 +236,29 @@ class Runner:
         check(lib.gdp_place(ctypes.byref(self.graph.c), self.node_emb.data_ptr(), self.graph_emb.data_ptr(),
                             ctypes.byref(self.policy.placer), self.logits.data_ptr(), self.lse.data_ptr(),
                             self.ws.data_ptr(), self.ws_bytes, _stream_handle(stream)))
+
+    def place_train(self, stream=None):
+        """place() that also keeps the placement network's output X [N, d] (fp32),
+        the head's input, for head_backward(); returns X."""
+        torch = _torch()
+        x = torch.empty((self.graph.n_nodes, self.policy.cfg.d_model), dtype=torch.float32, device=self.ws.device)
+        check(lib.gdp_place_train(ctypes.byref(self.graph.c), self.node_emb.data_ptr(), self.graph_emb.data_ptr(),
+                                  ctypes.byref(self.policy.placer), self.logits.data_ptr(), self.lse.data_ptr(),
+                                  x.data_ptr(), self.ws.data_ptr(), self.ws_bytes, _stream_handle(stream)))
+        return x
+
+    def head_backward(self, x, dlogits, stream=None):
+        """The head's backward pass for dL/dlogits: returns (dx, dw_out, db_out), fp32."""
+        torch = _torch()
+        N, d, D = self.graph.n_nodes, self.policy.cfg.d_model, self.policy.cfg.n_devices
+        dev = self.ws.device
+        dx = torch.empty((N, d), dtype=torch.float32, device=dev)
+        dw = torch.empty((D, d), dtype=torch.float32, device=dev)
+        db = torch.empty((D,), dtype=torch.float32, device=dev)
+        check(lib.gdp_head_backward(ctypes.byref(self.graph.c), ctypes.byref(self.policy.placer), x.data_ptr(),
+                                    dlogits.data_ptr(), dx.data_ptr(), dw.data_ptr(), db.data_ptr(),
+                                    self.ws.data_ptr(), self.ws_bytes, _stream_handle(stream)))
+        return dx, dw, db
 
     def sample(self, seed: int, uniforms=None, use_lse: bool = True, stream=None):
         check(lib.gdp_sample(ctypes.byref(self.graph.c), self.logits.data_ptr(),

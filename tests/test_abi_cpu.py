@@ -226,6 +226,24 @@ def test_ppo_grad_rejects():
     assert r == gdp.GDP_E_WORKSPACE
 
 
+def test_place_train_and_head_backward_reject():
+    """gdp_place_train needs an aligned x_out; gdp_head_backward checks its
+    pointers, the placer and the workspace size before any GPU work."""
+    cfg, gp, g, gl, gnn, pl, placer = _descs()
+    dev = 0x100000
+    for x_out in (None, dev + 4):
+        r = gdp.lib.gdp_place_train(ctypes.byref(g), dev, dev, ctypes.byref(placer), dev, None, x_out, 0x1000000,
+                                    1 << 30, None)
+        assert r == gdp.GDP_E_INVALID_ARG, gdp.last_error()
+        assert "x_out" in gdp.last_error()
+    hb = lambda x=dev, ws=1 << 30: gdp.lib.gdp_head_backward(ctypes.byref(g), ctypes.byref(placer), x, dev, dev, dev,
+                                                             dev, 0x1000000, ws, None)
+    assert hb(x=None) == gdp.GDP_E_INVALID_ARG
+    assert hb(ws=16) == gdp.GDP_E_WORKSPACE
+    placer.n_devices = 65
+    assert hb() == gdp.GDP_E_UNSUPPORTED
+
+
 def test_timer_state_machine():
     assert gdp.lib.gdp_timer_begin(1) == gdp.GDP_OK
     assert gdp.lib.gdp_timer_begin(1) == gdp.GDP_E_INVALID_ARG

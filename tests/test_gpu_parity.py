@@ -513,6 +513,69 @@ def test_ppo_grad_many_devices_no_lse_both_branches():
 
 
 # ----------------------------------------------------------------------------
+# The update path's second step: the head's backward pass, on the placement
+# network's output X that gdp_place_train keeps and the PPO logit gradient.
+def _check_head_backward(cfg, g, w, attention=True, label=""):
+    import torch
+    cfg = cfg.replace(attention=attention)
+    r = _runner(cfg, g, w)
+    r.embed()
+    r.place()
+    _sync()
+    logits_plain = _bits(r.logits)
+    x = r.place_train()
+    r.sample(cfg.sample_seed)
+    _sync()
+    assert _bits(r.logits) == logits_plain           # keeping X changes nothing else
+    _, pl, hd = w.f64()
+    p = O.place(to_np(r.node_emb), to_np(r.graph_emb), g.graph_ptr, pl, hd["w_out"], hd["b_out"], cfg.heads,
+                cfg.seg_len, cfg.mem_len, cfg.film, attention=attention)
+    err_x = rel_err_rows(to_np(x), p["x"])
+    G, K = r.logp.shape
+    rng = np.random.default_rng(5)
+    lo = (r.logp.cpu().numpy() + rng.normal(scale=0.3, size=(G, K))).astype(np.float32)
+    adv = rng.normal(size=(G, K)).astype(np.float32)
+    _, dl = r.ppo_grad(torch.from_numpy(lo).cuda(), torch.from_numpy(adv).cuda())
+    dx, dw, db = r.head_backward(x, dl)
+    _sync()
+    xg, dlg = to_np(x), to_np(dl)
+    ref = O.head_backward(xg, hd["w_out"], dlg)
+    err_dx = rel_err_rows(to_np(dx), ref["dx"])
+    # fp32 sums over all N rows: bounded against the sums of |terms|
+    bw = np.abs(dlg).T @ np.abs(xg)
+    bb = np.abs(dlg).sum(axis=0)
+    err_dw = float((np.abs(to_np(dw) - ref["dw_out"]) / np.maximum(bw, 1e-30)).max())
+    err_db = float((np.abs(to_np(db) - ref["db_out"]) / np.maximum(bb, 1e-30)).max())
+    _log(f"  head backward {label}: x err {err_x:.2e}  dx {err_dx:.2e}  dW {err_dw:.2e}  db {err_db:.2e}")
+    assert err_x <= TOL[cfg.dtype]
+    assert err_dx <= 1e-5 and err_dw <= 1e-5 and err_db <= 1e-5
+
+
+@pytest.mark.parametrize("name", ALL)
+def test_head_backward_parity(name):
+    cfg, g, w = workload(name)
+    _log("head backward", name)
+    _check_head_backward(cfg, g, w, label=name)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("label,over,attention", [
+    ("many_devices_ragged", dict(n_devices=20, graph_sizes=(300, 57, 1)), True),
+    ("max_devices_no_attention", dict(n_devices=64, graph_sizes=(513,)), False),
+    ("single_node", dict(graph_sizes=(1,)), True),
+], ids=lambda v: v if isinstance(v, str) else None)
+def test_head_backward_edges(label, over, attention, dtype):
+    over = dict(over)
+    if dtype == "bf16":
+        over = {**BF16_WIDTH, **over}
+    cfg = W.get_config("tiny_layered_256").replace(dtype=dtype, **over)
+    _log("head backward, edge", label, dtype)
+    g = _edge_graph(cfg, "single") if cfg.graph_sizes == (1,) else W.make_graph(cfg)
+    w = W.make_weights(cfg)
+    _check_head_backward(cfg, g, w, attention=attention, label=label)
+
+
+# ----------------------------------------------------------------------------
 # The implementation's limits at once: GDP_MAX_GRAPHS graphs of ragged sizes
 # (1 to 59 nodes, many segments with partial tails and memory resets at every
 # graph start), fanout GDP_MAX_FANOUT with hub nodes above it, and
