@@ -453,30 +453,43 @@ __global__ __launch_bounds__(256) void k_meanpool_partial(const T* __restrict__ 
   }
 }
 
-__global__ __launch_bounds__(256) void k_meanpool_final(const float* __restrict__ partial, int H, GraphTable ct,
-                                                        float* __restrict__ out) {
-  __shared__ float red[16][16];
+// graph_emb[g][col] = (sum over graph g's chunks of partial[c][col]) / |V_g|.
+// A block covers 64 columns of one graph; wave w adds chunks w, w + 16, ... into
+// eight running sums (chunk c0 + w + 16 (8 q + e) into sum e, so eight loads are
+// in flight), and the 16 waves' sums meet in LDS in a fixed pairwise order.
+constexpr int kPoolFinalWaves = 16;
+__global__ __launch_bounds__(64 * kPoolFinalWaves) void k_meanpool_final(const float* __restrict__ partial, int H,
+                                                                        GraphTable ct, float* __restrict__ out) {
+  constexpr int W = kPoolFinalWaves, E = 8;
+  __shared__ float red[W][64];
   const int g = blockIdx.x;
-  const int cl = threadIdx.x & 15, sl = threadIdx.x >> 4;
-  const int col = blockIdx.y * 16 + cl;
-  // slice sl adds chunks sl, sl + 16, ... : four running sums (chunks 64q + sl
-  // + 16e into sum e) keep four loads in flight, combined in a fixed order
-  float acc[4] = {0.f, 0.f, 0.f, 0.f};
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int col = blockIdx.y * 64 + lane;
+  const int c0 = ct.blk[g], c1 = ct.blk[g + 1];
+  float acc[E];
+#pragma unroll
+  for (int e = 0; e < E; ++e) acc[e] = 0.f;
+  // past-the-end chunks load the last one and add nothing: no branch, so the
+  // eight loads issue back to back
   if (col < H)
-    for (int c = ct.blk[g] + sl; c < ct.blk[g + 1]; c += 64) {
+    for (int c = c0 + w; c < c1; c += W * E) {
+      float v[E];
 #pragma unroll
-      for (int e = 0; e < 4; ++e)
-        if (c + 16 * e < ct.blk[g + 1]) acc[e] += partial[(size_t)(c + 16 * e) * H + col];
+      for (int e = 0; e < E; ++e) v[e] = partial[(size_t)min(c + W * e, c1 - 1) * H + col];
+#pragma unroll
+      for (int e = 0; e < E; ++e) acc[e] += c + W * e < c1 ? v[e] : 0.f;
     }
-  red[sl][cl] = (acc[0] + acc[1]) + (acc[2] + acc[3]);
+  red[w][lane] = ((acc[0] + acc[1]) + (acc[2] + acc[3])) + ((acc[4] + acc[5]) + (acc[6] + acc[7]));
   __syncthreads();
-  if (sl == 0 && col < H) {
-    float t[8];
+  if (w == 0 && col < H) {
+    float t[W / 2];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) t[i] = red[2 * i][cl] + red[2 * i + 1][cl];
+    for (int i = 0; i < W / 2; ++i) t[i] = red[2 * i][lane] + red[2 * i + 1][lane];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) t[i] = t[2 * i] + t[2 * i + 1];
-    const float sum = (t[0] + t[1]) + (t[2] + t[3]);
+    for (int i = 0; i < W / 4; ++i) t[i] = t[2 * i] + t[2 * i + 1];
+#pragma unroll
+    for (int i = 0; i < W / 8; ++i) t[i] = t[2 * i] + t[2 * i + 1];
+    const float sum = t[0] + t[1];
     out[(size_t)g * H + col] = sum / (float)(ct.ptr[g + 1] - ct.ptr[g]);
   }
 }
@@ -492,7 +505,8 @@ hipError_t launch_meanpool(const T* h, int H, const GraphTable& ct, int total_ch
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_meanpool_final, dim3(ct.n, (H + 15) / 16), dim3(256), 0, s, partial, H, ct, graph_emb);
+  hipLaunchKernelGGL(k_meanpool_final, dim3(ct.n, (H + 63) / 64), dim3(64 * kPoolFinalWaves), 0, s, partial, H, ct,
+                     graph_emb);
   return hipGetLastError();
 }
 template hipError_t launch_meanpool<float>(const float*, int, const GraphTable&, int, float*, float*, hipStream_t);

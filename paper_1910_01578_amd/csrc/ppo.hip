@@ -68,23 +68,37 @@ __global__ __launch_bounds__(256) void k_ppo_dlogits(const float* __restrict__ l
     for (int j = 0; j < D; ++j) s += expf(row[j] - m);
     lz = m + logf(s);
   }
+  // Loads past the end read the last element and are masked afterwards, so no
+  // load sits behind a branch and each group of eight issues back to back.
   float csum = 0.f;
-  for (int k = 0; k < K; ++k) csum += c[k];
+  for (int k0 = 0; k0 < K; k0 += 8) {
+    float cv[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) cv[u] = c[min(k0 + u, K - 1)];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) csum += k0 + u < K ? cv[u] : 0.0f;
+  }
   for (int jb = 0; jb < D; jb += 8) {
+    float rv[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) rv[e] = row[min(jb + e, D - 1)];
     float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
     for (int k0 = q; k0 < K; k0 += 8 * kPpoLanes) {
       int p[8];
+      float ck[8];
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
-        const int k = k0 + u * kPpoLanes;
-        p[u] = k < K ? placements[(size_t)k * n + vv] - jb : -1;
+        const int kc = min(k0 + u * kPpoLanes, K - 1);
+        p[u] = placements[(size_t)kc * n + vv];
+        ck[u] = c[kc];
       }
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
-        const int k = k0 + u * kPpoLanes;
-        const float ck = k < K ? c[k] : 0.0f;
+        const bool in = k0 + u * kPpoLanes < K;
+        const int pj = in ? p[u] - jb : -1;
+        const float cu = in ? ck[u] : 0.0f;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) acc[e] += p[u] == e ? ck : 0.0f;
+        for (int e = 0; e < 8; ++e) acc[e] += pj == e ? cu : 0.0f;
       }
     }
 #pragma unroll
@@ -96,7 +110,7 @@ __global__ __launch_bounds__(256) void k_ppo_dlogits(const float* __restrict__ l
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         const int j = jb + e;
-        if (j < D) dlogits[(size_t)v * D + j] = acc[e] - expf(row[j] - lz) * csum;
+        if (j < D) dlogits[(size_t)v * D + j] = acc[e] - expf(rv[e] - lz) * csum;
       }
     }
   }
@@ -275,11 +289,11 @@ __global__ __launch_bounds__(64 * kHeadReduceWaves) void k_head_bwd_reduce(const
   float a[4] = {0.f, 0.f, 0.f, 0.f};
   constexpr int S = kHeadReduceWaves;
   for (int c = w; c < chunks; c += 4 * S) {
+    float v[4];
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int ce = c + e * S;
-      if (ce < chunks) a[e] += partial[(size_t)ce * width + ic];
-    }
+    for (int e = 0; e < 4; ++e) v[e] = partial[(size_t)min(c + e * S, chunks - 1) * width + ic];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) a[e] += c + e * S < chunks ? v[e] : 0.f;
   }
   sw[w][lane] = (a[0] + a[1]) + (a[2] + a[3]);
   __syncthreads();
