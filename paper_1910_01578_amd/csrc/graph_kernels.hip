@@ -212,15 +212,36 @@ __global__ __launch_bounds__(256) void k_nbr_light(const int* __restrict__ row_p
   if (v >= n) return;
   const int o0 = row_ptr[v], o1 = row_ptr[v + 1];
   const int i0 = in_ptr[v], i1 = in_ptr[v + 1];
+  const int sp = s_ptr[v];                      // read with the others: one round of loads
   const int deg = (o1 - o0) + (i1 - i0);
   if (deg > fanout) {
     heavy[atomicAdd(heavy_count, 1)] = v;
     return;
   }
-  int* out = s_idx + s_ptr[v];
+  // groups of four loads issued before their stores (a list may be empty, and
+  // an empty edge array may not be read at all, so every load is guarded)
+  int* out = s_idx + sp;
   int w = 0;
-  for (int e = o0; e < o1; ++e) out[w++] = col_idx[e];
-  for (int e = i0; e < i1; ++e) out[w++] = in_idx[e];
+  for (int e = o0; e < o1; e += 4) {
+    int u[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+      if (e + k < o1) u[k] = col_idx[e + k];
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+      if (e + k < o1) out[w + k] = u[k];
+    w += min(4, o1 - e);
+  }
+  for (int e = i0; e < i1; e += 4) {
+    int u[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+      if (e + k < i1) u[k] = in_idx[e + k];
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+      if (e + k < i1) out[w + k] = u[k];
+    w += min(4, i1 - e);
+  }
 }
 
 __device__ __forceinline__ bool pair_less(uint64_t ka, int ua, uint64_t kb, int ub) {
@@ -286,10 +307,14 @@ __global__ __launch_bounds__(256) void k_nbr_heavy(const int* __restrict__ row_p
         key[r] = philox4x64_10((uint64_t)(v - g0), (uint64_t)(id[r] - g0), 1ull, 0ull, seed, 0ull).w[0];
       }
     }
-    // radix select: T = the fanout-th smallest key; need = how many key == T to take
+    // Radix select from the top bit.  The class is the keys whose bits above
+    // `bit` equal prefix's; it holds `cand` keys, and `need` of them are still
+    // to be taken (every key of a smaller class is taken).  Once cand == need
+    // the whole class is taken and the rest of the bits decide nothing.
     uint64_t prefix = 0;
-    int need = fanout;
-    for (int bit = 63; bit >= 0; --bit) {
+    int need = fanout, cand = deg;
+    int bit = 63;
+    for (; bit >= 0 && cand > need; --bit) {
       const uint64_t hi_mask = (bit == 63) ? 0ull : (~0ull << (bit + 1));
       int c0 = 0;
 #pragma unroll
@@ -302,23 +327,29 @@ __global__ __launch_bounds__(256) void k_nbr_heavy(const int* __restrict__ row_p
       if (need > c0) {
         prefix |= (1ull << bit);
         need -= c0;
+        cand -= c0;
+      } else {
+        cand = c0;
       }
     }
-    const uint64_t T = prefix;
-    // take every key < T, then the `need` smallest ids among key == T
+    const uint64_t cmask = (bit == 63) ? 0ull : (~0ull << (bit + 1));
+    const bool whole = cand == need;   // else: all 64 bits tie, decided by the smallest ids
+    // take every key of a smaller class (and, when whole, of the class itself)
     int base = 0;
     const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
 #pragma unroll
     for (int r = 0; r < kHeavyPerLane; ++r) {
       if (r >= R) break;
       const int e = lane + 64 * r;
-      const bool sel = e < deg && key[r] < T;
+      const uint64_t kc = key[r] & cmask;
+      const bool sel = e < deg && (kc < prefix || (whole && kc == prefix));
       const uint64_t bal = __ballot(sel);
       if (sel) out[base + __popcll(bal & lt_mask)] = id[r];
       base += __popcll(bal);
     }
+    const uint64_t T = prefix;
     int last = -1;   // ids strictly above `last` are still eligible
-    for (int t = 0; t < need; ++t) {
+    for (int t = 0; t < (whole ? 0 : need); ++t) {
       int best = 0x7fffffff;
 #pragma unroll
       for (int r = 0; r < kHeavyPerLane; ++r) {
