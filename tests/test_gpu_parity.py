@@ -78,6 +78,23 @@ def test_neighbors_bit_exact(name):
         assert np.array_equal(got, S[v]), v
 
 
+@pytest.mark.parametrize("sizes", [(65536,), (70000,), (40000, 30001)], ids=["n65536", "n70000", "n70001_two_graphs"])
+def test_neighbors_scan_paths(sizes):
+    """Graphs of 64 k nodes and more (the degree scan over 64+ blocks of 1,024,
+    one graph or two): S(v) and its offsets stay bit-exact."""
+    cfg = W.get_config("tiny_layered_256").replace(graph_sizes=sizes, fanout=4)
+    _log("neighbors, scan path", sizes)
+    g, w = W.make_graph(cfg), W.make_weights(cfg)
+    r = _runner(cfg, g, w)
+    s_ptr, s_idx = r.neighbors()
+    _sync()
+    s_ptr, s_idx = s_ptr.cpu().numpy(), s_idx.cpu().numpy()
+    S = O.sample_neighbours(O.neighbour_lists(g.row_ptr, g.col_idx), g.graph_ptr, cfg.fanout, cfg.nb_seed)
+    assert np.array_equal(s_ptr, np.concatenate([[0], np.cumsum([len(x) for x in S])]))
+    for v in range(g.n_nodes):
+        assert np.array_equal(np.sort(s_idx[s_ptr[v]:s_ptr[v + 1]]), S[v]), v
+
+
 def test_neighbors_heavy_sampling_and_order_invariance():
     cfg, g, w = workload("recurrent_12000")
     cfg = cfg.replace(fanout=2)
