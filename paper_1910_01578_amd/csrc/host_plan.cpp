@@ -187,7 +187,7 @@ void plan_sample(const gdp_graph* g, int32_t k, SamplePlan* p) {
   p->chunks = prefix_blocks_rows(g->graph_ptr_h, g->n_graphs, kSampleRows, blk);
   carve_init(&p->c);
   p->partial = carve_add(&p->c, (size_t)k * p->chunks * 4);
-  p->coef = carve_add(&p->c, (size_t)g->n_graphs * k * 4);
+  p->coef = carve_add(&p->c, (size_t)g->n_graphs * (k + 1) * 4);
 }
 
 }  // namespace gdp

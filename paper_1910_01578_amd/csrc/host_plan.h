@@ -52,7 +52,7 @@ constexpr int kHeadBwdRows = 128;   // rows per head-backward chunk
 struct SamplePlan {
   Carve c;
   size_t partial;
-  size_t coef;        // gdp_ppo_grad: G * K coefficients
+  size_t coef;        // gdp_ppo_grad: G * K coefficients, then their G per-graph sums
   int chunks;
 };
 void plan_embed(const gdp_graph* g, const gdp_gnn* gnn, EmbedPlan* p);

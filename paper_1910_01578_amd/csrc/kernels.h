@@ -186,7 +186,8 @@ hipError_t launch_debug_uniforms(uint64_t seed, int n, int K, int D, float* out,
 
 // ---- the update path's first step ---------------------------------------------
 // PPO's clipped surrogate per graph (loss [G]) and the gradient of the batch
-// loss with respect to the logits (dlogits [n, D]); coef: G * K floats of scratch.
+// loss with respect to the logits (dlogits [n, D]); coef: G * (K + 1) floats of
+// scratch (the coefficients, then each graph's sum of them).
 hipError_t launch_ppo(const float* logits, const float* lse, const int* placements, const float* logp,
                       const float* logp_old, const float* adv, float eps, const GraphTable& gt, int n, int D, int K,
                       float* coef, float* loss, float* dlogits, hipStream_t s);

@@ -8,8 +8,8 @@
 //             unclipped branch attains the min, 0 where the clipped constant does
 //   dL/dlogits[v, j] = sum_k c[g(v),k] 1[p_kv = j] - softmax(logits_v)_j sum_k c[g(v),k]
 //
-// Two kernels: one work-group per graph forms c and L_g (a fixed-order sum);
-// four lanes per node then walk its K placements.  Deterministic.
+// Two kernels: one work-group per graph forms c, L_g and sum_k c[g,k] (fixed-
+// order sums); four lanes per node then walk its K placements.  Deterministic.
 #include "device_common.h"
 #include "host_plan.h"
 #include "kernels.h"
@@ -19,9 +19,9 @@ namespace gdp {
 __global__ __launch_bounds__(256) void k_ppo_coef(const float* __restrict__ logp, const float* __restrict__ logp_old,
                                                   const float* __restrict__ adv, int G, int K, float eps,
                                                   float* __restrict__ coef, float* __restrict__ loss) {
-  __shared__ float red[256 / kWave];
+  __shared__ float red[256 / kWave], redc[256 / kWave];
   const int g = blockIdx.x;
-  float part = 0.f;
+  float part = 0.f, cpart = 0.f;
   for (int k = threadIdx.x; k < K; k += 256) {
     const size_t i = (size_t)g * K + k;
     const float r = expf(logp[i] - logp_old[i]);
@@ -29,17 +29,29 @@ __global__ __launch_bounds__(256) void k_ppo_coef(const float* __restrict__ logp
     const float un = r * a;
     const float cl = fminf(fmaxf(r, 1.0f - eps), 1.0f + eps) * a;
     part += fminf(un, cl);
-    coef[i] = un <= cl ? -un / ((float)K * (float)G) : 0.0f;
+    const float ck = un <= cl ? -un / ((float)K * (float)G) : 0.0f;
+    coef[i] = ck;
+    cpart += ck;
   }
   // work-group sum in a fixed order: each wave's butterfly, then the waves in index order
 #pragma unroll
-  for (int off = kWave / 2; off >= 1; off >>= 1) part += xor_shfl(part, off);
-  if ((threadIdx.x & (kWave - 1)) == 0) red[threadIdx.x / kWave] = part;
+  for (int off = kWave / 2; off >= 1; off >>= 1) {
+    part += xor_shfl(part, off);
+    cpart += xor_shfl(cpart, off);
+  }
+  if ((threadIdx.x & (kWave - 1)) == 0) {
+    red[threadIdx.x / kWave] = part;
+    redc[threadIdx.x / kWave] = cpart;
+  }
   __syncthreads();
   if (threadIdx.x == 0) {
-    float s = 0.f;
-    for (int w = 0; w < 256 / kWave; ++w) s += red[w];
+    float s = 0.f, sc = 0.f;
+    for (int w = 0; w < 256 / kWave; ++w) {
+      s += red[w];
+      sc += redc[w];
+    }
     loss[g] = -s / (float)K;
+    coef[(size_t)G * K + g] = sc;   // the graph's sum of coefficients
   }
 }
 
@@ -68,16 +80,9 @@ __global__ __launch_bounds__(256) void k_ppo_dlogits(const float* __restrict__ l
     for (int j = 0; j < D; ++j) s += expf(row[j] - m);
     lz = m + logf(s);
   }
+  const float csum = coef[(size_t)gt.n * K + g];   // sum_k c[g,k], formed with the coefficients
   // Loads past the end read the last element and are masked afterwards, so no
   // load sits behind a branch and each group of eight issues back to back.
-  float csum = 0.f;
-  for (int k0 = 0; k0 < K; k0 += 8) {
-    float cv[8];
-#pragma unroll
-    for (int u = 0; u < 8; ++u) cv[u] = c[min(k0 + u, K - 1)];
-#pragma unroll
-    for (int u = 0; u < 8; ++u) csum += k0 + u < K ? cv[u] : 0.0f;
-  }
   for (int jb = 0; jb < D; jb += 8) {
     float rv[8];
 #pragma unroll
