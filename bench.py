@@ -195,6 +195,28 @@ def main():
             ent.update({"achieved": rf["achieved"], "unit": rf["unit"], "frac": rf["frac"], "bound": rf["bound"]})
         kernels.append(ent)
 
+    # The same step captured once into a HIP graph and replayed K times (the
+    # library allocates nothing and records no memset, so a step can be
+    # captured): reported beside the eager figure, which is `value`.
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        runner.forward(seed)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        runner.forward(seed)
+    graph.replay()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        graph.replay()
+    torch.cuda.synchronize()
+    graph_s = (time.perf_counter() - t0) / args.steps
+    graph_replay = {"ms_per_step": round(1e3 * graph_s, 4), "value": round(g.n_nodes / graph_s, 1), "unit": "nodes/s"}
+    del graph
+
     # The update path's first step on the timed step's samples: PPO's clipped
     # surrogate and its logit gradient (HBM-bound: placements, logits, lse in,
     # the gradient out).
@@ -281,6 +303,7 @@ def main():
         "roofline": roofline,
         "cpu_baseline": cpu,
         "kernels": kernels,
+        "graph_replay": graph_replay,
         "ablation_no_attention": ablation,
         "ppo_grad": ppo,
         "head_backward": head_bwd,
