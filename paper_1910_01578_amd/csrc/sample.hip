@@ -102,8 +102,19 @@ __global__ __launch_bounds__(256) void k_logp_reduce(const float* __restrict__ p
   if (i >= ct.n * K) return;
   const int g = i / K, k = i % K;
   const float* p = partial + (size_t)k * total_chunks;
-  float acc = 0.f;
-  for (int c = ct.blk[g] + lane; c < ct.blk[g + 1]; c += 64) acc += p[c];
+  // lane l adds chunks c0 + l, c0 + l + 64, ... into four running sums; past
+  // the end a lane reloads the last chunk and adds nothing, so four loads are
+  // in flight with no branch between them
+  const int c0 = ct.blk[g], c1 = ct.blk[g + 1];
+  float a4[4] = {0.f, 0.f, 0.f, 0.f};
+  for (int c = c0 + lane; c < c1; c += 4 * 64) {
+    float v[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) v[e] = p[min(c + 64 * e, c1 - 1)];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) a4[e] += c + 64 * e < c1 ? v[e] : 0.f;
+  }
+  float acc = (a4[0] + a4[1]) + (a4[2] + a4[3]);
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) acc += xor_shfl(acc, off);
   if (lane == 0) logp[i] = acc;
