@@ -16,6 +16,10 @@
  *   gdp_embed   graph + features + GNN weights  -> node and graph embeddings
  *   gdp_place   embeddings + placer weights      -> device logits (+ lse)
  *   gdp_sample  logits + K + seed                -> K placements + log-probs
+ * and the first steps of the update path (Section 3, PPO) follow them:
+ *   gdp_ppo_grad       samples + old log-probs + advantages -> loss, dL/dlogits
+ *   gdp_place_train    gdp_place that also keeps the head's input X
+ *   gdp_head_backward  X + dL/dlogits -> dL/dX, dL/dW_out, dL/db_out
  *
  * Conventions shared by every call
  *  - Memory.  Every pointer documented "device" is HIP device memory owned by
