@@ -260,3 +260,24 @@ def test_one_hip_runtime_in_process():
             "print(len(paths))\n")
     out = subprocess.run([sys.executable, "-c", code], cwd=ROOT, check=True, capture_output=True, text=True)
     assert out.stdout.strip().split("\n")[-1] == "1", out.stdout
+
+
+def test_binding_fails_loudly_without_the_library(tmp_path):
+    """No fallback: loading the binding against a missing library raises, and
+    nothing under oracle/ is imported by the product package."""
+    import subprocess
+    import sys
+    code = ("import paper_1910_01578_amd.gdp as m\n"
+            f"m.LIB_PATH = {str(tmp_path / 'absent.so')!r}\n"
+            "try:\n"
+            "    m._load()\n"
+            "except ImportError as e:\n"
+            "    print('raised', 'no fallback' in str(e))\n")
+    r = subprocess.run([sys.executable, "-c", code], cwd=ROOT, capture_output=True, text=True, timeout=120)
+    assert r.stdout.strip().endswith("raised True"), r.stdout + r.stderr
+    pkg = os.path.join(ROOT, "paper_1910_01578_amd")
+    for dirpath, _, files in os.walk(pkg):
+        for f in files:
+            if f.endswith((".py", ".hip", ".cpp", ".h")):
+                text = open(os.path.join(dirpath, f), errors="replace").read()
+                assert "import oracle" not in text and "from oracle" not in text, f
