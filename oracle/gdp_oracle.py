@@ -386,6 +386,30 @@ def ppo_clipped_surrogate(logits, lse, graph_ptr, placements, logp, logp_old, ad
     return {"loss": loss, "coef": coef, "dlogits": dlogits}
 
 
+def rewards_advantages(run_time, valid, reward_sum, trial_count):
+    """Section 4's reward and advantage for measured run times t[g, k] of the
+    K placements of every graph: r = -sqrt(t) for a valid placement and -10
+    for an invalid one (out of memory, a broken co-location constraint); the
+    bias term is the average reward of all previous trials of the same graph,
+    and the advantage is r minus it.  Readings: the K trials of one batch are
+    not previous to each other, and a graph with no previous trial takes its
+    batch's own mean reward as the bias.  Returns the rewards, advantages and
+    bias terms, and the per-graph running state (sum of rewards, number of
+    trials) updated with this batch."""
+    t = np.asarray(run_time, np.float64)
+    G, K = t.shape
+    ok = np.ones((G, K), bool) if valid is None else np.asarray(valid, bool)
+    r = np.where(ok, -np.sqrt(np.where(ok, t, 0.0)), -10.0)
+    s = np.array(reward_sum, np.float64)
+    n = np.array(trial_count, np.int64)
+    base = np.empty(G)
+    for g in range(G):
+        base[g] = s[g] / n[g] if n[g] > 0 else r[g].mean()
+    adv = r - base[:, None]
+    return {"reward": r, "advantage": adv, "baseline": base, "reward_sum": s + r.sum(axis=1),
+            "trial_count": n + K}
+
+
 def head_backward(x, w_out, dlogits):
     """The head's backward pass (logits = x W_out^T + b_out): the gradients with
     respect to its input, weight and bias for a given dL/dlogits."""
