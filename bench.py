@@ -258,6 +258,23 @@ def main():
                 "frac": round(hb_bytes / (hb_us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4)}
     del x_keep, dl
 
+    # Section 4's reward and advantage of G x K measured run times (synthetic
+    # here), the advantages' producer: one small launch.
+    G, K = runner.logp.shape
+    rt = torch.from_numpy(rng.lognormal(mean=-1.0, sigma=0.3, size=(G, K)).astype(np.float32)).cuda()
+    baseline = gdp.RewardBaseline(G)
+    for _ in range(3):
+        baseline.advantages(rt)
+    torch.cuda.synchronize()
+    gdp.timer_begin(["advantages"])
+    for _ in range(args.steps):
+        baseline.advantages(rt)
+    torch.cuda.synchronize()
+    ar = gdp.timer_end()["advantages"]
+    adv_leg = {"us_per_call": round(1e3 * ar["ms"] / ar["launches"], 2), "values": G * K,
+               "note": "one work-group per graph; launch-bound at this size"}
+    del baseline
+
     # The ablation's placer without attention (Section 4.3) on the same DAG and
     # weights: the same embed and sample calls around one fused placer kernel.
     ab = gdp.Runner(gdp.DeviceGraph(g, cfg.dtype), gdp.DevicePolicy(cfg, w, attention=False), cfg.k_samples)
@@ -307,6 +324,7 @@ def main():
         "ablation_no_attention": ablation,
         "ppo_grad": ppo,
         "head_backward": head_bwd,
+        "advantages": adv_leg,
     }
     print(json.dumps(out), flush=True)
 

@@ -264,6 +264,28 @@ int gdp_head_backward(const gdp_graph* g, const gdp_placer* placer, const float*
                       float* dx, float* dw_out, float* db_out, void* workspace, size_t workspace_bytes,
                       void* stream);
 
+/*
+ * Reward and advantage (Section 4) of the K placements of each of G graphs
+ * from their measured run times, the input of gdp_ppo_grad's advantages:
+ *   reward[g, k]    = -sqrt(run_time[g, k]), or -10 where valid[g, k] == 0
+ *                     (an invalid placement: out of memory, a broken constraint)
+ *   advantage[g, k] = reward[g, k] - b[g],  b[g] = the average reward of all
+ *                     previous trials of graph g (reward_sum[g] / trial_count[g]),
+ *                     or this batch's mean for g when trial_count[g] == 0
+ * and then reward_sum[g] += sum_k reward[g, k], trial_count[g] += K.  The K
+ * trials of one call are not previous to each other.
+ *   run_time     device [G, K] fp32 (input, >= 0 where valid)
+ *   valid        device [G, K] uint8 (input, may be NULL: all valid)
+ *   reward_sum   device [G] fp64 (in/out: the running state, zero to start)
+ *   trial_count  device [G] int64 (in/out)
+ *   reward       device [G, K] fp32 (output, may be NULL)
+ *   advantage    device [G, K] fp32 (output)
+ * 1 <= n_graphs <= GDP_MAX_GRAPHS, k_samples >= 1.  No workspace.  Calls on one
+ * state must be ordered (same stream); deterministic.
+ */
+int gdp_advantages(int32_t n_graphs, int32_t k_samples, const float* run_time, const uint8_t* valid,
+                   double* reward_sum, int64_t* trial_count, float* reward, float* advantage, void* stream);
+
 int gdp_ppo_grad(const gdp_graph* g, const float* logits, const float* lse, int32_t n_devices,
                  int32_t k_samples, const int32_t* placements, const float* logp, const float* logp_old,
                  const float* advantages, float clip_eps, float* loss, float* dlogits, void* workspace,
@@ -323,6 +345,7 @@ typedef enum gdp_kernel_kind {
   GDP_K_MLP_PLACER,      /* the ablation's placer without attention, all layers */
   GDP_K_PPO,             /* PPO clipped surrogate and its logit gradient     */
   GDP_K_HEAD_BWD,        /* the head's backward pass                        */
+  GDP_K_ADVANTAGE,       /* reward and advantage of measured run times      */
   GDP_K_COUNT
 } gdp_kernel_kind;
 

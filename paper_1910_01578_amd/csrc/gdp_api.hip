@@ -399,6 +399,23 @@ extern "C" int gdp_head_backward(const gdp_graph* g, const gdp_placer* placer, c
   return GDP_OK;
 }
 
+extern "C" int gdp_advantages(int32_t n_graphs, int32_t k_samples, const float* run_time, const uint8_t* valid,
+                              double* reward_sum, int64_t* trial_count, float* reward, float* advantage,
+                              void* stream) {
+  clear_error();
+  if (n_graphs < 1 || n_graphs > GDP_MAX_GRAPHS)
+    return fail(GDP_E_UNSUPPORTED, "n_graphs = %d outside 1..%d", n_graphs, GDP_MAX_GRAPHS);
+  if (k_samples < 1) return fail(GDP_E_INVALID_ARG, "k_samples = %d < 1", k_samples);
+  if (!run_time || !reward_sum || !trial_count || !advantage)
+    return fail(GDP_E_INVALID_ARG, "run_time, reward_sum, trial_count or advantage is NULL");
+  int r;
+  if ((r = pending_hip_error()) != GDP_OK) return r;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  GDP_LAUNCH(GDP_K_ADVANTAGE, launch_advantages(run_time, valid, n_graphs, k_samples, reward_sum, trial_count, reward,
+                                                advantage, st));
+  return GDP_OK;
+}
+
 extern "C" int gdp_sample(const gdp_graph* g, const float* logits, const float* lse, int32_t n_devices,
                           int32_t k_samples, uint64_t seed, const float* uniforms, int32_t* placements, float* logp,
                           void* ws, size_t ws_bytes, void* stream) {
@@ -500,7 +517,7 @@ extern "C" const char* gdp_kernel_kind_name(int32_t kind) {
   static const char* names[GDP_K_COUNT] = {
       "graph_prep", "nbr_sample",    "gemm_pool_sigmoid", "gather_max", "gemm_update_relu",
       "meanpool",   "film",          "pre_layer",         "seg_attention", "post_attn",
-      "head_lse",   "gumbel_sample", "logp_reduce",       "mlp_placer", "ppo_grad",  "head_backward"};
+      "head_lse",   "gumbel_sample", "logp_reduce",       "mlp_placer", "ppo_grad",  "head_backward", "advantages"};
   if (kind < 0 || kind >= GDP_K_COUNT) return "";
   return names[kind];
 }

@@ -194,6 +194,10 @@ hipError_t launch_ppo(const float* logits, const float* lse, const int* placemen
 // The head's backward pass: dx [n, d] = dlogits W_out, dw_out [D, d] = dlogits^T x,
 // db_out [D] = column sums of dlogits; partial: ceil(n / kHeadBwdRows) * D * (d + 1)
 // floats of scratch.  d divides 256, D <= 64.
+// Section 4's reward and advantage per graph (one work-group each); the running
+// state reward_sum / trial_count [G] is read and updated.
+hipError_t launch_advantages(const float* run_time, const uint8_t* valid, int G, int K, double* reward_sum,
+                             int64_t* trial_count, float* reward, float* adv, hipStream_t s);
 template <typename T>
 hipError_t launch_head_backward(const float* x, const T* w_out, const float* dlogits, int n, int d, int D, float* dx,
                                 float* dw_out, float* db_out, float* partial, hipStream_t s);

@@ -335,3 +335,53 @@ template hipError_t launch_head_backward<bf16>(const float*, const bf16*, const 
                                                float*, float*, hipStream_t);
 
 }  // namespace gdp
+
+namespace gdp {
+
+// ---- Section 4: reward and advantage of measured run times ---------------------
+// One work-group per graph: r = -sqrt(t) (or -10 for an invalid placement);
+// the bias is the graph's running mean of all previous rewards (its batch
+// mean when there is none), and the batch then joins the running state.
+// The batch sum is taken in a fixed order (lanes, then waves in index order).
+__global__ __launch_bounds__(256) void k_advantages(const float* __restrict__ run_time,
+                                                    const uint8_t* __restrict__ valid, int K,
+                                                    double* __restrict__ reward_sum,
+                                                    int64_t* __restrict__ trial_count,
+                                                    float* __restrict__ reward, float* __restrict__ adv) {
+  __shared__ float red[256 / kWave];
+  __shared__ float s_base;
+  const int g = blockIdx.x;
+  auto reward_at = [&](size_t i) { return !valid || valid[i] ? -sqrtf(run_time[i]) : -10.0f; };
+  float part = 0.f;
+  for (int k = threadIdx.x; k < K; k += 256) part += reward_at((size_t)g * K + k);
+#pragma unroll
+  for (int off = kWave / 2; off >= 1; off >>= 1) part += xor_shfl(part, off);
+  if ((threadIdx.x & (kWave - 1)) == 0) red[threadIdx.x / kWave] = part;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    float s = 0.f;
+    for (int w = 0; w < 256 / kWave; ++w) s += red[w];
+    const int64_t n = trial_count[g];
+    const double prev = reward_sum[g];
+    s_base = n > 0 ? (float)(prev / (double)n) : s / (float)K;
+    reward_sum[g] = prev + (double)s;
+    trial_count[g] = n + K;
+  }
+  __syncthreads();
+  const float base = s_base;
+  for (int k = threadIdx.x; k < K; k += 256) {
+    const size_t i = (size_t)g * K + k;
+    const float r = reward_at(i);
+    if (reward) reward[i] = r;
+    adv[i] = r - base;
+  }
+}
+
+hipError_t launch_advantages(const float* run_time, const uint8_t* valid, int G, int K, double* reward_sum,
+                             int64_t* trial_count, float* reward, float* adv, hipStream_t s) {
+  hipLaunchKernelGGL(k_advantages, dim3(G), dim3(256), 0, s, run_time, valid, K, reward_sum, trial_count, reward,
+                     adv);
+  return hipGetLastError();
+}
+
+}  // namespace gdp

@@ -30,7 +30,7 @@ GDP_MAX_GRAPHS = 128
 
 KERNEL_KINDS = ["graph_prep", "nbr_sample", "gemm_pool_sigmoid", "gather_max", "gemm_update_relu",
                 "meanpool", "film", "pre_layer", "seg_attention", "post_attn",
-                "head_lse", "gumbel_sample", "logp_reduce", "mlp_placer", "ppo_grad", "head_backward"]
+                "head_lse", "gumbel_sample", "logp_reduce", "mlp_placer", "ppo_grad", "head_backward", "advantages"]
 K_COUNT = len(KERNEL_KINDS)
 
 
@@ -91,6 +91,8 @@ def _load():
         "gdp_validate_graph_host": (c_int32, [c_void_p, c_int32, c_void_p, c_int32, c_void_p, c_int64, c_uint32]),
         "gdp_last_error": (c_char_p, []),
         "gdp_abi_version": (c_int32, []),
+        "gdp_advantages": (c_int32, [c_int32, c_int32, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
+                                     c_void_p]),
         "gdp_place_train": (c_int32, [POINTER(GdpGraph), c_void_p, c_void_p, POINTER(GdpPlacer), c_void_p, c_void_p,
                                       c_void_p, c_void_p, c_size_t, c_void_p]),
         "gdp_head_backward": (c_int32, [POINTER(GdpGraph), POINTER(GdpPlacer), c_void_p, c_void_p, c_void_p, c_void_p,
@@ -296,6 +298,28 @@ class Runner:
                                       s_idx.data_ptr(), cap, self.ws.data_ptr(), self.ws_bytes,
                                       _stream_handle(stream)))
         return s_ptr, s_idx
+
+
+class RewardBaseline:
+    """Section 4's reward and advantage with the running average of previous
+    trials as the bias, one state per graph (device fp64 sums, int64 counts)."""
+
+    def __init__(self, n_graphs: int, device="cuda"):
+        torch = _torch()
+        self.reward_sum = torch.zeros(n_graphs, dtype=torch.float64, device=device)
+        self.trial_count = torch.zeros(n_graphs, dtype=torch.int64, device=device)
+
+    def advantages(self, run_time, valid=None, stream=None):
+        """run_time [G, K] fp32 (device), valid [G, K] uint8 or None; returns
+        (reward, advantage), both [G, K] fp32, and advances the state."""
+        torch = _torch()
+        G, K = run_time.shape
+        reward = torch.empty_like(run_time)
+        adv = torch.empty_like(run_time)
+        check(lib.gdp_advantages(G, K, run_time.data_ptr(), None if valid is None else valid.data_ptr(),
+                                 self.reward_sum.data_ptr(), self.trial_count.data_ptr(), reward.data_ptr(),
+                                 adv.data_ptr(), _stream_handle(stream)))
+        return reward, adv
 
 
 def debug_uniforms(seed: int, n: int, k: int, d: int, device="cuda", stream=None):

@@ -244,6 +244,18 @@ def test_place_train_and_head_backward_reject():
     assert hb() == gdp.GDP_E_UNSUPPORTED
 
 
+def test_advantages_reject():
+    dev = 0x100000
+    call = lambda G=2, K=4, rt=dev, st=dev, adv=dev: gdp.lib.gdp_advantages(G, K, rt, None, st, st, None, adv, None)
+    assert call(G=0) == gdp.GDP_E_UNSUPPORTED
+    assert call(G=129) == gdp.GDP_E_UNSUPPORTED
+    assert call(K=0) == gdp.GDP_E_INVALID_ARG
+    assert call(rt=None) == gdp.GDP_E_INVALID_ARG
+    assert call(st=None) == gdp.GDP_E_INVALID_ARG
+    assert call(adv=None) == gdp.GDP_E_INVALID_ARG
+    assert "NULL" in gdp.last_error()
+
+
 def test_timer_state_machine():
     assert gdp.lib.gdp_timer_begin(1) == gdp.GDP_OK
     assert gdp.lib.gdp_timer_begin(1) == gdp.GDP_E_INVALID_ARG

@@ -593,6 +593,33 @@ def test_head_backward_edges(label, over, attention, dtype):
 
 
 # ----------------------------------------------------------------------------
+# Section 4's reward and advantage over several batches of measured run times.
+@pytest.mark.parametrize("G,K,masked", [(3, 37, True), (2, 300, True), (128, 16, False)])
+def test_advantages_over_batches(G, K, masked):
+    import torch
+    from paper_1910_01578_amd import gdp
+    _log("advantages", G, K, masked)
+    rng = np.random.default_rng(17)
+    base = gdp.RewardBaseline(G)
+    s, n = np.zeros(G), np.zeros(G, np.int64)
+    for step in range(4):
+        t = rng.lognormal(mean=-1.0, sigma=0.5, size=(G, K)).astype(np.float32)
+        ok = (rng.random((G, K)) > 0.15) if masked else None
+        valid = None if ok is None else torch.from_numpy(ok.astype(np.uint8)).cuda()
+        reward, adv = base.advantages(torch.from_numpy(t).cuda(), valid)
+        _sync()
+        ref = O.rewards_advantages(t.astype(np.float64), ok, s, n)
+        scale = np.abs(ref["reward"]).max()
+        err_r = np.abs(reward.cpu().numpy() - ref["reward"]).max() / scale
+        err_a = np.abs(adv.cpu().numpy() - ref["advantage"]).max() / scale
+        assert err_r <= 1e-6 and err_a <= 1e-6, (step, err_r, err_a)
+        s, n = ref["reward_sum"], ref["trial_count"]
+        assert np.array_equal(base.trial_count.cpu().numpy(), n)
+        np.testing.assert_allclose(base.reward_sum.cpu().numpy(), s, rtol=1e-6, atol=0)
+    _log(f"  last batch: reward err {err_r:.2e}  advantage err {err_a:.2e}")
+
+
+# ----------------------------------------------------------------------------
 # The implementation's limits at once: GDP_MAX_GRAPHS graphs of ragged sizes
 # (1 to 59 nodes, many segments with partial tails and memory resets at every
 # graph start), fanout GDP_MAX_FANOUT with hub nodes above it, and
