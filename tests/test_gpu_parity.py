@@ -568,6 +568,65 @@ def _check_head_backward(cfg, g, w, attention=True, label=""):
     assert err_dx <= 1e-5 and err_dw <= 1e-5 and err_db <= 1e-5
 
 
+def test_update_path_directional_derivative():
+    """The update path end to end on the fp32 workload: one gradient step on
+    W_out and b_out along gdp_head_backward's dW_out, db_out (from
+    gdp_ppo_grad's dL/dlogits) changes the PPO loss, recomputed at the same
+    placements from the new logits: L(W - eta g) - L(W + eta g) = -2 eta |g|^2
+    up to third-order terms."""
+    import torch
+    cfg, g, w = workload("tiny_layered_256")
+    _log("update path: directional derivative")
+    r = _runner(cfg, g, w)
+    r.embed()
+    x = r.place_train()
+    r.sample(cfg.sample_seed)
+    _sync()
+    G, K = r.logp.shape
+    rng = np.random.default_rng(23)
+    lo = (r.logp.cpu().numpy() + rng.normal(scale=0.1, size=(G, K))).astype(np.float32)
+    adv = rng.normal(size=(G, K)).astype(np.float32)
+    eps = 0.2
+    loss0, dl = r.ppo_grad(torch.from_numpy(lo).cuda(), torch.from_numpy(adv).cuda(), eps)
+    _, dw, db = r.head_backward(x, dl)
+    _sync()
+    place = r.placements.cpu().numpy().astype(np.int64)
+    gp = g.graph_ptr
+
+    def batch_loss(logits):
+        lg = np.asarray(logits, np.float64)
+        ls = lg - np.log(np.exp(lg - lg.max(1, keepdims=True)).sum(1, keepdims=True)) - lg.max(1, keepdims=True)
+        tot = 0.0
+        for gi in range(G):
+            v = np.arange(gp[gi], gp[gi + 1])
+            logp = ls[v[None, :], place[:, v]].sum(axis=1)
+            ratio = np.exp(logp - lo[gi].astype(np.float64))
+            a = adv[gi].astype(np.float64)
+            tot += -np.minimum(ratio * a, np.clip(ratio, 1 - eps, 1 + eps) * a).mean()
+        return tot / G
+
+    L0 = batch_loss(to_np(r.logits))
+    assert abs(L0 - float(loss0.cpu().numpy().mean())) <= 1e-5 * max(1.0, abs(L0))
+    w_out, b_out = r.policy.head_t["w_out"], r.policy.head_t["b_out"]
+    gw, gb = dw.to(w_out.dtype), db.to(b_out.dtype)
+    sq = float((dw.double() ** 2).sum() + (db.double() ** 2).sum())
+    eta = 1e-4 / max(np.sqrt(sq), 1e-12)
+    w0, b0 = w_out.clone(), b_out.clone()
+    losses = []
+    for sign in (-1.0, 1.0):                 # W -/+ eta grad: a central difference
+        w_out.copy_(w0 + sign * eta * gw)
+        b_out.copy_(b0 + sign * eta * gb)
+        r.place()
+        _sync()
+        losses.append(batch_loss(to_np(r.logits)))
+    w_out.copy_(w0)
+    b_out.copy_(b0)
+    change, pred = losses[0] - losses[1], -2.0 * eta * sq
+    _log(f"  loss change {change:.4e}, first-order prediction {pred:.4e}")
+    assert losses[0] < L0 < losses[1]
+    assert abs(change - pred) <= 0.02 * abs(pred)
+
+
 @pytest.mark.parametrize("name", ALL)
 def test_head_backward_parity(name):
     cfg, g, w = workload(name)
