@@ -21,8 +21,22 @@ __global__ __launch_bounds__(256) void k_film_gemv(FilmLayers<T> w, int n_layers
   const int which = (rem / d) & 1;
   const int c = rem % d;
   const T* wr = (which ? w.wb[l] : w.wg[l]) + (size_t)c * H;
+  // four weight / input pairs per lane requested before any is used (indices
+  // past H reload the last element and add nothing), summed in k order
+  const float* xg = x0 + (size_t)g * H;
   float acc = 0.f;
-  for (int k = lane; k < H; k += 64) acc += to_f32(wr[k]) * x0[(size_t)g * H + k];
+  for (int k0 = lane; k0 < H; k0 += 4 * 64) {
+    float wv[4], xv[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int k = min(k0 + 64 * u, H - 1);
+      wv[u] = to_f32(wr[k]);
+      xv[u] = xg[k];
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      if (k0 + 64 * u < H) acc += wv[u] * xv[u];
+  }
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) acc += xor_shfl(acc, off);
   if (lane == 0) {
