@@ -275,7 +275,7 @@ def main():
                "note": "one work-group per graph; launch-bound at this size"}
     del baseline
 
-    # The ablation's placer without attention (Section 4.3) on the same DAG and
+    # The ablation's placer without attention (Section 4.4) on the same DAG and
     # weights: the same embed and sample calls around one fused placer kernel.
     ab = gdp.Runner(gdp.DeviceGraph(g, cfg.dtype), gdp.DevicePolicy(cfg, w, attention=False), cfg.k_samples)
     for _ in range(max(1, args.warmup)):
@@ -297,7 +297,7 @@ def main():
         if rf:
             ent.update({"achieved": rf["achieved"], "unit": rf["unit"], "frac": rf["frac"], "bound": rf["bound"]})
         ab_kernels.append(ent)
-    ablation = {"placer": "no attention (Section 4.3 ablation), all layers in one kernel",
+    ablation = {"placer": "no attention (Section 4.4 ablation), all layers in one kernel",
                 "value": round(g.n_nodes * args.steps / ab_elapsed, 1), "unit": "nodes/s",
                 "ms_per_step": round(1e3 * ab_elapsed / args.steps, 4), "kernels": ab_kernels}
     del ab

@@ -139,6 +139,8 @@ typedef struct gdp_gnn {
  * where MHA has no positional terms and no mask: the queries of a segment
  * [q0, q1) of graph g attend to the keys [max(g_start, q0 - mem_len), q1).
  * w_qkv stacks the Q, K and V projections; heads are contiguous column groups.
+ * w_qkv, b_qkv, w_o, w_1, b_1 and w_2 must be 16-byte aligned (checked before
+ * any launch: GDP_E_INVALID_ARG); the other vectors have no alignment rule.
  */
 typedef struct gdp_placer_layer {
   const void *film_wg, *film_bg;  /* [d, H], [d]  (ignored when film = 0)   */
@@ -153,7 +155,7 @@ typedef struct gdp_placer_layer {
 
 /*
  * attention = 0 selects the placement network of the paper's ablation
- * (Section 4.3) that has no attention: each layer is then
+ * (Section 4.4) that has no attention: each layer is then
  *   Y = FiLM_l(X),  X <- LN(Y + W_2 ReLU(W_1 Y + b_1) + b_2)   (LayerNorm ln2)
  * and w_qkv, b_qkv, w_o, b_o, ln1_g, ln1_b (may be NULL), n_heads, seg_len and
  * mem_len are not used; at most 16 layers.
@@ -219,28 +221,6 @@ int gdp_sample(const gdp_graph* g, const float* logits, const float* lse, int32_
                float* logp, void* workspace, size_t workspace_bytes, void* stream);
 
 /*
- * The first step of the policy update (Section 3: Eq. 1's objective, optimised
- * with PPO, Schulman et al. 2017): the clipped surrogate over the K sampled
- * placements of every graph and its gradient with respect to the logits.
- *   r[g, k]  = exp(logp[g, k] - logp_old[g, k])
- *   loss[g]  = -(1/K) sum_k min(r A[g, k], clip(r, 1 - clip_eps, 1 + clip_eps) A[g, k])
- *   dlogits  = d/d logits of (1/G) sum_g loss[g], through
- *              logp[g, k] = sum over v in g of (logits[v, p_kv] - lse[v])
- * The min takes the unclipped branch's slope where that branch attains it and
- * 0 where the clipped constant does.
- *   logits      device [N, D] fp32 (input, the ones the placements were drawn from)
- *   lse         device [N] fp32 (input, may be NULL: then recomputed)
- *   placements  device [K, N] int32 (input, from gdp_sample)
- *   logp        device [G, K] fp32 (input, from gdp_sample)
- *   logp_old    device [G, K] fp32 (input: the sampling policy's log-probs)
- *   advantages  device [G, K] fp32 (input)
- *   clip_eps    0 < clip_eps < 1
- *   loss        device [G] fp32 (output)
- *   dlogits     device [N, D] fp32 (output)
- * The workspace of gdp_workspace_bytes with the same k_samples suffices.
- * Deterministic (fixed summation orders).
- */
-/*
  * gdp_place that also writes the placement network's output X (the head's
  * input, the last layer's LN2 output), which the backward pass needs.
  *   x_out  device [N, d] fp32 (output, 16-byte aligned)
@@ -286,6 +266,28 @@ int gdp_head_backward(const gdp_graph* g, const gdp_placer* placer, const float*
 int gdp_advantages(int32_t n_graphs, int32_t k_samples, const float* run_time, const uint8_t* valid,
                    double* reward_sum, int64_t* trial_count, float* reward, float* advantage, void* stream);
 
+/*
+ * The first step of the policy update (Section 3: Eq. 1's objective, optimised
+ * with PPO, Schulman et al. 2017): the clipped surrogate over the K sampled
+ * placements of every graph and its gradient with respect to the logits.
+ *   r[g, k]  = exp(logp[g, k] - logp_old[g, k])
+ *   loss[g]  = -(1/K) sum_k min(r A[g, k], clip(r, 1 - clip_eps, 1 + clip_eps) A[g, k])
+ *   dlogits  = d/d logits of (1/G) sum_g loss[g], through
+ *              logp[g, k] = sum over v in g of (logits[v, p_kv] - lse[v])
+ * The min takes the unclipped branch's slope where that branch attains it and
+ * 0 where the clipped constant does.
+ *   logits      device [N, D] fp32 (input, the ones the placements were drawn from)
+ *   lse         device [N] fp32 (input, may be NULL: then recomputed)
+ *   placements  device [K, N] int32 (input, from gdp_sample)
+ *   logp        device [G, K] fp32 (input, from gdp_sample)
+ *   logp_old    device [G, K] fp32 (input: the sampling policy's log-probs)
+ *   advantages  device [G, K] fp32 (input)
+ *   clip_eps    0 < clip_eps < 1
+ *   loss        device [G] fp32 (output)
+ *   dlogits     device [N, D] fp32 (output)
+ * The workspace of gdp_workspace_bytes with the same k_samples suffices.
+ * Deterministic (fixed summation orders).
+ */
 int gdp_ppo_grad(const gdp_graph* g, const float* logits, const float* lse, int32_t n_devices,
                  int32_t k_samples, const int32_t* placements, const float* logp, const float* logp_old,
                  const float* advantages, float clip_eps, float* loss, float* dlogits, void* workspace,
@@ -355,7 +357,8 @@ typedef enum gdp_kernel_kind {
  * stream it is launched on.  gdp_timer_end synchronises those events and
  * writes, per kind, the summed elapsed milliseconds and the launch count
  * (arrays of GDP_K_COUNT entries; either may be NULL), then stops timing.
- * Process-wide state: not for concurrent use from several threads.
+ * The timer's state is per calling thread: only launches made by the thread
+ * that called gdp_timer_begin are timed, and that thread calls gdp_timer_end.
  */
 int gdp_timer_begin(uint32_t kind_mask);
 int gdp_timer_end(double* total_ms, int64_t* launches);

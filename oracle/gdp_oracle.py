@@ -255,7 +255,7 @@ def placer_band(node_emb, graph_ptr, gamma, beta, placer_layers, n_heads, seg_le
 
 
 # ----------------------------------------------------------------------------
-# Section 4.3 (ablation): the placement network with no attention.
+# Section 4.4 (ablation): the placement network with no attention.
 # ----------------------------------------------------------------------------
 
 def placer_no_attention(node_emb, graph_ptr, gamma, beta, placer_layers):

@@ -41,7 +41,8 @@ struct TimerState {
     return e;
   }
 };
-TimerState g_timer;
+// Per thread: launches of other threads are neither timed nor disturbed.
+thread_local TimerState g_timer;
 
 struct Timed {
   hipStream_t s;

@@ -28,6 +28,8 @@ size_t elem_size(int32_t dtype) { return dtype == GDP_BF16 ? 2 : 4; }
 
 static bool supported_width(int h) { return h == 64 || h == 128 || h == 256; }
 
+static bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
 int check_graph(const gdp_graph* g) {
   if (!g) return fail(GDP_E_INVALID_ARG, "graph is NULL");
   if (g->n_graphs < 1) return fail(GDP_E_INVALID_ARG, "n_graphs = %d < 1", g->n_graphs);
@@ -98,6 +100,10 @@ int check_placer(const gdp_graph* g, const gdp_placer* p) {
       return fail(GDP_E_INVALID_ARG, "placer layer %d has a NULL weight", l);
     if (p->film && (!L.film_wg || !L.film_bg || !L.film_wb || !L.film_bb))
       return fail(GDP_E_INVALID_ARG, "placer layer %d has a NULL FiLM weight", l);
+    // The layer kernels stage these matrices and vectors by 16-byte loads.
+    if (!aligned16(L.w_1) || !aligned16(L.b_1) || !aligned16(L.w_2) ||
+        (p->attention && (!aligned16(L.w_qkv) || !aligned16(L.b_qkv) || !aligned16(L.w_o))))
+      return fail(GDP_E_INVALID_ARG, "placer layer %d: w_qkv, b_qkv, w_o, w_1, b_1 and w_2 must be 16-byte aligned", l);
   }
   (void)g;
   return GDP_OK;

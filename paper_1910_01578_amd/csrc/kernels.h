@@ -114,7 +114,7 @@ struct PreLayerArgs {
 template <typename T>
 hipError_t launch_pre_layer(const PreLayerArgs<T>& a, const GraphTable& gt, hipStream_t s);
 
-// The ablation's placer without attention (Section 4.3), all layers and the
+// The ablation's placer without attention (Section 4.4), all layers and the
 // head in one kernel: X_0 = x; per layer Y = FiLM_l(X) (film: [L][2][G][d],
 // gamma then beta, or null), X <- LN2_l(Y + W_2 ReLU(W_1 Y + b_1) + b_2); then
 // logits = X W_out^T + b_out and lse when w_out is set (n_dev <= kFusedHeadDevices),

@@ -649,7 +649,7 @@ __device__ __forceinline__ void head_epilogue(const typename Geo<T, D>::RowAcc& 
           sum += expf(l[e] - mx);
           logits[(size_t)row * n_dev + e] = l[e];
         }
-      lse[row] = mx + logf(sum);
+      if (lse) lse[row] = mx + logf(sum);
     }
   }
 }
@@ -854,7 +854,7 @@ hipError_t launch_post_attention(const PostAttnArgs<T>& a, const GraphTable& gt,
   if (a.w_qkv && (!a.b_qkv || !a.qkv_out || a.ldq < 3 * a.d || a.ldq % EPV || !aligned_16(a.w_qkv) ||
                   !aligned_16(a.b_qkv) || !aligned_16(a.qkv_out)))
     return hipErrorInvalidValue;
-  if (a.w_out && (!a.b_out || !a.logits || !a.lse || a.n_dev < 1 || a.n_dev > kFusedHeadDevices || a.w_qkv))
+  if (a.w_out && (!a.b_out || !a.logits || a.n_dev < 1 || a.n_dev > kFusedHeadDevices || a.w_qkv))
     return hipErrorInvalidValue;
   if (a.film_gamma && (!a.film_beta || a.film_stride % 4 || !aligned_16(a.film_gamma) || !aligned_16(a.film_beta)))
     return hipErrorInvalidValue;
@@ -882,7 +882,7 @@ template hipError_t launch_post_attention<float>(const PostAttnArgs<float>&, con
 template hipError_t launch_post_attention<bf16>(const PostAttnArgs<bf16>&, const GraphTable&, hipStream_t);
 
 
-// The ablation's placement network without attention (Section 4.3): every
+// The ablation's placement network without attention (Section 4.4): every
 // layer is row-local, Y = FiLM_l(X), X <- LN2_l(Y + W_2 ReLU(W_1 Y + b_1) + b_2),
 // so one work-group runs all layers of its 128 rows with the activation in
 // its accumulators, and ends with the head.  Layer l's FFN chunk c uses the
@@ -945,7 +945,7 @@ hipError_t launch_mlp_placer(const MlpPlacerArgs<T>& a, const GraphTable& gt, hi
         !aligned_16(a.w2[l]) || !aligned_16(a.b1[l]))
       return hipErrorInvalidValue;
   if (a.film && (a.n_graphs < 1 || !aligned_16(a.film))) return hipErrorInvalidValue;
-  if (a.w_out && (!a.b_out || !a.logits || !a.lse || a.n_dev < 1 || a.n_dev > kFusedHeadDevices))
+  if (a.w_out && (!a.b_out || !a.logits || a.n_dev < 1 || a.n_dev > kFusedHeadDevices))
     return hipErrorInvalidValue;
   if (a.y_out && (a.ldyo % 4 || !aligned_16(a.y_out))) return hipErrorInvalidValue;
   if (!a.w_out && !a.y_out) return hipErrorInvalidValue;

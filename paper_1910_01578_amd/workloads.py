@@ -54,7 +54,7 @@ class Config:
     k_samples: int
     dtype: str                  # "f32" or "bf16"
     film: bool = True
-    attention: bool = True      # False: the ablation's placer without attention (Section 4.3)
+    attention: bool = True      # False: the ablation's placer without attention (Section 4.4)
 
     @property
     def n_nodes(self) -> int:

@@ -287,6 +287,11 @@ def _edge_graph(cfg, kind):
 # with bf16 activations a d = 64 model sits at the edge of the 2e-2 bar already
 # in an exact bf16-storage emulation, so it is checked in fp32 only.
 BF16_WIDTH = dict(hidden=128, heads=8, d_ff=512)
+# The edgeless 300-node graph is ill-conditioned under bf16 matrix-core
+# operands: an exact bf16-operand emulation of it already lands at 2.1e-2 end
+# to end, so for it bf16 is held to the bar stage by stage (embedding; placer
+# on the GPU's own embeddings).  Every other edge case is also held end to end.
+BF16_ILL_CONDITIONED = {"no_edges"}
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
@@ -320,15 +325,79 @@ def test_edge_cases(label, over, kind, dtype):
     err_p = rel_err_rows(logits, pg["logits"])
     _log(f"  node_emb err {err_h:.3e}  placer err {err_p:.3e}  end-to-end logits err {err_l:.3e}")
     assert err_h <= tol and err_p <= tol
-    if dtype == "f32":
-        # With bf16 matrix-core operands some of these small inputs are
-        # ill-conditioned end to end (an exact bf16-operand emulation of the
-        # edgeless graph already lands above 2e-2), so bf16 is held to the bar
-        # stage by stage and fp32 end to end.
+    if dtype == "f32" or label not in BF16_ILL_CONDITIONED:
         assert err_l <= tol
     ref = p if dtype == "f32" else pg
     check_placements(logits, ref["logits"], r.placements.cpu().numpy(), base.sample_seed, g.graph_ptr,
                      max_exempt=0.2)
+
+
+# ----------------------------------------------------------------------------
+# Every (dtype, width) pair the ABI accepts beyond the five workloads' own
+# (fp32 at 64, bf16 at 128 and 256): fp32 at d = 128 and 256, bf16 at d = 64.
+# 700 nodes span six 128-row blocks with a ragged tail.
+WIDTHS = [
+    ("f32_d128", "f32", dict(hidden=128, heads=8, d_ff=512, seg_len=96, mem_len=64)),
+    ("f32_d256", "f32", dict(hidden=256, heads=8, d_ff=1024, seg_len=128, mem_len=160)),
+    ("bf16_d64", "bf16", dict(hidden=64, heads=4, d_ff=256, seg_len=96, mem_len=64)),
+    ("bf16_d64_dh32", "bf16", dict(hidden=64, heads=2, d_ff=128, seg_len=64, mem_len=64)),
+]
+
+
+@pytest.mark.parametrize("attention", [True, False], ids=["attention", "no_attention"])
+@pytest.mark.parametrize("label,dtype,over", WIDTHS, ids=[x[0] for x in WIDTHS])
+def test_width_dtype_pairs(label, dtype, over, attention):
+    """Stage by stage and end to end: node and graph embeddings, the placer on the
+    GPU's own embeddings, end-to-end logits and placements."""
+    base = W.get_config("tiny_layered_256").replace(dtype=dtype, graph_sizes=(700,), attention=attention, **over)
+    _log("width", label, "attention" if attention else "no attention")
+    g, w = W.make_graph(base), W.make_weights(base)
+    r = _runner(base, g, w)
+    r.forward(base.sample_seed)
+    _sync()
+    gnn, pl, hd = w.f64()
+    e = O.embed(g.graph_ptr, g.row_ptr, g.col_idx, g.x, gnn, base.fanout, base.nb_seed)
+    kw = dict(film=base.film, attention=attention)
+    p = O.place(e["node_emb"], e["graph_emb"], g.graph_ptr, pl, hd["w_out"], hd["b_out"], base.heads,
+                base.seg_len, base.mem_len, **kw)
+    pg = O.place(to_np(r.node_emb), to_np(r.graph_emb), g.graph_ptr, pl, hd["w_out"], hd["b_out"], base.heads,
+                 base.seg_len, base.mem_len, **kw)
+    tol = TOL[dtype]
+    logits = to_np(r.logits)
+    err_h = rel_err_rows(to_np(r.node_emb), e["node_emb"])
+    err_x0 = rel_err_rows(to_np(r.graph_emb), e["graph_emb"])
+    err_p = rel_err_rows(logits, pg["logits"])
+    err_s = rel_err_rows(to_np(r.lse), pg["lse"])
+    err_l = rel_err_rows(logits, p["logits"])
+    _log(f"  node_emb {err_h:.3e}  graph_emb {err_x0:.3e}  placer {err_p:.3e}  lse {err_s:.3e}  end-to-end {err_l:.3e}")
+    assert err_h <= tol and err_x0 <= tol and err_p <= tol and err_s <= tol
+    assert err_l <= tol
+    check_placements(logits, p["logits"], r.placements.cpu().numpy(), base.sample_seed, g.graph_ptr)
+
+
+def test_place_lse_null_equals_with_lse():
+    """gdp_place with lse = NULL writes the same logits, bit for bit, with and
+    without attention (fused head, D <= 8) and with the head in its own kernel."""
+    import ctypes
+    import torch
+
+    from paper_1910_01578_amd import gdp
+    for attention, n_dev in ((True, 8), (False, 8), (True, 20)):
+        cfg = W.get_config("tiny_layered_256").replace(attention=attention, n_devices=n_dev)
+        g, w = W.make_graph(cfg), W.make_weights(cfg)
+        r = _runner(cfg, g, w)
+        r.embed()
+        r.place()
+        _sync()
+        with_lse = r.logits.clone()
+        r.logits.fill_(float("nan"))
+        _sync()
+        gdp.check(gdp.lib.gdp_place(ctypes.byref(r.graph.c), r.node_emb.data_ptr(), r.graph_emb.data_ptr(),
+                                    ctypes.byref(r.policy.placer), r.logits.data_ptr(), None, r.ws.data_ptr(),
+                                    r.ws_bytes, torch.cuda.current_stream().cuda_stream))
+        _sync()
+        _log("lse NULL", attention, n_dev)
+        assert _bits(r.logits) == _bits(with_lse)
 
 
 # ----------------------------------------------------------------------------
@@ -435,7 +504,7 @@ def test_attention_large_scores_bf16_uniform(sign):
 
 
 # ----------------------------------------------------------------------------
-# The ablation's placer without attention (Section 4.3): one fused kernel.
+# The ablation's placer without attention (Section 4.4): one fused kernel.
 def _place_no_attention(cfg, g, w):
     r = _runner(cfg.replace(attention=False), g, w)
     r.embed()

@@ -212,7 +212,7 @@ def test_i7_ragged_batch_equals_separate_graphs():
         np.testing.assert_allclose(full["logits"][sl], one["logits"], rtol=0, atol=1e-11)
 
 
-# ---- the ablation's placer without attention (Section 4.3) ---------------------
+# ---- the ablation's placer without attention (Section 4.4) ---------------------
 def _normalised_rows(rng, n, d, eps=1e-5):
     """Rows of zero mean and biased variance 1 - eps: LayerNorm with gain 1 and
     shift 0 maps them to themselves exactly."""
@@ -281,3 +281,80 @@ def test_no_attention_placer_is_row_local():
     p = O.place(x, rng.normal(size=(2, d)), gp, pl, hd["w_out"], hd["b_out"], c.heads, c.seg_len, c.mem_len,
                 attention=False)
     assert p["logits"].shape == (N, c.n_devices)
+
+
+# ---- Eq. 4's conditioning term c(x0): orientation and roles of W_gamma, W_beta --------
+def _film_layers(pl, rng):
+    """Placer layers with distinct, non-symmetric FiLM weights and biases."""
+    out = []
+    for lw in pl:
+        t = dict(lw)
+        d, H = lw["film_wg"].shape
+        t["film_wg"] = rng.normal(size=(d, H)) * 0.2
+        t["film_wb"] = rng.normal(size=(d, H)) * 0.2 + 0.05
+        t["film_bg"] = rng.normal(size=d) * 0.1
+        t["film_bb"] = rng.normal(size=d) * 0.1
+        assert not np.allclose(t["film_wg"], t["film_wg"].T)
+        assert not np.allclose(t["film_wg"], t["film_wb"])
+        out.append(t)
+    return out
+
+
+def test_film_unit_vector_closed_form():
+    """x0 = a * e_j selects column j of each matrix: gamma_i = 1 + a W_g[i, j] + b_g[i],
+    beta_i = a W_b[i, j] + b_b[i].  A transposed matrix would select row j instead and
+    swapped matrices would exchange scale and shift."""
+    c, pl, _ = _placer()
+    d = c.d_model
+    rng = np.random.default_rng(11)
+    fl = _film_layers(pl, rng)
+    for j in (0, 5, d - 1):
+        x0 = np.zeros((1, d))
+        x0[0, j] = 2.5
+        gamma, beta = O.film_params(x0, fl, film=True)
+        for l, lw in enumerate(fl):
+            for i in (0, 3, d - 2):
+                assert abs(gamma[0, l, i] - (1.0 + 2.5 * lw["film_wg"][i, j] + lw["film_bg"][i])) < 1e-14
+                assert abs(beta[0, l, i] - (2.5 * lw["film_wb"][i, j] + lw["film_bb"][i])) < 1e-14
+
+
+def test_film_conditioning_against_torch_linear():
+    """gamma = 1 + linear(x0, W_gamma, b_gamma), beta = linear(x0, W_beta, b_beta) for
+    non-zero x0 of several graphs, with distinct non-symmetric weights (fp64)."""
+    c, pl, _ = _placer()
+    d = c.d_model
+    rng = np.random.default_rng(12)
+    fl = _film_layers(pl, rng)
+    x0 = rng.normal(size=(3, d))
+    gamma, beta = O.film_params(x0, fl, film=True)
+    tx = torch.from_numpy(x0)
+    for l, lw in enumerate(fl):
+        g_ref = 1.0 + torch.nn.functional.linear(tx, torch.from_numpy(lw["film_wg"]),
+                                                 torch.from_numpy(lw["film_bg"])).numpy()
+        b_ref = torch.nn.functional.linear(tx, torch.from_numpy(lw["film_wb"]),
+                                           torch.from_numpy(lw["film_bb"])).numpy()
+        np.testing.assert_allclose(gamma[:, l], g_ref, rtol=0, atol=1e-12)
+        np.testing.assert_allclose(beta[:, l], b_ref, rtol=0, atol=1e-12)
+
+
+def test_t1_with_film_equals_torch_encoder_on_conditioned_input():
+    """One graph, one segment, FiLM on: each layer is torch's encoder layer applied to
+    gamma_l * x + beta_l with gamma_l, beta_l formed by torch from x0."""
+    c, pl, _ = _placer()
+    d = c.d_model
+    rng = np.random.default_rng(13)
+    fl = _film_layers(pl, rng)
+    N = 40
+    x = rng.normal(size=(N, d))
+    x0 = rng.normal(size=(1, d))
+    gamma, beta = O.film_params(x0, fl, film=True)
+    ours = O.placer_recurrent(x, np.array([0, N]), gamma, beta, fl, c.heads, seg_len=N, mem_len=0)
+    layers = _torch_stack(fl, d, c.heads, c.d_ff)
+    y = torch.from_numpy(x)[None]
+    tx0 = torch.from_numpy(x0)
+    with torch.no_grad():
+        for t, lw in zip(layers, fl):
+            g = 1.0 + torch.nn.functional.linear(tx0, torch.from_numpy(lw["film_wg"]), torch.from_numpy(lw["film_bg"]))
+            b = torch.nn.functional.linear(tx0, torch.from_numpy(lw["film_wb"]), torch.from_numpy(lw["film_bb"]))
+            y = t(g[:, None, :] * y + b[:, None, :])
+    np.testing.assert_allclose(ours, y[0].numpy(), rtol=0, atol=1e-10)
