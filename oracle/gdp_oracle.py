@@ -416,3 +416,58 @@ def head_backward(x, w_out, dlogits):
     x = np.asarray(x, np.float64)
     dl = np.asarray(dlogits, np.float64)
     return {"dx": dl @ np.asarray(w_out, np.float64), "dw_out": dl.T @ x, "db_out": dl.sum(axis=0)}
+
+
+# ----------------------------------------------------------------------------
+# Section 4.1 (a placement's run time and its validity) and Section 2 (graph
+# placement "with and without simulation"): a simulated step time of each
+# sampled placement, the input of the reward.  The paper measures run times
+# on hardware and defines no simulator; this is the reading used here.
+# ----------------------------------------------------------------------------
+
+def simulate_placements(graph_ptr, row_ptr, col_idx, placements, n_devices, op_cost, out_xfer, op_mem, mem_cap):
+    """In-order list scheduling of every graph under each of the K placements.
+
+    Every device runs its ops one at a time in node-id order (a topological
+    order).  Op v may start once its device has finished the device's previous
+    op and every input has arrived: the output of a predecessor u is available
+    on u's own device when u finishes and on any other device out_xfer[u] later
+    (transfers overlap with compute and with each other).  Then
+        ready(v)  = max over predecessors u of finish(u) + (p_u != p_v) * out_xfer[u]   (0 without one)
+        start(v)  = max(ready(v), free[p_v]),  finish(v) = start(v) + op_cost[v],  free[p_v] = finish(v)
+    and the graph's run time is its largest finish time.  A placement is valid
+    when every device holds at most mem_cap[g] of memory, the sum of op_mem over
+    the ops placed on it (out of memory makes it invalid).  All arithmetic is on
+    Python / numpy integers, so results are exact.
+
+    Returns makespan [G, K] int64, valid [G, K] bool and device_mem [G, K, D]."""
+    placements = np.asarray(placements, np.int64)
+    K, N = placements.shape
+    G = len(graph_ptr) - 1
+    cost = np.asarray(op_cost, np.int64)
+    xfer = np.asarray(out_xfer, np.int64)
+    mem = np.asarray(op_mem, np.int64)
+    pred: List[List[int]] = [[] for _ in range(N)]
+    for u in range(N):
+        for v in col_idx[row_ptr[u]:row_ptr[u + 1]]:
+            pred[int(v)].append(u)
+    makespan = np.zeros((G, K), np.int64)
+    device_mem = np.zeros((G, K, n_devices), np.int64)
+    ks = np.arange(K)
+    for g in range(G):
+        gs, ge = int(graph_ptr[g]), int(graph_ptr[g + 1])
+        finish = np.zeros((ge - gs, K), np.int64)
+        free = np.zeros((K, n_devices), np.int64)
+        for v in range(gs, ge):
+            pv = placements[:, v]
+            ready = np.zeros(K, np.int64)
+            for u in pred[v]:
+                arrive = finish[u - gs] + np.where(placements[:, u] != pv, xfer[u], 0)
+                ready = np.maximum(ready, arrive)
+            start = np.maximum(ready, free[ks, pv])
+            finish[v - gs] = start + cost[v]
+            free[ks, pv] = finish[v - gs]
+            device_mem[g, ks, pv] += mem[v]
+        makespan[g] = finish.max(axis=0)
+    valid = (device_mem <= np.asarray(mem_cap, np.int64)[:, None, None]).all(axis=2)
+    return {"makespan": makespan, "valid": valid, "device_mem": device_mem}

@@ -425,6 +425,37 @@ def prefix_graph(g: Graph, n: int) -> Graph:
 
 
 # ----------------------------------------------------------------------------
+# Per-op costs for the simulated run time of a placement (inputs only).
+# ----------------------------------------------------------------------------
+
+@dataclass
+class OpCosts:
+    """Integer inputs of the list-scheduling evaluator: per-op compute time,
+    time to ship the op's output to another device and memory held on the op's
+    device (time in microseconds, memory in KiB), and each graph's per-device
+    memory capacity."""
+    op_cost: np.ndarray    # [N] int32
+    out_xfer: np.ndarray   # [N] int32
+    op_mem: np.ndarray     # [N] int32
+    mem_cap: np.ndarray    # [G] int64
+
+
+def make_costs(cfg: Config, g: "Graph", mem_slack: float = 1.3) -> OpCosts:
+    """Costs read off each op's first three log-normal size features (the
+    output-shape meta features of Section 3.1), so larger tensors cost more to
+    compute, move and hold; a device holds mem_slack times an even share of its
+    graph's memory."""
+    s = g.x[:, cfg.n_types:cfg.n_types + 3]
+    op_cost = np.clip(1 + np.floor(20.0 * s[:, 0]), 1, 5000).astype(np.int32)
+    out_xfer = np.clip(np.floor(10.0 * s[:, 1]), 0, 5000).astype(np.int32)
+    op_mem = np.clip(1 + np.floor(100.0 * s[:, 2]), 1, 100000).astype(np.int32)
+    gp = g.graph_ptr
+    cap = np.array([int(np.ceil(mem_slack * int(op_mem[gp[i]:gp[i + 1]].astype(np.int64).sum()) / cfg.n_devices))
+                    for i in range(len(gp) - 1)], np.int64)
+    return OpCosts(op_cost, out_xfer, op_mem, cap)
+
+
+# ----------------------------------------------------------------------------
 # Weights.
 # ----------------------------------------------------------------------------
 
