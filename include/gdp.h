@@ -267,6 +267,23 @@ int gdp_advantages(int32_t n_graphs, int32_t k_samples, const float* run_time, c
                    double* reward_sum, int64_t* trial_count, float* reward, float* advantage, void* stream);
 
 /*
+ * gdp_sample without a workspace, for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc).  Same arguments, kernels and results as gdp_sample (bit
+ * for bit); the per-(sample, 256-node chunk) partial log-prob sums live in a
+ * library-owned device array of GDP_NOALLOC_SCRATCH_BYTES per GPU, held until
+ * the process ends.  K * (sum over graphs of ceil(nodes / 256)) * 4 bytes must
+ * fit in it, else GDP_E_UNSUPPORTED and nothing is enqueued.  The call
+ * allocates nothing.  Calls on one GPU share its array: calls that overlap in
+ * time on that GPU (different streams, or different threads without ordering)
+ * race and give undefined log-probs; calls ordered on one stream are safe.
+ */
+#define GDP_NOALLOC_SCRATCH_BYTES (4u << 20)
+int gdp_sample_noalloc(const gdp_graph* g, const float* logits, const float* lse, int32_t n_devices,
+                       int32_t k_samples, uint64_t seed, const float* uniforms, int32_t* placements,
+                       float* logp, void* stream);
+
+/*
  * The first step of the policy update (Section 3: Eq. 1's objective, optimised
  * with PPO, Schulman et al. 2017): the clipped surrogate over the K sampled
  * placements of every graph and its gradient with respect to the logits.

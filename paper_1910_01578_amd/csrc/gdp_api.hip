@@ -4,6 +4,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <mutex>
 #include <vector>
 
 #include "device_common.h"
@@ -433,6 +434,64 @@ extern "C" int gdp_sample(const gdp_graph* g, const float* logits, const float* 
   GraphTable ct = make_table(g);
   const int chunks = prefix_blocks_rows(g->graph_ptr_h, g->n_graphs, kSampleRows, ct.blk);
   float* partial = at<float>(ws, pl.partial);
+  GDP_LAUNCH(GDP_K_SAMPLE, launch_sample(logits, lse, g->n_nodes, n_devices, k_samples, seed, uniforms, ct, chunks,
+                                         placements, partial, st));
+  GDP_LAUNCH(GDP_K_LOGP_REDUCE, launch_logp_reduce(partial, ct, chunks, k_samples, logp, st));
+  return GDP_OK;
+}
+
+// ---------------------------------------------------------------------------
+// gdp_sample_noalloc: gdp_sample's kernels with their per-(k, chunk) partial
+// sums in a library-owned device array instead of the caller's workspace.
+// The array is a file-scope __device__ symbol: each GPU holds its own copy,
+// whose device address is looked up once per device (the first call made
+// with that device current) and used from then on.  The symbol's name in host
+// code is not a device address and is never passed to a kernel or copy.
+// ---------------------------------------------------------------------------
+static __device__ __align__(256) float scratch[GDP_NOALLOC_SCRATCH_BYTES / sizeof(float)];
+
+namespace {
+constexpr int kMaxScratchDevices = 64;
+std::mutex g_scratch_mu;
+float* g_scratch_ptr[kMaxScratchDevices] = {};
+}  // namespace
+
+static int scratch_for_current_device(float** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev < 0 || dev >= kMaxScratchDevices)
+    return fail(GDP_E_UNSUPPORTED, "device %d beyond the %d devices the scratch table holds", dev, kMaxScratchDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+    if (!p) return fail(GDP_E_HIP, "hipGetSymbolAddress(scratch) returned NULL");
+    g_scratch_ptr[dev] = static_cast<float*>(p);
+  }
+  *out = g_scratch_ptr[dev];
+  return GDP_OK;
+}
+
+extern "C" int gdp_sample_noalloc(const gdp_graph* g, const float* logits, const float* lse, int32_t n_devices,
+                                  int32_t k_samples, uint64_t seed, const float* uniforms, int32_t* placements,
+                                  float* logp, void* stream) {
+  clear_error();
+  int r;
+  if ((r = check_graph(g)) != GDP_OK) return r;
+  if ((r = check_sample(g, n_devices, k_samples)) != GDP_OK) return r;
+  if (!logits || !placements || !logp) return fail(GDP_E_INVALID_ARG, "logits, placements or logp is NULL");
+  GraphTable ct = make_table(g);
+  const int chunks = prefix_blocks_rows(g->graph_ptr_h, g->n_graphs, kSampleRows, ct.blk);
+  const size_t need = (size_t)k_samples * (size_t)chunks * sizeof(float);
+  if (need > GDP_NOALLOC_SCRATCH_BYTES)
+    return fail(GDP_E_UNSUPPORTED, "K * ceil(nodes / 256) partial sums need %zu bytes > GDP_NOALLOC_SCRATCH_BYTES = %zu",
+                need, (size_t)GDP_NOALLOC_SCRATCH_BYTES);
+  float* partial = nullptr;
+  if ((r = scratch_for_current_device(&partial)) != GDP_OK) return r;
+  if ((r = pending_hip_error()) != GDP_OK) return r;
+  hipStream_t st = static_cast<hipStream_t>(stream);
   GDP_LAUNCH(GDP_K_SAMPLE, launch_sample(logits, lse, g->n_nodes, n_devices, k_samples, seed, uniforms, ct, chunks,
                                          placements, partial, st));
   GDP_LAUNCH(GDP_K_LOGP_REDUCE, launch_logp_reduce(partial, ct, chunks, k_samples, logp, st));

@@ -27,6 +27,7 @@ GDP_F32 = 0
 GDP_BF16 = 1
 GDP_TOPO_IDS = 1
 GDP_MAX_GRAPHS = 128
+GDP_NOALLOC_SCRATCH_BYTES = 4 << 20
 
 KERNEL_KINDS = ["graph_prep", "nbr_sample", "gemm_pool_sigmoid", "gather_max", "gemm_update_relu",
                 "meanpool", "film", "pre_layer", "seg_attention", "post_attn",
@@ -88,6 +89,8 @@ def _load():
                                 c_void_p, c_size_t, c_void_p]),
         "gdp_sample": (c_int32, [POINTER(GdpGraph), c_void_p, c_void_p, c_int32, c_int32, c_uint64, c_void_p,
                                  c_void_p, c_void_p, c_void_p, c_size_t, c_void_p]),
+        "gdp_sample_noalloc": (c_int32, [POINTER(GdpGraph), c_void_p, c_void_p, c_int32, c_int32, c_uint64,
+                                         c_void_p, c_void_p, c_void_p, c_void_p]),
         "gdp_validate_graph_host": (c_int32, [c_void_p, c_int32, c_void_p, c_int32, c_void_p, c_int64, c_uint32]),
         "gdp_last_error": (c_char_p, []),
         "gdp_abi_version": (c_int32, []),
@@ -267,6 +270,18 @@ class Runner:
                              self.lse.data_ptr() if use_lse else None, self.policy.cfg.n_devices, self.k, seed,
                              None if uniforms is None else uniforms.data_ptr(), self.placements.data_ptr(),
                              self.logp.data_ptr(), self.ws.data_ptr(), self.ws_bytes, _stream_handle(stream)))
+
+    def sample_noalloc(self, seed: int, placements=None, logp=None, uniforms=None, use_lse: bool = True,
+                       stream=None):
+        """sample() through gdp_sample_noalloc (no workspace: the library's own
+        per-device scratch array); writes into the given or the runner's outputs."""
+        placements = self.placements if placements is None else placements
+        logp = self.logp if logp is None else logp
+        check(lib.gdp_sample_noalloc(ctypes.byref(self.graph.c), self.logits.data_ptr(),
+                                     self.lse.data_ptr() if use_lse else None, self.policy.cfg.n_devices,
+                                     int(placements.shape[0]), seed,
+                                     None if uniforms is None else uniforms.data_ptr(), placements.data_ptr(),
+                                     logp.data_ptr(), _stream_handle(stream)))
 
     def forward(self, seed: int, stream=None):
         """One pass of the hot path: embed -> place -> sample."""

@@ -212,6 +212,22 @@ def test_sample_rejects(D, K, code):
     assert r == gdp.GDP_E_INVALID_ARG
 
 
+def test_sample_noalloc_rejects_before_any_gpu_call():
+    """Argument errors and a problem beyond the fixed scratch array return before
+    the library touches the GPU (this host has none)."""
+    cfg, gp, g, gl, gnn, pl, placer = _descs()
+    dev = 0x100000
+    assert gdp.lib.gdp_sample_noalloc(ctypes.byref(g), dev, None, 1, 4, 1, None, dev, dev, None) == gdp.GDP_E_UNSUPPORTED
+    assert gdp.lib.gdp_sample_noalloc(ctypes.byref(g), dev, None, 8, 0, 1, None, dev, dev, None) == gdp.GDP_E_INVALID_ARG
+    assert gdp.lib.gdp_sample_noalloc(ctypes.byref(g), dev, None, 8, 4, 1, None, dev, None, None) == gdp.GDP_E_INVALID_ARG
+    cfg, gp, g, gl, gnn, pl, placer = _descs(graph_sizes=(4_000_000,))
+    chunks = sum((int(gp[i + 1]) - int(gp[i]) + 255) // 256 for i in range(len(gp) - 1))
+    k_over = gdp.GDP_NOALLOC_SCRATCH_BYTES // 4 // chunks + 1
+    assert k_over <= 65535
+    r = gdp.lib.gdp_sample_noalloc(ctypes.byref(g), dev, None, 8, k_over, 1, None, dev, dev, None)
+    assert r == gdp.GDP_E_UNSUPPORTED and "GDP_NOALLOC_SCRATCH_BYTES" in gdp.last_error()
+
+
 def test_ppo_grad_rejects():
     cfg, gp, g, gl, gnn, pl, placer = _descs()
     dev = 0x100000
