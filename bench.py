@@ -275,6 +275,25 @@ def main():
                "note": "one work-group per graph; launch-bound at this size"}
     del baseline
 
+    # The simulated run time of the timed step's K placements (in-order list
+    # scheduling with transfer costs, the memory check): latency-bound, one
+    # wavefront per graph and block of 64 samples walks the nodes in order.
+    costs = W.make_costs(cfg, g)
+    ev = gdp.Evaluator(runner.graph, cfg.n_devices, cfg.k_samples, costs)
+    for _ in range(2):
+        ev.evaluate(runner.placements)
+    torch.cuda.synchronize()
+    gdp.timer_begin(["evaluate"])
+    for _ in range(args.steps):
+        ev.evaluate(runner.placements)
+    torch.cuda.synchronize()
+    evr = gdp.timer_end()["evaluate"]
+    valid_frac = float(ev.valid.float().mean().item())
+    evaluate_leg = {"us_per_call": round(1e3 * evr["ms"] / args.steps, 2), "placements": cfg.k_samples,
+                    "nodes": g.n_nodes, "valid_fraction": round(valid_frac, 4),
+                    "ns_per_node": round(1e6 * evr["ms"] / args.steps / g.n_nodes, 2)}
+    del ev
+
     # The ablation's placer without attention (Section 4.4) on the same DAG and
     # weights: the same embed and sample calls around one fused placer kernel.
     ab = gdp.Runner(gdp.DeviceGraph(g, cfg.dtype), gdp.DevicePolicy(cfg, w, attention=False), cfg.k_samples)
@@ -325,6 +344,7 @@ def main():
         "ppo_grad": ppo,
         "head_backward": head_bwd,
         "advantages": adv_leg,
+        "evaluate": evaluate_leg,
     }
     print(json.dumps(out), flush=True)
 

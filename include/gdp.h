@@ -305,6 +305,41 @@ int gdp_sample_noalloc(const gdp_graph* g, const float* logits, const float* lse
  * The workspace of gdp_workspace_bytes with the same k_samples suffices.
  * Deterministic (fixed summation orders).
  */
+/*
+ * Simulated run time and validity of every sampled placement (Section 4.1:
+ * a placement is scored by the training step time it yields, and a placement
+ * that runs out of memory is invalid; Section 2: placement with and without
+ * simulation).  The paper measures on hardware; this call is an in-order list
+ * scheduler: every device runs its ops one at a time in node-id order, and op v
+ * on device p starts once p has finished its previous op and every input has
+ * arrived, where the output of a predecessor u reaches another device
+ * out_xfer[u] after u finishes (transfers overlap with compute and with each
+ * other):
+ *   finish(v)        = max(free[p], max_u finish(u) + [p_u != p] out_xfer[u]) + op_cost[v]
+ *   makespan[g, k]   = the largest finish time of graph g under placement k
+ *   valid[g, k]      = 1 if every device holds at most mem_cap_h[g] of op_mem
+ *   run_time[g, k]   = (float)(makespan[g, k] * time_unit), the input of gdp_advantages
+ * Integer arithmetic throughout, so results are exact and deterministic.
+ *   placements  device [K, N] int32 in [0, n_devices) (input, from gdp_sample)
+ *   op_cost     device [N] int32 >= 0 (compute time of each op)
+ *   out_xfer    device [N] int32 >= 0 (time to move the op's output to another device)
+ *   op_mem      device [N] int32 >= 0 (memory the op holds on its device)
+ *   mem_cap_h   host [G] int64 >= 0 (per-device capacity of each graph)
+ *   time_unit   >= 0, seconds per time unit (scales run_time only)
+ *   makespan    device [G, K] int64 (output, 8-byte aligned); -1 where the
+ *               graph's times leave 32 bits (sum of op_cost and out_xfer
+ *               over a graph below 2^32 rules this out)
+ *   valid       device [G, K] uint8 (output)
+ *   run_time    device [G, K] fp32 (output, may be NULL)
+ * The CSR must be valid (gdp_validate_graph_host); its device arrays are not
+ * read on the host.  Workspace: gdp_evaluate_workspace_bytes(g, n_devices, K).
+ */
+size_t gdp_evaluate_workspace_bytes(const gdp_graph* g, int32_t n_devices, int32_t k_samples);
+int gdp_evaluate(const gdp_graph* g, int32_t n_devices, int32_t k_samples, const int32_t* placements,
+                 const int32_t* op_cost, const int32_t* out_xfer, const int32_t* op_mem, const int64_t* mem_cap_h,
+                 double time_unit, int64_t* makespan, uint8_t* valid, float* run_time, void* workspace,
+                 size_t workspace_bytes, void* stream);
+
 int gdp_ppo_grad(const gdp_graph* g, const float* logits, const float* lse, int32_t n_devices,
                  int32_t k_samples, const int32_t* placements, const float* logp, const float* logp_old,
                  const float* advantages, float clip_eps, float* loss, float* dlogits, void* workspace,
@@ -365,6 +400,7 @@ typedef enum gdp_kernel_kind {
   GDP_K_PPO,             /* PPO clipped surrogate and its logit gradient     */
   GDP_K_HEAD_BWD,        /* the head's backward pass                        */
   GDP_K_ADVANTAGE,       /* reward and advantage of measured run times      */
+  GDP_K_EVALUATE,        /* simulated run time and validity of placements   */
   GDP_K_COUNT
 } gdp_kernel_kind;
 

@@ -17,6 +17,7 @@ namespace gdp {
 static_assert(kPoolRows == kMeanpoolRows, "mean-pool chunk size");
 static_assert(kAttnQ == kAttnBlockQ, "attention query block");
 static_assert(kSampleRows == kSampleChunk, "sampling chunk");
+static_assert(kEvalRows == kEvalChunk, "evaluator memory chunk");
 
 // ---------------------------------------------------------------------------
 // Event timer (diagnostics): an event pair around every launch of a selected
@@ -520,6 +521,78 @@ extern "C" int gdp_ppo_grad(const gdp_graph* g, const float* logits, const float
   return GDP_OK;
 }
 
+// ---------------------------------------------------------------------------
+// gdp_evaluate: the simulated run time and validity of every sampled placement.
+// ---------------------------------------------------------------------------
+extern "C" size_t gdp_evaluate_workspace_bytes(const gdp_graph* g, int32_t n_devices, int32_t k_samples) {
+  clear_error();
+  if (check_graph(g) != GDP_OK) return 0;
+  if (check_sample(g, n_devices, k_samples) != GDP_OK) return 0;
+  EvalPlan pl;
+  plan_evaluate(g, n_devices, k_samples, &pl);
+  return pl.c.total;
+}
+
+extern "C" int gdp_evaluate(const gdp_graph* g, int32_t n_devices, int32_t k_samples, const int32_t* placements,
+                            const int32_t* op_cost, const int32_t* out_xfer, const int32_t* op_mem,
+                            const int64_t* mem_cap_h, double time_unit, int64_t* makespan, uint8_t* valid,
+                            float* run_time, void* ws, size_t ws_bytes, void* stream) {
+  clear_error();
+  int r;
+  if ((r = check_graph(g)) != GDP_OK) return r;
+  if ((r = check_sample(g, n_devices, k_samples)) != GDP_OK) return r;
+  if (!placements || !op_cost || !out_xfer || !op_mem || !makespan || !valid)
+    return fail(GDP_E_INVALID_ARG, "an evaluator input or output is NULL");
+  if (!mem_cap_h) return fail(GDP_E_INVALID_ARG, "mem_cap_h is NULL");
+  for (int i = 0; i < g->n_graphs; ++i)
+    if (mem_cap_h[i] < 0) return fail(GDP_E_INVALID_ARG, "mem_cap_h[%d] = %lld < 0", i, (long long)mem_cap_h[i]);
+  if (!(time_unit >= 0.0) || time_unit > 1e30) return fail(GDP_E_INVALID_ARG, "time_unit = %g", time_unit);
+  if (((uintptr_t)makespan & 7u) != 0) return fail(GDP_E_INVALID_ARG, "makespan must be 8-byte aligned");
+  EvalPlan pl;
+  plan_evaluate(g, n_devices, k_samples, &pl);
+  if ((r = check_ws(ws, ws_bytes, pl.c.total)) != GDP_OK) return r;
+  if ((r = pending_hip_error()) != GDP_OK) return r;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const int N = g->n_nodes;
+  int* counters = at<int>(ws, pl.counters);
+  int* in_ptr = at<int>(ws, pl.in_ptr);
+  int* in_idx = at<int>(ws, pl.in_idx);
+  GDP_LAUNCH(GDP_K_EVALUATE, launch_fill_i32(counters, 2 * (int64_t)N + 1, 0, st));
+  GDP_LAUNCH(GDP_K_EVALUATE, launch_in_degree(g->col_idx, g->n_edges, counters, st));
+  GDP_LAUNCH(GDP_K_EVALUATE, launch_scan_degrees(g->row_ptr, counters, N, 1, in_ptr, at<int>(ws, pl.s_ptr),
+                                                 at<int>(ws, pl.scan_tmp), st));
+  GDP_LAUNCH(GDP_K_EVALUATE, launch_fill_reverse(g->row_ptr, g->col_idx, in_ptr, N, g->n_edges, counters + N, in_idx,
+                                                 st));
+  const GraphTable gt = make_table(g);
+  GraphTable ct = make_table(g);
+  const int chunks = prefix_blocks_rows(g->graph_ptr_h, g->n_graphs, kEvalRows, ct.blk);
+  EvalLaunch L;
+  L.placements = placements;
+  L.op_cost = op_cost;
+  L.out_xfer = out_xfer;
+  L.op_mem = op_mem;
+  L.mem_cap = mem_cap_h;
+  L.in_ptr = in_ptr;
+  L.in_idx = in_idx;
+  L.n_edges = g->n_edges;
+  L.gt = &gt;
+  L.chunk_table = &ct;
+  L.chunks = chunks;
+  L.n = N;
+  L.D = n_devices;
+  L.K = k_samples;
+  L.time_unit = time_unit;
+  L.rec = at<void>(ws, pl.rec);
+  L.memsum = at<void>(ws, pl.memsum);
+  L.far_fin = at<unsigned>(ws, pl.far_fin);
+  L.far_dev = at<unsigned char>(ws, pl.far_dev);
+  L.makespan = makespan;
+  L.valid = valid;
+  L.run_time = run_time;
+  GDP_LAUNCH(GDP_K_EVALUATE, launch_evaluate(L, st));
+  return GDP_OK;
+}
+
 extern "C" int gdp_debug_uniforms(uint64_t seed, int32_t n, int32_t k, int32_t d, float* out, void* stream) {
   clear_error();
   if (n < 1 || k < 1 || d < 1 || d > GDP_MAX_DEVICES || !out) return fail(GDP_E_INVALID_ARG, "bad arguments");
@@ -577,7 +650,8 @@ extern "C" const char* gdp_kernel_kind_name(int32_t kind) {
   static const char* names[GDP_K_COUNT] = {
       "graph_prep", "nbr_sample",    "gemm_pool_sigmoid", "gather_max", "gemm_update_relu",
       "meanpool",   "film",          "pre_layer",         "seg_attention", "post_attn",
-      "head_lse",   "gumbel_sample", "logp_reduce",       "mlp_placer", "ppo_grad",  "head_backward", "advantages"};
+      "head_lse",   "gumbel_sample", "logp_reduce",       "mlp_placer", "ppo_grad",  "head_backward", "advantages",
+      "evaluate"};
   if (kind < 0 || kind >= GDP_K_COUNT) return "";
   return names[kind];
 }

@@ -188,6 +188,23 @@ void plan_place(const gdp_graph* g, const gdp_placer* pl, PlacePlan* p) {
   p->o = carve_add(&p->c, N * d * es);
 }
 
+void plan_evaluate(const gdp_graph* g, int32_t n_devices, int32_t k, EvalPlan* p) {
+  const size_t N = (size_t)g->n_nodes, E = (size_t)g->n_edges;
+  const size_t kb = ((size_t)k + 63) / 64;
+  int32_t blk[GDP_MAX_GRAPHS + 1];
+  p->chunks = prefix_blocks_rows(g->graph_ptr_h, g->n_graphs, kEvalRows, blk);
+  carve_init(&p->c);
+  p->counters = carve_add(&p->c, (2 * N + 1) * 4);
+  p->scan_tmp = carve_add(&p->c, 2 * ((N + 1023) / 1024) * 4);
+  p->in_ptr = carve_add(&p->c, (N + 1) * 4);
+  p->s_ptr = carve_add(&p->c, (N + 1) * 4);
+  p->in_idx = carve_add(&p->c, (E > 0 ? E : 1) * 4);
+  p->rec = carve_add(&p->c, (E > 0 ? E : 1) * 8);
+  p->memsum = carve_add(&p->c, (size_t)g->n_graphs * (size_t)k * (size_t)n_devices * 8);
+  p->far_fin = carve_add(&p->c, kb * N * 64 * 4);
+  p->far_dev = carve_add(&p->c, kb * N * 64);
+}
+
 void plan_sample(const gdp_graph* g, int32_t k, SamplePlan* p) {
   int32_t blk[GDP_MAX_GRAPHS + 1];
   p->chunks = prefix_blocks_rows(g->graph_ptr_h, g->n_graphs, kSampleRows, blk);

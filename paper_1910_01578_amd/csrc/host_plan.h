@@ -55,6 +55,13 @@ struct SamplePlan {
   size_t coef;        // gdp_ppo_grad: G * K coefficients, then their G per-graph sums
   int chunks;
 };
+struct EvalPlan {
+  Carve c;
+  size_t counters;    // [in_deg: N | cursor: N | spare: 1]
+  size_t scan_tmp, in_ptr, s_ptr, in_idx, rec, memsum, far_fin, far_dev;
+  int chunks;
+};
+void plan_evaluate(const gdp_graph* g, int32_t n_devices, int32_t k_samples, EvalPlan* p);
 void plan_embed(const gdp_graph* g, const gdp_gnn* gnn, EmbedPlan* p);
 void plan_place(const gdp_graph* g, const gdp_placer* pl, PlacePlan* p);
 void plan_sample(const gdp_graph* g, int32_t k_samples, SamplePlan* p);
@@ -62,5 +69,6 @@ void plan_sample(const gdp_graph* g, int32_t k_samples, SamplePlan* p);
 constexpr int kPoolRows = 64;       // rows per mean-pool chunk
 constexpr int kAttnQ = 128;         // queries per attention work-group
 constexpr int kSampleRows = 256;    // nodes per sampling work-group
+constexpr int kEvalRows = 256;      // nodes per device-memory work-group of the evaluator
 
 }  // namespace gdp

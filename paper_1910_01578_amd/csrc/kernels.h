@@ -202,4 +202,32 @@ template <typename T>
 hipError_t launch_head_backward(const float* x, const T* w_out, const float* dlogits, int n, int d, int D, float* dx,
                                 float* dw_out, float* db_out, float* partial, hipStream_t s);
 
+// ---- the simulated run time of sampled placements ----------------------------
+// In-order list scheduling of every graph under each of K placements, with the
+// per-device memory check; in_ptr / in_idx is the reverse CSR (predecessors).
+struct EvalLaunch {
+  const int* placements;       // [K, n]
+  const int* op_cost;          // [n]
+  const int* out_xfer;         // [n]
+  const int* op_mem;           // [n]
+  const int64_t* mem_cap;      // host [G]
+  const int* in_ptr;           // [n + 1]
+  const int* in_idx;           // [n_edges]
+  int64_t n_edges;
+  const GraphTable* gt;        // graphs (ptr)
+  const GraphTable* chunk_table;   // graphs and their 256-node chunks (blk)
+  int chunks;
+  int n, D, K;
+  double time_unit;
+  void* rec;                   // scratch: n_edges int2
+  void* memsum;                // scratch: G * K * D uint64
+  unsigned* far_fin;           // scratch: ceil(K / 64) * n * 64 uint32
+  unsigned char* far_dev;      // scratch: ceil(K / 64) * n * 64 bytes
+  int64_t* makespan;           // [G, K]
+  unsigned char* valid;        // [G, K]
+  float* run_time;             // [G, K] or null
+};
+constexpr int kEvalChunk = 256;
+hipError_t launch_evaluate(const EvalLaunch& L, hipStream_t s);
+
 }  // namespace gdp

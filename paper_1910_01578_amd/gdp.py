@@ -31,7 +31,8 @@ GDP_NOALLOC_SCRATCH_BYTES = 4 << 20
 
 KERNEL_KINDS = ["graph_prep", "nbr_sample", "gemm_pool_sigmoid", "gather_max", "gemm_update_relu",
                 "meanpool", "film", "pre_layer", "seg_attention", "post_attn",
-                "head_lse", "gumbel_sample", "logp_reduce", "mlp_placer", "ppo_grad", "head_backward", "advantages"]
+                "head_lse", "gumbel_sample", "logp_reduce", "mlp_placer", "ppo_grad", "head_backward", "advantages",
+                "evaluate"]
 K_COUNT = len(KERNEL_KINDS)
 
 
@@ -91,6 +92,10 @@ def _load():
                                  c_void_p, c_void_p, c_void_p, c_size_t, c_void_p]),
         "gdp_sample_noalloc": (c_int32, [POINTER(GdpGraph), c_void_p, c_void_p, c_int32, c_int32, c_uint64,
                                          c_void_p, c_void_p, c_void_p, c_void_p]),
+        "gdp_evaluate_workspace_bytes": (c_size_t, [POINTER(GdpGraph), c_int32, c_int32]),
+        "gdp_evaluate": (c_int32, [POINTER(GdpGraph), c_int32, c_int32, c_void_p, c_void_p, c_void_p, c_void_p,
+                                   POINTER(c_int64), c_double, c_void_p, c_void_p, c_void_p, c_void_p, c_size_t,
+                                   c_void_p]),
         "gdp_validate_graph_host": (c_int32, [c_void_p, c_int32, c_void_p, c_int32, c_void_p, c_int64, c_uint32]),
         "gdp_last_error": (c_char_p, []),
         "gdp_abi_version": (c_int32, []),
@@ -313,6 +318,36 @@ class Runner:
                                       s_idx.data_ptr(), cap, self.ws.data_ptr(), self.ws_bytes,
                                       _stream_handle(stream)))
         return s_ptr, s_idx
+
+
+class Evaluator:
+    """Simulated run time and validity of sampled placements (gdp_evaluate) for
+    one graph batch: per-op costs in device memory, the workspace, the outputs."""
+
+    def __init__(self, graph: DeviceGraph, n_devices: int, k_samples: int, costs, device="cuda"):
+        torch = _torch()
+        self.graph, self.D, self.k = graph, int(n_devices), int(k_samples)
+        up = lambda a: torch.from_numpy(np.ascontiguousarray(a, np.int32)).to(device)
+        self.op_cost, self.out_xfer, self.op_mem = up(costs.op_cost), up(costs.out_xfer), up(costs.op_mem)
+        self.mem_cap = np.ascontiguousarray(costs.mem_cap, np.int64)
+        self.ws_bytes = lib.gdp_evaluate_workspace_bytes(ctypes.byref(graph.c), self.D, self.k)
+        if self.ws_bytes == 0:
+            raise GdpError(GDP_E_INVALID_ARG, last_error())
+        self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8, device=device)
+        G = graph.n_graphs
+        self.makespan = torch.empty((G, self.k), dtype=torch.int64, device=device)
+        self.valid = torch.empty((G, self.k), dtype=torch.uint8, device=device)
+        self.run_time = torch.empty((G, self.k), dtype=torch.float32, device=device)
+
+    def evaluate(self, placements, time_unit: float = 1e-6, stream=None):
+        """placements [K, N] int32 (device); returns (makespan, valid, run_time)."""
+        assert tuple(placements.shape) == (self.k, self.graph.n_nodes)
+        check(lib.gdp_evaluate(ctypes.byref(self.graph.c), self.D, self.k, placements.data_ptr(),
+                               self.op_cost.data_ptr(), self.out_xfer.data_ptr(), self.op_mem.data_ptr(),
+                               self.mem_cap.ctypes.data_as(POINTER(c_int64)), float(time_unit),
+                               self.makespan.data_ptr(), self.valid.data_ptr(), self.run_time.data_ptr(),
+                               self.ws.data_ptr(), self.ws_bytes, _stream_handle(stream)))
+        return self.makespan, self.valid, self.run_time
 
 
 class RewardBaseline:

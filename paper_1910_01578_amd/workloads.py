@@ -440,7 +440,7 @@ class OpCosts:
     mem_cap: np.ndarray    # [G] int64
 
 
-def make_costs(cfg: Config, g: "Graph", mem_slack: float = 1.3) -> OpCosts:
+def make_costs(cfg: Config, g: "Graph", mem_slack: float = 2.8) -> OpCosts:
     """Costs read off each op's first three log-normal size features (the
     output-shape meta features of Section 3.1), so larger tensors cost more to
     compute, move and hold; a device holds mem_slack times an even share of its

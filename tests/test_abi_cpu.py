@@ -228,6 +228,29 @@ def test_sample_noalloc_rejects_before_any_gpu_call():
     assert r == gdp.GDP_E_UNSUPPORTED and "GDP_NOALLOC_SCRATCH_BYTES" in gdp.last_error()
 
 
+def test_evaluate_rejects():
+    cfg, gp, g, gl, gnn, pl, placer = _descs()
+    dev = 0x100000
+    caps = (ctypes.c_int64 * 1)(100)
+    neg = (ctypes.c_int64 * 1)(-1)
+    ws = 0x1000000
+    need = gdp.lib.gdp_evaluate_workspace_bytes(ctypes.byref(g), 8, 4)
+    assert need > 0
+    assert gdp.lib.gdp_evaluate_workspace_bytes(ctypes.byref(g), 1, 4) == 0
+    call = lambda D=8, K=4, cap=caps, tu=1e-6, mk=dev, out=dev, size=need: gdp.lib.gdp_evaluate(
+        ctypes.byref(g), D, K, dev, dev, dev, dev, cap, tu, mk, out, None, ws, size, None)
+    assert call(D=1) == gdp.GDP_E_UNSUPPORTED
+    assert call(D=65) == gdp.GDP_E_UNSUPPORTED
+    assert call(K=0) == gdp.GDP_E_INVALID_ARG
+    assert call(cap=None) == gdp.GDP_E_INVALID_ARG
+    assert call(cap=neg) == gdp.GDP_E_INVALID_ARG
+    assert call(tu=-1.0) == gdp.GDP_E_INVALID_ARG
+    assert call(tu=float("nan")) == gdp.GDP_E_INVALID_ARG
+    assert call(mk=dev + 4) == gdp.GDP_E_INVALID_ARG
+    assert call(out=None) == gdp.GDP_E_INVALID_ARG
+    assert call(size=need - 1) == gdp.GDP_E_WORKSPACE
+
+
 def test_ppo_grad_rejects():
     cfg, gp, g, gl, gnn, pl, placer = _descs()
     dev = 0x100000
