@@ -18,6 +18,7 @@
 // times, with a wrap check that marks the graph's result -1.
 #include "device_common.h"
 #include "kernels.h"
+#include "lds_dma.h"
 
 namespace gdp {
 
@@ -60,8 +61,7 @@ struct EvalArgs {
   const int* in_ptr;       // [N + 1] reverse CSR
   const int2* rec;         // [E] (u, out_xfer[u])
   const unsigned long long* memsum;   // [G, K, D]
-  unsigned* far_fin;       // [KB, N, 64] finish times of every node, per sample lane
-  unsigned char* far_dev;  // [KB, N, 64]
+  unsigned* far;           // [KB, N, 64] packed (finish, device) of every node, per sample lane
   int n, D, K, KB;
   double time_unit;
   int64_t* makespan;       // [G, K]
@@ -73,62 +73,208 @@ struct CapTable {
   long long cap[GDP_MAX_GRAPHS];
 };
 
+// A finish time and the device it ran on share one word: time << 6 | device.
+constexpr unsigned kTimeLimit = 1u << 26;
+__device__ __forceinline__ unsigned pack(unsigned t, int dev) { return (t << 6) | (unsigned)dev; }
+
+// One direct global -> LDS load of a dword per lane: lane l reads base + voff
+// and writes it to LDS at lds + 4 l.  The compiler keeps no count of these
+// loads; the tile boundary waits for all of them (s_waitcnt vmcnt(0)).
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+__device__ __forceinline__ void dma4(dma::gptr_t base, uint32_t voff, const void* lds) {
+  const uint32_t la = (uint32_t)(uintptr_t)lds;
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dword %0, %1"
+               :: "v"(voff), "s"(base), "s"(__builtin_amdgcn_readfirstlane(la)) : "memory", "m0");
+}
+__device__ __forceinline__ void wait_all_memory() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+// A global load that waits for itself (and everything before it): the slow
+// path of a far predecessor that found no prefetch slot.  Written as inline
+// assembly so that the compiler cannot merge it with the LDS reads of the
+// common path into one generic (flat) load.
+__device__ __forceinline__ unsigned load_wait(const unsigned* p) {
+  unsigned w;
+  asm volatile("global_load_dword %0, %1, off\n\ts_waitcnt vmcnt(0)" : "=v"(w) : "v"(p) : "memory");
+  return w;
+}
+#pragma clang diagnostic pop
+
+constexpr int kRecSets = 4;                   // records per lane and tile: 4 * 64 per tile
+constexpr int kFarCap = 128;                  // far predecessors prefetched per tile
+
+// Lane i's view of node v0 + i of a tile: its predecessor range and cost.
+struct Hdr {
+  int ip0, ip1, cost;
+};
+// Lane i, set j: record rb + i + 64 j of a tile (rb its first record) and,
+// for a far predecessor, its prefetch slot (-1: none or beyond kFarCap).
+struct Recs {
+  int u[kRecSets], x[kRecSets], slot[kRecSets];
+};
+
+__device__ __forceinline__ Hdr load_hdr(const EvalArgs& a, int v0, int g1) {
+  const int v = v0 + (int)threadIdx.x;
+  Hdr h = {0, 0, 0};
+  if (v < g1) {
+    h.ip0 = a.in_ptr[v];
+    h.ip1 = a.in_ptr[v + 1];
+    h.cost = a.op_cost[v];
+  }
+  return h;
+}
+
+__device__ __forceinline__ Recs load_recs(const EvalArgs& a, const Hdr& h, int v0, int g1) {
+  Recs r;
+  const int cnt_nodes = min(kTile, g1 - v0);
+  const int rb = __builtin_amdgcn_readlane(h.ip0, 0);
+  const int re = cnt_nodes > 0 ? __builtin_amdgcn_readlane(h.ip1, cnt_nodes - 1) : rb;
+#pragma unroll
+  for (int j = 0; j < kRecSets; ++j) {
+    const int e = rb + (int)threadIdx.x + kWave * j;
+    r.u[j] = -1;
+    r.x[j] = 0;
+    r.slot[j] = -1;
+    if (e < re) {
+      const int2 q = a.rec[e];
+      r.u[j] = q.x;
+      r.x[j] = q.y;
+    }
+  }
+  return r;
+}
+
 __global__ __launch_bounds__(64) void k_list_schedule(EvalArgs a, GraphTable gt, CapTable caps) {
-  __shared__ unsigned ring_fin[kRing][kWave];
-  __shared__ unsigned char ring_dev[kRing][kWave];
+  // One LDS array holds the ring of packed (finish, device) words of nodes
+  // v - kRing .. v - 1 ([kRing][64]) and the two prefetch buffers of far
+  // predecessors ([2][kFarCap][64]), so a predecessor read is one LDS load from
+  // a computed offset.
+  __shared__ unsigned words[(kRing + 2 * kFarCap) * kWave];
+  unsigned (*ring)[kWave] = reinterpret_cast<unsigned (*)[kWave]>(&words[0]);
+  unsigned (*farbuf)[kFarCap][kWave] = reinterpret_cast<unsigned (*)[kFarCap][kWave]>(&words[kRing * kWave]);
+  __shared__ unsigned ptile[kTile / 4][kWave];            // devices of the tile's nodes, 4 per word
   __shared__ unsigned dev_free[GDP_MAX_DEVICES][kWave];
-  __shared__ unsigned char tile[kTile][kWave];
   const int lane = threadIdx.x;
   const int g = blockIdx.x / a.KB, kb = blockIdx.x % a.KB;
   const int k = kb * kWave + lane;
   const bool active = k < a.K;
   const int g0 = gt.ptr[g], g1 = gt.ptr[g + 1];
   for (int d = 0; d < a.D; ++d) dev_free[d][lane] = 0u;
-  unsigned* far_fin = a.far_fin + (size_t)kb * a.n * kWave;
-  unsigned char* far_dev = a.far_dev + (size_t)kb * a.n * kWave;
+  unsigned* far = a.far + (size_t)kb * a.n * kWave;
+  const dma::gptr_t far_base = dma::uniform_base(far);
   const int* prow = a.placements + (size_t)(active ? k : 0) * a.n;
   unsigned mk = 0u;
   bool wrapped = false;
-  for (int v0 = g0; v0 < g1; v0 += kTile) {
-    // this lane's devices for the next kTile nodes (its own column of the tile)
-    const int cnt = min(kTile, g1 - v0);
-    for (int t = 0; t < cnt; ++t) {
-      const int p = active ? prow[v0 + t] : 0;
-      tile[t][lane] = (unsigned char)((p >= 0 && p < a.D) ? p : 0);
+
+  // pipeline: headers three tiles ahead, records two, far predecessors and
+  // devices one
+  Hdr h0 = load_hdr(a, g0, g1), h1 = load_hdr(a, g0 + kTile, g1), h2 = load_hdr(a, g0 + 2 * kTile, g1);
+  Recs r0 = load_recs(a, h0, g0, g1), r1 = load_recs(a, h1, g0 + kTile, g1);
+  int pl[kTile];
+#pragma unroll
+  for (int i = 0; i < kTile; ++i) pl[i] = (g0 + i < g1) ? prow[g0 + i] : 0;
+
+  for (int v0 = g0, tl = 0; v0 < g1; v0 += kTile, ++tl) {
+    wait_all_memory();
+    // this tile's devices into LDS, 4 per word
+#pragma unroll
+    for (int q = 0; q < kTile / 4; ++q) {
+      unsigned w = 0u;
+#pragma unroll
+      for (int b = 0; b < 4; ++b) {
+        const int p = active ? pl[4 * q + b] : 0;
+        w |= (unsigned)((p >= 0 && p < a.D) ? p : 0) << (8 * b);
+      }
+      ptile[q][lane] = w;
     }
+    // far predecessors of the next tile (final since several tiles): slots and loads
+    const int v1 = v0 + kTile;
+    if (v1 < g1) {
+      const int limit = v1 + kTile - kRing;      // u below this is read from the prefetch
+      int base = 0;
+#pragma unroll
+      for (int j = 0; j < kRecSets; ++j) {
+        const bool f = r1.u[j] >= g0 && r1.u[j] < limit;
+        const uint64_t m = __ballot(f);
+        const int rank = __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0));
+        const int s = base + rank;
+        r1.slot[j] = f && s < kFarCap ? s : -1;
+        base += __popcll(m);
+        uint64_t mm = m;
+        while (mm) {
+          const int ln = __builtin_ctzll(mm);
+          mm &= mm - 1;
+          const int sl = __builtin_amdgcn_readlane(r1.slot[j], ln);
+          if (sl < 0) break;
+          const int u = __builtin_amdgcn_readlane(r1.u[j], ln);
+          dma4(far_base, (uint32_t)(((size_t)u * kWave + lane) * 4u), &farbuf[(tl + 1) & 1][sl][0]);
+        }
+      }
+    }
+    // records two tiles ahead, headers three tiles ahead, devices of the next tile
+    const Recs r2 = load_recs(a, h2, v0 + 2 * kTile, g1);
+    const Hdr h3 = load_hdr(a, v0 + 3 * kTile, g1);
+#pragma unroll
+    for (int i = 0; i < kTile; ++i) pl[i] = (v1 + i < g1) ? prow[v1 + i] : 0;
+
+    const int cnt = min(kTile, g1 - v0);
+    const int rb = __builtin_amdgcn_readlane(h0.ip0, 0);
+    const int limit = v0 + kTile - kRing;
+    const int fb_off = (kRing + (tl & 1) * kFarCap) * kWave;
     for (int t = 0; t < cnt; ++t) {
       const int v = v0 + t;
-      const int p = tile[t][lane];
+      const int p = (ptile[t >> 2][lane] >> (8 * (t & 3))) & 0xff;
+      const int e0 = __builtin_amdgcn_readlane(h0.ip0, t), e1 = __builtin_amdgcn_readlane(h0.ip1, t);
+      const int c = __builtin_amdgcn_readlane(h0.cost, t);
       unsigned ready = 0u;
-      const int e0 = a.in_ptr[v], e1 = a.in_ptr[v + 1];
       for (int e = e0; e < e1; ++e) {
-        const int2 r = a.rec[e];
-        const int u = r.x;
-        if (u < g0 || u >= v) continue;   // not a predecessor in this graph (invalid input)
-        unsigned fu;
-        int du;
-        if (v - u <= kRing) {
-          fu = ring_fin[u & (kRing - 1)][lane];
-          du = ring_dev[u & (kRing - 1)][lane];
+        const int r = e - rb;
+        int u, x, slot;
+        if (r < kRecSets * kWave) {
+          const int j = r >> 6, ln = r & 63;
+          const int uu = j == 0 ? r0.u[0] : j == 1 ? r0.u[1] : j == 2 ? r0.u[2] : r0.u[3];
+          const int xx = j == 0 ? r0.x[0] : j == 1 ? r0.x[1] : j == 2 ? r0.x[2] : r0.x[3];
+          const int ss = j == 0 ? r0.slot[0] : j == 1 ? r0.slot[1] : j == 2 ? r0.slot[2] : r0.slot[3];
+          u = __builtin_amdgcn_readlane(uu, ln);
+          x = __builtin_amdgcn_readlane(xx, ln);
+          slot = __builtin_amdgcn_readlane(ss, ln);
         } else {
-          fu = far_fin[(size_t)u * kWave + lane];
-          du = far_dev[(size_t)u * kWave + lane];
+          const int2 q = a.rec[e];
+          u = q.x;
+          x = q.y;
+          slot = -1;
         }
-        const unsigned arrive = fu + (du != p ? (unsigned)r.y : 0u);
-        wrapped |= arrive < fu;
+        if (u < g0 || u >= v) continue;   // not a predecessor in this graph (invalid input)
+        // Ring and prefetch buffer: one LDS read at a computed offset (a
+        // generic load here would wait for every outstanding memory operation
+        // of the wave, the prefetches and stores included).
+        unsigned w;
+        if (u >= limit || slot >= 0) {
+          const int off = u >= limit ? (u & (kRing - 1)) * kWave : fb_off + slot * kWave;
+          w = words[off + lane];
+        } else {
+          w = load_wait(&far[(size_t)u * kWave + lane]);
+        }
+        const unsigned fu = w >> 6;
+        const int du = (int)(w & 63u);
+        const unsigned arrive = fu + (du != p ? (unsigned)x : 0u);
         ready = max(ready, arrive);
       }
       const unsigned start = max(ready, dev_free[p][lane]);
-      const unsigned fin = start + (unsigned)a.op_cost[v];
-      wrapped |= fin < start;
+      const unsigned fin = start + (unsigned)c;
+      wrapped |= fin >= kTimeLimit || fin < start;
+      const unsigned pw = pack(fin & (kTimeLimit - 1), p);
       dev_free[p][lane] = fin;
-      ring_fin[v & (kRing - 1)][lane] = fin;
-      ring_dev[v & (kRing - 1)][lane] = (unsigned char)p;
-      far_fin[(size_t)v * kWave + lane] = fin;
-      far_dev[(size_t)v * kWave + lane] = (unsigned char)p;
+      ring[v & (kRing - 1)][lane] = pw;
+      far[(size_t)v * kWave + lane] = pw;
       mk = max(mk, fin);
     }
+    h0 = h1;
+    h1 = h2;
+    h2 = h3;
+    r0 = r1;
+    r1 = r2;
   }
+  wait_all_memory();
   if (!active) return;
   bool ok = true;
   const unsigned long long* ms = a.memsum + ((size_t)g * a.K + k) * a.D;
@@ -162,8 +308,7 @@ hipError_t launch_evaluate(const EvalLaunch& L, hipStream_t s) {
   a.in_ptr = L.in_ptr;
   a.rec = reinterpret_cast<const int2*>(L.rec);
   a.memsum = reinterpret_cast<const unsigned long long*>(L.memsum);
-  a.far_fin = L.far_fin;
-  a.far_dev = L.far_dev;
+  a.far = L.far;
   a.n = L.n;
   a.D = L.D;
   a.K = L.K;

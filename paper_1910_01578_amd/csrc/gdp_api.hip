@@ -584,8 +584,7 @@ extern "C" int gdp_evaluate(const gdp_graph* g, int32_t n_devices, int32_t k_sam
   L.time_unit = time_unit;
   L.rec = at<void>(ws, pl.rec);
   L.memsum = at<void>(ws, pl.memsum);
-  L.far_fin = at<unsigned>(ws, pl.far_fin);
-  L.far_dev = at<unsigned char>(ws, pl.far_dev);
+  L.far = at<unsigned>(ws, pl.far);
   L.makespan = makespan;
   L.valid = valid;
   L.run_time = run_time;

@@ -201,8 +201,7 @@ void plan_evaluate(const gdp_graph* g, int32_t n_devices, int32_t k, EvalPlan* p
   p->in_idx = carve_add(&p->c, (E > 0 ? E : 1) * 4);
   p->rec = carve_add(&p->c, (E > 0 ? E : 1) * 8);
   p->memsum = carve_add(&p->c, (size_t)g->n_graphs * (size_t)k * (size_t)n_devices * 8);
-  p->far_fin = carve_add(&p->c, kb * N * 64 * 4);
-  p->far_dev = carve_add(&p->c, kb * N * 64);
+  p->far = carve_add(&p->c, kb * N * 64 * 4);
 }
 
 void plan_sample(const gdp_graph* g, int32_t k, SamplePlan* p) {

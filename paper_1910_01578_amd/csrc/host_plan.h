@@ -58,7 +58,7 @@ struct SamplePlan {
 struct EvalPlan {
   Carve c;
   size_t counters;    // [in_deg: N | cursor: N | spare: 1]
-  size_t scan_tmp, in_ptr, s_ptr, in_idx, rec, memsum, far_fin, far_dev;
+  size_t scan_tmp, in_ptr, s_ptr, in_idx, rec, memsum, far;
   int chunks;
 };
 void plan_evaluate(const gdp_graph* g, int32_t n_devices, int32_t k_samples, EvalPlan* p);

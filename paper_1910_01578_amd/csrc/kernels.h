@@ -221,8 +221,7 @@ struct EvalLaunch {
   double time_unit;
   void* rec;                   // scratch: n_edges int2
   void* memsum;                // scratch: G * K * D uint64
-  unsigned* far_fin;           // scratch: ceil(K / 64) * n * 64 uint32
-  unsigned char* far_dev;      // scratch: ceil(K / 64) * n * 64 bytes
+  unsigned* far;               // scratch: ceil(K / 64) * n * 64 uint32
   int64_t* makespan;           // [G, K]
   unsigned char* valid;        // [G, K]
   float* run_time;             // [G, K] or null
