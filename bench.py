@@ -85,6 +85,119 @@ def measured_traffic(kind):
             "summary": rec["summary"]}
 
 
+def blas_info():
+    """The BLAS numpy uses (threadpoolctl's report) for the oracle's timing."""
+    try:
+        from threadpoolctl import threadpool_info
+        for rec in threadpool_info():
+            if rec.get("user_api") == "blas":
+                return {"internal_api": rec.get("internal_api"), "version": rec.get("version"),
+                        "library": os.path.basename(rec.get("filepath", ""))}
+    except Exception:   # reporting only
+        pass
+    return None
+
+
+def roofline_of(work, kind, ms_total, launches, dtype):
+    if kind not in work or launches == 0:
+        return None
+    bound, amount = work[kind]
+    sec = ms_total / launches / 1e3
+    if bound == "mfma":
+        ach = amount / sec / 1e12
+        peak = PEAK_TFLOPS[dtype]
+        return {"bound": "mfma", "achieved": round(ach, 2), "peak": peak, "unit": "TFLOP/s", "frac": round(ach / peak, 4)}
+    ach = amount / sec / 1e9
+    return {"bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+            "frac": round(ach / PEAK_HBM_GBS, 4)}
+
+
+def config_leg(cfg, steps, cores):
+    """One workload: the step's nodes/s (median of per-step events), the dominant
+    kernel's roofline fraction, and the whole oracle on the host cores."""
+    import numpy as np
+    import torch
+
+    from paper_1910_01578_amd import gdp, workloads as W
+    g, w = W.make_graph(cfg), W.make_weights(cfg)
+    stats = W.graph_stats(g, cfg.fanout)
+    r = gdp.Runner(gdp.DeviceGraph(g, cfg.dtype), gdp.DevicePolicy(cfg, w), cfg.k_samples)
+    for _ in range(2):
+        r.forward(cfg.sample_seed)
+    torch.cuda.synchronize()
+    gdp.timer_begin(range(gdp.K_COUNT))
+    r.forward(cfg.sample_seed)
+    bd = gdp.timer_end()
+    work, _ = flop_model(cfg, g, stats)
+    dominant = max(bd, key=lambda k: bd[k]["ms"])
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    torch.cuda.synchronize()
+    ev[0].record()
+    for i in range(steps):
+        r.forward(cfg.sample_seed)
+        ev[i + 1].record()
+    torch.cuda.synchronize()
+    ms = np.array([ev[i].elapsed_time(ev[i + 1]) for i in range(steps)])
+    med = float(np.median(ms))
+    rec = {"workload": cfg.name, "nodes": g.n_nodes, "dtype": cfg.dtype, "value": round(g.n_nodes / (med * 1e-3), 1),
+           "unit": "nodes/s", "median_ms": round(med, 4), "min_ms": round(float(ms.min()), 4),
+           "max_ms": round(float(ms.max()), 4), "dominant": dominant,
+           "roofline": roofline_of(work, dominant, bd[dominant]["ms"], bd[dominant]["launches"], cfg.dtype)}
+    del r
+    if cores:
+        base = cpu_baseline(cfg, g, w, g.n_nodes, cores)
+        rec["oracle"] = {"value": round(base["value"], 1), "unit": "nodes/s", "cores": cores,
+                         "seconds": round(g.n_nodes / base["value"], 2)}
+    return rec
+
+
+def training_leg(cfg, g, w, steps):
+    """The update step on the headline workload: training forward, backward and
+    Adam (median of event-timed calls), and whole GDP iterations."""
+    import numpy as np
+    import torch
+
+    from paper_1910_01578_amd import gdp, trainer as T, workloads as W
+    dg = gdp.DeviceGraph(g, cfg.dtype)
+    pol = gdp.DevicePolicy(cfg, w)
+    t = gdp.Trainer(dg, pol, cfg.k_samples)
+    rng = np.random.default_rng(cfg.cfg_id)
+    dl = torch.from_numpy((rng.normal(size=(g.n_nodes, cfg.n_devices)) / np.sqrt(g.n_nodes)).astype(np.float32)).cuda()
+    t.forward()
+    t.backward(dl)
+    torch.cuda.synchronize()
+    reps = max(3, min(steps, 5))
+    out = {"store_bytes": t.store_bytes, "workspace_bytes": t.ws_bytes}
+    for name, fn in (("train_forward", t.forward), ("backward", lambda: t.backward(dl)),
+                     ("adam", lambda: t.adam(1e-5))):
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(reps + 1)]
+        ev[0].record()
+        for i in range(reps):
+            fn()
+            ev[i + 1].record()
+        torch.cuda.synchronize()
+        ms = np.array([ev[i].elapsed_time(ev[i + 1]) for i in range(reps)])
+        out[name + "_ms"] = round(float(np.median(ms)), 3)
+    gdp.timer_begin(range(gdp.K_COUNT))
+    t.forward()
+    t.backward(dl)
+    bd = gdp.timer_end()
+    out["breakdown_ms"] = {k: round(v["ms"], 3) for k, v in bd.items()}
+    del t, pol, dg
+    b = T.GDPBatch(cfg, g, w, W.make_costs(cfg, g), cfg.k_samples)
+    b.step(0)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    hist = T.train(b, 3, seed0=1)
+    torch.cuda.synchronize()
+    out["gdp_iteration_ms"] = round(1e3 * (time.perf_counter() - t0) / 3, 2)
+    out["gdp_iteration"] = "sample K placements, evaluate, reward, 2 PPO epochs (forward, log-probs, PPO gradient, " \
+                           "backward, Adam)"
+    out["reward_last"] = [round(float(x), 4) for x in hist[-1]["reward"]]
+    del b
+    return out
+
+
 def cpu_baseline(cfg, g, w, n_sample, cores):
     """The fp64 oracle (untuned) on the first n_sample nodes of the same DAG."""
     from threadpoolctl import threadpool_limits
@@ -102,7 +215,8 @@ def cpu_baseline(cfg, g, w, n_sample, cores):
     what = (f"the whole {g.n_nodes}-node DAG" if n_sample == g.n_nodes else
             f"first {n_sample} nodes of the {g.n_nodes}-node DAG (induced sub-DAG)")
     return {"value": n_sample / dt, "unit": "nodes/s", "cores": cores, "kind": "oracle",
-            "sample": f"{what}, full embed+place+sample with K={cfg.k_samples}, numpy float64, {dt:.1f} s"}
+            "sample": f"{what}, full embed+place+sample with K={cfg.k_samples}, numpy float64, {dt:.1f} s",
+            "blas": blas_info()}
 
 
 def main():
@@ -113,6 +227,7 @@ def main():
     ap.add_argument("--config", default="gnmt8_52000")
     ap.add_argument("--cpu-sample", type=int, default=-1,
                     help="oracle sample: first N nodes (-1 = the whole workload, 0 = skip)")
+    ap.add_argument("--all-configs", type=int, default=1, help="also measure the four smaller workloads")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="run one plain device copy of this many MiB before the warm-up (counter calibration)")
     args = ap.parse_args()
@@ -153,18 +268,26 @@ def main():
     work, keys = flop_model(cfg, g, stats)
     dominant = max(breakdown, key=lambda k: breakdown[k]["ms"])
 
-    # Timed region: K steps; events only around the dominant kernel's launches.
+    # Timed region: K steps; events around every step on the launch stream and
+    # around the dominant kernel's launches.
     torch.cuda.synchronize()
     gdp.timer_begin([dominant])
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     t0 = time.perf_counter()
-    for _ in range(args.steps):
+    ev[0].record()
+    for i in range(args.steps):
         runner.forward(seed)
+        ev[i + 1].record()
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     dom = gdp.timer_end()[dominant]
     elapsed = t1 - t0
     ms_per_step = 1e3 * elapsed / args.steps
     value = g.n_nodes * args.steps / elapsed
+    step_ms = np.array([ev[i].elapsed_time(ev[i + 1]) for i in range(args.steps)])
+    step_events = {"median_ms": round(float(np.median(step_ms)), 4), "min_ms": round(float(step_ms.min()), 4),
+                   "max_ms": round(float(step_ms.max()), 4),
+                   "nodes_per_s_at_median": round(g.n_nodes / (float(np.median(step_ms)) * 1e-3), 1)}
 
     def roof(kind, ms_total, launches):
         if kind not in work or launches == 0:
@@ -321,9 +444,22 @@ def main():
                 "ms_per_step": round(1e3 * ab_elapsed / args.steps, 4), "kernels": ab_kernels}
     del ab
 
+    # The update step on the same DAG and weights: the training forward that
+    # keeps every intermediate, the backward pass and Adam (fp32 arithmetic),
+    # and one whole GDP iteration (sample, evaluate, reward, two PPO epochs).
+    training = training_leg(cfg, g, w, args.steps)
+
+    # Every other workload: nodes/s of the same step, its dominant kernel's
+    # roofline fraction, and the oracle's time on the host cores.
+    cores = len(os.sched_getaffinity(0))
+    configs = []
+    if args.all_configs:
+        for name in W.CONFIG_ORDER:
+            if name != cfg.name:
+                configs.append(config_leg(W.get_config(name), args.steps, cores if args.cpu_sample != 0 else 0))
+
     cpu = None
     if args.cpu_sample != 0:
-        cores = min(16, len(os.sched_getaffinity(0)))
         n = g.n_nodes if args.cpu_sample < 0 else min(args.cpu_sample, g.n_nodes)
         cpu = cpu_baseline(cfg, g, w, n, cores)
 
@@ -338,7 +474,10 @@ def main():
                    "attention_keys": keys, "parallelism": "single GPU"},
         "roofline": roofline,
         "cpu_baseline": cpu,
+        "step_events": step_events,
         "kernels": kernels,
+        "configs": configs,
+        "training": training,
         "graph_replay": graph_replay,
         "ablation_no_attention": ablation,
         "ppo_grad": ppo,

@@ -345,6 +345,99 @@ int gdp_ppo_grad(const gdp_graph* g, const float* logits, const float* lse, int3
                  const float* advantages, float clip_eps, float* loss, float* dlogits, void* workspace,
                  size_t workspace_bytes, void* stream);
 
+/* ---- the update step (Section 3: Eq. 1 with PPO) --------------------------
+ *
+ * The policy is trained end to end: the graph embedding network jointly with
+ * the placement network (Section 3.1), the cached segment memory passing no
+ * gradient (Section 3.2: hidden states of earlier segments are cached with
+ * gradient flow disabled, as in Transformer-XL: a query still reaches the
+ * memory's keys and values, so W_qkv receives their gradient, but the earlier
+ * segments' activations do not).  One update:
+ *   gdp_forward_train  the policy forward in fp32 arithmetic, keeping every
+ *                      intermediate in a caller-owned store, and the logits
+ *   gdp_log_prob       log pi(placement | graph) of given placements
+ *   gdp_ppo_grad       dL/dlogits of PPO's clipped surrogate
+ *   gdp_backward       dL/dtheta for every weight, from dL/dlogits and the store
+ *   gdp_adam_step      Adam on every weight (fp32 master copies and moments)
+ */
+
+/* Gradients of one layer: fp32 device arrays shaped like the weights. */
+typedef struct gdp_gnn_layer_grad {
+  float *w_pool, *b_pool, *w_self, *w_neigh, *b_upd;
+} gdp_gnn_layer_grad;
+typedef struct gdp_placer_layer_grad {
+  float *film_wg, *film_bg, *film_wb, *film_bb;  /* used when film = 1 (else may be NULL) */
+  float *w_qkv, *b_qkv, *w_o, *b_o, *ln1_g, *ln1_b;  /* used when attention = 1 (else may be NULL) */
+  float *w_1, *b_1, *w_2, *b_2, *ln2_g, *ln2_b;
+} gdp_placer_layer_grad;
+typedef struct gdp_grads {
+  const gdp_gnn_layer_grad* gnn;       /* host array [gnn.n_layers]    */
+  const gdp_placer_layer_grad* placer; /* host array [placer.n_layers] */
+  float* w_out;                        /* [D, d]                       */
+  float* b_out;                        /* [D]                          */
+} gdp_grads;
+
+/*
+ * Sizes of the training forward's store and of the workspace of
+ * gdp_forward_train / gdp_backward (bytes).  At most 8 GNN layers and 16
+ * placer layers; d_model must equal the GNN's hidden width.  Returns
+ * GDP_OK or an error (then the sizes are 0).
+ */
+int gdp_train_sizes(const gdp_graph* g, const gdp_gnn* gnn, const gdp_placer* placer, size_t* store_bytes,
+                    size_t* workspace_bytes);
+
+/*
+ * The policy forward (Eq. 2-3, the mean pool, Eq. 4's FiLM, the placer of
+ * Section 3.2 and the head) in fp32 arithmetic -- bf16 weights and features
+ * are widened on load -- keeping every intermediate the backward pass needs
+ * in store (256-byte aligned, gdp_train_sizes bytes; opaque layout, valid
+ * for the weights and graph of this call).
+ *   logits  device [N, D] fp32 (output)     lse  device [N] fp32 (output, may be NULL)
+ */
+int gdp_forward_train(const gdp_graph* g, const gdp_gnn* gnn, const gdp_placer* placer, void* store,
+                      size_t store_bytes, float* logits, float* lse, void* workspace, size_t workspace_bytes,
+                      void* stream);
+
+/*
+ * Gradient of L with respect to every weight, given dlogits = dL/dlogits
+ * [N, D] fp32 (e.g. from gdp_ppo_grad) and the store of gdp_forward_train with
+ * the same weights.  Writes (does not accumulate) every gradient array of
+ * grads that the configuration uses.  Deterministic (fixed summation orders).
+ */
+int gdp_backward(const gdp_graph* g, const gdp_gnn* gnn, const gdp_placer* placer, const void* store,
+                 size_t store_bytes, const float* dlogits, const gdp_grads* grads, void* workspace,
+                 size_t workspace_bytes, void* stream);
+
+/*
+ * logp[g, k] = sum over v in graph g of (logits[v, placements[k, v]] - lse[v])
+ * for given placements (the numerator of PPO's ratio after an update).
+ *   logits device [N, D]; lse device [N] (may be NULL: recomputed);
+ *   placements device [K, N] int32 in [0, D); logp device [G, K] (output).
+ * The workspace of gdp_workspace_bytes with the same K suffices.
+ */
+int gdp_log_prob(const gdp_graph* g, const float* logits, const float* lse, int32_t n_devices, int32_t k_samples,
+                 const int32_t* placements, float* logp, void* workspace, size_t workspace_bytes, void* stream);
+
+/* One tensor of gdp_adam_step: the weights the kernels read (dtype), their
+ * fp32 master copy, the gradient and Adam's two moments, n elements each. */
+typedef struct gdp_adam_tensor {
+  void* param;
+  float* master;
+  const float* grad;
+  float* m;
+  float* v;
+  int64_t n;
+} gdp_adam_tensor;
+
+/*
+ * Adam (Kingma and Ba, 2015), step t >= 1: m = b1 m + (1 - b1) g,
+ * v = b2 v + (1 - b2) g^2, master -= lr (m / (1 - b1^t)) / (sqrt(v / (1 - b2^t)) + eps),
+ * param = master rounded to dtype (GDP_F32 or GDP_BF16, round to nearest even).
+ * tensors is a host array.  No workspace.
+ */
+int gdp_adam_step(int32_t n_tensors, const gdp_adam_tensor* tensors, int32_t dtype, float lr, float beta1,
+                  float beta2, float eps, int64_t step, void* stream);
+
 /*
  * Host-side check of a graph batch (all pointers host memory): graph_ptr
  * strictly increasing from 0, row_ptr monotone from 0 to E, col_idx in range,
@@ -379,6 +472,17 @@ int gdp_debug_uniforms(uint64_t seed, int32_t n_nodes, int32_t k_samples, int32_
 int gdp_debug_neighbors(const gdp_graph* g, const gdp_gnn* gnn, int32_t* s_ptr, int32_t* s_idx,
                         int64_t capacity, void* workspace, size_t workspace_bytes, void* stream);
 
+/*
+ * One intermediate of gdp_forward_train's store, copied to out (device): the
+ * forward's discrete decisions, for comparisons that must take them the same
+ * way.  which = 0: the feed-forward hidden layer of placer layer `layer`
+ * ([N, d_ff] fp32, after ReLU); 1: the output of GNN layer `layer` ([N, H]
+ * fp32, after ReLU); 2: the winning neighbour of every element of GNN layer
+ * `layer`'s max-pool ([N, H] int32, -1 where S(v) is empty).
+ */
+int gdp_debug_train_tensor(const gdp_graph* g, const gdp_gnn* gnn, const gdp_placer* placer, const void* store,
+                           size_t store_bytes, int32_t which, int32_t layer, void* out, size_t out_bytes, void* stream);
+
 /* Kernel kinds for the event timer below. */
 typedef enum gdp_kernel_kind {
   GDP_K_GRAPH_PREP = 0,  /* degree count, scans, reverse-edge fill          */
@@ -401,6 +505,10 @@ typedef enum gdp_kernel_kind {
   GDP_K_HEAD_BWD,        /* the head's backward pass                        */
   GDP_K_ADVANTAGE,       /* reward and advantage of measured run times      */
   GDP_K_EVALUATE,        /* simulated run time and validity of placements   */
+  GDP_K_TRAIN_FWD,       /* the training forward (all intermediates kept)   */
+  GDP_K_BACKWARD,        /* the backward pass                               */
+  GDP_K_ADAM,            /* the Adam update                                 */
+  GDP_K_LOGPROB,         /* log-probabilities of given placements           */
   GDP_K_COUNT
 } gdp_kernel_kind;
 

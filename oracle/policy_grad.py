@@ -60,15 +60,21 @@ def _attention(yq, ykv, lw, n_heads):
     return torch.cat(heads, dim=1) @ lw["w_o"].T + lw["b_o"]
 
 
-def _ffn(z, lw):
-    return torch.relu(z @ lw["w_1"].T + lw["b_1"]) @ lw["w_2"].T + lw["b_2"]
+def _relu(u, mask=None):
+    """ReLU; with mask (the sign decisions of a run to compare against) the
+    decision is taken from the mask instead of from u's sign."""
+    return torch.relu(u) if mask is None else u * torch.as_tensor(mask, dtype=F64)
 
 
-def _block(y, mem, lw, n_heads):
+def _ffn(z, lw, mask=None):
+    return _relu(z @ lw["w_1"].T + lw["b_1"], mask) @ lw["w_2"].T + lw["b_2"]
+
+
+def _block(y, mem, lw, n_heads, mask=None):
     """Post-LN layer on the segment rows y with the cached rows mem (constants)."""
     ctx = torch.cat([mem, y], dim=0)
     z = _layer_norm(y + _attention(y, ctx, lw, n_heads), lw["ln1_g"], lw["ln1_b"])
-    return _layer_norm(z + _ffn(z, lw), lw["ln2_g"], lw["ln2_b"])
+    return _layer_norm(z + _ffn(z, lw, mask), lw["ln2_g"], lw["ln2_b"])
 
 
 def _film(x0, placer, film):
@@ -83,11 +89,14 @@ def _film(x0, placer, film):
     return out
 
 
-def _placer_forward(node_emb, x0, graph_ptr, placer, head, n_heads, seg_len, mem_len, film, attention):
+def _placer_forward(node_emb, x0, graph_ptr, placer, head, n_heads, seg_len, mem_len, film, attention,
+                    ffn_masks=None):
     """Formulation A (segment loop, per-graph memory caches of each layer's
-    conditioned input, detached), or the ablation's row-local layers."""
+    conditioned input, detached), or the ablation's row-local layers.
+    ffn_masks: optional per-layer [N, d_ff] sign decisions of the FFN's ReLU."""
     N, d = node_emb.shape
     cond = _film(x0, placer, film)
+    fm = (lambda l, a, b: None) if ffn_masks is None else (lambda l, a, b: ffn_masks[l][a:b])
     rows = []
     for g in range(len(graph_ptr) - 1):
         gs, ge = int(graph_ptr[g]), int(graph_ptr[g + 1])
@@ -95,7 +104,7 @@ def _placer_forward(node_emb, x0, graph_ptr, placer, head, n_heads, seg_len, mem
             x = node_emb[gs:ge]
             for l, lw in enumerate(placer):
                 y = cond[l][0][g] * x + cond[l][1][g]
-                x = _layer_norm(y + _ffn(y, lw), lw["ln2_g"], lw["ln2_b"])
+                x = _layer_norm(y + _ffn(y, lw, fm(l, gs, ge)), lw["ln2_g"], lw["ln2_b"])
             rows.append(x)
             continue
         mems = [torch.zeros(0, d, dtype=F64) for _ in placer]
@@ -105,7 +114,7 @@ def _placer_forward(node_emb, x0, graph_ptr, placer, head, n_heads, seg_len, mem
             for l, lw in enumerate(placer):
                 y = cond[l][0][g] * x + cond[l][1][g]
                 new_mem = torch.cat([mems[l], y], dim=0)
-                x_next = _block(y, mems[l], lw, n_heads)
+                x_next = _block(y, mems[l], lw, n_heads, fm(l, q0, q1))
                 mems[l] = new_mem[max(0, new_mem.shape[0] - mem_len):].detach() if mem_len > 0 \
                     else torch.zeros(0, d, dtype=F64)
                 x = x_next
@@ -114,10 +123,12 @@ def _placer_forward(node_emb, x0, graph_ptr, placer, head, n_heads, seg_len, mem
     return x @ head["w_out"].T + head["b_out"]
 
 
-def _gnn_forward(x, S, gnn):
+def _gnn_forward(x, S, gnn, decisions=None):
     """Eq. 2 and Eq. 3; the max over S(v) takes, per element, the first maximal
     row of S(v) in ascending node order (torch.max's documented tie rule), and
-    an empty S(v) aggregates to 0."""
+    an empty S(v) aggregates to 0.  decisions: optional per-layer (arg [N, H],
+    relu mask [N, H]) -- the winning neighbour of every element (-1: none) and
+    the update's ReLU signs of a run to compare against."""
     N = x.shape[0]
     width = max(1, max((len(s) for s in S), default=0))
     idx = np.full((N, width), N, np.int64)            # pad with the row index N (-inf below)
@@ -126,12 +137,20 @@ def _gnn_forward(x, S, gnn):
     has = torch.as_tensor(np.array([len(s) > 0 for s in S]))[:, None]
     idx_t = torch.as_tensor(idx)
     h = x
-    for lw in gnn:
+    for l, lw in enumerate(gnn):
         P = torch.sigmoid(h @ lw["w_pool"].T + lw["b_pool"])
-        pad = torch.cat([P, torch.full((1, P.shape[1]), -np.inf, dtype=F64)], dim=0)
-        A, _ = torch.max(pad[idx_t], dim=1)
-        A = torch.where(has, A, torch.zeros_like(A))
-        h = torch.relu(h @ lw["w_self"].T + A @ lw["w_neigh"].T + lw["b_upd"])
+        if decisions is None:
+            pad = torch.cat([P, torch.full((1, P.shape[1]), -np.inf, dtype=F64)], dim=0)
+            A, _ = torch.max(pad[idx_t], dim=1)
+            A = torch.where(has, A, torch.zeros_like(A))
+            mask = None
+        else:
+            arg, mask = decisions[l]
+            arg = np.asarray(arg, np.int64)
+            cols = np.broadcast_to(np.arange(P.shape[1]), arg.shape)
+            A = P[torch.as_tensor(np.maximum(arg, 0)), torch.as_tensor(cols)]
+            A = torch.where(torch.as_tensor(arg >= 0), A, torch.zeros_like(A))
+        h = _relu(h @ lw["w_self"].T + A @ lw["w_neigh"].T + lw["b_upd"], mask)
     return h
 
 
@@ -174,17 +193,26 @@ def gnn_backward(graph_ptr, row_ptr, col_idx, x, gnn_layers, dnode_emb, dgraph_e
 
 
 def policy_backward(graph_ptr, row_ptr, col_idx, x, gnn_layers, placer_layers, w_out, b_out, dlogits, *, fanout,
-                    nb_seed, n_heads, seg_len, mem_len, film=True, attention=True):
+                    nb_seed, n_heads, seg_len, mem_len, film=True, attention=True, decisions=None):
     """The whole chain in one graph: gradient of sum(dlogits * logits) with
-    respect to every weight of the GNN, the placer and the head."""
+    respect to every weight of the GNN, the placer and the head.
+
+    decisions (optional) fixes the forward's discrete choices -- each ReLU's
+    sign and each max-pool element's winning neighbour -- to those of another
+    run: {"gnn": [(arg, mask)] per GNN layer, "ffn": [mask] per placer layer}.
+    Where a pre-activation lies within rounding of zero, or two neighbours
+    within rounding of each other, the two runs may decide differently, and
+    the gradient jumps there; with the same decisions the comparison measures
+    the arithmetic alone."""
     S = O.sample_neighbours(O.neighbour_lists(row_ptr, col_idx), graph_ptr, fanout, nb_seed)
     gnn = _leaves(gnn_layers)
     pl = _leaves(placer_layers)
     hd = {"w_out": _t(w_out, True), "b_out": _t(b_out, True)}
-    h = _gnn_forward(_t(x), S, gnn)
+    dec = decisions or {}
+    h = _gnn_forward(_t(x), S, gnn, dec.get("gnn"))
     G = len(graph_ptr) - 1
     x0 = torch.stack([h[graph_ptr[g]:graph_ptr[g + 1]].mean(dim=0) for g in range(G)])
-    logits = _placer_forward(h, x0, graph_ptr, pl, hd, n_heads, seg_len, mem_len, film, attention)
+    logits = _placer_forward(h, x0, graph_ptr, pl, hd, n_heads, seg_len, mem_len, film, attention, dec.get("ffn"))
     (logits * _t(dlogits)).sum().backward()
     return {"logits": logits.detach().numpy(), "gnn": _grads(gnn), "placer": _grads(pl),
             "head": {k: v.grad.numpy().copy() for k, v in hd.items()}}

@@ -27,7 +27,7 @@ DEVICE = [f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang", "-p
 # avoids a copy to and from the accumulation registers around each use.
 FILE_FLAGS = {"attention.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form", "-Wno-pass-failed"]}
 
-SOURCES = ["graph_kernels.hip", "gemm.hip", "layer.hip", "attention.hip", "placer_kernels.hip", "sample.hip", "ppo.hip", "evaluate.hip",
+SOURCES = ["graph_kernels.hip", "gemm.hip", "layer.hip", "attention.hip", "placer_kernels.hip", "sample.hip", "ppo.hip", "evaluate.hip", "train.hip",
            "gdp_api.hip", "host_plan.cpp"]
 
 

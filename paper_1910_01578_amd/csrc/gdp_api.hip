@@ -11,6 +11,7 @@
 #include "gdp.h"
 #include "host_plan.h"
 #include "kernels.h"
+#include "train_kernels.h"
 
 namespace gdp {
 
@@ -71,14 +72,14 @@ static int hip_fail(hipError_t e, const char* what) {
   return fail(GDP_E_HIP, "%s: %s", what, hipGetErrorString(e));
 }
 
-#define GDP_LAUNCH(kind, call)                      \
-  do {                                              \
-    hipError_t _e;                                  \
-    {                                               \
-      Timed _t((kind), st);                         \
-      _e = (call);                                  \
-    }                                               \
-    if (_e != hipSuccess) return hip_fail(_e, #call); \
+#define GDP_LAUNCH(kind, ...)                                    \
+  do {                                                           \
+    hipError_t _e;                                               \
+    {                                                            \
+      Timed _t((kind), st);                                      \
+      _e = (__VA_ARGS__);                                        \
+    }                                                            \
+    if (_e != hipSuccess) return hip_fail(_e, #__VA_ARGS__);     \
   } while (0)
 
 static GraphTable make_table(const gdp_graph* g) {
@@ -592,6 +593,528 @@ extern "C" int gdp_evaluate(const gdp_graph* g, int32_t n_devices, int32_t k_sam
   return GDP_OK;
 }
 
+// ===========================================================================
+// The update step: training forward (all intermediates kept), backward, Adam.
+// ===========================================================================
+namespace gdp {
+namespace {
+
+inline void set_bias(tr::GemmStrided<float, float>& g, const float* b) { g.bias_f = b; }
+inline void set_bias(tr::GemmStrided<bf16, bf16>& g, const bf16* b) { g.bias_h = b; }
+inline void set_bias(tr::GemmStrided<float, bf16>& g, const bf16* b) { g.bias_h = b; }
+inline void set_bias(tr::GemmStrided<bf16, float>& g, const float* b) { g.bias_f = b; }
+
+struct TrainCtx {
+  hipStream_t st;
+  float* partial;          // split-k sums
+  size_t partial_floats;
+  float* colpart;          // column-sum partials
+  GraphTable rows;         // all rows as one segment (256-row chunks in blk)
+  int row_chunks;
+  GraphTable graphs;       // the graphs, each in 256-row chunks
+  int graph_chunks;
+};
+
+// C[M, N] (+)= act(A[M, K] W[N, K]^T + bias): a linear layer on row-major activations.
+template <typename TA, typename TW>
+hipError_t lin(const TA* A, int lda, const TW* W, int ldw, const TW* bias, int M, int N, int K, float* C, int ldc,
+               int act, bool acc, const TrainCtx& cx) {
+  tr::GemmStrided<TA, TW> g;
+  g.a = A; g.sam = lda; g.sak = 1;
+  g.b = W; g.sbk = 1; g.sbn = ldw;
+  g.M = M; g.N = N; g.K = K;
+  g.c = C; g.ldc = ldc;
+  if (bias) set_bias(g, bias);
+  g.act = act;
+  g.accumulate = acc;
+  return tr::launch_gemm_strided(g, nullptr, 0, cx.st);
+}
+
+// C[M, N] (+)= (dY[M, K] W[K, N]) masked where mask <= 0: a linear layer's input gradient.
+template <typename TW>
+hipError_t lin_dx(const float* dY, int ldy, const TW* W, int ldw, int M, int N, int K, float* C, int ldc,
+                  const float* mask, int ldm, bool acc, const TrainCtx& cx) {
+  tr::GemmStrided<float, TW> g;
+  g.a = dY; g.sam = ldy; g.sak = 1;
+  g.b = W; g.sbk = ldw; g.sbn = 1;
+  g.M = M; g.N = N; g.K = K;
+  g.c = C; g.ldc = ldc;
+  g.mask = mask; g.ldm = ldm;
+  g.accumulate = acc;
+  return tr::launch_gemm_strided(g, nullptr, 0, cx.st);
+}
+
+// dW[M, N] (+)= sum over rows r of dY[r][m] X[r][n]: a linear layer's weight gradient.
+template <typename TX>
+hipError_t lin_dw(const float* dY, int ldy, const TX* X, int ldx, int M, int N, int rows, float* C, int ldc, bool acc,
+                  const TrainCtx& cx) {
+  tr::GemmStrided<float, TX> g;
+  g.a = dY; g.sam = 1; g.sak = ldy;
+  g.b = X; g.sbk = ldx; g.sbn = 1;
+  g.M = M; g.N = N; g.K = rows;
+  g.c = C; g.ldc = ldc;
+  g.accumulate = acc;
+  return tr::launch_gemm_strided(g, cx.partial, cx.partial_floats, cx.st);
+}
+
+// out[c] (+)= sum over all rows of a[r][c] (* b[r][c])
+template <typename TA>
+hipError_t colsum(const TA* a, int lda, const float* b, int ldb, int C, float* out, bool acc, const TrainCtx& cx) {
+  return tr::launch_colsum(a, lda, b, ldb, C, cx.rows, cx.row_chunks, cx.colpart, out, 0, acc, cx.st);
+}
+
+GraphTable one_segment(int rows, int chunk_rows, int* chunks) {
+  GraphTable t;
+  memset(&t, 0, sizeof(t));
+  t.n = 1;
+  t.ptr[0] = 0;
+  t.ptr[1] = rows;
+  t.blk[0] = 0;
+  t.blk[1] = (rows + chunk_rows - 1) / chunk_rows;
+  *chunks = t.blk[1];
+  return t;
+}
+
+template <typename T>
+int train_forward_impl(const gdp_graph* g, const gdp_gnn* gnn, const gdp_placer* p, const TrainPlan& tp, char* store,
+                       char* ws, float* logits, float* lse, hipStream_t st) {
+  const int N = g->n_nodes, G = g->n_graphs, H = gnn->hidden, d = p->d_model, dff = p->d_ff, F = g->feat_dim;
+  const GraphTable gt = make_table(g);
+  TrainCtx cx;
+  cx.st = st;
+  auto S = [&](size_t off) { return reinterpret_cast<float*>(store + off); };
+  auto SI = [&](size_t off) { return reinterpret_cast<int*>(store + off); };
+  // neighbourhoods and their sample (as gdp_embed), in-edge rows sorted
+  {
+    int* counters = reinterpret_cast<int*>(ws + tp.counters);
+    int* in_ptr = SI(tp.in_ptr);
+    int* in_idx = SI(tp.in_idx);
+    GDP_LAUNCH(GDP_K_TRAIN_FWD, launch_fill_i32(counters, 2 * (int64_t)N + 1, 0, st));
+    GDP_LAUNCH(GDP_K_TRAIN_FWD, launch_in_degree(g->col_idx, g->n_edges, counters, st));
+    GDP_LAUNCH(GDP_K_TRAIN_FWD, launch_scan_degrees(g->row_ptr, counters, N, gnn->fanout, in_ptr, SI(tp.s_ptr),
+                                                    reinterpret_cast<int*>(ws + tp.scan_tmp), st));
+    GDP_LAUNCH(GDP_K_TRAIN_FWD, launch_fill_reverse(g->row_ptr, g->col_idx, in_ptr, N, g->n_edges, counters + N, in_idx,
+                                                    st));
+    GDP_LAUNCH(GDP_K_TRAIN_FWD, launch_nbr_sample(g->row_ptr, g->col_idx, in_ptr, in_idx, SI(tp.s_ptr), N, gnn->fanout,
+                                                  gnn->nbr_seed, gt, SI(tp.s_idx), reinterpret_cast<int*>(ws + tp.heavy),
+                                                  counters + 2 * N, st));
+    GDP_LAUNCH(GDP_K_TRAIN_FWD, tr::launch_sort_rows(in_ptr, N, in_idx, st));
+  }
+  // Eq. 2 and Eq. 3
+  const T* x = static_cast<const T*>(g->x);
+  for (int l = 0; l < gnn->n_layers; ++l) {
+    const gdp_gnn_layer& Lw = gnn->layers[l];
+    float* P = S(tp.P[l]);
+    float* A = S(tp.A[l]);
+    float* hout = S(tp.h[l + 1]);
+    const T* wp = static_cast<const T*>(Lw.w_pool);
+    const T* ws_ = static_cast<const T*>(Lw.w_self);
+    if (l == 0) {
+      GDP_LAUNCH(GDP_K_TRAIN_FWD, lin<T, T>(x, F, wp, F, static_cast<const T*>(Lw.b_pool), N, H, F, P, H,
+                                            tr::ACT_SIGMOID, false, cx));
+    } else {
+      GDP_LAUNCH(GDP_K_TRAIN_FWD, lin<float, T>(S(tp.h[l]), H, wp, H, static_cast<const T*>(Lw.b_pool), N, H, H, P, H,
+                                                tr::ACT_SIGMOID, false, cx));
+    }
+    GDP_LAUNCH(GDP_K_TRAIN_FWD, tr::launch_gather_max_arg(P, SI(tp.s_ptr), SI(tp.s_idx), N, H, A, SI(tp.arg[l]), st));
+    if (l == 0) {
+      GDP_LAUNCH(GDP_K_TRAIN_FWD, lin<T, T>(x, F, ws_, F, static_cast<const T*>(Lw.b_upd), N, H, F, hout, H,
+                                            tr::ACT_NONE, false, cx));
+    } else {
+      GDP_LAUNCH(GDP_K_TRAIN_FWD, lin<float, T>(S(tp.h[l]), H, ws_, H, static_cast<const T*>(Lw.b_upd), N, H, H, hout,
+                                                H, tr::ACT_NONE, false, cx));
+    }
+    GDP_LAUNCH(GDP_K_TRAIN_FWD, lin<float, T>(A, H, static_cast<const T*>(Lw.w_neigh), H, nullptr, N, H, H, hout, H,
+                                              tr::ACT_NONE, true, cx));
+    GDP_LAUNCH(GDP_K_TRAIN_FWD, tr::launch_ew(tr::EW_MASK_POS, hout, hout, nullptr, (size_t)N * H, hout, st));
+  }
+  float* x0 = S(tp.x0);
+  GDP_LAUNCH(GDP_K_TRAIN_FWD, tr::launch_meanpool_f32(S(tp.h[gnn->n_layers]), H, gt, x0, st));
+  // Eq. 4: gamma, beta of every layer
+  float* film = S(tp.film);
+  if (p->film) {
+    for (int l0 = 0; l0 < p->n_layers; l0 += kFilmLayersPerLaunch) {
+      const int nl = std::min(kFilmLayersPerLaunch, p->n_layers - l0);
+      FilmLayers<T> fw;
+      for (int i = 0; i < nl; ++i) {
+        const gdp_placer_layer& Ly = p->layers[l0 + i];
+        fw.wg[i] = static_cast<const T*>(Ly.film_wg);
+        fw.bg[i] = static_cast<const T*>(Ly.film_bg);
+        fw.wb[i] = static_cast<const T*>(Ly.film_wb);
+        fw.bb[i] = static_cast<const T*>(Ly.film_bb);
+      }
+      GDP_LAUNCH(GDP_K_TRAIN_FWD, launch_film_gemv<T>(fw, nl, x0, G, d, H, film + (size_t)l0 * 2 * G * d, st));
+    }
+  }
+  // the placer
+  for (int l = 0; l < p->n_layers; ++l) {
+    const gdp_placer_layer& Ly = p->layers[l];
+    const float* X = S(tp.X[l]);
+    float* Y = S(tp.Y[l]);
+    const float* gam = p->film ? film + (size_t)l * 2 * G * d : nullptr;
+    const float* bet = p->film ? gam + (size_t)G * d : nullptr;
+    GDP_LAUNCH(GDP_K_TRAIN_FWD, tr::launch_film_apply<float>(X, N, d, gam, bet, gt, Y, st));
+    const float* ffn_in = Y;
+    if (p->attention) {
+      float* qkv = S(tp.QKV[l]);
+      float* O = S(tp.O[l]);
+      float* R1 = S(tp.R1[l]);
+      float* Z = S(tp.Z[l]);
+      GDP_LAUNCH(GDP_K_TRAIN_FWD, lin<float, T>(Y, d, static_cast<const T*>(Ly.w_qkv), d,
+                                                static_cast<const T*>(Ly.b_qkv), N, 3 * d, d, qkv, 3 * d, tr::ACT_NONE,
+                                                false, cx));
+      GDP_LAUNCH(GDP_K_TRAIN_FWD, tr::launch_attn_fwd(qkv, N, d, p->n_heads, p->seg_len, p->mem_len, gt, O,
+                                                      S(tp.lse_att[l]), st));
+      GDP_LAUNCH(GDP_K_TRAIN_FWD, lin<float, T>(O, d, static_cast<const T*>(Ly.w_o), d, static_cast<const T*>(Ly.b_o),
+                                                N, d, d, R1, d, tr::ACT_NONE, false, cx));
+      GDP_LAUNCH(GDP_K_TRAIN_FWD, tr::launch_ew(tr::EW_ADD, R1, Y, nullptr, (size_t)N * d, R1, st));
+      GDP_LAUNCH(GDP_K_TRAIN_FWD, tr::launch_ln_fwd<T>(R1, N, d, static_cast<const T*>(Ly.ln1_g),
+                                                       static_cast<const T*>(Ly.ln1_b), Z, st));
+      ffn_in = Z;
+    }
+    float* H1 = S(tp.H1[l]);
+    float* R2 = S(tp.R2[l]);
+    GDP_LAUNCH(GDP_K_TRAIN_FWD, lin<float, T>(ffn_in, d, static_cast<const T*>(Ly.w_1), d,
+                                              static_cast<const T*>(Ly.b_1), N, dff, d, H1, dff, tr::ACT_RELU, false,
+                                              cx));
+    GDP_LAUNCH(GDP_K_TRAIN_FWD, lin<float, T>(H1, dff, static_cast<const T*>(Ly.w_2), dff,
+                                              static_cast<const T*>(Ly.b_2), N, d, dff, R2, d, tr::ACT_NONE, false,
+                                              cx));
+    GDP_LAUNCH(GDP_K_TRAIN_FWD, tr::launch_ew(tr::EW_ADD, R2, ffn_in, nullptr, (size_t)N * d, R2, st));
+    GDP_LAUNCH(GDP_K_TRAIN_FWD, tr::launch_ln_fwd<T>(R2, N, d, static_cast<const T*>(Ly.ln2_g),
+                                                     static_cast<const T*>(Ly.ln2_b), S(tp.X[l + 1]), st));
+  }
+  GDP_LAUNCH(GDP_K_TRAIN_FWD, launch_head<T>(S(tp.X[p->n_layers]), static_cast<const T*>(p->w_out),
+                                             static_cast<const T*>(p->b_out), N, d, p->n_devices, logits, lse, st));
+  return GDP_OK;
+}
+
+template <typename T>
+int backward_impl(const gdp_graph* g, const gdp_gnn* gnn, const gdp_placer* p, const TrainPlan& tp,
+                  const char* store, char* ws, const float* dlogits, const gdp_grads* gr, hipStream_t st) {
+  const int N = g->n_nodes, G = g->n_graphs, H = gnn->hidden, d = p->d_model, dff = p->d_ff, F = g->feat_dim;
+  const GraphTable gt = make_table(g);
+  auto S = [&](size_t off) { return reinterpret_cast<const float*>(store + off); };
+  auto SI = [&](size_t off) { return reinterpret_cast<const int*>(store + off); };
+  auto W = [&](size_t off) { return reinterpret_cast<float*>(ws + off); };
+  TrainCtx cx;
+  cx.st = st;
+  cx.partial = W(tp.gemm_partial);
+  cx.partial_floats = tp.gemm_partial_floats;
+  cx.colpart = W(tp.colpart);
+  cx.rows = one_segment(N, tr::kColChunkRows, &cx.row_chunks);
+  cx.graphs = make_table(g);
+  cx.graph_chunks = prefix_blocks_rows(g->graph_ptr_h, G, tr::kColChunkRows, cx.graphs.blk);
+  float* dX = W(tp.dX);
+  float* dY = W(tp.dY);
+  float* dR = W(tp.dR);
+  float* dZ = W(tp.dZ);
+  float* xg = W(tp.xg);
+  float* dH = W(tp.dH);
+  // the head
+  GDP_LAUNCH(GDP_K_BACKWARD, launch_head_backward<T>(S(tp.X[p->n_layers]), static_cast<const T*>(p->w_out), dlogits, N,
+                                                     d, p->n_devices, dX, gr->w_out, gr->b_out, W(tp.head_partial), st));
+  const float* film = S(tp.film);
+  float* dfilm = W(tp.dfilm);
+  for (int l = p->n_layers - 1; l >= 0; --l) {
+    const gdp_placer_layer& Ly = p->layers[l];
+    const gdp_placer_layer_grad& Gl = gr->placer[l];
+    const float* Xin = S(tp.X[l]);
+    const float* Y = S(tp.Y[l]);
+    const float* ffn_in = p->attention ? S(tp.Z[l]) : Y;
+    // LN2, the FFN and its residual: dZ = dR2 + dH W_1
+    GDP_LAUNCH(GDP_K_BACKWARD, tr::launch_ln_bwd<T>(S(tp.R2[l]), dX, N, d, static_cast<const T*>(Ly.ln2_g), dR, xg, st));
+    GDP_LAUNCH(GDP_K_BACKWARD, colsum<float>(xg, d, nullptr, 0, d, Gl.ln2_g, false, cx));
+    GDP_LAUNCH(GDP_K_BACKWARD, colsum<float>(dX, d, nullptr, 0, d, Gl.ln2_b, false, cx));
+    GDP_LAUNCH(GDP_K_BACKWARD, lin_dx<T>(dR, d, static_cast<const T*>(Ly.w_2), dff, N, dff, d, dH, dff, S(tp.H1[l]),
+                                         dff, false, cx));
+    GDP_LAUNCH(GDP_K_BACKWARD, lin_dw<float>(dR, d, S(tp.H1[l]), dff, d, dff, N, Gl.w_2, dff, false, cx));
+    GDP_LAUNCH(GDP_K_BACKWARD, colsum<float>(dR, d, nullptr, 0, d, Gl.b_2, false, cx));
+    GDP_LAUNCH(GDP_K_BACKWARD, lin_dx<T>(dH, dff, static_cast<const T*>(Ly.w_1), d, N, d, dff, dZ, d, nullptr, 0, false,
+                                         cx));
+    GDP_LAUNCH(GDP_K_BACKWARD, tr::launch_ew(tr::EW_ADD, dZ, dR, nullptr, (size_t)N * d, dZ, st));
+    GDP_LAUNCH(GDP_K_BACKWARD, lin_dw<float>(dH, dff, ffn_in, d, dff, d, N, Gl.w_1, d, false, cx));
+    GDP_LAUNCH(GDP_K_BACKWARD, colsum<float>(dH, dff, nullptr, 0, dff, Gl.b_1, false, cx));
+    const float* dYp = dZ;   // the gradient reaching Y
+    if (p->attention) {
+      const float* O = S(tp.O[l]);
+      const float* qkv = S(tp.QKV[l]);
+      float* dqkv = W(tp.dqkv);
+      float* dkvm = W(tp.dkvm);
+      // LN1 and the out-projection: dR = dR1, dO (in dX, free now)
+      GDP_LAUNCH(GDP_K_BACKWARD, tr::launch_ln_bwd<T>(S(tp.R1[l]), dZ, N, d, static_cast<const T*>(Ly.ln1_g), dR, xg,
+                                                      st));
+      GDP_LAUNCH(GDP_K_BACKWARD, colsum<float>(xg, d, nullptr, 0, d, Gl.ln1_g, false, cx));
+      GDP_LAUNCH(GDP_K_BACKWARD, colsum<float>(dZ, d, nullptr, 0, d, Gl.ln1_b, false, cx));
+      GDP_LAUNCH(GDP_K_BACKWARD, lin_dx<T>(dR, d, static_cast<const T*>(Ly.w_o), d, N, d, d, dX, d, nullptr, 0, false,
+                                           cx));
+      GDP_LAUNCH(GDP_K_BACKWARD, lin_dw<float>(dR, d, O, d, d, d, N, Gl.w_o, d, false, cx));
+      GDP_LAUNCH(GDP_K_BACKWARD, colsum<float>(dR, d, nullptr, 0, d, Gl.b_o, false, cx));
+      // attention: own-segment (live) and memory parts of dK, dV
+      GDP_LAUNCH(GDP_K_BACKWARD, tr::launch_attn_bwd(qkv, O, dX, S(tp.lse_att[l]), N, d, p->n_heads, p->seg_len,
+                                                     p->mem_len, gt, W(tp.Dq), dqkv, dkvm, st));
+      GDP_LAUNCH(GDP_K_BACKWARD, lin_dw<float>(dqkv, 3 * d, Y, d, 3 * d, d, N, Gl.w_qkv, d, false, cx));
+      GDP_LAUNCH(GDP_K_BACKWARD, lin_dw<float>(dkvm, 2 * d, Y, d, 2 * d, d, N, Gl.w_qkv + (size_t)d * d, d, true, cx));
+      GDP_LAUNCH(GDP_K_BACKWARD, colsum<float>(dqkv, 3 * d, nullptr, 0, 3 * d, Gl.b_qkv, false, cx));
+      GDP_LAUNCH(GDP_K_BACKWARD, colsum<float>(dkvm, 2 * d, nullptr, 0, 2 * d, Gl.b_qkv + d, true, cx));
+      // dY = dR1 + [dQ | dK | dV]_live W_qkv (the memory's part stops at the weights)
+      GDP_LAUNCH(GDP_K_BACKWARD, lin_dx<T>(dqkv, 3 * d, static_cast<const T*>(Ly.w_qkv), d, N, d, 3 * d, dY, d, nullptr,
+                                           0, false, cx));
+      GDP_LAUNCH(GDP_K_BACKWARD, tr::launch_ew(tr::EW_ADD, dY, dR, nullptr, (size_t)N * d, dY, st));
+      dYp = dY;
+    }
+    // FiLM: dX = gamma dY; dgamma[g] = sum_g dY X, dbeta[g] = sum_g dY
+    if (p->film) {
+      const float* gam = film + (size_t)l * 2 * G * d;
+      float* dg = dfilm + (size_t)l * 2 * G * d;
+      GDP_LAUNCH(GDP_K_BACKWARD, tr::launch_film_dx(dYp, N, d, gam, gt, dX, st));
+      GDP_LAUNCH(GDP_K_BACKWARD, tr::launch_colsum<float>(dYp, d, Xin, d, d, cx.graphs, cx.graph_chunks, cx.colpart, dg,
+                                                          d, false, st));
+      GDP_LAUNCH(GDP_K_BACKWARD, tr::launch_colsum<float>(dYp, d, nullptr, 0, d, cx.graphs, cx.graph_chunks, cx.colpart,
+                                                          dg + (size_t)G * d, d, false, st));
+    } else {
+      GDP_LAUNCH(GDP_K_BACKWARD, tr::launch_film_dx(dYp, N, d, nullptr, gt, dX, st));
+    }
+  }
+  // FiLM weights and the graph embeddings' gradient dx0 [G, H]
+  float* dx0 = W(tp.dx0);
+  GDP_LAUNCH(GDP_K_BACKWARD, launch_fill_i32(reinterpret_cast<int*>(dx0), (int64_t)G * H, 0, st));
+  if (p->film) {
+    int gch = 0;
+    const GraphTable grows = one_segment(G, tr::kColChunkRows, &gch);
+    const float* x0 = S(tp.x0);
+    for (int l = 0; l < p->n_layers; ++l) {
+      const gdp_placer_layer& Ly = p->layers[l];
+      const gdp_placer_layer_grad& Gl = gr->placer[l];
+      const float* dg = dfilm + (size_t)l * 2 * G * d;
+      const float* db = dg + (size_t)G * d;
+      GDP_LAUNCH(GDP_K_BACKWARD, lin_dw<float>(dg, d, x0, H, d, H, G, Gl.film_wg, H, false, cx));
+      GDP_LAUNCH(GDP_K_BACKWARD, lin_dw<float>(db, d, x0, H, d, H, G, Gl.film_wb, H, false, cx));
+      GDP_LAUNCH(GDP_K_BACKWARD, tr::launch_colsum<float>(dg, d, nullptr, 0, d, grows, gch, cx.colpart, Gl.film_bg, 0,
+                                                          false, st));
+      GDP_LAUNCH(GDP_K_BACKWARD, tr::launch_colsum<float>(db, d, nullptr, 0, d, grows, gch, cx.colpart, Gl.film_bb, 0,
+                                                          false, st));
+      GDP_LAUNCH(GDP_K_BACKWARD, lin_dx<T>(dg, d, static_cast<const T*>(Ly.film_wg), H, G, H, d, dx0, H, nullptr, 0,
+                                           true, cx));
+      GDP_LAUNCH(GDP_K_BACKWARD, lin_dx<T>(db, d, static_cast<const T*>(Ly.film_wb), H, G, H, d, dx0, H, nullptr, 0,
+                                           true, cx));
+    }
+  }
+  // the GNN: dh of the final embeddings = the placer's input gradient + the mean pool's share of dx0
+  GDP_LAUNCH(GDP_K_BACKWARD, tr::launch_meanpool_bwd(dx0, N, H, gt, dX, st));
+  float* dh_cur = dX;
+  float* dh_next = W(tp.dh);
+  float* dU = W(tp.dU);
+  float* dA = W(tp.dA);
+  float* dP = W(tp.dP);
+  const T* x = static_cast<const T*>(g->x);
+  for (int l = gnn->n_layers - 1; l >= 0; --l) {
+    const gdp_gnn_layer& Lw = gnn->layers[l];
+    const gdp_gnn_layer_grad& Gl = gr->gnn[l];
+    const int hin = l == 0 ? F : H;
+    GDP_LAUNCH(GDP_K_BACKWARD, tr::launch_ew(tr::EW_MASK_POS, dh_cur, S(tp.h[l + 1]), nullptr, (size_t)N * H, dU, st));
+    if (l == 0) {
+      GDP_LAUNCH(GDP_K_BACKWARD, lin_dw<T>(dU, H, x, F, H, F, N, Gl.w_self, F, false, cx));
+    } else {
+      GDP_LAUNCH(GDP_K_BACKWARD, lin_dw<float>(dU, H, S(tp.h[l]), H, H, H, N, Gl.w_self, H, false, cx));
+    }
+    GDP_LAUNCH(GDP_K_BACKWARD, lin_dw<float>(dU, H, S(tp.A[l]), H, H, H, N, Gl.w_neigh, H, false, cx));
+    GDP_LAUNCH(GDP_K_BACKWARD, colsum<float>(dU, H, nullptr, 0, H, Gl.b_upd, false, cx));
+    GDP_LAUNCH(GDP_K_BACKWARD, lin_dx<T>(dU, H, static_cast<const T*>(Lw.w_neigh), H, N, H, H, dA, H, nullptr, 0, false,
+                                         cx));
+    GDP_LAUNCH(GDP_K_BACKWARD, tr::launch_gather_max_bwd(dA, SI(tp.arg[l]), g->row_ptr, g->col_idx, SI(tp.in_ptr),
+                                                         SI(tp.in_idx), N, H, dP, st));
+    GDP_LAUNCH(GDP_K_BACKWARD, tr::launch_ew(tr::EW_SIGMOID_GRAD, dP, S(tp.P[l]), nullptr, (size_t)N * H, dP, st));
+    if (l == 0) {
+      GDP_LAUNCH(GDP_K_BACKWARD, lin_dw<T>(dP, H, x, F, H, F, N, Gl.w_pool, F, false, cx));
+    } else {
+      GDP_LAUNCH(GDP_K_BACKWARD, lin_dw<float>(dP, H, S(tp.h[l]), H, H, H, N, Gl.w_pool, H, false, cx));
+    }
+    GDP_LAUNCH(GDP_K_BACKWARD, colsum<float>(dP, H, nullptr, 0, H, Gl.b_pool, false, cx));
+    if (l > 0) {
+      GDP_LAUNCH(GDP_K_BACKWARD, lin_dx<T>(dU, H, static_cast<const T*>(Lw.w_self), hin, N, hin, H, dh_next, hin,
+                                           nullptr, 0, false, cx));
+      GDP_LAUNCH(GDP_K_BACKWARD, lin_dx<T>(dP, H, static_cast<const T*>(Lw.w_pool), hin, N, hin, H, dh_next, hin,
+                                           nullptr, 0, true, cx));
+      std::swap(dh_cur, dh_next);
+    }
+  }
+  return GDP_OK;
+}
+
+int check_grads(const gdp_gnn* gnn, const gdp_placer* p, const gdp_grads* gr) {
+  if (!gr || !gr->gnn || !gr->placer || !gr->w_out || !gr->b_out) return fail(GDP_E_INVALID_ARG, "grads has a NULL array");
+  for (int l = 0; l < gnn->n_layers; ++l) {
+    const gdp_gnn_layer_grad& G = gr->gnn[l];
+    if (!G.w_pool || !G.b_pool || !G.w_self || !G.w_neigh || !G.b_upd)
+      return fail(GDP_E_INVALID_ARG, "grads: GNN layer %d has a NULL array", l);
+  }
+  for (int l = 0; l < p->n_layers; ++l) {
+    const gdp_placer_layer_grad& G = gr->placer[l];
+    if (!G.w_1 || !G.b_1 || !G.w_2 || !G.b_2 || !G.ln2_g || !G.ln2_b)
+      return fail(GDP_E_INVALID_ARG, "grads: placer layer %d has a NULL array", l);
+    if (p->attention && (!G.w_qkv || !G.b_qkv || !G.w_o || !G.b_o || !G.ln1_g || !G.ln1_b))
+      return fail(GDP_E_INVALID_ARG, "grads: placer layer %d has a NULL attention array", l);
+    if (p->film && (!G.film_wg || !G.film_bg || !G.film_wb || !G.film_bb))
+      return fail(GDP_E_INVALID_ARG, "grads: placer layer %d has a NULL FiLM array", l);
+  }
+  return GDP_OK;
+}
+
+}  // namespace
+}  // namespace gdp
+
+extern "C" int gdp_train_sizes(const gdp_graph* g, const gdp_gnn* gnn, const gdp_placer* placer, size_t* store_bytes,
+                               size_t* workspace_bytes) {
+  clear_error();
+  if (store_bytes) *store_bytes = 0;
+  if (workspace_bytes) *workspace_bytes = 0;
+  int r;
+  if ((r = check_graph(g)) != GDP_OK) return r;
+  if ((r = check_train(g, gnn, placer)) != GDP_OK) return r;
+  if (!store_bytes || !workspace_bytes) return fail(GDP_E_INVALID_ARG, "store_bytes or workspace_bytes is NULL");
+  TrainPlan tp;
+  plan_train(g, gnn, placer, &tp);
+  *store_bytes = tp.store_total;
+  *workspace_bytes = tp.ws_total;
+  return GDP_OK;
+}
+
+static int check_store(const void* store, size_t have, size_t need) {
+  if (!store) return fail(GDP_E_INVALID_ARG, "store is NULL");
+  if (have < need) return fail(GDP_E_WORKSPACE, "store %zu bytes < %zu required", have, need);
+  if (((uintptr_t)store & 255u) != 0) return fail(GDP_E_INVALID_ARG, "store must be 256-byte aligned");
+  return GDP_OK;
+}
+
+extern "C" int gdp_forward_train(const gdp_graph* g, const gdp_gnn* gnn, const gdp_placer* placer, void* store,
+                                 size_t store_bytes, float* logits, float* lse, void* ws, size_t ws_bytes,
+                                 void* stream) {
+  clear_error();
+  int r;
+  if ((r = check_graph(g)) != GDP_OK) return r;
+  if ((r = check_train(g, gnn, placer)) != GDP_OK) return r;
+  if (!logits) return fail(GDP_E_INVALID_ARG, "logits is NULL");
+  TrainPlan tp;
+  plan_train(g, gnn, placer, &tp);
+  if ((r = check_store(store, store_bytes, tp.store_total)) != GDP_OK) return r;
+  if ((r = check_ws(ws, ws_bytes, tp.ws_total)) != GDP_OK) return r;
+  if ((r = pending_hip_error()) != GDP_OK) return r;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (g->dtype == GDP_BF16)
+    return train_forward_impl<bf16>(g, gnn, placer, tp, static_cast<char*>(store), static_cast<char*>(ws), logits, lse,
+                                    st);
+  return train_forward_impl<float>(g, gnn, placer, tp, static_cast<char*>(store), static_cast<char*>(ws), logits, lse,
+                                   st);
+}
+
+extern "C" int gdp_backward(const gdp_graph* g, const gdp_gnn* gnn, const gdp_placer* placer, const void* store,
+                            size_t store_bytes, const float* dlogits, const gdp_grads* grads, void* ws, size_t ws_bytes,
+                            void* stream) {
+  clear_error();
+  int r;
+  if ((r = check_graph(g)) != GDP_OK) return r;
+  if ((r = check_train(g, gnn, placer)) != GDP_OK) return r;
+  if (!dlogits) return fail(GDP_E_INVALID_ARG, "dlogits is NULL");
+  if ((r = check_grads(gnn, placer, grads)) != GDP_OK) return r;
+  TrainPlan tp;
+  plan_train(g, gnn, placer, &tp);
+  if ((r = check_store(store, store_bytes, tp.store_total)) != GDP_OK) return r;
+  if ((r = check_ws(ws, ws_bytes, tp.ws_total)) != GDP_OK) return r;
+  if ((r = pending_hip_error()) != GDP_OK) return r;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (g->dtype == GDP_BF16)
+    return backward_impl<bf16>(g, gnn, placer, tp, static_cast<const char*>(store), static_cast<char*>(ws), dlogits,
+                               grads, st);
+  return backward_impl<float>(g, gnn, placer, tp, static_cast<const char*>(store), static_cast<char*>(ws), dlogits,
+                              grads, st);
+}
+
+extern "C" int gdp_log_prob(const gdp_graph* g, const float* logits, const float* lse, int32_t n_devices,
+                            int32_t k_samples, const int32_t* placements, float* logp, void* ws, size_t ws_bytes,
+                            void* stream) {
+  clear_error();
+  int r;
+  if ((r = check_graph(g)) != GDP_OK) return r;
+  if ((r = check_sample(g, n_devices, k_samples)) != GDP_OK) return r;
+  if (!logits || !placements || !logp) return fail(GDP_E_INVALID_ARG, "logits, placements or logp is NULL");
+  SamplePlan pl;
+  plan_sample(g, k_samples, &pl);
+  if ((r = check_ws(ws, ws_bytes, pl.c.total)) != GDP_OK) return r;
+  if ((r = pending_hip_error()) != GDP_OK) return r;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  GraphTable ct = make_table(g);
+  const int chunks = prefix_blocks_rows(g->graph_ptr_h, g->n_graphs, kSampleRows, ct.blk);
+  float* partial = at<float>(ws, pl.partial);
+  GDP_LAUNCH(GDP_K_LOGPROB, launch_logp_given(logits, lse, g->n_nodes, n_devices, k_samples, placements, ct, chunks,
+                                              partial, st));
+  GDP_LAUNCH(GDP_K_LOGPROB, launch_logp_reduce(partial, ct, chunks, k_samples, logp, st));
+  return GDP_OK;
+}
+
+extern "C" int gdp_adam_step(int32_t n_tensors, const gdp_adam_tensor* tensors, int32_t dtype, float lr, float beta1,
+                             float beta2, float eps, int64_t step, void* stream) {
+  clear_error();
+  if (n_tensors < 0 || (n_tensors > 0 && !tensors)) return fail(GDP_E_INVALID_ARG, "tensors is NULL");
+  if (dtype != GDP_F32 && dtype != GDP_BF16) return fail(GDP_E_INVALID_ARG, "dtype = %d", dtype);
+  if (step < 1) return fail(GDP_E_INVALID_ARG, "step = %lld < 1", (long long)step);
+  if (!(lr >= 0.f) || !(beta1 >= 0.f && beta1 < 1.f) || !(beta2 >= 0.f && beta2 < 1.f) || !(eps > 0.f))
+    return fail(GDP_E_INVALID_ARG, "bad Adam hyper-parameters");
+  for (int i = 0; i < n_tensors; ++i) {
+    const gdp_adam_tensor& t = tensors[i];
+    if (t.n < 0) return fail(GDP_E_INVALID_ARG, "tensor %d: n < 0", i);
+    if (t.n > 0 && (!t.param || !t.master || !t.grad || !t.m || !t.v))
+      return fail(GDP_E_INVALID_ARG, "tensor %d has a NULL array", i);
+  }
+  int r;
+  if ((r = pending_hip_error()) != GDP_OK) return r;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const float c1 = (float)(1.0 - pow((double)beta1, (double)step));
+  const float c2 = (float)(1.0 - pow((double)beta2, (double)step));
+  for (int i = 0; i < n_tensors; ++i) {
+    const gdp_adam_tensor& t = tensors[i];
+    if (t.n == 0) continue;
+    if (dtype == GDP_BF16)
+      GDP_LAUNCH(GDP_K_ADAM, tr::launch_adam<bf16>(t.master, static_cast<bf16*>(t.param), t.grad, t.m, t.v, t.n, lr,
+                                                   beta1, beta2, eps, c1, c2, st));
+    else
+      GDP_LAUNCH(GDP_K_ADAM, tr::launch_adam<float>(t.master, static_cast<float*>(t.param), t.grad, t.m, t.v, t.n, lr,
+                                                    beta1, beta2, eps, c1, c2, st));
+  }
+  return GDP_OK;
+}
+
+extern "C" int gdp_debug_train_tensor(const gdp_graph* g, const gdp_gnn* gnn, const gdp_placer* placer,
+                                      const void* store, size_t store_bytes, int32_t which, int32_t layer, void* out,
+                                      size_t out_bytes, void* stream) {
+  clear_error();
+  int r;
+  if ((r = check_graph(g)) != GDP_OK) return r;
+  if ((r = check_train(g, gnn, placer)) != GDP_OK) return r;
+  TrainPlan tp;
+  plan_train(g, gnn, placer, &tp);
+  if ((r = check_store(store, store_bytes, tp.store_total)) != GDP_OK) return r;
+  const size_t N = (size_t)g->n_nodes;
+  size_t off = 0, bytes = 0;
+  if (which == 0 && layer >= 0 && layer < placer->n_layers) {
+    off = tp.H1[layer];
+    bytes = N * (size_t)placer->d_ff * 4;
+  } else if (which == 1 && layer >= 0 && layer < gnn->n_layers) {
+    off = tp.h[layer + 1];
+    bytes = N * (size_t)gnn->hidden * 4;
+  } else if (which == 2 && layer >= 0 && layer < gnn->n_layers) {
+    off = tp.arg[layer];
+    bytes = N * (size_t)gnn->hidden * 4;
+  } else {
+    return fail(GDP_E_INVALID_ARG, "which = %d, layer = %d", which, layer);
+  }
+  if (!out || out_bytes < bytes) return fail(GDP_E_INVALID_ARG, "out is NULL or smaller than %zu bytes", bytes);
+  const hipError_t e = hipMemcpyAsync(out, static_cast<const char*>(store) + off, bytes, hipMemcpyDeviceToDevice,
+                                      static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync");
+  return GDP_OK;
+}
+
 extern "C" int gdp_debug_uniforms(uint64_t seed, int32_t n, int32_t k, int32_t d, float* out, void* stream) {
   clear_error();
   if (n < 1 || k < 1 || d < 1 || d > GDP_MAX_DEVICES || !out) return fail(GDP_E_INVALID_ARG, "bad arguments");
@@ -650,7 +1173,7 @@ extern "C" const char* gdp_kernel_kind_name(int32_t kind) {
       "graph_prep", "nbr_sample",    "gemm_pool_sigmoid", "gather_max", "gemm_update_relu",
       "meanpool",   "film",          "pre_layer",         "seg_attention", "post_attn",
       "head_lse",   "gumbel_sample", "logp_reduce",       "mlp_placer", "ppo_grad",  "head_backward", "advantages",
-      "evaluate"};
+      "evaluate", "train_forward", "backward", "adam", "log_prob"};
   if (kind < 0 || kind >= GDP_K_COUNT) return "";
   return names[kind];
 }

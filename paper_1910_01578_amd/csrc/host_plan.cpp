@@ -204,6 +204,88 @@ void plan_evaluate(const gdp_graph* g, int32_t n_devices, int32_t k, EvalPlan* p
   p->far = carve_add(&p->c, kb * N * 64 * 4);
 }
 
+int check_train(const gdp_graph* g, const gdp_gnn* gnn, const gdp_placer* p) {
+  int r;
+  if ((r = check_gnn(g, gnn)) != GDP_OK) return r;
+  if ((r = check_placer(g, p)) != GDP_OK) return r;
+  if (gnn->n_layers > kMaxTrainGnnLayers)
+    return fail(GDP_E_UNSUPPORTED, "training supports at most %d GNN layers (got %d)", kMaxTrainGnnLayers, gnn->n_layers);
+  if (p->n_layers > kMaxTrainPlacerLayers)
+    return fail(GDP_E_UNSUPPORTED, "training supports at most %d placer layers (got %d)", kMaxTrainPlacerLayers,
+                p->n_layers);
+  if (p->d_model != gnn->hidden)
+    return fail(GDP_E_INVALID_ARG, "d_model = %d != gnn.hidden = %d", p->d_model, gnn->hidden);
+  return GDP_OK;
+}
+
+void plan_train(const gdp_graph* g, const gdp_gnn* gnn, const gdp_placer* pl, TrainPlan* t) {
+  const size_t N = (size_t)g->n_nodes, E = (size_t)g->n_edges, H = (size_t)gnn->hidden, d = (size_t)pl->d_model;
+  const size_t G = (size_t)g->n_graphs, dff = (size_t)pl->d_ff, F = (size_t)g->feat_dim;
+  const size_t heads = pl->attention ? (size_t)pl->n_heads : 1;
+  int32_t blk[GDP_MAX_GRAPHS + 1];
+  t->chunks = prefix_blocks_rows(g->graph_ptr_h, g->n_graphs, 256, blk);
+  const size_t cap_a = 2 * E, cap_b = N * (size_t)gnn->fanout;
+  t->s_cap = (int64_t)(cap_a < cap_b ? cap_a : cap_b);
+  Carve c;
+  carve_init(&c);
+  t->s_ptr = carve_add(&c, (N + 1) * 4);
+  t->s_idx = carve_add(&c, (t->s_cap > 0 ? (size_t)t->s_cap : 1) * 4);
+  t->in_ptr = carve_add(&c, (N + 1) * 4);
+  t->in_idx = carve_add(&c, (E > 0 ? E : 1) * 4);
+  t->x0 = carve_add(&c, G * H * 4);
+  t->film = carve_add(&c, (size_t)pl->n_layers * 2 * G * d * 4);
+  for (int l = 0; l < gnn->n_layers; ++l) {
+    t->P[l] = carve_add(&c, N * H * 4);
+    t->A[l] = carve_add(&c, N * H * 4);
+    t->arg[l] = carve_add(&c, N * H * 4);
+    t->h[l + 1] = carve_add(&c, N * H * 4);
+  }
+  t->h[0] = 0;
+  t->X[0] = t->h[gnn->n_layers];
+  for (int l = 0; l < pl->n_layers; ++l) {
+    t->Y[l] = carve_add(&c, N * d * 4);
+    t->QKV[l] = pl->attention ? carve_add(&c, N * 3 * d * 4) : 0;
+    t->O[l] = pl->attention ? carve_add(&c, N * d * 4) : 0;
+    t->lse_att[l] = pl->attention ? carve_add(&c, N * heads * 4) : 0;
+    t->R1[l] = pl->attention ? carve_add(&c, N * d * 4) : 0;
+    t->Z[l] = pl->attention ? carve_add(&c, N * d * 4) : 0;
+    t->H1[l] = carve_add(&c, N * dff * 4);
+    t->R2[l] = carve_add(&c, N * d * 4);
+    t->X[l + 1] = carve_add(&c, N * d * 4);
+  }
+  t->store_total = c.total;
+
+  const size_t wide = d > H ? d : H;
+  const size_t fin = F > wide ? F : wide;
+  carve_init(&c);
+  t->counters = carve_add(&c, (2 * N + 1) * 4);
+  t->scan_tmp = carve_add(&c, 2 * ((N + 1023) / 1024) * 4);
+  t->heavy = carve_add(&c, N * 4);
+  t->dX = carve_add(&c, N * d * 4);
+  t->dY = carve_add(&c, N * d * 4);
+  t->dR = carve_add(&c, N * d * 4);
+  t->dZ = carve_add(&c, N * d * 4);
+  t->xg = carve_add(&c, N * wide * 4);
+  t->dH = carve_add(&c, N * dff * 4);
+  t->dqkv = carve_add(&c, N * 3 * d * 4);
+  t->dkvm = carve_add(&c, N * 2 * d * 4);
+  t->Dq = carve_add(&c, N * heads * 4);
+  t->head_partial = carve_add(&c, ((N + kHeadBwdRows - 1) / kHeadBwdRows) * (size_t)pl->n_devices * (d + 1) * 4);
+  t->dfilm = carve_add(&c, (size_t)pl->n_layers * 2 * G * d * 4);
+  t->dx0 = carve_add(&c, G * H * 4);
+  t->dh = carve_add(&c, N * fin * 4);
+  t->dA = carve_add(&c, N * H * 4);
+  t->dP = carve_add(&c, N * H * 4);
+  t->dU = carve_add(&c, N * H * 4);
+  const size_t colw = 3 * d > dff ? 3 * d : dff;
+  t->colpart = carve_add(&c, ((size_t)t->chunks + G) * (colw > fin ? colw : fin) * 4);
+  const size_t big = (dff * d > 3 * d * d ? dff * d : 3 * d * d);
+  const size_t splits = (N + 1023) / 1024;   // weight gradients: k = N split into pieces of 1,024 rows
+  t->gemm_partial_floats = (splits > 1 ? splits : 1) * (big > H * fin ? big : H * fin);
+  t->gemm_partial = carve_add(&c, t->gemm_partial_floats * 4);
+  t->ws_total = c.total;
+}
+
 void plan_sample(const gdp_graph* g, int32_t k, SamplePlan* p) {
   int32_t blk[GDP_MAX_GRAPHS + 1];
   p->chunks = prefix_blocks_rows(g->graph_ptr_h, g->n_graphs, kSampleRows, blk);

@@ -62,6 +62,28 @@ struct EvalPlan {
   int chunks;
 };
 void plan_evaluate(const gdp_graph* g, int32_t n_devices, int32_t k_samples, EvalPlan* p);
+
+// The update step: what the training forward keeps (store) and the backward's
+// temporaries (workspace).  Offsets into the two buffers, 256-byte aligned.
+constexpr int kMaxTrainGnnLayers = 8;
+constexpr int kMaxTrainPlacerLayers = 16;
+struct TrainPlan {
+  size_t store_total, ws_total;
+  // store
+  size_t s_ptr, s_idx, in_ptr, in_idx, x0, film;
+  size_t P[kMaxTrainGnnLayers], A[kMaxTrainGnnLayers], arg[kMaxTrainGnnLayers], h[kMaxTrainGnnLayers + 1];
+  size_t X[kMaxTrainPlacerLayers + 1], Y[kMaxTrainPlacerLayers], QKV[kMaxTrainPlacerLayers], O[kMaxTrainPlacerLayers],
+      lse_att[kMaxTrainPlacerLayers], R1[kMaxTrainPlacerLayers], Z[kMaxTrainPlacerLayers], H1[kMaxTrainPlacerLayers],
+      R2[kMaxTrainPlacerLayers];
+  // workspace
+  size_t counters, scan_tmp, heavy, dX, dY, dR, dZ, xg, dH, dqkv, dkvm, Dq, head_partial, dfilm, dx0, dh, dA, dP, dU,
+      colpart, gemm_partial;
+  size_t gemm_partial_floats;
+  int chunks;      // 256-row chunks over the graphs (column sums)
+  int64_t s_cap;
+};
+int check_train(const gdp_graph* g, const gdp_gnn* gnn, const gdp_placer* p);
+void plan_train(const gdp_graph* g, const gdp_gnn* gnn, const gdp_placer* p, TrainPlan* t);
 void plan_embed(const gdp_graph* g, const gdp_gnn* gnn, EmbedPlan* p);
 void plan_place(const gdp_graph* g, const gdp_placer* pl, PlacePlan* p);
 void plan_sample(const gdp_graph* g, int32_t k_samples, SamplePlan* p);

@@ -183,6 +183,9 @@ hipError_t launch_sample(const float* logits, const float* lse, int n, int D, in
 hipError_t launch_logp_reduce(const float* partial, const GraphTable& chunks, int total_chunks, int K,
                               float* logp, hipStream_t s);
 hipError_t launch_debug_uniforms(uint64_t seed, int n, int K, int D, float* out, hipStream_t s);
+// Per-chunk partial log-probs of given placements (then launch_logp_reduce).
+hipError_t launch_logp_given(const float* logits, const float* lse, int n, int D, int K, const int* placements,
+                             const GraphTable& chunks, int total_chunks, float* partial, hipStream_t s);
 
 // ---- the update path's first step ---------------------------------------------
 // PPO's clipped surrogate per graph (loss [G]) and the gradient of the batch

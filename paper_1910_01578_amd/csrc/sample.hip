@@ -93,6 +93,52 @@ hipError_t launch_sample(const float* logits, const float* lse, int n, int D, in
   return hipGetLastError();
 }
 
+// The log-softmax term of given placements, summed per work-group in the same
+// fixed order as k_sample's (the numerator of PPO's ratio after an update).
+__global__ __launch_bounds__(kSampleChunk) void k_logp_given(const float* __restrict__ logits,
+                                                             const float* __restrict__ lse, int n, int D,
+                                                             const int* __restrict__ placements, GraphTable ct,
+                                                             int total_chunks, float* __restrict__ partial) {
+  __shared__ float red[kSampleChunk / kWave];
+  const int c = blockIdx.x, k = blockIdx.y;
+  const int g = graph_of_block(ct, c);
+  const int v = ct.ptr[g] + (c - ct.blk[g]) * kSampleChunk + threadIdx.x;
+  float term = 0.f;
+  if (v < ct.ptr[g + 1]) {
+    const float* row = logits + (size_t)v * D;
+    float lz;
+    if (lse) {
+      lz = lse[v];
+    } else {
+      float m = -INFINITY;
+      for (int j = 0; j < D; ++j) m = fmaxf(m, row[j]);
+      float s = 0.f;
+      for (int j = 0; j < D; ++j) s += expf(row[j] - m);
+      lz = m + logf(s);
+    }
+    int p = placements[(size_t)k * n + v];
+    p = p < 0 ? 0 : (p >= D ? D - 1 : p);
+    term = row[p] - lz;
+  }
+#pragma unroll
+  for (int off = kWave / 2; off >= 1; off >>= 1) term += xor_shfl(term, off);
+  if ((threadIdx.x & (kWave - 1)) == 0) red[threadIdx.x / kWave] = term;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    float sum = 0.f;
+#pragma unroll
+    for (int w = 0; w < kSampleChunk / kWave; ++w) sum += red[w];
+    partial[(size_t)k * total_chunks + c] = sum;
+  }
+}
+
+hipError_t launch_logp_given(const float* logits, const float* lse, int n, int D, int K, const int* placements,
+                             const GraphTable& ct, int total_chunks, float* partial, hipStream_t s) {
+  hipLaunchKernelGGL(k_logp_given, dim3(total_chunks, K), dim3(kSampleChunk), 0, s, logits, lse, n, D, placements, ct,
+                     total_chunks, partial);
+  return hipGetLastError();
+}
+
 // logp[g][k]: one wavefront per (g, k); lane l adds chunks l, l + 64, ... of
 // graph g in order, then a fixed butterfly combines the lanes.
 __global__ __launch_bounds__(256) void k_logp_reduce(const float* __restrict__ partial, GraphTable ct,

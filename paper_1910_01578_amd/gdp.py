@@ -32,7 +32,7 @@ GDP_NOALLOC_SCRATCH_BYTES = 4 << 20
 KERNEL_KINDS = ["graph_prep", "nbr_sample", "gemm_pool_sigmoid", "gather_max", "gemm_update_relu",
                 "meanpool", "film", "pre_layer", "seg_attention", "post_attn",
                 "head_lse", "gumbel_sample", "logp_reduce", "mlp_placer", "ppo_grad", "head_backward", "advantages",
-                "evaluate"]
+                "evaluate", "train_forward", "backward", "adam", "log_prob"]
 K_COUNT = len(KERNEL_KINDS)
 
 
@@ -72,6 +72,24 @@ class GdpPlacer(ctypes.Structure):
                 ("layers", POINTER(GdpPlacerLayer)), ("w_out", c_void_p), ("b_out", c_void_p)]
 
 
+class GdpGnnLayerGrad(ctypes.Structure):
+    _fields_ = [(n, c_void_p) for n in ("w_pool", "b_pool", "w_self", "w_neigh", "b_upd")]
+
+
+class GdpPlacerLayerGrad(ctypes.Structure):
+    _fields_ = [(n, c_void_p) for n in PLACER_LAYER_FIELDS]
+
+
+class GdpGrads(ctypes.Structure):
+    _fields_ = [("gnn", POINTER(GdpGnnLayerGrad)), ("placer", POINTER(GdpPlacerLayerGrad)), ("w_out", c_void_p),
+                ("b_out", c_void_p)]
+
+
+class GdpAdamTensor(ctypes.Structure):
+    _fields_ = [("param", c_void_p), ("master", c_void_p), ("grad", c_void_p), ("m", c_void_p), ("v", c_void_p),
+                ("n", c_int64)]
+
+
 def _load():
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_1910_01578_amd.build_lib` "
@@ -96,6 +114,18 @@ def _load():
         "gdp_evaluate": (c_int32, [POINTER(GdpGraph), c_int32, c_int32, c_void_p, c_void_p, c_void_p, c_void_p,
                                    POINTER(c_int64), c_double, c_void_p, c_void_p, c_void_p, c_void_p, c_size_t,
                                    c_void_p]),
+        "gdp_train_sizes": (c_int32, [POINTER(GdpGraph), POINTER(GdpGnn), POINTER(GdpPlacer), POINTER(c_size_t),
+                                      POINTER(c_size_t)]),
+        "gdp_forward_train": (c_int32, [POINTER(GdpGraph), POINTER(GdpGnn), POINTER(GdpPlacer), c_void_p, c_size_t,
+                                        c_void_p, c_void_p, c_void_p, c_size_t, c_void_p]),
+        "gdp_backward": (c_int32, [POINTER(GdpGraph), POINTER(GdpGnn), POINTER(GdpPlacer), c_void_p, c_size_t,
+                                   c_void_p, POINTER(GdpGrads), c_void_p, c_size_t, c_void_p]),
+        "gdp_log_prob": (c_int32, [POINTER(GdpGraph), c_void_p, c_void_p, c_int32, c_int32, c_void_p, c_void_p,
+                                   c_void_p, c_size_t, c_void_p]),
+        "gdp_adam_step": (c_int32, [c_int32, POINTER(GdpAdamTensor), c_int32, c_float, c_float, c_float, c_float,
+                                    c_int64, c_void_p]),
+        "gdp_debug_train_tensor": (c_int32, [POINTER(GdpGraph), POINTER(GdpGnn), POINTER(GdpPlacer), c_void_p,
+                                             c_size_t, c_int32, c_int32, c_void_p, c_size_t, c_void_p]),
         "gdp_validate_graph_host": (c_int32, [c_void_p, c_int32, c_void_p, c_int32, c_void_p, c_int64, c_uint32]),
         "gdp_last_error": (c_char_p, []),
         "gdp_abi_version": (c_int32, []),
@@ -348,6 +378,124 @@ class Evaluator:
                                self.makespan.data_ptr(), self.valid.data_ptr(), self.run_time.data_ptr(),
                                self.ws.data_ptr(), self.ws_bytes, _stream_handle(stream)))
         return self.makespan, self.valid, self.run_time
+
+
+class Trainer:
+    """The update step of a policy on one graph batch (Section 3, PPO): the
+    training forward that keeps every intermediate in a store, the log-probs of
+    given placements, the backward pass into fp32 gradients shaped like the
+    weights, and Adam on fp32 master copies (the policy's own device weights,
+    in its dtype, are rewritten after every step)."""
+
+    def __init__(self, graph: DeviceGraph, policy: DevicePolicy, k_samples: int, device="cuda"):
+        torch = _torch()
+        self.graph, self.policy, self.k = graph, policy, int(k_samples)
+        sb, wb = c_size_t(0), c_size_t(0)
+        check(lib.gdp_train_sizes(ctypes.byref(graph.c), ctypes.byref(policy.gnn), ctypes.byref(policy.placer),
+                                  ctypes.byref(sb), ctypes.byref(wb)))
+        self.store_bytes, self.ws_bytes = sb.value, wb.value
+        self.store = torch.empty(self.store_bytes, dtype=torch.uint8, device=device)
+        self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8, device=device)
+        self.sample_ws_bytes = lib.gdp_workspace_bytes(ctypes.byref(graph.c), None, None, self.k)
+        self.sample_ws = torch.empty(max(1, self.sample_ws_bytes), dtype=torch.uint8, device=device)
+        N, G, D = graph.n_nodes, graph.n_graphs, policy.cfg.n_devices
+        self.logits = torch.empty((N, D), dtype=torch.float32, device=device)
+        self.lse = torch.empty((N,), dtype=torch.float32, device=device)
+        z = lambda t: torch.zeros(t.shape, dtype=torch.float32, device=device)
+        self.grad_gnn = [{k: z(v) for k, v in l.items()} for l in policy.gnn_t]
+        self.grad_placer = [{k: z(v) for k, v in l.items()} for l in policy.placer_t]
+        self.grad_head = {k: z(v) for k, v in policy.head_t.items()}
+        self._gg = (GdpGnnLayerGrad * len(self.grad_gnn))(
+            *[GdpGnnLayerGrad(*[l[k].data_ptr() for k in ("w_pool", "b_pool", "w_self", "w_neigh", "b_upd")])
+              for l in self.grad_gnn])
+        self._gp = (GdpPlacerLayerGrad * len(self.grad_placer))(
+            *[GdpPlacerLayerGrad(*[l[k].data_ptr() for k in PLACER_LAYER_FIELDS]) for l in self.grad_placer])
+        self.grads = GdpGrads(self._gg, self._gp, self.grad_head["w_out"].data_ptr(),
+                              self.grad_head["b_out"].data_ptr())
+        # Adam: master copies and moments of every weight, in one list
+        pairs = []
+        for lw, lg in zip(policy.gnn_t, self.grad_gnn):
+            pairs += [(lw[k], lg[k]) for k in lw]
+        for lw, lg in zip(policy.placer_t, self.grad_placer):
+            pairs += [(lw[k], lg[k]) for k in lw]
+        pairs += [(policy.head_t[k], self.grad_head[k]) for k in policy.head_t]
+        self._adam = []
+        for prm, grd in pairs:
+            master = prm.float().clone()
+            self._adam.append((prm, master, grd, torch.zeros_like(master), torch.zeros_like(master)))
+        self._adam_c = (GdpAdamTensor * len(self._adam))(
+            *[GdpAdamTensor(prm.data_ptr(), ms.data_ptr(), grd.data_ptr(), m.data_ptr(), v.data_ptr(), prm.numel())
+              for prm, ms, grd, m, v in self._adam])
+        self.step_count = 0
+
+    def forward(self, stream=None):
+        """The training forward; returns (logits, lse) of the current weights."""
+        check(lib.gdp_forward_train(ctypes.byref(self.graph.c), ctypes.byref(self.policy.gnn),
+                                    ctypes.byref(self.policy.placer), self.store.data_ptr(), self.store_bytes,
+                                    self.logits.data_ptr(), self.lse.data_ptr(), self.ws.data_ptr(), self.ws_bytes,
+                                    _stream_handle(stream)))
+        return self.logits, self.lse
+
+    def log_prob(self, placements, stream=None):
+        """log pi(placements) [G, K] under the last forward's logits."""
+        torch = _torch()
+        logp = torch.empty((self.graph.n_graphs, int(placements.shape[0])), dtype=torch.float32,
+                           device=self.logits.device)
+        check(lib.gdp_log_prob(ctypes.byref(self.graph.c), self.logits.data_ptr(), self.lse.data_ptr(),
+                               self.policy.cfg.n_devices, int(placements.shape[0]), placements.data_ptr(),
+                               logp.data_ptr(), self.sample_ws.data_ptr(), self.sample_ws_bytes,
+                               _stream_handle(stream)))
+        return logp
+
+    def ppo_grad(self, placements, logp, logp_old, advantages, clip_eps=0.2, stream=None):
+        """PPO's clipped surrogate and dL/dlogits at the last forward's logits."""
+        torch = _torch()
+        G, N, D = self.graph.n_graphs, self.graph.n_nodes, self.policy.cfg.n_devices
+        K = int(placements.shape[0])
+        loss = torch.empty((G,), dtype=torch.float32, device=self.logits.device)
+        dlogits = torch.empty((N, D), dtype=torch.float32, device=self.logits.device)
+        check(lib.gdp_ppo_grad(ctypes.byref(self.graph.c), self.logits.data_ptr(), self.lse.data_ptr(), D, K,
+                               placements.data_ptr(), logp.data_ptr(), logp_old.data_ptr(), advantages.data_ptr(),
+                               float(clip_eps), loss.data_ptr(), dlogits.data_ptr(), self.sample_ws.data_ptr(),
+                               self.sample_ws_bytes, _stream_handle(stream)))
+        return loss, dlogits
+
+    def backward(self, dlogits, stream=None):
+        """Gradients of sum(dlogits * logits) into grad_gnn / grad_placer / grad_head."""
+        check(lib.gdp_backward(ctypes.byref(self.graph.c), ctypes.byref(self.policy.gnn),
+                               ctypes.byref(self.policy.placer), self.store.data_ptr(), self.store_bytes,
+                               dlogits.data_ptr(), ctypes.byref(self.grads), self.ws.data_ptr(), self.ws_bytes,
+                               _stream_handle(stream)))
+
+    def decisions(self, stream=None):
+        """The last forward's discrete choices, for comparisons that take them the
+        same way: {"gnn": [(winning neighbour [N, H], ReLU sign [N, H])] per GNN
+        layer, "ffn": [ReLU sign [N, d_ff]] per placer layer} (numpy)."""
+        torch = _torch()
+        N, H, dff = self.graph.n_nodes, self.policy.cfg.hidden, self.policy.cfg.d_ff
+        dev = self.store.device
+
+        def get(which, layer, shape, dtype):
+            out = torch.empty(shape, dtype=dtype, device=dev)
+            check(lib.gdp_debug_train_tensor(ctypes.byref(self.graph.c), ctypes.byref(self.policy.gnn),
+                                             ctypes.byref(self.policy.placer), self.store.data_ptr(), self.store_bytes,
+                                             which, layer, out.data_ptr(), out.numel() * out.element_size(),
+                                             _stream_handle(stream)))
+            return out
+        gnn = []
+        for l in range(len(self.policy.gnn_t)):
+            arg = get(2, l, (N, H), torch.int32).cpu().numpy()
+            sign = (get(1, l, (N, H), torch.float32) > 0).cpu().numpy()
+            gnn.append((arg, sign))
+        ffn = [(get(0, l, (N, dff), torch.float32) > 0).cpu().numpy() for l in range(len(self.policy.placer_t))]
+        return {"gnn": gnn, "ffn": ffn}
+
+    def adam(self, lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8, stream=None):
+        """One Adam step on every weight (master copies in fp32)."""
+        self.step_count += 1
+        dt = GDP_BF16 if self.graph.dtype == "bf16" else GDP_F32
+        check(lib.gdp_adam_step(len(self._adam), self._adam_c, dt, float(lr), float(beta1), float(beta2), float(eps),
+                                self.step_count, _stream_handle(stream)))
 
 
 class RewardBaseline:

@@ -370,6 +370,44 @@ static void plan_paths() {
   }
 }
 
+static void train_paths() {
+  const gdp_graph g = good_graph();
+  gdp_gnn n = good_gnn();
+  gdp_placer p = good_placer();
+  EXPECT(check_train(&g, &n, &p), GDP_OK);
+  p = good_placer(); p.d_model = 256; EXPECT(check_train(&g, &n, &p), GDP_E_INVALID_ARG);   // != gnn.hidden
+  {
+    static gdp_gnn_layer many[kMaxTrainGnnLayers + 1];
+    for (auto& L : many) L = g_gnn_layers[0];
+    n = good_gnn(); n.n_layers = kMaxTrainGnnLayers + 1; n.layers = many;
+    p = good_placer();
+    EXPECT(check_train(&g, &n, &p), GDP_E_UNSUPPORTED);
+  }
+  {
+    static gdp_placer_layer many[kMaxTrainPlacerLayers + 1];
+    for (auto& L : many) L = g_pl_layers[0];
+    n = good_gnn(); p = good_placer(); p.n_layers = kMaxTrainPlacerLayers + 1; p.layers = many;
+    EXPECT(check_train(&g, &n, &p), GDP_E_UNSUPPORTED);
+  }
+  n = good_gnn();
+  p = good_placer();
+  TrainPlan tp;
+  plan_train(&g, &n, &p, &tp);
+  ++g_checks;
+  if (tp.store_total == 0 || tp.ws_total == 0 || tp.store_total % 256 || tp.ws_total % 256 ||
+      tp.X[0] != tp.h[n.n_layers] || tp.X[p.n_layers] + 16ull * 128 * 4 > tp.store_total || tp.gemm_partial_floats == 0) {
+    ++g_failures;
+    printf("FAIL train plan\n");
+  }
+  p.attention = 0;
+  plan_train(&g, &n, &p, &tp);
+  ++g_checks;
+  if (tp.QKV[0] != 0 || tp.Z[0] != 0 || tp.store_total % 256) {
+    ++g_failures;
+    printf("FAIL train plan without attention\n");
+  }
+}
+
 static void error_text() {
   clear_error();
   ++g_checks;
@@ -391,6 +429,7 @@ int main() {
   placer_paths();
   sample_paths();
   plan_paths();
+  train_paths();
   error_text();
   printf("%d checks, %d failures\n", g_checks, g_failures);
   return g_failures == 0 ? 0 : 1;

@@ -251,6 +251,59 @@ def test_evaluate_rejects():
     assert call(size=need - 1) == gdp.GDP_E_WORKSPACE
 
 
+def test_training_entry_points_reject():
+    cfg, gp, g, gl, gnn, pl, placer = _descs()
+    sb, wb = ctypes.c_size_t(0), ctypes.c_size_t(0)
+    assert gdp.lib.gdp_train_sizes(ctypes.byref(g), ctypes.byref(gnn), ctypes.byref(placer), ctypes.byref(sb),
+                                   ctypes.byref(wb)) == gdp.GDP_OK
+    assert sb.value > 0 and wb.value > 0
+    assert gdp.lib.gdp_train_sizes(ctypes.byref(g), ctypes.byref(gnn), ctypes.byref(placer), None,
+                                   ctypes.byref(wb)) == gdp.GDP_E_INVALID_ARG
+    # more GNN layers than the training path supports
+    cfg9, _, g9, gl9, gnn9, pl9, placer9 = _descs(gnn_layers=9)
+    assert gdp.lib.gdp_train_sizes(ctypes.byref(g9), ctypes.byref(gnn9), ctypes.byref(placer9), ctypes.byref(sb),
+                                   ctypes.byref(wb)) == gdp.GDP_E_UNSUPPORTED
+    assert sb.value == 0 and wb.value == 0
+    # d_model must equal the GNN width
+    gnn_w = gdp.GdpGnn(gnn.n_layers, gnn.in_dim, 128, gnn.fanout, 7, gl)
+    assert gdp.lib.gdp_train_sizes(ctypes.byref(g), ctypes.byref(gnn_w), ctypes.byref(placer), ctypes.byref(sb),
+                                   ctypes.byref(wb)) == gdp.GDP_E_INVALID_ARG
+    assert gdp.lib.gdp_train_sizes(ctypes.byref(g), ctypes.byref(gnn), ctypes.byref(placer), ctypes.byref(sb),
+                                   ctypes.byref(wb)) == gdp.GDP_OK
+    dev = 0x100000
+    ws = 0x1000000
+    fwd = lambda store=ws, ssz=sb.value, wsz=wb.value, logits=dev: gdp.lib.gdp_forward_train(
+        ctypes.byref(g), ctypes.byref(gnn), ctypes.byref(placer), store, ssz, logits, None, ws, wsz, None)
+    assert fwd(store=None) == gdp.GDP_E_INVALID_ARG
+    assert fwd(store=ws + 16) == gdp.GDP_E_INVALID_ARG
+    assert fwd(ssz=sb.value - 1) == gdp.GDP_E_WORKSPACE
+    assert fwd(wsz=wb.value - 1) == gdp.GDP_E_WORKSPACE
+    assert fwd(logits=None) == gdp.GDP_E_INVALID_ARG
+    # backward: a NULL gradient array is rejected before any launch
+    gg = (gdp.GdpGnnLayerGrad * cfg.gnn_layers)(*[gdp.GdpGnnLayerGrad(dev, dev, dev, dev, dev)] * cfg.gnn_layers)
+    gpl = (gdp.GdpPlacerLayerGrad * cfg.placer_layers)(*[gdp.GdpPlacerLayerGrad(*([dev] * 16))] * cfg.placer_layers)
+    grads = gdp.GdpGrads(gg, gpl, dev, dev)
+    bwd = lambda gr: gdp.lib.gdp_backward(ctypes.byref(g), ctypes.byref(gnn), ctypes.byref(placer), ws, sb.value, dev,
+                                          ctypes.byref(gr), ws, wb.value, None)
+    bad = (gdp.GdpGnnLayerGrad * cfg.gnn_layers)(*[gdp.GdpGnnLayerGrad(dev, dev, dev, None, dev)] * cfg.gnn_layers)
+    assert bwd(gdp.GdpGrads(bad, gpl, dev, dev)) == gdp.GDP_E_INVALID_ARG
+    assert bwd(gdp.GdpGrads(gg, gpl, None, dev)) == gdp.GDP_E_INVALID_ARG
+    # log-probs and Adam
+    assert gdp.lib.gdp_log_prob(ctypes.byref(g), dev, None, 1, 4, dev, dev, ws, 1 << 20, None) == gdp.GDP_E_UNSUPPORTED
+    assert gdp.lib.gdp_log_prob(ctypes.byref(g), dev, None, 8, 4, dev, None, ws, 1 << 20, None) == gdp.GDP_E_INVALID_ARG
+    t = (gdp.GdpAdamTensor * 1)(gdp.GdpAdamTensor(dev, dev, dev, dev, None, 10))
+    assert gdp.lib.gdp_adam_step(1, t, gdp.GDP_F32, 1e-3, 0.9, 0.999, 1e-8, 1, None) == gdp.GDP_E_INVALID_ARG
+    t = (gdp.GdpAdamTensor * 1)(gdp.GdpAdamTensor(dev, dev, dev, dev, dev, 10))
+    assert gdp.lib.gdp_adam_step(1, t, gdp.GDP_F32, 1e-3, 0.9, 0.999, 1e-8, 0, None) == gdp.GDP_E_INVALID_ARG
+    assert gdp.lib.gdp_adam_step(1, t, gdp.GDP_F32, 1e-3, 1.0, 0.999, 1e-8, 1, None) == gdp.GDP_E_INVALID_ARG
+    assert gdp.lib.gdp_adam_step(1, t, 5, 1e-3, 0.9, 0.999, 1e-8, 1, None) == gdp.GDP_E_INVALID_ARG
+    # the decisions export checks its selector before touching memory
+    assert gdp.lib.gdp_debug_train_tensor(ctypes.byref(g), ctypes.byref(gnn), ctypes.byref(placer), ws, sb.value, 3, 0,
+                                          dev, 1 << 30, None) == gdp.GDP_E_INVALID_ARG
+    assert gdp.lib.gdp_debug_train_tensor(ctypes.byref(g), ctypes.byref(gnn), ctypes.byref(placer), ws, sb.value, 0,
+                                          cfg.placer_layers, dev, 1 << 30, None) == gdp.GDP_E_INVALID_ARG
+
+
 def test_ppo_grad_rejects():
     cfg, gp, g, gl, gnn, pl, placer = _descs()
     dev = 0x100000

@@ -213,3 +213,53 @@ def test_adam_against_torch_and_first_step_closed_form():
         if step == 1:
             np.testing.assert_allclose(p, first, rtol=0, atol=1e-15)
         np.testing.assert_allclose(p, t.detach().numpy(), rtol=0, atol=1e-14)
+
+
+def test_decisions_from_the_same_run_change_nothing():
+    """Fixing the ReLU signs and max-pool winners to the forward's own choices
+    reproduces the free forward and its gradients (the decision path is the same
+    function where the decisions agree)."""
+    c, g, gnn, pl, hd = _small(gnn_layers=2, placer_layers=2, fanout=3)
+    rng = np.random.default_rng(9)
+    dl = rng.normal(size=(g.n_nodes, c.n_devices))
+    kw = dict(fanout=c.fanout, nb_seed=c.nb_seed, n_heads=c.heads, seg_len=64, mem_len=64, film=True)
+    free = PG.policy_backward(g.graph_ptr, g.row_ptr, g.col_idx, g.x, gnn, pl, hd["w_out"], hd["b_out"], dl, **kw)
+    # the forward's own decisions, from the numpy oracle
+    S = O.sample_neighbours(O.neighbour_lists(g.row_ptr, g.col_idx), g.graph_ptr, c.fanout, c.nb_seed)
+    h = g.x
+    dec_gnn = []
+    for lw in gnn:
+        A, P = O.aggregate_maxpool(h, S, lw["w_pool"], lw["b_pool"])
+        arg = np.full(A.shape, -1, np.int64)
+        for v, s in enumerate(S):
+            if len(s):
+                s = np.sort(np.asarray(s))
+                arg[v] = s[np.argmax(P[s], axis=0)]           # first maximum in ascending order
+        pre = h @ lw["w_self"].T + A @ lw["w_neigh"].T + lw["b_upd"]
+        dec_gnn.append((arg, pre > 0))
+        h = O.relu(pre)
+    e = O.embed(g.graph_ptr, g.row_ptr, g.col_idx, g.x, gnn, c.fanout, c.nb_seed)
+    gamma, beta = O.film_params(e["graph_emb"], pl, True)
+    x = e["node_emb"]
+    dec_ffn = []
+    for l, lw in enumerate(pl):                      # one segment of 64 with memory 64 == the band form
+        y = gamma[0, l] * x + beta[0, l]
+        nxt = np.zeros_like(x)
+        mask = np.zeros((g.n_nodes, c.d_ff), bool)
+        for q0 in range(0, g.n_nodes, 64):
+            q1 = min(q0 + 64, g.n_nodes)
+            k0 = max(0, q0 - 64)
+            z = O.layer_norm(y[q0:q1] + O.attention(y[q0:q1], y[k0:q1], lw, c.heads), lw["ln1_g"], lw["ln1_b"])
+            u = z @ lw["w_1"].T + lw["b_1"]
+            mask[q0:q1] = u > 0
+            nxt[q0:q1] = O.layer_norm(z + O.relu(u) @ lw["w_2"].T + lw["b_2"], lw["ln2_g"], lw["ln2_b"])
+        dec_ffn.append(mask)
+        x = nxt
+    fixed = PG.policy_backward(g.graph_ptr, g.row_ptr, g.col_idx, g.x, gnn, pl, hd["w_out"], hd["b_out"], dl, **kw,
+                               decisions={"gnn": dec_gnn, "ffn": dec_ffn})
+    np.testing.assert_allclose(fixed["logits"], free["logits"], rtol=0, atol=1e-12)
+    for l in range(2):
+        for k in gnn[l]:
+            np.testing.assert_allclose(fixed["gnn"][l][k], free["gnn"][l][k], rtol=1e-10, atol=1e-12)
+        for k in pl[l]:
+            np.testing.assert_allclose(fixed["placer"][l][k], free["placer"][l][k], rtol=1e-10, atol=1e-12)
