@@ -204,7 +204,7 @@ def cpu_baseline(cfg, g, w, n_sample, cores):
 
     from oracle import gdp_oracle as O
     from paper_1910_01578_amd import workloads as W
-    sub = W.prefix_graph(g, n_sample)
+    sub = g if n_sample >= g.n_nodes else W.prefix_graph(g, n_sample)
     gnn, pl, hd = w.f64()
     with threadpool_limits(limits=cores):
         t0 = time.perf_counter()
