@@ -729,7 +729,12 @@ int train_forward_impl(const gdp_graph* g, const gdp_gnn* gnn, const gdp_placer*
     GDP_LAUNCH(GDP_K_TRAIN_FWD, tr::launch_ew(tr::EW_MASK_POS, hout, hout, nullptr, (size_t)N * H, hout, st));
   }
   float* x0 = S(tp.x0);
-  GDP_LAUNCH(GDP_K_TRAIN_FWD, tr::launch_meanpool_f32(S(tp.h[gnn->n_layers]), H, gt, x0, st));
+  {
+    GraphTable ct = make_table(g);
+    const int nch = prefix_blocks_rows(g->graph_ptr_h, G, tr::kColChunkRows, ct.blk);
+    GDP_LAUNCH(GDP_K_TRAIN_FWD, tr::launch_meanpool_f32(S(tp.h[gnn->n_layers]), H, ct, nch,
+                                                        reinterpret_cast<float*>(ws + tp.colpart), x0, st));
+  }
   // Eq. 4: gamma, beta of every layer
   float* film = S(tp.film);
   if (p->film) {

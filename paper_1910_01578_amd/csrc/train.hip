@@ -356,16 +356,17 @@ hipError_t launch_meanpool_bwd(const float* dx0, int n, int H, const GraphTable&
   return hipGetLastError();
 }
 
-// x0[g][c] = mean over the rows of graph g (fixed order; one thread per (g, c))
-__global__ void k_meanpool_f32(const float* h, int H, GraphTable gt, float* x0) {
+// x0[g][c] = mean over the rows of graph g: the graph's column sums (256-row
+// chunks, then the chunks in order), divided by its node count.
+__global__ void k_scale_rows_by_graph_size(float* x0, int H, GraphTable gt) {
   const int g = blockIdx.y, c = blockIdx.x * 256 + threadIdx.x;
-  if (c >= H) return;
-  float s = 0.f;
-  for (int v = gt.ptr[g]; v < gt.ptr[g + 1]; ++v) s += h[(size_t)v * H + c];
-  x0[(size_t)g * H + c] = s / (float)(gt.ptr[g + 1] - gt.ptr[g]);
+  if (c < H) x0[(size_t)g * H + c] /= (float)(gt.ptr[g + 1] - gt.ptr[g]);
 }
-hipError_t launch_meanpool_f32(const float* h, int H, const GraphTable& gt, float* x0, hipStream_t s) {
-  hipLaunchKernelGGL(k_meanpool_f32, dim3((H + 255) / 256, gt.n), dim3(256), 0, s, h, H, gt, x0);
+hipError_t launch_meanpool_f32(const float* h, int H, const GraphTable& chunks, int n_chunks, float* partial,
+                               float* x0, hipStream_t s) {
+  hipError_t e = launch_colsum<float>(h, H, nullptr, 0, H, chunks, n_chunks, partial, x0, H, false, s);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_scale_rows_by_graph_size, dim3((H + 255) / 256, chunks.n), dim3(256), 0, s, x0, H, chunks);
   return hipGetLastError();
 }
 

@@ -60,7 +60,10 @@ hipError_t launch_film_dx(const float* dy, int n, int d, const float* gamma, con
 enum Ew { EW_ADD = 0, EW_MASK_POS = 1, EW_SIGMOID_GRAD = 2, EW_SCALE_BY = 3 };
 hipError_t launch_ew(int op, const float* a, const float* b, const float* c, size_t n, float* out, hipStream_t s);
 
-hipError_t launch_meanpool_f32(const float* h, int H, const GraphTable& gt, float* x0, hipStream_t s);
+// x0[g] = mean of graph g's rows of h; chunks: the graphs with their 256-row chunks (n_chunks of them),
+// partial: n_chunks * H floats.
+hipError_t launch_meanpool_f32(const float* h, int H, const GraphTable& chunks, int n_chunks, float* partial,
+                               float* x0, hipStream_t s);
 hipError_t launch_meanpool_bwd(const float* dx0, int n, int H, const GraphTable& gt, float* dh, hipStream_t s);
 
 hipError_t launch_gather_max_arg(const float* P, const int* s_ptr, const int* s_idx, int n, int H, float* A, int* arg,
