@@ -326,9 +326,10 @@ int gdp_sample_noalloc(const gdp_graph* g, const float* logits, const float* lse
  *   op_mem      device [N] int32 >= 0 (memory the op holds on its device)
  *   mem_cap_h   host [G] int64 >= 0 (per-device capacity of each graph)
  *   time_unit   >= 0, seconds per time unit (scales run_time only)
- *   makespan    device [G, K] int64 (output, 8-byte aligned); -1 where the
- *               graph's times leave 32 bits (sum of op_cost and out_xfer
- *               over a graph below 2^32 rules this out)
+ *   makespan    device [G, K] int64 (output, 8-byte aligned); -1 where a
+ *               finish time of the graph reaches 2^26 time units (a finish
+ *               time shares a 32-bit word with its device); a sum of op_cost
+ *               and out_xfer over the graph below 2^26 rules this out
  *   valid       device [G, K] uint8 (output)
  *   run_time    device [G, K] fp32 (output, may be NULL)
  * The CSR must be valid (gdp_validate_graph_host); its device arrays are not

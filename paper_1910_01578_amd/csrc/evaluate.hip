@@ -14,8 +14,9 @@
 // structure in scalar registers).  Per-lane state lives in LDS: the last kRing
 // finish times and devices (a ring indexed by node), and each device's free
 // time.  Finish times of older nodes are read back from a global copy written
-// as the wave goes.  Integer arithmetic only, so the result is exact; 32-bit
-// times, with a wrap check that marks the graph's result -1.
+// as the wave goes.  Integer arithmetic only, so the result is exact; times
+// below 2^26 units (they share a word with the device), with a check that
+// marks the graph's result -1 once a finish time reaches 2^26 or wraps.
 #include "device_common.h"
 #include "kernels.h"
 #include "lds_dma.h"
