@@ -9,6 +9,7 @@
 
 #include "device_common.h"
 #include "kernels.h"
+#include "host_plan.h"
 #include "train_kernels.h"
 
 namespace gdp {
@@ -452,179 +453,366 @@ hipError_t launch_sort_rows(const int* ptr, int n, int* idx, hipStream_t s) {
 }
 
 // ---------------------------------------------------------------------------
-// Segment attention in fp32 for training (band form: the queries of a segment
-// [q0, q1) of graph g attend to keys [max(g_start, q0 - mem_len), q1)).  One
-// thread per (query, head); the softmax's log-sum-exp per (query, head) is
-// kept for the backward.  qkv: [n, 3d] (Q | K | V, heads contiguous).
+// Segment attention in fp32 for training, on the fp32 matrix cores
+// (16x16x4 MFMA).  Band form: the queries of a segment [seg0, seg1) of graph
+// g attend to keys [max(g_start, seg0 - mem_len), seg1).  qkv: [n, 3d]
+// (Q | K | V, heads contiguous).
+//
+// A work-group is 4 waves and one head; it owns 64 queries (forward, dQ) or
+// 64 keys (dK, dV) of one segment, 16 a wave, one per lane column.  Scores are
+// formed transposed, S^T = K Q^T (or S = Q K^T for the key-side kernel), so
+// that a lane's accumulator holds 4 keys (queries) of its own column, rows
+// 4 (lane / 16) + r.  The next product contracts over those keys (queries);
+// ordering its k steps as {16 b + 4 g + r : g = 0..3} for r = 0..3 lets each
+// lane pass its own accumulator values as the B operand, with the A operand
+// read transposed from LDS.  Products over the head dimension order it as
+// dim = (lane / 16) * DH / 4 + kk at k step kk, so that a lane's operand
+// values are DH / 4 consecutive floats.  Scores are kept in log2 units (Q
+// pre-multiplied by log2(e) / sqrt(d_h)).
 // ---------------------------------------------------------------------------
-struct BandInfo {
-  int k0, q0, q1;   // key start, segment [q0, q1)
+constexpr int kAttnRows = 64;    // queries (keys) per work-group, 16 per wave
+constexpr int kAttnTile = 64;    // keys (queries) staged per tile
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+
+// The segment rows [r0, r1) of work block b (segments split into blocks of
+// kAttnRows rows; gt.blk the per-graph prefix of blocks).
+struct SegRows {
+  int gs, ge, seg0, seg1, r0, r1;
 };
-__device__ __forceinline__ BandInfo band_of(const GraphTable& gt, int v, int seg, int mem) {
-  const int g = graph_of_node(gt, v);
-  const int gs = gt.ptr[g], ge = gt.ptr[g + 1];
-  const int q0 = gs + ((v - gs) / seg) * seg;
-  BandInfo b;
-  b.q0 = q0;
-  b.q1 = min(q0 + seg, ge);
-  b.k0 = max(gs, q0 - mem);
-  return b;
+__device__ __forceinline__ SegRows seg_rows(const GraphTable& gt, int b, int seg) {
+  const int g = graph_of_block(gt, b);
+  const int per = (seg + kAttnRows - 1) / kAttnRows;
+  const int local = b - gt.blk[g];
+  SegRows s;
+  s.gs = gt.ptr[g];
+  s.ge = gt.ptr[g + 1];
+  s.seg0 = s.gs + (local / per) * seg;
+  s.seg1 = min(s.seg0 + seg, s.ge);
+  s.r0 = s.seg0 + (local % per) * kAttnRows;
+  s.r1 = min(s.r0 + kAttnRows, s.seg1);
+  return s;
+}
+
+// Rows [t0, t0 + kAttnTile) of columns [c0, c0 + DH) of src (row stride ld) into
+// LDS, row-major with row stride DH + 4 (rows at or past t1 as zeros), times mul.
+template <int DH>
+__device__ __forceinline__ void stage_rows(float* dst, const float* src, int ld, int c0, int t0, int t1, float mul) {
+  constexpr int C4 = DH / 4;
+  for (int e = threadIdx.x; e < kAttnTile * C4; e += 256) {
+    const int r = e / C4, c = (e % C4) * 4;
+    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (t0 + r < t1) v = *reinterpret_cast<const float4*>(src + (size_t)(t0 + r) * ld + c0 + c);
+    v.x *= mul; v.y *= mul; v.z *= mul; v.w *= mul;
+    *reinterpret_cast<float4*>(dst + r * (DH + 4) + c) = v;
+  }
+}
+// The same rows transposed: dst[c][r], row stride kAttnTile + 4.
+template <int DH>
+__device__ __forceinline__ void stage_cols(float* dst, const float* src, int ld, int c0, int t0, int t1) {
+  constexpr int C4 = DH / 4, TS = kAttnTile + 4;
+  for (int e = threadIdx.x; e < kAttnTile * C4; e += 256) {
+    const int r = e % kAttnTile, c = (e / kAttnTile) * 4;
+    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (t0 + r < t1) v = *reinterpret_cast<const float4*>(src + (size_t)(t0 + r) * ld + c0 + c);
+    dst[(c + 0) * TS + r] = v.x;
+    dst[(c + 1) * TS + r] = v.y;
+    dst[(c + 2) * TS + r] = v.z;
+    dst[(c + 3) * TS + r] = v.w;
+  }
+}
+
+// acc[b] (b = 0..3, 16 rows each) += X[b*16 + col][dims] . y[dims] over the head
+// dimension: X a row-major LDS tile (stride DH + 4), y the lane's B operand.
+template <int DH>
+__device__ __forceinline__ void dot_tile(f32x4 (&acc)[4], const float* X, const float (&y)[DH / 4], int col, int g4) {
+  constexpr int KT = DH / 4;
+#pragma unroll
+  for (int b = 0; b < 4; ++b) {
+    acc[b] = zero4();
+    const float* xr = X + (b * 16 + col) * (DH + 4) + g4 * KT;
+    float x[KT];
+#pragma unroll
+    for (int k = 0; k < KT; k += 4) *reinterpret_cast<float4*>(&x[k]) = *reinterpret_cast<const float4*>(xr + k);
+#pragma unroll
+    for (int k = 0; k < KT; ++k) acc[b] = __builtin_amdgcn_mfma_f32_16x16x4f32(x[k], y[k], acc[b], 0, 0, 0);
+  }
+}
+
+// out[db] (head-dim rows db*16 + .., the lane's column) += Y^T . w over the 64
+// tile rows: Y^T a transposed LDS tile (stride kAttnTile + 4), w[b][r] the
+// lane's accumulator values for tile rows b*16 + 4 g4 + r.
+template <int DH>
+__device__ __forceinline__ void acc_tile(f32x4 (&out)[DH / 16], const float* Yt, const f32x4 (&w)[4], int col, int g4) {
+#pragma unroll
+  for (int db = 0; db < DH / 16; ++db)
+#pragma unroll
+    for (int b = 0; b < 4; ++b) {
+      const float4 y = *reinterpret_cast<const float4*>(Yt + (db * 16 + col) * (kAttnTile + 4) + b * 16 + 4 * g4);
+      out[db] = __builtin_amdgcn_mfma_f32_16x16x4f32(y.x, w[b][0], out[db], 0, 0, 0);
+      out[db] = __builtin_amdgcn_mfma_f32_16x16x4f32(y.y, w[b][1], out[db], 0, 0, 0);
+      out[db] = __builtin_amdgcn_mfma_f32_16x16x4f32(y.z, w[b][2], out[db], 0, 0, 0);
+      out[db] = __builtin_amdgcn_mfma_f32_16x16x4f32(y.w, w[b][3], out[db], 0, 0, 0);
+    }
+}
+
+// The lane's DH / 4 operand values of row v: src[v][c0 + g4 * DH/4 + k] * mul.
+template <int DH>
+__device__ __forceinline__ void lane_operand(float (&y)[DH / 4], const float* src, size_t ld, int v, bool ok, int c0,
+                                             int g4, float mul) {
+  constexpr int KT = DH / 4;
+#pragma unroll
+  for (int k = 0; k < KT; k += 4) {
+    float4 t = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (ok) t = *reinterpret_cast<const float4*>(src + (size_t)v * ld + c0 + g4 * KT + k);
+    y[k] = t.x * mul; y[k + 1] = t.y * mul; y[k + 2] = t.z * mul; y[k + 3] = t.w * mul;
+  }
 }
 
 template <int DH>
-__global__ __launch_bounds__(64) void k_attn_fwd(const float* qkv, int n, int d, int heads, int seg, int mem,
-                                                 GraphTable gt, float scale, float* o, float* lse) {
-  const int v = blockIdx.x * 64 + threadIdx.x;
-  const int h = blockIdx.y;
-  if (v >= n) return;
-  const BandInfo b = band_of(gt, v, seg, mem);
+__global__ __launch_bounds__(256) void k_attn_fwd(const float* __restrict__ qkv, int d, int heads, int seg, int mem,
+                                                  GraphTable gt, float scale, float* __restrict__ o,
+                                                  float* __restrict__ lse) {
+  constexpr int DB = DH / 16;
+  __shared__ __attribute__((aligned(16))) float sK[kAttnTile * (DH + 4)];
+  __shared__ __attribute__((aligned(16))) float sVt[DH * (kAttnTile + 4)];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, col = lane & 15, g4 = lane >> 4;
+  const int logical = xcd_remap(blockIdx.x, gridDim.x);
+  const int head = logical % heads;
+  const SegRows b = seg_rows(gt, logical / heads, seg);
   const int ld = 3 * d;
-  float q[DH], acc[DH];
+  const int k0 = max(b.gs, b.seg0 - mem), k1 = b.seg1;
+  const int q = b.r0 + wave * 16 + col;
+  const bool qok = q < b.r1;
+  float qf[DH / 4];
+  lane_operand<DH>(qf, qkv, ld, q, qok, head * DH, g4, scale * kLog2e);
+  f32x4 oacc[DB];
 #pragma unroll
-  for (int t = 0; t < DH; ++t) {
-    q[t] = qkv[(size_t)v * ld + h * DH + t] * scale;
-    acc[t] = 0.f;
-  }
-  float m = -INFINITY, l = 0.f;
-  for (int j = b.k0; j < b.q1; ++j) {
-    const float* kr = qkv + (size_t)j * ld + d + h * DH;
-    float sc = 0.f;
+  for (int db = 0; db < DB; ++db) oacc[db] = zero4();
+  float m = -INFINITY, lsum = 0.f;
+  for (int t0 = k0; t0 < k1; t0 += kAttnTile) {
+    __syncthreads();
+    stage_rows<DH>(sK, qkv, ld, d + head * DH, t0, k1, 1.0f);
+    stage_cols<DH>(sVt, qkv, ld, 2 * d + head * DH, t0, k1);
+    __syncthreads();
+    f32x4 s[4];
+    dot_tile<DH>(s, sK, qf, col, g4);
+    float tmax = -INFINITY;
 #pragma unroll
-    for (int t = 0; t < DH; ++t) sc = fmaf(q[t], kr[t], sc);
-    const float mn = fmaxf(m, sc);
-    const float corr = expf(m - mn), p = expf(sc - mn);
-    l = l * corr + p;
-    const float* vr = qkv + (size_t)j * ld + 2 * d + h * DH;
+    for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
-    for (int t = 0; t < DH; ++t) acc[t] = fmaf(p, vr[t], acc[t] * corr);
+      for (int r = 0; r < 4; ++r) {
+        if (t0 + kb * 16 + 4 * g4 + r >= k1) s[kb][r] = -INFINITY;
+        tmax = fmaxf(tmax, s[kb][r]);
+      }
+    tmax = fmaxf(tmax, xor_shfl(tmax, 16));
+    tmax = fmaxf(tmax, xor_shfl(tmax, 32));
+    const float mn = fmaxf(m, tmax);
+    const float corr = exp2f(m - mn);
     m = mn;
-  }
-  const float inv = 1.0f / l;
+    lsum *= corr;
 #pragma unroll
-  for (int t = 0; t < DH; ++t) o[(size_t)v * d + h * DH + t] = acc[t] * inv;
-  lse[(size_t)v * heads + h] = m + logf(l);
-}
-
-// dq for every query: p = exp(s - lse), ds = p (dO . v_j - Dq), dq = scale * sum ds k_j
-template <int DH>
-__global__ __launch_bounds__(64) void k_attn_bwd_q(const float* qkv, const float* dO, const float* Dq,
-                                                   const float* lse, int n, int d, int heads, int seg, int mem,
-                                                   GraphTable gt, float scale, float* dqkv, int lddq) {
-  const int v = blockIdx.x * 64 + threadIdx.x;
-  const int h = blockIdx.y;
-  if (v >= n) return;
-  const BandInfo b = band_of(gt, v, seg, mem);
-  const int ld = 3 * d;
-  float q[DH], dov[DH], dq[DH];
+    for (int db = 0; db < DB; ++db)
 #pragma unroll
-  for (int t = 0; t < DH; ++t) {
-    q[t] = qkv[(size_t)v * ld + h * DH + t] * scale;
-    dov[t] = dO[(size_t)v * d + h * DH + t];
-    dq[t] = 0.f;
-  }
-  const float L = lse[(size_t)v * heads + h], D = Dq[(size_t)v * heads + h];
-  for (int j = b.k0; j < b.q1; ++j) {
-    const float* kr = qkv + (size_t)j * ld + d + h * DH;
-    const float* vr = qkv + (size_t)j * ld + 2 * d + h * DH;
-    float sc = 0.f, dp = 0.f;
+      for (int r = 0; r < 4; ++r) oacc[db][r] *= corr;
 #pragma unroll
-    for (int t = 0; t < DH; ++t) {
-      sc = fmaf(q[t], kr[t], sc);
-      dp = fmaf(dov[t], vr[t], dp);
-    }
-    const float ds = expf(sc - L) * (dp - D);
+    for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
-    for (int t = 0; t < DH; ++t) dq[t] = fmaf(ds, kr[t], dq[t]);
-  }
-#pragma unroll
-  for (int t = 0; t < DH; ++t) dqkv[(size_t)v * lddq + h * DH + t] = dq[t] * scale;
-}
-
-// dk, dv for every key j, from the queries of its own segment (live: the key's
-// row receives the gradient) and separately from the later segments whose
-// memory holds it (the memory passes no gradient to its rows, only to the
-// projection weights).
-template <int DH>
-__global__ __launch_bounds__(64) void k_attn_bwd_kv(const float* qkv, const float* dO, const float* Dq,
-                                                    const float* lse, int n, int d, int heads, int seg, int mem,
-                                                    GraphTable gt, float scale, float* dqkv_live, int ldl,
-                                                    float* dkv_mem, int ldm) {
-  const int j = blockIdx.x * 64 + threadIdx.x;
-  const int h = blockIdx.y;
-  if (j >= n) return;
-  const int g = graph_of_node(gt, j);
-  const int gs = gt.ptr[g], ge = gt.ptr[g + 1];
-  const int ld = 3 * d;
-  float kr[DH], vr[DH], dk[2][DH], dv[2][DH];
-#pragma unroll
-  for (int t = 0; t < DH; ++t) {
-    kr[t] = qkv[(size_t)j * ld + d + h * DH + t];
-    vr[t] = qkv[(size_t)j * ld + 2 * d + h * DH + t];
-    dk[0][t] = dk[1][t] = dv[0][t] = dv[1][t] = 0.f;
-  }
-  const int s_own = (j - gs) / seg;
-  // segments that see key j: its own, and later ones with q0 - mem <= j
-  for (int s = s_own;; ++s) {
-    const int q0 = gs + s * seg;
-    if (q0 >= ge || (s > s_own && q0 - mem > j)) break;
-    const int q1 = min(q0 + seg, ge);
-    const int w = s == s_own ? 0 : 1;
-    for (int i = q0; i < q1; ++i) {
-      const float* qr = qkv + (size_t)i * ld + h * DH;
-      const float* dor = dO + (size_t)i * d + h * DH;
-      float sc = 0.f, dp = 0.f;
-#pragma unroll
-      for (int t = 0; t < DH; ++t) {
-        sc = fmaf(qr[t] * scale, kr[t], sc);
-        dp = fmaf(dor[t], vr[t], dp);
+      for (int r = 0; r < 4; ++r) {
+        s[kb][r] = exp2f(s[kb][r] - mn);
+        lsum += s[kb][r];
       }
-      const float p = expf(sc - lse[(size_t)i * heads + h]);
-      const float ds = p * (dp - Dq[(size_t)i * heads + h]);
+    acc_tile<DH>(oacc, sVt, s, col, g4);
+  }
+  lsum += xor_shfl(lsum, 16);
+  lsum += xor_shfl(lsum, 32);
+  if (qok) {
+    const float inv = 1.0f / lsum;
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+      *reinterpret_cast<float4*>(o + (size_t)q * d + head * DH + db * 16 + 4 * g4) =
+          make_float4(oacc[db][0] * inv, oacc[db][1] * inv, oacc[db][2] * inv, oacc[db][3] * inv);
+    if (g4 == 0) lse[(size_t)q * heads + head] = (m + log2f(lsum)) * kLn2;
+  }
+}
+
+// dQ for the work-group's queries: p = exp(s - lse), ds = p (dO . v - Dq),
+// dq = scale * sum_j ds_j k_j (into the Q columns of dqkv, row stride lddq).
+template <int DH>
+__global__ __launch_bounds__(256) void k_attn_bwd_q(const float* __restrict__ qkv, const float* __restrict__ dO,
+                                                    const float* __restrict__ Dq, const float* __restrict__ lse,
+                                                    int d, int heads, int seg, int mem, GraphTable gt, float scale,
+                                                    float* __restrict__ dqkv, int lddq) {
+  constexpr int DB = DH / 16;
+  __shared__ __attribute__((aligned(16))) float sK[kAttnTile * (DH + 4)];
+  __shared__ __attribute__((aligned(16))) float sV[kAttnTile * (DH + 4)];
+  __shared__ __attribute__((aligned(16))) float sKt[DH * (kAttnTile + 4)];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, col = lane & 15, g4 = lane >> 4;
+  const int logical = xcd_remap(blockIdx.x, gridDim.x);
+  const int head = logical % heads;
+  const SegRows b = seg_rows(gt, logical / heads, seg);
+  const int ld = 3 * d;
+  const int k0 = max(b.gs, b.seg0 - mem), k1 = b.seg1;
+  const int q = b.r0 + wave * 16 + col;
+  const bool qok = q < b.r1;
+  float qf[DH / 4], df[DH / 4];
+  lane_operand<DH>(qf, qkv, ld, q, qok, head * DH, g4, scale * kLog2e);
+  lane_operand<DH>(df, dO, d, q, qok, head * DH, g4, 1.0f);
+  const float L2 = qok ? lse[(size_t)q * heads + head] * kLog2e : 0.f;
+  const float Dv = qok ? Dq[(size_t)q * heads + head] : 0.f;
+  f32x4 dq[DB];
+#pragma unroll
+  for (int db = 0; db < DB; ++db) dq[db] = zero4();
+  for (int t0 = k0; t0 < k1; t0 += kAttnTile) {
+    __syncthreads();
+    stage_rows<DH>(sK, qkv, ld, d + head * DH, t0, k1, 1.0f);
+    stage_rows<DH>(sV, qkv, ld, 2 * d + head * DH, t0, k1, 1.0f);
+    stage_cols<DH>(sKt, qkv, ld, d + head * DH, t0, k1);
+    __syncthreads();
+    f32x4 s[4], dp[4];
+    dot_tile<DH>(s, sK, qf, col, g4);
+    dot_tile<DH>(dp, sV, df, col, g4);
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const bool ok = t0 + kb * 16 + 4 * g4 + r < k1;
+        s[kb][r] = ok ? exp2f(s[kb][r] - L2) * (dp[kb][r] - Dv) : 0.f;
+      }
+    acc_tile<DH>(dq, sKt, s, col, g4);
+  }
+  if (qok) {
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+      *reinterpret_cast<float4*>(dqkv + (size_t)q * lddq + head * DH + db * 16 + 4 * g4) =
+          make_float4(dq[db][0] * scale, dq[db][1] * scale, dq[db][2] * scale, dq[db][3] * scale);
+  }
+}
+
+// dK, dV for the work-group's keys, from the queries of their own segment
+// (live: the key's row receives the gradient) and separately from the later
+// segments whose memory holds them (that part stops at the projection
+// weights: the memory passes no gradient to its rows).
+template <int DH>
+__global__ __launch_bounds__(256) void k_attn_bwd_kv(const float* __restrict__ qkv, const float* __restrict__ dO,
+                                                     const float* __restrict__ Dq, const float* __restrict__ lse,
+                                                     int d, int heads, int seg, int mem, GraphTable gt, float scale,
+                                                     float* __restrict__ dqkv_live, int ldl,
+                                                     float* __restrict__ dkv_mem, int ldm) {
+  constexpr int DB = DH / 16;
+  __shared__ __attribute__((aligned(16))) float sQ[kAttnTile * (DH + 4)];
+  __shared__ __attribute__((aligned(16))) float sD[kAttnTile * (DH + 4)];
+  __shared__ __attribute__((aligned(16))) float sQt[DH * (kAttnTile + 4)];
+  __shared__ __attribute__((aligned(16))) float sDt[DH * (kAttnTile + 4)];
+  __shared__ float sL[kAttnTile], sDq[kAttnTile];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, col = lane & 15, g4 = lane >> 4;
+  const int logical = xcd_remap(blockIdx.x, gridDim.x);
+  const int head = logical % heads;
+  const SegRows b = seg_rows(gt, logical / heads, seg);
+  const int ld = 3 * d;
+  const int key = b.r0 + wave * 16 + col;
+  const bool kok = key < b.r1;
+  float kf[DH / 4], vf[DH / 4];
+  lane_operand<DH>(kf, qkv, ld, key, kok, d + head * DH, g4, 1.0f);
+  lane_operand<DH>(vf, qkv, ld, key, kok, 2 * d + head * DH, g4, 1.0f);
+  f32x4 dk[2][DB], dv[2][DB];
+#pragma unroll
+  for (int w = 0; w < 2; ++w)
+#pragma unroll
+    for (int db = 0; db < DB; ++db) dk[w][db] = dv[w][db] = zero4();
+  // the key's own segment, then later segments whose band starts before r1
+  for (int sg0 = b.seg0; sg0 < b.ge && (sg0 == b.seg0 || sg0 - mem < b.r1); sg0 += seg) {
+    const int sg1 = min(sg0 + seg, b.ge);
+    const int w = sg0 == b.seg0 ? 0 : 1;
+    const bool seen = w == 0 || key >= sg0 - mem;        // the band of segment sg0 holds the key
+    for (int t0 = sg0; t0 < sg1; t0 += kAttnTile) {
+      __syncthreads();
+      stage_rows<DH>(sQ, qkv, ld, head * DH, t0, sg1, scale * kLog2e);
+      stage_rows<DH>(sD, dO, d, head * DH, t0, sg1, 1.0f);
+      stage_cols<DH>(sQt, qkv, ld, head * DH, t0, sg1);
+      stage_cols<DH>(sDt, dO, d, head * DH, t0, sg1);
+      if (threadIdx.x < kAttnTile) {
+        const int qi = t0 + threadIdx.x;
+        sL[threadIdx.x] = qi < sg1 ? lse[(size_t)qi * heads + head] * kLog2e : 0.f;
+        sDq[threadIdx.x] = qi < sg1 ? Dq[(size_t)qi * heads + head] : 0.f;
+      }
+      __syncthreads();
+      f32x4 s[4], dp[4];
+      dot_tile<DH>(s, sQ, kf, col, g4);
+      dot_tile<DH>(dp, sD, vf, col, g4);
+#pragma unroll
+      for (int qb = 0; qb < 4; ++qb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int qi = qb * 16 + 4 * g4 + r;
+          const float p = seen && t0 + qi < sg1 ? exp2f(s[qb][r] - sL[qi]) : 0.f;
+          s[qb][r] = p;
+          dp[qb][r] = p * (dp[qb][r] - sDq[qi]);
+        }
       if (w == 0) {
-#pragma unroll
-        for (int t = 0; t < DH; ++t) {
-          dv[0][t] = fmaf(p, dor[t], dv[0][t]);
-          dk[0][t] = fmaf(ds, qr[t], dk[0][t]);
-        }
+        acc_tile<DH>(dv[0], sDt, s, col, g4);
+        acc_tile<DH>(dk[0], sQt, dp, col, g4);
       } else {
-#pragma unroll
-        for (int t = 0; t < DH; ++t) {
-          dv[1][t] = fmaf(p, dor[t], dv[1][t]);
-          dk[1][t] = fmaf(ds, qr[t], dk[1][t]);
-        }
+        acc_tile<DH>(dv[1], sDt, s, col, g4);
+        acc_tile<DH>(dk[1], sQt, dp, col, g4);
       }
     }
   }
+  if (kok) {
 #pragma unroll
-  for (int t = 0; t < DH; ++t) {
-    dqkv_live[(size_t)j * ldl + d + h * DH + t] = dk[0][t] * scale;
-    dqkv_live[(size_t)j * ldl + 2 * d + h * DH + t] = dv[0][t];
-    dkv_mem[(size_t)j * ldm + h * DH + t] = dk[1][t] * scale;
-    dkv_mem[(size_t)j * ldm + d + h * DH + t] = dv[1][t];
+    for (int db = 0; db < DB; ++db) {
+      const int c = head * DH + db * 16 + 4 * g4;
+      *reinterpret_cast<float4*>(dqkv_live + (size_t)key * ldl + d + c) =
+          make_float4(dk[0][db][0] * scale, dk[0][db][1] * scale, dk[0][db][2] * scale, dk[0][db][3] * scale);
+      *reinterpret_cast<float4*>(dqkv_live + (size_t)key * ldl + 2 * d + c) =
+          make_float4(dv[0][db][0], dv[0][db][1], dv[0][db][2], dv[0][db][3]);
+      *reinterpret_cast<float4*>(dkv_mem + (size_t)key * ldm + c) =
+          make_float4(dk[1][db][0] * scale, dk[1][db][1] * scale, dk[1][db][2] * scale, dk[1][db][3] * scale);
+      *reinterpret_cast<float4*>(dkv_mem + (size_t)key * ldm + d + c) =
+          make_float4(dv[1][db][0], dv[1][db][1], dv[1][db][2], dv[1][db][3]);
+    }
   }
 }
 
-// Dq[v][h] = dO[v] . O[v] over the head's columns
-__global__ void k_attn_dq_rowdot(const float* dO, const float* O, int n, int d, int heads, float* Dq) {
+// Dq[v][h] = dO[v] . O[v] over the head's columns, one thread per (v, h).
+template <int DH>
+__global__ void k_attn_dq_rowdot(const float* __restrict__ dO, const float* __restrict__ O, int n, int d, int heads,
+                                 float* __restrict__ Dq) {
   const size_t total = (size_t)n * heads;
-  const int dh = d / heads;
   for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < total; i += (size_t)gridDim.x * blockDim.x) {
-    const int v = (int)(i / heads), h = (int)(i % heads);
+    const size_t base = (i / heads) * d + (i % heads) * DH;
     float s = 0.f;
-    for (int t = 0; t < dh; ++t) s = fmaf(dO[(size_t)v * d + h * dh + t], O[(size_t)v * d + h * dh + t], s);
+#pragma unroll
+    for (int t = 0; t < DH; t += 4) {
+      const float4 a = *reinterpret_cast<const float4*>(dO + base + t);
+      const float4 c = *reinterpret_cast<const float4*>(O + base + t);
+      s = fmaf(a.x, c.x, s);
+      s = fmaf(a.y, c.y, s);
+      s = fmaf(a.z, c.z, s);
+      s = fmaf(a.w, c.w, s);
+    }
     Dq[i] = s;
   }
 }
 
+// The attention blocks of every graph: segments in blocks of kAttnRows rows.
+static int attn_table(const GraphTable& gt, int seg, GraphTable* t) {
+  *t = gt;
+  return prefix_blocks_attention(t->ptr, t->n, seg, kAttnRows, t->blk);
+}
+
 hipError_t launch_attn_fwd(const float* qkv, int n, int d, int heads, int seg, int mem, const GraphTable& gt,
                            float* o, float* lse, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
   const int dh = d / heads;
   const float scale = 1.0f / sqrtf((float)dh);
-  dim3 grid((n + 63) / 64, heads);
+  GraphTable t;
+  const int blocks = attn_table(gt, seg, &t);
+  dim3 grid(blocks * heads), block(256);
   switch (dh) {
-    case 16: hipLaunchKernelGGL((k_attn_fwd<16>), grid, dim3(64), 0, s, qkv, n, d, heads, seg, mem, gt, scale, o, lse); break;
-    case 32: hipLaunchKernelGGL((k_attn_fwd<32>), grid, dim3(64), 0, s, qkv, n, d, heads, seg, mem, gt, scale, o, lse); break;
-    case 64: hipLaunchKernelGGL((k_attn_fwd<64>), grid, dim3(64), 0, s, qkv, n, d, heads, seg, mem, gt, scale, o, lse); break;
+    case 16: hipLaunchKernelGGL((k_attn_fwd<16>), grid, block, 0, s, qkv, d, heads, seg, mem, t, scale, o, lse); break;
+    case 32: hipLaunchKernelGGL((k_attn_fwd<32>), grid, block, 0, s, qkv, d, heads, seg, mem, t, scale, o, lse); break;
+    case 64: hipLaunchKernelGGL((k_attn_fwd<64>), grid, block, 0, s, qkv, d, heads, seg, mem, t, scale, o, lse); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -633,21 +821,19 @@ hipError_t launch_attn_fwd(const float* qkv, int n, int d, int heads, int seg, i
 hipError_t launch_attn_bwd(const float* qkv, const float* O, const float* dO, const float* lse, int n, int d,
                            int heads, int seg, int mem, const GraphTable& gt, float* Dq, float* dqkv_live,
                            float* dkv_mem, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
   const int dh = d / heads;
   const float scale = 1.0f / sqrtf((float)dh);
-  {
-    const size_t total = (size_t)n * heads;
-    const unsigned blocks = (unsigned)std::min<size_t>((total + 255) / 256, 8192);
-    hipLaunchKernelGGL(k_attn_dq_rowdot, dim3(blocks), dim3(256), 0, s, dO, O, n, d, heads, Dq);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-  }
-  dim3 grid((n + 63) / 64, heads);
-#define GDP_ATTN_BWD(DH)                                                                                         \
-  hipLaunchKernelGGL((k_attn_bwd_q<DH>), grid, dim3(64), 0, s, qkv, dO, (const float*)Dq, lse, n, d, heads, seg, \
-                     mem, gt, scale, dqkv_live, 3 * d);                                                         \
-  hipLaunchKernelGGL((k_attn_bwd_kv<DH>), grid, dim3(64), 0, s, qkv, dO, (const float*)Dq, lse, n, d, heads, seg, \
-                     mem, gt, scale, dqkv_live, 3 * d, dkv_mem, 2 * d);
+  GraphTable t;
+  const int blocks = attn_table(gt, seg, &t);
+  const unsigned rd_blocks = (unsigned)std::min<size_t>(((size_t)n * heads + 255) / 256, 8192);
+  dim3 grid(blocks * heads), block(256);
+#define GDP_ATTN_BWD(DH)                                                                                          \
+  hipLaunchKernelGGL((k_attn_dq_rowdot<DH>), dim3(rd_blocks), dim3(256), 0, s, dO, O, n, d, heads, Dq);           \
+  hipLaunchKernelGGL((k_attn_bwd_q<DH>), grid, block, 0, s, qkv, dO, (const float*)Dq, lse, d, heads, seg, mem, t, \
+                     scale, dqkv_live, 3 * d);                                                                     \
+  hipLaunchKernelGGL((k_attn_bwd_kv<DH>), grid, block, 0, s, qkv, dO, (const float*)Dq, lse, d, heads, seg, mem,   \
+                     t, scale, dqkv_live, 3 * d, dkv_mem, 2 * d);
   switch (dh) {
     case 16: GDP_ATTN_BWD(16) break;
     case 32: GDP_ATTN_BWD(32) break;
