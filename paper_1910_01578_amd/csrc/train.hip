@@ -21,83 +21,75 @@ __device__ __forceinline__ float ld(const bf16* p, size_t i) { return (float)p[i
 __device__ __forceinline__ float sigmoidf_(float z) { return 1.0f / (1.0f + expf(-z)); }
 
 // ---------------------------------------------------------------------------
-// Strided GEMM: C(m, n) = epi(alpha * sum_k A(m, k) B(k, n)), tiles of 64 x 64
-// with k steps of 16, 256 threads of 4 x 4 outputs.  With splits > 1, grid.z
-// splits k and each split writes its raw sums to partial[z]; gemm_reduce adds
-// them in split order and applies the epilogue.
+// Strided GEMM on the fp32 matrix cores (16x16x4 MFMA): C(m, n) = epi(alpha *
+// sum_k A(m, k) B(k, n)).  A work-group (4 waves, 2 x 2) owns a BM x BM tile
+// of C, each wave a (BM/2)^2 block of 16 x 16 MFMA tiles; k advances in steps
+// of 16 through LDS tiles stored k-major (As[k][m], Bs[k][n], rows padded by
+// 16 floats so the 4 lane groups of a fragment read fall in distinct banks),
+// the next step's operands loaded into registers during this step's MFMAs.
+// With splits > 1, grid.z splits k and each split writes its raw sums to
+// partial[z]; gemm_reduce adds them in split order and applies the epilogue.
 // ---------------------------------------------------------------------------
-constexpr int GBM = 64, GBN = 64, GBK = 16;
+constexpr int GBK = 16;
 
-template <typename TA, typename TB>
-__global__ __launch_bounds__(256) void k_gemm_strided(GemmStrided<TA, TB> g, int k_per_split, float* partial) {
-  __shared__ float As[GBK][GBM + 4];
-  __shared__ float Bs[GBK][GBN + 4];
-  const int tid = threadIdx.x, tx = tid & 15, ty = tid >> 4;
-  const int m0 = blockIdx.y * GBM, n0 = blockIdx.x * GBN;
-  const int kb = blockIdx.z * k_per_split, ke = min(g.K, kb + k_per_split);
-  float acc[4][4];
+// Operand tile loader: R x GBK (A: R = rows m) or GBK x R (B: R = columns n)
+// elements, 4 consecutive elements of the fast dimension per vector.
+template <typename T, int R>
+struct TileLoad {
+  static constexpr int NV = R * GBK / 4 / 256;      // vectors per thread
+  float v[NV][4];
+  // element (r, k) = p[r * sr + k * sk]; kfast: sk == 1 (vectors along k),
+  // else sr == 1 (vectors along r); vec: every vector aligned and in one piece.
+  __device__ __forceinline__ void load(const T* p, long sr, long sk, bool kfast, bool vec, int r0, int rmax, int k0,
+                                       int kmax) {
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+    for (int q = 0; q < NV; ++q) {
+      const int e = threadIdx.x + 256 * q;
+      const int r = kfast ? e / (GBK / 4) : (e % (R / 4)) * 4;
+      const int k = kfast ? (e % (GBK / 4)) * 4 : e / (R / 4);
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = 0.f;
-  const bool a_kfast = g.sak == 1, b_nfast = g.sbn == 1;
-  for (int k0 = kb; k0 < ke; k0 += GBK) {
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int l = tid + 256 * e;
-      int mm, kk;
-      if (a_kfast) { kk = l & 15; mm = l >> 4; } else { mm = l & 63; kk = l >> 6; }
-      const int m = m0 + mm, k = k0 + kk;
-      As[kk][mm] = (m < g.M && k < ke) ? ld(g.a, (size_t)m * g.sam + (size_t)k * g.sak) : 0.f;
-      int nn;
-      if (b_nfast) { nn = l & 63; kk = l >> 6; } else { kk = l & 15; nn = l >> 4; }
-      const int n = n0 + nn, k2 = k0 + kk;
-      Bs[kk][nn] = (n < g.N && k2 < ke) ? ld(g.b, (size_t)k2 * g.sbk + (size_t)n * g.sbn) : 0.f;
-    }
-    __syncthreads();
-#pragma unroll
-    for (int kk = 0; kk < GBK; ++kk) {
-      float a[4], b[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) a[i] = As[kk][ty + 16 * i];
-#pragma unroll
-      for (int j = 0; j < 4; ++j) b[j] = Bs[kk][tx + 16 * j];
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(a[i], b[j], acc[i][j]);
-    }
-    __syncthreads();
-  }
-#pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int m = m0 + ty + 16 * i, n = n0 + tx + 16 * j;
-      if (m >= g.M || n >= g.N) continue;
-      if (partial) {
-        partial[((size_t)blockIdx.z * g.M + m) * g.N + n] = acc[i][j];
+      for (int t = 0; t < 4; ++t) v[q][t] = 0.f;
+      const int rr = r0 + r, kk = k0 + k;
+      if (vec && (kfast ? (rr < rmax && kk + 3 < kmax) : (rr + 3 < rmax && kk < kmax))) {
+        load4(p + (size_t)rr * sr + (size_t)kk * sk, v[q]);
       } else {
-        float v = g.alpha * acc[i][j];
-        if (g.bias_f) v += g.bias_f[n];
-        if (g.bias_h) v += (float)g.bias_h[n];
-        if (g.act == ACT_RELU) v = fmaxf(v, 0.f);
-        else if (g.act == ACT_SIGMOID) v = sigmoidf_(v);
-        if (g.mask && !(g.mask[(size_t)m * g.ldm + n] > 0.f)) v = 0.f;
-        float* c = g.c + (size_t)m * g.ldc + n;
-        *c = g.accumulate ? *c + v : v;
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          const int r2 = kfast ? rr : rr + t, k2 = kfast ? kk + t : kk;
+          if (r2 < rmax && k2 < kmax) v[q][t] = ld(p, (size_t)r2 * sr + (size_t)k2 * sk);
+        }
       }
     }
-}
+  }
+  __device__ __forceinline__ void store(float* s, bool kfast) const {
+    constexpr int LS = R + 16;
+#pragma unroll
+    for (int q = 0; q < NV; ++q) {
+      const int e = threadIdx.x + 256 * q;
+      if (kfast) {
+        const int r = e / (GBK / 4), k = (e % (GBK / 4)) * 4;
+#pragma unroll
+        for (int t = 0; t < 4; ++t) s[(k + t) * LS + r] = v[q][t];
+      } else {
+        const int r = (e % (R / 4)) * 4, k = e / (R / 4);
+        *reinterpret_cast<float4*>(&s[k * LS + r]) = make_float4(v[q][0], v[q][1], v[q][2], v[q][3]);
+      }
+    }
+  }
+  static __device__ __forceinline__ void load4(const float* p, float (&o)[4]) {
+    const float4 t = *reinterpret_cast<const float4*>(p);
+    o[0] = t.x; o[1] = t.y; o[2] = t.z; o[3] = t.w;
+  }
+  static __device__ __forceinline__ void load4(const bf16* p, float (&o)[4]) {
+    const uint2 t = *reinterpret_cast<const uint2*>(p);
+    o[0] = __uint_as_float(t.x << 16); o[1] = __uint_as_float(t.x & 0xffff0000u);
+    o[2] = __uint_as_float(t.y << 16); o[3] = __uint_as_float(t.y & 0xffff0000u);
+  }
+};
 
 template <typename TA, typename TB>
-__global__ __launch_bounds__(256) void k_gemm_reduce(GemmStrided<TA, TB> g, int splits, const float* partial) {
-  const size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x;
-  if (i >= (size_t)g.M * g.N) return;
-  const int m = (int)(i / g.N), n = (int)(i % g.N);
-  double s = 0.0;   // the splits' sums added in double: long reductions (k = rows) keep fp32 accuracy
-  for (int z = 0; z < splits; ++z) s += (double)partial[(size_t)z * g.M * g.N + i];
-  float v = g.alpha * (float)s;
+__device__ __forceinline__ void gemm_epilogue(const GemmStrided<TA, TB>& g, int m, int n, float acc) {
+  float v = g.alpha * acc;
   if (g.bias_f) v += g.bias_f[n];
   if (g.bias_h) v += (float)g.bias_h[n];
   if (g.act == ACT_RELU) v = fmaxf(v, 0.f);
@@ -107,23 +99,106 @@ __global__ __launch_bounds__(256) void k_gemm_reduce(GemmStrided<TA, TB> g, int 
   *c = g.accumulate ? *c + v : v;
 }
 
+// vec_a / vec_b: the operand's vectors are aligned (host-checked).
+template <typename TA, typename TB, int BM>
+__global__ __launch_bounds__(256) void k_gemm_strided(GemmStrided<TA, TB> g, int k_per_split, float* partial,
+                                                      int vec_a, int vec_b) {
+  constexpr int WT = BM / 2, NB = WT / 16, LS = BM + 16;
+  __shared__ __attribute__((aligned(16))) float As[GBK * LS];
+  __shared__ __attribute__((aligned(16))) float Bs[GBK * LS];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, col = lane & 15, g4 = lane >> 4;
+  const int mw = (wave >> 1) * WT, nw = (wave & 1) * WT;
+  const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BM;
+  const int kb = blockIdx.z * k_per_split, ke = min(g.K, kb + k_per_split);
+  const bool a_kfast = g.sak == 1, b_kfast = g.sbk == 1;
+  f32x4 acc[NB][NB];
+#pragma unroll
+  for (int i = 0; i < NB; ++i)
+#pragma unroll
+    for (int j = 0; j < NB; ++j) acc[i][j] = zero4();
+  TileLoad<TA, BM> la;
+  TileLoad<TB, BM> lb;
+  la.load(g.a, g.sam, g.sak, a_kfast, vec_a, m0, g.M, kb, ke);
+  lb.load(g.b, g.sbn, g.sbk, b_kfast, vec_b, n0, g.N, kb, ke);
+  for (int k0 = kb; k0 < ke; k0 += GBK) {
+    __syncthreads();                 // the previous step's fragment reads are done
+    la.store(As, a_kfast);
+    lb.store(Bs, b_kfast);
+    __syncthreads();
+    if (k0 + GBK < ke) {
+      la.load(g.a, g.sam, g.sak, a_kfast, vec_a, m0, g.M, k0 + GBK, ke);
+      lb.load(g.b, g.sbn, g.sbk, b_kfast, vec_b, n0, g.N, k0 + GBK, ke);
+    }
+#pragma unroll
+    for (int ks = 0; ks < GBK / 4; ++ks) {
+      float a[NB], b[NB];
+#pragma unroll
+      for (int i = 0; i < NB; ++i) a[i] = As[(ks * 4 + g4) * LS + mw + 16 * i + col];
+#pragma unroll
+      for (int j = 0; j < NB; ++j) b[j] = Bs[(ks * 4 + g4) * LS + nw + 16 * j + col];
+#pragma unroll
+      for (int i = 0; i < NB; ++i)
+#pragma unroll
+        for (int j = 0; j < NB; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i], b[j], acc[i][j], 0, 0, 0);
+    }
+  }
+  // lane: C rows mw + 16 i + 4 g4 + r, column nw + 16 j + col
+#pragma unroll
+  for (int i = 0; i < NB; ++i)
+#pragma unroll
+    for (int j = 0; j < NB; ++j)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int m = m0 + mw + 16 * i + 4 * g4 + r, n = n0 + nw + 16 * j + col;
+        if (m >= g.M || n >= g.N) continue;
+        if (partial) partial[((size_t)blockIdx.z * g.M + m) * g.N + n] = acc[i][j][r];
+        else gemm_epilogue(g, m, n, acc[i][j][r]);
+      }
+}
+
+template <typename TA, typename TB>
+__global__ __launch_bounds__(256) void k_gemm_reduce(GemmStrided<TA, TB> g, int splits, const float* partial) {
+  const size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x;
+  if (i >= (size_t)g.M * g.N) return;
+  const int m = (int)(i / g.N), n = (int)(i % g.N);
+  double s = 0.0;   // the splits' sums added in double: long reductions (k = rows) keep fp32 accuracy
+  for (int z = 0; z < splits; ++z) s += (double)partial[(size_t)z * g.M * g.N + i];
+  gemm_epilogue(g, m, n, (float)s);
+}
+
+// Vectors of 4 elements of T along the fast dimension are aligned when the
+// base and the other dimension's stride are multiples of 4 elements.
+template <typename T>
+static bool vec_aligned(const T* p, long stride) {
+  return ((uintptr_t)p % (4 * sizeof(T))) == 0 && stride % 4 == 0;
+}
+
 template <typename TA, typename TB>
 hipError_t launch_gemm_strided(const GemmStrided<TA, TB>& g, float* partial, size_t partial_floats, hipStream_t s) {
   if (g.M <= 0 || g.N <= 0) return hipSuccess;
-  const int tiles = ((g.M + GBM - 1) / GBM) * ((g.N + GBN - 1) / GBN);
+  if ((g.sak != 1 && g.sam != 1) || (g.sbk != 1 && g.sbn != 1)) return hipErrorInvalidValue;
   int splits = 1;
   // a long reduction (the weight gradients, k = rows) is split into pieces of
   // at most kSplitRows, each summed in fp32, the pieces added in double
   constexpr int kSplitRows = 1024;
-  (void)tiles;
   if (partial && g.K > kSplitRows) {
     splits = (g.K + kSplitRows - 1) / kSplitRows;
     while (splits > 1 && (size_t)splits * g.M * g.N > partial_floats) --splits;
   }
   const int kps = splits > 1 ? (((g.K + splits - 1) / splits + GBK - 1) / GBK) * GBK : std::max(g.K, 1);
   splits = splits > 1 ? (g.K + kps - 1) / kps : 1;
-  dim3 grid((g.N + GBN - 1) / GBN, (g.M + GBM - 1) / GBM, splits);
-  hipLaunchKernelGGL((k_gemm_strided<TA, TB>), grid, dim3(256), 0, s, g, kps, splits > 1 ? partial : nullptr);
+  const int va = vec_aligned(g.a, g.sak == 1 ? g.sam : g.sak) ? 1 : 0;
+  const int vb = vec_aligned(g.b, g.sbk == 1 ? g.sbn : g.sbk) ? 1 : 0;
+  float* part = splits > 1 ? partial : nullptr;
+  // 128 x 128 tiles when they give at least two work-groups per CU, else 64 x 64
+  const long tiles128 = (long)((g.M + 127) / 128) * ((g.N + 127) / 128) * splits;
+  if (tiles128 >= 512) {
+    dim3 grid((g.N + 127) / 128, (g.M + 127) / 128, splits);
+    hipLaunchKernelGGL((k_gemm_strided<TA, TB, 128>), grid, dim3(256), 0, s, g, kps, part, va, vb);
+  } else {
+    dim3 grid((g.N + 63) / 64, (g.M + 63) / 64, splits);
+    hipLaunchKernelGGL((k_gemm_strided<TA, TB, 64>), grid, dim3(256), 0, s, g, kps, part, va, vb);
+  }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || splits == 1) return e;
   const size_t n = (size_t)g.M * g.N;
