@@ -231,24 +231,52 @@ __global__ __launch_bounds__(256) void k_colsum_partial(const TA* a, int lda, co
   const int g = graph_of_block(ct, chunk);
   const int r0 = ct.ptr[g] + (chunk - ct.blk[g]) * kColRows;
   const int r1 = min(r0 + kColRows, ct.ptr[g + 1]);
-  float s = 0.f;
-  for (int r = r0; r < r1; ++r) {
+  // eight interleaved partial sums (rows r0 + 8 i + u go to sum u), combined in order
+  float s[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  int r = r0;
+  for (; r + 8 <= r1; r += 8) {
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      float v = ld(a, (size_t)(r + u) * lda + c);
+      if (b) v *= b[(size_t)(r + u) * ldb + c];
+      s[u] += v;
+    }
+  }
+  for (; r < r1; ++r) {             // the last (at most 7) rows into sum 0
     float v = ld(a, (size_t)r * lda + c);
     if (b) v *= b[(size_t)r * ldb + c];
-    s += v;
+    s[0] += v;
   }
-  partial[(size_t)chunk * C + c] = s;
+  partial[(size_t)chunk * C + c] = ((s[0] + s[1]) + (s[2] + s[3])) + ((s[4] + s[5]) + (s[6] + s[7]));
 }
 
+// out[g][c] (+)= the graph's chunk sums added in double; 64 columns x 4 chunk
+// quarters per work-group, the quarters combined in order.
 __global__ __launch_bounds__(256) void k_colsum_final(const float* partial, int C, GraphTable ct, float* out, int ldo,
                                                       int accumulate) {
+  __shared__ double q4[4][64];
   const int g = blockIdx.y;
-  const int c = blockIdx.x * 256 + threadIdx.x;
-  if (c >= C) return;
-  double s = 0.0;   // chunk sums added in double
-  for (int k = ct.blk[g]; k < ct.blk[g + 1]; ++k) s += (double)partial[(size_t)k * C + c];
-  float* o = out + (size_t)g * ldo + c;
-  *o = accumulate ? *o + (float)s : (float)s;
+  const int cl = threadIdx.x & 63, part = threadIdx.x >> 6;
+  const int c = blockIdx.x * 64 + cl;
+  const int k0 = ct.blk[g], k1 = ct.blk[g + 1];
+  const int per = (k1 - k0 + 3) / 4;
+  const int ka = k0 + part * per, kz = min(k1, ka + per);
+  double s[4] = {0.0, 0.0, 0.0, 0.0};
+  if (c < C) {
+    int k = ka;
+    for (; k + 4 <= kz; k += 4) {
+#pragma unroll
+      for (int u = 0; u < 4; ++u) s[u] += (double)partial[(size_t)(k + u) * C + c];
+    }
+    for (; k < kz; ++k) s[0] += (double)partial[(size_t)k * C + c];
+  }
+  q4[part][cl] = (s[0] + s[1]) + (s[2] + s[3]);
+  __syncthreads();
+  if (part == 0 && c < C) {
+    const double t = (q4[0][cl] + q4[1][cl]) + (q4[2][cl] + q4[3][cl]);
+    float* o = out + (size_t)g * ldo + c;
+    *o = accumulate ? *o + (float)t : (float)t;
+  }
 }
 
 template <typename TA>
@@ -259,7 +287,7 @@ hipError_t launch_colsum(const TA* a, int lda, const float* b, int ldb, int C, c
                      partial);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_colsum_final, dim3((C + 255) / 256, ct.n), dim3(256), 0, s, (const float*)partial, C, ct, out,
+  hipLaunchKernelGGL(k_colsum_final, dim3((C + 63) / 64, ct.n), dim3(256), 0, s, (const float*)partial, C, ct, out,
                      ldo, accumulate ? 1 : 0);
   return hipGetLastError();
 }
