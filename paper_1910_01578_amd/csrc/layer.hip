@@ -979,22 +979,16 @@ __global__ __launch_bounds__(LNT) void k_pre_layer(PreLayerArgs<T> p, GraphTable
   for (int i = 0; i < G::MB2; ++i) {
     const int row = m0 + rbase + i * 16;
     const int rr = row < p.M ? row : p.M - 1;
-    const float* fg = nullptr;
-    const float* fb = nullptr;
-    if (p.film_gamma) {
-      const size_t g = (size_t)graph_of_node(gt, rr) * p.film_stride;
-      fg = p.film_gamma + g;
-      fb = p.film_beta + g;
-    }
 #pragma unroll
     for (int j = 0; j < G::NB2; ++j) {
-      const int cn = cbase + j * 16;
       float x[4];
-      load4f(p.x + (size_t)rr * p.ldx + cn, x);
+      load4f(p.x + (size_t)rr * p.ldx + cbase + j * 16, x);
 #pragma unroll
-      for (int r = 0; r < 4; ++r) acc[i][j][r] = fg ? fg[cn + r] * x[r] + fb[cn + r] : x[r];
+      for (int r = 0; r < 4; ++r) acc[i][j][r] = x[r];
     }
   }
+  // gamma / beta as 16-byte vectors, loaded again only where a row block starts another graph
+  if (p.film_gamma) film_rows<T, D>(acc, p.film_gamma, p.film_beta, p.film_stride, gt, ln, m0, p.M);
   store_residual<T, D>(acc, L, ln, m0, p.M, p.y_out, p.ldyo);
   typename G::ActFrags af;
   qkv_phase<T, D, 0>(acc, L, af, ln, m0, p.M, p.w_qkv, p.b_qkv, p.qkv_out, p.ldq, p.q_scale);
@@ -1007,6 +1001,8 @@ hipError_t launch_pre_layer(const PreLayerArgs<T>& a, const GraphTable& gt, hipS
   if (!aligned_16(a.w_qkv) || !aligned_16(a.b_qkv) || !aligned_16(a.qkv_out) || a.ldq % (16 / (int)sizeof(T)))
     return hipErrorInvalidValue;
   if (a.ldyo % 4 || !aligned_16(a.y_out)) return hipErrorInvalidValue;
+  if (a.film_gamma && (!a.film_beta || a.film_stride % 4 || !aligned_16(a.film_gamma) || !aligned_16(a.film_beta)))
+    return hipErrorInvalidValue;
   dim3 grid((a.M + LBM - 1) / LBM), block(LNT);
   switch (a.d) {
     case 64: hipLaunchKernelGGL((k_pre_layer<T, 64>), grid, block, 0, s, a, gt); break;
