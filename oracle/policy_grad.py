@@ -148,7 +148,7 @@ def _gnn_forward(x, S, gnn, decisions=None):
             arg, mask = decisions[l]
             arg = np.asarray(arg, np.int64)
             cols = np.broadcast_to(np.arange(P.shape[1]), arg.shape)
-            A = P[torch.as_tensor(np.maximum(arg, 0).copy()), torch.as_tensor(np.ascontiguousarray(cols))]
+            A = P[torch.as_tensor(np.maximum(arg, 0)), torch.as_tensor(np.array(cols))]
             A = torch.where(torch.as_tensor(arg >= 0), A, torch.zeros_like(A))
         h = _relu(h @ lw["w_self"].T + A @ lw["w_neigh"].T + lw["b_upd"], mask)
     return h
