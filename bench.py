@@ -24,8 +24,12 @@ PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}
 PEAK_HBM_GBS = 8000.0
 
 
-def flop_model(cfg, g, stats):
+def flop_model(cfg, g, stats, fused_gnn=False):
     """Algorithmic work per launch of each kernel kind (one layer's launch).
+
+    fused_gnn: the run formed each layer's transform inside the previous
+    layer's update (kind gemm_update_pool), so the separate transform ran for
+    layer 0 only and the plain update for the last layer only.
 
     GEMMs: 2 * M * K * N.  Attention: 4 * d * sum over queries of the keys it
     attends to (QK^T and PV, all heads).  Gather-max: bytes of the sampled
@@ -44,9 +48,11 @@ def flop_model(cfg, g, stats):
     pool = [2.0 * N * (F if l == 0 else H) * H for l in range(L)]
     upd = [2.0 * N * ((F if l == 0 else H) + H) * H for l in range(L)]
     gather_bytes = stats["sum_s"] * (H * b + 4) + N * H * b + 4 * (N + 1)
+    fused = [upd[l] + pool[l + 1] for l in range(L - 1)]
     return {
-        "gemm_pool_sigmoid": ("mfma", float(np.mean(pool))),
-        "gemm_update_relu": ("mfma", float(np.mean(upd))),
+        "gemm_pool_sigmoid": ("mfma", float(pool[0] if fused_gnn else np.mean(pool))),
+        "gemm_update_relu": ("mfma", float(upd[-1] if fused_gnn else np.mean(upd))),
+        "gemm_update_pool": ("mfma", float(np.mean(fused)) if fused else 0.0),
         "gather_max": ("hbm", float(gather_bytes)),
         "pre_layer": ("mfma", 2.0 * N * d * 3 * d),
         "seg_attention": ("mfma", 4.0 * d * keys),
@@ -128,7 +134,7 @@ def config_leg(cfg, steps, cores):
     gdp.timer_begin(range(gdp.K_COUNT))
     r.forward(cfg.sample_seed)
     bd = gdp.timer_end()
-    work, _ = flop_model(cfg, g, stats)
+    work, _ = flop_model(cfg, g, stats, "gemm_update_pool" in bd)
     dominant = max(bd, key=lambda k: bd[k]["ms"])
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
     torch.cuda.synchronize()
@@ -265,7 +271,7 @@ def main():
     gdp.timer_begin(range(gdp.K_COUNT))
     runner.forward(seed)
     breakdown = gdp.timer_end()
-    work, keys = flop_model(cfg, g, stats)
+    work, keys = flop_model(cfg, g, stats, "gemm_update_pool" in breakdown)
     dominant = max(breakdown, key=lambda k: breakdown[k]["ms"])
 
     # Timed region: K steps; events around every step on the launch stream and

@@ -510,6 +510,8 @@ typedef enum gdp_kernel_kind {
   GDP_K_BACKWARD,        /* the backward pass                               */
   GDP_K_ADAM,            /* the Adam update                                 */
   GDP_K_LOGPROB,         /* log-probabilities of given placements           */
+  GDP_K_GEMM_UPDATE_POOL, /* Eq. 3's update fused with the next layer's
+                             Eq. 2 transform of the same rows               */
   GDP_K_COUNT
 } gdp_kernel_kind;
 

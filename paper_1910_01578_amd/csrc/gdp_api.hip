@@ -152,20 +152,36 @@ static int embed_impl(const gdp_graph* g, const gdp_gnn* gnn, T* node_emb, float
   T* hb[2] = {at<T>(ws, pl.h0), at<T>(ws, pl.h1)};
   const T* h = static_cast<const T*>(g->x);
   const int L = gnn->n_layers;
+  bool p_ready = false;                       // P of layer l already formed by layer l - 1's update
   for (int l = 0; l < L; ++l) {
     const gdp_gnn_layer& Lw = gnn->layers[l];
     const int hin = l == 0 ? g->feat_dim : H;
     T* hout = (l == L - 1) ? node_emb : hb[l & 1];
-    const GemmArgs<T, T, T> pool = {h, hin, static_cast<const T*>(Lw.w_pool), hin, nullptr, 0, nullptr, 0,
-                                    static_cast<const T*>(Lw.b_pool), P, H, N, H};
-    if (row_gemm_supported(pool)) GDP_LAUNCH(GDP_K_GEMM_POOL, (launch_row_gemm<T>(pool, EPI_SIGMOID, st)));
-    else GDP_LAUNCH(GDP_K_GEMM_POOL, (launch_gemm<T, T, T>(pool, EPI_SIGMOID, st)));
+    if (!p_ready) {
+      const GemmArgs<T, T, T> pool = {h, hin, static_cast<const T*>(Lw.w_pool), hin, nullptr, 0, nullptr, 0,
+                                      static_cast<const T*>(Lw.b_pool), P, H, N, H};
+      if (row_gemm_supported(pool)) GDP_LAUNCH(GDP_K_GEMM_POOL, (launch_row_gemm<T>(pool, EPI_SIGMOID, st)));
+      else GDP_LAUNCH(GDP_K_GEMM_POOL, (launch_gemm<T, T, T>(pool, EPI_SIGMOID, st)));
+    }
     GDP_LAUNCH(GDP_K_GATHER_MAX, launch_gather_max<T>(P, s_ptr, s_idx, N, H, A, st));
     const GemmArgs<T, T, T> upd = {h, hin, static_cast<const T*>(Lw.w_self), hin, A, H,
                                    static_cast<const T*>(Lw.w_neigh), H, static_cast<const T*>(Lw.b_upd), hout, H,
                                    N, H};
-    if (row_gemm_supported(upd)) GDP_LAUNCH(GDP_K_GEMM_UPDATE, (launch_row_gemm<T>(upd, EPI_RELU, st)));
-    else GDP_LAUNCH(GDP_K_GEMM_UPDATE, (launch_gemm<T, T, T>(upd, EPI_RELU, st)));
+    // the next layer's transform of these rows in the same kernel (P is free:
+    // this layer's gather has read it)
+    p_ready = false;
+    if (l + 1 < L) {
+      const gdp_gnn_layer& Ln = gnn->layers[l + 1];
+      const RowPoolArgs<T> nxt = {static_cast<const T*>(Ln.w_pool), static_cast<const T*>(Ln.b_pool), P, H};
+      if (row_gemm_pool_supported(upd, nxt)) {
+        GDP_LAUNCH(GDP_K_GEMM_UPDATE_POOL, launch_row_gemm_pool<T>(upd, nxt, st));
+        p_ready = true;
+      }
+    }
+    if (!p_ready) {
+      if (row_gemm_supported(upd)) GDP_LAUNCH(GDP_K_GEMM_UPDATE, (launch_row_gemm<T>(upd, EPI_RELU, st)));
+      else GDP_LAUNCH(GDP_K_GEMM_UPDATE, (launch_gemm<T, T, T>(upd, EPI_RELU, st)));
+    }
     h = hout;
   }
   GraphTable ct = make_table(g);
@@ -1178,7 +1194,7 @@ extern "C" const char* gdp_kernel_kind_name(int32_t kind) {
       "graph_prep", "nbr_sample",    "gemm_pool_sigmoid", "gather_max", "gemm_update_relu",
       "meanpool",   "film",          "pre_layer",         "seg_attention", "post_attn",
       "head_lse",   "gumbel_sample", "logp_reduce",       "mlp_placer", "ppo_grad",  "head_backward", "advantages",
-      "evaluate", "train_forward", "backward", "adam", "log_prob"};
+      "evaluate", "train_forward", "backward", "adam", "log_prob", "gemm_update_pool"};
   if (kind < 0 || kind >= GDP_K_COUNT) return "";
   return names[kind];
 }

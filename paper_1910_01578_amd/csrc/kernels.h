@@ -64,6 +64,21 @@ template <typename T>
 bool row_gemm_supported(const GemmArgs<T, T, T>& a);
 template <typename T>
 hipError_t launch_row_gemm(const GemmArgs<T, T, T>& a, int epi, hipStream_t s);
+// Eq. 3's update (EPI_RELU, a.out = h') fused with the next layer's Eq. 2
+// transform of the same rows: p_out = sigmoid(h' w_pool^T + b_pool), w_pool
+// [N, N].  Needs row_gemm_supported(a) and N / chunk <= the A ring (bf16: N =
+// 64, 128, 256; fp32: N = 64); row_gemm_pool_supported says whether it applies.
+template <typename T>
+struct RowPoolArgs {
+  const T* w_pool;
+  const T* b_pool;
+  T* p_out;
+  int ldp;
+};
+template <typename T>
+bool row_gemm_pool_supported(const GemmArgs<T, T, T>& a, const RowPoolArgs<T>& q);
+template <typename T>
+hipError_t launch_row_gemm_pool(const GemmArgs<T, T, T>& a, const RowPoolArgs<T>& q, hipStream_t s);
 
 // Everything of a placer layer after its attention, and the start of the next:
 //   Z    = LN1(y + o W_o^T + b_o)

@@ -1031,11 +1031,12 @@ template hipError_t launch_pre_layer<bf16>(const PreLayerArgs<bf16>&, const Grap
 // A(c + R - 2) loads (vmcnt) before its barrier.
 using dma::wait_vm_barrier;
 
-template <typename T, int D, int EPI>
-__global__ __launch_bounds__(LNT) void k_row_gemm(GemmArgs<T, T, T> p) {
+template <typename T, int D, int EPI, bool POOL>
+__global__ __launch_bounds__(LNT) void k_row_gemm(GemmArgs<T, T, T> p, RowPoolArgs<T> q) {
   using G = Geo<T, D>;
   constexpr int FC = G::FC;
   constexpr int R = D >= 256 ? 4 : 2;                     // A ring slots
+  static_assert(!POOL || (EPI == EPI_RELU && D / FC <= R), "the update's output fits the A ring");
   constexpr int AS = LBM * FC, WS = D * FC;               // elements of an A / W chunk
   constexpr int WC = G::NB2 * 16;                         // a row-tiling wave's columns
   using TA = DmaTile<T, LBM, FC>;
@@ -1064,6 +1065,8 @@ __global__ __launch_bounds__(LNT) void k_row_gemm(GemmArgs<T, T, T> p) {
     const int cc = (s1 ? c : c - nk1) * FC;
     dma_tile<T, D, FC>(buf, (s1 ? p.w1 : p.w2) + cc, s1 ? p.k1 : p.k2, D - 1);
   };
+  // pool transform weights, chunk c: columns c*FC .. + FC of W_pool [D, D]
+  auto issue_wp = [&](int c, T* buf) { dma_tile<T, D, FC>(buf, q.w_pool + c * FC, D, D - 1); };
   for (int c = 0; c < R - 1 && c < nk; ++c) issue_a(c);
   issue_w(0, sW0);
   chunk_pairs<0, false>(nk, [&](int c, auto pc) {
@@ -1072,27 +1075,79 @@ __global__ __launch_bounds__(LNT) void k_row_gemm(GemmArgs<T, T, T> p) {
     if (R > 2 && c >= 1 && c + R - 2 < nk) wait_vm_barrier<TA::PER>();
     else wait_vm_barrier<0>();
     if (c + 1 < nk) issue_w(c + 1, P ? sW0 : sW1);      // buffer of chunk c - 1
+    else if (POOL) issue_wp(0, P ? sW0 : sW1);          // the transform's first chunk
     if (c + R - 1 < nk) issue_a(c + R - 1);             // slot of chunk c - 1
     row_mma<T, D>(acc, sA + (c % R) * AS, P ? sW1 : sW0, ln);
   });
 
   // bias + activation
   const int cbase = ln.w2n * G::NB2 * 16 + 4 * ln.g4;
+  auto bias_act = [&](const T* bias, auto epi) {
+    constexpr int E = decltype(epi)::v;
 #pragma unroll
-  for (int j = 0; j < G::NB2; ++j) {
-    float b[4];
+    for (int j = 0; j < G::NB2; ++j) {
+      float b[4];
 #pragma unroll
-    for (int r = 0; r < 4; ++r) b[r] = to_f32(p.bias[cbase + j * 16 + r]);
+      for (int r = 0; r < 4; ++r) b[r] = to_f32(bias[cbase + j * 16 + r]);
+#pragma unroll
+      for (int i = 0; i < G::MB2; ++i)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          float v = acc[i][j][r] + b[r];
+          if (E == EPI_RELU) v = fmaxf(v, 0.f);
+          // the reciprocal instruction (about 1 ulp) instead of an IEEE division
+          if (E == EPI_SIGMOID) v = __builtin_amdgcn_rcpf(1.0f + __expf(-v));
+          acc[i][j][r] = v;
+        }
+    }
+  };
+  bias_act(p.bias, Par<EPI>{});
+  T* out = p.out;
+  int ldo = p.ldo;
+  if constexpr (POOL) {
+    // Eq. 2 of the next layer on the same rows: h' (rounded to T, as the
+    // separate transform would read it) becomes the A operand in the ring
+    // slots; W_pool streams through the two W buffers, chunk c in the buffer
+    // of parity PL ^ 1 ^ (c & 1) (PL: the update's last chunk).
+    constexpr int NC2 = D / FC;
+    using TW = DmaTile<T, D, FC>;
+    const int pl = (nk - 1) & 1;
+    bar_lds();                                          // every wave is done with the update's tiles
+    if (NC2 > 1) issue_wp(1, pl ? sW1 : sW0);           // into the update's last W buffer
+    const int rbase = ln.w2m * G::MB2 * 16 + ln.col;
 #pragma unroll
     for (int i = 0; i < G::MB2; ++i)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        float v = acc[i][j][r] + b[r];
-        if (EPI == EPI_RELU) v = fmaxf(v, 0.f);
-        // the reciprocal instruction (about 1 ulp) instead of an IEEE division
-        if (EPI == EPI_SIGMOID) v = __builtin_amdgcn_rcpf(1.0f + __expf(-v));
-        acc[i][j][r] = v;
+      for (int j = 0; j < G::NB2; ++j) {
+        const int c = cbase + j * 16;
+        const float v[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
+        store4(&sA[(c / FC) * AS + swz<T, FC>(rbase + i * 16, c % FC)], v);
+        acc[i][j] = zero4();
       }
+    // Chunk c: W_pool(c) and h' in place (chunk 0 leaves W_pool(1), the
+    // wave's only later load, in flight); W_pool(c + 1), c >= 1, goes into the
+    // buffer of chunk c - 1.  Once the last chunk's barrier has passed, no
+    // wait for loads follows, so h' leaves then, from the ring slots as whole
+    // 16-byte granules of its rows, beside that chunk's products.
+    for (int c = 0; c < NC2; ++c) {
+      if (c == 0 && NC2 > 1) wait_vm_barrier<TW::PER>();
+      else wait_vm_barrier<0>();
+      T* cur = ((pl ^ 1 ^ c) & 1) ? sW1 : sW0;
+      if (c >= 1 && c + 1 < NC2) issue_wp(c + 1, cur == sW0 ? sW1 : sW0);
+      if (c == NC2 - 1) {
+        constexpr int EPV = 16 / (int)sizeof(T), GR = D / EPV, GC = FC / EPV;
+        for (int e = threadIdx.x; e < LBM * GR; e += LNT) {
+          const int row = e / GR, gc = e % GR;
+          if (m0 + row < p.M)
+            *reinterpret_cast<uint4*>(p.out + (size_t)(m0 + row) * p.ldo + gc * EPV) =
+                *reinterpret_cast<const uint4*>(&sA[(gc / GC) * AS + swz<T, FC>(row, (gc % GC) * EPV)]);
+        }
+      }
+      row_mma<T, D>(acc, sA + c * AS, cur, ln);
+    }
+    bias_act(q.b_pool, Par<EPI_SIGMOID>{});
+    out = q.p_out;
+    ldo = q.ldp;
   }
   constexpr int RB = WC * (int)sizeof(T);                 // bytes of a row of the wave's columns
   if constexpr (sizeof(T) == 2 && RB >= 64) {
@@ -1113,7 +1168,7 @@ __global__ __launch_bounds__(LNT) void k_row_gemm(GemmArgs<T, T, T> p) {
         const int rr = ln.lane / LPR + RPI * hf, gg = ln.lane % LPR;
         const uint4 v = *reinterpret_cast<const uint4*>(&reg[swz<T, WC>(rr, gg * EPV)]);
         if (rblk + rr < p.M)
-          *reinterpret_cast<uint4*>(p.out + (size_t)(rblk + rr) * p.ldo + ln.w2n * WC + gg * EPV) = v;
+          *reinterpret_cast<uint4*>(out + (size_t)(rblk + rr) * ldo + ln.w2n * WC + gg * EPV) = v;
       }
     }
   } else {
@@ -1124,7 +1179,7 @@ __global__ __launch_bounds__(LNT) void k_row_gemm(GemmArgs<T, T, T> p) {
 #pragma unroll
         for (int j = 0; j < G::NB2; ++j) {
           const float v[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
-          store4(p.out + (size_t)row * p.ldo + cbase + j * 16, v);
+          store4(out + (size_t)row * ldo + cbase + j * 16, v);
         }
       }
     }
@@ -1147,12 +1202,15 @@ hipError_t launch_row_gemm(const GemmArgs<T, T, T>& a, int epi, hipStream_t s) {
   if (a.M <= 0) return hipSuccess;
   if (!row_gemm_supported(a)) return hipErrorInvalidValue;
   dim3 grid((a.M + LBM - 1) / LBM), block(LNT);
-#define GDP_ROW_GEMM(DV)                                                                                      \
-  switch (epi) {                                                                                              \
-    case EPI_BIAS: hipLaunchKernelGGL((k_row_gemm<T, DV, EPI_BIAS>), grid, block, 0, s, a); break;            \
-    case EPI_RELU: hipLaunchKernelGGL((k_row_gemm<T, DV, EPI_RELU>), grid, block, 0, s, a); break;            \
-    case EPI_SIGMOID: hipLaunchKernelGGL((k_row_gemm<T, DV, EPI_SIGMOID>), grid, block, 0, s, a); break;      \
-    default: return hipErrorInvalidValue;                                                                     \
+  const RowPoolArgs<T> none = {};
+#define GDP_ROW_GEMM(DV)                                                                                          \
+  switch (epi) {                                                                                                  \
+    case EPI_BIAS: hipLaunchKernelGGL((k_row_gemm<T, DV, EPI_BIAS, false>), grid, block, 0, s, a, none); break;   \
+    case EPI_RELU: hipLaunchKernelGGL((k_row_gemm<T, DV, EPI_RELU, false>), grid, block, 0, s, a, none); break;   \
+    case EPI_SIGMOID:                                                                                             \
+      hipLaunchKernelGGL((k_row_gemm<T, DV, EPI_SIGMOID, false>), grid, block, 0, s, a, none);                    \
+      break;                                                                                                      \
+    default: return hipErrorInvalidValue;                                                                         \
   }
   switch (a.N) {
     case 64: GDP_ROW_GEMM(64) break;
@@ -1165,5 +1223,37 @@ hipError_t launch_row_gemm(const GemmArgs<T, T, T>& a, int epi, hipStream_t s) {
 }
 template hipError_t launch_row_gemm<float>(const GemmArgs<float, float, float>&, int, hipStream_t);
 template hipError_t launch_row_gemm<bf16>(const GemmArgs<bf16, bf16, bf16>&, int, hipStream_t);
+
+template <typename T>
+bool row_gemm_pool_supported(const GemmArgs<T, T, T>& a, const RowPoolArgs<T>& q) {
+  return row_gemm_supported(a) && a.N / LayerCfg<T>::FC <= (a.N >= 256 ? 4 : 2) && q.w_pool && q.b_pool &&
+         q.p_out && aligned_16(q.w_pool) && aligned_16(q.p_out) && q.ldp % (16 / (int)sizeof(T)) == 0;
+}
+template bool row_gemm_pool_supported<float>(const GemmArgs<float, float, float>&, const RowPoolArgs<float>&);
+template bool row_gemm_pool_supported<bf16>(const GemmArgs<bf16, bf16, bf16>&, const RowPoolArgs<bf16>&);
+
+template <typename T>
+hipError_t launch_row_gemm_pool(const GemmArgs<T, T, T>& a, const RowPoolArgs<T>& q, hipStream_t s) {
+  if (a.M <= 0) return hipSuccess;
+  if (!row_gemm_pool_supported(a, q)) return hipErrorInvalidValue;
+  dim3 grid((a.M + LBM - 1) / LBM), block(LNT);
+  switch (a.N) {
+    case 64: hipLaunchKernelGGL((k_row_gemm<T, 64, EPI_RELU, true>), grid, block, 0, s, a, q); break;
+    case 128:
+      if constexpr (LayerCfg<T>::FC == 64) hipLaunchKernelGGL((k_row_gemm<T, 128, EPI_RELU, true>), grid, block, 0, s, a, q);
+      else return hipErrorInvalidValue;
+      break;
+    case 256:
+      if constexpr (LayerCfg<T>::FC == 64) hipLaunchKernelGGL((k_row_gemm<T, 256, EPI_RELU, true>), grid, block, 0, s, a, q);
+      else return hipErrorInvalidValue;
+      break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+template hipError_t launch_row_gemm_pool<float>(const GemmArgs<float, float, float>&, const RowPoolArgs<float>&,
+                                                hipStream_t);
+template hipError_t launch_row_gemm_pool<bf16>(const GemmArgs<bf16, bf16, bf16>&, const RowPoolArgs<bf16>&,
+                                               hipStream_t);
 
 }  // namespace gdp

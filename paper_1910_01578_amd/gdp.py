@@ -32,7 +32,7 @@ GDP_NOALLOC_SCRATCH_BYTES = 4 << 20
 KERNEL_KINDS = ["graph_prep", "nbr_sample", "gemm_pool_sigmoid", "gather_max", "gemm_update_relu",
                 "meanpool", "film", "pre_layer", "seg_attention", "post_attn",
                 "head_lse", "gumbel_sample", "logp_reduce", "mlp_placer", "ppo_grad", "head_backward", "advantages",
-                "evaluate", "train_forward", "backward", "adam", "log_prob"]
+                "evaluate", "train_forward", "backward", "adam", "log_prob", "gemm_update_pool"]
 K_COUNT = len(KERNEL_KINDS)
 
 

@@ -57,6 +57,23 @@ def test_headline_workload_work_model():
     assert work["gather_max"][0] == "hbm" and abs(work["gather_max"][1] / 1e6 - 134.07) < 0.005
 
 
+def test_fused_gnn_work_model():
+    """With the update of layer l fused to the transform of layer l + 1, the
+    three GNN kinds together still count every layer's products once."""
+    cfg = W.get_config("gnmt8_52000")
+    g = types.SimpleNamespace(n_nodes=52000, graph_ptr=np.array([0, 52000]))
+    N, H, F, L = 52000, cfg.hidden, cfg.feat_dim, cfg.gnn_layers
+    plain, _ = bench.flop_model(cfg, g, {"sum_s": 0})
+    fused, _ = bench.flop_model(cfg, g, {"sum_s": 0}, fused_gnn=True)
+    total_plain = L * (plain["gemm_pool_sigmoid"][1] + plain["gemm_update_relu"][1])
+    total_fused = fused["gemm_pool_sigmoid"][1] + fused["gemm_update_relu"][1] + (L - 1) * fused["gemm_update_pool"][1]
+    assert abs(total_fused - total_plain) <= 1e-6 * total_plain
+    assert fused["gemm_pool_sigmoid"][1] == 2.0 * N * F * H                       # layer 0 only
+    # launch l: layer l's update (layer 0 reads the F input features) and layer l + 1's transform
+    per_launch = [2.0 * N * ((F if l == 0 else H) + H) * H + 2.0 * N * H * H for l in range(L - 1)]
+    assert abs(fused["gemm_update_pool"][1] - sum(per_launch) / (L - 1)) <= 1e-9 * per_launch[0]
+
+
 def test_recorded_traffic_goes_stale_with_its_source(monkeypatch):
     rec = bench.measured_traffic("post_attn")
     if rec is not None:
