@@ -13,7 +13,9 @@ every step of an iteration runs in the library's kernels:
              gdp_ppo_grad, gdp_backward, gdp_adam_step
 
 The paper trains on measured run times of real placements; here the
-simulated run time of gdp_evaluate stands in for them.
+simulated run time of gdp_evaluate stands in for them.  Evaluation and reward
+run on a second stream, beside the first epoch's training forward and
+log-probs (which need only the placements); the PPO gradient waits for both.
 """
 from __future__ import annotations
 
@@ -54,6 +56,9 @@ class GDPBatch:
         self.evaluator = gdp.Evaluator(self.dg, cfg.n_devices, self.k, costs, device)
         self.baseline = gdp.RewardBaseline(self.dg.n_graphs, device)
         self.history: List[Dict[str, np.ndarray]] = []
+        # the simulated run times and rewards run here, beside the first PPO
+        # epoch's forward and log-probs, which need only the placements
+        self.side = gdp._torch().cuda.Stream(device=device)
 
     def step(self, seed: int) -> Dict[str, np.ndarray]:
         """One iteration: sample, evaluate, reward, PPO update.  Returns the
@@ -62,10 +67,16 @@ class GDPBatch:
         r, t, p = self.runner, self.trainer, self.ppo
         r.forward(seed)
         placements = r.placements
-        mk, valid, run_time = self.evaluator.evaluate(placements, p.time_unit)
-        reward, adv = self.baseline.advantages(run_time, valid)
+        main = torch.cuda.current_stream()
+        self.side.wait_stream(main)                 # the placements are complete
+        with torch.cuda.stream(self.side):
+            mk, valid, run_time = self.evaluator.evaluate(placements, p.time_unit)
+            reward, adv = self.baseline.advantages(run_time, valid)
         t.forward()
         logp_old = t.log_prob(placements)
+        main.wait_stream(self.side)                 # rewards and advantages are complete
+        for x in (reward, adv):
+            x.record_stream(main)                   # allocated on the side stream, used on this one
         loss = None
         for e in range(p.epochs):
             if e > 0:
