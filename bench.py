@@ -24,12 +24,15 @@ PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}
 PEAK_HBM_GBS = 8000.0
 
 
-def flop_model(cfg, g, stats, fused_gnn=False):
+def flop_model(cfg, g, stats, fused_gnn=False, launches=None):
     """Algorithmic work per launch of each kernel kind (one layer's launch).
 
     fused_gnn: the run formed each layer's transform inside the previous
     layer's update (kind gemm_update_pool), so the separate transform ran for
     layer 0 only and the plain update for the last layer only.
+    launches: launches per step of each kind, where the run split a layer's
+    projection, attention and post-attention kernels over two row ranges (two
+    launches each); the work of a step is then averaged over its launches.
 
     GEMMs: 2 * M * K * N.  Attention: 4 * d * sum over queries of the keys it
     attends to (QK^T and PV, all heads).  Gather-max: bytes of the sampled
@@ -49,17 +52,21 @@ def flop_model(cfg, g, stats, fused_gnn=False):
     upd = [2.0 * N * ((F if l == 0 else H) + H) * H for l in range(L)]
     gather_bytes = stats["sum_s"] * (H * b + 4) + N * H * b + 4 * (N + 1)
     fused = [upd[l] + pool[l + 1] for l in range(L - 1)]
+    P = cfg.placer_layers
+    # per step: one projection, P attention and P post-attention passes (W_o,
+    # the FFN, and all but the last layer's next QKV projection)
+    step = {"pre_layer": (2.0 * N * d * 3 * d, 1),
+            "seg_attention": (4.0 * d * keys * P, P),
+            "post_attn": (P * (2.0 * N * d * d + 4.0 * N * d * dff) + (P - 1) * 2.0 * N * d * 3 * d, P)}
+    per_launch = {k: tot / ((launches or {}).get(k) or n) for k, (tot, n) in step.items()}
     return {
         "gemm_pool_sigmoid": ("mfma", float(pool[0] if fused_gnn else np.mean(pool))),
         "gemm_update_relu": ("mfma", float(upd[-1] if fused_gnn else np.mean(upd))),
         "gemm_update_pool": ("mfma", float(np.mean(fused)) if fused else 0.0),
         "gather_max": ("hbm", float(gather_bytes)),
-        "pre_layer": ("mfma", 2.0 * N * d * 3 * d),
-        "seg_attention": ("mfma", 4.0 * d * keys),
-        # per launch, averaged over the placer layers: W_o, the FFN, and (all but
-        # the last layer) the next layer's QKV projection
-        "post_attn": ("mfma", 2.0 * N * d * d + 4.0 * N * d * dff
-                      + (cfg.placer_layers - 1) / cfg.placer_layers * 2.0 * N * d * 3 * d),
+        "pre_layer": ("mfma", per_launch["pre_layer"]),
+        "seg_attention": ("mfma", per_launch["seg_attention"]),
+        "post_attn": ("mfma", per_launch["post_attn"]),
         # the ablation's placer without attention: every layer's FFN and the head, one launch
         "mlp_placer": ("mfma", 4.0 * N * d * dff * cfg.placer_layers + 2.0 * N * d * cfg.n_devices),
     }, keys
@@ -134,7 +141,7 @@ def config_leg(cfg, steps, cores):
     gdp.timer_begin(range(gdp.K_COUNT))
     r.forward(cfg.sample_seed)
     bd = gdp.timer_end()
-    work, _ = flop_model(cfg, g, stats, "gemm_update_pool" in bd)
+    work, _ = flop_model(cfg, g, stats, "gemm_update_pool" in bd, {k: v["launches"] for k, v in bd.items()})
     dominant = max(bd, key=lambda k: bd[k]["ms"])
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
     torch.cuda.synchronize()
@@ -271,7 +278,8 @@ def main():
     gdp.timer_begin(range(gdp.K_COUNT))
     runner.forward(seed)
     breakdown = gdp.timer_end()
-    work, keys = flop_model(cfg, g, stats, "gemm_update_pool" in breakdown)
+    work, keys = flop_model(cfg, g, stats, "gemm_update_pool" in breakdown,
+                            {k: v["launches"] for k, v in breakdown.items()})
     dominant = max(breakdown, key=lambda k: breakdown[k]["ms"])
 
     # Timed region: K steps; events around every step on the launch stream and
@@ -295,10 +303,11 @@ def main():
                    "max_ms": round(float(step_ms.max()), 4),
                    "nodes_per_s_at_median": round(g.n_nodes / (float(np.median(step_ms)) * 1e-3), 1)}
 
-    def roof(kind, ms_total, launches):
-        if kind not in work or launches == 0:
+    def roof(kind, ms_total, launches, wk=None):
+        wk = work if wk is None else wk
+        if kind not in wk or launches == 0:
             return None
-        bound, amount = work[kind]
+        bound, amount = wk[kind]
         sec = ms_total / launches / 1e3
         if bound == "mfma":
             ach = amount / sec / 1e12
@@ -316,13 +325,50 @@ def main():
     roofline["avg_launch_us"] = round(1e3 * dom["ms"] / dom["launches"], 2)
     roofline["traffic"] = measured_traffic(dominant)
 
-    kernels = []
-    for kind, v in sorted(breakdown.items(), key=lambda kv: -kv[1]["ms"]):
-        ent = {"kernel": kind, "ms_per_step": round(v["ms"], 4), "launches": v["launches"]}
-        rf = roof(kind, v["ms"], v["launches"])
-        if rf:
-            ent.update({"achieved": rf["achieved"], "unit": rf["unit"], "frac": rf["frac"], "bound": rf["bound"]})
-        kernels.append(ent)
+    def kernel_table(bd, wk):
+        rows = []
+        for kind, v in sorted(bd.items(), key=lambda kv: -kv[1]["ms"]):
+            ent = {"kernel": kind, "ms_per_step": round(v["ms"], 4), "launches": v["launches"]}
+            rf = roof(kind, v["ms"], v["launches"], wk)
+            if rf:
+                ent.update({"achieved": rf["achieved"], "unit": rf["unit"], "frac": rf["frac"], "bound": rf["bound"]})
+            rows.append(ent)
+        return rows
+
+    kernels = kernel_table(breakdown, work)
+    two_part = breakdown.get("post_attn", {}).get("launches", 0) > cfg.placer_layers
+    roofline["schedule"] = "two-part" if two_part else "one stream"
+
+    # The same step with every launch on the caller's stream (one launch per
+    # kernel and layer, nothing overlapping): each kernel's own duration.  In
+    # the two-part schedule a launch shares the chip with the other part's
+    # kernels, and its event-timed duration includes that sharing.
+    kernels_one_stream = None
+    if two_part:
+        gdp.set_place_streams(1)
+        try:
+            runner.forward(seed)
+            gdp.timer_begin(range(gdp.K_COUNT))
+            runner.forward(seed)
+            bd1 = gdp.timer_end()
+            work1, _ = flop_model(cfg, g, stats, "gemm_update_pool" in bd1,
+                                  {k: v["launches"] for k, v in bd1.items()})
+            n_iso = max(1, min(args.steps, 10))
+            t0 = time.perf_counter()
+            gdp.timer_begin([dominant])
+            for _ in range(n_iso):
+                runner.forward(seed)
+            torch.cuda.synchronize()
+            iso = gdp.timer_end()[dominant]
+            iso_s = (time.perf_counter() - t0) / n_iso
+        finally:
+            gdp.set_place_streams(2)
+        rf1 = roof(dominant, iso["ms"], iso["launches"], work1) or {}
+        roofline["one_stream"] = {"avg_launch_us": round(1e3 * iso["ms"] / iso["launches"], 2),
+                                  "launches_per_step": iso["launches"] // n_iso,
+                                  "achieved": rf1.get("achieved"), "frac": rf1.get("frac"),
+                                  "ms_per_step": round(1e3 * iso_s, 4)}
+        kernels_one_stream = kernel_table(bd1, work1)
 
     # The same step captured once into a HIP graph and replayed K times (the
     # library allocates nothing and records no memset, so a step can be
@@ -482,6 +528,7 @@ def main():
         "cpu_baseline": cpu,
         "step_events": step_events,
         "kernels": kernels,
+        "kernels_one_stream": kernels_one_stream,
         "configs": configs,
         "training": training,
         "graph_replay": graph_replay,

@@ -35,6 +35,11 @@
  *  - Streams.  `stream` is a hipStream_t (NULL = the default stream).  Calls
  *    only enqueue work and return without synchronising.  A workspace may be
  *    shared by several calls only if they are ordered on one stream.
+ *    gdp_place and gdp_place_train may run part of their work on a second
+ *    stream of the library's (see gdp_set_place_streams); it starts after
+ *    the work enqueued on `stream` before the call, and work enqueued on
+ *    `stream` after the call waits for it, so the ordering seen on `stream`
+ *    is that of a single-stream call, HIP graph capture included.
  *  - Errors.  Calls return GDP_OK (0) or a negative gdp_status.  On a
  *    validation error nothing is enqueued and no output is touched;
  *    gdp_last_error() then describes the failure (thread-local string).
@@ -200,6 +205,21 @@ int gdp_embed(const gdp_graph* g, const gdp_gnn* gnn, void* node_emb, float* gra
 int gdp_place(const gdp_graph* g, const void* node_emb, const float* graph_emb,
               const gdp_placer* placer, float* logits, float* lse,
               void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Stream schedule of gdp_place and gdp_place_train for the calling thread
+ * (a scheduling choice only: the results are the same bit for bit).
+ *   n = 2 (the default): with attention and at least 40,960 nodes, the rows
+ *     are split at a segment start near row 32,768 into parts A and B;
+ *     every kernel of a layer runs once per part, A's on a second stream
+ *     (one per device and calling thread, default priority, created at the
+ *     first such call and kept until the process ends) and B's on `stream`,
+ *     so that the parts of consecutive layers overlap.  The workspace holds
+ *     a second copy of the QKV buffer for it.
+ *   n = 1: every launch on `stream`, one launch per kernel and layer.
+ * Returns GDP_E_INVALID_ARG for any other n.
+ */
+int gdp_set_place_streams(int32_t n);
 
 /*
  * Whole-graph sampling: K placements of every op at once (Section 3), by

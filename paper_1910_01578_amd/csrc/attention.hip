@@ -167,7 +167,7 @@ void k_seg_attention(AttnArgs<T> p, GraphTable gt) {
   const int col = lane & 15, g4 = lane >> 4;
   // heads fastest, remapped so that the heads of one query block (whose K/V
   // slices share cache lines) run on one XCD
-  const int logical = xcd_remap(blockIdx.x, gridDim.x);
+  const int logical = p.qblock0 * p.heads + xcd_remap(blockIdx.x, gridDim.x);
   const int head = logical % p.heads;
   const int qblk = logical / p.heads;
 
@@ -500,6 +500,7 @@ void k_seg_attention(AttnArgs<T> p, GraphTable gt) {
 template <typename T>
 hipError_t launch_attention(const AttnArgs<T>& a, const GraphTable& gt, hipStream_t s) {
   if (a.total_qblocks <= 0) return hipSuccess;
+  if (a.qblock0 < 0) return hipErrorInvalidValue;
   const int dh = a.d / a.heads;
   dim3 grid(a.total_qblocks * a.heads), block(256);
   switch (dh) {

@@ -72,15 +72,73 @@ static int hip_fail(hipError_t e, const char* what) {
   return fail(GDP_E_HIP, "%s: %s", what, hipGetErrorString(e));
 }
 
-#define GDP_LAUNCH(kind, ...)                                    \
+// A launch on stream `stream` (timed there when its kind is selected).
+#define GDP_LAUNCH_ON(kind, stream, ...)                         \
   do {                                                           \
     hipError_t _e;                                               \
     {                                                            \
-      Timed _t((kind), st);                                      \
+      Timed _t((kind), (stream));                                \
       _e = (__VA_ARGS__);                                        \
     }                                                            \
     if (_e != hipSuccess) return hip_fail(_e, #__VA_ARGS__);     \
   } while (0)
+// A launch on the call's stream st.
+#define GDP_LAUNCH(kind, ...) GDP_LAUNCH_ON(kind, st, __VA_ARGS__)
+
+#define GDP_HIP(...)                                             \
+  do {                                                           \
+    const hipError_t _e = (__VA_ARGS__);                         \
+    if (_e != hipSuccess) return hip_fail(_e, #__VA_ARGS__);     \
+  } while (0)
+
+namespace {
+// A second stream of the calling thread on one device, for the two-part
+// layer schedule of gdp_place, with the events that order it against the
+// call's stream: fork and join, and two alternating pairs for the
+// cross-part dependencies.  Created at a thread's first such call on the
+// device (default priority, non-blocking) and held until the process ends.
+struct SideStream {
+  int device = -1;
+  hipStream_t s = nullptr;
+  hipEvent_t fork = nullptr, join = nullptr;
+  hipEvent_t a[2] = {nullptr, nullptr}, b[2] = {nullptr, nullptr};
+};
+thread_local std::vector<SideStream> g_side;
+// gdp_set_place_streams: 2 = two-part schedule where it applies, 1 = one stream
+thread_local int g_place_streams = 2;
+
+int side_stream(hipStream_t st, SideStream** out) {
+  int dev = -1;
+  hipError_t e = hipStreamGetDevice(st, &dev);
+  if (e != hipSuccess) return hip_fail(e, "hipStreamGetDevice");
+  for (SideStream& x : g_side)
+    if (x.device == dev) {
+      *out = &x;
+      return GDP_OK;
+    }
+  int cur = -1;
+  if ((e = hipGetDevice(&cur)) != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (cur != dev && (e = hipSetDevice(dev)) != hipSuccess) return hip_fail(e, "hipSetDevice");
+  SideStream x;
+  x.device = dev;
+  e = hipStreamCreateWithFlags(&x.s, hipStreamNonBlocking);
+  hipEvent_t* evs[6] = {&x.fork, &x.join, &x.a[0], &x.a[1], &x.b[0], &x.b[1]};
+  for (int i = 0; i < 6 && e == hipSuccess; ++i) e = hipEventCreateWithFlags(evs[i], hipEventDisableTiming);
+  if (cur != dev) {
+    const hipError_t e2 = hipSetDevice(cur);
+    if (e == hipSuccess) e = e2;
+  }
+  if (e != hipSuccess) {   // release what was created
+    for (int i = 0; i < 6; ++i)
+      if (*evs[i]) (void)hipEventDestroy(*evs[i]);
+    if (x.s) (void)hipStreamDestroy(x.s);
+    return hip_fail(e, "side stream");
+  }
+  g_side.push_back(x);
+  *out = &g_side.back();
+  return GDP_OK;
+}
+}  // namespace
 
 static GraphTable make_table(const gdp_graph* g) {
   GraphTable t;
@@ -203,10 +261,8 @@ static int place_impl(const gdp_graph* g, const T* node_emb, const float* graph_
   auto beta_of = [&](int l) { return film + (size_t)l * 2 * G * d + (size_t)G * d; };
   // Residual stream (layer inputs Y) in fp32; attention inputs and outputs in T.
   float* ybuf[2] = {at<float>(ws, pl.y0), at<float>(ws, pl.y1)};
-  T* qkv = at<T>(ws, pl.qkv);
   T* o = at<T>(ws, pl.o);
 
-  const float* y = ybuf[0];
   if (p->film) {
     for (int l0 = 0; l0 < L; l0 += kFilmLayersPerLaunch) {
       const int nl = std::min(kFilmLayersPerLaunch, L - l0);
@@ -265,52 +321,117 @@ static int place_impl(const gdp_graph* g, const T* node_emb, const float* graph_
   GraphTable qt = make_table(g);
   const int qblocks = prefix_blocks_attention(g->graph_ptr_h, G, p->seg_len, kAttnQ, qt.blk);
   const float q_scale = attn_q_scale(d / p->n_heads);
-  // Layer 0's FiLM and projection run in their own kernel; every later
-  // projection is fused into the previous layer's post-attention kernel.
-  {
-    const gdp_placer_layer& L0 = p->layers[0];
-    const PreLayerArgs<T> a_pre = {node_emb, d, p->film ? gamma_of(0) : nullptr, p->film ? beta_of(0) : nullptr, d,
-                                   ybuf[0], d, static_cast<const T*>(L0.w_qkv), static_cast<const T*>(L0.b_qkv),
-                                   qkv, 3 * d, N, d, q_scale};
-    GDP_LAUNCH(GDP_K_PRE_LAYER, launch_pre_layer<T>(a_pre, gt, st));
-  }
   // The head runs inside the last layer's kernel when D is small enough.
   const bool fused_head = p->n_devices <= kFusedHeadDevices;
-  int cur = 0;
-  for (int l = 0; l < L; ++l) {
+  // Layer 0's FiLM and projection run in their own kernel; every later
+  // projection is fused into the previous layer's post-attention kernel.
+  auto pre_args = [&](T* qkv_out, int row0) {
+    const gdp_placer_layer& L0 = p->layers[0];
+    PreLayerArgs<T> a = {node_emb, d, p->film ? gamma_of(0) : nullptr, p->film ? beta_of(0) : nullptr, d,
+                         ybuf[0], d, static_cast<const T*>(L0.w_qkv), static_cast<const T*>(L0.b_qkv),
+                         qkv_out, 3 * d, N, d, q_scale};
+    a.row0 = row0;
+    return a;
+  };
+  auto attn_args = [&](const T* qkv_in, int qb0, int nqb) {
+    AttnArgs<T> a = {qkv_in, 3 * d, o, d, d, p->n_heads, p->seg_len, p->mem_len, nqb};
+    a.qblock0 = qb0;
+    return a;
+  };
+  // Layer l's post-attention kernel on rows row0 .. N - 1, reading layer l's
+  // input y and writing ynext and the next layer's QKV into qkv_out.
+  auto post_args = [&](int l, const float* yin, float* ynext, T* qkv_out, int row0) {
     const gdp_placer_layer& Ly = p->layers[l];
-    const AttnArgs<T> a_att = {qkv, 3 * d, o, d, d, p->n_heads, p->seg_len, p->mem_len, qblocks};
-    GDP_LAUNCH(GDP_K_ATTENTION, launch_attention<T>(a_att, qt, st));
     const bool last = l + 1 == L;
     const bool next_film = p->film && !last;
     const gdp_placer_layer* Ln = last ? nullptr : &p->layers[l + 1];
-    float* ynext = last && x_out ? x_out : ybuf[cur ^ 1];
-    PostAttnArgs<T> a_post = {o, d, y, d,
-                                    static_cast<const T*>(Ly.w_o), static_cast<const T*>(Ly.b_o),
-                                    static_cast<const T*>(Ly.ln1_g), static_cast<const T*>(Ly.ln1_b),
-                                    static_cast<const T*>(Ly.w_1), static_cast<const T*>(Ly.b_1),
-                                    static_cast<const T*>(Ly.w_2), static_cast<const T*>(Ly.b_2),
-                                    static_cast<const T*>(Ly.ln2_g), static_cast<const T*>(Ly.ln2_b),
-                                    next_film ? gamma_of(l + 1) : nullptr, next_film ? beta_of(l + 1) : nullptr, d,
-                                    ynext, d,
-                                    Ln ? static_cast<const T*>(Ln->w_qkv) : nullptr,
-                                    Ln ? static_cast<const T*>(Ln->b_qkv) : nullptr,
-                                    Ln ? qkv : nullptr, 3 * d, N, d, p->d_ff, q_scale};
+    PostAttnArgs<T> a = {o, d, yin, d,
+                         static_cast<const T*>(Ly.w_o), static_cast<const T*>(Ly.b_o),
+                         static_cast<const T*>(Ly.ln1_g), static_cast<const T*>(Ly.ln1_b),
+                         static_cast<const T*>(Ly.w_1), static_cast<const T*>(Ly.b_1),
+                         static_cast<const T*>(Ly.w_2), static_cast<const T*>(Ly.b_2),
+                         static_cast<const T*>(Ly.ln2_g), static_cast<const T*>(Ly.ln2_b),
+                         next_film ? gamma_of(l + 1) : nullptr, next_film ? beta_of(l + 1) : nullptr, d,
+                         ynext, d,
+                         Ln ? static_cast<const T*>(Ln->w_qkv) : nullptr,
+                         Ln ? static_cast<const T*>(Ln->b_qkv) : nullptr,
+                         Ln ? qkv_out : nullptr, 3 * d, N, d, p->d_ff, q_scale};
     if (last && fused_head) {
-      a_post.y_out = x_out;                  // only the head reads the last layer's output, unless asked for
-      a_post.w_out = static_cast<const T*>(p->w_out);
-      a_post.b_out = static_cast<const T*>(p->b_out);
-      a_post.n_dev = p->n_devices;
-      a_post.logits = logits;
-      a_post.lse = lse;
+      a.y_out = x_out;                  // only the head reads the last layer's output, unless asked for
+      a.w_out = static_cast<const T*>(p->w_out);
+      a.b_out = static_cast<const T*>(p->b_out);
+      a.n_dev = p->n_devices;
+      a.logits = logits;
+      a.lse = lse;
     }
-    GDP_LAUNCH(GDP_K_POST_ATTN, launch_post_attention<T>(a_post, gt, st));
-    cur ^= 1;
-    y = ynext;
+    a.row0 = row0;
+    return a;
+  };
+  auto ynext_of = [&](int l) { return l + 1 == L && x_out ? x_out : ybuf[(l + 1) & 1]; };
+
+  if (pl.split <= 0 || g_place_streams == 1) {
+    // one stream: projection, then per layer attention and post-attention
+    T* qkv = at<T>(ws, pl.qkv);
+    GDP_LAUNCH(GDP_K_PRE_LAYER, launch_pre_layer<T>(pre_args(qkv, 0), gt, st));
+    for (int l = 0; l < L; ++l) {
+      GDP_LAUNCH(GDP_K_ATTENTION, launch_attention<T>(attn_args(qkv, 0, qblocks), qt, st));
+      GDP_LAUNCH(GDP_K_POST_ATTN, launch_post_attention<T>(post_args(l, ybuf[l & 1], ynext_of(l), qkv, 0), gt, st));
+    }
+  } else {
+    // Two parts, rows A = [0, R) and B = [R, N) with R a segment start, so
+    // that A's queries attend to keys of A only, while B's reach back into A
+    // by up to mem_len rows.  A's launches go to a second stream s2, B's to
+    // st; the two parts of consecutive layers overlap, which fills the
+    // compute units that one part's last round of work-groups leaves idle.
+    // Layer l reads QKV(l) from qkv[l & 1] and writes QKV(l + 1) to the
+    // other buffer.  Orderings across the streams:
+    //   A(l)  after A's QKV(l) rows are written (the projection or post-
+    //         attention of part A): before B's attention of layer l, which
+    //         reads those rows as memory;
+    //   B(l)  after B's attention of layer l: before A's post-attention of
+    //         layer l + 1, which overwrites the buffer that attention read.
+    // Events a[l & 1] and b[l & 1] hold A(l) and B(l); each is waited on
+    // (in host order) before it is recorded again.
+    SideStream* sd = nullptr;
+    int r;
+    if ((r = side_stream(st, &sd)) != GDP_OK) return r;
+    hipStream_t s2 = sd->s;
+    const int R = pl.split, QA = pl.split_qblocks;
+    T* qkv[2] = {at<T>(ws, pl.qkv), at<T>(ws, pl.qkv2)};
+    GDP_HIP(hipEventRecord(sd->fork, st));
+    GDP_HIP(hipStreamWaitEvent(s2, sd->fork, 0));
+    {
+      PreLayerArgs<T> a = pre_args(qkv[0], 0);
+      a.M = R;
+      GDP_LAUNCH_ON(GDP_K_PRE_LAYER, s2, launch_pre_layer<T>(a, gt, s2));
+      GDP_HIP(hipEventRecord(sd->a[0], s2));
+      GDP_LAUNCH(GDP_K_PRE_LAYER, launch_pre_layer<T>(pre_args(qkv[0], R), gt, st));
+    }
+    for (int l = 0; l < L; ++l) {
+      T* qin = qkv[l & 1];
+      T* qout = qkv[(l + 1) & 1];
+      // part B's attention
+      GDP_HIP(hipStreamWaitEvent(st, sd->a[l & 1], 0));
+      GDP_LAUNCH(GDP_K_ATTENTION, launch_attention<T>(attn_args(qin, QA, qblocks - QA), qt, st));
+      GDP_HIP(hipEventRecord(sd->b[l & 1], st));
+      // part A's attention and post-attention
+      GDP_LAUNCH_ON(GDP_K_ATTENTION, s2, launch_attention<T>(attn_args(qin, 0, QA), qt, s2));
+      if (l > 0) GDP_HIP(hipStreamWaitEvent(s2, sd->b[(l - 1) & 1], 0));
+      {
+        PostAttnArgs<T> a = post_args(l, ybuf[l & 1], ynext_of(l), qout, 0);
+        a.M = R;
+        GDP_LAUNCH_ON(GDP_K_POST_ATTN, s2, launch_post_attention<T>(a, gt, s2));
+      }
+      if (l + 1 < L) GDP_HIP(hipEventRecord(sd->a[(l + 1) & 1], s2));
+      // part B's post-attention
+      GDP_LAUNCH(GDP_K_POST_ATTN, launch_post_attention<T>(post_args(l, ybuf[l & 1], ynext_of(l), qout, R), gt, st));
+    }
+    GDP_HIP(hipEventRecord(sd->join, s2));
+    GDP_HIP(hipStreamWaitEvent(st, sd->join, 0));
   }
   if (!fused_head)
-    GDP_LAUNCH(GDP_K_HEAD, launch_head<T>(y, static_cast<const T*>(p->w_out), static_cast<const T*>(p->b_out), N,
-                                          d, p->n_devices, logits, lse, st));
+    GDP_LAUNCH(GDP_K_HEAD, launch_head<T>(ynext_of(L - 1), static_cast<const T*>(p->w_out),
+                                          static_cast<const T*>(p->b_out), N, d, p->n_devices, logits, lse, st));
   return GDP_OK;
 }
 
@@ -1158,6 +1279,13 @@ extern "C" int gdp_debug_neighbors(const gdp_graph* g, const gdp_gnn* gnn, int32
   if ((r = check_ws(ws, ws_bytes, pl.c.total)) != GDP_OK) return r;
   if ((r = pending_hip_error()) != GDP_OK) return r;
   return prep_neighbors(g, gnn, pl, ws, s_ptr, s_idx, static_cast<hipStream_t>(stream));
+}
+
+extern "C" int gdp_set_place_streams(int32_t n) {
+  clear_error();
+  if (n != 1 && n != 2) return fail(GDP_E_INVALID_ARG, "place streams must be 1 or 2, got %d", (int)n);
+  g_place_streams = n;
+  return GDP_OK;
 }
 
 extern "C" int gdp_timer_begin(uint32_t mask) {

@@ -148,6 +148,31 @@ int prefix_blocks_attention(const int32_t* gp, int G, int seg_len, int bq, int32
   return blk[G];
 }
 
+int segment_split(const int32_t* gp, int G, int seg_len, int bq, int target, int* qblocks_below) {
+  const int qbs = (seg_len + bq - 1) / bq;
+  const int N = gp[G];
+  int best = 0, best_q = 0;
+  long best_dist = -1;
+  int qb = 0;   // query blocks of the graphs before g
+  for (int g = 0; g < G; ++g) {
+    const int n = gp[g + 1] - gp[g];
+    const int nseg = (n + seg_len - 1) / seg_len;
+    for (int k = 0; k < nseg; ++k) {
+      const int b = gp[g] + k * seg_len;
+      if (b <= 0 || b >= N) continue;
+      const long dist = b > target ? (long)b - target : (long)target - b;
+      if (best_dist < 0 || dist < best_dist) {
+        best = b;
+        best_q = qb + k * qbs;
+        best_dist = dist;
+      }
+    }
+    if (nseg > 0) qb += (nseg - 1) * qbs + (n - (nseg - 1) * seg_len + bq - 1) / bq;
+  }
+  *qblocks_below = best_q;
+  return best;
+}
+
 void plan_embed(const gdp_graph* g, const gdp_gnn* gnn, EmbedPlan* p) {
   const size_t N = (size_t)g->n_nodes, E = (size_t)g->n_edges, H = (size_t)gnn->hidden;
   const size_t es = elem_size(g->dtype);
@@ -177,15 +202,21 @@ void plan_place(const gdp_graph* g, const gdp_placer* pl, PlacePlan* p) {
   p->film = carve_add(&p->c, (size_t)pl->n_layers * g->n_graphs * d * 2 * 4);
   p->y0 = carve_add(&p->c, N * d * 4);      // residual stream: fp32
   p->head_partial = carve_add(&p->c, ((N + kHeadBwdRows - 1) / kHeadBwdRows) * (size_t)pl->n_devices * (d + 1) * 4);
+  p->split = p->split_qblocks = 0;
   if (!pl->attention) {                     // only the head's input, when the head runs on its own
     p->qblocks = 0;
-    p->y1 = p->qkv = p->o = p->y0;
+    p->y1 = p->qkv = p->qkv2 = p->o = p->y0;
     return;
   }
   p->qblocks = prefix_blocks_attention(g->graph_ptr_h, g->n_graphs, pl->seg_len, kAttnQ, blk);
   p->y1 = carve_add(&p->c, N * d * 4);
   p->qkv = carve_add(&p->c, N * 3 * d * es);
   p->o = carve_add(&p->c, N * d * es);
+  // Two parts only where part B still fills a round of its own (and a
+  // layer is long enough that the overlap outweighs the extra launches).
+  if (N >= (size_t)kSplitRows + kSplitRows / 4)
+    p->split = segment_split(g->graph_ptr_h, g->n_graphs, pl->seg_len, kAttnQ, kSplitRows, &p->split_qblocks);
+  p->qkv2 = p->split > 0 ? carve_add(&p->c, N * 3 * d * es) : p->qkv;
 }
 
 void plan_evaluate(const gdp_graph* g, int32_t n_devices, int32_t k, EvalPlan* p) {

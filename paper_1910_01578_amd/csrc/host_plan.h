@@ -33,6 +33,11 @@ size_t carve_add(Carve* c, size_t bytes);   // returns the offset of the new reg
 // Per-graph block counts -> prefix (blk[0] = 0 .. blk[G] = total).
 int prefix_blocks_rows(const int32_t* graph_ptr, int G, int rows_per_block, int32_t* blk);
 int prefix_blocks_attention(const int32_t* graph_ptr, int G, int seg_len, int block_q, int32_t* blk);
+// The segment start (of any graph of the batch) nearest `target` rows and
+// strictly inside (0, N), or 0 when there is none; *qblocks_below receives
+// the number of attention query blocks (prefix_blocks_attention's order)
+// whose queries lie below it.
+int segment_split(const int32_t* graph_ptr, int G, int seg_len, int block_q, int target, int* qblocks_below);
 
 struct EmbedPlan {
   Carve c;
@@ -45,8 +50,11 @@ struct EmbedPlan {
 struct PlacePlan {
   Carve c;
   size_t film, y0, y1, qkv, o;
+  size_t qkv2;           // the second QKV buffer of the two-part layer schedule (split > 0)
   size_t head_partial;   // gdp_head_backward: per row chunk, D x d weight and D bias partial sums
   int qblocks;
+  int split;             // rows 0 .. split - 1 form part A of the two-part layer schedule; 0: one part
+  int split_qblocks;     // attention query blocks of part A
 };
 constexpr int kHeadBwdRows = 128;   // rows per head-backward chunk
 struct SamplePlan {
@@ -90,6 +98,9 @@ void plan_sample(const gdp_graph* g, int32_t k_samples, SamplePlan* p);
 
 constexpr int kPoolRows = 64;       // rows per mean-pool chunk
 constexpr int kAttnQ = 128;         // queries per attention work-group
+// Rows of part A of the two-part layer schedule: 256 blocks of 128 rows, one
+// post-attention work-group per compute unit.
+constexpr int kSplitRows = 256 * 128;
 constexpr int kSampleRows = 256;    // nodes per sampling work-group
 constexpr int kEvalRows = 256;      // nodes per device-memory work-group of the evaluator
 

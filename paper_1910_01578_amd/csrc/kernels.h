@@ -106,6 +106,7 @@ struct PostAttnArgs {
   // logits [M, n_dev] = y' W_out^T + b_out and lse [M], for n_dev <= kFusedHeadDevices.
   const T* w_out = nullptr; const T* b_out = nullptr; int n_dev = 0;
   float* logits = nullptr; float* lse = nullptr;
+  int row0 = 0;                     // the launch covers rows row0 .. M - 1
 };
 constexpr int kFusedHeadDevices = 8;
 template <typename T>
@@ -125,6 +126,7 @@ struct PreLayerArgs {
   T* qkv_out; int ldq;              // [M, ldq >= 3d]
   int M, d;
   float q_scale;
+  int row0 = 0;                     // the launch covers rows row0 .. M - 1
 };
 template <typename T>
 hipError_t launch_pre_layer(const PreLayerArgs<T>& a, const GraphTable& gt, hipStream_t s);
@@ -164,7 +166,8 @@ struct AttnArgs {
   const T* qkv; int ldq;
   T* out; int ldo;
   int d, heads, seg_len, mem_len;
-  int total_qblocks;
+  int total_qblocks;                // query blocks of this launch: qblock0 .. qblock0 + total_qblocks - 1
+  int qblock0 = 0;
 };
 constexpr int kAttnBlockQ = 128;
 // log2(e) / sqrt(d_head): the softmax runs in the log2 domain on 2^x.

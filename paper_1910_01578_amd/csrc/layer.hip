@@ -769,7 +769,7 @@ __global__ __launch_bounds__(LNT) void k_post_attention(PostAttnArgs<T> p, Graph
   typename G::Red* red = reinterpret_cast<typename G::Red*>(L.red);
 
   const Lanes ln = make_lanes<T, D>();
-  const int m0 = blockIdx.x * LBM;
+  const int m0 = p.row0 + blockIdx.x * LBM;
   const int rows_valid = p.M - m0;
   const int rbase = ln.w2m * G::MB2 * 16 + ln.col;      // row tiling: rows rbase + 16 i
   const int cbase = ln.w2n * G::NB2 * 16 + 4 * ln.g4;   //             columns cbase + 16 j + [0, 4)
@@ -859,7 +859,9 @@ hipError_t launch_post_attention(const PostAttnArgs<T>& a, const GraphTable& gt,
   if (a.film_gamma && (!a.film_beta || a.film_stride % 4 || !aligned_16(a.film_gamma) || !aligned_16(a.film_beta)))
     return hipErrorInvalidValue;
   if (a.y_out && (a.ldyo % 4 || !aligned_16(a.y_out))) return hipErrorInvalidValue;
-  dim3 grid((a.M + LBM - 1) / LBM), block(LNT);
+  if (a.row0 < 0) return hipErrorInvalidValue;
+  if (a.row0 >= a.M) return hipSuccess;
+  dim3 grid((a.M - a.row0 + LBM - 1) / LBM), block(LNT);
   const bool head = a.w_out != nullptr;
   switch (a.d) {
     case 64:
@@ -970,7 +972,7 @@ __global__ __launch_bounds__(LNT) void k_pre_layer(PreLayerArgs<T> p, GraphTable
   using G = Geo<T, D>;
   GDP_LAYER_LDS(T, G);
   const Lanes ln = make_lanes<T, D>();
-  const int m0 = blockIdx.x * LBM;
+  const int m0 = p.row0 + blockIdx.x * LBM;
   const int rbase = ln.w2m * G::MB2 * 16 + ln.col;
   const int cbase = ln.w2n * G::NB2 * 16 + 4 * ln.g4;
   if constexpr (G::NZ == 2) qkv_chunk<T, D, 0>(L, p.w_qkv, p.b_qkv, 0).all();
@@ -1003,7 +1005,9 @@ hipError_t launch_pre_layer(const PreLayerArgs<T>& a, const GraphTable& gt, hipS
   if (a.ldyo % 4 || !aligned_16(a.y_out)) return hipErrorInvalidValue;
   if (a.film_gamma && (!a.film_beta || a.film_stride % 4 || !aligned_16(a.film_gamma) || !aligned_16(a.film_beta)))
     return hipErrorInvalidValue;
-  dim3 grid((a.M + LBM - 1) / LBM), block(LNT);
+  if (a.row0 < 0) return hipErrorInvalidValue;
+  if (a.row0 >= a.M) return hipSuccess;
+  dim3 grid((a.M - a.row0 + LBM - 1) / LBM), block(LNT);
   switch (a.d) {
     case 64: hipLaunchKernelGGL((k_pre_layer<T, 64>), grid, block, 0, s, a, gt); break;
     case 128: hipLaunchKernelGGL((k_pre_layer<T, 128>), grid, block, 0, s, a, gt); break;

@@ -140,6 +140,7 @@ def _load():
         "gdp_debug_uniforms": (c_int32, [c_uint64, c_int32, c_int32, c_int32, c_void_p, c_void_p]),
         "gdp_debug_neighbors": (c_int32, [POINTER(GdpGraph), POINTER(GdpGnn), c_void_p, c_void_p, c_int64,
                                           c_void_p, c_size_t, c_void_p]),
+        "gdp_set_place_streams": (c_int32, [c_int32]),
         "gdp_timer_begin": (c_int32, [c_uint32]),
         "gdp_timer_end": (c_int32, [POINTER(c_double), POINTER(c_int64)]),
         "gdp_kernel_kind_name": (c_char_p, [c_int32]),
@@ -525,6 +526,13 @@ def debug_uniforms(seed: int, n: int, k: int, d: int, device="cuda", stream=None
     out = torch.empty((k, n, d), dtype=torch.float32, device=device)
     check(lib.gdp_debug_uniforms(seed, n, k, d, out.data_ptr(), _stream_handle(stream)))
     return out
+
+
+def set_place_streams(n: int) -> None:
+    """gdp_place's stream schedule for this thread: 2 (the default) splits a
+    large placer pass into two row parts on two streams, 1 keeps every launch
+    on the caller's stream.  The results are the same bit for bit."""
+    check(lib.gdp_set_place_streams(int(n)))
 
 
 def timer_begin(kinds) -> None:

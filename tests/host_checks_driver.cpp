@@ -370,6 +370,57 @@ static void plan_paths() {
   }
 }
 
+// segment_split: the segment start nearest the target, strictly inside
+// (0, N), ties to the lower one, and the query blocks below it.
+static void split_paths() {
+  struct Case {
+    std::vector<int32_t> gp;
+    int seg, target, want, want_q;
+  };
+  const Case cases[] = {
+      {{0, 52000}, 512, 32768, 32768, 256},
+      {{0, 36000, 72000}, 512, 32768, 32768, 256},
+      {{0, 32768, 65536}, 512, 32768, 32768, 256},
+      // graph 0: 3 full segments of 3 query blocks and one of 100 rows; then 63 segments of graph 1
+      {{0, 1000, 40000}, 300, 20000, 19900, 10 + 63 * 3},
+      {{0, 1000, 40000}, 300, 450, 300, 3},          // 300 and 600 are equally near
+      {{0, 400}, 512, 200, 0, 0},                    // one segment: no inner start
+      {{0, 5, 10}, 512, 0, 5, 1},                    // a graph start is a segment start
+  };
+  for (const Case& c : cases) {
+    int q = -1;
+    const int b = segment_split(c.gp.data(), (int)c.gp.size() - 1, c.seg, 128, c.target, &q);
+    ++g_checks;
+    if (b != c.want || q != c.want_q) {
+      ++g_failures;
+      printf("FAIL segment_split target %d: %d (%d blocks), expected %d (%d)\n", c.target, b, q, c.want, c.want_q);
+    }
+  }
+  // the place plan: a second QKV buffer only with two parts
+  gdp_graph g = good_graph();
+  gdp_placer p = good_placer();
+  PlacePlan pp;
+  plan_place(&g, &p, &pp);
+  ++g_checks;
+  if (pp.split != 0 || pp.qkv2 != pp.qkv) {
+    ++g_failures;
+    printf("FAIL place plan of a small graph: split %d\n", pp.split);
+  }
+  static int32_t big[2] = {0, 52000};
+  g.graph_ptr_h = big;
+  g.n_graphs = 1;
+  g.n_nodes = 52000;
+  g.n_edges = 0;
+  p.seg_len = 512;
+  p.mem_len = 512;
+  plan_place(&g, &p, &pp);
+  ++g_checks;
+  if (!carve_ok(pp.c) || pp.split != 32768 || pp.split_qblocks != 256 || pp.qkv2 == pp.qkv) {
+    ++g_failures;
+    printf("FAIL place plan of 52000 rows: split %d, %d blocks\n", pp.split, pp.split_qblocks);
+  }
+}
+
 static void train_paths() {
   const gdp_graph g = good_graph();
   gdp_gnn n = good_gnn();
@@ -429,6 +480,7 @@ int main() {
   placer_paths();
   sample_paths();
   plan_paths();
+  split_paths();
   train_paths();
   error_text();
   printf("%d checks, %d failures\n", g_checks, g_failures);

@@ -26,6 +26,15 @@ def test_exports_every_declared_symbol():
     assert gdp.abi_version() == 2
 
 
+def test_place_streams_setting():
+    """The stream schedule takes 1 or 2 and nothing else (no GPU work)."""
+    for bad in (0, 3, -1):
+        assert gdp.lib.gdp_set_place_streams(bad) == gdp.GDP_E_INVALID_ARG
+        assert "place streams" in gdp.last_error()
+    assert gdp.lib.gdp_set_place_streams(1) == gdp.GDP_OK
+    assert gdp.lib.gdp_set_place_streams(2) == gdp.GDP_OK
+
+
 def test_kernel_kind_names_match_binding():
     for i, n in enumerate(gdp.KERNEL_KINDS):
         assert gdp.lib.gdp_kernel_kind_name(i).decode() == n

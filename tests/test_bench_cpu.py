@@ -53,8 +53,23 @@ def test_headline_workload_work_model():
     assert keys == 52921344 == _keys_brute(gp, cfg.seg_len, cfg.mem_len)
     N, d, dff, L = 52000, cfg.d_model, cfg.d_ff, cfg.placer_layers
     assert abs(work["post_attn"][1] / 1e9 - 78.4) < 0.05
-    assert work["post_attn"][1] == 2.0 * N * d * d + 4.0 * N * d * dff + (L - 1) / L * 6.0 * N * d * d
+    want = 2.0 * N * d * d + 4.0 * N * d * dff + (L - 1) / L * 6.0 * N * d * d
+    assert abs(work["post_attn"][1] - want) <= 1e-12 * want
     assert work["gather_max"][0] == "hbm" and abs(work["gather_max"][1] / 1e6 - 134.07) < 0.005
+
+
+def test_split_layer_work_model():
+    """With each layer's kernels launched over two row ranges, the work per
+    launch is the step's work over twice the launches: totals are unchanged."""
+    cfg = W.get_config("gnmt8_52000")
+    g = types.SimpleNamespace(n_nodes=52000, graph_ptr=np.array([0, 52000]))
+    L = cfg.placer_layers
+    one, _ = bench.flop_model(cfg, g, {"sum_s": 0})
+    two, _ = bench.flop_model(cfg, g, {"sum_s": 0}, launches={"pre_layer": 2, "seg_attention": 2 * L,
+                                                             "post_attn": 2 * L})
+    for k in ("pre_layer", "seg_attention", "post_attn"):
+        assert abs(2 * two[k][1] - one[k][1]) <= 1e-12 * one[k][1]
+    assert two["gather_max"] == one["gather_max"]
 
 
 def test_fused_gnn_work_model():

@@ -1,5 +1,7 @@
 """One step of the hot path captured into a HIP graph (torch.cuda.CUDAGraph):
 the library allocates nothing and records no memset, so the step replays.
+At 52,000 nodes the placer's two-part schedule forks to its second stream
+and joins back inside the capture.
 Every replay, with eager work of another seed between replays, must give the
 eager step's logits, placements and log-probs bit for bit."""
 import sys
@@ -17,7 +19,7 @@ def _bits(t):
     return t.detach().contiguous().cpu().view(torch.uint8).numpy().tobytes()
 
 
-@pytest.mark.parametrize("name", ["tiny_layered_256", "superposition_4x"])
+@pytest.mark.parametrize("name", ["tiny_layered_256", "superposition_4x", "gnmt8_52000"])
 def test_step_graph_replays_equal_eager(name):
     import torch
     from paper_1910_01578_amd import gdp
