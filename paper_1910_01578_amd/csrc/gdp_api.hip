@@ -39,8 +39,10 @@ struct TimerState {
       pool.pop_back();
       return e;
     }
+    // Timing only: without the system-scope fence a record costs no cache
+    // write-back (which would idle the GPU between the launches it brackets).
     hipEvent_t e = nullptr;
-    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    if (hipEventCreateWithFlags(&e, hipEventDisableSystemFence) != hipSuccess) return nullptr;
     return e;
   }
 };
@@ -123,7 +125,9 @@ int side_stream(hipStream_t st, SideStream** out) {
   x.device = dev;
   e = hipStreamCreateWithFlags(&x.s, hipStreamNonBlocking);
   hipEvent_t* evs[6] = {&x.fork, &x.join, &x.a[0], &x.a[1], &x.b[0], &x.b[1]};
-  for (int i = 0; i < 6 && e == hipSuccess; ++i) e = hipEventCreateWithFlags(evs[i], hipEventDisableTiming);
+  // Ordering between streams of one device needs no system-scope fence.
+  for (int i = 0; i < 6 && e == hipSuccess; ++i)
+    e = hipEventCreateWithFlags(evs[i], hipEventDisableTiming | hipEventDisableSystemFence);
   if (cur != dev) {
     const hipError_t e2 = hipSetDevice(cur);
     if (e == hipSuccess) e = e2;
