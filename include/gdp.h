@@ -215,7 +215,10 @@ int gdp_place(const gdp_graph* g, const void* node_emb, const float* graph_emb,
  *     (one per device and calling thread, default priority, created at the
  *     first such call and kept until the process ends) and B's on `stream`,
  *     so that the parts of consecutive layers overlap.  The workspace holds
- *     a second copy of the QKV buffer for it.
+ *     a second copy of the QKV buffer for it.  A call made while `stream`
+ *     is being captured into a HIP graph, before that thread has made an
+ *     uncaptured one on the device, keeps every launch on `stream` (no
+ *     stream is created during a capture).
  *   n = 1: every launch on `stream`, one launch per kernel and layer.
  * Returns GDP_E_INVALID_ARG for any other n.
  */

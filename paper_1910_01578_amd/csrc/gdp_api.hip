@@ -109,7 +109,11 @@ thread_local std::vector<SideStream> g_side;
 // gdp_set_place_streams: 2 = two-part schedule where it applies, 1 = one stream
 thread_local int g_place_streams = 2;
 
+// *out = nullptr (and GDP_OK) when the stream does not exist yet and st is
+// being captured into a graph: no stream is created during a capture, and
+// the caller then keeps every launch on st.
 int side_stream(hipStream_t st, SideStream** out) {
+  *out = nullptr;
   int dev = -1;
   hipError_t e = hipStreamGetDevice(st, &dev);
   if (e != hipSuccess) return hip_fail(e, "hipStreamGetDevice");
@@ -118,6 +122,9 @@ int side_stream(hipStream_t st, SideStream** out) {
       *out = &x;
       return GDP_OK;
     }
+  hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+  if ((e = hipStreamIsCapturing(st, &cap)) != hipSuccess) return hip_fail(e, "hipStreamIsCapturing");
+  if (cap != hipStreamCaptureStatusNone) return GDP_OK;
   int cur = -1;
   if ((e = hipGetDevice(&cur)) != hipSuccess) return hip_fail(e, "hipGetDevice");
   if (cur != dev && (e = hipSetDevice(dev)) != hipSuccess) return hip_fail(e, "hipSetDevice");
@@ -373,7 +380,12 @@ static int place_impl(const gdp_graph* g, const T* node_emb, const float* graph_
   };
   auto ynext_of = [&](int l) { return l + 1 == L && x_out ? x_out : ybuf[(l + 1) & 1]; };
 
-  if (pl.split <= 0 || g_place_streams == 1) {
+  SideStream* sd = nullptr;
+  if (pl.split > 0 && g_place_streams == 2) {
+    const int r = side_stream(st, &sd);
+    if (r != GDP_OK) return r;
+  }
+  if (!sd) {
     // one stream: projection, then per layer attention and post-attention
     T* qkv = at<T>(ws, pl.qkv);
     GDP_LAUNCH(GDP_K_PRE_LAYER, launch_pre_layer<T>(pre_args(qkv, 0), gt, st));
@@ -396,9 +408,6 @@ static int place_impl(const gdp_graph* g, const T* node_emb, const float* graph_
     //         layer l + 1, which overwrites the buffer that attention read.
     // Events a[l & 1] and b[l & 1] hold A(l) and B(l); each is waited on
     // (in host order) before it is recorded again.
-    SideStream* sd = nullptr;
-    int r;
-    if ((r = side_stream(st, &sd)) != GDP_OK) return r;
     hipStream_t s2 = sd->s;
     const int R = pl.split, QA = pl.split_qblocks;
     T* qkv[2] = {at<T>(ws, pl.qkv), at<T>(ws, pl.qkv2)};

@@ -1,6 +1,7 @@
 // Whole-graph placement sampling: one fused Gumbel-max pass over (k, v).
 //
-// Thread (k, v): D uniforms from Philox4x64-10 with counter (v, k, 2, j >> 3)
+// Thread (k, v), for a few consecutive k: D uniforms from Philox4x64-10 with
+// counter (v, k, 2, j >> 3)
 // and key (seed, 0) (one call yields 8 devices), Gumbel noise -ln(-ln u),
 // argmax of logits + noise (first maximum wins), and the chosen device's
 // log-softmax term.  The log-prob terms are summed per work-group in a fixed
@@ -28,17 +29,25 @@ __device__ __forceinline__ float gumbel_score(float logit, float u) {
   return fmaf(logit, 1.4426950408889634f, -fast_log2(-fast_log2(u)));
 }
 
+// Thread (k, v) for kSamplesPerThread consecutive k: their Philox calls are
+// independent, so interleaving them hides each call's chain of dependent
+// 64-bit products behind the other's.
+constexpr int kSamplesPerThread = 4;
+
 __global__ __launch_bounds__(kSampleChunk) void k_sample(const float* __restrict__ logits,
-                                                         const float* __restrict__ lse, int n, int D,
+                                                         const float* __restrict__ lse, int n, int D, int K,
                                                          uint64_t seed, const float* __restrict__ uniforms,
                                                          GraphTable ct, int total_chunks,
                                                          int* __restrict__ placements,
                                                          float* __restrict__ partial) {
-  __shared__ float red[kSampleChunk / kWave];
-  const int c = blockIdx.x, k = blockIdx.y;
+  constexpr int S = kSamplesPerThread;
+  __shared__ float red[S][kSampleChunk / kWave];
+  const int c = blockIdx.x, k0 = blockIdx.y * S;
   const int g = graph_of_block(ct, c);
   const int v = ct.ptr[g] + (c - ct.blk[g]) * kSampleChunk + threadIdx.x;
-  float term = 0.f;
+  float term[S];
+#pragma unroll
+  for (int q = 0; q < S; ++q) term[q] = 0.f;
   if (v < ct.ptr[g + 1]) {
     const float* row = logits + (size_t)v * D;
     float lz;
@@ -51,44 +60,67 @@ __global__ __launch_bounds__(kSampleChunk) void k_sample(const float* __restrict
       for (int j = 0; j < D; ++j) s += expf(row[j] - m);
       lz = m + logf(s);
     }
-    float best = -INFINITY;
-    int arg = 0;
+    float best[S];
+    int arg[S];
+#pragma unroll
+    for (int q = 0; q < S; ++q) {
+      best[q] = -INFINITY;
+      arg[q] = 0;
+    }
     // one Philox call covers 8 devices; the 8 are unrolled so that every
     // uniform is taken from a fixed word of the result
     for (int jb = 0; jb < D; jb += 8) {
-      U64x4 r;
-      if (!uniforms) r = philox4x64_10((uint64_t)v, (uint64_t)k, 2ull, (uint64_t)(jb >> 3), seed, 0ull);
+      U64x4 r[S];
+      if (!uniforms) {
+#pragma unroll
+        for (int q = 0; q < S; ++q)   // (k beyond K: computed, never used)
+          r[q] = philox4x64_10((uint64_t)v, (uint64_t)(k0 + q), 2ull, (uint64_t)(jb >> 3), seed, 0ull);
+      }
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         const int j = jb + e;
         if (j < D) {
-          const float u = uniforms ? uniforms[((size_t)k * n + v) * D + j] : uniform_at(r, e);
-          const float sc = gumbel_score(row[j], u);
-          if (sc > best) { best = sc; arg = j; }   // first maximum wins
+          const float lj = row[j];
+#pragma unroll
+          for (int q = 0; q < S; ++q) {
+            if (k0 + q < K) {
+              const float u = uniforms ? uniforms[((size_t)(k0 + q) * n + v) * D + j] : uniform_at(r[q], e);
+              const float sc = gumbel_score(lj, u);
+              if (sc > best[q]) { best[q] = sc; arg[q] = j; }   // first maximum wins
+            }
+          }
         }
       }
     }
-    placements[(size_t)k * n + v] = arg;
-    term = row[arg] - lz;
-  }
-  // work-group sum in a fixed order: each wave's butterfly, then the waves in index order
 #pragma unroll
-  for (int off = kWave / 2; off >= 1; off >>= 1) term += xor_shfl(term, off);
-  if ((threadIdx.x & (kWave - 1)) == 0) red[threadIdx.x / kWave] = term;
+    for (int q = 0; q < S; ++q)
+      if (k0 + q < K) {
+        placements[(size_t)(k0 + q) * n + v] = arg[q];
+        term[q] = row[arg[q]] - lz;
+      }
+  }
+  // work-group sums in a fixed order: each wave's butterfly, then the waves in index order
+#pragma unroll
+  for (int q = 0; q < S; ++q) {
+#pragma unroll
+    for (int off = kWave / 2; off >= 1; off >>= 1) term[q] += xor_shfl(term[q], off);
+    if ((threadIdx.x & (kWave - 1)) == 0) red[q][threadIdx.x / kWave] = term[q];
+  }
   __syncthreads();
-  if (threadIdx.x == 0) {
+  if (threadIdx.x < S && k0 + (int)threadIdx.x < K) {
+    const int q = threadIdx.x;
     float sum = 0.f;
 #pragma unroll
-    for (int w = 0; w < kSampleChunk / kWave; ++w) sum += red[w];
-    partial[(size_t)k * total_chunks + c] = sum;
+    for (int w = 0; w < kSampleChunk / kWave; ++w) sum += red[q][w];
+    partial[(size_t)(k0 + q) * total_chunks + c] = sum;
   }
 }
 
 hipError_t launch_sample(const float* logits, const float* lse, int n, int D, int K, uint64_t seed,
                          const float* uniforms, const GraphTable& ct, int total_chunks, int* placements,
                          float* partial, hipStream_t s) {
-  dim3 grid(total_chunks, K), block(kSampleChunk);
-  hipLaunchKernelGGL(k_sample, grid, block, 0, s, logits, lse, n, D, seed, uniforms, ct, total_chunks,
+  dim3 grid(total_chunks, (K + kSamplesPerThread - 1) / kSamplesPerThread), block(kSampleChunk);
+  hipLaunchKernelGGL(k_sample, grid, block, 0, s, logits, lse, n, D, K, seed, uniforms, ct, total_chunks,
                      placements, partial);
   return hipGetLastError();
 }

@@ -101,3 +101,42 @@ def test_schedules_agree_on_the_52000_node_workload():
     finally:
         gdp.set_place_streams(2)
     assert out[1] == out[2]
+
+
+def test_first_call_under_capture_keeps_one_stream():
+    """A thread whose first two-part gdp_place call is captured into a HIP
+    graph creates no stream and keeps every launch on the capturing stream;
+    the replay equals the eager two-part result bit for bit."""
+    import threading
+    import torch
+    from paper_1910_01578_amd import gdp
+    from tests.parity import workload
+    cfg, g, w = workload("gnmt8_52000")
+    _log("capture in a fresh thread", cfg.name)
+    r = gdp.Runner(gdp.DeviceGraph(g, cfg.dtype), gdp.DevicePolicy(cfg, w), 1)
+    r.embed()
+    r.place()
+    torch.cuda.synchronize()
+    want = (_bits(r.logits), _bits(r.lse))
+    res = {}
+
+    def work():
+        try:
+            torch.cuda.set_device(0)
+            graph = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(graph):
+                r.place()
+            torch.cuda.synchronize()
+            r.logits.fill_(float("nan"))
+            torch.cuda.synchronize()
+            graph.replay()
+            torch.cuda.synchronize()
+            res["got"] = (_bits(r.logits), _bits(r.lse))
+        except Exception as e:   # reported in the main thread
+            res["err"] = e
+
+    t = threading.Thread(target=work)
+    t.start()
+    t.join()
+    assert "err" not in res, res.get("err")
+    assert res["got"] == want
