@@ -37,7 +37,8 @@ hipError_t launch_in_degree(const int* col_idx, int64_t n_edges, int* in_deg, hi
 }
 
 // ---------------------------------------------------------------------------
-// Exclusive scans of the two degree arrays, in three launches:
+// Exclusive scans of the two degree arrays, in three launches (two for up
+// to kScanDirectBlocks blocks, below):
 //   in_ptr[i] = sum_{j<i} in_deg[j]
 //   s_ptr[i]  = sum_{j<i} min(out_deg[j] + in_deg[j], fanout)
 // (1) per-block totals of kScanBlock entries, (2) one work-group scans the
@@ -144,12 +145,58 @@ __global__ __launch_bounds__(256) void k_scan_apply(const int* __restrict__ row_
   }
 }
 
+// (3) without (2), for up to kScanDirectBlocks blocks: each block adds up the
+// totals of the blocks before it itself (at most a few KB from L2), and the
+// last block writes the grand totals.  One launch fewer.
+constexpr int kScanDirectBlocks = 1024;
+
+__global__ __launch_bounds__(256) void k_scan_apply_direct(const int* __restrict__ row_ptr,
+                                                           const int* __restrict__ in_deg, int n, int fanout,
+                                                           const int* __restrict__ bsum, int nblocks,
+                                                           int* __restrict__ in_ptr, int* __restrict__ s_ptr) {
+  int pa = 0, pb = 0;
+  for (int i = threadIdx.x; i < (int)blockIdx.x; i += 256) {
+    pa += bsum[2 * i];
+    pb += bsum[2 * i + 1];
+  }
+  int xa, xb, off_a, off_b;
+  block_scan2(pa, pb, xa, xb, &off_a, &off_b);
+  const int base = blockIdx.x * kScanBlock + threadIdx.x * 4;
+  int da[4], db[4], sa = 0, sb = 0;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    degree_pair(row_ptr, in_deg, base + j, n, fanout, da[j], db[j]);
+    sa += da[j];
+    sb += db[j];
+  }
+  int ea, eb, ta, tb;
+  block_scan2(sa, sb, ea, eb, &ta, &tb);
+  ea += off_a;
+  eb += off_b;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int i = base + j;
+    if (i < n) { in_ptr[i] = ea; s_ptr[i] = eb; }
+    ea += da[j];
+    eb += db[j];
+  }
+  if (blockIdx.x == nblocks - 1 && threadIdx.x == 0) {
+    in_ptr[n] = off_a + ta;
+    s_ptr[n] = off_b + tb;
+  }
+}
+
 hipError_t launch_scan_degrees(const int* row_ptr, const int* in_deg, int n, int fanout, int* in_ptr,
                                int* s_ptr, int* block_tmp, hipStream_t s) {
   const int nb = (n + kScanBlock - 1) / kScanBlock;
   hipLaunchKernelGGL(k_scan_block_sums, dim3(nb), dim3(256), 0, s, row_ptr, in_deg, n, fanout, block_tmp);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
+  if (nb <= kScanDirectBlocks) {
+    hipLaunchKernelGGL(k_scan_apply_direct, dim3(nb), dim3(256), 0, s, row_ptr, in_deg, n, fanout, block_tmp, nb,
+                       in_ptr, s_ptr);
+    return hipGetLastError();
+  }
   hipLaunchKernelGGL(k_scan_block_offsets, dim3(1), dim3(256), 0, s, block_tmp, nb, n, in_ptr, s_ptr);
   e = hipGetLastError();
   if (e != hipSuccess) return e;

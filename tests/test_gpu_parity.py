@@ -95,6 +95,38 @@ def test_neighbors_scan_paths(sizes):
         assert np.array_equal(np.sort(s_idx[s_ptr[v]:s_ptr[v + 1]]), S[v]), v
 
 
+def test_neighbors_scan_over_a_million_nodes():
+    """1,100,000 nodes: the degree scan spans more than 1,024 blocks and takes
+    its three-launch path.  The offsets equal the exclusive prefix sums of
+    min(in + out degree, fanout) (numpy), and every sampled id of 4,000 random
+    nodes is a distinct neighbour of its node."""
+    n, e, fanout = 1_100_000, 2_000_000, 4
+    rng = np.random.default_rng(11)
+    a, b = rng.integers(0, n, e), rng.integers(0, n, e)
+    keep = a != b
+    key = np.unique(np.minimum(a, b)[keep] * n + np.maximum(a, b)[keep])   # distinct edges u < v, sorted
+    src, dst = key // n, key % n
+    row_ptr = np.concatenate([[0], np.cumsum(np.bincount(src, minlength=n))]).astype(np.int32)
+    col_idx = dst.astype(np.int32)
+    by_dst = np.argsort(dst, kind="stable")
+    in_ptr = np.concatenate([[0], np.cumsum(np.bincount(dst, minlength=n))])
+    in_src = src[by_dst]
+    cfg = W.get_config("tiny_layered_256").replace(graph_sizes=(n,), fanout=fanout)
+    _log("neighbors, three-launch scan", n)
+    x = np.zeros((n, cfg.feat_dim))
+    g = W.Graph(np.array([0, n], np.int32), row_ptr, col_idx, x, x.astype(np.float32))
+    r = _runner(cfg, g, W.make_weights(cfg))
+    s_ptr, s_idx = r.neighbors()
+    _sync()
+    s_ptr, s_idx = s_ptr.cpu().numpy(), s_idx.cpu().numpy()
+    deg = np.diff(row_ptr) + np.bincount(col_idx, minlength=n)
+    assert np.array_equal(s_ptr, np.concatenate([[0], np.cumsum(np.minimum(deg, fanout))]))
+    for v in rng.choice(n, 4000, replace=False):
+        nbrs = set(col_idx[row_ptr[v]:row_ptr[v + 1]].tolist()) | set(in_src[in_ptr[v]:in_ptr[v + 1]].tolist())
+        got = s_idx[s_ptr[v]:s_ptr[v + 1]].tolist()
+        assert len(set(got)) == len(got) and set(got) <= nbrs, v
+
+
 def test_neighbors_heavy_sampling_and_order_invariance():
     cfg, g, w = workload("recurrent_12000")
     cfg = cfg.replace(fanout=2)
