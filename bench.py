@@ -31,13 +31,12 @@ def flop_model(cfg, g, stats, fused_gnn=False, launches=None):
     layer's update (kind gemm_update_pool), so the separate transform ran for
     layer 0 only and the plain update for the last layer only.
     launches: launches per step of each kind, where the run split a layer's
-    projection, attention and post-attention kernels over two row ranges (two
-    launches each); the work of a step is then averaged over its launches.
+    kernels over two row ranges (two launches each); the work of a step is
+    then averaged over its launches.
 
     GEMMs: 2 * M * K * N.  Attention: 4 * d * sum over queries of the keys it
     attends to (QK^T and PV, all heads).  Gather-max: bytes of the sampled
     neighbour rows and their ids, the pointer array and the output rows."""
-    import numpy as np
     N, H, F, d, dff = g.n_nodes, cfg.hidden, cfg.feat_dim, cfg.d_model, cfg.d_ff
     b = 2 if cfg.dtype == "bf16" else 4
     keys = 0
@@ -53,17 +52,23 @@ def flop_model(cfg, g, stats, fused_gnn=False, launches=None):
     gather_bytes = stats["sum_s"] * (H * b + 4) + N * H * b + 4 * (N + 1)
     fused = [upd[l] + pool[l + 1] for l in range(L - 1)]
     P = cfg.placer_layers
-    # per step: one projection, P attention and P post-attention passes (W_o,
-    # the FFN, and all but the last layer's next QKV projection)
-    step = {"pre_layer": (2.0 * N * d * 3 * d, 1),
+    # per step, with the launch count of the one-stream schedule: the GNN's
+    # transforms, gathers and updates (fused: layer l's update with layer
+    # l + 1's transform), one projection, P attention and P post-attention
+    # passes (W_o, the FFN, and all but the last layer's next QKV projection)
+    step = {"gemm_pool_sigmoid": (pool[0], 1) if fused_gnn else (sum(pool), L),
+            "gemm_update_relu": (upd[-1], 1) if fused_gnn else (sum(upd), L),
+            "gemm_update_pool": (sum(fused), L - 1) if fused_gnn and fused else (0.0, 1),
+            "gather_max": (L * gather_bytes, L),
+            "pre_layer": (2.0 * N * d * 3 * d, 1),
             "seg_attention": (4.0 * d * keys * P, P),
             "post_attn": (P * (2.0 * N * d * d + 4.0 * N * d * dff) + (P - 1) * 2.0 * N * d * 3 * d, P)}
-    per_launch = {k: tot / ((launches or {}).get(k) or n) for k, (tot, n) in step.items()}
+    per_launch = {k: float(tot) / ((launches or {}).get(k) or n) for k, (tot, n) in step.items()}
     return {
-        "gemm_pool_sigmoid": ("mfma", float(pool[0] if fused_gnn else np.mean(pool))),
-        "gemm_update_relu": ("mfma", float(upd[-1] if fused_gnn else np.mean(upd))),
-        "gemm_update_pool": ("mfma", float(np.mean(fused)) if fused else 0.0),
-        "gather_max": ("hbm", float(gather_bytes)),
+        "gemm_pool_sigmoid": ("mfma", per_launch["gemm_pool_sigmoid"]),
+        "gemm_update_relu": ("mfma", per_launch["gemm_update_relu"]),
+        "gemm_update_pool": ("mfma", per_launch["gemm_update_pool"]),
+        "gather_max": ("hbm", per_launch["gather_max"]),
         "pre_layer": ("mfma", per_launch["pre_layer"]),
         "seg_attention": ("mfma", per_launch["seg_attention"]),
         "post_attn": ("mfma", per_launch["post_attn"]),

@@ -59,17 +59,20 @@ def test_headline_workload_work_model():
 
 
 def test_split_layer_work_model():
-    """With each layer's kernels launched over two row ranges, the work per
-    launch is the step's work over twice the launches: totals are unchanged."""
+    """With each layer's kernels launched over two row ranges (the GNN's layer-0
+    transform stays one launch), the work per launch is the step's work over
+    twice the launches: totals are unchanged."""
     cfg = W.get_config("gnmt8_52000")
     g = types.SimpleNamespace(n_nodes=52000, graph_ptr=np.array([0, 52000]))
     L = cfg.placer_layers
-    one, _ = bench.flop_model(cfg, g, {"sum_s": 0})
-    two, _ = bench.flop_model(cfg, g, {"sum_s": 0}, launches={"pre_layer": 2, "seg_attention": 2 * L,
-                                                             "post_attn": 2 * L})
-    for k in ("pre_layer", "seg_attention", "post_attn"):
+    G = cfg.gnn_layers
+    one, _ = bench.flop_model(cfg, g, {"sum_s": 1000}, fused_gnn=True)
+    two, _ = bench.flop_model(cfg, g, {"sum_s": 1000}, fused_gnn=True,
+                              launches={"pre_layer": 2, "seg_attention": 2 * L, "post_attn": 2 * L,
+                                        "gather_max": 2 * G, "gemm_update_pool": 2 * (G - 1), "gemm_update_relu": 2})
+    for k in ("pre_layer", "seg_attention", "post_attn", "gather_max", "gemm_update_pool", "gemm_update_relu"):
         assert abs(2 * two[k][1] - one[k][1]) <= 1e-12 * one[k][1]
-    assert two["gather_max"] == one["gather_max"]
+    assert two["gemm_pool_sigmoid"] == one["gemm_pool_sigmoid"]
 
 
 def test_fused_gnn_work_model():
