@@ -413,34 +413,41 @@ static int place_impl(const gdp_graph* g, const T* node_emb, const float* graph_
     T* qkv[2] = {at<T>(ws, pl.qkv), at<T>(ws, pl.qkv2)};
     GDP_HIP(hipEventRecord(sd->fork, st));
     GDP_HIP(hipStreamWaitEvent(s2, sd->fork, 0));
-    {
-      PreLayerArgs<T> a = pre_args(qkv[0], 0);
-      a.M = R;
-      GDP_LAUNCH_ON(GDP_K_PRE_LAYER, s2, launch_pre_layer<T>(a, gt, s2));
-      GDP_HIP(hipEventRecord(sd->a[0], s2));
-      GDP_LAUNCH(GDP_K_PRE_LAYER, launch_pre_layer<T>(pre_args(qkv[0], R), gt, st));
-    }
-    for (int l = 0; l < L; ++l) {
-      T* qin = qkv[l & 1];
-      T* qout = qkv[(l + 1) & 1];
-      // part B's attention
-      GDP_HIP(hipStreamWaitEvent(st, sd->a[l & 1], 0));
-      GDP_LAUNCH(GDP_K_ATTENTION, launch_attention<T>(attn_args(qin, QA, qblocks - QA), qt, st));
-      GDP_HIP(hipEventRecord(sd->b[l & 1], st));
-      // part A's attention and post-attention
-      GDP_LAUNCH_ON(GDP_K_ATTENTION, s2, launch_attention<T>(attn_args(qin, 0, QA), qt, s2));
-      if (l > 0) GDP_HIP(hipStreamWaitEvent(s2, sd->b[(l - 1) & 1], 0));
+    // the launches, then the join, which st gets even when a launch fails
+    auto parts = [&]() -> int {
       {
-        PostAttnArgs<T> a = post_args(l, ybuf[l & 1], ynext_of(l), qout, 0);
+        PreLayerArgs<T> a = pre_args(qkv[0], 0);
         a.M = R;
-        GDP_LAUNCH_ON(GDP_K_POST_ATTN, s2, launch_post_attention<T>(a, gt, s2));
+        GDP_LAUNCH_ON(GDP_K_PRE_LAYER, s2, launch_pre_layer<T>(a, gt, s2));
+        GDP_HIP(hipEventRecord(sd->a[0], s2));
+        GDP_LAUNCH(GDP_K_PRE_LAYER, launch_pre_layer<T>(pre_args(qkv[0], R), gt, st));
       }
-      if (l + 1 < L) GDP_HIP(hipEventRecord(sd->a[(l + 1) & 1], s2));
-      // part B's post-attention
-      GDP_LAUNCH(GDP_K_POST_ATTN, launch_post_attention<T>(post_args(l, ybuf[l & 1], ynext_of(l), qout, R), gt, st));
-    }
-    GDP_HIP(hipEventRecord(sd->join, s2));
-    GDP_HIP(hipStreamWaitEvent(st, sd->join, 0));
+      for (int l = 0; l < L; ++l) {
+        T* qin = qkv[l & 1];
+        T* qout = qkv[(l + 1) & 1];
+        // part B's attention
+        GDP_HIP(hipStreamWaitEvent(st, sd->a[l & 1], 0));
+        GDP_LAUNCH(GDP_K_ATTENTION, launch_attention<T>(attn_args(qin, QA, qblocks - QA), qt, st));
+        GDP_HIP(hipEventRecord(sd->b[l & 1], st));
+        // part A's attention and post-attention
+        GDP_LAUNCH_ON(GDP_K_ATTENTION, s2, launch_attention<T>(attn_args(qin, 0, QA), qt, s2));
+        if (l > 0) GDP_HIP(hipStreamWaitEvent(s2, sd->b[(l - 1) & 1], 0));
+        {
+          PostAttnArgs<T> a = post_args(l, ybuf[l & 1], ynext_of(l), qout, 0);
+          a.M = R;
+          GDP_LAUNCH_ON(GDP_K_POST_ATTN, s2, launch_post_attention<T>(a, gt, s2));
+        }
+        if (l + 1 < L) GDP_HIP(hipEventRecord(sd->a[(l + 1) & 1], s2));
+        // part B's post-attention
+        GDP_LAUNCH(GDP_K_POST_ATTN, launch_post_attention<T>(post_args(l, ybuf[l & 1], ynext_of(l), qout, R), gt, st));
+      }
+      return GDP_OK;
+    };
+    const int r = parts();
+    const hipError_t ej = hipEventRecord(sd->join, s2);
+    const hipError_t ew = ej == hipSuccess ? hipStreamWaitEvent(st, sd->join, 0) : ej;
+    if (r != GDP_OK) return r;
+    if (ew != hipSuccess) return hip_fail(ew, "join of the second stream");
   }
   if (!fused_head)
     GDP_LAUNCH(GDP_K_HEAD, launch_head<T>(ynext_of(L - 1), static_cast<const T*>(p->w_out),
