@@ -98,9 +98,12 @@ def measured_traffic(kind):
     with open(src, "rb") as f:
         if hashlib.sha256(f.read()).hexdigest() != rec["source_sha256"]:
             return None
-    return {"bytes_per_launch": rec["bytes_per_launch"], "fetch_bytes": rec["fetch_bytes"],
-            "write_bytes": rec["write_bytes"], "algorithmic_bytes": rec.get("algorithmic_bytes"),
-            "summary": rec["summary"]}
+    out = {"bytes_per_launch": rec["bytes_per_launch"], "fetch_bytes": rec["fetch_bytes"],
+           "write_bytes": rec["write_bytes"], "algorithmic_bytes": rec.get("algorithmic_bytes"),
+           "summary": rec["summary"]}
+    if "one_stream" in rec:      # the same kernel's launches over all rows (one-stream schedule)
+        out["one_stream"] = rec["one_stream"]
+    return out
 
 
 def blas_info():
@@ -330,13 +333,23 @@ def main():
     roofline["avg_launch_us"] = round(1e3 * dom["ms"] / dom["launches"], 2)
     roofline["traffic"] = measured_traffic(dominant)
 
-    def kernel_table(bd, wk):
+    def kernel_table(bd, wk, one_stream=False):
         rows = []
         for kind, v in sorted(bd.items(), key=lambda kv: -kv[1]["ms"]):
             ent = {"kernel": kind, "ms_per_step": round(v["ms"], 4), "launches": v["launches"]}
             rf = roof(kind, v["ms"], v["launches"], wk)
             if rf:
                 ent.update({"achieved": rf["achieved"], "unit": rf["unit"], "frac": rf["frac"], "bound": rf["bound"]})
+            # the counted HBM bytes of a launch of this shape, where recorded
+            tr = measured_traffic(kind)
+            if tr and one_stream and kind != "gather_max":
+                tr = tr.get("one_stream")
+            if tr:
+                ent["traffic_bytes_per_launch"] = tr["bytes_per_launch"]
+                if rf and rf["bound"] == "hbm":
+                    gbs = tr["bytes_per_launch"] / (v["ms"] / v["launches"] * 1e-3) / 1e9
+                    ent["counted_achieved"] = round(gbs, 1)
+                    ent["counted_frac"] = round(gbs / PEAK_HBM_GBS, 4)
             rows.append(ent)
         return rows
 
@@ -373,7 +386,7 @@ def main():
                                   "launches_per_step": iso["launches"] // n_iso,
                                   "achieved": rf1.get("achieved"), "frac": rf1.get("frac"),
                                   "ms_per_step": round(1e3 * iso_s, 4)}
-        kernels_one_stream = kernel_table(bd1, work1)
+        kernels_one_stream = kernel_table(bd1, work1, one_stream=True)
 
     # The same step captured once into a HIP graph and replayed K times (the
     # library allocates nothing and records no memset, so a step can be
