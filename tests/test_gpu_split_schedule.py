@@ -53,20 +53,23 @@ def _place(cfg, w, sizes, node_emb, graph_emb, train):
     return r.logits, r.lse, x
 
 
-@pytest.mark.parametrize("n,n_dev,mem_len,train", [
-    (36000, 8, 512, False),       # part A ends inside the first copy
-    (36000, 20, 512, True),       # head in its own kernel; final activations kept
-    (36000, 8, 1024, False),      # part B's memory reaches two segments into part A
-    (32768, 8, 512, True),        # part A ends at the second copy's first row
+@pytest.mark.parametrize("base,n,n_dev,mem_len,train,over", [
+    ("gnmt8_52000", 36000, 8, 512, False, {}),      # part A ends inside the first copy
+    ("gnmt8_52000", 36000, 20, 512, True, {}),      # head in its own kernel; final activations kept
+    ("gnmt8_52000", 36000, 8, 1024, False, {}),     # part B's memory reaches two segments into part A
+    ("gnmt8_52000", 32768, 8, 512, True, {}),       # part A ends at the second copy's first row
+    ("gnmt8_52000", 36000, 8, 0, False, {"film": False}),   # no memory, no conditioning
+    ("tiny_layered_256", 36000, 4, 64, True, {"seg_len": 256}),   # fp32, d = 64
 ])
-def test_two_part_schedule_equals_one_stream(n, n_dev, mem_len, train):
+def test_two_part_schedule_equals_one_stream(base, n, n_dev, mem_len, train, over):
     import torch
     assert n < SPLIT_ROWS + SPLIT_ROWS // 4 <= 2 * n
-    cfg = W.get_config("gnmt8_52000").replace(graph_sizes=(n,), n_devices=n_dev, mem_len=mem_len)
+    cfg = W.get_config(base).replace(graph_sizes=(n,), n_devices=n_dev, mem_len=mem_len, **over)
     w = W.make_weights(cfg)
-    _log("split schedule", n, n_dev, mem_len, train)
+    _log("split schedule", base, n, n_dev, mem_len, train, over)
     gen = torch.Generator().manual_seed(n + n_dev + mem_len)
-    emb = torch.rand((n, cfg.hidden), generator=gen).to(torch.bfloat16).cuda()
+    tdt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+    emb = torch.rand((n, cfg.hidden), generator=gen).to(tdt).cuda()
     gemb = torch.randn((1, cfg.hidden), generator=gen).cuda()
     one = _place(cfg, w, (n,), emb, gemb, train)
     two = _place(cfg, w, (n, n), torch.cat([emb, emb]), torch.cat([gemb, gemb]), train)
