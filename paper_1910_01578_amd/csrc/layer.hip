@@ -496,6 +496,10 @@ __device__ __forceinline__ ChunkDma<T, D, Geo<T, D>::QH == 2 ? 2 : 0, Geo<T, D>:
 // so that each SIMD keeps one wave free of load stalls, measured slower.)
 constexpr int kDmaWaves = kLayerWaves;
 
+// bf16 layers whose QKV chunks span both buffers of a pair (d = 128, 256) use
+// qkv_phase_wide (below) for their QKV projection.
+template <typename T, int D> constexpr bool kWideQkv = sizeof(T) == 2 && Geo<T, D>::QH == 2;
+
 // wave index as a scalar (uniform) value
 __device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6); }
 
@@ -578,6 +582,128 @@ __device__ __forceinline__ void qkv_phase(const typename Geo<T, D>::RowAcc& acc,
       for (int r = 0; r < 4; ++r) b[r] = to_f32(sB[hc + r]);
 #pragma unroll
       for (int i = 0; i < G::RB1; ++i)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) out[i][j][r] = (hacc[i][j][r] + b[r]) * scale;
+    }
+    out_q = q;
+  });
+  store_out();
+}
+
+// The QKV phase for bf16 with 64-row unit-tiling waves: the residual
+// accumulator is dead here, so a wave can hold 64 rows of the activation (4
+// row blocks) instead of 32 and each W_qkv fragment read from LDS feeds 4
+// MFMAs, read by 2 waves instead of 4.  Waves form 2 row groups x 4 unit
+// groups of 32 units; otherwise as qkv_phase.
+template <typename T, int D>
+struct GeoQW {
+  using G = Geo<T, D>;
+  static constexpr int RB = 4;                       // 16-row blocks per wave
+  static constexpr int PM = LBM / (16 * RB);         // 2 row groups
+  static constexpr int PN = kLayerWaves / PM;        // 4 unit groups
+  static constexpr int HPW = G::FCQ / PN;            // 32 units a wave and chunk
+  static constexpr int JB = HPW / 16;
+  static_assert(G::QH == 2 && G::FC % HPW == 0 && PM * PN == kLayerWaves, "wide QKV tiling");
+};
+
+template <typename T, int D, int QP>
+__device__ __forceinline__ void qkv_phase_wide(const typename Geo<T, D>::RowAcc& acc, const Lds<T>& L, const Lanes& ln,
+                                               int m0, int M, const T* w_qkv, const T* b_qkv, T* qkv_out, int ldq,
+                                               float q_scale) {
+  using G = Geo<T, D>;
+  using Q = GeoQW<T, D>;
+  using MF = Mfma<T>;
+  constexpr int ZC = G::ZC, RB = Q::RB, JB = Q::JB, FCQ = G::FCQ, WU = Q::HPW;
+  static_assert(G::NZ == 2, "the activation passes through one buffer pair");
+  const int pm = ln.wave / Q::PN, pn = ln.wave % Q::PN;
+  // row tiling -> this wave's 64 rows of the activation, through the parity QP ^ 1 pair
+  typename MF::frag af[RB][G::KS1];
+  {
+    const int rbase = ln.w2m * G::MB2 * 16 + ln.col;
+    const int cbase = ln.w2n * G::NB2 * 16 + 4 * ln.g4;
+    const int zpart = ln.w2n * G::NB2 * 16 / ZC;     // wave-uniform
+    T* part = zpart == 0 ? L.template u<QP ^ 1>() : L.template r<QP ^ 1>();
+#pragma unroll
+    for (int i = 0; i < G::MB2; ++i)
+#pragma unroll
+      for (int j = 0; j < G::NB2; ++j) {
+        const float v[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
+        store4(&part[swz<T, ZC>(rbase + i * 16, cbase + j * 16 - zpart * ZC)], v);
+      }
+    bar_lds();
+#pragma unroll
+    for (int s = 0; s < G::KS1; ++s) {
+      const int z = s * MF::K / ZC;
+      const T* src = z == 0 ? L.template u<QP ^ 1>() : L.template r<QP ^ 1>();
+#pragma unroll
+      for (int i = 0; i < RB; ++i)
+        af[i][s] = MF::load(&src[swz<T, ZC>((pm * RB + i) * 16 + ln.col, s * MF::K - z * ZC + MF::KV * ln.g4)]);
+    }
+  }
+  // Chunk q's outputs stay in registers until after the barrier that opens
+  // chunk q + 1 (see qkv_phase).  They leave through the wave's own 1 KB of
+  // H, 16 rows x 32 units at a time, read back as 16-byte pieces of whole
+  // 64-byte row segments.
+  float out[RB][JB][4];
+  int out_q = -1;
+  auto store_out = [&]() {
+    if (out_q < 0) return;
+    static_assert(kLayerWaves * 16 * WU <= LBM * G::FC && WU * sizeof(T) == 64, "per-wave staging in H");
+    T* reg = L.h + ln.wave * (16 * WU);
+    const int col0 = out_q * FCQ + pn * WU;
+#pragma unroll
+    for (int i = 0; i < RB; ++i) {
+#pragma unroll
+      for (int j = 0; j < JB; ++j) store4(&reg[swz<T, WU>(ln.col, j * 16 + 4 * ln.g4)], out[i][j]);
+      const int rblk = m0 + (pm * RB + i) * 16;
+      const int rr = ln.lane >> 2, gg = ln.lane & 3;
+      const uint4 v = *reinterpret_cast<const uint4*>(&reg[swz<T, WU>(rr, gg * 8)]);
+      if (rblk + rr < M) *reinterpret_cast<uint4*>(qkv_out + (size_t)(rblk + rr) * ldq + col0 + gg * 8) = v;
+    }
+  };
+  chunk_pairs<QP, (G::NQ % 2) == 0>(G::NQ, [&](int q, auto pc) {
+    constexpr int P = decltype(pc)::v;
+    publish();                       // chunk q in place; chunk q - 1's buffers (and the parts) free
+    store_out();
+    const bool more = q + 1 < G::NQ;
+    const auto next = qkv_chunk<T, D, P ^ 1, kDmaWaves>(L, w_qkv, b_qkv, more ? q + 1 : q);
+    const bool loader = wave_id() < kDmaWaves;
+    // the wave's units: pn * 32 .. + 32 of the chunk, in the u (first half) or r buffer
+    const T* sW = pn * WU < G::FC ? L.template u<P>() : L.template r<P>();
+    const int u0 = (pn * WU) % G::FC;
+    f32x4 hacc[RB][JB];
+#pragma unroll
+    for (int i = 0; i < RB; ++i)
+#pragma unroll
+      for (int j = 0; j < JB; ++j) hacc[i][j] = zero4();
+    typename MF::frag bw[2][JB];
+#pragma unroll
+    for (int j = 0; j < JB; ++j) bw[0][j] = MF::load(&sW[swz<T, D>(u0 + j * 16 + ln.col, MF::KV * ln.g4)]);
+#pragma unroll
+    for (int s = 0; s < G::KS1; ++s) {
+      if (s + 1 < G::KS1) {
+#pragma unroll
+        for (int j = 0; j < JB; ++j)
+          bw[(s + 1) & 1][j] = MF::load(&sW[swz<T, D>(u0 + j * 16 + ln.col, (s + 1) * MF::K + MF::KV * ln.g4)]);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int j = 0; j < JB; ++j)
+#pragma unroll
+        for (int i = 0; i < RB; ++i) hacc[i][j] = MF::mma(bw[s & 1][j], af[i][s], hacc[i][j]);
+      __builtin_amdgcn_sched_barrier(0);
+      if (more && loader) next.step(s);
+    }
+    const float scale = q * FCQ < D ? q_scale : 1.0f;   // a chunk lies wholly in q, k or v
+    const T* sB = L.template b<P>();
+#pragma unroll
+    for (int j = 0; j < JB; ++j) {
+      const int hc = pn * WU + j * 16 + 4 * ln.g4;
+      float b[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) b[r] = to_f32(sB[hc + r]);
+#pragma unroll
+      for (int i = 0; i < RB; ++i)
 #pragma unroll
         for (int r = 0; r < 4; ++r) out[i][j][r] = (hacc[i][j][r] + b[r]) * scale;
     }
@@ -839,7 +965,10 @@ __global__ __launch_bounds__(LNT) void k_post_attention(PostAttnArgs<T> p, Graph
   } else {
     if (!qkv_next) return;
     // the FFN's last chunk used parity (NK0 + 1) & 1 (an even number of chunks)
-    qkv_phase<T, D, NK0 & 1>(acc, L, af, ln, m0, p.M, p.w_qkv, p.b_qkv, p.qkv_out, p.ldq, p.q_scale);
+    if constexpr (kWideQkv<T, D>)
+      qkv_phase_wide<T, D, NK0 & 1>(acc, L, ln, m0, p.M, p.w_qkv, p.b_qkv, p.qkv_out, p.ldq, p.q_scale);
+    else
+      qkv_phase<T, D, NK0 & 1>(acc, L, af, ln, m0, p.M, p.w_qkv, p.b_qkv, p.qkv_out, p.ldq, p.q_scale);
   }
 }
 
@@ -992,8 +1121,12 @@ __global__ __launch_bounds__(LNT) void k_pre_layer(PreLayerArgs<T> p, GraphTable
   // gamma / beta as 16-byte vectors, loaded again only where a row block starts another graph
   if (p.film_gamma) film_rows<T, D>(acc, p.film_gamma, p.film_beta, p.film_stride, gt, ln, m0, p.M);
   store_residual<T, D>(acc, L, ln, m0, p.M, p.y_out, p.ldyo);
-  typename G::ActFrags af;
-  qkv_phase<T, D, 0>(acc, L, af, ln, m0, p.M, p.w_qkv, p.b_qkv, p.qkv_out, p.ldq, p.q_scale);
+  if constexpr (kWideQkv<T, D>) {
+    qkv_phase_wide<T, D, 0>(acc, L, ln, m0, p.M, p.w_qkv, p.b_qkv, p.qkv_out, p.ldq, p.q_scale);
+  } else {
+    typename G::ActFrags af;
+    qkv_phase<T, D, 0>(acc, L, af, ln, m0, p.M, p.w_qkv, p.b_qkv, p.qkv_out, p.ldq, p.q_scale);
+  }
 }
 
 template <typename T>

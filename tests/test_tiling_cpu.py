@@ -324,6 +324,66 @@ def test_layer_qkv_store_transpose(d):
 
 
 @pytest.mark.parametrize("d", [128, 256])
+def test_layer_wide_qkv_tiling(d):
+    """The bf16 QKV phase with 64-row waves (2 row groups x 4 unit groups of 32
+    units): over the 8 waves every (row, unit) of a 128-unit chunk is formed
+    exactly once, each wave's weight fragments lie in one 64-unit half (the u
+    or r buffer), the activation reads stay inside the two ZC-column parts,
+    and the 16 x 32 staging block in the wave's own 1 KB of H is read back as
+    16-byte pieces of whole 64-byte rows, every (row, unit) exactly once."""
+    g = _geo("bf16", d)
+    assert g["qh"] == 2
+    fc, fcq, epv = g["fc"], 2 * g["fc"], 8
+    rb, pm, pn = 4, LAYER_ROWS // 64, LAYER_WAVES // (LAYER_ROWS // 64)
+    wu = fcq // pn
+    assert (pm, pn, wu) == (2, 4, 32)
+    nz = LAYER_ROWS // fc
+    zc = d // nz
+    formed = []
+    for wave in range(LAYER_WAVES):
+        wm, wn = wave // pn, wave % pn
+        half, u0 = (wn * wu) // fc, (wn * wu) % fc
+        assert u0 + wu <= fc                                  # one buffer of the pair
+        for i in range(rb):
+            for j in range(wu // 16):
+                for col in range(16):
+                    for g4 in range(4):
+                        for r in range(4):
+                            formed.append(((wm * rb + i) * 16 + col, half * fc + u0 + j * 16 + 4 * g4 + r))
+        for s in range(d // 32):                              # activation fragment reads
+            z = s * 32 // zc
+            for i in range(rb):
+                for col in range(16):
+                    for g4 in range(4):
+                        c = s * 32 - z * zc + 8 * g4
+                        assert 0 <= c and c + 8 <= zc and z < nz
+                        t = _swz(zc, epv, (wm * rb + i) * 16 + col, c)
+                        assert 0 <= t and t + 8 <= LAYER_ROWS * zc
+        base = wave * 16 * wu                                 # staging
+        assert base + 16 * wu <= LAYER_ROWS * fc
+        written = {}
+        for lane in range(64):
+            col, g4 = lane & 15, lane >> 4
+            for j in range(wu // 16):
+                u = j * 16 + 4 * g4
+                t = _swz(wu, epv, col, u)
+                for e in range(4):
+                    written[base + t + e] = (col, u + e)
+        assert len(written) == 16 * wu
+        read = []
+        for lane in range(64):
+            rr, gg = lane >> 2, lane & 3
+            t = base + _swz(wu, epv, rr, gg * 8)
+            assert t % epv == 0
+            for e in range(8):
+                row, unit = written[t + e]
+                assert row == rr and unit == gg * 8 + e       # stored at column wn*32 + gg*8 + e
+                read.append((row, unit))
+        assert sorted(read) == sorted(written.values())
+    assert sorted(formed) == [(r, u) for r in range(LAYER_ROWS) for u in range(fcq)]
+
+
+@pytest.mark.parametrize("d", [128, 256])
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_layer_residual_store_transpose(d, dtype):
     """Y' (fp32) leaves the row tiling through each wave's 2 KB of H in
