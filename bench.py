@@ -260,7 +260,7 @@ def main():
                     help="run one plain device copy of this many MiB before the warm-up (counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1 "
+        print(json.dumps({"error": "the library runs on one GPU only; --gpus must be 1 "
                                    "(multi-GPU sharding is described but not built)"}))
         sys.exit(2)
 
