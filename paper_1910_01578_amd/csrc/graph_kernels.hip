@@ -425,48 +425,81 @@ hipError_t launch_nbr_sample(const int* row_ptr, const int* col_idx, const int* 
   return hipGetLastError();
 }
 
-// ---------------------------------------------------------------------------
-// Eq. 2 gather: one wavefront per node.  A row of P is H * sizeof(T) bytes,
-// read as 16-byte lane chunks; LPR lanes cover a row, so 64 / LPR neighbour
-// rows are in flight per load instruction (twice that per unrolled step).
-// The running max starts at 0: sigmoid outputs are positive, so this equals
-// the max over a non-empty set and gives 0 for an empty one.
+// Eq. 2's max over sampled neighbours.  A group of LPR lanes owns one node,
+// each lane a 16-byte slice of the row: the group loads its node's sampled
+// neighbour ids with one load (an id per lane, LPR at a time), then fetches
+// the neighbours' rows four at a time, each lane taking the ids from the
+// group's lanes by a shuffle.  So a node costs three dependent memory
+// latencies (its range, its ids, its rows) whatever its degree, and a wave
+// carries 64 / LPR nodes.  The max does not depend on the order of the
+// rows, so the result is the same for any grouping.  Nodes without sampled
+// neighbours get 0 (the rows are sigmoid outputs, all positive).
+template <typename T, int H>
+struct GatherGeo {
+  static constexpr int VEC = 16 / sizeof(T);
+  static constexpr int LPR = H / VEC;          // lanes per row
+  static constexpr int NPW = 64 / LPR;         // nodes per wave
+  static constexpr int RB = 4;                 // rows in flight per lane
+  static_assert(LPR >= RB && LPR <= 64 && 64 % LPR == 0 && LPR % RB == 0, "row width");
+};
+
 template <typename T, int H>
 __global__ __launch_bounds__(256) void k_gather_max(const T* __restrict__ P,
                                                     const int* __restrict__ s_ptr,
                                                     const int* __restrict__ s_idx, int n,
                                                     T* __restrict__ A) {
-  constexpr int VEC = 16 / sizeof(T);
-  constexpr int LPR = H / VEC;
-  static_assert(LPR >= 1 && LPR <= 64 && (64 % LPR) == 0, "row width");
-  constexpr int RPW = 64 / LPR;
+  using G = GatherGeo<T, H>;
+  constexpr int VEC = G::VEC, LPR = G::LPR, NPW = G::NPW, RB = G::RB;
   const int lane = threadIdx.x & 63;
-  const int v = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (v >= n) return;
-  const int grp = lane / LPR;
-  const int col = (lane % LPR) * VEC;
-  const int b = s_ptr[v], e = s_ptr[v + 1];
+  const int v0 = (blockIdx.x * 4 + (threadIdx.x >> 6)) * NPW;   // the wave's first node
+  if (v0 >= n) return;                                          // whole waves
+  const int grp = lane / LPR, sub = lane % LPR;
+  const int v = v0 + grp;
+  const bool live = v < n;
+  // Every load below is unconditional, so none waits behind a branch: groups
+  // past the last node read node n - 1's range, and masked slots read index
+  // 0 and row 0 (s_idx is non-empty whenever some node of the wave has a
+  // sampled neighbour, the only case in which the loop runs).
+  const int vc = live ? v : n - 1;
+  const int b = s_ptr[vc];
+  const int e = s_ptr[vc + 1];
+  const int cnt = live ? e - b : 0;
+  // the largest count among the wave's nodes bounds every group's loop, so
+  // all lanes take part in each shuffle
+  int cmax = cnt;
+#pragma unroll
+  for (int off = LPR; off < 64; off <<= 1) cmax = max(cmax, xor_shfl(cmax, off));
+  cmax = __builtin_amdgcn_readfirstlane(cmax);
+  const int col = sub * VEC;
   float m[VEC];
 #pragma unroll
   for (int j = 0; j < VEC; ++j) m[j] = 0.f;
-  int i = b + grp;
-  for (; i + RPW < e; i += 2 * RPW) {
-    const int u0 = s_idx[i], u1 = s_idx[i + RPW];
-    const Vec16<T> r0 = load16(P + (size_t)u0 * H + col);
-    const Vec16<T> r1 = load16(P + (size_t)u1 * H + col);
+  for (int k0 = 0; k0 < cmax; k0 += LPR) {
+    const bool have = k0 + sub < cnt;
+    int ids = s_idx[have ? b + k0 + sub : 0];
+    ids = have ? ids : 0;
+    const int nb = min(cmax - k0, LPR);
+    for (int j0 = 0; j0 < nb; j0 += RB) {
+      // j0 + q < LPR: the source lanes stay inside the group
+      int u[RB];
 #pragma unroll
-    for (int j = 0; j < VEC; ++j) m[j] = fmaxf(m[j], fmaxf(to_f32(r0.v[j]), to_f32(r1.v[j])));
+      for (int q = 0; q < RB; ++q) u[q] = __shfl(ids, grp * LPR + j0 + q, 64);
+      uint4 r[RB];
+#pragma unroll
+      for (int q = 0; q < RB; ++q) r[q] = *reinterpret_cast<const uint4*>(P + (size_t)u[q] * H + col);
+#pragma unroll
+      for (int q = 0; q < RB; ++q) {
+        // a slot past the node's count becomes +0, which leaves the max of
+        // positive rows as it is (an AND, not a branch around the load)
+        const uint32_t keep = k0 + j0 + q < cnt ? 0xffffffffu : 0u;
+        const uint4 w = make_uint4(r[q].x & keep, r[q].y & keep, r[q].z & keep, r[q].w & keep);
+        const Vec16<T> x = __builtin_bit_cast(Vec16<T>, w);
+#pragma unroll
+        for (int j = 0; j < VEC; ++j) m[j] = fmaxf(m[j], to_f32(x.v[j]));
+      }
+    }
   }
-  if (i < e) {
-    const Vec16<T> r0 = load16(P + (size_t)s_idx[i] * H + col);
-#pragma unroll
-    for (int j = 0; j < VEC; ++j) m[j] = fmaxf(m[j], to_f32(r0.v[j]));
-  }
-#pragma unroll
-  for (int off = LPR; off < 64; off <<= 1)
-#pragma unroll
-    for (int j = 0; j < VEC; ++j) m[j] = fmaxf(m[j], xor_shfl(m[j], off));
-  if (grp == 0) {
+  if (live) {
     Vec16<T> o;
 #pragma unroll
     for (int j = 0; j < VEC; ++j) o.v[j] = from_f32<T>(m[j]);
@@ -474,14 +507,20 @@ __global__ __launch_bounds__(256) void k_gather_max(const T* __restrict__ P,
   }
 }
 
+template <typename T, int H>
+static void launch_gather_max_h(const T* P, const int* s_ptr, const int* s_idx, int n, T* A, hipStream_t s) {
+  constexpr int NODES = 4 * GatherGeo<T, H>::NPW;   // per 256-thread work-group
+  hipLaunchKernelGGL((k_gather_max<T, H>), dim3((n + NODES - 1) / NODES), dim3(256), 0, s, P, s_ptr, s_idx, n, A);
+}
+
 template <typename T>
 hipError_t launch_gather_max(const T* P, const int* s_ptr, const int* s_idx, int n, int H, T* A,
                              hipStream_t s) {
-  dim3 grid((n + 3) / 4), block(256);
+  if (n <= 0) return hipSuccess;
   switch (H) {
-    case 64: hipLaunchKernelGGL((k_gather_max<T, 64>), grid, block, 0, s, P, s_ptr, s_idx, n, A); break;
-    case 128: hipLaunchKernelGGL((k_gather_max<T, 128>), grid, block, 0, s, P, s_ptr, s_idx, n, A); break;
-    case 256: hipLaunchKernelGGL((k_gather_max<T, 256>), grid, block, 0, s, P, s_ptr, s_idx, n, A); break;
+    case 64: launch_gather_max_h<T, 64>(P, s_ptr, s_idx, n, A, s); break;
+    case 128: launch_gather_max_h<T, 128>(P, s_ptr, s_idx, n, A, s); break;
+    case 256: launch_gather_max_h<T, 256>(P, s_ptr, s_idx, n, A, s); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

@@ -816,11 +816,14 @@ def _max_batch(cfg):
     return W.graph_from_arrays(cfg, gp, row_ptr, d, x)
 
 
-@pytest.mark.parametrize("dtype", ["f32", "bf16"])
-def test_limits_max_graphs_fanout_devices(dtype):
+# bf16 at d = 64 puts 8 lanes on a row in the gather, so a node's 32 sampled
+# ids arrive in four batches; at d = 128 two, and in fp32 at d = 64 two.
+@pytest.mark.parametrize("dtype,width", [("f32", None), ("bf16", BF16_WIDTH),
+                                         ("bf16", dict(hidden=64, heads=4, d_ff=256))], ids=["f32", "bf16", "bf16_d64"])
+def test_limits_max_graphs_fanout_devices(dtype, width):
     over = dict(fanout=32, n_devices=64, k_samples=3, seg_len=16, mem_len=8)
-    if dtype == "bf16":
-        over = {**BF16_WIDTH, **over}
+    if width:
+        over = {**width, **over}
     cfg = W.get_config("tiny_layered_256").replace(dtype=dtype, **over)
     g = _max_batch(cfg)
     deg = np.diff(g.row_ptr)
