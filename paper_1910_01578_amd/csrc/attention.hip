@@ -279,6 +279,19 @@ void k_seg_attention(AttnArgs<T> p, GraphTable gt) {
   // with a block of ones, from the same rounded P as the numerator).
   f32x4 oacc[DB][2];
   f32x4 osum[2];
+  // With direct loads and one K fragment per key block (d_h = 32), a tile's
+  // K fragments are read right after the barrier that publishes the tile,
+  // which sits after the previous tile's score products: their LDS latency
+  // then hides under that tile's exponentials and P V product instead of
+  // opening the next one.
+  constexpr bool KP = VDMA && QS::STEPS == 1;
+  typename QF::t kfn[4];
+  auto read_k = [&](int buf) {
+    if constexpr (KP) {
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb) kfn[kb] = QF::load(&sK[buf][dma::swz<T, DH>(kb * 16 + col, QS::KV * g4)]);
+    }
+  };
 
   // One pass over the segment's key tiles.  EXACT: scores relative to a
   // running offset m per query column (log2 domain).
@@ -291,8 +304,11 @@ void k_seg_attention(AttnArgs<T> p, GraphTable gt) {
     float mrun[2] = {0.f, 0.f};
 
     // Tile t sits in buffer t % NS.  Direct loads: tiles t + 1 and t + 2 are
-    // in flight while tile t is consumed, and a tile's end waits for the
-    // older of the two only.  Register path: tile t + 1 travels through
+    // in flight while tile t is consumed, and the barrier that publishes
+    // tile t + 1 waits for the older of the two only; it comes after tile
+    // t's score products (KP) or at tile t's end.  Tile t + 2 goes into tile
+    // t - 1's buffer, whose reads every wave finished before the barrier
+    // that published tile t.  Register path: tile t + 1 travels through
     // registers during tile t and is stored at its end.
     // Q is requested in the first pass after the first tiles, and the wait
     // for all of them is one the compiler sees: inside the loop it then
@@ -303,6 +319,7 @@ void k_seg_attention(AttnArgs<T> p, GraphTable gt) {
     if constexpr (!EXACT) load_q();
     store_tile(0);
     dma::wait_loads_then_barrier();
+    read_k(0);
     int cur = 0;
     for (int t = 0; t < ntiles; ++t) {
       const int nxt = cur + 1 == NS ? 0 : cur + 1;
@@ -326,7 +343,7 @@ void k_seg_attention(AttnArgs<T> p, GraphTable gt) {
           int kidx;
           if constexpr (KDMA) kidx = dma::swz<T, DH>(krow, kcol);
           else kidx = krow * KS + kcol;
-          const typename QF::t kf = QF::load(&sK[cur][kidx]);
+          const typename QF::t kf = KP ? kfn[kb] : QF::load(&sK[cur][kidx]);
           sacc[kb][0] = QF::mma(kf, qf[0][s], sacc[kb][0]);
           sacc[kb][1] = QF::mma(kf, qf[1][s], sacc[kb][1]);
         }
@@ -365,6 +382,14 @@ void k_seg_attention(AttnArgs<T> p, GraphTable gt) {
         if (t + 1 < ntiles) load_tile(t + 1, nxt);
       }
 
+      if constexpr (KP) {
+        // tile t + 1 in place (tile t + 2 may stay in flight)
+        if (t + 1 < ntiles) {
+          if (t + 2 < ntiles) dma::wait_vm_barrier<VMT>();
+          else dma::wait_vm_barrier<0>();
+          read_k(nxt);
+        }
+      }
       // mask keys past the band end (only the last tile has them)
       if (kvalid < BKV) {
 #pragma unroll
@@ -460,7 +485,9 @@ void k_seg_attention(AttnArgs<T> p, GraphTable gt) {
           }
       }
 
-      if constexpr (VDMA) {
+      if constexpr (KP) {
+        // published after the score products above
+      } else if constexpr (VDMA) {
         // tile t + 1 in place; buffer cur free for tile t + 3
         if (t + 2 < ntiles) dma::wait_vm_barrier<VMT>();
         else dma::wait_vm_barrier<0>();

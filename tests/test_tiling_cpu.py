@@ -541,3 +541,72 @@ def test_attention_v_fragments(dh, row_max):
                 for i in range(8):
                     key = 32 * c2 + 4 * g4 + (i if i < 4 else 16 + i - 4)
                     assert frag[(lane, i)] == (min(key, row_max), 16 * b + col)
+
+
+# ---- segment attention: the K/V tile ring ---------------------------------------
+def _attention_ring_program(ntiles, kp, ns=3):
+    """One wave's program order over a segment's key tiles, as the kernel issues
+    it (direct loads, ring of ns buffers, loads ns - 1 tiles ahead): ("load", t,
+    buf), ("wait", t, tiles allowed to stay in flight), ("barrier",),
+    ("read", t, buf)."""
+    prog = [("load", 0, 0)]
+    if ntiles > 1:
+        prog.append(("load", 1, 1))
+    prog += [("wait", min(ntiles, 2) - 1, 0), ("barrier",)]        # every load so far
+    if kp:
+        prog.append(("read", 0, 0))                       # K fragments of tile 0
+    for t in range(ntiles):
+        cur = t % ns
+        if not kp:
+            prog.append(("read", t, cur))                 # K fragments
+        prog.append(("read", t, cur))                     # V fragments
+        if t + ns - 1 < ntiles:
+            prog.append(("load", t + ns - 1, (t + ns - 1) % ns))
+        if kp and t + 1 < ntiles:
+            prog += [("wait", t + 1, 1 if t + 2 < ntiles else 0), ("barrier",), ("read", t + 1, (t + 1) % ns)]
+        if not kp:                                        # after the last tile: a full wait
+            prog += [("wait", min(t + 1, ntiles - 1), 1 if t + 2 < ntiles else 0), ("barrier",)]
+    return prog
+
+
+@pytest.mark.parametrize("kp", [True, False], ids=["k_prefetch", "end_barrier"])
+@pytest.mark.parametrize("ntiles", list(range(1, 10)))
+def test_attention_ring_schedule(ntiles, kp):
+    """Replay of the tile ring: every wave runs the same program and passes each
+    barrier only when all have reached it, so (1) a tile is read only after a
+    barrier that follows the wait covering its loads, (2) a buffer is loaded
+    again only after a barrier that follows every read of its previous tile,
+    and (3) each wait's count leaves in flight exactly the loads issued after
+    the tile it waits for (vector memory operations complete in issue order)."""
+    prog = _attention_ring_program(ntiles, kp)
+    barriers = [i for i, x in enumerate(prog) if x[0] == "barrier"]
+
+    def barrier_before(i):
+        b = [j for j in barriers if j < i]
+        return b[-1] if b else -1
+
+    load_pos = {x[1]: i for i, x in enumerate(prog) if x[0] == "load"}
+    assert sorted(load_pos) == list(range(ntiles))
+    occupant = {}
+    last_read = {}
+    for i, x in enumerate(prog):
+        if x[0] == "load":
+            t, buf = x[1], x[2]
+            if buf in occupant:                           # (2)
+                assert last_read[occupant[buf]] < barrier_before(i), (t, buf)
+            occupant[buf] = t
+        elif x[0] == "read":
+            t, buf = x[1], x[2]
+            assert occupant.get(buf) == t
+            waits = [j for j, y in enumerate(prog[:i]) if y[0] == "wait" and y[1] >= t]
+            assert waits and waits[0] < barrier_before(i), t   # (1)
+            last_read[t] = i
+        elif x[0] == "wait":
+            t, allowed = x[1], x[2]
+            later = [u for u, p in load_pos.items() if u > t and p < i]
+            # (3): vmcnt(N) covers all but the N most recent operations, so the
+            # count may not exceed the loads issued after tile t (equal: no over-wait)
+            assert allowed == len(later), (t, later)
+            # the tiles it must cover were all issued before it
+            assert all(load_pos[u] < i for u in range(t + 1))
+    assert set(last_read) == set(range(ntiles))
