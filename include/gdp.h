@@ -35,8 +35,8 @@
  *  - Streams.  `stream` is a hipStream_t (NULL = the default stream).  Calls
  *    only enqueue work and return without synchronising.  A workspace may be
  *    shared by several calls only if they are ordered on one stream.
- *    gdp_place and gdp_place_train may run part of their work on a second
- *    stream of the library's (see gdp_set_place_streams); it starts after
+ *    gdp_place, gdp_place_train and gdp_place_sample may run part of their
+ *    work on a second stream of the library's (see gdp_set_place_streams); it starts after
  *    the work enqueued on `stream` before the call, and work enqueued on
  *    `stream` after the call waits for it, so the ordering seen on `stream`
  *    is that of a single-stream call, HIP graph capture included.
@@ -181,7 +181,9 @@ typedef struct gdp_placer {
 } gdp_placer;
 
 /* Bytes of workspace needed by gdp_embed, gdp_place and gdp_sample for this
- * problem (the maximum of the three).  Returns 0 on invalid arguments. */
+ * problem (the maximum of the three), and with a placer and k_samples > 0 also
+ * by gdp_place_sample (whose sample regions follow the placer's).  Returns 0
+ * on invalid arguments. */
 size_t gdp_workspace_bytes(const gdp_graph* g, const gdp_gnn* gnn, const gdp_placer* placer,
                            int32_t k_samples);
 
@@ -242,6 +244,22 @@ int gdp_set_place_streams(int32_t n);
 int gdp_sample(const gdp_graph* g, const float* logits, const float* lse, int32_t n_devices,
                int32_t k_samples, uint64_t seed, const float* uniforms, int32_t* placements,
                float* logp, void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * gdp_place followed by gdp_sample with n_devices = placer->n_devices, as one
+ * call (Section 3: the policy's logits, then whole-graph sampling from them):
+ * logits, lse, placements and logp are those of the two calls bit for bit.
+ * In the two-part schedule with the head inside the last layer's kernel
+ * (n_devices <= 8), the sampling of the nodes below the split row starts on
+ * the second stream as soon as their logits are final, beside the other
+ * part's last layer.  The workspace of gdp_workspace_bytes with this placer
+ * and k_samples suffices (the placer's regions, then the sample's); the same
+ * errors as either call, checked before anything is enqueued.
+ */
+int gdp_place_sample(const gdp_graph* g, const void* node_emb, const float* graph_emb,
+                     const gdp_placer* placer, float* logits, float* lse, int32_t k_samples,
+                     uint64_t seed, const float* uniforms, int32_t* placements, float* logp,
+                     void* workspace, size_t workspace_bytes, void* stream);
 
 /*
  * gdp_place that also writes the placement network's output X (the head's

@@ -262,9 +262,38 @@ static int embed_impl(const gdp_graph* g, const gdp_gnn* gnn, T* node_emb, float
 // ---------------------------------------------------------------------------
 // gdp_place: FiLM (Eq. 4) + segment-recurrent Transformer layers + head.
 // ---------------------------------------------------------------------------
+// The policy sample that gdp_place_sample draws from the logits it has just
+// formed (gdp_sample's kernels and their per-chunk partial sums).  Chunks
+// [first, last) on stream s; launch_sample's chunks are the same whichever
+// launch forms them, so splitting them over launches and streams changes no
+// result.
+struct SampleTail {
+  int n_devices, k_samples;
+  uint64_t seed;
+  const float* uniforms;
+  int32_t* placements;
+  float* logp;
+  float* partial;                 // [k_samples][chunks], outside the placer's workspace
+  GraphTable ct;                  // the sampling chunks (kSampleRows rows, none across graphs)
+  int chunks;
+};
+
+static int sample_chunks(const SampleTail& t, const gdp_graph* g, const float* logits, const float* lse, int first,
+                         int last, hipStream_t s) {
+  GDP_LAUNCH_ON(GDP_K_SAMPLE, s, launch_sample(logits, lse, g->n_nodes, t.n_devices, t.k_samples, t.seed, t.uniforms,
+                                               t.ct, t.chunks, t.placements, t.partial, s, first, last));
+  return GDP_OK;
+}
+
+static int sample_reduce(const SampleTail& t, hipStream_t st) {
+  GDP_LAUNCH(GDP_K_LOGP_REDUCE, launch_logp_reduce(t.partial, t.ct, t.chunks, t.k_samples, t.logp, st));
+  return GDP_OK;
+}
+
 template <typename T>
 static int place_impl(const gdp_graph* g, const T* node_emb, const float* graph_emb, const gdp_placer* p,
-                      float* logits, float* lse, float* x_out, const PlacePlan& pl, void* ws, hipStream_t st) {
+                      float* logits, float* lse, float* x_out, const PlacePlan& pl, void* ws, hipStream_t st,
+                      const SampleTail* tail = nullptr) {
   const int N = g->n_nodes, G = g->n_graphs, d = p->d_model, L = p->n_layers;
   const GraphTable gt = make_table(g);
   float* film = at<float>(ws, pl.film);       // [L][2][G][d]: gamma then beta
@@ -326,7 +355,9 @@ static int place_impl(const gdp_graph* g, const T* node_emb, const float* graph_
     if (!fused)
       GDP_LAUNCH(GDP_K_HEAD, launch_head<T>(xfinal, static_cast<const T*>(p->w_out),
                                             static_cast<const T*>(p->b_out), N, d, p->n_devices, logits, lse, st));
-    return GDP_OK;
+    if (!tail) return GDP_OK;
+    int r = sample_chunks(*tail, g, logits, lse, 0, tail->chunks, st);
+    return r != GDP_OK ? r : sample_reduce(*tail, st);
   }
 
   GraphTable qt = make_table(g);
@@ -381,6 +412,7 @@ static int place_impl(const gdp_graph* g, const T* node_emb, const float* graph_
   auto ynext_of = [&](int l) { return l + 1 == L && x_out ? x_out : ybuf[(l + 1) & 1]; };
 
   SideStream* sd = nullptr;
+  int tail_straddle[2] = {0, 0};   // sampling chunks with rows on both sides of the split
   if (pl.split > 0 && g_place_streams == 2) {
     const int r = side_stream(st, &sd);
     if (r != GDP_OK) return r;
@@ -410,6 +442,11 @@ static int place_impl(const gdp_graph* g, const T* node_emb, const float* graph_
     // (in host order) before it is recorded again.
     hipStream_t s2 = sd->s;
     const int R = pl.split, QA = pl.split_qblocks;
+    // sampling chunks [0, tail_a) lie below R, [tail_b, chunks) at or above it
+    int tail_b = 0;
+    const int tail_a = tail ? blocks_below(g->graph_ptr_h, G, kSampleRows, R, &tail_b) : 0;
+    tail_straddle[0] = tail_a;
+    tail_straddle[1] = tail_b;
     T* qkv[2] = {at<T>(ws, pl.qkv), at<T>(ws, pl.qkv2)};
     GDP_HIP(hipEventRecord(sd->fork, st));
     GDP_HIP(hipStreamWaitEvent(s2, sd->fork, 0));
@@ -441,6 +478,15 @@ static int place_impl(const gdp_graph* g, const T* node_emb, const float* graph_
         // part B's post-attention
         GDP_LAUNCH(GDP_K_POST_ATTN, launch_post_attention<T>(post_args(l, ybuf[l & 1], ynext_of(l), qout, R), gt, st));
       }
+      // With the head fused, part A's logits are final once its last
+      // post-attention has run: the sampling chunks wholly below R go on s2
+      // beside part B's last layer, those wholly at or above R on st after
+      // it; a chunk with rows on both sides waits for the join.
+      if (tail && fused_head) {
+        int r = sample_chunks(*tail, g, logits, lse, 0, tail_a, s2);
+        if (r == GDP_OK) r = sample_chunks(*tail, g, logits, lse, tail_b, tail->chunks, st);
+        if (r != GDP_OK) return r;
+      }
       return GDP_OK;
     };
     const int r = parts();
@@ -452,7 +498,15 @@ static int place_impl(const gdp_graph* g, const T* node_emb, const float* graph_
   if (!fused_head)
     GDP_LAUNCH(GDP_K_HEAD, launch_head<T>(ynext_of(L - 1), static_cast<const T*>(p->w_out),
                                           static_cast<const T*>(p->b_out), N, d, p->n_devices, logits, lse, st));
-  return GDP_OK;
+  if (!tail) return GDP_OK;
+  if (!(sd && fused_head)) {
+    const int r = sample_chunks(*tail, g, logits, lse, 0, tail->chunks, st);
+    if (r != GDP_OK) return r;
+  } else if (tail_straddle[1] > tail_straddle[0]) {
+    const int r = sample_chunks(*tail, g, logits, lse, tail_straddle[0], tail_straddle[1], st);
+    if (r != GDP_OK) return r;
+  }
+  return sample_reduce(*tail, st);
 }
 
 }  // namespace gdp
@@ -476,6 +530,12 @@ extern "C" size_t gdp_workspace_bytes(const gdp_graph* g, const gdp_gnn* gnn, co
     PlacePlan p;
     plan_place(g, placer, &p);
     if (p.c.total > need) need = p.c.total;
+    if (k_samples > 0) {
+      // gdp_place_sample: the sample's regions after the placer's
+      SamplePlan s;
+      plan_sample(g, k_samples, &s);
+      if (p.c.total + s.c.total > need) need = p.c.total + s.c.total;
+    }
   }
   if (k_samples > 0) {
     SamplePlan s;
@@ -502,9 +562,19 @@ extern "C" int gdp_embed(const gdp_graph* g, const gdp_gnn* gnn, void* node_emb,
   return embed_impl<float>(g, gnn, static_cast<float*>(node_emb), graph_emb, pl, ws, st);
 }
 
+// The sample, when given, must already have passed check_sample and the
+// pointer checks of gdp_sample; its partial sums go after the placer's regions.
+struct SampleRequest {
+  int32_t k_samples;
+  uint64_t seed;
+  const float* uniforms;
+  int32_t* placements;
+  float* logp;
+};
+
 static int place_entry(const gdp_graph* g, const void* node_emb, const float* graph_emb, const gdp_placer* placer,
-                       float* logits, float* lse, float* x_out, void* ws, size_t ws_bytes, void* stream) {
-  clear_error();
+                       float* logits, float* lse, float* x_out, void* ws, size_t ws_bytes, void* stream,
+                       const SampleRequest* sample = nullptr) {
   int r;
   if ((r = check_graph(g)) != GDP_OK) return r;
   if ((r = check_placer(g, placer)) != GDP_OK) return r;
@@ -513,26 +583,58 @@ static int place_entry(const gdp_graph* g, const void* node_emb, const float* gr
   if (!aligned16(node_emb)) return fail(GDP_E_INVALID_ARG, "node_emb must be 16-byte aligned");
   PlacePlan pl;
   plan_place(g, placer, &pl);
-  if ((r = check_ws(ws, ws_bytes, pl.c.total)) != GDP_OK) return r;
+  SamplePlan sp;
+  SampleTail tail;
+  size_t need = pl.c.total;
+  if (sample) {
+    plan_sample(g, sample->k_samples, &sp);
+    need += sp.c.total;
+  }
+  if ((r = check_ws(ws, ws_bytes, need)) != GDP_OK) return r;
   if ((r = pending_hip_error()) != GDP_OK) return r;
+  if (sample) {
+    tail.n_devices = placer->n_devices;
+    tail.k_samples = sample->k_samples;
+    tail.seed = sample->seed;
+    tail.uniforms = sample->uniforms;
+    tail.placements = sample->placements;
+    tail.logp = sample->logp;
+    tail.partial = at<float>(ws, pl.c.total + sp.partial);
+    tail.ct = make_table(g);
+    tail.chunks = prefix_blocks_rows(g->graph_ptr_h, g->n_graphs, kSampleRows, tail.ct.blk);
+  }
+  const SampleTail* t = sample ? &tail : nullptr;
   hipStream_t st = static_cast<hipStream_t>(stream);
   if (g->dtype == GDP_BF16)
-    return place_impl<bf16>(g, static_cast<const bf16*>(node_emb), graph_emb, placer, logits, lse, x_out, pl, ws, st);
-  return place_impl<float>(g, static_cast<const float*>(node_emb), graph_emb, placer, logits, lse, x_out, pl, ws, st);
+    return place_impl<bf16>(g, static_cast<const bf16*>(node_emb), graph_emb, placer, logits, lse, x_out, pl, ws, st, t);
+  return place_impl<float>(g, static_cast<const float*>(node_emb), graph_emb, placer, logits, lse, x_out, pl, ws, st, t);
 }
 
 extern "C" int gdp_place(const gdp_graph* g, const void* node_emb, const float* graph_emb, const gdp_placer* placer,
                          float* logits, float* lse, void* ws, size_t ws_bytes, void* stream) {
+  clear_error();
   return place_entry(g, node_emb, graph_emb, placer, logits, lse, nullptr, ws, ws_bytes, stream);
+}
+
+extern "C" int gdp_place_sample(const gdp_graph* g, const void* node_emb, const float* graph_emb,
+                                const gdp_placer* placer, float* logits, float* lse, int32_t k_samples, uint64_t seed,
+                                const float* uniforms, int32_t* placements, float* logp, void* ws, size_t ws_bytes,
+                                void* stream) {
+  clear_error();
+  int r;
+  if ((r = check_graph(g)) != GDP_OK) return r;
+  if ((r = check_placer(g, placer)) != GDP_OK) return r;
+  if ((r = check_sample(g, placer->n_devices, k_samples)) != GDP_OK) return r;
+  if (!placements || !logp) return fail(GDP_E_INVALID_ARG, "placements or logp is NULL");
+  const SampleRequest req = {k_samples, seed, uniforms, placements, logp};
+  return place_entry(g, node_emb, graph_emb, placer, logits, lse, nullptr, ws, ws_bytes, stream, &req);
 }
 
 extern "C" int gdp_place_train(const gdp_graph* g, const void* node_emb, const float* graph_emb,
                                const gdp_placer* placer, float* logits, float* lse, float* x_out, void* ws,
                                size_t ws_bytes, void* stream) {
-  if (!x_out || !aligned16(x_out)) {
-    clear_error();
-    return fail(GDP_E_INVALID_ARG, "x_out is NULL or not 16-byte aligned");
-  }
+  clear_error();
+  if (!x_out || !aligned16(x_out)) return fail(GDP_E_INVALID_ARG, "x_out is NULL or not 16-byte aligned");
   return place_entry(g, node_emb, graph_emb, placer, logits, lse, x_out, ws, ws_bytes, stream);
 }
 

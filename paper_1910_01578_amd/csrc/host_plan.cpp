@@ -136,6 +136,26 @@ int prefix_blocks_rows(const int32_t* gp, int G, int rows, int32_t* blk) {
   return blk[G];
 }
 
+int blocks_below(const int32_t* gp, int G, int rows, int R, int* started) {
+  int n = 0, s = 0;
+  for (int g = 0; g < G; ++g) {
+    if (gp[g + 1] <= R) {
+      n += (gp[g + 1] - gp[g] + rows - 1) / rows;
+      s = n;
+    } else {
+      if (gp[g] < R) {
+        n += (R - gp[g]) / rows;                // block b ends at gp[g] + (b + 1) rows <= R
+        s = n + ((R - gp[g]) % rows != 0);      // a block starts below R and ends above it
+      } else {
+        s = n;
+      }
+      break;
+    }
+  }
+  if (started) *started = s;
+  return n;
+}
+
 int prefix_blocks_attention(const int32_t* gp, int G, int seg_len, int bq, int32_t* blk) {
   const int qbs = (seg_len + bq - 1) / bq;
   blk[0] = 0;

@@ -33,6 +33,11 @@ size_t carve_add(Carve* c, size_t bytes);   // returns the offset of the new reg
 // Per-graph block counts -> prefix (blk[0] = 0 .. blk[G] = total).
 int prefix_blocks_rows(const int32_t* graph_ptr, int G, int rows_per_block, int32_t* blk);
 int prefix_blocks_attention(const int32_t* graph_ptr, int G, int seg_len, int block_q, int32_t* blk);
+// Of the blocks prefix_blocks_rows counts, the number (a prefix of them) whose
+// rows all lie below row R; *started (if not null) receives the number whose
+// first row lies below R, which exceeds the first by one when a block holds
+// rows on both sides of R.
+int blocks_below(const int32_t* graph_ptr, int G, int rows_per_block, int R, int* started = nullptr);
 // The segment start (of any graph of the batch) nearest `target` rows and
 // strictly inside (0, N), or 0 when there is none; *qblocks_below receives
 // the number of attention query blocks (prefix_blocks_attention's order)

@@ -195,9 +195,11 @@ hipError_t launch_head(const float* x, const T* w_out, const T* b_out, int n, in
 
 // ---- sampling ---------------------------------------------------------------
 constexpr int kSampleChunk = 256;
+// Chunks [chunk0, chunk1) of the total_chunks (chunk1 < 0: to the end); each
+// chunk's placements and partial sums are the same whichever launch forms them.
 hipError_t launch_sample(const float* logits, const float* lse, int n, int D, int K, uint64_t seed,
                          const float* uniforms, const GraphTable& chunks, int total_chunks,
-                         int* placements, float* partial, hipStream_t s);
+                         int* placements, float* partial, hipStream_t s, int chunk0 = 0, int chunk1 = -1);
 hipError_t launch_logp_reduce(const float* partial, const GraphTable& chunks, int total_chunks, int K,
                               float* logp, hipStream_t s);
 hipError_t launch_debug_uniforms(uint64_t seed, int n, int K, int D, float* out, hipStream_t s);

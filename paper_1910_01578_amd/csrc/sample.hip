@@ -37,12 +37,12 @@ constexpr int kSamplesPerThread = 4;
 __global__ __launch_bounds__(kSampleChunk) void k_sample(const float* __restrict__ logits,
                                                          const float* __restrict__ lse, int n, int D, int K,
                                                          uint64_t seed, const float* __restrict__ uniforms,
-                                                         GraphTable ct, int total_chunks,
+                                                         GraphTable ct, int total_chunks, int chunk0,
                                                          int* __restrict__ placements,
                                                          float* __restrict__ partial) {
   constexpr int S = kSamplesPerThread;
   __shared__ float red[S][kSampleChunk / kWave];
-  const int c = blockIdx.x, k0 = blockIdx.y * S;
+  const int c = chunk0 + blockIdx.x, k0 = blockIdx.y * S;
   const int g = graph_of_block(ct, c);
   const int v = ct.ptr[g] + (c - ct.blk[g]) * kSampleChunk + threadIdx.x;
   float term[S];
@@ -118,9 +118,12 @@ __global__ __launch_bounds__(kSampleChunk) void k_sample(const float* __restrict
 
 hipError_t launch_sample(const float* logits, const float* lse, int n, int D, int K, uint64_t seed,
                          const float* uniforms, const GraphTable& ct, int total_chunks, int* placements,
-                         float* partial, hipStream_t s) {
-  dim3 grid(total_chunks, (K + kSamplesPerThread - 1) / kSamplesPerThread), block(kSampleChunk);
-  hipLaunchKernelGGL(k_sample, grid, block, 0, s, logits, lse, n, D, K, seed, uniforms, ct, total_chunks,
+                         float* partial, hipStream_t s, int chunk0, int chunk1) {
+  if (chunk1 < 0) chunk1 = total_chunks;
+  if (chunk0 < 0 || chunk0 > chunk1 || chunk1 > total_chunks) return hipErrorInvalidValue;
+  if (chunk0 == chunk1) return hipSuccess;
+  dim3 grid(chunk1 - chunk0, (K + kSamplesPerThread - 1) / kSamplesPerThread), block(kSampleChunk);
+  hipLaunchKernelGGL(k_sample, grid, block, 0, s, logits, lse, n, D, K, seed, uniforms, ct, total_chunks, chunk0,
                      placements, partial);
   return hipGetLastError();
 }

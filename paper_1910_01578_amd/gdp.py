@@ -108,6 +108,9 @@ def _load():
                                 c_void_p, c_size_t, c_void_p]),
         "gdp_sample": (c_int32, [POINTER(GdpGraph), c_void_p, c_void_p, c_int32, c_int32, c_uint64, c_void_p,
                                  c_void_p, c_void_p, c_void_p, c_size_t, c_void_p]),
+        "gdp_place_sample": (c_int32, [POINTER(GdpGraph), c_void_p, c_void_p, POINTER(GdpPlacer), c_void_p,
+                                       c_void_p, c_int32, c_uint64, c_void_p, c_void_p, c_void_p, c_void_p,
+                                       c_size_t, c_void_p]),
         "gdp_sample_noalloc": (c_int32, [POINTER(GdpGraph), c_void_p, c_void_p, c_int32, c_int32, c_uint64,
                                          c_void_p, c_void_p, c_void_p, c_void_p]),
         "gdp_evaluate_workspace_bytes": (c_size_t, [POINTER(GdpGraph), c_int32, c_int32]),
@@ -319,11 +322,19 @@ class Runner:
                                      None if uniforms is None else uniforms.data_ptr(), placements.data_ptr(),
                                      logp.data_ptr(), _stream_handle(stream)))
 
+    def place_sample(self, seed: int, uniforms=None, use_lse: bool = True, stream=None):
+        """place() then sample() as one call (gdp_place_sample); with use_lse
+        False the placer writes no lse and the sampling forms it."""
+        check(lib.gdp_place_sample(ctypes.byref(self.graph.c), self.node_emb.data_ptr(), self.graph_emb.data_ptr(),
+                                   ctypes.byref(self.policy.placer), self.logits.data_ptr(),
+                                   self.lse.data_ptr() if use_lse else None, self.k, seed,
+                                   None if uniforms is None else uniforms.data_ptr(), self.placements.data_ptr(),
+                                   self.logp.data_ptr(), self.ws.data_ptr(), self.ws_bytes, _stream_handle(stream)))
+
     def forward(self, seed: int, stream=None):
-        """One pass of the hot path: embed -> place -> sample."""
+        """One pass of the hot path: embed -> place -> sample (the last two as one call)."""
         self.embed(stream)
-        self.place(stream)
-        self.sample(seed, stream=stream)
+        self.place_sample(seed, stream=stream)
 
     def ppo_grad(self, logp_old, advantages, clip_eps: float = 0.2, use_lse: bool = True, stream=None):
         """PPO's clipped surrogate per graph and its gradient with respect to the

@@ -8,6 +8,7 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <algorithm>
 #include <vector>
 
 #include "gdp.h"
@@ -421,6 +422,44 @@ static void split_paths() {
   }
 }
 
+// blocks_below: the per-graph row blocks of prefix_blocks_rows whose rows all
+// lie below R, and those whose first row does, against counts over the blocks
+// one by one; at most one block holds rows on both sides of R.
+static void blocks_below_paths() {
+  const std::vector<std::vector<int32_t>> graphs = {
+      {0, 52000}, {0, 45000}, {0, 1000, 40000}, {0, 300, 301, 5000, 5001}, {0, 1}, {0, 256, 512}};
+  for (const auto& gp : graphs) {
+    const int G = (int)gp.size() - 1;
+    for (int R : {0, 1, 255, 256, 257, 300, 1000, 1255, 1256, 19900, 32700, 32768, gp[G] - 1, gp[G]}) {
+      if (R < 0 || R > gp[G]) continue;
+      int want = 0;
+      for (int g = 0; g < G; ++g)
+        for (int lo = gp[g]; lo < gp[g + 1]; lo += 256)
+          if (std::min(lo + 256, (int)gp[g + 1]) <= R) ++want;
+      // the counted blocks are a prefix of prefix_blocks_rows's order
+      int prefix = 0;
+      bool in_prefix = true;
+      for (int g = 0; g < G && in_prefix; ++g)
+        for (int lo = gp[g]; lo < gp[g + 1]; lo += 256) {
+          if (std::min(lo + 256, (int)gp[g + 1]) <= R) ++prefix;
+          else { in_prefix = false; break; }
+        }
+      int started_want = 0;
+      for (int g = 0; g < G; ++g)
+        for (int lo = gp[g]; lo < gp[g + 1]; lo += 256)
+          if (lo < R) ++started_want;
+      int started = -1;
+      const int got = blocks_below(gp.data(), G, 256, R, &started);
+      ++g_checks;
+      if (got != want || got != prefix || started != started_want || started - got > 1) {
+        ++g_failures;
+        printf("FAIL blocks_below R %d over %d graphs: %d (started %d), expected %d (prefix %d, started %d)\n", R, G,
+               got, started, want, prefix, started_want);
+      }
+    }
+  }
+}
+
 static void train_paths() {
   const gdp_graph g = good_graph();
   gdp_gnn n = good_gnn();
@@ -481,6 +520,7 @@ int main() {
   sample_paths();
   plan_paths();
   split_paths();
+  blocks_below_paths();
   train_paths();
   error_text();
   printf("%d checks, %d failures\n", g_checks, g_failures);
