@@ -28,6 +28,7 @@ namespace {
 struct TimerRec {
   int kind;
   hipEvent_t a, b;
+  bool recorded;    // false when the closing record failed: the launch is not counted
 };
 struct TimerState {
   uint32_t mask = 0;
@@ -49,23 +50,28 @@ struct TimerState {
 // Per thread: launches of other threads are neither timed nor disturbed.
 thread_local TimerState g_timer;
 
+// A launch whose opening or closing record fails is left out of the totals
+// (the failure itself surfaces through the launch or the next call).
 struct Timed {
   hipStream_t s;
   hipEvent_t b = nullptr;
+  size_t idx = 0;
   bool on;
   Timed(int kind, hipStream_t st) : s(st), on(((g_timer.mask >> kind) & 1u) != 0) {
     if (!on) return;
     hipEvent_t a = g_timer.take();
     b = g_timer.take();
-    if (!a || !b) {
+    if (!a || !b || hipEventRecord(a, s) != hipSuccess) {
+      if (a) g_timer.pool.push_back(a);
+      if (b) g_timer.pool.push_back(b);
       on = false;
       return;
     }
-    hipEventRecord(a, s);
-    g_timer.recs.push_back({kind, a, b});
+    idx = g_timer.recs.size();
+    g_timer.recs.push_back({kind, a, b, true});
   }
   ~Timed() {
-    if (on) hipEventRecord(b, s);
+    if (on && hipEventRecord(b, s) != hipSuccess) g_timer.recs[idx].recorded = false;
   }
 };
 }  // namespace
@@ -1425,6 +1431,11 @@ extern "C" int gdp_timer_end(double* total_ms, int64_t* launches) {
   if (launches)
     for (int k = 0; k < GDP_K_COUNT; ++k) launches[k] = 0;
   for (const TimerRec& rec : g_timer.recs) {
+    if (!rec.recorded) {
+      g_timer.pool.push_back(rec.a);
+      g_timer.pool.push_back(rec.b);
+      continue;
+    }
     float ms = 0.f;
     hipError_t e = hipEventSynchronize(rec.b);
     if (e == hipSuccess) e = hipEventElapsedTime(&ms, rec.a, rec.b);

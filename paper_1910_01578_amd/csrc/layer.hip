@@ -513,7 +513,6 @@ __device__ __forceinline__ void qkv_phase(const typename Geo<T, D>::RowAcc& acc,
                                           typename Geo<T, D>::ActFrags& af, const Lanes& ln, int m0, int M,
                                           const T* w_qkv, const T* b_qkv, T* qkv_out, int ldq, float q_scale) {
   using G = Geo<T, D>;
-  constexpr int FC = G::FC;
   to_unit_tiling<T, D, QP ^ 1>(acc, L, af, ln);
   if constexpr (G::NZ == 4) qkv_chunk<T, D, QP>(L, w_qkv, b_qkv, 0).all();
   constexpr int FCQ = G::FCQ, JB = G::JBQ;
