@@ -106,21 +106,24 @@ def test_schedules_agree_on_the_52000_node_workload():
     assert out[1] == out[2]
 
 
-def test_first_call_under_capture_keeps_one_stream():
-    """A thread whose first two-part gdp_place call is captured into a HIP
-    graph creates no stream and keeps every launch on the capturing stream;
-    the replay equals the eager two-part result bit for bit."""
+@pytest.mark.parametrize("call", ["place", "place_sample"])
+def test_first_call_under_capture_keeps_one_stream(call):
+    """A thread whose first two-part gdp_place (or gdp_place_sample) call is
+    captured into a HIP graph creates no stream and keeps every launch on the
+    capturing stream; the replay equals the eager two-part result bit for bit."""
     import threading
     import torch
     from paper_1910_01578_amd import gdp
     from tests.parity import workload
     cfg, g, w = workload("gnmt8_52000")
-    _log("capture in a fresh thread", cfg.name)
-    r = gdp.Runner(gdp.DeviceGraph(g, cfg.dtype), gdp.DevicePolicy(cfg, w), 1)
+    _log("capture in a fresh thread", cfg.name, call)
+    r = gdp.Runner(gdp.DeviceGraph(g, cfg.dtype), gdp.DevicePolicy(cfg, w), 4)
     r.embed()
-    r.place()
+    run = (lambda: r.place()) if call == "place" else (lambda: r.place_sample(cfg.sample_seed))
+    outs = (r.logits, r.lse) if call == "place" else (r.logits, r.lse, r.placements, r.logp)
+    run()
     torch.cuda.synchronize()
-    want = (_bits(r.logits), _bits(r.lse))
+    want = tuple(_bits(t) for t in outs)
     res = {}
 
     def work():
@@ -128,13 +131,14 @@ def test_first_call_under_capture_keeps_one_stream():
             torch.cuda.set_device(0)
             graph = torch.cuda.CUDAGraph()
             with torch.cuda.graph(graph):
-                r.place()
+                run()
             torch.cuda.synchronize()
             r.logits.fill_(float("nan"))
+            r.placements.fill_(-1)
             torch.cuda.synchronize()
             graph.replay()
             torch.cuda.synchronize()
-            res["got"] = (_bits(r.logits), _bits(r.lse))
+            res["got"] = tuple(_bits(t) for t in outs)
         except Exception as e:   # reported in the main thread
             res["err"] = e
 
