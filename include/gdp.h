@@ -250,9 +250,10 @@ int gdp_sample(const gdp_graph* g, const float* logits, const float* lse, int32_
  * call (Section 3: the policy's logits, then whole-graph sampling from them):
  * logits, lse, placements and logp are those of the two calls bit for bit.
  * In the two-part schedule with the head inside the last layer's kernel
- * (n_devices <= 8), the sampling of the nodes below the split row starts on
- * the second stream as soon as their logits are final, beside the other
- * part's last layer.  The workspace of gdp_workspace_bytes with this placer
+ * (n_devices <= 8), the sampling of the 256-node chunks that lie wholly below
+ * the split row starts on the second stream as soon as their logits are
+ * final, beside the other part's last layer; a chunk with nodes on both sides
+ * is sampled after the two streams join.  The workspace of gdp_workspace_bytes with this placer
  * and k_samples suffices (the placer's regions, then the sample's); the same
  * errors as either call, checked before anything is enqueued.
  */
